@@ -1,0 +1,14 @@
+"""CPU oracle for Scattered Linear Attention -- test infrastructure only.
+
+Only the test suite, the smoke check and the benchmark's CPU-baseline leg may use
+this package.  It shares no code with the HIP library and imports nothing from it.
+"""
+from .sla_ref import (  # noqa: F401
+    chunk_plan_ref,
+    dphi,
+    phi,
+    segments_ref,
+    sla_backward_ref,
+    sla_forward_ref,
+    widen,
+)

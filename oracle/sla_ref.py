@@ -1,0 +1,223 @@
+"""CPU oracle for Scattered Linear Attention (SLA) -- TEST INFRASTRUCTURE ONLY.
+
+This module is the slow, obviously-correct reference that the HIP path is checked
+against.  Only the test suite, the smoke check and the benchmark's CPU-baseline leg
+may import it; the product path never calls it and has no CPU fallback.
+
+Everything is plain numpy in float64.  Inputs stored in 16-bit formats are widened
+exactly (float16 through numpy, bfloat16 bit patterns by a 16-bit shift), so the
+oracle sees exactly the values the GPU sees.  There is no chunking, blocking or
+reordering beyond what the definitions below state.
+
+Paper: "ScatterFormer: Efficient Voxel Transformer with Scattered Linear Attention"
+(He, Li, Zhang, Zhang; arXiv 2401.00912).
+
+What is computed, and the passage it follows
+--------------------------------------------
+* ``phi`` / ``dphi``: the kernel feature map.  Sec. 3.2 (after Eq. (3)) only names
+  "the kernel function" and attributes LA to the linear-transformer paper it cites,
+  whose feature map is elu(x)+1.  Reading taken: phi(x) = x + 1 for x > 0 and
+  exp(x) otherwise.
+* ``segments_ref``: Sec. 3.2 orders all voxels of the scene by window so that each
+  window is one contiguous sub-matrix of a single flattened matrix.  Read as a
+  stable sort of rows by window id plus CSR offsets over the window slots; this
+  result is unique.
+* ``chunk_plan_ref``: Sec. 3.2 / Fig. 3(a) partition the flattened matrix into
+  chunks, and the Fig. 5 caption defines "offsets generation" as computing each
+  chunk's start row.  The packing rule written here is this library's own plan
+  rule (the paper does not give one); it is pinned by its invariants.
+* ``sla_forward_ref``: Eq. (2) (concatenation over the M non-empty windows of
+  per-window linear attention) and Eq. (3) (per-window normalised linear
+  attention), evaluated in the phi(Q)(phi(K)^T V) order of Sec. 3.1.  Non-causal:
+  every row of a window sees the whole window (Eq. (3) sums over all m^j rows).
+  No 1/sqrt(d) scale and no epsilon in the denominator (Eq. (3) has neither).
+* ``sla_backward_ref``: the paper trains the model but does not write the
+  backward pass; the gradients here are derived from Eq. (3) by the chain rule
+  (derivation in the docstring).
+"""
+from __future__ import annotations
+
+import numpy as np
+
+__all__ = [
+    "widen",
+    "phi",
+    "dphi",
+    "segments_ref",
+    "chunk_plan_ref",
+    "sla_forward_ref",
+    "sla_backward_ref",
+]
+
+
+# --------------------------------------------------------------------------- inputs
+def widen(x: np.ndarray, dtype: str) -> np.ndarray:
+    """Exact widening of a stored input array to float64.
+
+    dtype: "f32" (numpy float32), "f16" (numpy float16) or "bf16" (numpy uint16
+    holding bfloat16 bit patterns: the float32 with those 16 high bits).
+    """
+    if dtype == "f32":
+        return np.asarray(x, dtype=np.float32).astype(np.float64)
+    if dtype == "f16":
+        return np.asarray(x, dtype=np.float16).astype(np.float64)
+    if dtype == "bf16":
+        bits = np.asarray(x, dtype=np.uint16).astype(np.uint32) << np.uint32(16)
+        return bits.view(np.float32).astype(np.float64)
+    raise ValueError(f"unknown dtype {dtype!r}")
+
+
+# --------------------------------------------------------------------- feature map
+def phi(x: np.ndarray) -> np.ndarray:
+    """elu(x) + 1: x + 1 for x > 0, exp(x) for x <= 0 (Sec. 3.2, reading above)."""
+    x = np.asarray(x, dtype=np.float64)
+    return np.where(x > 0.0, x + 1.0, np.exp(np.minimum(x, 0.0)))
+
+
+def dphi(x: np.ndarray) -> np.ndarray:
+    """Derivative of phi: 1 for x > 0, exp(x) for x <= 0 (continuous at 0)."""
+    x = np.asarray(x, dtype=np.float64)
+    return np.where(x > 0.0, 1.0, np.exp(np.minimum(x, 0.0)))
+
+
+# ------------------------------------------------------------------ segment builder
+def segments_ref(ids: np.ndarray, num_windows: int):
+    """Stable sort of rows by window id (Sec. 3.2, flattened window-sorted matrix).
+
+    Returns (perm, offsets, invalid_count):
+      perm[p]    original row of sorted position p, ties in original row order;
+                 rows whose id is outside [0, num_windows) are left out.
+      offsets    int64 [num_windows + 1], offsets[w] = first sorted position of
+                 window w; empty windows have offsets[w] == offsets[w + 1].
+      invalid_count  number of rows with an out-of-range id.
+    """
+    ids = np.asarray(ids, dtype=np.int64)
+    valid = (ids >= 0) & (ids < num_windows)
+    rows = np.nonzero(valid)[0]
+    order = np.argsort(ids[rows], kind="stable")
+    perm = rows[order]
+    counts = np.bincount(ids[rows], minlength=num_windows)
+    offsets = np.zeros(num_windows + 1, dtype=np.int64)
+    offsets[1:] = np.cumsum(counts)
+    return perm.astype(np.int64), offsets, int((~valid).sum())
+
+
+def chunk_plan_ref(offsets: np.ndarray, chunk_rows: int):
+    """This library's chunk plan over window-sorted rows (plain sequential rule).
+
+    With L = chunk_rows and P = L // 2:
+      * an empty window gets no chunk;
+      * a window with more than P rows ("long") is one chunk of its own;
+      * windows with 1..P rows ("short") are packed: a short window opens a new
+        chunk unless the previous non-empty window is short and starts in the
+        same P-row page (page = start_row // P).  A packed chunk therefore never
+        splits a window and never exceeds 2P - 1 = L - 1 rows.
+    A chunk runs from its first window's start row to the next chunk's start row
+    (the last one to offsets[-1]); its window range runs to the next chunk's first
+    window (the last one to num_windows), so trailing empty windows are included.
+
+    Returns an int64 array [n_chunks, 4] of (row_begin, row_end, win_begin, win_end).
+    """
+    off = [int(x) for x in offsets]
+    nw = len(off) - 1
+    page = chunk_rows // 2
+    starts = []  # (row_begin, win_begin)
+    prev = None  # (start_row, is_long) of the previous non-empty window
+    for w in range(nw):
+        n = off[w + 1] - off[w]
+        if n <= 0:
+            continue
+        is_long = n > page
+        if is_long or prev is None or prev[1] or (prev[0] // page) != (off[w] // page):
+            starts.append((off[w], w))
+        prev = (off[w], is_long)
+    chunks = []
+    for i, (rb, wb) in enumerate(starts):
+        if i + 1 < len(starts):
+            re, we = starts[i + 1]
+        else:
+            re, we = off[nw], nw
+        chunks.append((rb, re, wb, we))
+    return np.asarray(chunks, dtype=np.int64).reshape(-1, 4)
+
+
+def _window_rows(offsets, perm, w):
+    lo, hi = int(offsets[w]), int(offsets[w + 1])
+    if perm is None:
+        return np.arange(lo, hi)
+    return np.asarray(perm[lo:hi], dtype=np.int64)
+
+
+# -------------------------------------------------------------------------- forward
+def sla_forward_ref(q, k, v, offsets, perm=None):
+    """SLA forward, Eq. (2)-(3), per window and per head.
+
+    q, k, v: float64 [n, H, d] in original row order.  offsets: [W + 1] CSR over
+    sorted positions; perm: sorted position -> original row (None = identity,
+    i.e. rows already window-sorted).  For window w with rows R and each head:
+        S = sum_{j in R} phi(k_j)^T v_j      (d x d)
+        z = sum_{j in R} phi(k_j)            (d)
+        o_i = (phi(q_i) S) / (phi(q_i) . z)  for every i in R.
+    Rows that belong to no window are NaN.
+    """
+    q = np.asarray(q, dtype=np.float64)
+    k = np.asarray(k, dtype=np.float64)
+    v = np.asarray(v, dtype=np.float64)
+    out = np.full(q.shape, np.nan)
+    for w in range(len(offsets) - 1):
+        rows = _window_rows(offsets, perm, w)
+        if rows.size == 0:
+            continue
+        fq = phi(q[rows])  # [m, H, d]
+        fk = phi(k[rows])
+        vv = v[rows]
+        S = np.einsum("mhe,mhc->hec", fk, vv)
+        z = fk.sum(axis=0)  # [H, d]
+        num = np.einsum("mhe,hec->mhc", fq, S)
+        den = np.einsum("mhe,he->mh", fq, z)
+        out[rows] = num / den[:, :, None]
+    return out
+
+
+# ------------------------------------------------------------------------- backward
+def sla_backward_ref(q, k, v, dout, offsets, perm=None):
+    """Gradients of sum(dout * SLA(q, k, v)) with respect to q, k, v.
+
+    Derived from Eq. (3) by the chain rule (the paper does not write them out).
+    Per window and head, with fq_i = phi(q_i), fk_j = phi(k_j), S, z as in the
+    forward, den_i = fq_i . z and o_i = fq_i S / den_i:
+        g_i   = dout_i / den_i                      d loss / d num_i
+        s_i   = -(dout_i . o_i) / den_i             d loss / d den_i
+        dfq_i = g_i S^T + s_i z                     d loss / d phi(q_i)
+        dS    = sum_i fq_i^T g_i ,  dz = sum_i s_i fq_i
+        dfk_j = v_j dS^T + dz ,     dv_j = fk_j dS
+        dq = dfq * phi'(q) ,        dk = dfk * phi'(k)
+    Rows that belong to no window are NaN.
+    """
+    q = np.asarray(q, dtype=np.float64)
+    k = np.asarray(k, dtype=np.float64)
+    v = np.asarray(v, dtype=np.float64)
+    dout = np.asarray(dout, dtype=np.float64)
+    dq = np.full(q.shape, np.nan)
+    dk = np.full(q.shape, np.nan)
+    dv = np.full(q.shape, np.nan)
+    for w in range(len(offsets) - 1):
+        rows = _window_rows(offsets, perm, w)
+        if rows.size == 0:
+            continue
+        qq, kk, vv, do = q[rows], k[rows], v[rows], dout[rows]
+        fq, fk = phi(qq), phi(kk)
+        S = np.einsum("mhe,mhc->hec", fk, vv)
+        z = fk.sum(axis=0)
+        den = np.einsum("mhe,he->mh", fq, z)
+        o = np.einsum("mhe,hec->mhc", fq, S) / den[:, :, None]
+        g = do / den[:, :, None]
+        s = -np.einsum("mhc,mhc->mh", do, o) / den
+        dfq = np.einsum("mhc,hec->mhe", g, S) + s[:, :, None] * z[None, :, :]
+        dS = np.einsum("mhe,mhc->hec", fq, g)
+        dz = np.einsum("mh,mhe->he", s, fq)
+        dfk = np.einsum("mhc,hec->mhe", vv, dS) + dz[None, :, :]
+        dv[rows] = np.einsum("mhe,hec->mhc", fk, dS)
+        dq[rows] = dfq * dphi(qq)
+        dk[rows] = dfk * dphi(kk)
+    return dq, dk, dv

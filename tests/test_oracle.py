@@ -1,0 +1,227 @@
+"""CPU tests: the oracle against its pins, and mutation tests showing that a
+plausible mistake planted in a copy of the oracle fails at least one pin."""
+import importlib.util
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+from oracle import sla_ref
+from tests import pins
+
+import workloads
+
+
+# ------------------------------------------------------------------ widening
+def test_widen_exact():
+    assert oracle.widen(np.array([0x3F80, 0xC000, 0x0000, 0x3E80], dtype=np.uint16), "bf16").tolist() == [
+        1.0, -2.0, 0.0, 0.25]
+    x = np.array([1.0, -2.5, 65504.0, 6.103515625e-05], dtype=np.float16)
+    assert oracle.widen(x, "f16").tolist() == [1.0, -2.5, 65504.0, 6.103515625e-05]
+    # bf16 rounding of the generator is round-to-nearest-even
+    f = np.array([1.0 + 2 ** -8, 1.0 + 3 * 2 ** -8, -(1.0 + 2 ** -9)], dtype=np.float32)
+    assert oracle.widen(workloads.to_bf16_bits(f), "bf16").tolist() == [1.0, 1.0 + 2 ** -6, -1.0]
+
+
+def test_phi_values():
+    x = np.array([-1000.0, -1.0, 0.0, 0.5, 3.0])
+    assert np.allclose(oracle.phi(x), [0.0, np.exp(-1.0), 1.0, 1.5, 4.0], rtol=0, atol=1e-300)
+    assert np.allclose(oracle.dphi(x), [0.0, np.exp(-1.0), 1.0, 1.0, 1.0], rtol=0, atol=1e-300)
+
+
+# ------------------------------------------------------------ segment builder
+@pytest.mark.parametrize("seed", range(6))
+def test_segments_vs_enumeration(seed):
+    rng = np.random.default_rng(seed)
+    W = int(rng.integers(1, 40))
+    n = int(rng.integers(0, 300))
+    ids = rng.integers(-2, W + 2, size=n)
+    perm, off, inv = oracle.segments_ref(ids, W)
+    p2, o2 = pins.segments_plain(ids, W)
+    assert np.array_equal(perm, p2)
+    assert np.array_equal(off, o2)
+    assert inv == int(((ids < 0) | (ids >= W)).sum())
+    # invariants: ids[perm] non-decreasing, ties ascending, offsets[W] = #valid
+    s = ids[perm]
+    assert np.all(np.diff(s) >= 0)
+    same = np.diff(s) == 0
+    assert np.all(np.diff(perm)[same] > 0)
+    assert off[-1] == n - inv
+
+
+# ---------------------------------------------------------------- chunk plan
+def _check_plan_invariants(off, L, chunks):
+    off = np.asarray(off)
+    nw = len(off) - 1
+    page = L // 2
+    lengths = np.diff(off)
+    # covers [first non-empty start, N) exactly once, in order
+    nonempty = np.nonzero(lengths > 0)[0]
+    if nonempty.size == 0:
+        assert len(chunks) == 0
+        return
+    assert chunks[0][0] == off[nonempty[0]]
+    assert chunks[-1][1] == off[-1]
+    assert chunks[-1][3] == nw
+    for a, b in zip(chunks[:-1], chunks[1:]):
+        assert a[1] == b[0] and a[3] == b[2]
+    for rb, re, wb, we in chunks:
+        assert rb < re and wb < we
+        assert off[wb] == rb and off[we] == re          # whole windows only
+        inside = lengths[wb:we]
+        if (inside > page).any():                      # a long window is alone
+            assert (inside > 0).sum() == 1
+        else:
+            assert re - rb <= L - 1                     # packs stay under L rows
+            starts = off[wb:we][inside > 0]
+            assert np.all(starts // page == starts[0] // page)
+
+
+@pytest.mark.parametrize("seed", range(8))
+@pytest.mark.parametrize("L", [32, 64, 128, 256])
+def test_chunk_plan_invariants(seed, L):
+    rng = np.random.default_rng([seed, L])
+    W = int(rng.integers(1, 200))
+    lengths = rng.integers(0, 3 * L, size=W) * (rng.random(W) < 0.8)
+    if seed % 3 == 0:
+        lengths = rng.integers(0, 8, size=W)
+    off = workloads.offsets_from_lengths(lengths).astype(np.int64)
+    _check_plan_invariants(off, L, oracle.chunk_plan_ref(off, L).tolist())
+
+
+def test_chunk_plan_hand_example():
+    # L = 8, pages of 4 rows.  Windows: 3, 0, 2, 5, 1, 1, 0, 2 rows.
+    # rows:  w0 [0,3)  w1 empty  w2 [3,5)  w3 [5,10) long  w4 [10,11)  w5 [11,12)
+    #        w6 empty  w7 [12,14)
+    # w0 opens; w2 starts at row 3 (page 0, same as w0) -> joins; w3 is long -> alone;
+    # w4 follows a long window -> opens; w5 starts at 11 (page 2, same as w4's 10) ->
+    # joins; w7 starts at 12 (page 3) -> opens.
+    off = workloads.offsets_from_lengths(np.array([3, 0, 2, 5, 1, 1, 0, 2]))
+    got = oracle.chunk_plan_ref(off, 8).tolist()
+    assert got == [[0, 5, 0, 3], [5, 10, 3, 4], [10, 12, 4, 7], [12, 14, 7, 8]]
+
+
+def test_chunk_plan_empty():
+    assert oracle.chunk_plan_ref(np.zeros(5, dtype=np.int64), 64).shape == (0, 4)
+
+
+# ------------------------------------------------------------------ forward pins
+def test_forward_pins():
+    assert pins.forward_pin_failures(oracle.sla_forward_ref, oracle.segments_ref) == []
+
+
+def test_forward_single_window_is_plain_linear_attention():
+    # Sec. 3.1: with one window SLA is kernelised linear attention on the whole
+    # sequence, phi(Q)(phi(K)^T V) / phi(Q)(phi(K)^T 1).
+    rng = np.random.default_rng(1)
+    q, k, v = (rng.standard_normal((20, 3, 6)) for _ in range(3))
+    fq = np.where(q > 0, q + 1, np.exp(np.minimum(q, 0)))
+    fk = np.where(k > 0, k + 1, np.exp(np.minimum(k, 0)))
+    ref = np.stack([fq[:, h] @ (fk[:, h].T @ v[:, h]) / (fq[:, h] @ fk[:, h].sum(0))[:, None]
+                    for h in range(3)], axis=1)
+    out = oracle.sla_forward_ref(q, k, v, np.array([0, 20]), None)
+    assert pins.rel_err(out, ref) < 1e-13
+
+
+def test_forward_empty_and_invalid_rows():
+    ids = np.array([3, -1, 3, 7, 0])
+    rng = np.random.default_rng(2)
+    q, k, v = (rng.standard_normal((5, 1, 2)) for _ in range(3))
+    perm, off, inv = oracle.segments_ref(ids, 5)
+    assert inv == 2
+    o = oracle.sla_forward_ref(q, k, v, off, perm)
+    assert np.isnan(o[1]).all() and np.isnan(o[3]).all()
+    assert np.isfinite(o[[0, 2, 4]]).all()
+    assert np.allclose(o[4], v[4], rtol=1e-15)
+
+
+# ----------------------------------------------------------------- backward pins
+def test_backward_pins():
+    assert pins.backward_pin_failures(oracle.sla_backward_ref, oracle.sla_forward_ref,
+                                      oracle.segments_ref) == []
+
+
+# -------------------------------------------------------------- mutation tests
+class _NumpyProxy:
+    """numpy with einsum rewritten for chosen subscripts (mutation tests only)."""
+
+    def __init__(self, rewrite):
+        self._rewrite = rewrite
+
+    def __getattr__(self, name):
+        return getattr(np, name)
+
+    def einsum(self, sub, *ops):
+        if sub in self._rewrite:
+            return self._rewrite[sub](*ops)
+        return np.einsum(sub, *ops)
+
+
+def _fresh_oracle():
+    path = os.path.join(os.path.dirname(sla_ref.__file__), "sla_ref.py")
+    spec = importlib.util.spec_from_file_location("sla_ref_mutant", path)
+    mod = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(mod)
+    return mod
+
+
+FWD_MUTANTS = {
+    "state_transposed": {"einsum": {"mhe,mhc->hec": lambda a, b: np.einsum("mhe,mhc->hce", a, b)}},
+    "no_normaliser": {"einsum": {"mhe,he->mh": lambda a, b: np.ones(a.shape[:2])}},
+    "normaliser_from_first_feature": {"einsum": {"mhe,he->mh": lambda a, b: a[:, :, 0] * b[None, :, 0]}},
+    "phi_relu_plus_one": {"phi": lambda x: np.maximum(np.asarray(x, float), 0) + 1},
+    "phi_exp_everywhere": {"phi": lambda x: np.exp(np.asarray(x, float))},
+    "phi_shifted_branch": {"phi": lambda x: np.where(np.asarray(x) > 0, np.asarray(x) + 1, np.exp(np.asarray(x)) + 1e-3)},
+}
+
+BWD_MUTANTS = {
+    "dS_transposed": {"einsum": {"mhc,hec->mhe": lambda a, b: np.einsum("mhc,hce->mhe", a, b)}},
+    "no_dz": {"einsum": {"mh,mhe->he": lambda a, b: np.zeros(b.shape[1:])}},
+    "wrong_sign_s": {"einsum": {"mhc,mhc->mh": lambda a, b: -np.einsum("mhc,mhc->mh", a, b)}},
+    "no_dphi": {"dphi": lambda x: np.ones_like(np.asarray(x, float))},
+    "dv_uses_transposed_dS": {"einsum": {"mhe,hec->mhc": lambda a, b: np.einsum("mhe,hce->mhc", a, b)}},
+}
+
+
+def _apply(mod, spec):
+    if "einsum" in spec:
+        mod.np = _NumpyProxy(spec["einsum"])
+    for name in ("phi", "dphi"):
+        if name in spec:
+            setattr(mod, name, spec[name])
+    return mod
+
+
+@pytest.mark.parametrize("name", sorted(FWD_MUTANTS))
+def test_forward_mutant_is_caught(name):
+    mod = _apply(_fresh_oracle(), FWD_MUTANTS[name])
+    with np.errstate(all="ignore"):
+        fails = pins.forward_pin_failures(mod.sla_forward_ref, oracle.segments_ref)
+    assert fails, f"planted mistake {name} passed every forward pin"
+
+
+@pytest.mark.parametrize("name", sorted(BWD_MUTANTS))
+def test_backward_mutant_is_caught(name):
+    mod = _apply(_fresh_oracle(), BWD_MUTANTS[name])
+    with np.errstate(all="ignore"):
+        fails = pins.backward_pin_failures(mod.sla_backward_ref, oracle.sla_forward_ref,
+                                           oracle.segments_ref)
+    assert fails, f"planted mistake {name} passed every backward pin"
+
+
+def test_segments_mutant_is_caught():
+    # an unstable sort is a plausible mistake: ties must keep row order
+    def unstable(ids, W):
+        ids = np.asarray(ids)
+        valid = (ids >= 0) & (ids < W)
+        rows = np.nonzero(valid)[0]
+        perm = rows[np.argsort(-ids[rows], kind="stable")[::-1]]
+        off = np.concatenate([[0], np.cumsum(np.bincount(ids[rows], minlength=W))])
+        return perm, off, int((~valid).sum())
+
+    rng = np.random.default_rng(0)
+    ids = rng.integers(0, 5, size=50)
+    p1, _, _ = unstable(ids, 5)
+    p2, _ = pins.segments_plain(ids, 5)
+    assert not np.array_equal(p1, p2)
