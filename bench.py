@@ -1,0 +1,290 @@
+#!/usr/bin/env python3
+"""Benchmark of the SLA hot path on one MI355X.
+
+Default workload: the training step on Waymo-like frame shapes -- segment build
+(window-id sort, offsets, chunk plan) + SLA forward + SLA backward, fp16 storage
+with fp32 accumulation, H = 4 heads of d = 32 (C = 128), ~60k voxels in 1,521
+window slots, rows re-shuffled every step so the builder really sorts.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 5]
+
+Prints ONE JSON line.  `value` is voxels per second over the timed K steps
+(inputs resident in HBM, buffers rotated over enough sets that the 256 MB
+Infinity Cache cannot serve repeats).  The timed steps are replayed from HIP
+graphs, one per buffer set, so host launch overhead is not measured.  A second,
+eager pass times every kernel with HIP events on the launch stream; the
+dominant kernel's average duration gives `roofline.achieved`.  `cpu_baseline`
+times the CPU oracle (test infrastructure) on a bounded sample on this host.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0       # MI355X HBM3E, AMD published peak
+MALL_BYTES = 256 << 20      # Infinity Cache
+METRIC = "SLA fwd+bwd voxels/s and ms/frame (N≈60k, C=128); % of HBM roofline"
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=300)
+    p.add_argument("--warmup", type=int, default=30)
+    p.add_argument("--config", type=int, default=5, choices=[1, 2, 3, 4, 5])
+    p.add_argument("--chunk-rows", type=int, default=0)
+    p.add_argument("--no-graph", action="store_true", help="time eager launches instead of graph replay")
+    p.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    p.add_argument("--cpu-seconds", type=float, default=12.0)
+    return p.parse_args()
+
+
+def elem_size(dtype):
+    return {"f32": 4, "f16": 2, "bf16": 2}[dtype]
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py: this build measures one GPU only (asked for --gpus {args.gpus}); "
+              "SLA shards by window ranges with no exchange, see DESIGN.md", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    import workloads
+    from paper_2401_00912_amd import sla
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    sla.lib()
+
+    cfg = args.config
+    training = cfg == 5
+    base = workloads.make_config(cfg, with_grad=training)
+    n, H, d, W, dt = base["n"], base["heads"], base["head_dim"], base["num_windows"], base["dtype"]
+    e = elem_size(dt)
+    C = H * d
+    row_bytes = C * e
+    tdt = {"f32": torch.float32, "f16": torch.float16, "bf16": torch.bfloat16}[dt]
+
+    def dev_vals(a):
+        t = torch.from_numpy(np.ascontiguousarray(a))
+        if dt == "bf16":
+            t = t.view(torch.bfloat16)
+        return t.to(dev)
+
+    per_set = (8 if training else 4) * n * row_bytes + 8 * n + sla.plan_bytes(n, W)
+    nsets = max(3, int(np.ceil(2 * MALL_BYTES / per_set)) + 1)
+    sets = []
+    for s in range(nsets):
+        wl = workloads.shuffled(base, [cfg, 2, s]) if base["ids"] is not None else base
+        st = {
+            "q": dev_vals(wl["q"]), "k": dev_vals(wl["k"]), "v": dev_vals(wl["v"]),
+            "o": torch.empty((n, H, d), dtype=tdt, device=dev),
+        }
+        if base["ids"] is not None:
+            st["ids"] = torch.from_numpy(wl["ids"]).to(dev)
+        else:
+            st["offsets"] = torch.from_numpy(wl["offsets"].astype(np.int32)).to(dev)
+        st["plan_buf"] = sla.new_plan_buffer(n, W, dev)
+        if training:
+            st["dout"] = dev_vals(wl["dout"])
+            st["dq"] = torch.empty_like(st["q"])
+            st["dk"] = torch.empty_like(st["q"])
+            st["dv"] = torch.empty_like(st["q"])
+        sets.append(st)
+
+    def build(st):
+        if "ids" in st:
+            return sla.build_segments(st["ids"], num_windows=W, chunk_rows=args.chunk_rows,
+                                      plan_buf=st["plan_buf"], want_perm=False)
+        return sla.build_segments(None, num_windows=W, chunk_rows=args.chunk_rows, offsets=st["offsets"],
+                                  n=n, plan_buf=st["plan_buf"])
+
+    plans = [build(st) for st in sets]   # forward-only configs time forward given a plan
+    torch.cuda.synchronize()
+
+    def step(i, ev=None):
+        st = sets[i % nsets]
+        if ev is not None:
+            ev[0].record()
+        if training:
+            plan = build(st)
+        else:
+            plan = plans[i % nsets]
+        if ev is not None:
+            ev[1].record()
+        sla.forward(plan, st["q"], st["k"], st["v"], out=st["o"])
+        if ev is not None:
+            ev[2].record()
+        if training:
+            sla.backward(plan, st["q"], st["k"], st["v"], st["dout"], st["dq"], st["dk"], st["dv"])
+        if ev is not None:
+            ev[3].record()
+
+    stream = torch.cuda.current_stream(dev)
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+
+    # ---- headline: K steps, graph replay (one graph per buffer set)
+    graphs = None
+    if not args.no_graph:
+        try:
+            graphs = []
+            cap = torch.cuda.Stream(dev)
+            cap.wait_stream(stream)
+            with torch.cuda.stream(cap):
+                for s in range(nsets):
+                    g = torch.cuda.CUDAGraph()
+                    with torch.cuda.graph(g, stream=cap):
+                        step(s)
+                    graphs.append(g)
+            stream.wait_stream(cap)
+            for g in graphs:          # replays must reproduce eager results: run each once
+                g.replay()
+            torch.cuda.synchronize()
+        except Exception as exc:  # noqa: BLE001
+            print(f"bench.py: graph capture unavailable ({exc}); timing eager launches", file=sys.stderr)
+            graphs = None
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0.record()
+    for i in range(args.steps):
+        if graphs is not None:
+            graphs[i % nsets].replay()
+        else:
+            step(i)
+    t1.record()
+    torch.cuda.synchronize()
+    ms_total = t0.elapsed_time(t1)
+    ms_step = ms_total / args.steps
+
+    # ---- per-kernel breakdown: eager launches bracketed by events on the launch stream.
+    # A spin kernel first lets the host enqueue every step before the GPU reaches them,
+    # so the events bracket device time only.
+    nb = min(args.steps, 100)
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(nb)]
+    torch.cuda.synchronize()
+    try:
+        torch.cuda._sleep(int(2e8))
+    except Exception:  # noqa: BLE001
+        pass
+    for i in range(nb):
+        step(i, evs[i])
+    torch.cuda.synchronize()
+    t_build = float(np.mean([a[0].elapsed_time(a[1]) for a in evs])) if training else 0.0
+    t_fwd = float(np.mean([a[1].elapsed_time(a[2]) for a in evs]))
+    t_bwd = float(np.mean([a[2].elapsed_time(a[3]) for a in evs])) if training else 0.0
+
+    fwd_bytes = 4 * n * row_bytes
+    bwd_bytes = 7 * n * row_bytes
+    if training:
+        dom, dom_ms, dom_bytes = "k_sla_bwd", t_bwd, bwd_bytes
+    else:
+        dom, dom_ms, dom_bytes = "k_sla_fwd", t_fwd, fwd_bytes
+    achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
+    step_bytes = (fwd_bytes + bwd_bytes + 8 * n) if training else fwd_bytes
+
+    nonempty = int((np.diff(plans[0].offsets.cpu().numpy()) > 0).sum())
+    frames = base.get("frames", 1)
+    out = {
+        "metric": METRIC,
+        "value": n / (ms_step * 1e-3),
+        "unit": "voxels/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "ms_per_frame": ms_step / frames,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": dt,
+        "data": "synthetic",
+        "config": {
+            "workload": base["name"],
+            "phases": "build+forward+backward" if training else "forward (plan built outside the timed region)",
+            "n": n, "heads": H, "head_dim": d, "num_windows": W, "nonempty_windows": nonempty,
+            "frames": frames, "buffer_sets": nsets, "graph_replay": graphs is not None,
+            "chunk_rows": args.chunk_rows or int(sla.lib().sla_default_chunk_rows()),
+        },
+        "roofline": {
+            "bound": "hbm",
+            "kernel": dom,
+            "achieved": achieved,
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": achieved / HBM_PEAK_GBS,
+            "traffic": None,
+            "algorithmic_bytes": dom_bytes,
+            "avg_ms": dom_ms,
+        },
+        "breakdown_ms": {"build": t_build, "forward": t_fwd, "backward": t_bwd},
+        "step_roofline_frac": step_bytes / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS,
+    }
+    if not args.no_cpu:
+        out["cpu_baseline"] = cpu_baseline(base, training, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+def cpu_baseline(base, training, budget_s):
+    """The CPU oracle as it stands, on whole frames of the same workload."""
+    import oracle
+
+    try:
+        from threadpoolctl import threadpool_limits
+    except ImportError:  # pragma: no cover
+        threadpool_limits = None
+    dt = base["dtype"]
+    q, k, v = (oracle.widen(base[x], dt) for x in ("q", "k", "v"))
+    do = oracle.widen(base["dout"], dt) if training else None
+
+    def one():
+        if base["ids"] is not None:
+            perm, off, _ = oracle.segments_ref(base["ids"], base["num_windows"])
+        else:
+            perm, off = None, base["offsets"].astype(np.int64)
+        oracle.sla_forward_ref(q, k, v, off, perm)
+        if training:
+            oracle.sla_backward_ref(q, k, v, do, off, perm)
+
+    ctx = threadpool_limits(limits=1) if threadpool_limits else None
+    if ctx:
+        ctx.__enter__()
+    try:
+        reps, t_start = 0, time.perf_counter()
+        while True:
+            one()
+            reps += 1
+            if time.perf_counter() - t_start >= budget_s:
+                break
+        el = time.perf_counter() - t_start
+    finally:
+        if ctx:
+            ctx.__exit__(None, None, None)
+    per = el / reps
+    return {
+        "value": base["n"] / per,
+        "unit": "voxels/s",
+        "cores": 1,
+        "kind": "oracle",
+        "sample": f"{reps} whole frame(s) of N={base['n']} voxels, "
+                  f"{'segments+forward+backward' if training else 'segments+forward'} in numpy float64, "
+                  f"{el:.1f} s wall, 1 thread",
+        "ms_per_frame": per * 1e3,
+    }
+
+
+if __name__ == "__main__":
+    main()

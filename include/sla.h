@@ -1,0 +1,159 @@
+/*
+ * sla.h -- C ABI of libsla, Scattered Linear Attention (SLA) on AMD Instinct
+ * MI355X (gfx950).
+ *
+ * SLA ("ScatterFormer", He et al., arXiv 2401.00912, Sec. 3.2) applies linear
+ * attention separately inside every window of a voxel scene, with all voxels of
+ * the scene held in ONE flattened matrix ordered by window (Sec. 3.2, Fig. 3(a)):
+ *
+ *   Eq. (2)  SLA(Q, K, V) = Concat_j LA(Q^j, K^j, V^j) over the non-empty windows;
+ *   Eq. (3)  for window w and each head, with phi the kernel feature map,
+ *              S_w = sum_{i in w} phi(k_i)^T v_i ,   z_w = sum_{i in w} phi(k_i),
+ *              o_i = phi(q_i) S_w / (phi(q_i) . z_w)     for every i in w.
+ *
+ * Readings of the paper fixed by this library:
+ *   phi(x) = elu(x) + 1 (x + 1 for x > 0, exp(x) otherwise): the feature map of
+ *     the linear-attention paper Sec. 3.2 cites for LA;
+ *   attention is non-causal inside a window (Eq. (3) sums over the whole window);
+ *   no 1/sqrt(d) scale and no epsilon in the denominator (Eq. (3) has neither);
+ *   heads are independent; channel c of a row is head c / head_dim.
+ *
+ * Conventions shared by every entry point:
+ *   - Every pointer argument except `plan_bytes`-style sizes is a DEVICE pointer
+ *     on the current HIP device.  The caller owns all memory; the library never
+ *     allocates, frees or synchronises.
+ *   - `stream` is a hipStream_t (NULL = the null stream).  All device work is
+ *     enqueued on it, in order; calls return before the work finishes.
+ *   - Argument errors that the host can see are reported synchronously, before
+ *     anything is enqueued, by the returned status.  A failed launch gives
+ *     SLA_E_HIP.
+ *   - Rows: q, k, v, o, dout, dq, dk, dv are row-major contiguous
+ *     [n, heads, head_dim] arrays of `dtype`, in the caller's ORIGINAL row order
+ *     (the library gathers and scatters through the plan's permutation), with
+ *     16-byte aligned base pointers.  head_dim must be 16 or 32.
+ *   - Stateless and re-entrant: concurrent calls on different streams are safe
+ *     when they use different output buffers and different plans.
+ */
+#ifndef SLA_H
+#define SLA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  SLA_OK = 0,
+  SLA_E_ARG = 1,          /* null / misaligned pointer, negative size, bad enum  */
+  SLA_E_UNSUPPORTED = 2,  /* head_dim not 16/32, too many windows                */
+  SLA_E_WORKSPACE = 3,    /* plan buffer smaller than sla_plan_bytes()           */
+  SLA_E_HIP = 4           /* a HIP launch or runtime call failed                 */
+} sla_status_t;
+
+typedef enum { SLA_F32 = 0, SLA_F16 = 1, SLA_BF16 = 2 } sla_dtype_t;
+
+typedef void* sla_stream_t; /* hipStream_t */
+
+/* Version of this interface (bumped on any incompatible change). */
+int32_t sla_abi_version(void);
+
+/* Static description of a status code; never NULL. */
+const char* sla_status_string(sla_status_t status);
+
+/* Largest window-slot count supported (window tables live in on-chip memory). */
+int32_t sla_max_windows(void);
+
+/* Chunk length used when sla_build_segments() is given chunk_rows = 0. */
+int32_t sla_default_chunk_rows(void);
+
+/*
+ * Bytes of the plan buffer for n rows and num_windows window slots.
+ * The plan holds the window-sorted view of the rows (Sec. 3.2: the flattened,
+ * window-ordered matrix), its CSR window offsets, the chunk table (Fig. 3(a); the
+ * Fig. 5 caption's "offsets generation" = start row of each chunk) and the
+ * builder's scratch.  Returns 0 for invalid sizes.
+ */
+size_t sla_plan_bytes(int64_t n, int32_t num_windows);
+
+/* Byte offsets of the plan's sections (for inspection by tests and tools). */
+typedef struct {
+  size_t header;     /* 64-byte header, see below                          */
+  size_t perm;       /* int32[n]: sorted position -> original row           */
+  size_t offsets;    /* int32[num_windows + 1]: CSR over sorted positions   */
+  size_t chunks;     /* int32[max_chunks][4]: row_begin, row_end,
+                        win_begin, win_end                                  */
+  size_t total;      /* == sla_plan_bytes(n, num_windows)                   */
+  int32_t max_chunks;
+} sla_plan_layout_t;
+/* Plan header (int32 fields in order): magic, n, num_windows, chunk_rows,
+ * n_chunks, csr (1 = rows were already window-sorted), invalid. */
+
+sla_status_t sla_plan_layout(int64_t n, int32_t num_windows, sla_plan_layout_t* out /* host */);
+
+/*
+ * Segment builder: the "sort by window, flatten, partition into chunks" steps of
+ * Sec. 3.2 / Fig. 3(a) and the chunk offsets of the Fig. 5 caption.
+ *
+ * Mode A, window_ids != NULL (int32[n], one window slot per row, rows in any
+ * order): stable sort of the rows by window id.  Writes into the plan
+ *   perm[p]     original row at sorted position p; rows of one window keep their
+ *               original relative order, so the result is unique;
+ *   offsets[w]  first sorted position of window w (empty windows allowed);
+ * and the chunk table.  If perm_out / offsets are not NULL they receive copies
+ * (int32[n] / int32[num_windows + 1]).  Rows whose id is outside
+ * [0, num_windows) are counted and left out of every window; their output rows
+ * are then never written.
+ *
+ * Mode B, window_ids == NULL: rows are already window-sorted and `offsets`
+ * (int32[num_windows + 1], device) is an INPUT: offsets[0] = 0, non-decreasing,
+ * offsets[num_windows] = n.  perm_out must be NULL (the permutation is the
+ * identity).  Violations are counted; the plan is then clamped into range so no
+ * kernel reads out of bounds, but outputs are undefined.
+ *
+ * Chunk table (both modes), with L = chunk_rows (0 = default; else even, 32..4096)
+ * and pages of L/2 rows: an empty window gets no chunk; a window of more than L/2
+ * rows is a chunk of its own; shorter windows are packed into one chunk while
+ * they start in the same page, so a packed chunk never splits a window and never
+ * exceeds L - 1 rows.
+ *
+ * invalid_count (device int32, may be NULL) receives the number of out-of-range
+ * ids (mode A) or offset violations (mode B).  The plan must be at least
+ * sla_plan_bytes(n, num_windows) bytes, 256-byte aligned.  Valid for num_windows
+ * in [1, sla_max_windows()].
+ */
+sla_status_t sla_build_segments(const int32_t* window_ids, int64_t n, int32_t num_windows,
+                                int32_t chunk_rows, int32_t* perm_out, int32_t* offsets,
+                                int32_t* invalid_count, void* plan, size_t plan_bytes,
+                                sla_stream_t stream);
+
+/*
+ * Forward, Eq. (2)-(3): o = SLA(q, k, v).  `plan` must have been built by
+ * sla_build_segments() with the same n and num_windows (the kernels check the
+ * plan header and write nothing otherwise).  Every row that belongs to a window
+ * is written; a window of one row returns its own value (to rounding).
+ * Arithmetic: phi and the normaliser in fp32; the two contractions phi(K)^T V and
+ * phi(Q) S on the matrix cores with fp32 accumulation, their operands rounded to
+ * `dtype` (fp32 stays fp32).
+ */
+sla_status_t sla_forward(const void* plan, size_t plan_bytes, int64_t n, int32_t num_windows,
+                         sla_dtype_t dtype, int32_t heads, int32_t head_dim, const void* q,
+                         const void* k, const void* v, void* o, sla_stream_t stream);
+
+/*
+ * Backward of Eq. (3) (the paper trains the model but does not write the
+ * gradients; they follow from Eq. (3) by the chain rule): given dout = dL/do,
+ * writes dq, dk, dv for every row that belongs to a window.  Window states are
+ * recomputed from k and v; the state gradients are accumulated in fp32.
+ */
+sla_status_t sla_backward(const void* plan, size_t plan_bytes, int64_t n, int32_t num_windows,
+                          sla_dtype_t dtype, int32_t heads, int32_t head_dim, const void* q,
+                          const void* k, const void* v, const void* dout, void* dq, void* dk,
+                          void* dv, sla_stream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SLA_H */

@@ -1,0 +1,129 @@
+// C ABI of libsla: argument validation (synchronous, before any launch) and
+// dispatch to the kernels.  No allocation, no synchronisation.
+#include "sla.h"
+#include "sla_common.h"
+
+#define SLA_EXPORT extern "C" __attribute__((visibility("default")))
+
+namespace sla {
+hipError_t launch_build(const int32_t* ids, int32_t n, int32_t W, int32_t L, int32_t* perm_out,
+                        int32_t* offsets_io, int32_t* invalid_out, void* plan, hipStream_t stream);
+hipError_t launch_forward(const void* plan, int32_t n, int32_t W, int dtype, int32_t H, int32_t d,
+                          const void* q, const void* k, const void* v, void* o,
+                          hipStream_t stream);
+hipError_t launch_backward(const void* plan, int32_t n, int32_t W, int dtype, int32_t H,
+                           int32_t d, const void* q, const void* k, const void* v,
+                           const void* dout, void* dq, void* dk, void* dv, hipStream_t stream);
+}  // namespace sla
+
+namespace {
+
+constexpr int32_t kAbiVersion = 1;
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
+
+bool sizes_ok(int64_t n, int32_t W) { return n >= 0 && n < INT32_MAX && W >= 1; }
+
+sla_status_t check_tensor_args(int64_t n, int32_t W, int dtype, int32_t heads, int32_t head_dim,
+                               const void* plan, size_t plan_bytes) {
+  if (!sizes_ok(n, W) || heads < 1) return SLA_E_ARG;
+  if (dtype < 0 || dtype > 2) return SLA_E_ARG;
+  if (head_dim != 16 && head_dim != 32) return SLA_E_UNSUPPORTED;
+  if (W > sla::kMaxWindows) return SLA_E_UNSUPPORTED;
+  if ((int64_t)heads * head_dim > (1 << 20)) return SLA_E_UNSUPPORTED;
+  if (n > 0 && (int64_t)n * heads * head_dim > ((int64_t)1 << 40)) return SLA_E_UNSUPPORTED;
+  if (plan == nullptr || !aligned(plan, 256)) return SLA_E_ARG;
+  if (plan_bytes < sla::plan_layout(n, W).total) return SLA_E_WORKSPACE;
+  return SLA_OK;
+}
+
+sla_status_t hip_status(hipError_t e) { return e == hipSuccess ? SLA_OK : SLA_E_HIP; }
+
+}  // namespace
+
+SLA_EXPORT int32_t sla_abi_version(void) { return kAbiVersion; }
+
+SLA_EXPORT const char* sla_status_string(sla_status_t s) {
+  switch (s) {
+    case SLA_OK: return "SLA_OK";
+    case SLA_E_ARG: return "SLA_E_ARG: invalid argument (null/misaligned pointer, bad size or enum)";
+    case SLA_E_UNSUPPORTED: return "SLA_E_UNSUPPORTED: head_dim must be 16 or 32; too many windows";
+    case SLA_E_WORKSPACE: return "SLA_E_WORKSPACE: plan buffer smaller than sla_plan_bytes()";
+    case SLA_E_HIP: return "SLA_E_HIP: HIP runtime or launch failure";
+  }
+  return "SLA: unknown status";
+}
+
+SLA_EXPORT int32_t sla_max_windows(void) { return sla::kMaxWindows; }
+
+SLA_EXPORT int32_t sla_default_chunk_rows(void) { return sla::kDefaultChunkRows; }
+
+SLA_EXPORT size_t sla_plan_bytes(int64_t n, int32_t num_windows) {
+  if (!sizes_ok(n, num_windows) || num_windows > sla::kMaxWindows) return 0;
+  return sla::plan_layout(n, num_windows).total;
+}
+
+SLA_EXPORT sla_status_t sla_plan_layout(int64_t n, int32_t num_windows, sla_plan_layout_t* out) {
+  if (out == nullptr || !sizes_ok(n, num_windows)) return SLA_E_ARG;
+  if (num_windows > sla::kMaxWindows) return SLA_E_UNSUPPORTED;
+  const sla::PlanLayout L = sla::plan_layout(n, num_windows);
+  out->header = L.header;
+  out->perm = L.perm;
+  out->offsets = L.offsets;
+  out->chunks = L.chunks;
+  out->total = L.total;
+  out->max_chunks = L.max_chunks;
+  return SLA_OK;
+}
+
+SLA_EXPORT sla_status_t sla_build_segments(const int32_t* window_ids, int64_t n,
+                                           int32_t num_windows, int32_t chunk_rows,
+                                           int32_t* perm_out, int32_t* offsets,
+                                           int32_t* invalid_count, void* plan, size_t plan_bytes,
+                                           sla_stream_t stream) {
+  if (!sizes_ok(n, num_windows)) return SLA_E_ARG;
+  if (num_windows > sla::kMaxWindows) return SLA_E_UNSUPPORTED;
+  if (chunk_rows == 0) chunk_rows = sla::kDefaultChunkRows;
+  if (chunk_rows < sla::kMinChunkRows || chunk_rows > sla::kMaxChunkRows || (chunk_rows & 1))
+    return SLA_E_ARG;
+  if (plan == nullptr || !aligned(plan, 256)) return SLA_E_ARG;
+  if (plan_bytes < sla::plan_layout(n, num_windows).total) return SLA_E_WORKSPACE;
+  if (window_ids == nullptr) {
+    if (offsets == nullptr || perm_out != nullptr) return SLA_E_ARG;  // CSR input mode
+  } else if (n > 0 && !aligned(window_ids, 4)) {
+    return SLA_E_ARG;
+  }
+  return hip_status(sla::launch_build(window_ids,
+                                      (int32_t)n, num_windows, chunk_rows, perm_out, offsets,
+                                      invalid_count, plan, static_cast<hipStream_t>(stream)));
+}
+
+SLA_EXPORT sla_status_t sla_forward(const void* plan, size_t plan_bytes, int64_t n,
+                                    int32_t num_windows, sla_dtype_t dtype, int32_t heads,
+                                    int32_t head_dim, const void* q, const void* k, const void* v,
+                                    void* o, sla_stream_t stream) {
+  const sla_status_t st = check_tensor_args(n, num_windows, (int)dtype, heads, head_dim, plan, plan_bytes);
+  if (st != SLA_OK) return st;
+  if (n == 0) return SLA_OK;
+  if (!q || !k || !v || !o) return SLA_E_ARG;
+  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(o, 16)) return SLA_E_ARG;
+  return hip_status(sla::launch_forward(plan, (int32_t)n, num_windows, (int)dtype, heads, head_dim,
+                                        q, k, v, o, static_cast<hipStream_t>(stream)));
+}
+
+SLA_EXPORT sla_status_t sla_backward(const void* plan, size_t plan_bytes, int64_t n,
+                                     int32_t num_windows, sla_dtype_t dtype, int32_t heads,
+                                     int32_t head_dim, const void* q, const void* k,
+                                     const void* v, const void* dout, void* dq, void* dk, void* dv,
+                                     sla_stream_t stream) {
+  const sla_status_t st = check_tensor_args(n, num_windows, (int)dtype, heads, head_dim, plan, plan_bytes);
+  if (st != SLA_OK) return st;
+  if (n == 0) return SLA_OK;
+  if (!q || !k || !v || !dout || !dq || !dk || !dv) return SLA_E_ARG;
+  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(dout, 16) ||
+      !aligned(dq, 16) || !aligned(dk, 16) || !aligned(dv, 16))
+    return SLA_E_ARG;
+  return hip_status(sla::launch_backward(plan, (int32_t)n, num_windows, (int)dtype, heads,
+                                         head_dim, q, k, v, dout, dq, dk, dv,
+                                         static_cast<hipStream_t>(stream)));
+}

@@ -1,0 +1,241 @@
+"""Python binding of libsla (ctypes).  Argument marshalling only: every step of
+the SLA path runs in the HIP library; torch supplies device memory and the
+current stream.  There is no fallback: if the library is missing or no GPU is
+present the calls raise.
+
+Functions mirror the C ABI in include/sla.h:
+    plan_bytes(n, num_windows)
+    plan_layout(n, num_windows)
+    build_segments(ids | offsets, num_windows, chunk_rows=0) -> Plan
+    forward(plan, q, k, v, out=None) -> o
+    backward(plan, q, k, v, dout, dq=None, dk=None, dv=None) -> (dq, dk, dv)
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsla.so")
+
+SLA_OK, SLA_E_ARG, SLA_E_UNSUPPORTED, SLA_E_WORKSPACE, SLA_E_HIP = range(5)
+
+EXPORTED = (
+    "sla_abi_version",
+    "sla_status_string",
+    "sla_max_windows",
+    "sla_default_chunk_rows",
+    "sla_plan_bytes",
+    "sla_plan_layout",
+    "sla_build_segments",
+    "sla_forward",
+    "sla_backward",
+)
+
+
+class SlaError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        self.status = status
+        super().__init__(f"{what}: {status_string(status)}")
+
+
+class PlanLayout(ctypes.Structure):
+    _fields_ = [
+        ("header", ctypes.c_size_t),
+        ("perm", ctypes.c_size_t),
+        ("offsets", ctypes.c_size_t),
+        ("chunks", ctypes.c_size_t),
+        ("total", ctypes.c_size_t),
+        ("max_chunks", ctypes.c_int32),
+    ]
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load libsla.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"libsla.so not built at {LIB_PATH}; run python -m paper_2401_00912_amd.build")
+    L = ctypes.CDLL(LIB_PATH)
+    i32, i64, sz, vp = ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t, ctypes.c_void_p
+    L.sla_abi_version.restype = i32
+    L.sla_abi_version.argtypes = []
+    L.sla_status_string.restype = ctypes.c_char_p
+    L.sla_status_string.argtypes = [ctypes.c_int]
+    L.sla_max_windows.restype = i32
+    L.sla_max_windows.argtypes = []
+    L.sla_default_chunk_rows.restype = i32
+    L.sla_default_chunk_rows.argtypes = []
+    L.sla_plan_bytes.restype = sz
+    L.sla_plan_bytes.argtypes = [i64, i32]
+    L.sla_plan_layout.restype = ctypes.c_int
+    L.sla_plan_layout.argtypes = [i64, i32, ctypes.POINTER(PlanLayout)]
+    L.sla_build_segments.restype = ctypes.c_int
+    L.sla_build_segments.argtypes = [vp, i64, i32, i32, vp, vp, vp, vp, sz, vp]
+    L.sla_forward.restype = ctypes.c_int
+    L.sla_forward.argtypes = [vp, sz, i64, i32, ctypes.c_int, i32, i32, vp, vp, vp, vp, vp]
+    L.sla_backward.restype = ctypes.c_int
+    L.sla_backward.argtypes = [vp, sz, i64, i32, ctypes.c_int, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp]
+    _lib = L
+    return L
+
+
+def status_string(status: int) -> str:
+    return lib().sla_status_string(int(status)).decode()
+
+
+def _check(status: int, what: str):
+    if status != SLA_OK:
+        raise SlaError(status, what)
+
+
+def plan_bytes(n: int, num_windows: int) -> int:
+    return int(lib().sla_plan_bytes(int(n), int(num_windows)))
+
+
+def plan_layout(n: int, num_windows: int) -> PlanLayout:
+    out = PlanLayout()
+    _check(lib().sla_plan_layout(int(n), int(num_windows), ctypes.byref(out)), "sla_plan_layout")
+    return out
+
+
+# ----------------------------------------------------------------- torch glue
+def _torch():
+    import torch
+
+    return torch
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(device):
+    torch = _torch()
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _dtype_code(dt) -> int:
+    torch = _torch()
+    codes = {torch.float32: 0, torch.float16: 1, torch.bfloat16: 2}
+    if dt not in codes:
+        raise TypeError(f"SLA supports float32, float16 and bfloat16, not {dt}")
+    return codes[dt]
+
+
+@dataclass
+class Plan:
+    """Device plan of one scene: window-sorted row order, offsets and chunks."""
+
+    buf: object          # torch uint8 tensor on the device (the plan bytes)
+    n: int
+    num_windows: int
+    chunk_rows: int
+    perm: object         # int32 [n] copy of the permutation, or None (CSR mode)
+    offsets: object      # int32 [num_windows + 1]
+    invalid: object      # int32 [1]
+
+    @property
+    def nbytes(self) -> int:
+        return int(self.buf.numel())
+
+
+def new_plan_buffer(n: int, num_windows: int, device):
+    torch = _torch()
+    nb = plan_bytes(n, num_windows)
+    if nb == 0:
+        raise SlaError(SLA_E_ARG, "sla_plan_bytes")
+    return torch.empty(nb, dtype=torch.uint8, device=device)
+
+
+def build_segments(ids=None, num_windows: int = 0, chunk_rows: int = 0, offsets=None,
+                   plan_buf=None, want_perm: bool = True, n: int | None = None) -> Plan:
+    """Mode A: ids (int32 [n] device tensor).  Mode B: offsets (int32 [W+1]) of
+    already window-sorted rows, with n given."""
+    torch = _torch()
+    if ids is not None:
+        if ids.dtype != torch.int32 or not ids.is_contiguous():
+            raise TypeError("window ids must be a contiguous int32 tensor")
+        n = ids.numel()
+        device = ids.device
+    else:
+        if offsets is None or n is None:
+            raise ValueError("give ids, or offsets and n")
+        device = offsets.device
+    if plan_buf is None:
+        plan_buf = new_plan_buffer(n, num_windows, device)
+    invalid = torch.empty(1, dtype=torch.int32, device=device)  # always written by the builder
+    perm = None
+    ids_arg = ids
+    if ids is not None:
+        perm = torch.empty(n, dtype=torch.int32, device=device) if want_perm else None
+        if offsets is None:
+            offsets = torch.empty(num_windows + 1, dtype=torch.int32, device=device)
+        if n == 0:
+            # an empty tensor has a NULL data pointer, which the C ABI reads as CSR mode
+            ids_arg = torch.zeros(1, dtype=torch.int32, device=device)
+    st = lib().sla_build_segments(_ptr(ids_arg), int(n), int(num_windows), int(chunk_rows), _ptr(perm),
+                                  _ptr(offsets), _ptr(invalid), _ptr(plan_buf),
+                                  int(plan_buf.numel()), _stream(device))
+    _check(st, "sla_build_segments")
+    cr = chunk_rows if chunk_rows else int(lib().sla_default_chunk_rows())
+    return Plan(plan_buf, int(n), int(num_windows), cr, perm, offsets, invalid)
+
+
+def _check_rows(name, t, n, like=None):
+    if t.dim() != 3 or t.shape[0] != n or not t.is_contiguous():
+        raise ValueError(f"{name} must be a contiguous [n, heads, head_dim] tensor with n={n}")
+    if like is not None and (t.shape != like.shape or t.dtype != like.dtype or t.device != like.device):
+        raise ValueError(f"{name} must match q in shape, dtype and device")
+
+
+def forward(plan: Plan, q, k, v, out=None):
+    torch = _torch()
+    _check_rows("q", q, plan.n)
+    _check_rows("k", k, plan.n, q)
+    _check_rows("v", v, plan.n, q)
+    if out is None:
+        out = torch.empty_like(q)
+    _check_rows("out", out, plan.n, q)
+    H, d = q.shape[1], q.shape[2]
+    st = lib().sla_forward(_ptr(plan.buf), plan.nbytes, plan.n, plan.num_windows, _dtype_code(q.dtype),
+                           H, d, _ptr(q), _ptr(k), _ptr(v), _ptr(out), _stream(q.device))
+    _check(st, "sla_forward")
+    return out
+
+
+def backward(plan: Plan, q, k, v, dout, dq=None, dk=None, dv=None):
+    torch = _torch()
+    for name, t in (("q", q), ("k", k), ("v", v), ("dout", dout)):
+        _check_rows(name, t, plan.n, q)
+    dq = torch.empty_like(q) if dq is None else dq
+    dk = torch.empty_like(q) if dk is None else dk
+    dv = torch.empty_like(q) if dv is None else dv
+    for name, t in (("dq", dq), ("dk", dk), ("dv", dv)):
+        _check_rows(name, t, plan.n, q)
+    H, d = q.shape[1], q.shape[2]
+    st = lib().sla_backward(_ptr(plan.buf), plan.nbytes, plan.n, plan.num_windows, _dtype_code(q.dtype),
+                            H, d, _ptr(q), _ptr(k), _ptr(v), _ptr(dout), _ptr(dq), _ptr(dk), _ptr(dv),
+                            _stream(q.device))
+    _check(st, "sla_backward")
+    return dq, dk, dv
+
+
+def read_plan(plan: Plan):
+    """Host copy of the plan's header, perm, offsets and chunk table (tests)."""
+    import numpy as np
+
+    lay = plan_layout(plan.n, plan.num_windows)
+    raw = plan.buf.cpu().numpy()
+    hdr = raw[lay.header: lay.header + 64].view(np.int32)
+    header = dict(zip(("magic", "n", "num_windows", "chunk_rows", "n_chunks", "csr", "invalid"),
+                      hdr[:7].tolist()))
+    perm = raw[lay.perm: lay.perm + 4 * plan.n].view(np.int32)
+    offs = raw[lay.offsets: lay.offsets + 4 * (plan.num_windows + 1)].view(np.int32)
+    nc = max(0, min(header["n_chunks"], lay.max_chunks))
+    chunks = raw[lay.chunks: lay.chunks + 16 * nc].view(np.int32).reshape(nc, 4)
+    return header, perm, offs, chunks

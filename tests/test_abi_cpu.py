@@ -1,0 +1,120 @@
+"""CPU tests of the C ABI: the built library loads, exports every function that
+include/sla.h declares, and rejects bad arguments synchronously (host-side checks
+run before anything is launched, so no GPU is needed)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2401_00912_amd import sla
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "sla.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(sla_[a-z_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(sla.LIB_PATH):
+        from paper_2401_00912_amd import build
+
+        build.build()
+    return sla.lib()
+
+
+def test_header_declares_the_abi():
+    assert declared_functions() == sorted(sla.EXPORTED)
+
+
+def test_every_declared_symbol_is_exported(L):
+    for name in declared_functions():
+        assert hasattr(L, name), name
+
+
+def test_only_the_abi_is_exported():
+    import subprocess
+
+    out = subprocess.run(["nm", "-D", "--defined-only", sla.LIB_PATH], capture_output=True, text=True).stdout
+    ours = sorted({l.split()[-1] for l in out.splitlines() if " T sla_" in l})
+    assert ours == sorted(sla.EXPORTED)
+
+
+def test_queries(L):
+    assert L.sla_abi_version() == 1
+    assert L.sla_max_windows() == 16384
+    assert L.sla_default_chunk_rows() == 128
+    for s in range(5):
+        assert sla.status_string(s).startswith("SLA_")
+    assert sla.plan_bytes(0, 1) > 0
+    assert sla.plan_bytes(-1, 4) == 0
+    assert sla.plan_bytes(10, 0) == 0
+    assert sla.plan_bytes(10, 16385) == 0
+    lay = sla.plan_layout(60000, 1521)
+    assert lay.total == sla.plan_bytes(60000, 1521)
+    assert lay.header == 0 and lay.perm % 256 == 0 and lay.offsets % 256 == 0 and lay.chunks % 256 == 0
+    assert lay.offsets >= lay.perm + 4 * 60000
+    assert lay.chunks >= lay.offsets + 4 * 1522
+    assert lay.max_chunks == 1521
+
+
+FAKE = 1 << 20  # a 256-aligned fake device address: never dereferenced, every call below fails validation
+
+
+def fwd(L, **kw):
+    a = dict(plan=FAKE, plan_bytes=sla.plan_bytes(100, 8), n=100, W=8, dtype=1, H=4, d=32,
+             q=FAKE, k=FAKE, v=FAKE, o=FAKE)
+    a.update(kw)
+    return L.sla_forward(a["plan"], a["plan_bytes"], a["n"], a["W"], a["dtype"], a["H"], a["d"],
+                         a["q"], a["k"], a["v"], a["o"], None)
+
+
+def test_forward_argument_errors(L):
+    assert fwd(L, d=24) == sla.SLA_E_UNSUPPORTED
+    assert fwd(L, d=64) == sla.SLA_E_UNSUPPORTED
+    assert fwd(L, H=0) == sla.SLA_E_ARG
+    assert fwd(L, n=-1) == sla.SLA_E_ARG
+    assert fwd(L, W=0) == sla.SLA_E_ARG
+    assert fwd(L, W=20000, plan_bytes=1 << 30) == sla.SLA_E_UNSUPPORTED
+    assert fwd(L, dtype=7) == sla.SLA_E_ARG
+    assert fwd(L, plan=None) == sla.SLA_E_ARG
+    assert fwd(L, plan=FAKE + 16) == sla.SLA_E_ARG
+    assert fwd(L, plan_bytes=100) == sla.SLA_E_WORKSPACE
+    assert fwd(L, q=None) == sla.SLA_E_ARG
+    assert fwd(L, o=FAKE + 2) == sla.SLA_E_ARG
+    assert fwd(L, n=0) == sla.SLA_OK  # nothing to do, nothing launched
+
+
+def test_backward_argument_errors(L):
+    nb = sla.plan_bytes(100, 8)
+    args = [FAKE, nb, 100, 8, 1, 4, 32] + [FAKE] * 7 + [None]
+    bad = list(args)
+    bad[6] = 8
+    assert L.sla_backward(*bad) == sla.SLA_E_UNSUPPORTED
+    bad = list(args)
+    bad[10] = None  # dout
+    assert L.sla_backward(*bad) == sla.SLA_E_ARG
+    bad = list(args)
+    bad[1] = 10
+    assert L.sla_backward(*bad) == sla.SLA_E_WORKSPACE
+
+
+def test_build_argument_errors(L):
+    nb = sla.plan_bytes(100, 8)
+    b = lambda ids, n, W, L_, perm, off, plan, pb: L.sla_build_segments(  # noqa: E731
+        ids, n, W, L_, perm, off, None, plan, pb, None)
+    assert b(FAKE, 100, 8, 33, None, None, FAKE, nb) == sla.SLA_E_ARG       # odd chunk rows
+    assert b(FAKE, 100, 8, 16, None, None, FAKE, nb) == sla.SLA_E_ARG       # too small
+    assert b(FAKE, 100, 8, 8192, None, None, FAKE, nb) == sla.SLA_E_ARG     # too large
+    assert b(FAKE, 100, 8, 0, None, None, FAKE, 64) == sla.SLA_E_WORKSPACE
+    assert b(FAKE, 100, 8, 0, None, None, None, nb) == sla.SLA_E_ARG
+    assert b(None, 100, 8, 0, None, None, FAKE, nb) == sla.SLA_E_ARG        # CSR mode needs offsets
+    assert b(None, 100, 8, 0, FAKE, FAKE, FAKE, nb) == sla.SLA_E_ARG        # CSR mode has no perm
+    assert b(FAKE + 1, 100, 8, 0, None, None, FAKE, nb) == sla.SLA_E_ARG    # misaligned ids
+    assert b(FAKE, 100, 16385, 0, None, None, FAKE, 1 << 30) == sla.SLA_E_UNSUPPORTED
+    assert b(FAKE, -5, 8, 0, None, None, FAKE, nb) == sla.SLA_E_ARG

@@ -1,0 +1,315 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle.
+
+Builder outputs (perm, offsets, chunk table) must match bit for bit; outputs and
+gradients must match within 1e-5 (fp32) or 2e-2 (fp16/bf16) per head, measured
+as max|x - ref| / max(max|ref|, floor) with floor = 1e-3 max|v| (o),
+1e-3 max|dout| (dv) and 1e-3 max|dout| max|v| (dq, dk).
+"""
+from __future__ import annotations
+
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+import workloads
+from tests.gpu_util import TOL, p999, rel_err_per_head, to_dev, to_host64
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def sla():
+    import torch
+
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2401_00912_amd import sla as S
+
+    S.lib()
+    return S
+
+
+# ------------------------------------------------------------------- helpers
+def build(S, ids=None, W=None, chunk_rows=0, offsets=None, n=None):
+    import torch
+
+    if ids is not None:
+        plan = S.build_segments(to_dev(ids.astype(np.int32)), num_windows=W, chunk_rows=chunk_rows)
+    else:
+        plan = S.build_segments(None, num_windows=W, chunk_rows=chunk_rows,
+                                offsets=to_dev(offsets.astype(np.int32)), n=n)
+    torch.cuda.synchronize()
+    return plan
+
+
+def check_plan(S, plan, ids, W, chunk_rows, offsets_in=None):
+    header, perm, offs, chunks = S.read_plan(plan)
+    L = chunk_rows or 128
+    if ids is not None:
+        p_ref, o_ref, inv = oracle.segments_ref(ids, W)
+        nvalid = len(p_ref)
+        assert header["invalid"] == inv
+        assert int(plan.invalid.cpu()[0]) == inv
+        assert np.array_equal(offs.astype(np.int64), o_ref), "offsets differ"
+        assert np.array_equal(perm[:nvalid].astype(np.int64), p_ref), "perm differs"
+        assert np.array_equal(plan.perm.cpu().numpy()[:nvalid].astype(np.int64), p_ref)
+        assert np.array_equal(plan.offsets.cpu().numpy().astype(np.int64), o_ref)
+        assert header["csr"] == 0
+    else:
+        o_ref = offsets_in.astype(np.int64)
+        assert np.array_equal(offs.astype(np.int64), o_ref)
+        assert header["csr"] == 1
+    ch_ref = oracle.chunk_plan_ref(o_ref, L)
+    assert header["n_chunks"] == len(ch_ref)
+    assert np.array_equal(chunks.astype(np.int64), ch_ref), "chunk table differs"
+    assert header["magic"] == 0x534C4131 and header["chunk_rows"] == L
+    return o_ref, (p_ref if ids is not None else None)
+
+
+def run_forward(S, plan, wl_q, wl_k, wl_v, dtype):
+    import torch
+
+    q, k, v = to_dev(wl_q, dtype), to_dev(wl_k, dtype), to_dev(wl_v, dtype)
+    o = torch.full_like(q, float("nan"))
+    S.forward(plan, q, k, v, out=o)
+    torch.cuda.synchronize()
+    return to_host64(o, dtype)
+
+
+def forward_parity(S, ids, offsets, n, W, q, k, v, dtype, chunk_rows=0, label=""):
+    plan = build(S, ids=ids, W=W, chunk_rows=chunk_rows, offsets=offsets, n=n)
+    off, perm = check_plan(S, plan, ids, W, chunk_rows, offsets)
+    got = run_forward(S, plan, q, k, v, dtype)
+    w = lambda a: oracle.widen(a, dtype)  # noqa: E731
+    ref = oracle.sla_forward_ref(w(q), w(k), w(v), off, perm)
+    rows = ~np.isnan(ref[:, 0, 0])
+    floor = 1e-3 * max(float(np.abs(w(v)).max()) if v.size else 1.0, 1e-30)
+    err = rel_err_per_head(got, ref, floor, rows)
+    _say(f"[fwd {label}] n={n} W={W} dtype={dtype} rel_err={err:.3e} p99.9={p999(got[rows], ref[rows]):.3e}")
+    assert err <= TOL[dtype], f"{label}: forward relative error {err:.3e}"
+    return got, ref
+
+
+def backward_parity(S, ids, offsets, n, W, q, k, v, do, dtype, chunk_rows=0, label=""):
+    import torch
+
+    plan = build(S, ids=ids, W=W, chunk_rows=chunk_rows, offsets=offsets, n=n)
+    off, perm = check_plan(S, plan, ids, W, chunk_rows, offsets)
+    tq, tk, tv, tdo = (to_dev(a, dtype) for a in (q, k, v, do))
+    outs = [torch.full_like(tq, float("nan")) for _ in range(3)]
+    S.backward(plan, tq, tk, tv, tdo, *outs)
+    torch.cuda.synchronize()
+    got = [to_host64(t, dtype) for t in outs]
+    w = lambda a: oracle.widen(a, dtype)  # noqa: E731
+    ref = oracle.sla_backward_ref(w(q), w(k), w(v), w(do), off, perm)
+    rows = ~np.isnan(ref[0][:, 0, 0])
+    mv, mdo = float(np.abs(w(v)).max()), float(np.abs(w(do)).max())
+    floors = (1e-3 * mdo * mv, 1e-3 * mdo * mv, 1e-3 * mdo)
+    for name, x, r, fl in zip(("dq", "dk", "dv"), got, ref, floors):
+        err = rel_err_per_head(x, r, fl, rows)
+        _say(f"[bwd {label}] {name} n={n} dtype={dtype} rel_err={err:.3e}")
+        assert err <= TOL[dtype], f"{label}: {name} relative error {err:.3e}"
+    return got, ref
+
+
+# ------------------------------------------------------------------- builder
+@pytest.mark.parametrize("cfg", [2, 3, 4, 5])
+def test_builder_configs(sla, cfg):
+    wl = workloads.make_config(cfg, with_grad=False)
+    _say(f"[builder cfg{cfg}] n={wl['n']} W={wl['num_windows']}")
+    for L in (0, 64, 256):
+        plan = build(sla, ids=wl["ids"], W=wl["num_windows"], chunk_rows=L)
+        check_plan(sla, plan, wl["ids"], wl["num_windows"], L)
+
+
+@pytest.mark.parametrize("seed", range(10))
+def test_builder_random(sla, seed):
+    rng = np.random.default_rng([7, seed])
+    W = int(rng.choice([1, 2, 3, 63, 64, 1000, 4096, 8192, 8193, 16384]))
+    n = int(rng.choice([0, 1, 5, 777, 4096, 65537, 130000]))
+    ids = rng.integers(0, W, size=n).astype(np.int32)
+    if seed % 3 == 1 and n:
+        bad = rng.random(n) < 0.01
+        ids[bad] = rng.choice([-1, W, W + 5, -(2 ** 31)], size=int(bad.sum()))
+    if seed % 4 == 2:
+        ids = np.sort(ids)
+    L = int(rng.choice([32, 64, 128, 512, 4096]))
+    _say(f"[builder random {seed}] n={n} W={W} L={L}")
+    plan = build(sla, ids=ids, W=W, chunk_rows=L)
+    check_plan(sla, plan, ids, W, L)
+
+
+def test_builder_degenerate(sla):
+    for ids, W in ((np.zeros(5000, np.int32), 1), (np.full(5000, 7, np.int32), 64),
+                   (np.arange(3000, dtype=np.int32)[::-1].copy(), 3000),
+                   (np.full(10, -3, np.int32), 4)):
+        plan = build(sla, ids=ids, W=W)
+        check_plan(sla, plan, ids, W, 0)
+
+
+def test_builder_csr(sla):
+    wl = workloads.make_config(1)
+    plan = build(sla, W=wl["num_windows"], offsets=wl["offsets"], n=wl["n"])
+    check_plan(sla, plan, None, wl["num_windows"], 0, wl["offsets"])
+    # violations are counted and the plan stays in range
+    bad = wl["offsets"].copy()
+    bad[10], bad[11] = bad[11] + 5, bad[10]
+    plan = build(sla, W=wl["num_windows"], offsets=bad, n=wl["n"])
+    header, _, offs, chunks = sla.read_plan(plan)
+    assert header["invalid"] > 0
+    assert np.all(np.diff(offs) >= 0) and offs.min() >= 0 and offs.max() <= wl["n"]
+    assert np.all(chunks[:, 0] <= chunks[:, 1]) and chunks[:, 1].max() <= wl["n"]
+
+
+# ------------------------------------------------------------------- forward
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4])
+def test_forward_config(sla, cfg):
+    wl = workloads.make_config(cfg)
+    _say(f"[fwd cfg{cfg}] {wl['name']}")
+    forward_parity(sla, wl["ids"], wl["offsets"], wl["n"], wl["num_windows"], wl["q"], wl["k"], wl["v"],
+                   wl["dtype"], label=f"cfg{cfg}")
+
+
+SHAPES = [(2, 32), (4, 32), (8, 16), (8, 32), (1, 16), (3, 32)]
+
+
+def _adversarial_lengths(rng, L):
+    return np.array([0, 1, 1, L - 1, L, L + 1, 1024, 2, 0, 0, L // 2, L // 2 + 1, 3, 17, 33, 31, 32,
+                     64, 65, 1, 100, 5], dtype=np.int64)[rng.permutation(22)]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "f16", "bf16"])
+@pytest.mark.parametrize("shape", SHAPES)
+def test_forward_shapes(sla, dtype, shape):
+    H, d = shape
+    rng = np.random.default_rng([11, H, d, len(dtype)])
+    lengths = _adversarial_lengths(rng, 128)
+    ids = workloads.ids_from_lengths(lengths, rng)
+    n, W = ids.size, lengths.size
+    q, k, v = (workloads.normal_values(rng, n, H, d, dtype) for _ in range(3))
+    forward_parity(sla, ids, None, n, W, q, k, v, dtype, label=f"shape{shape}")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "f16", "bf16"])
+def test_forward_special_layouts(sla, dtype):
+    rng = np.random.default_rng([12, len(dtype)])
+    H, d = 4, 32
+    cases = {
+        "one_window": np.array([3000]),
+        "all_singletons": np.ones(2000, dtype=np.int64),
+        "empty_slots": np.array([0, 0, 5, 0, 0, 0, 40, 0]),
+        "long_window": np.array([2500, 3, 1]),
+    }
+    for name, lengths in cases.items():
+        ids = workloads.ids_from_lengths(lengths, rng)
+        n, W = ids.size, lengths.size
+        q, k, v = (workloads.normal_values(rng, n, H, d, dtype) for _ in range(3))
+        got, ref = forward_parity(sla, ids, None, n, W, q, k, v, dtype, label=name)
+        if name == "all_singletons":
+            vv = oracle.widen(v, dtype)
+            assert rel_err_per_head(got, vv, 1e-3) <= TOL[dtype]
+
+
+@pytest.mark.parametrize("L", [32, 64, 256, 4096])
+def test_forward_chunk_rows(sla, L):
+    wl = workloads.make_config(2)
+    forward_parity(sla, wl["ids"], None, wl["n"], wl["num_windows"], wl["q"], wl["k"], wl["v"], wl["dtype"],
+                   chunk_rows=L, label=f"L{L}")
+
+
+def test_forward_large_values(sla):
+    # operands are scaled before rounding to 16 bits: big windows of big values must not overflow
+    rng = np.random.default_rng(13)
+    lengths = np.array([1024, 500, 7, 1])
+    ids = workloads.ids_from_lengths(lengths, rng)
+    n = ids.size
+    q = workloads.cast_values(rng.standard_normal((n, 2, 32)).astype(np.float32) * 4, "f16")
+    k = workloads.cast_values(rng.standard_normal((n, 2, 32)).astype(np.float32) * 4, "f16")
+    v = workloads.cast_values(rng.standard_normal((n, 2, 32)).astype(np.float32) * 3000, "f16")
+    forward_parity(sla, ids, None, n, 4, q, k, v, "f16", label="large")
+
+
+def test_forward_window_independence_and_determinism(sla):
+    import torch
+
+    wl = workloads.make_config(2)
+    dtype = wl["dtype"]
+    plan = build(sla, ids=wl["ids"], W=wl["num_windows"])
+    a = run_forward(sla, plan, wl["q"], wl["k"], wl["v"], dtype)
+    b = run_forward(sla, plan, wl["q"], wl["k"], wl["v"], dtype)
+    assert np.array_equal(a, b), "repeat runs differ"
+    # change every value outside window 0 of the rows' windows: window 0's rows are unchanged
+    target = int(np.bincount(wl["ids"]).argmax())
+    other = wl["ids"] != target
+    q2, k2, v2 = wl["q"].copy(), wl["k"].copy(), wl["v"].copy()
+    q2[other] = -q2[other]
+    k2[other] = k2[other] * 2
+    v2[other] = v2[other] + 1
+    c = run_forward(sla, plan, q2, k2, v2, dtype)
+    mine = ~other
+    assert np.array_equal(a[mine], c[mine])
+    torch.cuda.synchronize()
+
+
+def test_n_zero(sla):
+    import torch
+
+    plan = build(sla, ids=np.zeros(0, np.int32), W=5)
+    header, _, offs, chunks = sla.read_plan(plan)
+    assert header["n_chunks"] == 0 and np.all(offs == 0)
+    q = torch.empty((0, 2, 32), dtype=torch.float16, device="cuda")
+    sla.forward(plan, q, q, q)
+    sla.backward(plan, q, q, q, q)
+    torch.cuda.synchronize()
+
+
+# ------------------------------------------------------------------ backward
+def test_backward_config5(sla):
+    wl = workloads.make_config(5)
+    _say(f"[bwd cfg5] {wl['name']}")
+    backward_parity(sla, wl["ids"], None, wl["n"], wl["num_windows"], wl["q"], wl["k"], wl["v"], wl["dout"],
+                    wl["dtype"], label="cfg5")
+    # cfg 5 re-shuffles rows every iteration: a re-shuffled frame must also match
+    sh = workloads.shuffled(wl, [5, 2, 0])
+    backward_parity(sla, sh["ids"], None, sh["n"], sh["num_windows"], sh["q"], sh["k"], sh["v"], sh["dout"],
+                    sh["dtype"], label="cfg5-shuffled")
+    forward_parity(sla, sh["ids"], None, sh["n"], sh["num_windows"], sh["q"], sh["k"], sh["v"], sh["dtype"],
+                   label="cfg5-shuffled")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "f16", "bf16"])
+@pytest.mark.parametrize("shape", SHAPES)
+def test_backward_shapes(sla, dtype, shape):
+    H, d = shape
+    rng = np.random.default_rng([21, H, d, len(dtype)])
+    lengths = _adversarial_lengths(rng, 128)
+    ids = workloads.ids_from_lengths(lengths, rng)
+    n, W = ids.size, lengths.size
+    q, k, v, do = (workloads.normal_values(rng, n, H, d, dtype) for _ in range(4))
+    backward_parity(sla, ids, None, n, W, q, k, v, do, dtype, label=f"shape{shape}")
+
+
+def test_backward_csr_fp32(sla):
+    wl = workloads.make_config(1, with_grad=True)
+    backward_parity(sla, None, wl["offsets"], wl["n"], wl["num_windows"], wl["q"], wl["k"], wl["v"],
+                    wl["dout"], wl["dtype"], label="cfg1-bwd")
+
+
+def test_backward_determinism(sla):
+    import torch
+
+    wl = workloads.make_config(5)
+    plan = build(sla, ids=wl["ids"], W=wl["num_windows"])
+    tq, tk, tv, tdo = (to_dev(wl[x], "f16") for x in ("q", "k", "v", "dout"))
+    r1 = [t.clone() for t in sla.backward(plan, tq, tk, tv, tdo)]
+    r2 = sla.backward(plan, tq, tk, tv, tdo)
+    torch.cuda.synchronize()
+    for a, b in zip(r1, r2):
+        assert torch.equal(a, b)
