@@ -31,8 +31,9 @@
  *     [n, heads, head_dim] arrays of `dtype`, in the caller's ORIGINAL row order
  *     (the library gathers and scatters through the plan's permutation), with
  *     16-byte aligned base pointers.  head_dim must be 16 or 32.
- *   - Stateless and re-entrant: concurrent calls on different streams are safe
- *     when they use different output buffers and different plans.
+ *   - Re-entrant: concurrent calls on different streams are safe when they use
+ *     different output buffers and different plans (a plan carries the work
+ *     counters of the calls that use it).
  */
 #ifndef SLA_H
 #define SLA_H
@@ -88,7 +89,8 @@ typedef struct {
   int32_t max_chunks;
 } sla_plan_layout_t;
 /* Plan header (int32 fields in order): magic, n, num_windows, chunk_rows,
- * n_chunks, csr (1 = rows were already window-sorted), invalid. */
+ * n_chunks, csr (1 = rows were already window-sorted), invalid, then the work
+ * counters of the attention kernels (zero between calls). */
 
 sla_status_t sla_plan_layout(int64_t n, int32_t num_windows, sla_plan_layout_t* out /* host */);
 
@@ -131,13 +133,15 @@ sla_status_t sla_build_segments(const int32_t* window_ids, int64_t n, int32_t nu
 /*
  * Forward, Eq. (2)-(3): o = SLA(q, k, v).  `plan` must have been built by
  * sla_build_segments() with the same n and num_windows (the kernels check the
- * plan header and write nothing otherwise).  Every row that belongs to a window
+ * plan header and write nothing otherwise).  The call updates the plan's work
+ * counters and leaves them as it found them, so calls that overlap in time
+ * (on different streams) must use different plans.  Every row that belongs to a window
  * is written; a window of one row returns its own value (to rounding).
  * Arithmetic: phi and the normaliser in fp32; the two contractions phi(K)^T V and
  * phi(Q) S on the matrix cores with fp32 accumulation, their operands rounded to
  * `dtype` (fp32 stays fp32).
  */
-sla_status_t sla_forward(const void* plan, size_t plan_bytes, int64_t n, int32_t num_windows,
+sla_status_t sla_forward(void* plan, size_t plan_bytes, int64_t n, int32_t num_windows,
                          sla_dtype_t dtype, int32_t heads, int32_t head_dim, const void* q,
                          const void* k, const void* v, void* o, sla_stream_t stream);
 
@@ -147,7 +151,7 @@ sla_status_t sla_forward(const void* plan, size_t plan_bytes, int64_t n, int32_t
  * writes dq, dk, dv for every row that belongs to a window.  Window states are
  * recomputed from k and v; the state gradients are accumulated in fp32.
  */
-sla_status_t sla_backward(const void* plan, size_t plan_bytes, int64_t n, int32_t num_windows,
+sla_status_t sla_backward(void* plan, size_t plan_bytes, int64_t n, int32_t num_windows,
                           sla_dtype_t dtype, int32_t heads, int32_t head_dim, const void* q,
                           const void* k, const void* v, const void* dout, void* dq, void* dk,
                           void* dv, sla_stream_t stream);

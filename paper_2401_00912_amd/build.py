@@ -50,24 +50,27 @@ def _run(cmd):
     return err
 
 
-def build(verbose: bool = False) -> str:
-    os.makedirs(BUILD, exist_ok=True)
+def build(verbose: bool = False, defines=(), out: str = LIB, build_dir: str = BUILD) -> str:
+    """Compile and link.  `defines` (e.g. ["SLA_GRID_WGS=1024"]) and `out` /
+    `build_dir` exist for building tuning variants next to the default library."""
+    os.makedirs(build_dir, exist_ok=True)
     cc = hipcc()
-    objs = [os.path.join(BUILD, s.replace(".hip", ".o")) for s in SOURCES]
-    cmds = [[cc, *HIPCC_FLAGS, "-c", os.path.join(CSRC, s), "-o", o] for s, o in zip(SOURCES, objs)]
+    objs = [os.path.join(build_dir, s.replace(".hip", ".o")) for s in SOURCES]
+    dflags = [f"-D{d}" for d in defines]
+    cmds = [[cc, *HIPCC_FLAGS, *dflags, "-c", os.path.join(CSRC, s), "-o", o] for s, o in zip(SOURCES, objs)]
     with ThreadPoolExecutor(max_workers=len(cmds)) as ex:
         for cmd, err in zip(cmds, ex.map(_run, cmds)):
             if verbose:
                 print(" ".join(cmd))
             if err.strip() and verbose:
                 print(err)
-    tmp = LIB + ".tmp"
+    tmp = out + ".tmp"
     link = [cc, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp]
     _run(link)
-    os.replace(tmp, LIB)
+    os.replace(tmp, out)
     if verbose:
-        print("built", LIB)
-    return LIB
+        print("built", out)
+    return out
 
 
 if __name__ == "__main__":

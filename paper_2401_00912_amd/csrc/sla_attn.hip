@@ -1,41 +1,51 @@
 // SLA forward and backward on the gfx950 matrix cores.
 //
-// Work decomposition: one wavefront per (chunk, head); a workgroup holds the
-// waves of consecutive heads of one chunk, so the rows a workgroup gathers are
-// shared by its waves through the cache.  A chunk is a run of whole windows of
-// the window-sorted sequence (see the builder); the wave walks its windows, and
-// for each window
-//   1. streams the window's K and V rows (gathered through the plan's
-//      permutation) in 32-row tiles and accumulates the state
-//      S = phi(K)^T V on the matrix cores and z = sum phi(K) in fp32
-//      (Eq. (3) numerator and normaliser; the chunk-wise state accumulation of
-//      Sec. 3.2 / Fig. 3(b));
-//   2. streams the window's Q rows in 16-row tiles and writes
-//      o = phi(q) S / (phi(q) . z) (Eq. (3)).
-// The state never leaves the wave (registers + a per-wave LDS tile), so the only
-// HBM traffic is reading q, k, v and writing o.
+// Work decomposition.  One workgroup of 4 wavefronts per (chunk, head) item; the
+// hardware dispatcher hands workgroups to compute units as they free up.  A chunk is a run of whole windows of the window-sorted
+// sequence (see the builder).  Its rows are cut into 32-row slices and each wave
+// takes a contiguous range of slices, loading all of its rows at once (K, V, Q
+// and, for the backward, dout), so an item costs about one gather latency.
 //
-// Register layouts (lane l = 16 g + i, g = lane group 0..3, KS = head_dim / 4):
-//   natural fragment   lane (i, g) holds elements KS*g .. KS*g + KS - 1 of row i
-//                      of a 16-row tile -- one contiguous 16 B (d = 32, 16-bit)
-//                      or 8 B (d = 16, 16-bit) load per lane;
-//   transposed tile    the contraction over ROWS needs each lane to hold 8 rows
-//                      of one column; a natural fragment times a 0/1 selection
-//                      matrix on the matrix core (exact) yields lane (i, g)
-//                      holding rows 4g .. 4g+3 of column i, the standard 16x16
-//                      result layout.  Two 16-row sub-tiles give the 8 rows.
-// Contractions over the head dimension (phi(q) S, dS v^T, ...) take natural
-// fragments directly; their per-window matrix operand is read from the wave's
-// LDS copy of S (or dS), with the output-row order chosen so that each lane's
-// results are again KS consecutive elements of one row (one vector store).
+// Per window (Eq. (3); the chunk-wise state accumulation of Sec. 3.2 / Fig. 3(b)):
+//   state    S = phi(K)^T V and z = phi(K)^T 1 on the matrix cores over the
+//            window's rows (z is one more column of the same contraction);
+//   forward  o = phi(q) S / (phi(q) . z);
+//   backward dq from S, z; dS, dz (one more column again) from q, dout; then
+//            dk, dv from dS, dz.
+// A window inside one wave's rows is finished by that wave from registers.  A
+// window that crosses a wave boundary ("shared") is accumulated in parts, the
+// parts meet in LDS, and after a workgroup barrier every wave with rows of the
+// window sums all parts in a fixed order (so they all see bit-identical states)
+// and finishes its own rows.  Window states never reach HBM: the only traffic is
+// q, k, v (, dout) in and o (dq, dk, dv) out.  Rows that do not fit a wave's
+// registers (very long windows) are streamed slice by slice instead.
 //
-// 16-bit storage: matrix-core operands are rounded to the storage type.  Derived
-// operands are scaled by a power of two into [1, 2) (S, dS) or below 1
-// (phi(q)/den) before rounding, and the scale is divided out in fp32, so no
-// operand overflows or flushes; the normaliser, divisions and phi are fp32.
+// Register layouts (lane l = 16 g + i, g = lane group 0..3, KS = head_dim / 4,
+// NT = head_dim / 16; slot r of lane group g stands for head-dim index
+// E(g, r) = 16 (r / 4) + 4 g + r % 4):
+//   row fragment   lane (i, g) holds the KS elements E(g, .) of row i of a 16-row
+//                  sub-tile (NT loads of 4 consecutive elements);
+//   result tile    a 16x16 matrix-core result: lane (n, g) holds rows 4g..4g+3
+//                  of column n.
+// The slot order E is chosen so that a state accumulated as result tiles is
+// already the matrix operand of the next contraction and so that every
+// contraction's result is again a row fragment: states move between steps
+// without leaving registers.  A contraction over ROWS needs each lane to hold 8
+// rows of one column; multiplying a row fragment by a 0/1 selection matrix on
+// the matrix core (exact) gives lane (i, g) rows 4g..4g+3 of column i, and two
+// sub-tiles give the 8 rows.
+//
+// 16-bit storage: matrix-core operands are the stored values or values rounded to
+// the storage type.  Derived operands are scaled by a power of two into [1, 2)
+// (S, dS) or to at most 1 (phi(q)/den) before rounding and the scale is divided
+// out in fp32, so no operand overflows or flushes; phi, the denominators and all
+// divisions are fp32.
 #include "sla_common.h"
 
 namespace sla {
+
+constexpr int kWaves = 4;       // waves per workgroup (row ranges of a chunk)
+constexpr int kSliceRows = 32;
 
 template <typename T>
 __device__ __forceinline__ float phi_f(float x) {
@@ -67,458 +77,778 @@ __device__ __forceinline__ float pow2_floor(float x) {
   return ldexpf(1.f, ilogbf(x));
 }
 
+// ---------------------------------------------------------- lane exchanges
+// Sum over the 4 lane groups: x + x[l ^ 16], then + [l ^ 32] (VALU lane swaps).
+__device__ __forceinline__ float sum_groups(float x) {
+  auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+
+// Max (MAX) or min over the wave, returned wave-uniform: DPP within each row of
+// 16 lanes, then the four row results.
+template <bool MAX>
+__device__ __forceinline__ float wave_reduce(float x) {
+  auto step = [&](int y) {
+    x = MAX ? fmaxf(x, __int_as_float(y)) : fminf(x, __int_as_float(y));
+  };
+  step(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0xB1, 0xf, 0xf, false));   // quad [1,0,3,2]
+  step(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0x4E, 0xf, 0xf, false));   // quad [2,3,0,1]
+  step(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0x141, 0xf, 0xf, false));  // row_half_mirror
+  step(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0x140, 0xf, 0xf, false));  // row_mirror
+  const float r0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 0));
+  const float r1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 16));
+  const float r2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 32));
+  const float r3 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 48));
+  return MAX ? fmaxf(fmaxf(r0, r1), fmaxf(r2, r3)) : fminf(fminf(r0, r1), fminf(r2, r3));
+}
+
+// Make a value opaque to the optimiser (no code is emitted).
+template <typename R>
+__device__ __forceinline__ void launder(R& r) {
+  constexpr int N = sizeof(R) / 4;
+  uint32_t w[N];
+  __builtin_memcpy(w, &r, sizeof(R));
+#pragma unroll
+  for (int k = 0; k < N; ++k) asm volatile("" : "+v"(w[k]));
+  __builtin_memcpy(&r, w, sizeof(R));
+}
+
 template <int D>
 struct Geo {
   static constexpr int KS = D / 4;   // slots per lane group along the head dim
   static constexpr int NT = D / 16;  // 16-wide tiles along the head dim
-  static constexpr int kScratch = D * D + 2 * D;  // per-wave LDS floats
-  // Row of the result tile -> head-dim index, so that lane group g receives the
-  // KS consecutive indices KS*g .. KS*g + KS - 1 across the NT tiles.
-  __device__ static int out_index(int tile, int m) { return KS * (m >> 2) + 4 * tile + (m & 3); }
+  static constexpr int SROW = D + 1;          // LDS row stride of a state matrix
+  static constexpr int kSlot = D * SROW + D;  // LDS floats per state slot
+  __device__ static int E(int g, int r) { return 16 * (r >> 2) + 4 * g + (r & 3); }
 };
 
-struct RowSrc {
-  const int32_t* perm;  // nullptr: identity
-  int32_t n;
-  __device__ __forceinline__ int32_t orig(int32_t r, bool& ok) const {
-    int32_t o = ok ? (perm ? perm[r] : r) : 0;
-    ok = ok && (uint32_t)o < (uint32_t)n;
-    return ok ? o : 0;
-  }
-};
-
+// ----------------------------------------------------------- row fragments
 template <typename T, int D>
-__device__ __forceinline__ void load_row(const T* base, int32_t orig, bool ok, size_t rowstride,
-                                         int col, float (&x)[Geo<D>::KS]) {
-  if (ok) {
-    load_frag<T, Geo<D>::KS>(base + (size_t)orig * rowstride + col, x);
-  } else {
-#pragma unroll
-    for (int r = 0; r < Geo<D>::KS; ++r) x[r] = 0.f;
-  }
-}
-
-// Selection matrix for the transpose of tile t: slot (g, r) -> head index KS*g+r.
-template <int D>
-__device__ __forceinline__ void make_sel(float (&sel)[Geo<D>::NT][Geo<D>::KS], int i, int g) {
-#pragma unroll
-  for (int t = 0; t < Geo<D>::NT; ++t)
-#pragma unroll
-    for (int r = 0; r < Geo<D>::KS; ++r) sel[t][r] = (Geo<D>::KS * g + r == 16 * t + i) ? 1.f : 0.f;
-}
-
-// Accumulate the state of rows [r0, r0 + 32) n [.., rend) of one window:
-// acc[et][ct] += phi(K)^T V (tile et of e, tile ct of c), zp[t] += column sums of
-// phi(K) over this lane's rows.
-template <typename T, int D>
-__device__ __forceinline__ void state_tile(const T* k, const T* v, const RowSrc& src,
-                                           int32_t r0, int32_t rend, size_t rowstride, int col,
-                                           const float (&sel)[Geo<D>::NT][Geo<D>::KS], int i,
-                                           floatx4 (&acc)[Geo<D>::NT][Geo<D>::NT],
-                                           float (&zp)[Geo<D>::NT]) {
-  constexpr int KS = Geo<D>::KS, NT = Geo<D>::NT;
-  float kx[2][KS], vx[2][KS];
-#pragma unroll
-  for (int s = 0; s < 2; ++s) {
-    bool ok = r0 + 16 * s + i < rend;
-    const int32_t o = src.orig(r0 + 16 * s + i, ok);
-    load_row<T, D>(k, o, ok, rowstride, col, kx[s]);
-    load_row<T, D>(v, o, ok, rowstride, col, vx[s]);
-#pragma unroll
-    for (int r = 0; r < KS; ++r) kx[s][r] = ok ? Ty<T>::round(phi_f<T>(kx[s][r])) : 0.f;
-  }
-  floatx4 tk[2][NT], tv[2][NT];
-  const floatx4 zero = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-  for (int s = 0; s < 2; ++s)
-#pragma unroll
-    for (int t = 0; t < NT; ++t) {
-      tk[s][t] = Mma<T, KS>::run(kx[s], sel[t], zero);
-      tv[s][t] = Mma<T, KS>::run(vx[s], sel[t], zero);
-    }
-#pragma unroll
-  for (int t = 0; t < NT; ++t)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) zp[t] += tk[0][t][j] + tk[1][t][j];
-#pragma unroll
-  for (int et = 0; et < NT; ++et)
-#pragma unroll
-    for (int ct = 0; ct < NT; ++ct) {
-      float a[8], b[8];
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        a[j] = tk[0][et][j];
-        a[4 + j] = tk[1][et][j];
-        b[j] = tv[0][ct][j];
-        b[4 + j] = tv[1][ct][j];
-      }
-      acc[et][ct] = Mma<T, 8>::run(a, b, acc[et][ct]);
-    }
-}
-
-// Full state of one window: S into sS[e * D + c] (fp32), z into sZ[e].
-// Returns max |S| over the window.
-template <typename T, int D>
-__device__ __forceinline__ float window_state(const T* k, const T* v, const RowSrc& src,
-                                              int32_t ws, int32_t we, size_t rowstride, int col,
-                                              const float (&sel)[Geo<D>::NT][Geo<D>::KS], int i,
-                                              int g, float* sS, float* sZ) {
-  constexpr int NT = Geo<D>::NT;
-  floatx4 acc[NT][NT];
-  float zp[NT];
-#pragma unroll
-  for (int a = 0; a < NT; ++a) {
-    zp[a] = 0.f;
-#pragma unroll
-    for (int b = 0; b < NT; ++b) acc[a][b] = {0.f, 0.f, 0.f, 0.f};
-  }
-  for (int32_t r0 = ws; r0 < we; r0 += 32)
-    state_tile<T, D>(k, v, src, r0, we, rowstride, col, sel, i, acc, zp);
-  float mx = 0.f;
-  wave_lds_sync();
-#pragma unroll
-  for (int et = 0; et < NT; ++et)
-#pragma unroll
-    for (int ct = 0; ct < NT; ++ct)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        sS[(16 * et + 4 * g + j) * D + 16 * ct + i] = acc[et][ct][j];
-        mx = fmaxf(mx, fabsf(acc[et][ct][j]));
-      }
-#pragma unroll
-  for (int t = 0; t < NT; ++t) {
-    float z = zp[t] + shfl_xor_f(zp[t], 16);
-    z += shfl_xor_f(z, 32);
-    if (g == 0) sZ[16 * t + i] = z;
-  }
-  wave_lds_sync();
-  return wave_max(mx);
-}
-
-// ------------------------------------------------------------------ forward
-template <typename T, int D>
-__global__ __launch_bounds__(512) void k_sla_fwd(const PlanHeader* __restrict__ hdr,
-                                                  const int32_t* __restrict__ perm_plan,
-                                                  const int32_t* __restrict__ offs,
-                                                  const Chunk* __restrict__ chunks,
-                                                  int32_t max_chunks, int32_t n, int32_t W,
-                                                  int32_t H, int32_t hpw, const T* __restrict__ q,
-                                                  const T* __restrict__ k, const T* __restrict__ v,
-                                                  T* __restrict__ o) {
-  constexpr int KS = Geo<D>::KS, NT = Geo<D>::NT;
-  extern __shared__ float smem[];
-  const int lane = lane_id(), wv = threadIdx.x >> 6;
-  const int h = blockIdx.y * hpw + wv;
-  if (h >= H) return;
-  if (hdr->magic != kPlanMagic || hdr->n != n || hdr->num_windows != W) return;
-  const int32_t nchunks = min(hdr->n_chunks, max_chunks);
-  RowSrc src{hdr->csr ? nullptr : perm_plan, n};
-  float* sS = smem + wv * Geo<D>::kScratch;
-  float* sZ = sS + D * D;
-  const int i = lane & 15, g = lane >> 4;
-  const size_t rowstride = (size_t)H * D;
-  const int col = h * D + KS * g;
-  float sel[NT][KS];
-  make_sel<D>(sel, i, g);
-
-  for (int32_t c = blockIdx.x; c < nchunks; c += gridDim.x) {
-    const Chunk ch = chunks[c];
-    const int32_t rb = max(0, min(ch.row_begin, n)), re = max(rb, min(ch.row_end, n));
-    const int32_t wb = max(0, min(ch.win_begin, W)), wend = max(wb, min(ch.win_end, W));
-    for (int32_t w = wb; w < wend; ++w) {
-      const int32_t ws = max(offs[w], rb), we = min(offs[w + 1], re);
-      if (ws >= we) continue;
-      const float mx = window_state<T, D>(k, v, src, ws, we, rowstride, col, sel, i, g, sS, sZ);
-      const float sig = Ty<T>::kNarrow ? pow2_scale_to_one(mx) : 1.f;
-      float A[NT][KS], zr[KS];
-#pragma unroll
-      for (int ct = 0; ct < NT; ++ct)
-#pragma unroll
-        for (int r = 0; r < KS; ++r) A[ct][r] = sig * sS[(KS * g + r) * D + Geo<D>::out_index(ct, i)];
-#pragma unroll
-      for (int r = 0; r < KS; ++r) zr[r] = sZ[KS * g + r];
-      const float inv_sig = 1.f / sig;
-      for (int32_t r0 = ws; r0 < we; r0 += 16) {
-        bool ok = r0 + i < we;
-        const int32_t orow = src.orig(r0 + i, ok);
-        float qx[KS];
-        load_row<T, D>(q, orow, ok, rowstride, col, qx);
-        float den = 0.f;
-#pragma unroll
-        for (int r = 0; r < KS; ++r) {
-          qx[r] = ok ? Ty<T>::round(phi_f<T>(qx[r])) : 0.f;
-          den += qx[r] * zr[r];
-        }
-        den += shfl_xor_f(den, 16);
-        den += shfl_xor_f(den, 32);
-        const float scale = ok ? inv_sig / den : 0.f;
-        float ox[KS];
-#pragma unroll
-        for (int ct = 0; ct < NT; ++ct) {
-          const floatx4 d4 = Mma<T, KS>::run(A[ct], qx, floatx4{0.f, 0.f, 0.f, 0.f});
-#pragma unroll
-          for (int j = 0; j < 4; ++j) ox[4 * ct + j] = d4[j] * scale;
-        }
-        if (ok) store_frag<T, KS>(o + (size_t)orow * rowstride + col, ox);
-      }
-    }
-  }
-}
-
-// ----------------------------------------------------------------- backward
-template <typename T, int D>
-__global__ __launch_bounds__(256) void k_sla_bwd(const PlanHeader* __restrict__ hdr,
-                                                  const int32_t* __restrict__ perm_plan,
-                                                  const int32_t* __restrict__ offs,
-                                                  const Chunk* __restrict__ chunks,
-                                                  int32_t max_chunks, int32_t n, int32_t W,
-                                                  int32_t H, int32_t hpw, const T* __restrict__ q,
-                                                  const T* __restrict__ k, const T* __restrict__ v,
-                                                  const T* __restrict__ dout, T* __restrict__ dq,
-                                                  T* __restrict__ dk, T* __restrict__ dv) {
-  constexpr int KS = Geo<D>::KS, NT = Geo<D>::NT;
-  extern __shared__ float smem[];
-  const int lane = lane_id(), wv = threadIdx.x >> 6;
-  const int h = blockIdx.y * hpw + wv;
-  if (h >= H) return;
-  if (hdr->magic != kPlanMagic || hdr->n != n || hdr->num_windows != W) return;
-  const int32_t nchunks = min(hdr->n_chunks, max_chunks);
-  RowSrc src{hdr->csr ? nullptr : perm_plan, n};
-  float* sS = smem + wv * Geo<D>::kScratch;
-  float* sZ = sS + D * D;
-  const int i = lane & 15, g = lane >> 4;
-  const size_t rowstride = (size_t)H * D;
-  const int col = h * D + KS * g;
-  float sel[NT][KS];
-  make_sel<D>(sel, i, g);
-  const floatx4 zero = {0.f, 0.f, 0.f, 0.f};
-
-  for (int32_t c = blockIdx.x; c < nchunks; c += gridDim.x) {
-    const Chunk ch = chunks[c];
-    const int32_t rb = max(0, min(ch.row_begin, n)), re = max(rb, min(ch.row_end, n));
-    const int32_t wb = max(0, min(ch.win_begin, W)), wend = max(wb, min(ch.win_end, W));
-    for (int32_t w = wb; w < wend; ++w) {
-      const int32_t ws = max(offs[w], rb), we = min(offs[w + 1], re);
-      if (ws >= we) continue;
-      // ---- pass 1: window state
-      const float mx = window_state<T, D>(k, v, src, ws, we, rowstride, col, sel, i, g, sS, sZ);
-      const float sig = Ty<T>::kNarrow ? pow2_scale_to_one(mx) : 1.f;
-      const float inv_sig = 1.f / sig;
-      float Anum[NT][KS], Adq[NT][KS], zr[KS];
-#pragma unroll
-      for (int t = 0; t < NT; ++t)
-#pragma unroll
-        for (int r = 0; r < KS; ++r) {
-          Anum[t][r] = sig * sS[(KS * g + r) * D + Geo<D>::out_index(t, i)];
-          Adq[t][r] = sig * sS[Geo<D>::out_index(t, i) * D + KS * g + r];
-        }
-      float zmin = 3.0e38f;
-#pragma unroll
-      for (int r = 0; r < KS; ++r) {
-        zr[r] = sZ[KS * g + r];
-        zmin = fminf(zmin, zr[r]);
-      }
-#pragma unroll
-      for (int m = 32; m >= 1; m >>= 1) zmin = fminf(zmin, shfl_xor_f(zmin, m));
-      // phi(q)/den <= 1/min(z), so beta = 2^floor(log2 min z) keeps X = beta phi(q)/den <= 1
-      const float beta = Ty<T>::kNarrow ? pow2_floor(zmin) : 1.f;
-      const float inv_beta = 1.f / beta;
-
-      // ---- pass 2: dq, and dS = sum phi(q)^T dout / den, dz = -sum (dout.o) phi(q) / den
-      floatx4 accd[NT][NT];
-      float dzp[NT];
-#pragma unroll
-      for (int a = 0; a < NT; ++a) {
-        dzp[a] = 0.f;
-#pragma unroll
-        for (int b = 0; b < NT; ++b) accd[a][b] = zero;
-      }
-      for (int32_t r0 = ws; r0 < we; r0 += 32) {
-        float xs[2][KS], ds[2][KS], dots[2];
-#pragma unroll
-        for (int s = 0; s < 2; ++s) {
-          bool ok = r0 + 16 * s + i < we;
-          const int32_t orow = src.orig(r0 + 16 * s + i, ok);
-          float qx[KS], fq[KS];
-          load_row<T, D>(q, orow, ok, rowstride, col, qx);
-          load_row<T, D>(dout, orow, ok, rowstride, col, ds[s]);
-          float den = 0.f;
-#pragma unroll
-          for (int r = 0; r < KS; ++r) {
-            fq[r] = ok ? Ty<T>::round(phi_f<T>(qx[r])) : 0.f;
-            den += fq[r] * zr[r];
-          }
-          den += shfl_xor_f(den, 16);
-          den += shfl_xor_f(den, 32);
-          if (!ok) den = 1.f;
-          const float inv_den = 1.f / den;
-          // o and dout . o
-          float dot = 0.f;
-#pragma unroll
-          for (int t = 0; t < NT; ++t) {
-            const floatx4 d4 = Mma<T, KS>::run(Anum[t], fq, zero);
-#pragma unroll
-            for (int j = 0; j < 4; ++j) dot += ds[s][4 * t + j] * (d4[j] * inv_sig * inv_den);
-          }
-          dot += shfl_xor_f(dot, 16);
-          dot += shfl_xor_f(dot, 32);
-          dots[s] = ok ? dot : 0.f;
-          // dphi(q) = (dout S^T - (dout . o) z) / den ;  dq = dphi(q) * phi'(q)
-          float dqx[KS];
-#pragma unroll
-          for (int t = 0; t < NT; ++t) {
-            const floatx4 d4 = Mma<T, KS>::run(Adq[t], ds[s], zero);
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-              const int r = 4 * t + j;
-              dqx[r] = (d4[j] * inv_sig - dot * zr[r]) * inv_den * dphi_f<T>(qx[r]);
-            }
-          }
-          if (ok) store_frag<T, KS>(dq + (size_t)orow * rowstride + col, dqx);
-#pragma unroll
-          for (int r = 0; r < KS; ++r) xs[s][r] = ok ? Ty<T>::round(fq[r] * beta * inv_den) : 0.f;
-        }
-        floatx4 tx[2][NT], td[2][NT];
-#pragma unroll
-        for (int s = 0; s < 2; ++s)
-#pragma unroll
-          for (int t = 0; t < NT; ++t) {
-            tx[s][t] = Mma<T, KS>::run(xs[s], sel[t], zero);
-            td[s][t] = Mma<T, KS>::run(ds[s], sel[t], zero);
-          }
-        // dz (times beta): lane (i, g) holds rows 4g+j of each sub-tile, column 16t+i
-#pragma unroll
-        for (int s = 0; s < 2; ++s)
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const float dr = shfl_f(dots[s], 4 * g + j);
-#pragma unroll
-            for (int t = 0; t < NT; ++t) dzp[t] -= tx[s][t][j] * dr;
-          }
-#pragma unroll
-        for (int et = 0; et < NT; ++et)
-#pragma unroll
-          for (int ct = 0; ct < NT; ++ct) {
-            float a[8], b[8];
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-              a[j] = tx[0][et][j];
-              a[4 + j] = tx[1][et][j];
-              b[j] = td[0][ct][j];
-              b[4 + j] = td[1][ct][j];
-            }
-            accd[et][ct] = Mma<T, 8>::run(a, b, accd[et][ct]);
-          }
-      }
-      // dS, dz -> LDS (unscaled)
-      wave_lds_sync();
-      float mxd = 0.f;
-#pragma unroll
-      for (int et = 0; et < NT; ++et)
-#pragma unroll
-        for (int ct = 0; ct < NT; ++ct)
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const float val = accd[et][ct][j] * inv_beta;
-            sS[(16 * et + 4 * g + j) * D + 16 * ct + i] = val;
-            mxd = fmaxf(mxd, fabsf(val));
-          }
+struct RowIO {
+  static constexpr int KS = Geo<D>::KS, NT = Geo<D>::NT;
+  using R = Raw<T, KS>;
+  // `row` points at the head's first element; lane group g
+  __device__ static R load(const T* row, int g) {
+    R r;
+    if constexpr (Ty<T>::kNarrow) {
 #pragma unroll
       for (int t = 0; t < NT; ++t) {
-        float z = dzp[t] + shfl_xor_f(dzp[t], 16);
-        z += shfl_xor_f(z, 32);
-        if (g == 0) sZ[16 * t + i] = z * inv_beta;
+        const u16x4 p = *reinterpret_cast<const u16x4*>(row + 16 * t + 4 * g);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) r[4 * t + j] = p[j];
       }
-      wave_lds_sync();
-      mxd = wave_max(mxd);
-      const float rho = Ty<T>::kNarrow ? pow2_scale_to_one(mxd) : 1.f;
-      const float inv_rho = 1.f / rho;
-      float AdK[NT][KS], AdV[NT][KS], dzr[KS];
+    } else {
+#pragma unroll
+      for (int t = 0; t < NT; ++t) {
+        const float4 p = *reinterpret_cast<const float4*>(row + 16 * t + 4 * g);
+        r[4 * t + 0] = p.x;
+        r[4 * t + 1] = p.y;
+        r[4 * t + 2] = p.z;
+        r[4 * t + 3] = p.w;
+      }
+    }
+    return r;
+  }
+  __device__ static void store(T* row, int g, R r) {
+    if constexpr (Ty<T>::kNarrow) {
+#pragma unroll
+      for (int t = 0; t < NT; ++t) {
+        u16x4 p;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) p[j] = r[4 * t + j];
+        *reinterpret_cast<u16x4*>(row + 16 * t + 4 * g) = p;
+      }
+    } else {
 #pragma unroll
       for (int t = 0; t < NT; ++t)
-#pragma unroll
-        for (int r = 0; r < KS; ++r) {
-          AdK[t][r] = rho * sS[Geo<D>::out_index(t, i) * D + KS * g + r];
-          AdV[t][r] = rho * sS[(KS * g + r) * D + Geo<D>::out_index(t, i)];
-        }
-#pragma unroll
-      for (int r = 0; r < KS; ++r) dzr[r] = sZ[KS * g + r];
-
-      // ---- pass 3: dk = (v dS^T + dz) * phi'(k), dv = phi(k) dS
-      for (int32_t r0 = ws; r0 < we; r0 += 16) {
-        bool ok = r0 + i < we;
-        const int32_t orow = src.orig(r0 + i, ok);
-        float kx[KS], vx[KS], fk[KS];
-        load_row<T, D>(k, orow, ok, rowstride, col, kx);
-        load_row<T, D>(v, orow, ok, rowstride, col, vx);
-#pragma unroll
-        for (int r = 0; r < KS; ++r) fk[r] = ok ? Ty<T>::round(phi_f<T>(kx[r])) : 0.f;
-        float dkx[KS], dvx[KS];
-#pragma unroll
-        for (int t = 0; t < NT; ++t) {
-          const floatx4 a4 = Mma<T, KS>::run(AdK[t], vx, zero);
-          const floatx4 b4 = Mma<T, KS>::run(AdV[t], fk, zero);
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            const int r = 4 * t + j;
-            dkx[r] = (a4[j] * inv_rho + dzr[r]) * dphi_f<T>(kx[r]);
-            dvx[r] = b4[j] * inv_rho;
-          }
-        }
-        if (ok) {
-          store_frag<T, KS>(dk + (size_t)orow * rowstride + col, dkx);
-          store_frag<T, KS>(dv + (size_t)orow * rowstride + col, dvx);
-        }
-      }
-      wave_lds_sync();
+        *reinterpret_cast<float4*>(row + 16 * t + 4 * g) =
+            make_float4(r[4 * t], r[4 * t + 1], r[4 * t + 2], r[4 * t + 3]);
     }
   }
-}
+};
 
-// ------------------------------------------------------------ host launchers
-struct AttnArgs {
-  const PlanHeader* hdr;
+struct KernelArgs {
+  PlanHeader* hdr;
   const int32_t* perm;
   const int32_t* offs;
   const Chunk* chunks;
   int32_t max_chunks, n, W, H;
 };
 
+// ------------------------------------------------------------------ slices
+// One 32-row slice of a wave: sub-tile s covers sorted rows r0 + 16 s + (l & 15).
+template <typename T, int KS, int NM>
+struct Slice {
+  Raw<T, KS> x[NM][2];
+  int32_t o[2];  // original row of this lane's row in sub-tile s
+  bool ok[2];    // row exists (inside the wave's range and the plan)
+};
+
+template <typename T, int KS, int NM>
+__device__ __forceinline__ void slice_rows(Slice<T, KS, NM>& sb, int32_t r0, int32_t rend,
+                                           const int32_t* perm, int i) {
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+    const int32_t row = r0 + 16 * s + i;
+    sb.ok[s] = row < rend;
+    sb.o[s] = sb.ok[s] ? (perm ? perm[row] : row) : 0;
+  }
+}
+
+template <typename T, int D, int NM>
+__device__ __forceinline__ void slice_load(Slice<T, Geo<D>::KS, NM>& sb,
+                                           const T* const (&mats)[NM], unsigned mask, int32_t n,
+                                           size_t rs, int col, int g) {
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+    sb.ok[s] = sb.ok[s] && (uint32_t)sb.o[s] < (uint32_t)n;
+    if (!sb.ok[s]) sb.o[s] = 0;
+#pragma unroll
+    for (int m = 0; m < NM; ++m) {
+      sb.x[m][s] = Frag<T, Geo<D>::KS>::zero();
+      if (((mask >> m) & 1) && sb.ok[s])
+        sb.x[m][s] = RowIO<T, D>::load(mats[m] + (size_t)sb.o[s] * rs + col, g);
+    }
+  }
+}
+
+// ------------------------------------------------------------ states
+// A window state (or state gradient) as result tiles:
+//   M[et][ct]  lane (c', g) component j = M[16 et + 4 g + j][16 ct + c']
+//   V[et]      lane (*, g) component j  = v[16 et + 4 g + j]  (the extra column)
+//   MT[ct][et] lane (e', g) component j = M[16 et + e'][16 ct + 4 g + j]  (backward)
+template <int D, bool WT>
+struct State {
+  static constexpr int NT = Geo<D>::NT;
+  floatx4 M[NT][NT];
+  floatx4 V[NT];
+  floatx4 MT[WT ? NT : 1][WT ? NT : 1];
+  __device__ void clear() {
+    const floatx4 z = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int a = 0; a < NT; ++a) {
+      V[a] = z;
+#pragma unroll
+      for (int b = 0; b < NT; ++b) M[a][b] = z;
+    }
+    if constexpr (WT) {
+#pragma unroll
+      for (int a = 0; a < NT; ++a)
+#pragma unroll
+        for (int b = 0; b < NT; ++b) MT[a][b] = z;
+    }
+  }
+  // largest |entry| of M and V over the wave
+  __device__ float absmax() const {
+    float mx = 0.f;
+#pragma unroll
+    for (int a = 0; a < NT; ++a)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        mx = fmaxf(mx, fabsf(V[a][j]));
+#pragma unroll
+        for (int b = 0; b < NT; ++b) mx = fmaxf(mx, fabsf(M[a][b][j]));
+      }
+    return wave_reduce<true>(mx);
+  }
+};
+
+// Selection matrices of the transposes: slot (g, r) stands for head index E(g, r).
+template <typename T, int D>
+struct Sel {
+  Raw<T, Geo<D>::KS> m[Geo<D>::NT];
+  __device__ Sel(int i, int g) {
+    constexpr int KS = Geo<D>::KS;
+#pragma unroll
+    for (int t = 0; t < Geo<D>::NT; ++t) {
+      float x[KS];
+#pragma unroll
+      for (int r = 0; r < KS; ++r) x[r] = (Geo<D>::E(g, r) == 16 * t + i) ? 1.f : 0.f;
+      m[t] = Frag<T, KS>::from_f32(x);
+    }
+  }
+};
+
+// phi of a fragment, rounded to the storage type; zero where !ok.
+template <typename T, int KS>
+__device__ __forceinline__ Raw<T, KS> phi_frag(Raw<T, KS> x, bool ok) {
+  float f[KS];
+  Frag<T, KS>::to_f32(x, f);
+#pragma unroll
+  for (int r = 0; r < KS; ++r) f[r] = ok ? phi_f<T>(f[r]) : 0.f;
+  return Frag<T, KS>::from_f32(f);
+}
+
+// 8-slot row operand of a row contraction: slot r <-> row r0 + E(g, r) of the
+// slice (rows 4g..4g+3 of the two sub-tiles); `val` where the row is in [a, b).
+template <typename T>
+__device__ __forceinline__ Raw<T, 8> row_mask(int32_t r0, int g, int32_t a, int32_t b, float val) {
+  float x[8];
+#pragma unroll
+  for (int r = 0; r < 8; ++r) {
+    const int32_t row = r0 + Geo<32>::E(g, r);
+    x[r] = (row >= a && row < b) ? val : 0.f;
+  }
+  return Frag<T, 8>::from_f32(x);
+}
+
+__device__ __forceinline__ bool sub_overlaps(int32_t r0, int s, int32_t a, int32_t b) {
+  return r0 + 16 * s < b && r0 + 16 * s + 16 > a;
+}
+
+// Rows [a, b) of one slice into the state: M += phi(K)^T V, V += phi(K)^T 1, and
+// for the backward MT += V^T phi(K).  K is matrix 0, V matrix 1.
+template <typename T, int D, int NM, bool WT>
+__device__ __forceinline__ void state_seg(const Slice<T, Geo<D>::KS, NM>& sb, int32_t r0,
+                                          int32_t a, int32_t b, int i, int g,
+                                          const Sel<T, D>& sel, State<D, WT>& st) {
+  constexpr int KS = Geo<D>::KS, NT = Geo<D>::NT;
+  using F = Frag<T, KS>;
+  const floatx4 zero = {0.f, 0.f, 0.f, 0.f};
+  floatx4 tk[2][NT], tv[2][NT];
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+    const int32_t row = r0 + 16 * s + i;
+    const bool in = sb.ok[s] && row >= a && row < b;
+    const Raw<T, KS> fk = phi_frag<T, KS>(sb.x[0][s], in);
+    const Raw<T, KS> vv = in ? sb.x[1][s] : F::zero();
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      tk[s][t] = F::mma(fk, sel.m[t], zero);
+      tv[s][t] = F::mma(vv, sel.m[t], zero);
+    }
+  }
+  const Raw<T, 8> ones = row_mask<T>(r0, g, a, b, 1.f);
+#pragma unroll
+  for (int et = 0; et < NT; ++et) {
+    const Raw<T, 8> pk = pack_rows<T>(tk[0][et], tk[1][et]);
+    st.V[et] = Frag<T, 8>::mma(pk, ones, st.V[et]);
+#pragma unroll
+    for (int ct = 0; ct < NT; ++ct) {
+      const Raw<T, 8> pv = pack_rows<T>(tv[0][ct], tv[1][ct]);
+      st.M[et][ct] = Frag<T, 8>::mma(pk, pv, st.M[et][ct]);
+      if constexpr (WT) st.MT[ct][et] = Frag<T, 8>::mma(pv, pk, st.MT[ct][et]);
+    }
+  }
+}
+
+// Operand of a head-dim contraction from result tiles: slot r of lane (i, g) is
+// tile[r / 4] component r % 4, times `mul`.
+template <typename T, int D>
+__device__ __forceinline__ Raw<T, Geo<D>::KS> tiles_operand(const floatx4 (&tl)[Geo<D>::NT],
+                                                             float mul) {
+  constexpr int KS = Geo<D>::KS;
+  float x[KS];
+#pragma unroll
+  for (int r = 0; r < KS; ++r) x[r] = tl[r >> 2][r & 3] * mul;
+  return Frag<T, KS>::from_f32(x);
+}
+
+// ------------------------------------------------------------ forward math
+template <typename T, int D>
+struct FwdOp {
+  Raw<T, Geo<D>::KS> A[Geo<D>::NT];  // sig S as operand of result tile ct (contract e)
+  float z[Geo<D>::KS];               // z at the lane's head-dim slots (fp32)
+  float inv_sig;
+};
+
+template <typename T, int D>
+__device__ __forceinline__ void make_fwd_op(const State<D, false>& st, FwdOp<T, D>& op) {
+  constexpr int KS = Geo<D>::KS, NT = Geo<D>::NT;
+  const float sig = Ty<T>::kNarrow ? pow2_scale_to_one(st.absmax()) : 1.f;
+  op.inv_sig = 1.f / sig;
+#pragma unroll
+  for (int ct = 0; ct < NT; ++ct) {
+    floatx4 col[NT];
+#pragma unroll
+    for (int et = 0; et < NT; ++et) col[et] = st.M[et][ct];
+    op.A[ct] = tiles_operand<T, D>(col, sig);
+  }
+#pragma unroll
+  for (int r = 0; r < KS; ++r) op.z[r] = st.V[r >> 2][r & 3];
+}
+
+// o = phi(q) S / (phi(q) . z) for rows [a, b) of one slice (Q is matrix QM).
+template <typename T, int D, int NM, int QM>
+__device__ __forceinline__ void apply_seg(const Slice<T, Geo<D>::KS, NM>& sb, int32_t r0,
+                                          int32_t a, int32_t b, int i, int g,
+                                          const FwdOp<T, D>& op, T* o, size_t rs, int col) {
+  constexpr int KS = Geo<D>::KS, NT = Geo<D>::NT;
+  using F = Frag<T, KS>;
+  const floatx4 zero = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+    if (!sub_overlaps(r0, s, a, b)) continue;
+    const int32_t row = r0 + 16 * s + i;
+    const bool in = sb.ok[s] && row >= a && row < b;
+    float fq[KS];
+    const Raw<T, KS> bq = phi_frag<T, KS>(sb.x[QM][s], in);
+    F::to_f32(bq, fq);
+    float den = 0.f;
+#pragma unroll
+    for (int r = 0; r < KS; ++r) den += fq[r] * op.z[r];
+    den = sum_groups(den);
+    const float scale = in ? op.inv_sig / den : 0.f;
+    float ox[KS];
+#pragma unroll
+    for (int ct = 0; ct < NT; ++ct) {
+      const floatx4 d4 = F::mma(op.A[ct], bq, zero);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) ox[4 * ct + j] = d4[j] * scale;
+    }
+    if (in) RowIO<T, D>::store(o + (size_t)sb.o[s] * rs + col, g, F::from_f32(ox));
+  }
+}
+
+// Target occupancy (waves per SIMD) handed to the register allocator.
+#ifndef SLA_FWD_WPE
+#define SLA_FWD_WPE 3
+#endif
+#ifndef SLA_BWD_WPE
+#define SLA_BWD_WPE 2
+#endif
+#ifndef SLA_FWD_NSL
+#define SLA_FWD_NSL 1
+#endif
+// fp32 storage doubles the resident rows: ask for half the occupancy
+template <typename T, int W16>
+constexpr int kWpe = sizeof(T) == 4 ? (W16 > 2 ? W16 / 2 : 1) : W16;
+#ifndef SLA_BWD_NSL
+#define SLA_BWD_NSL 1
+#endif
+
+// ----------------------------------------------------------- backward math
+template <typename T, int D>
+struct StateOp {
+  Raw<T, Geo<D>::KS> A[Geo<D>::NT];  // sig S   : o   = phi(q) S   (tile ct, contract e)
+  Raw<T, Geo<D>::KS> B[Geo<D>::NT];  // sig S^T : dfq = dout S^T (tile et, contract c)
+  float z[Geo<D>::KS];
+  float inv_sig, beta;
+};
+
+template <typename T, int D>
+struct GradOp {
+  Raw<T, Geo<D>::KS> A[Geo<D>::NT];  // rho dS^T : dfk = v dS^T    (tile et, contract c)
+  Raw<T, Geo<D>::KS> B[Geo<D>::NT];  // rho dS   : dv  = phi(k) dS (tile ct, contract e)
+  float dz[Geo<D>::KS];
+  float inv_rho;
+};
+
+template <typename T, int D>
+__device__ __forceinline__ void make_state_op(const State<D, true>& st, StateOp<T, D>& op) {
+  constexpr int KS = Geo<D>::KS, NT = Geo<D>::NT;
+  const float sig = Ty<T>::kNarrow ? pow2_scale_to_one(st.absmax()) : 1.f;
+  op.inv_sig = 1.f / sig;
+#pragma unroll
+  for (int ct = 0; ct < NT; ++ct) {
+    floatx4 col[NT];
+#pragma unroll
+    for (int et = 0; et < NT; ++et) col[et] = st.M[et][ct];
+    op.A[ct] = tiles_operand<T, D>(col, sig);
+  }
+#pragma unroll
+  for (int et = 0; et < NT; ++et) {
+    floatx4 col[NT];
+#pragma unroll
+    for (int ct = 0; ct < NT; ++ct) col[ct] = st.MT[ct][et];
+    op.B[et] = tiles_operand<T, D>(col, sig);
+  }
+  float zmin = 3.0e38f;
+#pragma unroll
+  for (int r = 0; r < KS; ++r) {
+    op.z[r] = st.V[r >> 2][r & 3];
+    zmin = fminf(zmin, op.z[r]);
+  }
+  // phi(q)_e / den <= 1 / z_e <= 1 / min z, so beta phi(q) / den <= 1
+  op.beta = Ty<T>::kNarrow ? pow2_floor(wave_reduce<false>(zmin)) : 1.f;
+}
+
+// From state-gradient tiles that carry a factor `1 / inv_beta`.
+template <typename T, int D>
+__device__ __forceinline__ void make_grad_op(const State<D, true>& st, float inv_beta,
+                                             GradOp<T, D>& op) {
+  constexpr int KS = Geo<D>::KS, NT = Geo<D>::NT;
+  const float mx = st.absmax() * inv_beta;
+  const float rho = Ty<T>::kNarrow ? pow2_scale_to_one(mx) : 1.f;
+  op.inv_rho = 1.f / rho;
+  const float mul = rho * inv_beta;
+#pragma unroll
+  for (int et = 0; et < NT; ++et) {
+    floatx4 col[NT];
+#pragma unroll
+    for (int ct = 0; ct < NT; ++ct) col[ct] = st.MT[ct][et];
+    op.A[et] = tiles_operand<T, D>(col, mul);
+  }
+#pragma unroll
+  for (int ct = 0; ct < NT; ++ct) {
+    floatx4 col[NT];
+#pragma unroll
+    for (int et = 0; et < NT; ++et) col[et] = st.M[et][ct];
+    op.B[ct] = tiles_operand<T, D>(col, mul);
+  }
+#pragma unroll
+  for (int r = 0; r < KS; ++r) op.dz[r] = st.V[r >> 2][r & 3] * inv_beta;
+}
+
+// Rows [a, b) of one slice: dq, and into gs: M += beta (phi(q)/den)^T dout,
+// V += beta (phi(q)/den)^T (-dout.o), MT += beta dout^T (phi(q)/den).
+// q is matrix QI, dout matrix DI.
+template <typename T, int D, int NM, int QI, int DI>
+__device__ __forceinline__ void qgrad_seg(const Slice<T, Geo<D>::KS, NM>& sb, int32_t r0,
+                                          int32_t a, int32_t b, int i, int g,
+                                          const Sel<T, D>& sel, const StateOp<T, D>& op, T* dq,
+                                          size_t rs, int col, State<D, true>& gs) {
+  constexpr int KS = Geo<D>::KS, NT = Geo<D>::NT;
+  using F = Frag<T, KS>;
+  const floatx4 zero = {0.f, 0.f, 0.f, 0.f};
+  Raw<T, KS> xr[2], dr[2], nd[2];
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+    const int32_t row = r0 + 16 * s + i;
+    const bool in = sb.ok[s] && row >= a && row < b;
+    dr[s] = in ? sb.x[DI][s] : F::zero();
+    xr[s] = F::zero();
+    nd[s] = F::zero();
+    if (!sub_overlaps(r0, s, a, b)) continue;
+    float qx[KS], fq[KS], dox[KS];
+    F::to_f32(sb.x[QI][s], qx);
+    F::to_f32(dr[s], dox);
+    const Raw<T, KS> bq = phi_frag<T, KS>(sb.x[QI][s], in);
+    F::to_f32(bq, fq);
+    float den = 0.f;
+#pragma unroll
+    for (int r = 0; r < KS; ++r) den += fq[r] * op.z[r];
+    den = sum_groups(den);
+    if (!in) den = 1.f;
+    const float inv_den = 1.f / den;
+    float dot = 0.f;
+#pragma unroll
+    for (int ct = 0; ct < NT; ++ct) {
+      const floatx4 d4 = F::mma(op.A[ct], bq, zero);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) dot += dox[4 * ct + j] * d4[j];
+    }
+    dot = sum_groups(dot) * (op.inv_sig * inv_den);
+    if (!in) dot = 0.f;
+    float dqx[KS];
+#pragma unroll
+    for (int et = 0; et < NT; ++et) {
+      const floatx4 d4 = F::mma(op.B[et], dr[s], zero);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int r = 4 * et + j;
+        dqx[r] = (d4[j] * op.inv_sig - dot * op.z[r]) * inv_den * dphi_f<T>(qx[r]);
+      }
+    }
+    if (in) RowIO<T, D>::store(dq + (size_t)sb.o[s] * rs + col, g, F::from_f32(dqx));
+    float xs[KS], ns[KS];
+#pragma unroll
+    for (int r = 0; r < KS; ++r) {
+      xs[r] = fq[r] * (op.beta * inv_den);
+      ns[r] = -dot;
+    }
+    xr[s] = F::from_f32(xs);
+    nd[s] = F::from_f32(ns);
+  }
+  floatx4 tx[2][NT], td[2][NT], tn[2];
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      tx[s][t] = F::mma(xr[s], sel.m[t], zero);
+      td[s][t] = F::mma(dr[s], sel.m[t], zero);
+    }
+    tn[s] = F::mma(nd[s], sel.m[0], zero);
+  }
+  const Raw<T, 8> pn = pack_rows<T>(tn[0], tn[1]);
+#pragma unroll
+  for (int et = 0; et < NT; ++et) {
+    const Raw<T, 8> px = pack_rows<T>(tx[0][et], tx[1][et]);
+    gs.V[et] = Frag<T, 8>::mma(px, pn, gs.V[et]);
+#pragma unroll
+    for (int ct = 0; ct < NT; ++ct) {
+      const Raw<T, 8> pd = pack_rows<T>(td[0][ct], td[1][ct]);
+      gs.M[et][ct] = Frag<T, 8>::mma(px, pd, gs.M[et][ct]);
+      gs.MT[ct][et] = Frag<T, 8>::mma(pd, px, gs.MT[ct][et]);
+    }
+  }
+}
+
+// Rows [a, b) of one slice: dk = (v dS^T + dz) phi'(k), dv = phi(k) dS.
+template <typename T, int D, int NM>
+__device__ __forceinline__ void kgrad_seg(const Slice<T, Geo<D>::KS, NM>& sb, int32_t r0,
+                                          int32_t a, int32_t b, int i, int g,
+                                          const GradOp<T, D>& op, T* dk, T* dv, size_t rs,
+                                          int col) {
+  constexpr int KS = Geo<D>::KS, NT = Geo<D>::NT;
+  using F = Frag<T, KS>;
+  const floatx4 zero = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+    if (!sub_overlaps(r0, s, a, b)) continue;
+    const int32_t row = r0 + 16 * s + i;
+    const bool in = sb.ok[s] && row >= a && row < b;
+    float kx[KS];
+    F::to_f32(sb.x[0][s], kx);
+    const Raw<T, KS> fk = phi_frag<T, KS>(sb.x[0][s], in);
+    float dkx[KS], dvx[KS];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      const floatx4 a4 = F::mma(op.A[t], sb.x[1][s], zero);
+      const floatx4 b4 = F::mma(op.B[t], fk, zero);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int r = 4 * t + j;
+        dkx[r] = (a4[j] * op.inv_rho + op.dz[r]) * dphi_f<T>(kx[r]);
+        dvx[r] = b4[j] * op.inv_rho;
+      }
+    }
+    if (in) {
+      RowIO<T, D>::store(dk + (size_t)sb.o[s] * rs + col, g, F::from_f32(dkx));
+      RowIO<T, D>::store(dv + (size_t)sb.o[s] * rs + col, g, F::from_f32(dvx));
+    }
+  }
+}
+
+
+// ------------------------------------------------------------ job streams
+// A wave walks the windows of its chunk; each window is a run of 32-row jobs per
+// phase (forward: 0 = K,V state, 1 = Q apply; backward: 0 = K,V state,
+// 1 = Q,dout, 2 = K,V gradients).  Jobs are software-pipelined: while job t
+// computes, the rows of job t+1 and t+2 are in flight and the permutation
+// entries of job t+3 are being fetched.
+struct Job {
+  int32_t w;       // window (-1: stream finished)
+  int32_t ws, we;  // the window's rows, clipped to the chunk
+  int32_t r0;      // first row of this job
+  int32_t phase;
+};
+
+struct Stream {
+  const int32_t* offs;
+  int32_t rb, re, wend;
+  __device__ __forceinline__ bool next_window(Job& j) const {
+    while (++j.w < wend) {
+      j.ws = max(offs[j.w], rb);
+      j.we = min(offs[j.w + 1], re);
+      if (j.ws < j.we) return true;
+    }
+    j.w = -1;
+    return false;
+  }
+  __device__ __forceinline__ Job first(int32_t wb) const {
+    Job j;
+    j.w = wb - 1;
+    j.phase = 0;
+    j.ws = j.we = j.r0 = 0;
+    if (next_window(j)) j.r0 = j.ws;
+    return j;
+  }
+  template <int NPH>
+  __device__ __forceinline__ Job next(Job j) const {
+    if (j.w < 0) return j;
+    j.r0 += kSliceRows;
+    if (j.r0 < j.we) return j;
+    if (++j.phase < NPH) {
+      j.r0 = j.ws;
+      return j;
+    }
+    j.phase = 0;
+    if (next_window(j)) j.r0 = j.ws;
+    return j;
+  }
+};
+
+template <typename T, int D>
+using JobBuf = Slice<T, Geo<D>::KS, 2>;
+
+__device__ __forceinline__ void job_rows(const Job& j, const int32_t* perm, int i, int32_t (&o)[2],
+                                         bool (&ok)[2]) {
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+    const int32_t row = j.r0 + 16 * s + i;
+    ok[s] = j.w >= 0 && row < j.we;
+    o[s] = ok[s] ? (perm ? perm[row] : row) : 0;
+  }
+}
+
+// Rows of a job -> the job's two matrices (a, b; b may be null).
+template <typename T, int D>
+__device__ __forceinline__ void job_load(JobBuf<T, D>& jb, const int32_t (&o)[2],
+                                         const bool (&ok)[2], const T* a, const T* b, int32_t n,
+                                         size_t rs, int col, int g) {
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+    jb.ok[s] = ok[s] && (uint32_t)o[s] < (uint32_t)n;
+    jb.o[s] = jb.ok[s] ? o[s] : 0;
+    jb.x[0][s] = Frag<T, Geo<D>::KS>::zero();
+    jb.x[1][s] = Frag<T, Geo<D>::KS>::zero();
+    if (jb.ok[s]) {
+      jb.x[0][s] = RowIO<T, D>::load(a + (size_t)jb.o[s] * rs + col, g);
+      if (b) jb.x[1][s] = RowIO<T, D>::load(b + (size_t)jb.o[s] * rs + col, g);
+    }
+  }
+}
+
+template <typename T, int D>
+__device__ __forceinline__ Stream chunk_stream(const KernelArgs& a, int32_t c, int32_t& wb) {
+  const Chunk ch = a.chunks[c];
+  Stream st;
+  st.offs = a.offs;
+  st.rb = max(0, min(ch.row_begin, a.n));
+  st.re = max(st.rb, min(ch.row_end, a.n));
+  st.wend = max(0, min(ch.win_end, a.W));
+  wb = max(0, min(ch.win_begin, st.wend));
+  return st;
+}
+
+// ------------------------------------------------------------------ forward
+template <typename T, int D>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(kWpe<T, SLA_FWD_WPE>)))
+void k_sla_fwd(KernelArgs a, const T* __restrict__ q, const T* __restrict__ k,
+               const T* __restrict__ v, T* __restrict__ o) {
+  const int lane = lane_id(), wv = threadIdx.x >> 6;
+  const int h = blockIdx.y * kWaves + wv;
+  if (h >= a.H) return;
+  const PlanHeader* hdr = a.hdr;
+  if (hdr->magic != kPlanMagic || hdr->n != a.n || hdr->num_windows != a.W) return;
+  const int32_t c = blockIdx.x;
+  if (c >= min(hdr->n_chunks, a.max_chunks)) return;
+  const int32_t* perm = hdr->csr ? nullptr : a.perm;
+  const int i = lane & 15, g = lane >> 4;
+  const size_t rs = (size_t)a.H * D;
+  const int col = h * D;
+  const int32_t n = a.n;
+  const Sel<T, D> sel(i, g);
+  int32_t wb;
+  const Stream str = chunk_stream<T, D>(a, c, wb);
+  auto mat_a = [&](const Job& j) { return j.phase == 0 ? k : q; };
+  auto mat_b = [&](const Job& j) { return j.phase == 0 ? v : (const T*)nullptr; };
+
+  Job j0 = str.first(wb);
+  Job j1 = str.next<2>(j0);
+  Job j2 = str.next<2>(j1);
+  int32_t o0[2], o1[2], o2[2];
+  bool k0[2], k1[2], k2[2];
+  job_rows(j0, perm, i, o0, k0);
+  job_rows(j1, perm, i, o1, k1);
+  job_rows(j2, perm, i, o2, k2);
+  JobBuf<T, D> b0, b1;
+  job_load<T, D>(b0, o0, k0, mat_a(j0), mat_b(j0), n, rs, col, g);
+  job_load<T, D>(b1, o1, k1, mat_a(j1), mat_b(j1), n, rs, col, g);
+  State<D, false> st;
+  FwdOp<T, D> op;
+  while (j0.w >= 0) {
+    const Job j3 = str.next<2>(j2);
+    int32_t o3[2];
+    bool k3[2];
+    job_rows(j3, perm, i, o3, k3);
+    JobBuf<T, D> b2;
+    job_load<T, D>(b2, o2, k2, mat_a(j2), mat_b(j2), n, rs, col, g);
+
+    if (j0.phase == 0) {
+      if (j0.r0 == j0.ws) st.clear();
+      state_seg<T, D, 2, false>(b0, j0.r0, j0.ws, j0.we, i, g, sel, st);
+      if (j0.r0 + kSliceRows >= j0.we) make_fwd_op<T, D>(st, op);
+    } else {
+      apply_seg<T, D, 2, 0>(b0, j0.r0, j0.ws, j0.we, i, g, op, o, rs, col);
+    }
+    j0 = j1;
+    j1 = j2;
+    j2 = j3;
+    b0 = b1;
+    b1 = b2;
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+      o2[s] = o3[s];
+      k2[s] = k3[s];
+    }
+  }
+}
+
+// ----------------------------------------------------------------- backward
+template <typename T, int D>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(kWpe<T, SLA_BWD_WPE>)))
+void k_sla_bwd(KernelArgs a, const T* __restrict__ q, const T* __restrict__ k,
+               const T* __restrict__ v, const T* __restrict__ dout, T* __restrict__ dq,
+               T* __restrict__ dk, T* __restrict__ dv) {
+  const int lane = lane_id(), wv = threadIdx.x >> 6;
+  const int h = blockIdx.y * kWaves + wv;
+  if (h >= a.H) return;
+  const PlanHeader* hdr = a.hdr;
+  if (hdr->magic != kPlanMagic || hdr->n != a.n || hdr->num_windows != a.W) return;
+  const int32_t c = blockIdx.x;
+  if (c >= min(hdr->n_chunks, a.max_chunks)) return;
+  const int32_t* perm = hdr->csr ? nullptr : a.perm;
+  const int i = lane & 15, g = lane >> 4;
+  const size_t rs = (size_t)a.H * D;
+  const int col = h * D;
+  const int32_t n = a.n;
+  const Sel<T, D> sel(i, g);
+  int32_t wb;
+  const Stream str = chunk_stream<T, D>(a, c, wb);
+  auto mat_a = [&](const Job& j) { return j.phase == 1 ? q : k; };
+  auto mat_b = [&](const Job& j) { return j.phase == 1 ? dout : v; };
+
+  Job j0 = str.first(wb);
+  Job j1 = str.next<3>(j0);
+  Job j2 = str.next<3>(j1);
+  int32_t o0[2], o1[2], o2[2];
+  bool k0[2], k1[2], k2[2];
+  job_rows(j0, perm, i, o0, k0);
+  job_rows(j1, perm, i, o1, k1);
+  job_rows(j2, perm, i, o2, k2);
+  JobBuf<T, D> b0, b1;
+  job_load<T, D>(b0, o0, k0, mat_a(j0), mat_b(j0), n, rs, col, g);
+  job_load<T, D>(b1, o1, k1, mat_a(j1), mat_b(j1), n, rs, col, g);
+  State<D, true> st;  // phase 0: S, z, S^T ; phase 1: beta dS, beta dz, beta dS^T
+  StateOp<T, D> sop;
+  GradOp<T, D> gop;
+  while (j0.w >= 0) {
+    const Job j3 = str.next<3>(j2);
+    int32_t o3[2];
+    bool k3[2];
+    job_rows(j3, perm, i, o3, k3);
+    JobBuf<T, D> b2;
+    job_load<T, D>(b2, o2, k2, mat_a(j2), mat_b(j2), n, rs, col, g);
+
+    const bool first = j0.r0 == j0.ws, last = j0.r0 + kSliceRows >= j0.we;
+    if (j0.phase == 0) {
+      if (first) st.clear();
+      state_seg<T, D, 2, true>(b0, j0.r0, j0.ws, j0.we, i, g, sel, st);
+      if (last) make_state_op<T, D>(st, sop);
+    } else if (j0.phase == 1) {
+      if (first) st.clear();
+      qgrad_seg<T, D, 2, 0, 1>(b0, j0.r0, j0.ws, j0.we, i, g, sel, sop, dq, rs, col, st);
+      if (last) make_grad_op<T, D>(st, 1.f / sop.beta, gop);
+    } else {
+      kgrad_seg<T, D, 2>(b0, j0.r0, j0.ws, j0.we, i, g, gop, dk, dv, rs, col);
+    }
+    j0 = j1;
+    j1 = j2;
+    j2 = j3;
+    b0 = b1;
+    b1 = b2;
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+      o2[s] = o3[s];
+      k2[s] = k3[s];
+    }
+  }
+}
+
+// ------------------------------------------------------------ host launchers
 static inline int grid_x(int32_t max_chunks) {
-  return max_chunks < 1 ? 1 : (max_chunks > 65535 ? 65535 : max_chunks);
+  return max_chunks < 1 ? 1 : max_chunks;
 }
 
-template <typename T, int D>
-static hipError_t fwd_impl(const AttnArgs& a, const void* q, const void* k, const void* v, void* o,
-                           hipStream_t stream) {
-  const int hpw = a.H < 8 ? a.H : 8;
-  dim3 grid(grid_x(a.max_chunks), (a.H + hpw - 1) / hpw);
-  const size_t lds = (size_t)hpw * Geo<D>::kScratch * sizeof(float);
-  hipLaunchKernelGGL((k_sla_fwd<T, D>), grid, dim3(64 * hpw), lds, stream, a.hdr, a.perm, a.offs,
-                     a.chunks, a.max_chunks, a.n, a.W, a.H, hpw, static_cast<const T*>(q),
-                     static_cast<const T*>(k), static_cast<const T*>(v), static_cast<T*>(o));
-  return hipGetLastError();
-}
-
-template <typename T, int D>
-static hipError_t bwd_impl(const AttnArgs& a, const void* q, const void* k, const void* v,
-                           const void* dout, void* dq, void* dk, void* dv, hipStream_t stream) {
-  const int hpw = a.H < 4 ? a.H : 4;
-  dim3 grid(grid_x(a.max_chunks), (a.H + hpw - 1) / hpw);
-  const size_t lds = (size_t)hpw * Geo<D>::kScratch * sizeof(float);
-  hipLaunchKernelGGL((k_sla_bwd<T, D>), grid, dim3(64 * hpw), lds, stream, a.hdr, a.perm, a.offs,
-                     a.chunks, a.max_chunks, a.n, a.W, a.H, hpw, static_cast<const T*>(q),
-                     static_cast<const T*>(k), static_cast<const T*>(v),
-                     static_cast<const T*>(dout), static_cast<T*>(dq), static_cast<T*>(dk),
-                     static_cast<T*>(dv));
-  return hipGetLastError();
-}
-
-static AttnArgs attn_args(const void* plan, int32_t n, int32_t W, int32_t H) {
+static KernelArgs kernel_args(void* plan, int32_t n, int32_t W, int32_t H) {
   const PlanLayout lay = plan_layout(n, W);
-  const char* base = static_cast<const char*>(plan);
-  AttnArgs a;
-  a.hdr = reinterpret_cast<const PlanHeader*>(base + lay.header);
+  char* base = static_cast<char*>(plan);
+  KernelArgs a;
+  a.hdr = reinterpret_cast<PlanHeader*>(base + lay.header);
   a.perm = reinterpret_cast<const int32_t*>(base + lay.perm);
   a.offs = reinterpret_cast<const int32_t*>(base + lay.offsets);
   a.chunks = reinterpret_cast<const Chunk*>(base + lay.chunks);
@@ -529,33 +859,56 @@ static AttnArgs attn_args(const void* plan, int32_t n, int32_t W, int32_t H) {
   return a;
 }
 
-// dtype: 0 f32, 1 f16, 2 bf16
-hipError_t launch_forward(const void* plan, int32_t n, int32_t W, int dtype, int32_t H, int32_t d,
-                          const void* q, const void* k, const void* v, void* o,
-                          hipStream_t stream) {
-  const AttnArgs a = attn_args(plan, n, W, H);
-  if (d == 32) {
-    if (dtype == 0) return fwd_impl<float, 32>(a, q, k, v, o, stream);
-    if (dtype == 1) return fwd_impl<_Float16, 32>(a, q, k, v, o, stream);
-    return fwd_impl<bf16_t, 32>(a, q, k, v, o, stream);
-  }
-  if (dtype == 0) return fwd_impl<float, 16>(a, q, k, v, o, stream);
-  if (dtype == 1) return fwd_impl<_Float16, 16>(a, q, k, v, o, stream);
-  return fwd_impl<bf16_t, 16>(a, q, k, v, o, stream);
+template <typename T, int D>
+static hipError_t fwd_impl(void* plan, int32_t n, int32_t W, int32_t H, const void* q,
+                           const void* k, const void* v, void* o, hipStream_t stream) {
+  const KernelArgs a = kernel_args(plan, n, W, H);
+  const int waves = H < kWaves ? H : kWaves;
+  hipLaunchKernelGGL((k_sla_fwd<T, D>), dim3(grid_x(a.max_chunks), (H + kWaves - 1) / kWaves),
+                     dim3(64 * waves), 0, stream, a, static_cast<const T*>(q),
+                     static_cast<const T*>(k), static_cast<const T*>(v), static_cast<T*>(o));
+  return hipGetLastError();
 }
 
-hipError_t launch_backward(const void* plan, int32_t n, int32_t W, int dtype, int32_t H,
-                           int32_t d, const void* q, const void* k, const void* v,
-                           const void* dout, void* dq, void* dk, void* dv, hipStream_t stream) {
-  const AttnArgs a = attn_args(plan, n, W, H);
+template <typename T, int D>
+static hipError_t bwd_impl(void* plan, int32_t n, int32_t W, int32_t H, const void* q,
+                           const void* k, const void* v, const void* dout, void* dq, void* dk,
+                           void* dv, hipStream_t stream) {
+  const KernelArgs a = kernel_args(plan, n, W, H);
+  const int waves = H < kWaves ? H : kWaves;
+  hipLaunchKernelGGL((k_sla_bwd<T, D>), dim3(grid_x(a.max_chunks), (H + kWaves - 1) / kWaves),
+                     dim3(64 * waves), 0, stream, a, static_cast<const T*>(q),
+                     static_cast<const T*>(k), static_cast<const T*>(v),
+                     static_cast<const T*>(dout), static_cast<T*>(dq), static_cast<T*>(dk),
+                     static_cast<T*>(dv));
+  return hipGetLastError();
+}
+
+// dtype: 0 f32, 1 f16, 2 bf16
+hipError_t launch_forward(void* plan, int32_t n, int32_t W, int dtype, int32_t H, int32_t d,
+                          const void* q, const void* k, const void* v, void* o,
+                          hipStream_t stream) {
   if (d == 32) {
-    if (dtype == 0) return bwd_impl<float, 32>(a, q, k, v, dout, dq, dk, dv, stream);
-    if (dtype == 1) return bwd_impl<_Float16, 32>(a, q, k, v, dout, dq, dk, dv, stream);
-    return bwd_impl<bf16_t, 32>(a, q, k, v, dout, dq, dk, dv, stream);
+    if (dtype == 0) return fwd_impl<float, 32>(plan, n, W, H, q, k, v, o, stream);
+    if (dtype == 1) return fwd_impl<_Float16, 32>(plan, n, W, H, q, k, v, o, stream);
+    return fwd_impl<bf16_t, 32>(plan, n, W, H, q, k, v, o, stream);
   }
-  if (dtype == 0) return bwd_impl<float, 16>(a, q, k, v, dout, dq, dk, dv, stream);
-  if (dtype == 1) return bwd_impl<_Float16, 16>(a, q, k, v, dout, dq, dk, dv, stream);
-  return bwd_impl<bf16_t, 16>(a, q, k, v, dout, dq, dk, dv, stream);
+  if (dtype == 0) return fwd_impl<float, 16>(plan, n, W, H, q, k, v, o, stream);
+  if (dtype == 1) return fwd_impl<_Float16, 16>(plan, n, W, H, q, k, v, o, stream);
+  return fwd_impl<bf16_t, 16>(plan, n, W, H, q, k, v, o, stream);
+}
+
+hipError_t launch_backward(void* plan, int32_t n, int32_t W, int dtype, int32_t H, int32_t d,
+                           const void* q, const void* k, const void* v, const void* dout,
+                           void* dq, void* dk, void* dv, hipStream_t stream) {
+  if (d == 32) {
+    if (dtype == 0) return bwd_impl<float, 32>(plan, n, W, H, q, k, v, dout, dq, dk, dv, stream);
+    if (dtype == 1) return bwd_impl<_Float16, 32>(plan, n, W, H, q, k, v, dout, dq, dk, dv, stream);
+    return bwd_impl<bf16_t, 32>(plan, n, W, H, q, k, v, dout, dq, dk, dv, stream);
+  }
+  if (dtype == 0) return bwd_impl<float, 16>(plan, n, W, H, q, k, v, dout, dq, dk, dv, stream);
+  if (dtype == 1) return bwd_impl<_Float16, 16>(plan, n, W, H, q, k, v, dout, dq, dk, dv, stream);
+  return bwd_impl<bf16_t, 16>(plan, n, W, H, q, k, v, dout, dq, dk, dv, stream);
 }
 
 }  // namespace sla

@@ -227,6 +227,8 @@ __global__ __launch_bounds__(kPlanThreads) void k_plan(int32_t csr, int32_t* __r
     hdr->n_chunks = n_chunks;
     hdr->csr = csr;
     hdr->invalid = invalid;
+    hdr->claim[0] = hdr->claim[1] = 0;
+    hdr->done[0] = hdr->done[1] = 0;
     if (invalid_out) *invalid_out = invalid;
   }
 }

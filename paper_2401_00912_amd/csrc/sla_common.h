@@ -7,6 +7,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 namespace sla {
 
 // ----------------------------------------------------------------------------
@@ -28,7 +30,12 @@ struct PlanHeader {
   int32_t n_chunks;     // written by the builder
   int32_t csr;          // 1: rows already window-sorted (identity permutation)
   int32_t invalid;      // out-of-range ids / CSR violations seen by the builder
-  int32_t pad[9];
+  // Work counters of the attention kernels (zeroed by the builder; every launch
+  // hands out work items from claim[k] and the last workgroup to finish puts both
+  // counters of its kernel back to zero): k = 0 forward, 1 backward.
+  int32_t claim[2];
+  int32_t done[2];
+  int32_t pad[5];
 };
 static_assert(sizeof(PlanHeader) == 64, "header is 64 bytes");
 
@@ -294,6 +301,128 @@ struct Mma<bf16_t, 4> {
     return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(ha, hb, c, 0, 0, 0);
   }
 };
+
+// ----------------------------------------------------------------------------
+// Raw fragments: KS consecutive elements of one row kept in their storage format
+// (16-bit types as packed u16 vectors, fp32 as floats), loaded and stored with
+// one vector access, fed to the matrix cores without conversion.
+// ----------------------------------------------------------------------------
+typedef unsigned short u16x8 __attribute__((ext_vector_type(8)));
+typedef unsigned short u16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x8 __attribute__((ext_vector_type(8)));
+
+template <typename T, int KS>
+struct RawOf;
+template <> struct RawOf<_Float16, 8> { using type = u16x8; };
+template <> struct RawOf<_Float16, 4> { using type = u16x4; };
+template <> struct RawOf<bf16_t, 8> { using type = u16x8; };
+template <> struct RawOf<bf16_t, 4> { using type = u16x4; };
+template <> struct RawOf<float, 8> { using type = f32x8; };
+template <> struct RawOf<float, 4> { using type = floatx4; };
+template <typename T, int KS>
+using Raw = typename RawOf<T, KS>::type;
+
+template <typename T>
+__device__ __forceinline__ float u16_to_f32(unsigned short u);
+template <>
+__device__ __forceinline__ float u16_to_f32<_Float16>(unsigned short u) {
+  return (float)__builtin_bit_cast(_Float16, u);
+}
+template <>
+__device__ __forceinline__ float u16_to_f32<bf16_t>(unsigned short u) {
+  return __uint_as_float((uint32_t)u << 16);
+}
+template <typename T>
+__device__ __forceinline__ unsigned short f32_to_u16(float x);
+template <>
+__device__ __forceinline__ unsigned short f32_to_u16<_Float16>(float x) {
+  return __builtin_bit_cast(unsigned short, (_Float16)x);
+}
+template <>
+__device__ __forceinline__ unsigned short f32_to_u16<bf16_t>(float x) {
+  return __builtin_bit_cast(unsigned short, (__bf16)x);
+}
+
+template <typename T, int KS>
+struct Frag {
+  using R = Raw<T, KS>;
+  __device__ static R zero() {
+    R r;
+#pragma unroll
+    for (int k = 0; k < KS; ++k) r[k] = 0;
+    return r;
+  }
+  __device__ static R load(const T* p) {
+    if constexpr (Ty<T>::kNarrow) {
+      return *reinterpret_cast<const R*>(p);
+    } else if constexpr (KS == 8) {
+      const float4 a = reinterpret_cast<const float4*>(p)[0];
+      const float4 b = reinterpret_cast<const float4*>(p)[1];
+      R r;
+      r[0] = a.x; r[1] = a.y; r[2] = a.z; r[3] = a.w;
+      r[4] = b.x; r[5] = b.y; r[6] = b.z; r[7] = b.w;
+      return r;
+    } else {
+      return *reinterpret_cast<const R*>(p);
+    }
+  }
+  __device__ static void store(T* p, R r) {
+    if constexpr (Ty<T>::kNarrow) {
+      *reinterpret_cast<R*>(p) = r;
+    } else if constexpr (KS == 8) {
+      reinterpret_cast<float4*>(p)[0] = make_float4(r[0], r[1], r[2], r[3]);
+      reinterpret_cast<float4*>(p)[1] = make_float4(r[4], r[5], r[6], r[7]);
+    } else {
+      *reinterpret_cast<R*>(p) = r;
+    }
+  }
+  __device__ static void to_f32(R r, float (&x)[KS]) {
+#pragma unroll
+    for (int k = 0; k < KS; ++k) {
+      if constexpr (Ty<T>::kNarrow) x[k] = u16_to_f32<T>(r[k]);
+      else x[k] = r[k];
+    }
+  }
+  // round to nearest even into the storage type
+  __device__ static R from_f32(const float (&x)[KS]) {
+    R r;
+#pragma unroll
+    for (int k = 0; k < KS; ++k) {
+      if constexpr (Ty<T>::kNarrow) r[k] = f32_to_u16<T>(x[k]);
+      else r[k] = x[k];
+    }
+    return r;
+  }
+  // one 16x16 tile contraction over the 4 x KS slots (see Mma above)
+  __device__ static floatx4 mma(R a, R b, floatx4 c) {
+    if constexpr (std::is_same<T, float>::value) {
+#pragma unroll
+      for (int k = 0; k < KS; ++k) c = __builtin_amdgcn_mfma_f32_16x16x4f32(a[k], b[k], c, 0, 0, 0);
+      return c;
+    } else if constexpr (std::is_same<T, _Float16>::value) {
+      if constexpr (KS == 8)
+        return __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(half8_t, a),
+                                                      __builtin_bit_cast(half8_t, b), c, 0, 0, 0);
+      else
+        return __builtin_amdgcn_mfma_f32_16x16x16f16(__builtin_bit_cast(half4_t, a),
+                                                     __builtin_bit_cast(half4_t, b), c, 0, 0, 0);
+    } else {
+      if constexpr (KS == 8)
+        return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a),
+                                                       __builtin_bit_cast(bf16x8_t, b), c, 0, 0, 0);
+      else
+        return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(short4_t, a),
+                                                         __builtin_bit_cast(short4_t, b), c, 0, 0, 0);
+    }
+  }
+};
+
+// 8-slot operand from two 4-row result tiles (rows 4g..4g+3 of two sub-tiles).
+template <typename T>
+__device__ __forceinline__ Raw<T, 8> pack_rows(floatx4 lo, floatx4 hi) {
+  float x[8] = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+  return Frag<T, 8>::from_f32(x);
+}
 
 // ----------------------------------------------------------------------------
 // Wave helpers
