@@ -44,6 +44,11 @@ def parse():
     p.add_argument("--no-graph", action="store_true", help="time eager launches instead of graph replay")
     p.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     p.add_argument("--cpu-seconds", type=float, default=12.0)
+    p.add_argument("--copy-probe", action="store_true",
+                   help="after timing, run plain copies of known size (calibrates PMC byte counters)")
+    p.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                   help="no GPU work: summarise two rocprofv3 --pmc counter_collection.csv files "
+                        "(FETCH_SIZE run, WRITE_SIZE run) of `bench.py --no-graph --copy-probe`")
     return p.parse_args()
 
 
@@ -51,8 +56,91 @@ def elem_size(dtype):
     return {"f32": 4, "f16": 2, "bf16": 2}[dtype]
 
 
+COPY_PROBE_BYTES = 256 << 20   # per copy, 3 copies from distinct buffers
+KERNEL_SOURCES = ["paper_2401_00912_amd/csrc/sla_attn.hip", "paper_2401_00912_amd/csrc/sla_common.h"]
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_sla_bwd_training_step_pmc.txt")
+
+
+def kernel_source_hash():
+    import hashlib
+
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def short_kernel(name):
+    for k in ("k_sla_bwd", "k_sla_fwd", "k_count", "k_plan", "k_scatter"):
+        if k in name:
+            return k
+    if "copyBuffer" in name:    # the runtime's device-to-device copy kernel
+        return "copy"
+    return None
+
+
+def pmc_summary(fetch_csv, write_csv):
+    """Per-dispatch FETCH_SIZE / WRITE_SIZE of every kernel of the step, scaled by
+    what the same counters read for the plain copy of known size."""
+    import csv
+
+    def per_kernel(path, counter):
+        acc = {}
+        with open(path) as fh:
+            for r in csv.DictReader(fh):
+                if r["Counter_Name"] != counter:
+                    continue
+                k = short_kernel(r["Kernel_Name"])
+                if k is None:
+                    continue
+                acc.setdefault(k, []).append(float(r["Counter_Value"]) * 1024.0)  # KiB -> bytes
+        if "copy" in acc:          # the probe's copies, not the binding's small ones
+            acc["copy"] = [x for x in acc["copy"] if x > 0.01 * COPY_PROBE_BYTES] or acc.pop("copy")
+        return {k: (float(np.mean(v)), len(v)) for k, v in acc.items() if v}
+
+    f, w = per_kernel(fetch_csv, "FETCH_SIZE"), per_kernel(write_csv, "WRITE_SIZE")
+    if "copy" not in f or "copy" not in w:
+        raise SystemExit("pmc summary: no copy-probe dispatch in the counter files")
+    ff, fw = f["copy"][0] / COPY_PROBE_BYTES, w["copy"][0] / COPY_PROBE_BYTES
+    lines = [
+        f"kernel_source_sha256: {kernel_source_hash()}",
+        f"copy_probe_bytes: {COPY_PROBE_BYTES}",
+        f"fetch_factor: {ff:.4f}   (FETCH_SIZE bytes read by the copy / bytes it reads)",
+        f"write_factor: {fw:.4f}   (WRITE_SIZE bytes by the copy / bytes it writes)",
+        "kernel      dispatches  FETCH_raw_B   WRITE_raw_B   fetch_scaled_B  write_scaled_B  traffic_scaled_B",
+    ]
+    for k in ("k_count", "k_plan", "k_scatter", "k_sla_fwd", "k_sla_bwd", "copy"):
+        if k in f and k in w:
+            fr, wr = f[k][0], w[k][0]
+            lines.append(f"{k:<11} {f[k][1]:>10}  {fr:>12.0f}  {wr:>12.0f}  {fr / ff:>14.0f}  "
+                         f"{wr / fw:>14.0f}  {fr / ff + wr / fw:>16.0f}")
+    return "\n".join(lines)
+
+
+def stored_traffic(kernel):
+    """Scaled HBM bytes per launch of `kernel` from the committed counter summary,
+    or None when there is none or the kernel source changed since it was taken."""
+    try:
+        with open(TRAFFIC_FILE) as fh:
+            text = fh.read().splitlines()
+    except OSError:
+        return None
+    sha = next((l.split()[1] for l in text if l.startswith("kernel_source_sha256:")), None)
+    if sha != kernel_source_hash():
+        return None
+    for l in text:
+        parts = l.split()
+        if parts and parts[0] == kernel and len(parts) == 7:
+            return float(parts[6])
+    return None
+
+
 def main():
     args = parse()
+    if args.pmc_summary:
+        print(pmc_summary(*args.pmc_summary))
+        return
     if args.gpus != 1:
         print(f"bench.py: this build measures one GPU only (asked for --gpus {args.gpus}); "
               "SLA shards by window ranges with no exchange, see DESIGN.md", file=sys.stderr)
@@ -194,6 +282,15 @@ def main():
     else:
         dom, dom_ms, dom_bytes = "k_sla_fwd", t_fwd, fwd_bytes
     achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
+
+    if args.copy_probe:
+        for _ in range(3):
+            a = torch.empty(COPY_PROBE_BYTES, dtype=torch.uint8, device=dev).fill_(1)
+            b = torch.empty_like(a)
+            torch.cuda.synchronize()
+            b.copy_(a)
+            torch.cuda.synchronize()
+            del a, b
     step_bytes = (fwd_bytes + bwd_bytes + 8 * n) if training else fwd_bytes
 
     nonempty = int((np.diff(plans[0].offsets.cpu().numpy()) > 0).sum())
@@ -226,7 +323,7 @@ def main():
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBS,
-            "traffic": None,
+            "traffic": stored_traffic(dom),
             "algorithmic_bytes": dom_bytes,
             "avg_ms": dom_ms,
         },

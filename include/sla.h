@@ -31,9 +31,9 @@
  *     [n, heads, head_dim] arrays of `dtype`, in the caller's ORIGINAL row order
  *     (the library gathers and scatters through the plan's permutation), with
  *     16-byte aligned base pointers.  head_dim must be 16 or 32.
- *   - Re-entrant: concurrent calls on different streams are safe when they use
- *     different output buffers and different plans (a plan carries the work
- *     counters of the calls that use it).
+ *   - Re-entrant: sla_forward / sla_backward only read the plan, so calls on
+ *     different streams may share one plan; they must not share outputs, and a
+ *     plan must not be rebuilt while a call that reads it is in flight.
  */
 #ifndef SLA_H
 #define SLA_H
@@ -89,8 +89,7 @@ typedef struct {
   int32_t max_chunks;
 } sla_plan_layout_t;
 /* Plan header (int32 fields in order): magic, n, num_windows, chunk_rows,
- * n_chunks, csr (1 = rows were already window-sorted), invalid, then the work
- * counters of the attention kernels (zero between calls). */
+ * n_chunks, csr (1 = rows were already window-sorted), invalid, then padding. */
 
 sla_status_t sla_plan_layout(int64_t n, int32_t num_windows, sla_plan_layout_t* out /* host */);
 
@@ -118,7 +117,7 @@ sla_status_t sla_plan_layout(int64_t n, int32_t num_windows, sla_plan_layout_t* 
  * and pages of L/2 rows: an empty window gets no chunk; a window of more than L/2
  * rows is a chunk of its own; shorter windows are packed into one chunk while
  * they start in the same page, so a packed chunk never splits a window and never
- * exceeds L - 1 rows.
+ * exceeds L - 1 rows.  Chunks are listed in sequence order.
  *
  * invalid_count (device int32, may be NULL) receives the number of out-of-range
  * ids (mode A) or offset violations (mode B).  The plan must be at least
@@ -133,15 +132,13 @@ sla_status_t sla_build_segments(const int32_t* window_ids, int64_t n, int32_t nu
 /*
  * Forward, Eq. (2)-(3): o = SLA(q, k, v).  `plan` must have been built by
  * sla_build_segments() with the same n and num_windows (the kernels check the
- * plan header and write nothing otherwise).  The call updates the plan's work
- * counters and leaves them as it found them, so calls that overlap in time
- * (on different streams) must use different plans.  Every row that belongs to a window
- * is written; a window of one row returns its own value (to rounding).
+ * plan header and write nothing otherwise); it is only read.  Every row that
+ * belongs to a window is written; a window of one row returns its own value (to rounding).
  * Arithmetic: phi and the normaliser in fp32; the two contractions phi(K)^T V and
  * phi(Q) S on the matrix cores with fp32 accumulation, their operands rounded to
  * `dtype` (fp32 stays fp32).
  */
-sla_status_t sla_forward(void* plan, size_t plan_bytes, int64_t n, int32_t num_windows,
+sla_status_t sla_forward(const void* plan, size_t plan_bytes, int64_t n, int32_t num_windows,
                          sla_dtype_t dtype, int32_t heads, int32_t head_dim, const void* q,
                          const void* k, const void* v, void* o, sla_stream_t stream);
 
@@ -151,7 +148,7 @@ sla_status_t sla_forward(void* plan, size_t plan_bytes, int64_t n, int32_t num_w
  * writes dq, dk, dv for every row that belongs to a window.  Window states are
  * recomputed from k and v; the state gradients are accumulated in fp32.
  */
-sla_status_t sla_backward(void* plan, size_t plan_bytes, int64_t n, int32_t num_windows,
+sla_status_t sla_backward(const void* plan, size_t plan_bytes, int64_t n, int32_t num_windows,
                           sla_dtype_t dtype, int32_t heads, int32_t head_dim, const void* q,
                           const void* k, const void* v, const void* dout, void* dq, void* dk,
                           void* dv, sla_stream_t stream);

@@ -8,10 +8,10 @@
 namespace sla {
 hipError_t launch_build(const int32_t* ids, int32_t n, int32_t W, int32_t L, int32_t* perm_out,
                         int32_t* offsets_io, int32_t* invalid_out, void* plan, hipStream_t stream);
-hipError_t launch_forward(void* plan, int32_t n, int32_t W, int dtype, int32_t H, int32_t d,
+hipError_t launch_forward(const void* plan, int32_t n, int32_t W, int dtype, int32_t H, int32_t d,
                           const void* q, const void* k, const void* v, void* o,
                           hipStream_t stream);
-hipError_t launch_backward(void* plan, int32_t n, int32_t W, int dtype, int32_t H,
+hipError_t launch_backward(const void* plan, int32_t n, int32_t W, int dtype, int32_t H,
                            int32_t d, const void* q, const void* k, const void* v,
                            const void* dout, void* dq, void* dk, void* dv, hipStream_t stream);
 }  // namespace sla
@@ -99,7 +99,7 @@ SLA_EXPORT sla_status_t sla_build_segments(const int32_t* window_ids, int64_t n,
                                       invalid_count, plan, static_cast<hipStream_t>(stream)));
 }
 
-SLA_EXPORT sla_status_t sla_forward(void* plan, size_t plan_bytes, int64_t n,
+SLA_EXPORT sla_status_t sla_forward(const void* plan, size_t plan_bytes, int64_t n,
                                     int32_t num_windows, sla_dtype_t dtype, int32_t heads,
                                     int32_t head_dim, const void* q, const void* k, const void* v,
                                     void* o, sla_stream_t stream) {
@@ -112,7 +112,7 @@ SLA_EXPORT sla_status_t sla_forward(void* plan, size_t plan_bytes, int64_t n,
                                         q, k, v, o, static_cast<hipStream_t>(stream)));
 }
 
-SLA_EXPORT sla_status_t sla_backward(void* plan, size_t plan_bytes, int64_t n,
+SLA_EXPORT sla_status_t sla_backward(const void* plan, size_t plan_bytes, int64_t n,
                                      int32_t num_windows, sla_dtype_t dtype, int32_t heads,
                                      int32_t head_dim, const void* q, const void* k,
                                      const void* v, const void* dout, void* dq, void* dk, void* dv,

@@ -1,10 +1,17 @@
 // SLA forward and backward on the gfx950 matrix cores.
 //
-// Work decomposition.  One workgroup of 4 wavefronts per (chunk, head) item; the
-// hardware dispatcher hands workgroups to compute units as they free up.  A chunk is a run of whole windows of the window-sorted
-// sequence (see the builder).  Its rows are cut into 32-row slices and each wave
-// takes a contiguous range of slices, loading all of its rows at once (K, V, Q
-// and, for the backward, dout), so an item costs about one gather latency.
+// Work decomposition.  One wavefront per (chunk, head); a workgroup holds the
+// waves of up to four heads of one chunk, and the grid has one workgroup column
+// per chunk-table entry, so that every (chunk, head) of a scene is resident at
+// once (about 6 k waves for 1.5 k chunks and 4 heads) and the hardware
+// dispatcher balances them.  A chunk is a run of whole windows of the
+// window-sorted sequence (see the builder); its rows are read through the plan's
+// permutation, so q, k, v stay in the caller's order.
+//
+// A wave walks its chunk window by window as a stream of 32-row jobs (forward:
+// K,V rows into the state, then Q rows through it; backward: K,V, then Q,dout,
+// then K,V again) and keeps two jobs' rows in flight ahead of the one it
+// computes, so each wave has about three gathers outstanding at any time.
 //
 // Per window (Eq. (3); the chunk-wise state accumulation of Sec. 3.2 / Fig. 3(b)):
 //   state    S = phi(K)^T V and z = phi(K)^T 1 on the matrix cores over the
@@ -12,13 +19,8 @@
 //   forward  o = phi(q) S / (phi(q) . z);
 //   backward dq from S, z; dS, dz (one more column again) from q, dout; then
 //            dk, dv from dS, dz.
-// A window inside one wave's rows is finished by that wave from registers.  A
-// window that crosses a wave boundary ("shared") is accumulated in parts, the
-// parts meet in LDS, and after a workgroup barrier every wave with rows of the
-// window sums all parts in a fixed order (so they all see bit-identical states)
-// and finishes its own rows.  Window states never reach HBM: the only traffic is
-// q, k, v (, dout) in and o (dq, dk, dv) out.  Rows that do not fit a wave's
-// registers (very long windows) are streamed slice by slice instead.
+// Window states live in registers only: the HBM traffic is q, k, v (, dout) in,
+// o (dq, dk, dv) out, and the plan's permutation and offsets.
 //
 // Register layouts (lane l = 16 g + i, g = lane group 0..3, KS = head_dim / 4,
 // NT = head_dim / 16; slot r of lane group g stands for head-dim index
@@ -44,8 +46,8 @@
 
 namespace sla {
 
-constexpr int kWaves = 4;       // waves per workgroup (row ranges of a chunk)
-constexpr int kSliceRows = 32;
+constexpr int kWaves = 4;       // waves (heads) per workgroup
+constexpr int kSliceRows = 32;  // rows per job
 
 template <typename T>
 __device__ __forceinline__ float phi_f(float x) {
@@ -104,45 +106,61 @@ __device__ __forceinline__ float wave_reduce(float x) {
   return MAX ? fmaxf(fmaxf(r0, r1), fmaxf(r2, r3)) : fminf(fminf(r0, r1), fminf(r2, r3));
 }
 
-// Make a value opaque to the optimiser (no code is emitted).
-template <typename R>
-__device__ __forceinline__ void launder(R& r) {
-  constexpr int N = sizeof(R) / 4;
-  uint32_t w[N];
-  __builtin_memcpy(w, &r, sizeof(R));
-#pragma unroll
-  for (int k = 0; k < N; ++k) asm volatile("" : "+v"(w[k]));
-  __builtin_memcpy(&r, w, sizeof(R));
-}
-
 template <int D>
 struct Geo {
   static constexpr int KS = D / 4;   // slots per lane group along the head dim
   static constexpr int NT = D / 16;  // 16-wide tiles along the head dim
-  static constexpr int SROW = D + 1;          // LDS row stride of a state matrix
-  static constexpr int kSlot = D * SROW + D;  // LDS floats per state slot
   __device__ static int E(int g, int r) { return 16 * (r >> 2) + 4 * g + (r & 3); }
 };
 
 // ----------------------------------------------------------- row fragments
+// A row fragment (KS elements of one head of one row, in slot order E) moves
+// between registers and memory.  16-bit types with head_dim 32: each lane group
+// g reads / writes the 8 contiguous elements 8g..8g+7 as one 16-byte access,
+// and two lane swaps turn those into slot order: with P_g = elements 8g..8g+3
+// and Q_g = 8g+4..8g+7, swapping lane rows 1<->0 and 3<->2 between P and Q, then
+// lanes 32..63 of P with lanes 0..31 of Q, leaves elements 4g..4g+3 (slots
+// 0..3) in P and 16+4g..16+4g+3 (slots 4..7) in Q.  Stores apply the inverse
+// (the swaps in reverse order).  Other types and sizes read and write the NT
+// pieces of 4 elements at 16t + 4g directly.  The swaps are cross-lane, so
+// fetch/put run them unmasked and guard only the memory access.
 template <typename T, int D>
 struct RowIO {
   static constexpr int KS = Geo<D>::KS, NT = Geo<D>::NT;
+  static constexpr bool kSwizzle = Ty<T>::kNarrow && D == 32;
   using R = Raw<T, KS>;
-  // `row` points at the head's first element; lane group g
-  __device__ static R load(const T* row, int g) {
+  __device__ static void swap16(uint32_t& x, uint32_t& y) {
+    const auto r = __builtin_amdgcn_permlane16_swap(x, y, false, false);
+    x = r[0];
+    y = r[1];
+  }
+  __device__ static void swap32(uint32_t& x, uint32_t& y) {
+    const auto r = __builtin_amdgcn_permlane32_swap(x, y, false, false);
+    x = r[0];
+    y = r[1];
+  }
+  // `row` points at the head's first element; ok == false gives zeros.  The
+  // result is in memory order until arrange() puts it into slot order (kept
+  // apart so that a prefetched fragment is not waited for at load time).
+  __device__ static R fetch(const T* row, int g, bool ok) {
     R r;
-    if constexpr (Ty<T>::kNarrow) {
+    if constexpr (kSwizzle) {
+      uint4 w = make_uint4(0, 0, 0, 0);
+      if (ok) w = *reinterpret_cast<const uint4*>(row + 8 * g);
+      r = __builtin_bit_cast(R, w);
+    } else if constexpr (Ty<T>::kNarrow) {
 #pragma unroll
       for (int t = 0; t < NT; ++t) {
-        const u16x4 p = *reinterpret_cast<const u16x4*>(row + 16 * t + 4 * g);
+        u16x4 p = {0, 0, 0, 0};
+        if (ok) p = *reinterpret_cast<const u16x4*>(row + 16 * t + 4 * g);
 #pragma unroll
         for (int j = 0; j < 4; ++j) r[4 * t + j] = p[j];
       }
     } else {
 #pragma unroll
       for (int t = 0; t < NT; ++t) {
-        const float4 p = *reinterpret_cast<const float4*>(row + 16 * t + 4 * g);
+        float4 p = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (ok) p = *reinterpret_cast<const float4*>(row + 16 * t + 4 * g);
         r[4 * t + 0] = p.x;
         r[4 * t + 1] = p.y;
         r[4 * t + 2] = p.z;
@@ -151,68 +169,59 @@ struct RowIO {
     }
     return r;
   }
-  __device__ static void store(T* row, int g, R r) {
-    if constexpr (Ty<T>::kNarrow) {
+  __device__ static void arrange(R& r) {
+    if constexpr (kSwizzle) {
+      uint4 w = __builtin_bit_cast(uint4, r);
+      swap16(w.x, w.z);
+      swap16(w.y, w.w);
+      swap32(w.x, w.z);
+      swap32(w.y, w.w);
+      r = __builtin_bit_cast(R, w);
+    }
+  }
+  __device__ static void put(T* row, int g, R r, bool ok) {
+    if constexpr (kSwizzle) {
+      uint4 w = __builtin_bit_cast(uint4, r);
+      swap32(w.x, w.z);
+      swap32(w.y, w.w);
+      swap16(w.x, w.z);
+      swap16(w.y, w.w);
+      if (ok) *reinterpret_cast<uint4*>(row + 8 * g) = w;
+    } else if constexpr (Ty<T>::kNarrow) {
 #pragma unroll
       for (int t = 0; t < NT; ++t) {
         u16x4 p;
 #pragma unroll
         for (int j = 0; j < 4; ++j) p[j] = r[4 * t + j];
-        *reinterpret_cast<u16x4*>(row + 16 * t + 4 * g) = p;
+        if (ok) *reinterpret_cast<u16x4*>(row + 16 * t + 4 * g) = p;
       }
     } else {
 #pragma unroll
       for (int t = 0; t < NT; ++t)
-        *reinterpret_cast<float4*>(row + 16 * t + 4 * g) =
-            make_float4(r[4 * t], r[4 * t + 1], r[4 * t + 2], r[4 * t + 3]);
+        if (ok)
+          *reinterpret_cast<float4*>(row + 16 * t + 4 * g) =
+              make_float4(r[4 * t], r[4 * t + 1], r[4 * t + 2], r[4 * t + 3]);
     }
   }
 };
 
 struct KernelArgs {
-  PlanHeader* hdr;
+  const PlanHeader* hdr;
   const int32_t* perm;
   const int32_t* offs;
   const Chunk* chunks;
   int32_t max_chunks, n, W, H;
 };
 
-// ------------------------------------------------------------------ slices
-// One 32-row slice of a wave: sub-tile s covers sorted rows r0 + 16 s + (l & 15).
+// ------------------------------------------------------------------ jobs
+// The rows of one 32-row job: sub-tile s covers sorted rows r0 + 16 s + (l & 15);
+// NM matrices (K,V / Q / Q,dout) as row fragments.
 template <typename T, int KS, int NM>
 struct Slice {
   Raw<T, KS> x[NM][2];
   int32_t o[2];  // original row of this lane's row in sub-tile s
-  bool ok[2];    // row exists (inside the wave's range and the plan)
+  bool ok[2];    // row exists (inside the job and the plan)
 };
-
-template <typename T, int KS, int NM>
-__device__ __forceinline__ void slice_rows(Slice<T, KS, NM>& sb, int32_t r0, int32_t rend,
-                                           const int32_t* perm, int i) {
-#pragma unroll
-  for (int s = 0; s < 2; ++s) {
-    const int32_t row = r0 + 16 * s + i;
-    sb.ok[s] = row < rend;
-    sb.o[s] = sb.ok[s] ? (perm ? perm[row] : row) : 0;
-  }
-}
-
-template <typename T, int D, int NM>
-__device__ __forceinline__ void slice_load(Slice<T, Geo<D>::KS, NM>& sb,
-                                           const T* const (&mats)[NM], unsigned mask, int32_t n,
-                                           size_t rs, int col, int g) {
-#pragma unroll
-  for (int s = 0; s < 2; ++s) {
-    sb.ok[s] = sb.ok[s] && (uint32_t)sb.o[s] < (uint32_t)n;
-    if (!sb.ok[s]) sb.o[s] = 0;
-#pragma unroll
-    for (int m = 0; m < NM; ++m) {
-      sb.x[m][s] = Frag<T, Geo<D>::KS>::zero();
-      if (((mask >> m) & 1) && sb.ok[s])
-        sb.x[m][s] = RowIO<T, D>::load(mats[m] + (size_t)sb.o[s] * rs + col, g);
-    }
-  }
-}
 
 // ------------------------------------------------------------ states
 // A window state (or state gradient) as result tiles:
@@ -398,7 +407,7 @@ __device__ __forceinline__ void apply_seg(const Slice<T, Geo<D>::KS, NM>& sb, in
 #pragma unroll
       for (int j = 0; j < 4; ++j) ox[4 * ct + j] = d4[j] * scale;
     }
-    if (in) RowIO<T, D>::store(o + (size_t)sb.o[s] * rs + col, g, F::from_f32(ox));
+    RowIO<T, D>::put(o + (size_t)sb.o[s] * rs + col, g, F::from_f32(ox), in);
   }
 }
 
@@ -409,38 +418,28 @@ __device__ __forceinline__ void apply_seg(const Slice<T, Geo<D>::KS, NM>& sb, in
 #ifndef SLA_BWD_WPE
 #define SLA_BWD_WPE 2
 #endif
-#ifndef SLA_FWD_NSL
-#define SLA_FWD_NSL 1
-#endif
 // fp32 storage doubles the resident rows: ask for half the occupancy
 template <typename T, int W16>
 constexpr int kWpe = sizeof(T) == 4 ? (W16 > 2 ? W16 / 2 : 1) : W16;
-#ifndef SLA_BWD_NSL
-#define SLA_BWD_NSL 1
-#endif
 
 // ----------------------------------------------------------- backward math
+// Operands of the backward's head-dim contractions for one window.  The same
+// registers first hold the state operands (for the Q,dout rows) and are then
+// overwritten with the state-gradient operands (for the K,V gradient rows).
 template <typename T, int D>
-struct StateOp {
-  Raw<T, Geo<D>::KS> A[Geo<D>::NT];  // sig S   : o   = phi(q) S   (tile ct, contract e)
-  Raw<T, Geo<D>::KS> B[Geo<D>::NT];  // sig S^T : dfq = dout S^T (tile et, contract c)
-  float z[Geo<D>::KS];
-  float inv_sig, beta;
+struct BwdOp {
+  Raw<T, Geo<D>::KS> A[Geo<D>::NT];  // sig S   (o = phi(q) S, tile ct)  | rho dS^T (dfk = v dS^T, tile et)
+  Raw<T, Geo<D>::KS> B[Geo<D>::NT];  // sig S^T (dfq = dout S^T, tile et) | rho dS  (dv = phi(k) dS, tile ct)
+  float z[Geo<D>::KS];               // z                                 | dz
+  float inv_scale;                   // 1 / sig                           | 1 / rho
+  float beta;                        // scale of phi(q) / den in the state gradients
 };
 
 template <typename T, int D>
-struct GradOp {
-  Raw<T, Geo<D>::KS> A[Geo<D>::NT];  // rho dS^T : dfk = v dS^T    (tile et, contract c)
-  Raw<T, Geo<D>::KS> B[Geo<D>::NT];  // rho dS   : dv  = phi(k) dS (tile ct, contract e)
-  float dz[Geo<D>::KS];
-  float inv_rho;
-};
-
-template <typename T, int D>
-__device__ __forceinline__ void make_state_op(const State<D, true>& st, StateOp<T, D>& op) {
+__device__ __forceinline__ void make_state_op(const State<D, true>& st, BwdOp<T, D>& op) {
   constexpr int KS = Geo<D>::KS, NT = Geo<D>::NT;
   const float sig = Ty<T>::kNarrow ? pow2_scale_to_one(st.absmax()) : 1.f;
-  op.inv_sig = 1.f / sig;
+  op.inv_scale = 1.f / sig;
 #pragma unroll
   for (int ct = 0; ct < NT; ++ct) {
     floatx4 col[NT];
@@ -468,11 +467,11 @@ __device__ __forceinline__ void make_state_op(const State<D, true>& st, StateOp<
 // From state-gradient tiles that carry a factor `1 / inv_beta`.
 template <typename T, int D>
 __device__ __forceinline__ void make_grad_op(const State<D, true>& st, float inv_beta,
-                                             GradOp<T, D>& op) {
+                                             BwdOp<T, D>& op) {
   constexpr int KS = Geo<D>::KS, NT = Geo<D>::NT;
   const float mx = st.absmax() * inv_beta;
   const float rho = Ty<T>::kNarrow ? pow2_scale_to_one(mx) : 1.f;
-  op.inv_rho = 1.f / rho;
+  op.inv_scale = 1.f / rho;
   const float mul = rho * inv_beta;
 #pragma unroll
   for (int et = 0; et < NT; ++et) {
@@ -489,7 +488,7 @@ __device__ __forceinline__ void make_grad_op(const State<D, true>& st, float inv
     op.B[ct] = tiles_operand<T, D>(col, mul);
   }
 #pragma unroll
-  for (int r = 0; r < KS; ++r) op.dz[r] = st.V[r >> 2][r & 3] * inv_beta;
+  for (int r = 0; r < KS; ++r) op.z[r] = st.V[r >> 2][r & 3] * inv_beta;
 }
 
 // Rows [a, b) of one slice: dq, and into gs: M += beta (phi(q)/den)^T dout,
@@ -498,7 +497,7 @@ __device__ __forceinline__ void make_grad_op(const State<D, true>& st, float inv
 template <typename T, int D, int NM, int QI, int DI>
 __device__ __forceinline__ void qgrad_seg(const Slice<T, Geo<D>::KS, NM>& sb, int32_t r0,
                                           int32_t a, int32_t b, int i, int g,
-                                          const Sel<T, D>& sel, const StateOp<T, D>& op, T* dq,
+                                          const Sel<T, D>& sel, const BwdOp<T, D>& op, T* dq,
                                           size_t rs, int col, State<D, true>& gs) {
   constexpr int KS = Geo<D>::KS, NT = Geo<D>::NT;
   using F = Frag<T, KS>;
@@ -530,7 +529,7 @@ __device__ __forceinline__ void qgrad_seg(const Slice<T, Geo<D>::KS, NM>& sb, in
 #pragma unroll
       for (int j = 0; j < 4; ++j) dot += dox[4 * ct + j] * d4[j];
     }
-    dot = sum_groups(dot) * (op.inv_sig * inv_den);
+    dot = sum_groups(dot) * (op.inv_scale * inv_den);
     if (!in) dot = 0.f;
     float dqx[KS];
 #pragma unroll
@@ -539,10 +538,10 @@ __device__ __forceinline__ void qgrad_seg(const Slice<T, Geo<D>::KS, NM>& sb, in
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int r = 4 * et + j;
-        dqx[r] = (d4[j] * op.inv_sig - dot * op.z[r]) * inv_den * dphi_f<T>(qx[r]);
+        dqx[r] = (d4[j] * op.inv_scale - dot * op.z[r]) * inv_den * dphi_f<T>(qx[r]);
       }
     }
-    if (in) RowIO<T, D>::store(dq + (size_t)sb.o[s] * rs + col, g, F::from_f32(dqx));
+    RowIO<T, D>::put(dq + (size_t)sb.o[s] * rs + col, g, F::from_f32(dqx), in);
     float xs[KS], ns[KS];
 #pragma unroll
     for (int r = 0; r < KS; ++r) {
@@ -580,7 +579,7 @@ __device__ __forceinline__ void qgrad_seg(const Slice<T, Geo<D>::KS, NM>& sb, in
 template <typename T, int D, int NM>
 __device__ __forceinline__ void kgrad_seg(const Slice<T, Geo<D>::KS, NM>& sb, int32_t r0,
                                           int32_t a, int32_t b, int i, int g,
-                                          const GradOp<T, D>& op, T* dk, T* dv, size_t rs,
+                                          const BwdOp<T, D>& op, T* dk, T* dv, size_t rs,
                                           int col) {
   constexpr int KS = Geo<D>::KS, NT = Geo<D>::NT;
   using F = Frag<T, KS>;
@@ -601,14 +600,12 @@ __device__ __forceinline__ void kgrad_seg(const Slice<T, Geo<D>::KS, NM>& sb, in
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int r = 4 * t + j;
-        dkx[r] = (a4[j] * op.inv_rho + op.dz[r]) * dphi_f<T>(kx[r]);
-        dvx[r] = b4[j] * op.inv_rho;
+        dkx[r] = (a4[j] * op.inv_scale + op.z[r]) * dphi_f<T>(kx[r]);
+        dvx[r] = b4[j] * op.inv_scale;
       }
     }
-    if (in) {
-      RowIO<T, D>::store(dk + (size_t)sb.o[s] * rs + col, g, F::from_f32(dkx));
-      RowIO<T, D>::store(dv + (size_t)sb.o[s] * rs + col, g, F::from_f32(dvx));
-    }
+    RowIO<T, D>::put(dk + (size_t)sb.o[s] * rs + col, g, F::from_f32(dkx), in);
+    RowIO<T, D>::put(dv + (size_t)sb.o[s] * rs + col, g, F::from_f32(dvx), in);
   }
 }
 
@@ -626,19 +623,47 @@ struct Job {
   int32_t phase;
 };
 
+// The windows of a chunk, 64 at a time in registers: lane l holds the rows of
+// window wp + l clipped to the chunk, and a ballot marks the non-empty ones, so
+// that moving to the next window is a few scalar instructions, not a chain of
+// dependent loads of the offsets (chunks of small windows also hold many empty
+// ones).
 struct Stream {
   const int32_t* offs;
   int32_t rb, re, wend;
-  __device__ __forceinline__ bool next_window(Job& j) const {
-    while (++j.w < wend) {
-      j.ws = max(offs[j.w], rb);
-      j.we = min(offs[j.w + 1], re);
-      if (j.ws < j.we) return true;
+  int32_t wp;      // first window of the loaded page
+  int32_t a, b;    // rows of window wp + lane, clipped to [rb, re)
+  uint64_t live;   // lanes whose window is non-empty
+  int lane;
+  __device__ __forceinline__ void load_page(int32_t w0) {
+    wp = w0;
+    const int32_t w = wp + lane;
+    a = b = 0;
+    if (w < wend) {
+      a = max(offs[w], rb);
+      b = min(offs[w + 1], re);
+    }
+    live = __ballot(a < b);
+  }
+  __device__ __forceinline__ bool next_window(Job& j) {
+    for (;;) {
+      const int sh = j.w + 1 - wp;   // first lane after the current window
+      const uint64_t m = sh <= 0 ? live : (sh >= 64 ? 0ull : live & (~0ull << sh));
+      if (m) {
+        const int l = __builtin_ctzll(m);
+        j.w = wp + l;
+        j.ws = __builtin_amdgcn_readlane(a, l);
+        j.we = __builtin_amdgcn_readlane(b, l);
+        return true;
+      }
+      if (wp + 64 >= wend) break;
+      load_page(wp + 64);
     }
     j.w = -1;
     return false;
   }
-  __device__ __forceinline__ Job first(int32_t wb) const {
+  __device__ __forceinline__ Job first(int32_t wb) {
+    load_page(wb);
     Job j;
     j.w = wb - 1;
     j.phase = 0;
@@ -647,7 +672,7 @@ struct Stream {
     return j;
   }
   template <int NPH>
-  __device__ __forceinline__ Job next(Job j) const {
+  __device__ __forceinline__ Job next(Job j) {
     if (j.w < 0) return j;
     j.r0 += kSliceRows;
     if (j.r0 < j.we) return j;
@@ -664,8 +689,47 @@ struct Stream {
 template <typename T, int D>
 using JobBuf = Slice<T, Geo<D>::KS, 2>;
 
-__device__ __forceinline__ void job_rows(const Job& j, const int32_t* perm, int i, int32_t (&o)[2],
-                                         bool (&ok)[2]) {
+// The permutation entries of the first 64 kPermRegs rows of a chunk, held by the
+// wave: register m of lane l is the original row of sorted row rb + 64 m + l.
+// Jobs inside that range take their rows from here with lane permutes; rows
+// beyond it (windows longer than the range) are read from the plan.
+#ifndef SLA_PERM_REGS
+#define SLA_PERM_REGS 2
+#endif
+constexpr int kPermRegs = SLA_PERM_REGS;
+
+struct PermRegs {
+  int32_t rb;
+  int32_t r[kPermRegs];
+  __device__ __forceinline__ void load(const int32_t* perm, int32_t rb_, int32_t re, int lane) {
+    rb = rb_;
+#pragma unroll
+    for (int m = 0; m < kPermRegs; ++m) {
+      const int32_t row = rb + 64 * m + lane;
+      r[m] = (perm && row < re) ? perm[row] : row;
+    }
+  }
+};
+
+// Original rows of a job's two sub-tiles (o = 0 and ok = false past the job).
+__device__ __forceinline__ void job_rows(const Job& j, const int32_t* perm, const PermRegs& pr,
+                                         int i, int32_t (&o)[2], bool (&ok)[2]) {
+  if (j.w >= 0 && j.r0 + kSliceRows <= pr.rb + 64 * kPermRegs) {
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+      const int32_t row = j.r0 + 16 * s + i;
+      const int32_t rel = row - pr.rb;
+      int32_t x = 0;
+#pragma unroll
+      for (int m = 0; m < kPermRegs; ++m) {
+        const int32_t t = __builtin_amdgcn_ds_bpermute((rel & 63) << 2, pr.r[m]);
+        if ((rel >> 6) == m) x = t;
+      }
+      ok[s] = row < j.we;
+      o[s] = ok[s] ? x : 0;
+    }
+    return;
+  }
 #pragma unroll
   for (int s = 0; s < 2; ++s) {
     const int32_t row = j.r0 + 16 * s + i;
@@ -683,19 +747,28 @@ __device__ __forceinline__ void job_load(JobBuf<T, D>& jb, const int32_t (&o)[2]
   for (int s = 0; s < 2; ++s) {
     jb.ok[s] = ok[s] && (uint32_t)o[s] < (uint32_t)n;
     jb.o[s] = jb.ok[s] ? o[s] : 0;
-    jb.x[0][s] = Frag<T, Geo<D>::KS>::zero();
-    jb.x[1][s] = Frag<T, Geo<D>::KS>::zero();
-    if (jb.ok[s]) {
-      jb.x[0][s] = RowIO<T, D>::load(a + (size_t)jb.o[s] * rs + col, g);
-      if (b) jb.x[1][s] = RowIO<T, D>::load(b + (size_t)jb.o[s] * rs + col, g);
-    }
+    jb.x[0][s] = RowIO<T, D>::fetch(a + (size_t)jb.o[s] * rs + col, g, jb.ok[s]);
+    jb.x[1][s] = b ? RowIO<T, D>::fetch(b + (size_t)jb.o[s] * rs + col, g, jb.ok[s])
+                   : Frag<T, Geo<D>::KS>::zero();
+  }
+}
+
+// Slot order for the rows of the job about to be computed.
+template <typename T, int D>
+__device__ __forceinline__ void job_arrange(JobBuf<T, D>& jb) {
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+    RowIO<T, D>::arrange(jb.x[0][s]);
+    RowIO<T, D>::arrange(jb.x[1][s]);
   }
 }
 
 template <typename T, int D>
-__device__ __forceinline__ Stream chunk_stream(const KernelArgs& a, int32_t c, int32_t& wb) {
+__device__ __forceinline__ Stream chunk_stream(const KernelArgs& a, int32_t c, int32_t& wb,
+                                               int lane) {
   const Chunk ch = a.chunks[c];
   Stream st;
+  st.lane = lane;
   st.offs = a.offs;
   st.rb = max(0, min(ch.row_begin, a.n));
   st.re = max(st.rb, min(ch.row_end, a.n));
@@ -723,7 +796,9 @@ void k_sla_fwd(KernelArgs a, const T* __restrict__ q, const T* __restrict__ k,
   const int32_t n = a.n;
   const Sel<T, D> sel(i, g);
   int32_t wb;
-  const Stream str = chunk_stream<T, D>(a, c, wb);
+  Stream str = chunk_stream<T, D>(a, c, wb, lane);
+  PermRegs pr;
+  pr.load(perm, str.rb, str.re, lane);
   auto mat_a = [&](const Job& j) { return j.phase == 0 ? k : q; };
   auto mat_b = [&](const Job& j) { return j.phase == 0 ? v : (const T*)nullptr; };
 
@@ -732,9 +807,9 @@ void k_sla_fwd(KernelArgs a, const T* __restrict__ q, const T* __restrict__ k,
   Job j2 = str.next<2>(j1);
   int32_t o0[2], o1[2], o2[2];
   bool k0[2], k1[2], k2[2];
-  job_rows(j0, perm, i, o0, k0);
-  job_rows(j1, perm, i, o1, k1);
-  job_rows(j2, perm, i, o2, k2);
+  job_rows(j0, perm, pr, i, o0, k0);
+  job_rows(j1, perm, pr, i, o1, k1);
+  job_rows(j2, perm, pr, i, o2, k2);
   JobBuf<T, D> b0, b1;
   job_load<T, D>(b0, o0, k0, mat_a(j0), mat_b(j0), n, rs, col, g);
   job_load<T, D>(b1, o1, k1, mat_a(j1), mat_b(j1), n, rs, col, g);
@@ -744,10 +819,11 @@ void k_sla_fwd(KernelArgs a, const T* __restrict__ q, const T* __restrict__ k,
     const Job j3 = str.next<2>(j2);
     int32_t o3[2];
     bool k3[2];
-    job_rows(j3, perm, i, o3, k3);
+    job_rows(j3, perm, pr, i, o3, k3);
     JobBuf<T, D> b2;
     job_load<T, D>(b2, o2, k2, mat_a(j2), mat_b(j2), n, rs, col, g);
 
+    job_arrange<T, D>(b0);
     if (j0.phase == 0) {
       if (j0.r0 == j0.ws) st.clear();
       state_seg<T, D, 2, false>(b0, j0.r0, j0.ws, j0.we, i, g, sel, st);
@@ -788,7 +864,9 @@ void k_sla_bwd(KernelArgs a, const T* __restrict__ q, const T* __restrict__ k,
   const int32_t n = a.n;
   const Sel<T, D> sel(i, g);
   int32_t wb;
-  const Stream str = chunk_stream<T, D>(a, c, wb);
+  Stream str = chunk_stream<T, D>(a, c, wb, lane);
+  PermRegs pr;
+  pr.load(perm, str.rb, str.re, lane);
   auto mat_a = [&](const Job& j) { return j.phase == 1 ? q : k; };
   auto mat_b = [&](const Job& j) { return j.phase == 1 ? dout : v; };
 
@@ -797,34 +875,34 @@ void k_sla_bwd(KernelArgs a, const T* __restrict__ q, const T* __restrict__ k,
   Job j2 = str.next<3>(j1);
   int32_t o0[2], o1[2], o2[2];
   bool k0[2], k1[2], k2[2];
-  job_rows(j0, perm, i, o0, k0);
-  job_rows(j1, perm, i, o1, k1);
-  job_rows(j2, perm, i, o2, k2);
+  job_rows(j0, perm, pr, i, o0, k0);
+  job_rows(j1, perm, pr, i, o1, k1);
+  job_rows(j2, perm, pr, i, o2, k2);
   JobBuf<T, D> b0, b1;
   job_load<T, D>(b0, o0, k0, mat_a(j0), mat_b(j0), n, rs, col, g);
   job_load<T, D>(b1, o1, k1, mat_a(j1), mat_b(j1), n, rs, col, g);
   State<D, true> st;  // phase 0: S, z, S^T ; phase 1: beta dS, beta dz, beta dS^T
-  StateOp<T, D> sop;
-  GradOp<T, D> gop;
+  BwdOp<T, D> op;
   while (j0.w >= 0) {
     const Job j3 = str.next<3>(j2);
     int32_t o3[2];
     bool k3[2];
-    job_rows(j3, perm, i, o3, k3);
+    job_rows(j3, perm, pr, i, o3, k3);
     JobBuf<T, D> b2;
     job_load<T, D>(b2, o2, k2, mat_a(j2), mat_b(j2), n, rs, col, g);
 
+    job_arrange<T, D>(b0);
     const bool first = j0.r0 == j0.ws, last = j0.r0 + kSliceRows >= j0.we;
     if (j0.phase == 0) {
       if (first) st.clear();
       state_seg<T, D, 2, true>(b0, j0.r0, j0.ws, j0.we, i, g, sel, st);
-      if (last) make_state_op<T, D>(st, sop);
+      if (last) make_state_op<T, D>(st, op);
     } else if (j0.phase == 1) {
       if (first) st.clear();
-      qgrad_seg<T, D, 2, 0, 1>(b0, j0.r0, j0.ws, j0.we, i, g, sel, sop, dq, rs, col, st);
-      if (last) make_grad_op<T, D>(st, 1.f / sop.beta, gop);
+      qgrad_seg<T, D, 2, 0, 1>(b0, j0.r0, j0.ws, j0.we, i, g, sel, op, dq, rs, col, st);
+      if (last) make_grad_op<T, D>(st, 1.f / op.beta, op);
     } else {
-      kgrad_seg<T, D, 2>(b0, j0.r0, j0.ws, j0.we, i, g, gop, dk, dv, rs, col);
+      kgrad_seg<T, D, 2>(b0, j0.r0, j0.ws, j0.we, i, g, op, dk, dv, rs, col);
     }
     j0 = j1;
     j1 = j2;
@@ -844,11 +922,11 @@ static inline int grid_x(int32_t max_chunks) {
   return max_chunks < 1 ? 1 : max_chunks;
 }
 
-static KernelArgs kernel_args(void* plan, int32_t n, int32_t W, int32_t H) {
+static KernelArgs kernel_args(const void* plan, int32_t n, int32_t W, int32_t H) {
   const PlanLayout lay = plan_layout(n, W);
-  char* base = static_cast<char*>(plan);
+  const char* base = static_cast<const char*>(plan);
   KernelArgs a;
-  a.hdr = reinterpret_cast<PlanHeader*>(base + lay.header);
+  a.hdr = reinterpret_cast<const PlanHeader*>(base + lay.header);
   a.perm = reinterpret_cast<const int32_t*>(base + lay.perm);
   a.offs = reinterpret_cast<const int32_t*>(base + lay.offsets);
   a.chunks = reinterpret_cast<const Chunk*>(base + lay.chunks);
@@ -860,7 +938,7 @@ static KernelArgs kernel_args(void* plan, int32_t n, int32_t W, int32_t H) {
 }
 
 template <typename T, int D>
-static hipError_t fwd_impl(void* plan, int32_t n, int32_t W, int32_t H, const void* q,
+static hipError_t fwd_impl(const void* plan, int32_t n, int32_t W, int32_t H, const void* q,
                            const void* k, const void* v, void* o, hipStream_t stream) {
   const KernelArgs a = kernel_args(plan, n, W, H);
   const int waves = H < kWaves ? H : kWaves;
@@ -871,7 +949,7 @@ static hipError_t fwd_impl(void* plan, int32_t n, int32_t W, int32_t H, const vo
 }
 
 template <typename T, int D>
-static hipError_t bwd_impl(void* plan, int32_t n, int32_t W, int32_t H, const void* q,
+static hipError_t bwd_impl(const void* plan, int32_t n, int32_t W, int32_t H, const void* q,
                            const void* k, const void* v, const void* dout, void* dq, void* dk,
                            void* dv, hipStream_t stream) {
   const KernelArgs a = kernel_args(plan, n, W, H);
@@ -885,7 +963,7 @@ static hipError_t bwd_impl(void* plan, int32_t n, int32_t W, int32_t H, const vo
 }
 
 // dtype: 0 f32, 1 f16, 2 bf16
-hipError_t launch_forward(void* plan, int32_t n, int32_t W, int dtype, int32_t H, int32_t d,
+hipError_t launch_forward(const void* plan, int32_t n, int32_t W, int dtype, int32_t H, int32_t d,
                           const void* q, const void* k, const void* v, void* o,
                           hipStream_t stream) {
   if (d == 32) {
@@ -898,7 +976,7 @@ hipError_t launch_forward(void* plan, int32_t n, int32_t W, int dtype, int32_t H
   return fwd_impl<bf16_t, 16>(plan, n, W, H, q, k, v, o, stream);
 }
 
-hipError_t launch_backward(void* plan, int32_t n, int32_t W, int dtype, int32_t H, int32_t d,
+hipError_t launch_backward(const void* plan, int32_t n, int32_t W, int dtype, int32_t H, int32_t d,
                            const void* q, const void* k, const void* v, const void* dout,
                            void* dq, void* dk, void* dv, hipStream_t stream) {
   if (d == 32) {

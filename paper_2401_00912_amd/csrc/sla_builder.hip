@@ -3,24 +3,29 @@
 // flattened matrix that is partitioned into chunks; Fig. 5 caption: "offsets
 // generation" computes the start of every chunk).
 //
-// Three launches in mode A (ids given), one in mode B (CSR given):
-//   k_count    per builder block, a histogram of its rows' window ids (LDS atomics;
-//              the counts are order-free, hence deterministic);
-//   k_plan     one workgroup: per-window column prefix over the blocks, exclusive
-//              scan -> offsets, then the chunk table from the offsets;
-//   k_scatter  per builder block, the stable rank of every row among the rows of
-//              the same window in this block (wave ballots on the id bits give the
-//              set of lanes sharing an id; waves then take their base in order),
-//              and perm[offsets[id] + block prefix + rank] = row.
+// Mode A (ids given), two launches over builder blocks of E rows:
+//   k_count    per block, a histogram of its rows' window ids (LDS atomics; the
+//              counts are order-free, hence deterministic) -> count matrix;
+//   k_scatter  per block: the column prefix of the count matrix over the blocks
+//              before it and the column totals (read straight from the matrix),
+//              the exclusive scan of the totals (= offsets) in LDS, then the
+//              stable rank of every row among the rows of its window in this
+//              block (wave ballots on the id bits give the lanes sharing an id;
+//              waves take their bases in order) and perm[offsets[id] + block
+//              prefix + rank] = row.  Block 0 also publishes the offsets, the
+//              chunk table and the header.
+// Mode B (CSR offsets given) and n = 0: one workgroup, k_plan, validates the
+// offsets and writes the chunk table and header.
 #include "sla_common.h"
 
 namespace sla {
 
-constexpr int kPlanThreads = 1024;
+constexpr int kBuildThreads = 1024;  // threads of every builder workgroup
 
 // ------------------------------------------------------------------ k_count
-__global__ __launch_bounds__(256) void k_count(const int32_t* __restrict__ ids, int32_t n,
-                                                int32_t W, int32_t E, int32_t* __restrict__ counts) {
+__global__ __launch_bounds__(kBuildThreads) void k_count(const int32_t* __restrict__ ids, int32_t n,
+                                                         int32_t W, int32_t E, int32_t ld,
+                                                         int32_t* __restrict__ counts) {
   __shared__ int32_t hist[kMaxWindows + 1];
   for (int i = threadIdx.x; i <= W; i += blockDim.x) hist[i] = 0;
   __syncthreads();
@@ -31,8 +36,8 @@ __global__ __launch_bounds__(256) void k_count(const int32_t* __restrict__ ids, 
     atomicAdd(&hist[(uint32_t)id < (uint32_t)W ? id : W], 1);
   }
   __syncthreads();
-  int32_t* row = counts + (size_t)blockIdx.x * (W + 1);
-  for (int i = threadIdx.x; i <= W; i += blockDim.x) row[i] = hist[i];
+  int32_t* row = counts + (size_t)blockIdx.x * ld;
+  for (int i = threadIdx.x; i < ld; i += blockDim.x) row[i] = i <= W ? hist[i] : 0;
 }
 
 // -------------------------------------------------------- block-wide scans
@@ -43,98 +48,126 @@ struct OpMax {
   __device__ int32_t operator()(int32_t a, int32_t b) const { return a > b ? a : b; }
 };
 
+
 // Exclusive scan of one value per thread in thread order; *total gets the
 // reduction of all values.  Uses s[0..32]; ends with a barrier so s can be reused.
-template <class Op>
-__device__ int32_t block_exscan(int32_t x, int32_t identity, Op op, int32_t* s, int32_t* total) {
+template <class Op, typename V = int32_t>
+__device__ V block_exscan(V x, V identity, Op op, V* s, V* total) {
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6, nwv = blockDim.x >> 6;
-  int32_t inc = x;
+  V inc = x;
 #pragma unroll
   for (int d = 1; d < 64; d <<= 1) {
-    const int32_t y = __shfl_up(inc, d, 64);
+    const V y = __shfl_up(inc, d, 64);
     if (lane >= d) inc = op(inc, y);
   }
   if (lane == 63) s[wv] = inc;
   __syncthreads();
   if (wv == 0) {
-    const int32_t v = lane < nwv ? s[lane] : identity;
-    int32_t inc2 = v;
+    const V v = lane < nwv ? s[lane] : identity;
+    V inc2 = v;
 #pragma unroll
     for (int d = 1; d < 64; d <<= 1) {
-      const int32_t y = __shfl_up(inc2, d, 64);
+      const V y = __shfl_up(inc2, d, 64);
       if (lane >= d) inc2 = op(inc2, y);
     }
-    int32_t ex2 = __shfl_up(inc2, 1, 64);
+    V ex2 = __shfl_up(inc2, 1, 64);
     if (lane == 0) ex2 = identity;
     if (lane < nwv) s[lane] = ex2;
     if (lane == nwv - 1) s[32] = inc2;
   }
   __syncthreads();
-  int32_t ex = __shfl_up(inc, 1, 64);
+  V ex = __shfl_up(inc, 1, 64);
   if (lane == 0) ex = identity;
-  const int32_t r = op(s[wv], ex);
+  const V r = op(s[wv], ex);
   *total = s[32];
   __syncthreads();
   return r;
 }
 
+// ------------------------------------------------------------- chunk table
+// Chunk table from the offsets in LDS (page rule, pages of L/2 rows), in
+// sequence order.  s_aux: LDS scratch of at least W ints.  Every thread of the
+// block calls it; returns the number of chunks.
+__device__ int32_t build_chunks(const int32_t* s_off, int32_t* s_aux, int32_t W, int32_t L,
+                                Chunk* __restrict__ chunks, int32_t* s_scan) {
+  const int tid = threadIdx.x, T = blockDim.x;
+  const int32_t page = L >> 1;
+  const int P = (W + T - 1) / T;
+  const int w0 = min(tid * P, W), w1 = min(w0 + P, W);
+  // the last non-empty window start and the end of the last long window before
+  // my range decide whether my first non-empty window starts a chunk
+  int32_t aggStart = -1, aggLong = -1;
+  for (int w = w0; w < w1; ++w) {
+    const int32_t len = s_off[w + 1] - s_off[w];
+    if (len > 0) aggStart = s_off[w];
+    if (len > page) aggLong = s_off[w + 1];
+  }
+  int32_t tmp;
+  const int32_t lastStart = block_exscan(aggStart, -1, OpMax(), s_scan, &tmp);
+  const int32_t lastLongEnd = block_exscan(aggLong, -1, OpMax(), s_scan, &tmp);
+  auto starts = [&](int32_t& ls, int32_t& ll, int w) {
+    const int32_t a = s_off[w], len = s_off[w + 1] - a;
+    if (len <= 0) return false;
+    const bool is_long = len > page;
+    const bool st = is_long || ls < 0 || ll == a || (ls / page) != (a / page);
+    ls = a;
+    if (is_long) ll = a + len;
+    return st;
+  };
+  int32_t cnt = 0;
+  {
+    int32_t ls = lastStart, ll = lastLongEnd;
+    for (int w = w0; w < w1; ++w) cnt += starts(ls, ll, w);
+  }
+  int32_t n_chunks = 0;
+  int32_t c = block_exscan(cnt, 0, OpSum(), s_scan, &n_chunks);
+  {
+    int32_t ls = lastStart, ll = lastLongEnd;
+    for (int w = w0; w < w1; ++w)
+      if (starts(ls, ll, w)) s_aux[c++] = w;   // first window of chunk c (sequence order)
+  }
+  __syncthreads();
+  for (int i = tid; i < n_chunks; i += T) {
+    Chunk ch;
+    ch.win_begin = s_aux[i];
+    ch.win_end = i + 1 < n_chunks ? s_aux[i + 1] : W;
+    ch.row_begin = s_off[ch.win_begin];
+    ch.row_end = s_off[ch.win_end];
+    chunks[i] = ch;
+  }
+  return n_chunks;
+}
+
+__device__ void write_header(PlanHeader* hdr, int32_t n, int32_t W, int32_t L, int32_t n_chunks,
+                             int32_t csr, int32_t invalid, int32_t* invalid_out) {
+  hdr->magic = kPlanMagic;
+  hdr->n = n;
+  hdr->num_windows = W;
+  hdr->chunk_rows = L;
+  hdr->n_chunks = n_chunks;
+  hdr->csr = csr;
+  hdr->invalid = invalid;
+  if (invalid_out) *invalid_out = invalid;
+}
+
 // ------------------------------------------------------------------ k_plan
-// csr == 0: counts holds the [n_blocks][W + 1] block histograms (column W =
-// out-of-range ids).  Each column is replaced by its exclusive prefix over the
-// blocks (k_scatter reads it) and the column totals are scanned into offsets.
-// csr == 1: offsets_io is the caller's CSR input; it is validated and clamped.
-__global__ __launch_bounds__(kPlanThreads) void k_plan(int32_t csr, int32_t* __restrict__ counts,
-                                                       int32_t nb, int32_t W, int32_t n, int32_t L,
-                                                       int32_t* __restrict__ offsets_io,
-                                                       int32_t* __restrict__ invalid_out,
-                                                       PlanHeader* __restrict__ hdr,
-                                                       int32_t* __restrict__ plan_offsets,
-                                                       Chunk* __restrict__ chunks) {
+// One workgroup.  csr == 1: offsets_io is the caller's CSR input; it is validated
+// and clamped.  csr == 0 (n = 0 in mode A): every window is empty.
+__global__ __launch_bounds__(kBuildThreads) void k_plan(int32_t csr, int32_t W, int32_t n,
+                                                        int32_t L, int32_t* __restrict__ offsets_io,
+                                                        int32_t* __restrict__ invalid_out,
+                                                        PlanHeader* __restrict__ hdr,
+                                                        int32_t* __restrict__ plan_offsets,
+                                                        Chunk* __restrict__ chunks) {
   __shared__ int32_t s_off[kMaxWindows + 1];
   __shared__ int32_t s_aux[kMaxWindows + 1];
   __shared__ int32_t s_scan[33];
   const int tid = threadIdx.x, T = blockDim.x;
   int32_t invalid = 0, total = 0;
-
-  if (!csr) {
-    // column prefix over blocks, window totals into s_aux (s_aux[W] = invalid rows)
-    for (int w = tid; w <= W; w += T) {
-      int32_t run = 0;
-      int b = 0;
-      for (; b + 8 <= nb; b += 8) {
-        int32_t c[8];
-#pragma unroll
-        for (int u = 0; u < 8; ++u) c[u] = counts[(size_t)(b + u) * (W + 1) + w];
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-          counts[(size_t)(b + u) * (W + 1) + w] = run;
-          run += c[u];
-        }
-      }
-      for (; b < nb; ++b) {
-        const int32_t c = counts[(size_t)b * (W + 1) + w];
-        counts[(size_t)b * (W + 1) + w] = run;
-        run += c;
-      }
-      s_aux[w] = run;
-    }
-    __syncthreads();
-    invalid = s_aux[W];
-    // exclusive scan of the totals: thread t owns windows [t P, t P + P)
-    const int P = (W + T - 1) / T;
-    const int w0 = tid * P, w1 = min(w0 + P, W);
-    int32_t local = 0;
-    for (int w = w0; w < w1; ++w) local += s_aux[w];
-    int32_t ex = block_exscan(local, 0, OpSum(), s_scan, &total);
-    for (int w = w0; w < w1; ++w) {
-      s_off[w] = ex;
-      ex += s_aux[w];
-    }
-    if (tid == 0) s_off[W] = total;
-  } else {
-    // validate and clamp the caller's offsets: s_off = running max of clamp(x, 0, n)
+  if (csr) {
+    // s_off = running max of clamp(x, 0, n)
     const int P = (W + 1 + T - 1) / T;
-    const int w0 = tid * P, w1 = min(w0 + P, W + 1);
+    const int w0 = min(tid * P, W + 1), w1 = min(w0 + P, W + 1);
     int32_t bad = 0, mx = 0;
     for (int w = w0; w < w1; ++w) {
       const int32_t x = offsets_io[w];
@@ -143,7 +176,7 @@ __global__ __launch_bounds__(kPlanThreads) void k_plan(int32_t csr, int32_t* __r
       const int32_t cx = x < 0 ? 0 : (x > n ? n : x);
       mx = cx > mx ? cx : mx;
     }
-    int32_t ex_max = block_exscan(mx, 0, OpMax(), s_scan, &total);
+    const int32_t ex_max = block_exscan(mx, 0, OpMax(), s_scan, &total);
     int32_t bad_total = 0;
     block_exscan(bad, 0, OpSum(), s_scan, &bad_total);
     int32_t run = ex_max;
@@ -154,83 +187,17 @@ __global__ __launch_bounds__(kPlanThreads) void k_plan(int32_t csr, int32_t* __r
       s_off[w] = run;
     }
     invalid = bad_total;
-    if (tid == 0) {
-      invalid += (offsets_io[0] != 0) + (offsets_io[W] != n);
-    }
+    if (tid == 0) invalid += (offsets_io[0] != 0) + (offsets_io[W] != n);
+  } else {
+    for (int w = tid; w <= W; w += T) s_off[w] = 0;
   }
   __syncthreads();
-
-  // publish offsets
   for (int w = tid; w <= W; w += T) {
     plan_offsets[w] = s_off[w];
     if (!csr && offsets_io) offsets_io[w] = s_off[w];
   }
-
-  // ---- chunk table (page rule) ----
-  const int32_t page = L >> 1;
-  const int P = (W + T - 1) / T;
-  const int w0 = tid * P, w1 = min(w0 + P, W);
-  int32_t aggStart = -1, aggLong = -1;
-  for (int w = w0; w < w1; ++w) {
-    const int32_t len = s_off[w + 1] - s_off[w];
-    if (len > 0) aggStart = s_off[w];
-    if (len > page) aggLong = s_off[w + 1];
-  }
-  int32_t tmp;
-  int32_t lastStart = block_exscan(aggStart, -1, OpMax(), s_scan, &tmp);
-  int32_t lastLongEnd = block_exscan(aggLong, -1, OpMax(), s_scan, &tmp);
-  // count chunk starts among my windows
-  int32_t cnt = 0;
-  {
-    int32_t ls = lastStart, ll = lastLongEnd;
-    for (int w = w0; w < w1; ++w) {
-      const int32_t a = s_off[w], len = s_off[w + 1] - a;
-      if (len <= 0) continue;
-      const bool is_long = len > page;
-      const bool start = is_long || ls < 0 || ll == a || (ls / page) != (a / page);
-      cnt += start;
-      ls = a;
-      if (is_long) ll = a + len;
-    }
-  }
-  int32_t n_chunks = 0;
-  int32_t c = block_exscan(cnt, 0, OpSum(), s_scan, &n_chunks);
-  // s_aux is free again: record each chunk's first window
-  {
-    int32_t ls = lastStart, ll = lastLongEnd;
-    for (int w = w0; w < w1; ++w) {
-      const int32_t a = s_off[w], len = s_off[w + 1] - a;
-      if (len <= 0) continue;
-      const bool is_long = len > page;
-      const bool start = is_long || ls < 0 || ll == a || (ls / page) != (a / page);
-      if (start) s_aux[c++] = w;
-      ls = a;
-      if (is_long) ll = a + len;
-    }
-  }
-  __syncthreads();
-  for (int i = tid; i < n_chunks; i += T) {
-    const int32_t wb = s_aux[i];
-    const int32_t we = i + 1 < n_chunks ? s_aux[i + 1] : W;
-    Chunk ch;
-    ch.row_begin = s_off[wb];
-    ch.row_end = s_off[we];
-    ch.win_begin = wb;
-    ch.win_end = we;
-    chunks[i] = ch;
-  }
-  if (tid == 0) {
-    hdr->magic = kPlanMagic;
-    hdr->n = n;
-    hdr->num_windows = W;
-    hdr->chunk_rows = L;
-    hdr->n_chunks = n_chunks;
-    hdr->csr = csr;
-    hdr->invalid = invalid;
-    hdr->claim[0] = hdr->claim[1] = 0;
-    hdr->done[0] = hdr->done[1] = 0;
-    if (invalid_out) *invalid_out = invalid;
-  }
+  const int32_t n_chunks = build_chunks(s_off, s_aux, W, L, chunks, s_scan);
+  if (tid == 0) write_header(hdr, n, W, L, n_chunks, csr, invalid, invalid_out);
 }
 
 // --------------------------------------------------------------- k_scatter
@@ -250,60 +217,161 @@ __device__ __forceinline__ uint64_t lanemask_lt(int lane) {
   return lane == 0 ? 0ull : (~0ull >> (64 - lane));
 }
 
-__global__ __launch_bounds__(256) void k_scatter(const int32_t* __restrict__ ids, int32_t n,
-                                                  int32_t W, int32_t E,
-                                                  const int32_t* __restrict__ colpref,
-                                                  const int32_t* __restrict__ offs,
-                                                  int32_t* __restrict__ perm,
-                                                  int32_t* __restrict__ perm_out) {
-  __shared__ int32_t hist[2 * kMaxWindows];
-  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6, nw = blockDim.x >> 6;
-  const int nbits = W > 1 ? 32 - __clz(W - 1) : 0;
-  for (int i = threadIdx.x; i < nw * W; i += blockDim.x) hist[i] = 0;
-  __syncthreads();
-  const int64_t span = E / nw;
-  const int64_t wbeg = (int64_t)blockIdx.x * E + wv * span;
-  const int64_t wend = wbeg + span < n ? wbeg + span : n;
-  int32_t* h = hist + wv * W;
-  const uint64_t lt = lanemask_lt(lane);
+// Dynamic LDS: base[W + 1] then hist[max(nws W, W + 1)], nws = waves that rank rows.
+__global__ __launch_bounds__(kBuildThreads) void k_scatter(
+    const int32_t* __restrict__ ids, int32_t n, int32_t W, int32_t L, int32_t E, int32_t nb,
+    int32_t ld, int32_t nws, const int32_t* __restrict__ counts, int32_t* __restrict__ perm,
+    int32_t* __restrict__ perm_out, int32_t* __restrict__ plan_offsets,
+    int32_t* __restrict__ offsets_out, Chunk* __restrict__ chunks, PlanHeader* __restrict__ hdr,
+    int32_t* __restrict__ invalid_out) {
+  extern __shared__ int32_t lds[];
+  __shared__ int32_t s_scan[33];
+  int32_t* base = lds;               // offsets[w] + rows of window w in earlier blocks
+  int32_t* hist = lds + (W + 1);     // column totals, then the per-wave row counts
+  const int tid = threadIdx.x, T = blockDim.x;
+  const int lane = tid & 63, wv = tid >> 6;
+  const int32_t blk = blockIdx.x;
 
-  // per-wave histogram, rows in order
-  for (int64_t g = wbeg; g < wend; g += 64) {
-    const int64_t i = g + lane;
-    const bool in = i < wend;
-    const int32_t id = in ? ids[i] : -1;
-    const bool valid = in && (uint32_t)id < (uint32_t)W;
-    const uint64_t m = match_key(id, valid, nbits);
-    if (valid && (m & lt) == 0) h[id] += __popcll(m);
+  // (1) column prefix over the earlier blocks and column totals.  Thread (part,
+  // g) sums rows [part RP, part RP + RP) of column group g (4 columns, one 16-B
+  // load per row), so all of a thread's loads are in flight together.
+  for (int w = tid; w <= W; w += T) {
+    base[w] = 0;
+    hist[w] = 0;
   }
   __syncthreads();
-  // base of every wave inside the block, per window
-  for (int w = threadIdx.x; w < W; w += blockDim.x) {
+  {
+    const int G = ld >> 2;
+    const int R = G >= T ? 1 : min(T / G, nb);
+    const int RP = (nb + R - 1) / R;
+    for (int item = tid; item < R * G; item += T) {
+      const int part = item / G, g = item - part * G;
+      const int b0 = part * RP, b1 = min(b0 + RP, nb);
+      int4 pre = make_int4(0, 0, 0, 0), tot = make_int4(0, 0, 0, 0);
+      for (int b = b0; b < b1; b += 16) {
+        int4 x[16];
+#pragma unroll
+        for (int u = 0; u < 16; ++u)
+          x[u] = b + u < b1 ? reinterpret_cast<const int4*>(counts + (size_t)(b + u) * ld)[g]
+                            : make_int4(0, 0, 0, 0);
+#pragma unroll
+        for (int u = 0; u < 16; ++u) {
+          tot.x += x[u].x; tot.y += x[u].y; tot.z += x[u].z; tot.w += x[u].w;
+          if (b + u < blk) { pre.x += x[u].x; pre.y += x[u].y; pre.z += x[u].z; pre.w += x[u].w; }
+        }
+      }
+      const int w = 4 * g;
+      const int32_t p4[4] = {pre.x, pre.y, pre.z, pre.w}, t4[4] = {tot.x, tot.y, tot.z, tot.w};
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        if (w + k <= W) {
+          if (R > 1) {
+            atomicAdd(&base[w + k], p4[k]);
+            atomicAdd(&hist[w + k], t4[k]);
+          } else {
+            base[w + k] = p4[k];
+            hist[w + k] = t4[k];
+          }
+        }
+      }
+    }
+  }
+  __syncthreads();
+  const int32_t invalid = hist[W];   // column W counts the out-of-range ids
+
+  // (2) offsets = exclusive scan of the column totals; base += offsets
+  {
+    const int P = (W + T - 1) / T;
+    const int w0 = min(tid * P, W), w1 = min(w0 + P, W);
+    int32_t local = 0;
+    for (int w = w0; w < w1; ++w) local += hist[w];
+    int32_t total = 0;
+    int32_t ex = block_exscan(local, 0, OpSum(), s_scan, &total);
+    for (int w = w0; w < w1; ++w) {
+      const int32_t t = hist[w];
+      base[w] += ex;
+      ex += t;
+    }
+    if (tid == 0) base[W] = total;   // for block 0, base[0..W] are then the offsets
+  }
+  __syncthreads();
+  if (blk == 0) {
+    for (int w = tid; w <= W; w += T) {
+      plan_offsets[w] = base[w];
+      if (offsets_out) offsets_out[w] = base[w];
+    }
+  }
+
+  // (3) stable ranks: wave v of the first nws takes rows [v span, v span + span)
+  // of the block; per-wave window counts, their prefix over the waves, then the
+  // scatter with each wave's running counters.
+  for (int i = tid; i < nws * W; i += T) hist[i] = 0;
+  __syncthreads();
+  const int nbits = W > 1 ? 32 - __clz(W - 1) : 0;
+  const int64_t span = E / nws;
+  const int64_t rbeg = (int64_t)blk * E + wv * span;
+  const int64_t rend = rbeg + span < n ? rbeg + span : n;
+  int32_t* h = hist + wv * W;
+  const uint64_t lt = lanemask_lt(lane);
+  if (wv < nws) {
+    for (int64_t r = rbeg; r < rend; r += 64) {
+      const int64_t i = r + lane;
+      const bool in = i < rend;
+      const int32_t id = in ? ids[i] : -1;
+      const bool valid = in && (uint32_t)id < (uint32_t)W;
+      const uint64_t m = match_key(id, valid, nbits);
+      if (valid && (m & lt) == 0) h[id] += __popcll(m);
+    }
+  }
+  __syncthreads();
+  for (int w = tid; w < W; w += T) {
     int32_t run = 0;
-    for (int v = 0; v < nw; ++v) {
+    for (int v = 0; v < nws; ++v) {
       const int32_t t = hist[v * W + w];
       hist[v * W + w] = run;
       run += t;
     }
   }
   __syncthreads();
-  const int32_t* cp = colpref + (size_t)blockIdx.x * (W + 1);
-  for (int64_t g = wbeg; g < wend; g += 64) {
-    const int64_t i = g + lane;
-    const bool in = i < wend;
-    const int32_t id = in ? ids[i] : -1;
-    const bool valid = in && (uint32_t)id < (uint32_t)W;
-    const uint64_t m = match_key(id, valid, nbits);
-    if (valid) {
-      const int32_t base = h[id];
-      const int32_t pos = offs[id] + cp[id] + base + __popcll(m & lt);
-      if ((uint32_t)pos < (uint32_t)n) {
-        perm[pos] = (int32_t)i;
-        if (perm_out) perm_out[pos] = (int32_t)i;
+  if (wv < nws) {
+    for (int64_t r = rbeg; r < rend; r += 64) {
+      const int64_t i = r + lane;
+      const bool in = i < rend;
+      const int32_t id = in ? ids[i] : -1;
+      const bool valid = in && (uint32_t)id < (uint32_t)W;
+      const uint64_t m = match_key(id, valid, nbits);
+      if (valid) {
+        const int32_t hb = h[id];
+        const int32_t pos = base[id] + hb + __popcll(m & lt);
+        if ((uint32_t)pos < (uint32_t)n) {
+          perm[pos] = (int32_t)i;
+          if (perm_out) perm_out[pos] = (int32_t)i;
+        }
+        if ((m & lt) == 0) h[id] = hb + __popcll(m);
       }
-      if ((m & lt) == 0) h[id] = base + __popcll(m);
     }
   }
+
+  // (4) block 0: chunk table and header (hist is free again)
+  if (blk == 0) {
+    __syncthreads();
+    const int32_t n_chunks = build_chunks(base, hist, W, L, chunks, s_scan);
+    if (tid == 0) write_header(hdr, n, W, L, n_chunks, 0, invalid, invalid_out);
+  }
+}
+
+// Waves of k_scatter that rank rows: as many as the LDS holds (<= 16), and at
+// most one per 64 rows of a block.
+static int scatter_waves(int32_t W, int32_t E, size_t* lds_bytes) {
+  constexpr size_t kLds = 160 * 1024 - 1024;   // leave room for the static arrays
+  int nws = kBuildThreads / 64;
+  auto bytes = [&](int v) {
+    const size_t h = (size_t)v * W > (size_t)W + 1 ? (size_t)v * W : (size_t)W + 1;
+    return ((size_t)W + 1 + h) * 4;
+  };
+  while (nws > 1 && (bytes(nws) > kLds || (int64_t)nws * 64 > E)) nws >>= 1;
+  *lds_bytes = bytes(nws);
+  return nws;
 }
 
 // ------------------------------------------------------------ host launchers
@@ -317,17 +385,29 @@ hipError_t launch_build(const int32_t* ids, int32_t n, int32_t W, int32_t L, int
   Chunk* chunks = reinterpret_cast<Chunk*>(base + lay.chunks);
   int32_t* counts = reinterpret_cast<int32_t*>(base + lay.counts);
   const int csr = ids == nullptr;
-  if (!csr && lay.n_blocks > 0) {
-    hipLaunchKernelGGL(k_count, dim3(lay.n_blocks), dim3(256), 0, stream, ids, n, W,
-                       lay.block_elems, counts);
+  if (csr || lay.n_blocks == 0) {
+    hipLaunchKernelGGL(k_plan, dim3(1), dim3(kBuildThreads), 0, stream, csr, W, n, L, offsets_io,
+                       invalid_out, hdr, offs, chunks);
+    return hipGetLastError();
   }
-  hipLaunchKernelGGL(k_plan, dim3(1), dim3(kPlanThreads), 0, stream, csr, counts,
-                     csr ? 0 : lay.n_blocks, W, n, L, offsets_io, invalid_out, hdr, offs, chunks);
-  if (!csr && lay.n_blocks > 0) {
-    const int nw = W <= kMaxWindows / 2 ? 4 : 2;
-    hipLaunchKernelGGL(k_scatter, dim3(lay.n_blocks), dim3(64 * nw), 0, stream, ids, n, W,
-                       lay.block_elems, counts, offs, perm, perm_out);
+  hipLaunchKernelGGL(k_count, dim3(lay.n_blocks), dim3(kBuildThreads), 0, stream, ids, n, W,
+                     lay.block_elems, lay.counts_ld, counts);
+  size_t lds = 0;
+  const int nws = scatter_waves(W, lay.block_elems, &lds);
+  // the dynamic LDS of k_scatter exceeds the default limit: raise it once per device
+  static bool lds_attr[64] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= 64 || !lds_attr[dev]) {
+    e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_scatter),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024 - 1024);
+    if (e != hipSuccess) return e;
+    if (dev >= 0 && dev < 64) lds_attr[dev] = true;
   }
+  hipLaunchKernelGGL(k_scatter, dim3(lay.n_blocks), dim3(kBuildThreads), lds, stream, ids, n, W, L,
+                     lay.block_elems, lay.n_blocks, lay.counts_ld, nws, counts, perm, perm_out,
+                     offs, offsets_io, chunks, hdr, invalid_out);
   return hipGetLastError();
 }
 

@@ -146,6 +146,22 @@ def test_builder_random(sla, seed):
     check_plan(sla, plan, ids, W, L)
 
 
+# block sizes (2048 rows and up, at most 32 blocks), LDS limits of the scatter
+# (fewer ranking waves for large W) and the block prefix over many blocks
+@pytest.mark.parametrize("W,n,L,srt", [(16384, 1_000_000, 128, False), (8193, 100_000, 64, False),
+                                       (6000, 65_536, 128, False), (1, 200_000, 32, False),
+                                       (2, 65_537, 4096, True), (1521, 2_000_000, 128, False),
+                                       (300, 4097, 256, True)])
+def test_builder_shapes(sla, W, n, L, srt):
+    rng = np.random.default_rng([8, W, n])
+    ids = rng.integers(0, W, size=n).astype(np.int32)
+    if srt:
+        ids = np.sort(ids)
+    _say(f"[builder shapes] n={n} W={W} L={L} sorted={srt}")
+    plan = build(sla, ids=ids, W=W, chunk_rows=L)
+    check_plan(sla, plan, ids, W, L)
+
+
 def test_builder_degenerate(sla):
     for ids, W in ((np.zeros(5000, np.int32), 1), (np.full(5000, 7, np.int32), 64),
                    (np.arange(3000, dtype=np.int32)[::-1].copy(), 3000),
