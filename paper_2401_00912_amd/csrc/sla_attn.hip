@@ -49,10 +49,15 @@ namespace sla {
 constexpr int kWaves = 4;       // waves (heads) per workgroup
 constexpr int kSliceRows = 32;  // rows per job
 
+constexpr float kLog2e = 1.4426950408889634f;
+
+// phi(x) = x + 1 for x > 0, exp(x) otherwise, and its derivative.  With 16-bit
+// storage the result is rounded to 16 bits for the matrix cores, so the
+// hardware exp2 (about 1 ulp of fp32) is ample; fp32 storage keeps expf.
 template <typename T>
 __device__ __forceinline__ float phi_f(float x) {
   if constexpr (Ty<T>::kNarrow) {
-    return x > 0.f ? x + 1.f : __expf(x);
+    return x > 0.f ? x + 1.f : __builtin_amdgcn_exp2f(x * kLog2e);
   } else {
     return x > 0.f ? x + 1.f : expf(x);
   }
@@ -61,9 +66,20 @@ __device__ __forceinline__ float phi_f(float x) {
 template <typename T>
 __device__ __forceinline__ float dphi_f(float x) {
   if constexpr (Ty<T>::kNarrow) {
-    return x > 0.f ? 1.f : __expf(x);
+    return x > 0.f ? 1.f : __builtin_amdgcn_exp2f(x * kLog2e);
   } else {
     return x > 0.f ? 1.f : expf(x);
+  }
+}
+
+// 1 / x: the hardware reciprocal (1 ulp) for 16-bit storage, a correctly
+// rounded division for fp32.
+template <typename T>
+__device__ __forceinline__ float recip(float x) {
+  if constexpr (Ty<T>::kNarrow) {
+    return __builtin_amdgcn_rcpf(x);
+  } else {
+    return 1.f / x;
   }
 }
 
@@ -86,6 +102,13 @@ __device__ __forceinline__ float sum_groups(float x) {
   x = __uint_as_float(a[0]) + __uint_as_float(a[1]);
   auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
   return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+
+// Make this wave's LDS writes visible to its other lanes.
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
 }
 
 // Max (MAX) or min over the wave, returned wave-uniform: DPP within each row of
@@ -139,35 +162,35 @@ struct RowIO {
     x = r[0];
     y = r[1];
   }
-  // `row` points at the head's first element; ok == false gives zeros.  The
-  // result is in memory order until arrange() puts it into slot order (kept
+  // `row` points at the head's first element.  The load is unconditional (the
+  // caller passes a valid row for rows past a job and masks them in the math):
+  // merging a guarded load with a default would wait for the load right here.
+  // The result is in memory order until arrange() puts it into slot order (kept
   // apart so that a prefetched fragment is not waited for at load time).
-  __device__ static R fetch(const T* row, int g, bool ok) {
-    R r;
+  __device__ static R fetch(const T* row, int g) {
     if constexpr (kSwizzle) {
-      uint4 w = make_uint4(0, 0, 0, 0);
-      if (ok) w = *reinterpret_cast<const uint4*>(row + 8 * g);
-      r = __builtin_bit_cast(R, w);
+      return __builtin_bit_cast(R, *reinterpret_cast<const uint4*>(row + 8 * g));
     } else if constexpr (Ty<T>::kNarrow) {
+      R r;
 #pragma unroll
       for (int t = 0; t < NT; ++t) {
-        u16x4 p = {0, 0, 0, 0};
-        if (ok) p = *reinterpret_cast<const u16x4*>(row + 16 * t + 4 * g);
+        const u16x4 p = *reinterpret_cast<const u16x4*>(row + 16 * t + 4 * g);
 #pragma unroll
         for (int j = 0; j < 4; ++j) r[4 * t + j] = p[j];
       }
+      return r;
     } else {
+      R r;
 #pragma unroll
       for (int t = 0; t < NT; ++t) {
-        float4 p = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (ok) p = *reinterpret_cast<const float4*>(row + 16 * t + 4 * g);
+        const float4 p = *reinterpret_cast<const float4*>(row + 16 * t + 4 * g);
         r[4 * t + 0] = p.x;
         r[4 * t + 1] = p.y;
         r[4 * t + 2] = p.z;
         r[4 * t + 3] = p.w;
       }
+      return r;
     }
-    return r;
   }
   __device__ static void arrange(R& r) {
     if constexpr (kSwizzle) {
@@ -227,13 +250,11 @@ struct Slice {
 // A window state (or state gradient) as result tiles:
 //   M[et][ct]  lane (c', g) component j = M[16 et + 4 g + j][16 ct + c']
 //   V[et]      lane (*, g) component j  = v[16 et + 4 g + j]  (the extra column)
-//   MT[ct][et] lane (e', g) component j = M[16 et + e'][16 ct + 4 g + j]  (backward)
-template <int D, bool WT>
+template <int D>
 struct State {
   static constexpr int NT = Geo<D>::NT;
   floatx4 M[NT][NT];
   floatx4 V[NT];
-  floatx4 MT[WT ? NT : 1][WT ? NT : 1];
   __device__ void clear() {
     const floatx4 z = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -241,12 +262,6 @@ struct State {
       V[a] = z;
 #pragma unroll
       for (int b = 0; b < NT; ++b) M[a][b] = z;
-    }
-    if constexpr (WT) {
-#pragma unroll
-      for (int a = 0; a < NT; ++a)
-#pragma unroll
-        for (int b = 0; b < NT; ++b) MT[a][b] = z;
     }
   }
   // largest |entry| of M and V over the wave
@@ -280,14 +295,78 @@ struct Sel {
   }
 };
 
-// phi of a fragment, rounded to the storage type; zero where !ok.
+// phi of a fragment, rounded to the storage type; zero where !ok.  fp16 works on
+// packed halves, phi(x) = 2^(min(x, 0) log2 e) + max(x, 0), which equals the
+// definition on both branches.
+typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
+
 template <typename T, int KS>
 __device__ __forceinline__ Raw<T, KS> phi_frag(Raw<T, KS> x, bool ok) {
-  float f[KS];
-  Frag<T, KS>::to_f32(x, f);
+  if constexpr (std::is_same<T, _Float16>::value) {
+    constexpr int NW = KS / 2;
+    using W = uint32_t __attribute__((ext_vector_type(NW)));
+    const W w = __builtin_bit_cast(W, x);
+    W out;
+    const half2_t zero = {0, 0};
+    const half2_t l2e = {(_Float16)kLog2e, (_Float16)kLog2e};
 #pragma unroll
-  for (int r = 0; r < KS; ++r) f[r] = ok ? phi_f<T>(f[r]) : 0.f;
-  return Frag<T, KS>::from_f32(f);
+    for (int k = 0; k < NW; ++k) {
+      const half2_t p = __builtin_bit_cast(half2_t, (uint32_t)w[k]);
+      const half2_t mn = __builtin_elementwise_min(p, zero) * l2e;
+      const half2_t mx = __builtin_elementwise_max(p, zero);
+      half2_t e;
+      e.x = __builtin_exp2f16(mn.x);
+      e.y = __builtin_exp2f16(mn.y);
+      const uint32_t r = __builtin_bit_cast(uint32_t, mx + e);
+      out[k] = ok ? r : 0u;
+    }
+    return __builtin_bit_cast(Raw<T, KS>, out);
+  } else {
+    float f[KS];
+    Frag<T, KS>::to_f32(x, f);
+#pragma unroll
+    for (int r = 0; r < KS; ++r) f[r] = ok ? phi_f<T>(f[r]) : 0.f;
+    return Frag<T, KS>::from_f32(f);
+  }
+}
+
+// phi of a fragment (as phi_frag) and phi' at the same slots in fp32, sharing
+// the exponential: with e = exp(min(x, 0)), phi(x) = e + max(x, 0), phi'(x) = e.
+template <typename T, int KS>
+__device__ __forceinline__ void phi_dphi(Raw<T, KS> x, bool ok, Raw<T, KS>& phi,
+                                         float (&dphi)[KS]) {
+  if constexpr (std::is_same<T, _Float16>::value) {
+    constexpr int NW = KS / 2;
+    using W = uint32_t __attribute__((ext_vector_type(NW)));
+    const W w = __builtin_bit_cast(W, x);
+    W out;
+    const half2_t zero = {0, 0};
+    const half2_t l2e = {(_Float16)kLog2e, (_Float16)kLog2e};
+#pragma unroll
+    for (int k = 0; k < NW; ++k) {
+      const half2_t p = __builtin_bit_cast(half2_t, (uint32_t)w[k]);
+      const half2_t mn = __builtin_elementwise_min(p, zero) * l2e;
+      const half2_t mx = __builtin_elementwise_max(p, zero);
+      half2_t e;
+      e.x = __builtin_exp2f16(mn.x);
+      e.y = __builtin_exp2f16(mn.y);
+      out[k] = ok ? __builtin_bit_cast(uint32_t, mx + e) : 0u;
+      dphi[2 * k] = (float)e.x;
+      dphi[2 * k + 1] = (float)e.y;
+    }
+    phi = __builtin_bit_cast(Raw<T, KS>, out);
+  } else {
+    float f[KS];
+    Frag<T, KS>::to_f32(x, f);
+#pragma unroll
+    for (int r = 0; r < KS; ++r) {
+      const float m = fminf(f[r], 0.f);
+      const float e = Ty<T>::kNarrow ? __builtin_amdgcn_exp2f(m * kLog2e) : expf(m);
+      dphi[r] = e;
+      f[r] = ok ? e + fmaxf(f[r], 0.f) : 0.f;
+    }
+    phi = Frag<T, KS>::from_f32(f);
+  }
 }
 
 // 8-slot row operand of a row contraction: slot r <-> row r0 + E(g, r) of the
@@ -307,12 +386,12 @@ __device__ __forceinline__ bool sub_overlaps(int32_t r0, int s, int32_t a, int32
   return r0 + 16 * s < b && r0 + 16 * s + 16 > a;
 }
 
-// Rows [a, b) of one slice into the state: M += phi(K)^T V, V += phi(K)^T 1, and
-// for the backward MT += V^T phi(K).  K is matrix 0, V matrix 1.
-template <typename T, int D, int NM, bool WT>
+// Rows [a, b) of one slice into the state: M += phi(K)^T V, V += phi(K)^T 1.
+// K is matrix 0, V matrix 1.
+template <typename T, int D, int NM>
 __device__ __forceinline__ void state_seg(const Slice<T, Geo<D>::KS, NM>& sb, int32_t r0,
                                           int32_t a, int32_t b, int i, int g,
-                                          const Sel<T, D>& sel, State<D, WT>& st) {
+                                          const Sel<T, D>& sel, State<D>& st) {
   constexpr int KS = Geo<D>::KS, NT = Geo<D>::NT;
   using F = Frag<T, KS>;
   const floatx4 zero = {0.f, 0.f, 0.f, 0.f};
@@ -329,7 +408,9 @@ __device__ __forceinline__ void state_seg(const Slice<T, Geo<D>::KS, NM>& sb, in
       tv[s][t] = F::mma(vv, sel.m[t], zero);
     }
   }
-  const Raw<T, 8> ones = row_mask<T>(r0, g, a, b, 1.f);
+  // phi(K) is already zero outside [a, b), so z needs no row mask
+  float one8[8] = {1.f, 1.f, 1.f, 1.f, 1.f, 1.f, 1.f, 1.f};
+  const Raw<T, 8> ones = Frag<T, 8>::from_f32(one8);
 #pragma unroll
   for (int et = 0; et < NT; ++et) {
     const Raw<T, 8> pk = pack_rows<T>(tk[0][et], tk[1][et]);
@@ -338,7 +419,6 @@ __device__ __forceinline__ void state_seg(const Slice<T, Geo<D>::KS, NM>& sb, in
     for (int ct = 0; ct < NT; ++ct) {
       const Raw<T, 8> pv = pack_rows<T>(tv[0][ct], tv[1][ct]);
       st.M[et][ct] = Frag<T, 8>::mma(pk, pv, st.M[et][ct]);
-      if constexpr (WT) st.MT[ct][et] = Frag<T, 8>::mma(pv, pk, st.MT[ct][et]);
     }
   }
 }
@@ -359,15 +439,14 @@ __device__ __forceinline__ Raw<T, Geo<D>::KS> tiles_operand(const floatx4 (&tl)[
 template <typename T, int D>
 struct FwdOp {
   Raw<T, Geo<D>::KS> A[Geo<D>::NT];  // sig S as operand of result tile ct (contract e)
-  float z[Geo<D>::KS];               // z at the lane's head-dim slots (fp32)
-  float inv_sig;
+  Raw<T, Geo<D>::KS> Az;             // sig z in rows 0, 4, 8, 12: the normaliser of every
+                                     // row lands in component 0 of every lane group
 };
 
 template <typename T, int D>
-__device__ __forceinline__ void make_fwd_op(const State<D, false>& st, FwdOp<T, D>& op) {
+__device__ __forceinline__ void make_fwd_op(const State<D>& st, FwdOp<T, D>& op, int i) {
   constexpr int KS = Geo<D>::KS, NT = Geo<D>::NT;
   const float sig = Ty<T>::kNarrow ? pow2_scale_to_one(st.absmax()) : 1.f;
-  op.inv_sig = 1.f / sig;
 #pragma unroll
   for (int ct = 0; ct < NT; ++ct) {
     floatx4 col[NT];
@@ -375,11 +454,16 @@ __device__ __forceinline__ void make_fwd_op(const State<D, false>& st, FwdOp<T, 
     for (int et = 0; et < NT; ++et) col[et] = st.M[et][ct];
     op.A[ct] = tiles_operand<T, D>(col, sig);
   }
+  const float zmul = (i & 3) == 0 ? sig : 0.f;
+  float zx[KS];
 #pragma unroll
-  for (int r = 0; r < KS; ++r) op.z[r] = st.V[r >> 2][r & 3];
+  for (int r = 0; r < KS; ++r) zx[r] = st.V[r >> 2][r & 3] * zmul;
+  op.Az = Frag<T, KS>::from_f32(zx);
 }
 
-// o = phi(q) S / (phi(q) . z) for rows [a, b) of one slice (Q is matrix QM).
+// o = phi(q) S / (phi(q) . z) for rows [a, b) of one slice (Q is matrix QM):
+// numerator and normaliser both come from the matrix cores with the same
+// rounded phi(q) and the same scale sig, which cancels.
 template <typename T, int D, int NM, int QM>
 __device__ __forceinline__ void apply_seg(const Slice<T, Geo<D>::KS, NM>& sb, int32_t r0,
                                           int32_t a, int32_t b, int i, int g,
@@ -392,14 +476,9 @@ __device__ __forceinline__ void apply_seg(const Slice<T, Geo<D>::KS, NM>& sb, in
     if (!sub_overlaps(r0, s, a, b)) continue;
     const int32_t row = r0 + 16 * s + i;
     const bool in = sb.ok[s] && row >= a && row < b;
-    float fq[KS];
     const Raw<T, KS> bq = phi_frag<T, KS>(sb.x[QM][s], in);
-    F::to_f32(bq, fq);
-    float den = 0.f;
-#pragma unroll
-    for (int r = 0; r < KS; ++r) den += fq[r] * op.z[r];
-    den = sum_groups(den);
-    const float scale = in ? op.inv_sig / den : 0.f;
+    const floatx4 den = F::mma(op.Az, bq, zero);
+    const float scale = recip<T>(den[0]);
     float ox[KS];
 #pragma unroll
     for (int ct = 0; ct < NT; ++ct) {
@@ -430,16 +509,53 @@ template <typename T, int D>
 struct BwdOp {
   Raw<T, Geo<D>::KS> A[Geo<D>::NT];  // sig S   (o = phi(q) S, tile ct)  | rho dS^T (dfk = v dS^T, tile et)
   Raw<T, Geo<D>::KS> B[Geo<D>::NT];  // sig S^T (dfq = dout S^T, tile et) | rho dS  (dv = phi(k) dS, tile ct)
-  float z[Geo<D>::KS];               // z                                 | dz
-  float inv_scale;                   // 1 / sig                           | 1 / rho
-  float beta;                        // scale of phi(q) / den in the state gradients
+  Raw<T, Geo<D>::KS> Az;             // sig z in rows 0, 4, 8, 12 (normaliser) | unused
+  float z[Geo<D>::KS];               // sig z                             | dz
+  float inv_scale;                   // unused                            | 1 / rho
+  float bsig;                        // beta sig: phi(q) / den in the state gradients is
+                                     // scaled by beta (<= min z, so beta phi(q) / den <= 1)
+  float inv_beta;                    // 1 / beta
 };
 
+// The transpose of a state as operands of a head-dim contraction: slot r of lane
+// (e', g) of tile et is M[16 et + e'][E(g, r)] * mul.  Goes through the wave's
+// own LDS tile (row e, column c, rows padded to keep 16-byte reads aligned).
+template <int D>
+constexpr int kTrLd = D + 4;
+
 template <typename T, int D>
-__device__ __forceinline__ void make_state_op(const State<D, true>& st, BwdOp<T, D>& op) {
+__device__ __forceinline__ void transposed_operand(const State<D>& st, float mul, float* tile,
+                                                   int i, int g,
+                                                   Raw<T, Geo<D>::KS> (&out)[Geo<D>::NT]) {
+  constexpr int KS = Geo<D>::KS, NT = Geo<D>::NT, LD = kTrLd<D>;
+#pragma unroll
+  for (int et = 0; et < NT; ++et)
+#pragma unroll
+    for (int ct = 0; ct < NT; ++ct)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) tile[(16 * et + 4 * g + j) * LD + 16 * ct + i] = st.M[et][ct][j];
+  wave_lds_sync();
+#pragma unroll
+  for (int et = 0; et < NT; ++et) {
+    float x[KS];
+#pragma unroll
+    for (int ct = 0; ct < NT; ++ct) {
+      const float4 p = *reinterpret_cast<const float4*>(tile + (16 * et + i) * LD + 16 * ct + 4 * g);
+      x[4 * ct + 0] = p.x * mul;
+      x[4 * ct + 1] = p.y * mul;
+      x[4 * ct + 2] = p.z * mul;
+      x[4 * ct + 3] = p.w * mul;
+    }
+    out[et] = Frag<T, KS>::from_f32(x);
+  }
+  wave_lds_sync();   // the tile may be written again by the next call
+}
+
+template <typename T, int D>
+__device__ __forceinline__ void make_state_op(const State<D>& st, BwdOp<T, D>& op, float* tile,
+                                              int i, int g) {
   constexpr int KS = Geo<D>::KS, NT = Geo<D>::NT;
   const float sig = Ty<T>::kNarrow ? pow2_scale_to_one(st.absmax()) : 1.f;
-  op.inv_scale = 1.f / sig;
 #pragma unroll
   for (int ct = 0; ct < NT; ++ct) {
     floatx4 col[NT];
@@ -447,39 +563,34 @@ __device__ __forceinline__ void make_state_op(const State<D, true>& st, BwdOp<T,
     for (int et = 0; et < NT; ++et) col[et] = st.M[et][ct];
     op.A[ct] = tiles_operand<T, D>(col, sig);
   }
-#pragma unroll
-  for (int et = 0; et < NT; ++et) {
-    floatx4 col[NT];
-#pragma unroll
-    for (int ct = 0; ct < NT; ++ct) col[ct] = st.MT[ct][et];
-    op.B[et] = tiles_operand<T, D>(col, sig);
-  }
+  transposed_operand<T, D>(st, sig, tile, i, g, op.B);
   float zmin = 3.0e38f;
+  const float zmul = (i & 3) == 0 ? sig : 0.f;
+  float zx[KS];
 #pragma unroll
   for (int r = 0; r < KS; ++r) {
-    op.z[r] = st.V[r >> 2][r & 3];
-    zmin = fminf(zmin, op.z[r]);
+    const float z = st.V[r >> 2][r & 3];
+    zmin = fminf(zmin, z);
+    op.z[r] = z * sig;
+    zx[r] = z * zmul;
   }
+  op.Az = Frag<T, KS>::from_f32(zx);
   // phi(q)_e / den <= 1 / z_e <= 1 / min z, so beta phi(q) / den <= 1
-  op.beta = Ty<T>::kNarrow ? pow2_floor(wave_reduce<false>(zmin)) : 1.f;
+  const float beta = Ty<T>::kNarrow ? pow2_floor(wave_reduce<false>(zmin)) : 1.f;
+  op.bsig = beta * sig;
+  op.inv_beta = 1.f / beta;
 }
 
 // From state-gradient tiles that carry a factor `1 / inv_beta`.
 template <typename T, int D>
-__device__ __forceinline__ void make_grad_op(const State<D, true>& st, float inv_beta,
-                                             BwdOp<T, D>& op) {
+__device__ __forceinline__ void make_grad_op(const State<D>& st, float inv_beta, BwdOp<T, D>& op,
+                                             float* tile, int i, int g) {
   constexpr int KS = Geo<D>::KS, NT = Geo<D>::NT;
   const float mx = st.absmax() * inv_beta;
   const float rho = Ty<T>::kNarrow ? pow2_scale_to_one(mx) : 1.f;
   op.inv_scale = 1.f / rho;
   const float mul = rho * inv_beta;
-#pragma unroll
-  for (int et = 0; et < NT; ++et) {
-    floatx4 col[NT];
-#pragma unroll
-    for (int ct = 0; ct < NT; ++ct) col[ct] = st.MT[ct][et];
-    op.A[et] = tiles_operand<T, D>(col, mul);
-  }
+  transposed_operand<T, D>(st, mul, tile, i, g, op.A);
 #pragma unroll
   for (int ct = 0; ct < NT; ++ct) {
     floatx4 col[NT];
@@ -492,13 +603,14 @@ __device__ __forceinline__ void make_grad_op(const State<D, true>& st, float inv
 }
 
 // Rows [a, b) of one slice: dq, and into gs: M += beta (phi(q)/den)^T dout,
-// V += beta (phi(q)/den)^T (-dout.o), MT += beta dout^T (phi(q)/den).
-// q is matrix QI, dout matrix DI.
+// V += beta (phi(q)/den)^T (-dout.o).  q is matrix QI, dout matrix DI.  The
+// normaliser comes from the matrix cores (den' = sig den); with sig folded into
+// z, dphi(q) = (sig dfq - dot sig z) / den'.
 template <typename T, int D, int NM, int QI, int DI>
 __device__ __forceinline__ void qgrad_seg(const Slice<T, Geo<D>::KS, NM>& sb, int32_t r0,
                                           int32_t a, int32_t b, int i, int g,
                                           const Sel<T, D>& sel, const BwdOp<T, D>& op, T* dq,
-                                          size_t rs, int col, State<D, true>& gs) {
+                                          size_t rs, int col, State<D>& gs) {
   constexpr int KS = Geo<D>::KS, NT = Geo<D>::NT;
   using F = Frag<T, KS>;
   const floatx4 zero = {0.f, 0.f, 0.f, 0.f};
@@ -511,17 +623,13 @@ __device__ __forceinline__ void qgrad_seg(const Slice<T, Geo<D>::KS, NM>& sb, in
     xr[s] = F::zero();
     nd[s] = F::zero();
     if (!sub_overlaps(r0, s, a, b)) continue;
-    float qx[KS], fq[KS], dox[KS];
-    F::to_f32(sb.x[QI][s], qx);
-    F::to_f32(dr[s], dox);
-    const Raw<T, KS> bq = phi_frag<T, KS>(sb.x[QI][s], in);
+    Raw<T, KS> bq;
+    float dphq[KS], fq[KS], dox[KS];
+    phi_dphi<T, KS>(sb.x[QI][s], in, bq, dphq);
     F::to_f32(bq, fq);
-    float den = 0.f;
-#pragma unroll
-    for (int r = 0; r < KS; ++r) den += fq[r] * op.z[r];
-    den = sum_groups(den);
-    if (!in) den = 1.f;
-    const float inv_den = 1.f / den;
+    F::to_f32(dr[s], dox);
+    const floatx4 den4 = F::mma(op.Az, bq, zero);
+    const float rden = recip<T>(in ? den4[0] : 1.f);
     float dot = 0.f;
 #pragma unroll
     for (int ct = 0; ct < NT; ++ct) {
@@ -529,7 +637,7 @@ __device__ __forceinline__ void qgrad_seg(const Slice<T, Geo<D>::KS, NM>& sb, in
 #pragma unroll
       for (int j = 0; j < 4; ++j) dot += dox[4 * ct + j] * d4[j];
     }
-    dot = sum_groups(dot) * (op.inv_scale * inv_den);
+    dot = sum_groups(dot) * rden;  // lane exchange: every lane takes part
     if (!in) dot = 0.f;
     float dqx[KS];
 #pragma unroll
@@ -538,14 +646,15 @@ __device__ __forceinline__ void qgrad_seg(const Slice<T, Geo<D>::KS, NM>& sb, in
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int r = 4 * et + j;
-        dqx[r] = (d4[j] * op.inv_scale - dot * op.z[r]) * inv_den * dphi_f<T>(qx[r]);
+        dqx[r] = (d4[j] - dot * op.z[r]) * rden * dphq[r];
       }
     }
     RowIO<T, D>::put(dq + (size_t)sb.o[s] * rs + col, g, F::from_f32(dqx), in);
     float xs[KS], ns[KS];
+    const float w = op.bsig * rden;
 #pragma unroll
     for (int r = 0; r < KS; ++r) {
-      xs[r] = fq[r] * (op.beta * inv_den);
+      xs[r] = fq[r] * w;
       ns[r] = -dot;
     }
     xr[s] = F::from_f32(xs);
@@ -570,7 +679,6 @@ __device__ __forceinline__ void qgrad_seg(const Slice<T, Geo<D>::KS, NM>& sb, in
     for (int ct = 0; ct < NT; ++ct) {
       const Raw<T, 8> pd = pack_rows<T>(td[0][ct], td[1][ct]);
       gs.M[et][ct] = Frag<T, 8>::mma(px, pd, gs.M[et][ct]);
-      gs.MT[ct][et] = Frag<T, 8>::mma(pd, px, gs.MT[ct][et]);
     }
   }
 }
@@ -589,9 +697,9 @@ __device__ __forceinline__ void kgrad_seg(const Slice<T, Geo<D>::KS, NM>& sb, in
     if (!sub_overlaps(r0, s, a, b)) continue;
     const int32_t row = r0 + 16 * s + i;
     const bool in = sb.ok[s] && row >= a && row < b;
-    float kx[KS];
-    F::to_f32(sb.x[0][s], kx);
-    const Raw<T, KS> fk = phi_frag<T, KS>(sb.x[0][s], in);
+    Raw<T, KS> fk;
+    float dphk[KS];
+    phi_dphi<T, KS>(sb.x[0][s], in, fk, dphk);
     float dkx[KS], dvx[KS];
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
@@ -600,7 +708,7 @@ __device__ __forceinline__ void kgrad_seg(const Slice<T, Geo<D>::KS, NM>& sb, in
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int r = 4 * t + j;
-        dkx[r] = (a4[j] * op.inv_scale + op.z[r]) * dphi_f<T>(kx[r]);
+        dkx[r] = (a4[j] * op.inv_scale + op.z[r]) * dphk[r];
         dvx[r] = b4[j] * op.inv_scale;
       }
     }
@@ -689,56 +797,61 @@ struct Stream {
 template <typename T, int D>
 using JobBuf = Slice<T, Geo<D>::KS, 2>;
 
-// The permutation entries of the first 64 kPermRegs rows of a chunk, held by the
-// wave: register m of lane l is the original row of sorted row rb + 64 m + l.
-// Jobs inside that range take their rows from here with lane permutes; rows
-// beyond it (windows longer than the range) are read from the plan.
+// A page of the chunk's permutation, held by the wave: register m of lane l is
+// the original row of sorted row pb + 64 m + l.  Jobs take their rows from the
+// page with lane permutes; a job outside the page (windows longer than it)
+// first reloads the page at its own first row.  The reload waits for its loads
+// inside its own branch, so the common path never waits on the permutation and
+// the prefetched rows stay in flight.
 #ifndef SLA_PERM_REGS
-#define SLA_PERM_REGS 2
+#define SLA_PERM_REGS 4
 #endif
 constexpr int kPermRegs = SLA_PERM_REGS;
 
 struct PermRegs {
-  int32_t rb;
+  const int32_t* perm;  // null: identity (rows already window-sorted)
+  int32_t re;           // end of the chunk's rows
+  int32_t pb;           // first sorted row of the page
   int32_t r[kPermRegs];
-  __device__ __forceinline__ void load(const int32_t* perm, int32_t rb_, int32_t re, int lane) {
-    rb = rb_;
+  __device__ __forceinline__ void load(int32_t pb_, int lane) {
+    pb = pb_;
+    int32_t x[kPermRegs];
 #pragma unroll
     for (int m = 0; m < kPermRegs; ++m) {
-      const int32_t row = rb + 64 * m + lane;
-      r[m] = (perm && row < re) ? perm[row] : row;
+      const int32_t row = pb + 64 * m + lane;
+      x[m] = perm ? perm[row < re ? row : pb] : row;
+    }
+#pragma unroll
+    for (int m = 0; m < kPermRegs; ++m) {
+      asm volatile("" : "+v"(x[m]));  // consumed here: the wait stays in this branch
+      r[m] = x[m];
     }
   }
 };
 
 // Original rows of a job's two sub-tiles (o = 0 and ok = false past the job).
-__device__ __forceinline__ void job_rows(const Job& j, const int32_t* perm, const PermRegs& pr,
-                                         int i, int32_t (&o)[2], bool (&ok)[2]) {
-  if (j.w >= 0 && j.r0 + kSliceRows <= pr.rb + 64 * kPermRegs) {
-#pragma unroll
-    for (int s = 0; s < 2; ++s) {
-      const int32_t row = j.r0 + 16 * s + i;
-      const int32_t rel = row - pr.rb;
-      int32_t x = 0;
-#pragma unroll
-      for (int m = 0; m < kPermRegs; ++m) {
-        const int32_t t = __builtin_amdgcn_ds_bpermute((rel & 63) << 2, pr.r[m]);
-        if ((rel >> 6) == m) x = t;
-      }
-      ok[s] = row < j.we;
-      o[s] = ok[s] ? x : 0;
-    }
-    return;
-  }
+__device__ __forceinline__ void job_rows(const Job& j, PermRegs& pr, int lane, int32_t (&o)[2],
+                                         bool (&ok)[2]) {
+  if (j.w >= 0 && (j.r0 < pr.pb || j.r0 + kSliceRows > pr.pb + 64 * kPermRegs)) pr.load(j.r0, lane);
+  const int i = lane & 15;
 #pragma unroll
   for (int s = 0; s < 2; ++s) {
     const int32_t row = j.r0 + 16 * s + i;
+    const int32_t rel = row - pr.pb;
+    int32_t x = 0;
+#pragma unroll
+    for (int m = 0; m < kPermRegs; ++m) {
+      const int32_t t = __builtin_amdgcn_ds_bpermute((rel & 63) << 2, pr.r[m]);
+      if ((rel >> 6) == m) x = t;
+    }
     ok[s] = j.w >= 0 && row < j.we;
-    o[s] = ok[s] ? (perm ? perm[row] : row) : 0;
+    o[s] = ok[s] ? x : 0;
   }
 }
 
-// Rows of a job -> the job's two matrices (a, b; b may be null).
+// Rows of a job -> the job's two matrices (a, b; b null: the second fragment is
+// left as it is, the job's math does not read it).  Rows past the job read row
+// 0 (the math masks them; n >= 1 whenever a kernel runs).
 template <typename T, int D>
 __device__ __forceinline__ void job_load(JobBuf<T, D>& jb, const int32_t (&o)[2],
                                          const bool (&ok)[2], const T* a, const T* b, int32_t n,
@@ -747,9 +860,8 @@ __device__ __forceinline__ void job_load(JobBuf<T, D>& jb, const int32_t (&o)[2]
   for (int s = 0; s < 2; ++s) {
     jb.ok[s] = ok[s] && (uint32_t)o[s] < (uint32_t)n;
     jb.o[s] = jb.ok[s] ? o[s] : 0;
-    jb.x[0][s] = RowIO<T, D>::fetch(a + (size_t)jb.o[s] * rs + col, g, jb.ok[s]);
-    jb.x[1][s] = b ? RowIO<T, D>::fetch(b + (size_t)jb.o[s] * rs + col, g, jb.ok[s])
-                   : Frag<T, Geo<D>::KS>::zero();
+    jb.x[0][s] = RowIO<T, D>::fetch(a + (size_t)jb.o[s] * rs + col, g);
+    if (b) jb.x[1][s] = RowIO<T, D>::fetch(b + (size_t)jb.o[s] * rs + col, g);
   }
 }
 
@@ -798,49 +910,48 @@ void k_sla_fwd(KernelArgs a, const T* __restrict__ q, const T* __restrict__ k,
   int32_t wb;
   Stream str = chunk_stream<T, D>(a, c, wb, lane);
   PermRegs pr;
-  pr.load(perm, str.rb, str.re, lane);
-  auto mat_a = [&](const Job& j) { return j.phase == 0 ? k : q; };
-  auto mat_b = [&](const Job& j) { return j.phase == 0 ? v : (const T*)nullptr; };
+  pr.perm = perm;
+  pr.re = str.re;
+  pr.load(str.rb, lane);
+  auto load_job = [&](JobBuf<T, D>& jb, const Job& j) {
+    int32_t o[2];
+    bool ok[2];
+    job_rows(j, pr, lane, o, ok);
+    job_load<T, D>(jb, o, ok, j.phase == 0 ? k : q, j.phase == 0 ? v : (const T*)nullptr, n, rs,
+                   col, g);
+  };
 
+  // Three buffers used in turn (the loop is unrolled by three so that rows in
+  // flight are never copied between registers, which would wait for them).
   Job j0 = str.first(wb);
   Job j1 = str.next<2>(j0);
   Job j2 = str.next<2>(j1);
-  int32_t o0[2], o1[2], o2[2];
-  bool k0[2], k1[2], k2[2];
-  job_rows(j0, perm, pr, i, o0, k0);
-  job_rows(j1, perm, pr, i, o1, k1);
-  job_rows(j2, perm, pr, i, o2, k2);
-  JobBuf<T, D> b0, b1;
-  job_load<T, D>(b0, o0, k0, mat_a(j0), mat_b(j0), n, rs, col, g);
-  job_load<T, D>(b1, o1, k1, mat_a(j1), mat_b(j1), n, rs, col, g);
-  State<D, false> st;
+  JobBuf<T, D> b0, b1, b2;
+  load_job(b0, j0);
+  load_job(b1, j1);
+  State<D> st;
   FwdOp<T, D> op;
-  while (j0.w >= 0) {
-    const Job j3 = str.next<2>(j2);
-    int32_t o3[2];
-    bool k3[2];
-    job_rows(j3, perm, pr, i, o3, k3);
-    JobBuf<T, D> b2;
-    job_load<T, D>(b2, o2, k2, mat_a(j2), mat_b(j2), n, rs, col, g);
-
-    job_arrange<T, D>(b0);
+  auto step = [&](JobBuf<T, D>& cur, JobBuf<T, D>& nxt) {
+    load_job(nxt, j2);
+    job_arrange<T, D>(cur);
     if (j0.phase == 0) {
       if (j0.r0 == j0.ws) st.clear();
-      state_seg<T, D, 2, false>(b0, j0.r0, j0.ws, j0.we, i, g, sel, st);
-      if (j0.r0 + kSliceRows >= j0.we) make_fwd_op<T, D>(st, op);
+      state_seg<T, D, 2>(cur, j0.r0, j0.ws, j0.we, i, g, sel, st);
+      if (j0.r0 + kSliceRows >= j0.we) make_fwd_op<T, D>(st, op, i);
     } else {
-      apply_seg<T, D, 2, 0>(b0, j0.r0, j0.ws, j0.we, i, g, op, o, rs, col);
+      apply_seg<T, D, 2, 0>(cur, j0.r0, j0.ws, j0.we, i, g, op, o, rs, col);
     }
     j0 = j1;
     j1 = j2;
-    j2 = j3;
-    b0 = b1;
-    b1 = b2;
-#pragma unroll
-    for (int s = 0; s < 2; ++s) {
-      o2[s] = o3[s];
-      k2[s] = k3[s];
-    }
+    j2 = str.next<2>(j2);
+  };
+  for (;;) {
+    if (j0.w < 0) break;
+    step(b0, b2);
+    if (j0.w < 0) break;
+    step(b1, b0);
+    if (j0.w < 0) break;
+    step(b2, b1);
   }
 }
 
@@ -866,54 +977,52 @@ void k_sla_bwd(KernelArgs a, const T* __restrict__ q, const T* __restrict__ k,
   int32_t wb;
   Stream str = chunk_stream<T, D>(a, c, wb, lane);
   PermRegs pr;
-  pr.load(perm, str.rb, str.re, lane);
-  auto mat_a = [&](const Job& j) { return j.phase == 1 ? q : k; };
-  auto mat_b = [&](const Job& j) { return j.phase == 1 ? dout : v; };
+  pr.perm = perm;
+  pr.re = str.re;
+  pr.load(str.rb, lane);
+  auto load_job = [&](JobBuf<T, D>& jb, const Job& j) {
+    int32_t o[2];
+    bool ok[2];
+    job_rows(j, pr, lane, o, ok);
+    job_load<T, D>(jb, o, ok, j.phase == 1 ? q : k, j.phase == 1 ? dout : v, n, rs, col, g);
+  };
 
   Job j0 = str.first(wb);
   Job j1 = str.next<3>(j0);
   Job j2 = str.next<3>(j1);
-  int32_t o0[2], o1[2], o2[2];
-  bool k0[2], k1[2], k2[2];
-  job_rows(j0, perm, pr, i, o0, k0);
-  job_rows(j1, perm, pr, i, o1, k1);
-  job_rows(j2, perm, pr, i, o2, k2);
-  JobBuf<T, D> b0, b1;
-  job_load<T, D>(b0, o0, k0, mat_a(j0), mat_b(j0), n, rs, col, g);
-  job_load<T, D>(b1, o1, k1, mat_a(j1), mat_b(j1), n, rs, col, g);
-  State<D, true> st;  // phase 0: S, z, S^T ; phase 1: beta dS, beta dz, beta dS^T
+  JobBuf<T, D> b0, b1, b2;
+  load_job(b0, j0);
+  load_job(b1, j1);
+  State<D> st;  // phase 0: S, z ; phase 1: beta dS, beta dz
+  __shared__ float s_tr[kWaves][D * kTrLd<D>];  // transposes, one tile per wave
+  float* tile = s_tr[wv];
   BwdOp<T, D> op;
-  while (j0.w >= 0) {
-    const Job j3 = str.next<3>(j2);
-    int32_t o3[2];
-    bool k3[2];
-    job_rows(j3, perm, pr, i, o3, k3);
-    JobBuf<T, D> b2;
-    job_load<T, D>(b2, o2, k2, mat_a(j2), mat_b(j2), n, rs, col, g);
-
-    job_arrange<T, D>(b0);
+  auto step = [&](JobBuf<T, D>& cur, JobBuf<T, D>& nxt) {
+    load_job(nxt, j2);
+    job_arrange<T, D>(cur);
     const bool first = j0.r0 == j0.ws, last = j0.r0 + kSliceRows >= j0.we;
     if (j0.phase == 0) {
       if (first) st.clear();
-      state_seg<T, D, 2, true>(b0, j0.r0, j0.ws, j0.we, i, g, sel, st);
-      if (last) make_state_op<T, D>(st, op);
+      state_seg<T, D, 2>(cur, j0.r0, j0.ws, j0.we, i, g, sel, st);
+      if (last) make_state_op<T, D>(st, op, tile, i, g);
     } else if (j0.phase == 1) {
       if (first) st.clear();
-      qgrad_seg<T, D, 2, 0, 1>(b0, j0.r0, j0.ws, j0.we, i, g, sel, op, dq, rs, col, st);
-      if (last) make_grad_op<T, D>(st, 1.f / op.beta, op);
+      qgrad_seg<T, D, 2, 0, 1>(cur, j0.r0, j0.ws, j0.we, i, g, sel, op, dq, rs, col, st);
+      if (last) make_grad_op<T, D>(st, op.inv_beta, op, tile, i, g);
     } else {
-      kgrad_seg<T, D, 2>(b0, j0.r0, j0.ws, j0.we, i, g, op, dk, dv, rs, col);
+      kgrad_seg<T, D, 2>(cur, j0.r0, j0.ws, j0.we, i, g, op, dk, dv, rs, col);
     }
     j0 = j1;
     j1 = j2;
-    j2 = j3;
-    b0 = b1;
-    b1 = b2;
-#pragma unroll
-    for (int s = 0; s < 2; ++s) {
-      o2[s] = o3[s];
-      k2[s] = k3[s];
-    }
+    j2 = str.next<3>(j2);
+  };
+  for (;;) {
+    if (j0.w < 0) break;
+    step(b0, b2);
+    if (j0.w < 0) break;
+    step(b1, b0);
+    if (j0.w < 0) break;
+    step(b2, b1);
   }
 }
 
