@@ -66,15 +66,15 @@ const char* sla_status_string(sla_status_t status);
 /* Largest window-slot count supported (window tables live in on-chip memory). */
 int32_t sla_max_windows(void);
 
-/* Chunk length used when sla_build_segments() is given chunk_rows = 0. */
+/* Chunk length L used when sla_build_segments() is given chunk_rows = 0. */
 int32_t sla_default_chunk_rows(void);
 
 /*
  * Bytes of the plan buffer for n rows and num_windows window slots.
  * The plan holds the window-sorted view of the rows (Sec. 3.2: the flattened,
  * window-ordered matrix), its CSR window offsets, the chunk table (Fig. 3(a); the
- * Fig. 5 caption's "offsets generation" = start row of each chunk) and the
- * builder's scratch.  Returns 0 for invalid sizes.
+ * Fig. 5 caption's "offsets generation" = start row of each chunk), the table of
+ * long windows and the builder's scratch.  Returns 0 for invalid sizes.
  */
 size_t sla_plan_bytes(int64_t n, int32_t num_windows);
 
@@ -85,11 +85,14 @@ typedef struct {
   size_t offsets;    /* int32[num_windows + 1]: CSR over sorted positions   */
   size_t chunks;     /* int32[max_chunks][4]: row_begin, row_end,
                         win_begin, win_end                                  */
+  size_t longs;      /* int32[max_long][4]: window, row_begin, row_end, 0   */
   size_t total;      /* == sla_plan_bytes(n, num_windows)                   */
   int32_t max_chunks;
+  int32_t max_long;
 } sla_plan_layout_t;
 /* Plan header (int32 fields in order): magic, n, num_windows, chunk_rows,
- * n_chunks, csr (1 = rows were already window-sorted), invalid, then padding. */
+ * n_chunks, csr (1 = rows were already window-sorted), invalid, n_long, then
+ * padding. */
 
 sla_status_t sla_plan_layout(int64_t n, int32_t num_windows, sla_plan_layout_t* out /* host */);
 
@@ -113,11 +116,14 @@ sla_status_t sla_plan_layout(int64_t n, int32_t num_windows, sla_plan_layout_t* 
  * identity).  Violations are counted; the plan is then clamped into range so no
  * kernel reads out of bounds, but outputs are undefined.
  *
- * Chunk table (both modes), with L = chunk_rows (0 = default; else even, 32..4096)
- * and pages of L/2 rows: an empty window gets no chunk; a window of more than L/2
- * rows is a chunk of its own; shorter windows are packed into one chunk while
- * they start in the same page, so a packed chunk never splits a window and never
- * exceeds L - 1 rows.  Chunks are listed in sequence order.
+ * Work tables (both modes), with L = chunk_rows (0 = default 64; else even,
+ * 32..64) and pages of L/2 rows: a window of more than L rows is "long" and is
+ * listed in the long-window table (the forward and backward split its rows among
+ * the wavefronts of one workgroup, which add their partial window states); a
+ * window of L/2 + 1 .. L rows is a chunk of its own; shorter windows are packed
+ * into one chunk while they start in the same page, so a packed chunk never
+ * splits a window and never exceeds L - 1 rows.  Empty windows get nothing.  Both
+ * tables are in sequence order.
  *
  * invalid_count (device int32, may be NULL) receives the number of out-of-range
  * ids (mode A) or offset violations (mode B).  The plan must be at least

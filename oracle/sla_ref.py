@@ -24,8 +24,10 @@ What is computed, and the passage it follows
   result is unique.
 * ``chunk_plan_ref``: Sec. 3.2 / Fig. 3(a) partition the flattened matrix into
   chunks, and the Fig. 5 caption defines "offsets generation" as computing each
-  chunk's start row.  The packing rule written here is this library's own plan
-  rule (the paper does not give one); it is pinned by its invariants.
+  chunk's start row.  The packing rule written here (chunks of whole short
+  windows, a table of long windows that are split among workers) is this
+  library's own plan rule (the paper does not give one); it is pinned by its
+  invariants.
 * ``sla_forward_ref``: Eq. (2) (concatenation over the M non-empty windows of
   per-window linear attention) and Eq. (3) (per-window normalised linear
   attention), evaluated in the phi(Q)(phi(K)^T V) order of Sec. 3.1.  Non-causal:
@@ -103,42 +105,53 @@ def segments_ref(ids: np.ndarray, num_windows: int):
 
 
 def chunk_plan_ref(offsets: np.ndarray, chunk_rows: int):
-    """This library's chunk plan over window-sorted rows (plain sequential rule).
+    """This library's work plan over window-sorted rows (plain sequential rule).
 
-    With L = chunk_rows and P = L // 2:
-      * an empty window gets no chunk;
-      * a window with more than P rows ("long") is one chunk of its own;
-      * windows with 1..P rows ("short") are packed: a short window opens a new
-        chunk unless the previous non-empty window is short and starts in the
-        same P-row page (page = start_row // P).  A packed chunk therefore never
-        splits a window and never exceeds 2P - 1 = L - 1 rows.
-    A chunk runs from its first window's start row to the next chunk's start row
-    (the last one to offsets[-1]); its window range runs to the next chunk's first
-    window (the last one to num_windows), so trailing empty windows are included.
+    Sec. 3.2 / Fig. 3(a) cut the flattened matrix into pieces that are processed
+    independently; the paper fixes no packing rule, so this is the library's own,
+    pinned by its invariants.  With L = chunk_rows (even) and pages of P = L // 2
+    rows, every non-empty window is exactly one of:
+      * long  (more than L rows): listed in the long-window table and nowhere
+        else (its rows are split among several workers, whose partial states are
+        added before the output is formed);
+      * mid   (P < rows <= L): a chunk of its own;
+      * short (1..P rows): opens a new chunk unless the previous non-empty window
+        is short and starts in the same page (page = start_row // P); otherwise it
+        joins that chunk.  A chunk of short windows therefore never splits a
+        window and never exceeds 2P - 1 = L - 1 rows.
+    A chunk runs from its first window to the next "event" (the next chunk's first
+    window or the next long window, whichever comes first; the last one to
+    num_windows), so empty windows between are included; its rows are
+    [offsets[win_begin], offsets[win_end]).
 
-    Returns an int64 array [n_chunks, 4] of (row_begin, row_end, win_begin, win_end).
+    Returns (chunks, longs): int64 [n_chunks, 4] of (row_begin, row_end,
+    win_begin, win_end) in sequence order, and int64 [n_long] window ids in
+    sequence order.
     """
     off = [int(x) for x in offsets]
     nw = len(off) - 1
     page = chunk_rows // 2
-    starts = []  # (row_begin, win_begin)
-    prev = None  # (start_row, is_long) of the previous non-empty window
+    events = []  # (window, is_chunk_start) in sequence order
+    prev = None  # (start_row, is_short) of the previous non-empty window
     for w in range(nw):
         n = off[w + 1] - off[w]
         if n <= 0:
             continue
-        is_long = n > page
-        if is_long or prev is None or prev[1] or (prev[0] // page) != (off[w] // page):
-            starts.append((off[w], w))
-        prev = (off[w], is_long)
-    chunks = []
-    for i, (rb, wb) in enumerate(starts):
-        if i + 1 < len(starts):
-            re, we = starts[i + 1]
-        else:
-            re, we = off[nw], nw
-        chunks.append((rb, re, wb, we))
-    return np.asarray(chunks, dtype=np.int64).reshape(-1, 4)
+        short = n <= page
+        if n > chunk_rows:
+            events.append((w, False))
+        elif not short or prev is None or not prev[1] or (prev[0] // page) != (off[w] // page):
+            events.append((w, True))
+        prev = (off[w], short)
+    chunks, longs = [], []
+    for e, (w, is_chunk) in enumerate(events):
+        if not is_chunk:
+            longs.append(w)
+            continue
+        we = events[e + 1][0] if e + 1 < len(events) else nw
+        chunks.append((off[w], off[we], w, we))
+    return (np.asarray(chunks, dtype=np.int64).reshape(-1, 4),
+            np.asarray(longs, dtype=np.int64))
 
 
 def _window_rows(offsets, perm, w):

@@ -18,7 +18,7 @@ hipError_t launch_backward(const void* plan, int32_t n, int32_t W, int dtype, in
 
 namespace {
 
-constexpr int32_t kAbiVersion = 1;
+constexpr int32_t kAbiVersion = 2;
 
 bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
 
@@ -32,7 +32,9 @@ sla_status_t check_tensor_args(int64_t n, int32_t W, int dtype, int32_t heads, i
   if (head_dim != 16 && head_dim != 32) return SLA_E_UNSUPPORTED;
   if (W > sla::kMaxWindows) return SLA_E_UNSUPPORTED;
   if ((int64_t)heads * head_dim > (1 << 20)) return SLA_E_UNSUPPORTED;
-  if (n > 0 && (int64_t)n * heads * head_dim > ((int64_t)1 << 40)) return SLA_E_UNSUPPORTED;
+  // the kernels address rows with 32-bit byte offsets: every tensor < 4 GiB
+  const int64_t esize = dtype == 0 ? 4 : 2;
+  if (n > 0 && (int64_t)n * heads * head_dim * esize > (int64_t)UINT32_MAX) return SLA_E_UNSUPPORTED;
   if (plan == nullptr || !aligned(plan, 256)) return SLA_E_ARG;
   if (plan_bytes < sla::plan_layout(n, W).total) return SLA_E_WORKSPACE;
   return SLA_OK;
@@ -72,8 +74,10 @@ SLA_EXPORT sla_status_t sla_plan_layout(int64_t n, int32_t num_windows, sla_plan
   out->perm = L.perm;
   out->offsets = L.offsets;
   out->chunks = L.chunks;
+  out->longs = L.longs;
   out->total = L.total;
   out->max_chunks = L.max_chunks;
+  out->max_long = L.max_long;
   return SLA_OK;
 }
 

@@ -228,12 +228,27 @@ struct RowIO {
   }
 };
 
+// Row head `col` of row o of a [n, H, d] tensor: byte offsets fit in 32 bits (the
+// host checks that every tensor is smaller than 4 GiB), so the address is a
+// uniform base plus one 32-bit lane offset.
+template <typename T>
+__device__ __forceinline__ const T* row_at(const T* base, int32_t o, size_t rs, int col) {
+  const uint32_t off = ((uint32_t)o * (uint32_t)rs + (uint32_t)col) * (uint32_t)sizeof(T);
+  return reinterpret_cast<const T*>(reinterpret_cast<const char*>(base) + off);
+}
+template <typename T>
+__device__ __forceinline__ T* row_at(T* base, int32_t o, size_t rs, int col) {
+  const uint32_t off = ((uint32_t)o * (uint32_t)rs + (uint32_t)col) * (uint32_t)sizeof(T);
+  return reinterpret_cast<T*>(reinterpret_cast<char*>(base) + off);
+}
+
 struct KernelArgs {
   const PlanHeader* hdr;
   const int32_t* perm;
   const int32_t* offs;
   const Chunk* chunks;
-  int32_t max_chunks, n, W, H;
+  const LongWin* longs;
+  int32_t max_chunks, max_long, n, W, H;
 };
 
 // ------------------------------------------------------------------ jobs
@@ -486,7 +501,7 @@ __device__ __forceinline__ void apply_seg(const Slice<T, Geo<D>::KS, NM>& sb, in
 #pragma unroll
       for (int j = 0; j < 4; ++j) ox[4 * ct + j] = d4[j] * scale;
     }
-    RowIO<T, D>::put(o + (size_t)sb.o[s] * rs + col, g, F::from_f32(ox), in);
+    RowIO<T, D>::put(row_at(o, sb.o[s], rs, col), g, F::from_f32(ox), in);
   }
 }
 
@@ -649,7 +664,7 @@ __device__ __forceinline__ void qgrad_seg(const Slice<T, Geo<D>::KS, NM>& sb, in
         dqx[r] = (d4[j] - dot * op.z[r]) * rden * dphq[r];
       }
     }
-    RowIO<T, D>::put(dq + (size_t)sb.o[s] * rs + col, g, F::from_f32(dqx), in);
+    RowIO<T, D>::put(row_at(dq, sb.o[s], rs, col), g, F::from_f32(dqx), in);
     float xs[KS], ns[KS];
     const float w = op.bsig * rden;
 #pragma unroll
@@ -712,30 +727,130 @@ __device__ __forceinline__ void kgrad_seg(const Slice<T, Geo<D>::KS, NM>& sb, in
         dvx[r] = b4[j] * op.inv_scale;
       }
     }
-    RowIO<T, D>::put(dk + (size_t)sb.o[s] * rs + col, g, F::from_f32(dkx), in);
-    RowIO<T, D>::put(dv + (size_t)sb.o[s] * rs + col, g, F::from_f32(dvx), in);
+    RowIO<T, D>::put(row_at(dk, sb.o[s], rs, col), g, F::from_f32(dkx), in);
+    RowIO<T, D>::put(row_at(dv, sb.o[s], rs, col), g, F::from_f32(dvx), in);
   }
 }
 
 
-// ------------------------------------------------------------ job streams
-// A wave walks the windows of its chunk; each window is a run of 32-row jobs per
-// phase (forward: 0 = K,V state, 1 = Q apply; backward: 0 = K,V state,
-// 1 = Q,dout, 2 = K,V gradients).  Jobs are software-pipelined: while job t
-// computes, the rows of job t+1 and t+2 are in flight and the permutation
-// entries of job t+3 are being fetched.
-struct Job {
-  int32_t w;       // window (-1: stream finished)
-  int32_t ws, we;  // the window's rows, clipped to the chunk
-  int32_t r0;      // first row of this job
-  int32_t phase;
+// ------------------------------------------------------------- work items
+// A launch walks a list of work items; workgroup b takes items b, b + G, ...
+// (G = grid size, a multiple of 8, about the number of resident workgroups).
+// In order:
+//   long items   one per (long window, head): the four waves of the workgroup
+//                take a quarter of the window's rows each, add their partial
+//                states in LDS (in wave order, so every wave holds the same sum)
+//                and then form their rows' outputs.  Item numbers are laid out so
+//                that the heads of one window share an item residue mod 8, i.e.
+//                run on one XCD (workgroups are dealt to the 8 XCDs round-robin),
+//                where the L2 serves the other heads' halves of each row.
+//   chunk items  one per chunk and group of up to 4 heads (one wave per head;
+//                with fewer than 4 heads, several chunks share a workgroup).
+// Long items come first: they are the longest-running ones.
+//
+// Each wave software-pipelines its items: while item k computes, the plan entry
+// of item k + 2 and the permutation entries and window offsets of item k + 1 are
+// in flight, so an item's row gathers start as soon as the previous item's rows
+// have been requested and its data path is one memory round trip long.
+struct Items {
+  int32_t nL, nC, H, hw, cpw, hg;
+  int32_t itemsL, total;
 };
 
+__device__ __forceinline__ Items work_items(const KernelArgs& a, const PlanHeader* hdr) {
+  Items it;
+  it.nL = max(0, min(hdr->n_long, a.max_long));
+  it.nC = max(0, min(hdr->n_chunks, a.max_chunks));
+  it.H = a.H;
+  it.hw = min(a.H, 4);
+  it.cpw = 4 / it.hw;
+  it.hg = (a.H + 3) / 4;
+  it.itemsL = ((it.nL + 7) & ~7) * a.H;
+  it.total = it.itemsL + (it.nC + it.cpw - 1) / it.cpw * it.hg;
+  return it;
+}
+
+struct WaveWork {
+  int kind;        // 0: nothing, 1: a chunk, 2: a quarter of a long window
+  int h;           // head
+  int32_t ra, rb;  // rows (sorted positions)
+  int32_t wb, we;  // windows
+};
+
+// Where item `item` puts wave wv (wave-uniform): table entry index (-1: none),
+// the table (0: long windows, 1: chunks) and the head.
+struct Slot {
+  int32_t idx;
+  int table, h;
+};
+
+__device__ __forceinline__ Slot item_slot(const Items& it, int32_t item, int wv) {
+  Slot sl;
+  sl.idx = -1;
+  sl.table = 0;
+  sl.h = 0;
+  if (item >= it.total) return sl;
+  if (item < it.itemsL) {
+    const int32_t r = item >> 3;
+    const int32_t j = (r / it.H) * 8 + (item & 7);
+    sl.h = r % it.H;
+    if (j < it.nL) sl.idx = j;
+  } else {
+    const int32_t b = item - it.itemsL;
+    const int32_t grp = b / it.hg;
+    const int sub = wv / it.hw;
+    const int32_t c = grp * it.cpw + sub;
+    sl.table = 1;
+    sl.h = (b - grp * it.hg) * 4 + wv % it.hw;
+    if (sub < it.cpw && c < it.nC && sl.h < it.H) sl.idx = c;
+  }
+  return sl;
+}
+
+// The plan entry of a slot (4 ints; Chunk and LongWin have the same size).
+__device__ __forceinline__ int4 slot_entry(const KernelArgs& a, const Slot& sl) {
+  if (sl.idx < 0) return make_int4(0, 0, 0, 0);
+  if (sl.table == 0) return reinterpret_cast<const int4*>(a.longs)[sl.idx];
+  return reinterpret_cast<const int4*>(a.chunks)[sl.idx];
+}
+
+__device__ __forceinline__ WaveWork decode_work(const KernelArgs& a, const Slot& sl, int4 e,
+                                                int wv) {
+  WaveWork ww;
+  ww.kind = 0;
+  ww.h = sl.h;
+  ww.ra = ww.rb = ww.wb = ww.we = 0;
+  if (sl.idx < 0) return ww;
+  if (sl.table == 0) {  // LongWin: window, row_begin, row_end
+    const int32_t rs = max(0, min(e.y, a.n));
+    const int32_t re = max(rs, min(e.z, a.n));
+    const int64_t len = re - rs;
+    ww.ra = rs + (int32_t)((len * wv) >> 2);
+    ww.rb = rs + (int32_t)((len * (wv + 1)) >> 2);
+    ww.wb = e.x;
+    ww.we = e.x + 1;
+    ww.kind = 2;
+  } else {  // Chunk: row_begin, row_end, win_begin, win_end
+    ww.ra = max(0, min(e.x, a.n));
+    ww.rb = max(ww.ra, min(min(e.y, a.n), ww.ra + kMaxChunkRows));
+    ww.we = max(0, min(e.w, a.W));
+    ww.wb = max(0, min(e.z, ww.we));
+    ww.kind = 1;
+  }
+  return ww;
+}
+
+// ---------------------------------------------------------- windows of a chunk
 // The windows of a chunk, 64 at a time in registers: lane l holds the rows of
 // window wp + l clipped to the chunk, and a ballot marks the non-empty ones, so
-// that moving to the next window is a few scalar instructions, not a chain of
-// dependent loads of the offsets (chunks of small windows also hold many empty
-// ones).
+// that moving to the next window is a few scalar instructions (chunks of small
+// windows may also hold many empty ones).  request() issues the loads of a page,
+// settle() takes the ballot (so a page can be requested ahead of its use).
+struct WinCursor {
+  int32_t w;       // current window (-1: finished)
+  int32_t ws, we;  // its rows, clipped to the chunk
+};
+
 struct Stream {
   const int32_t* offs;
   int32_t rb, re, wend;
@@ -743,7 +858,7 @@ struct Stream {
   int32_t a, b;    // rows of window wp + lane, clipped to [rb, re)
   uint64_t live;   // lanes whose window is non-empty
   int lane;
-  __device__ __forceinline__ void load_page(int32_t w0) {
+  __device__ __forceinline__ void request(int32_t w0) {
     wp = w0;
     const int32_t w = wp + lane;
     a = b = 0;
@@ -751,9 +866,9 @@ struct Stream {
       a = max(offs[w], rb);
       b = min(offs[w + 1], re);
     }
-    live = __ballot(a < b);
   }
-  __device__ __forceinline__ bool next_window(Job& j) {
+  __device__ __forceinline__ void settle() { live = __ballot(a < b); }
+  __device__ __forceinline__ bool next_window(WinCursor& j) {
     for (;;) {
       const int sh = j.w + 1 - wp;   // first lane after the current window
       const uint64_t m = sh <= 0 ? live : (sh >= 64 ? 0ull : live & (~0ull << sh));
@@ -765,281 +880,429 @@ struct Stream {
         return true;
       }
       if (wp + 64 >= wend) break;
-      load_page(wp + 64);
+      request(wp + 64);
+      settle();
     }
     j.w = -1;
     return false;
   }
-  __device__ __forceinline__ Job first(int32_t wb) {
-    load_page(wb);
-    Job j;
-    j.w = wb - 1;
-    j.phase = 0;
-    j.ws = j.we = j.r0 = 0;
-    if (next_window(j)) j.r0 = j.ws;
-    return j;
-  }
-  template <int NPH>
-  __device__ __forceinline__ Job next(Job j) {
-    if (j.w < 0) return j;
-    j.r0 += kSliceRows;
-    if (j.r0 < j.we) return j;
-    if (++j.phase < NPH) {
-      j.r0 = j.ws;
-      return j;
-    }
-    j.phase = 0;
-    if (next_window(j)) j.r0 = j.ws;
-    return j;
-  }
 };
 
-template <typename T, int D>
-using JobBuf = Slice<T, Geo<D>::KS, 2>;
+// ------------------------------------------------------------- row blocks
+// Up to kBlockJobs 32-row jobs of one head held in registers: NM matrices as row
+// fragments (forward: K, V, Q; backward: K, V, Q, dout).
+constexpr int kBlockJobs = kMaxChunkRows / kSliceRows;
+constexpr int kBlockRows = kBlockJobs * kSliceRows;
 
-// A page of the chunk's permutation, held by the wave: register m of lane l is
-// the original row of sorted row pb + 64 m + l.  Jobs take their rows from the
-// page with lane permutes; a job outside the page (windows longer than it)
-// first reloads the page at its own first row.  The reload waits for its loads
-// inside its own branch, so the common path never waits on the permutation and
-// the prefetched rows stay in flight.
-#ifndef SLA_PERM_REGS
-#define SLA_PERM_REGS 4
-#endif
-constexpr int kPermRegs = SLA_PERM_REGS;
-
-struct PermRegs {
-  const int32_t* perm;  // null: identity (rows already window-sorted)
-  int32_t re;           // end of the chunk's rows
-  int32_t pb;           // first sorted row of the page
-  int32_t r[kPermRegs];
-  __device__ __forceinline__ void load(int32_t pb_, int lane) {
-    pb = pb_;
-    int32_t x[kPermRegs];
-#pragma unroll
-    for (int m = 0; m < kPermRegs; ++m) {
-      const int32_t row = pb + 64 * m + lane;
-      x[m] = perm ? perm[row < re ? row : pb] : row;
-    }
-#pragma unroll
-    for (int m = 0; m < kPermRegs; ++m) {
-      asm volatile("" : "+v"(x[m]));  // consumed here: the wait stays in this branch
-      r[m] = x[m];
-    }
-  }
+template <typename T, int D, int NM>
+struct Block {
+  Slice<T, Geo<D>::KS, NM> j[kBlockJobs];
 };
 
-// Original rows of a job's two sub-tiles (o = 0 and ok = false past the job).
-__device__ __forceinline__ void job_rows(const Job& j, PermRegs& pr, int lane, int32_t (&o)[2],
-                                         bool (&ok)[2]) {
-  if (j.w >= 0 && (j.r0 < pr.pb || j.r0 + kSliceRows > pr.pb + 64 * kPermRegs)) pr.load(j.r0, lane);
+// Original rows of sorted rows [base, min(end, base + kBlockRows)): lane (i, g)
+// of sub-tile s of job jj takes row base + 32 jj + 16 s + i (-1: none).
+struct BlockRows {
+  int32_t o[kBlockJobs][2];
+};
+
+__device__ __forceinline__ void block_rows(BlockRows& br, int32_t base, int32_t end,
+                                           const int32_t* perm, int lane) {
   const int i = lane & 15;
 #pragma unroll
-  for (int s = 0; s < 2; ++s) {
-    const int32_t row = j.r0 + 16 * s + i;
-    const int32_t rel = row - pr.pb;
-    int32_t x = 0;
+  for (int jj = 0; jj < kBlockJobs; ++jj)
 #pragma unroll
-    for (int m = 0; m < kPermRegs; ++m) {
-      const int32_t t = __builtin_amdgcn_ds_bpermute((rel & 63) << 2, pr.r[m]);
-      if ((rel >> 6) == m) x = t;
+    for (int s = 0; s < 2; ++s) {
+      const int32_t row = base + kSliceRows * jj + 16 * s + i;
+      br.o[jj][s] = row < end ? (perm ? perm[row] : row) : -1;
     }
-    ok[s] = j.w >= 0 && row < j.we;
-    o[s] = ok[s] ? x : 0;
-  }
 }
 
-// Rows of a job -> the job's two matrices (a, b; b null: the second fragment is
-// left as it is, the job's math does not read it).  Rows past the job read row
-// 0 (the math masks them; n >= 1 whenever a kernel runs).
-template <typename T, int D>
-__device__ __forceinline__ void job_load(JobBuf<T, D>& jb, const int32_t (&o)[2],
-                                         const bool (&ok)[2], const T* a, const T* b, int32_t n,
-                                         size_t rs, int col, int g) {
+// The matrices selected by `which` (bit m: mats[m]) of the block's rows into slot
+// order.  Sub-tiles past `end` are not read (and are zero); rows past `end`
+// inside a read sub-tile read row 0, which the math masks.
+template <typename T, int D, int NM>
+__device__ __forceinline__ void block_fetch(Block<T, D, NM>& bk, const BlockRows& br, int32_t base,
+                                            int32_t end, int32_t n, const T* const (&mats)[NM],
+                                            unsigned which, size_t rs, int col, int g) {
+  using F = Frag<T, Geo<D>::KS>;
 #pragma unroll
-  for (int s = 0; s < 2; ++s) {
-    jb.ok[s] = ok[s] && (uint32_t)o[s] < (uint32_t)n;
-    jb.o[s] = jb.ok[s] ? o[s] : 0;
-    jb.x[0][s] = RowIO<T, D>::fetch(a + (size_t)jb.o[s] * rs + col, g);
-    if (b) jb.x[1][s] = RowIO<T, D>::fetch(b + (size_t)jb.o[s] * rs + col, g);
-  }
-}
-
-// Slot order for the rows of the job about to be computed.
-template <typename T, int D>
-__device__ __forceinline__ void job_arrange(JobBuf<T, D>& jb) {
+  for (int jj = 0; jj < kBlockJobs; ++jj)
 #pragma unroll
-  for (int s = 0; s < 2; ++s) {
-    RowIO<T, D>::arrange(jb.x[0][s]);
-    RowIO<T, D>::arrange(jb.x[1][s]);
+    for (int s = 0; s < 2; ++s) {
+      const bool ok = (uint32_t)br.o[jj][s] < (uint32_t)n;
+      bk.j[jj].ok[s] = ok;
+      bk.j[jj].o[s] = ok ? br.o[jj][s] : 0;
+      const bool live = base + kSliceRows * jj + 16 * s < end;
+#pragma unroll
+      for (int m = 0; m < NM; ++m) {
+        if (!(which & (1u << m))) continue;
+        if (live) bk.j[jj].x[m][s] = RowIO<T, D>::fetch(row_at(mats[m], bk.j[jj].o[s], rs, col), g);
+        else bk.j[jj].x[m][s] = F::zero();
+      }
+    }
+}
+
+template <typename T, int D, int NM>
+__device__ __forceinline__ void block_arrange(Block<T, D, NM>& bk, unsigned which) {
+#pragma unroll
+  for (int jj = 0; jj < kBlockJobs; ++jj)
+#pragma unroll
+    for (int s = 0; s < 2; ++s)
+#pragma unroll
+      for (int m = 0; m < NM; ++m)
+        if (which & (1u << m)) RowIO<T, D>::arrange(bk.j[jj].x[m][s]);
+}
+
+__device__ __forceinline__ bool job_overlaps(int32_t r0, int32_t a, int32_t b) {
+  return r0 < b && r0 + kSliceRows > a;
+}
+
+// An item of this wave whose row permutation and windows have been requested.
+struct Pending {
+  WaveWork ww;
+  BlockRows br;
+  Stream str;
+};
+
+__device__ __forceinline__ void pending_request(Pending& p, const KernelArgs& a, const Slot& sl,
+                                                int4 e, int wv, const int32_t* perm, int lane) {
+  p.ww = decode_work(a, sl, e, wv);
+  p.str.lane = lane;
+  p.str.offs = a.offs;
+  p.str.rb = p.ww.ra;
+  p.str.re = p.ww.rb;
+  p.str.wend = p.ww.we;
+  p.str.wp = p.ww.wb;
+  p.str.a = p.str.b = 0;
+  p.str.live = 0;
+  if (p.ww.kind != 0) block_rows(p.br, p.ww.ra, min(p.ww.rb, p.ww.ra + kBlockRows), perm, lane);
+  if (p.ww.kind == 1) p.str.request(p.ww.wb);
+}
+
+// Block until every wave of the workgroup gets here, with this wave's LDS writes
+// done (LDS only: loads in flight stay in flight).
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+// ------------------------------------------------------ partial-state exchange
+// A state as result tiles in LDS, one floatx4 per (tile, lane), so that waves of
+// a workgroup can add their partial states.
+template <int D>
+constexpr int kStateTiles = Geo<D>::NT * Geo<D>::NT + Geo<D>::NT;
+
+template <int D>
+__device__ __forceinline__ void publish(const State<D>& st, floatx4* slot, int lane) {
+  constexpr int NT = Geo<D>::NT;
+  int t = 0;
+#pragma unroll
+  for (int a = 0; a < NT; ++a)
+#pragma unroll
+    for (int b = 0; b < NT; ++b) slot[(t++) * 64 + lane] = st.M[a][b];
+#pragma unroll
+  for (int a = 0; a < NT; ++a) slot[(t++) * 64 + lane] = st.V[a];
+}
+
+// st = sum of the kWaves published states, in wave order.
+template <int D>
+__device__ __forceinline__ void combine(State<D>& st, const floatx4* slots, int lane) {
+  constexpr int NT = Geo<D>::NT, KT = kStateTiles<D>;
+  st.clear();
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) {
+    const floatx4* sl = slots + w * KT * 64;
+    int t = 0;
+#pragma unroll
+    for (int a = 0; a < NT; ++a)
+#pragma unroll
+      for (int b = 0; b < NT; ++b) st.M[a][b] += sl[(t++) * 64 + lane];
+#pragma unroll
+    for (int a = 0; a < NT; ++a) st.V[a] += sl[(t++) * 64 + lane];
   }
 }
 
-template <typename T, int D>
-__device__ __forceinline__ Stream chunk_stream(const KernelArgs& a, int32_t c, int32_t& wb,
-                                               int lane) {
-  const Chunk ch = a.chunks[c];
-  Stream st;
-  st.lane = lane;
-  st.offs = a.offs;
-  st.rb = max(0, min(ch.row_begin, a.n));
-  st.re = max(st.rb, min(ch.row_end, a.n));
-  st.wend = max(0, min(ch.win_end, a.W));
-  wb = max(0, min(ch.win_begin, st.wend));
-  return st;
-}
+// The windows an item gives a wave: the windows of a chunk (each one whole), or
+// one quarter of a long window (shared: its partial state is added to the other
+// three quarters' before use).
+struct WinIter {
+  WinCursor wc;
+  bool shared;
+  __device__ __forceinline__ bool first(const WaveWork& ww, Stream& str) {
+    shared = ww.kind == 2;
+    wc.w = ww.wb - 1;
+    if (ww.kind == 1) {
+      str.settle();
+      return str.next_window(wc);
+    }
+    wc.ws = ww.ra;
+    wc.we = ww.rb;
+    return ww.kind == 2;
+  }
+  __device__ __forceinline__ bool next(const WaveWork& ww, Stream& str) {
+    return ww.kind == 1 && str.next_window(wc);
+  }
+};
 
 // ------------------------------------------------------------------ forward
 template <typename T, int D>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(kWpe<T, SLA_FWD_WPE>)))
 void k_sla_fwd(KernelArgs a, const T* __restrict__ q, const T* __restrict__ k,
                const T* __restrict__ v, T* __restrict__ o) {
-  const int lane = lane_id(), wv = threadIdx.x >> 6;
-  const int h = blockIdx.y * kWaves + wv;
-  if (h >= a.H) return;
+  constexpr int KT = kStateTiles<D>;
+  __shared__ floatx4 s_part[kWaves * KT * 64];  // partial states of a long window
+  const int lane = lane_id();
+  const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const PlanHeader* hdr = a.hdr;
   if (hdr->magic != kPlanMagic || hdr->n != a.n || hdr->num_windows != a.W) return;
-  const int32_t c = blockIdx.x;
-  if (c >= min(hdr->n_chunks, a.max_chunks)) return;
+  const Items it = work_items(a, hdr);
   const int32_t* perm = hdr->csr ? nullptr : a.perm;
   const int i = lane & 15, g = lane >> 4;
   const size_t rs = (size_t)a.H * D;
-  const int col = h * D;
-  const int32_t n = a.n;
+  const int32_t n = a.n, G = gridDim.x;
   const Sel<T, D> sel(i, g);
-  int32_t wb;
-  Stream str = chunk_stream<T, D>(a, c, wb, lane);
-  PermRegs pr;
-  pr.perm = perm;
-  pr.re = str.re;
-  pr.load(str.rb, lane);
-  auto load_job = [&](JobBuf<T, D>& jb, const Job& j) {
-    int32_t o[2];
-    bool ok[2];
-    job_rows(j, pr, lane, o, ok);
-    job_load<T, D>(jb, o, ok, j.phase == 0 ? k : q, j.phase == 0 ? v : (const T*)nullptr, n, rs,
-                   col, g);
-  };
+  const T* const mats[3] = {k, v, q};
+  constexpr unsigned kKV = 3u, kQ = 4u, kAll = 7u;
 
-  // Three buffers used in turn (the loop is unrolled by three so that rows in
-  // flight are never copied between registers, which would wait for them).
-  Job j0 = str.first(wb);
-  Job j1 = str.next<2>(j0);
-  Job j2 = str.next<2>(j1);
-  JobBuf<T, D> b0, b1, b2;
-  load_job(b0, j0);
-  load_job(b1, j1);
-  State<D> st;
-  FwdOp<T, D> op;
-  auto step = [&](JobBuf<T, D>& cur, JobBuf<T, D>& nxt) {
-    load_job(nxt, j2);
-    job_arrange<T, D>(cur);
-    if (j0.phase == 0) {
-      if (j0.r0 == j0.ws) st.clear();
-      state_seg<T, D, 2>(cur, j0.r0, j0.ws, j0.we, i, g, sel, st);
-      if (j0.r0 + kSliceRows >= j0.we) make_fwd_op<T, D>(st, op, i);
-    } else {
-      apply_seg<T, D, 2, 0>(cur, j0.r0, j0.ws, j0.we, i, g, op, o, rs, col);
+  int32_t item = blockIdx.x;
+  Pending cur;
+  {
+    const Slot sl = item_slot(it, item, wv);
+    pending_request(cur, a, sl, slot_entry(a, sl), wv, perm, lane);
+  }
+  Slot nsl = item_slot(it, item + G, wv);
+  int4 ne = slot_entry(a, nsl);
+  while (item < it.total) {
+    const WaveWork ww = cur.ww;
+    const int col = ww.h * D;
+    // a range of more than kBlockRows rows (a quarter of a very long window) is
+    // streamed through the block: K, V for the state, then Q for the outputs
+    const bool resident = ww.rb - ww.ra <= kBlockRows;
+    const unsigned first = resident ? kAll : kKV;
+    Block<T, D, 3> bk;
+    if (ww.kind != 0) block_fetch<T, D, 3>(bk, cur.br, ww.ra, ww.rb, n, mats, first, rs, col, g);
+    // the next item: its rows and windows are requested now, its successor's entry too
+    Pending nxt;
+    pending_request(nxt, a, nsl, ne, wv, perm, lane);
+    nsl = item_slot(it, item + 2 * G, wv);
+    ne = slot_entry(a, nsl);
+
+    block_arrange<T, D, 3>(bk, first);
+    WinIter wi;
+    for (bool more = wi.first(ww, cur.str); more; more = wi.next(ww, cur.str)) {
+      const int32_t wa = wi.wc.ws, wb = wi.wc.we;
+      State<D> st;
+      st.clear();
+      for (int32_t base = ww.ra; base < ww.rb; base += kBlockRows) {
+        if (base != ww.ra) {
+          BlockRows br;
+          block_rows(br, base, ww.rb, perm, lane);
+          block_fetch<T, D, 3>(bk, br, base, ww.rb, n, mats, kKV, rs, col, g);
+          block_arrange<T, D, 3>(bk, kKV);
+        }
+#pragma unroll
+        for (int jj = 0; jj < kBlockJobs; ++jj) {
+          const int32_t r0 = base + kSliceRows * jj;
+          if (job_overlaps(r0, wa, wb)) state_seg<T, D, 3>(bk.j[jj], r0, wa, wb, i, g, sel, st);
+        }
+      }
+      if (wi.shared) {
+        publish<D>(st, s_part + wv * KT * 64, lane);
+        lds_barrier();
+        combine<D>(st, s_part, lane);
+        lds_barrier();  // the slots may be written by the next long item
+      }
+      FwdOp<T, D> op;
+      make_fwd_op<T, D>(st, op, i);
+      for (int32_t base = ww.ra; base < ww.rb; base += kBlockRows) {
+        if (!resident) {
+          BlockRows br;
+          block_rows(br, base, ww.rb, perm, lane);
+          block_fetch<T, D, 3>(bk, br, base, ww.rb, n, mats, kQ, rs, col, g);
+          block_arrange<T, D, 3>(bk, kQ);
+        }
+#pragma unroll
+        for (int jj = 0; jj < kBlockJobs; ++jj) {
+          const int32_t r0 = base + kSliceRows * jj;
+          if (job_overlaps(r0, wa, wb)) apply_seg<T, D, 3, 2>(bk.j[jj], r0, wa, wb, i, g, op, o, rs, col);
+        }
+      }
     }
-    j0 = j1;
-    j1 = j2;
-    j2 = str.next<2>(j2);
-  };
-  for (;;) {
-    if (j0.w < 0) break;
-    step(b0, b2);
-    if (j0.w < 0) break;
-    step(b1, b0);
-    if (j0.w < 0) break;
-    step(b2, b1);
+    item += G;
+    cur = nxt;
   }
 }
 
 // ----------------------------------------------------------------- backward
+// Per window: state S, z from K, V; then dq and the state gradients from Q, dout;
+// then dk, dv from K, V (held in registers since the first phase).
 template <typename T, int D>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(kWpe<T, SLA_BWD_WPE>)))
 void k_sla_bwd(KernelArgs a, const T* __restrict__ q, const T* __restrict__ k,
                const T* __restrict__ v, const T* __restrict__ dout, T* __restrict__ dq,
                T* __restrict__ dk, T* __restrict__ dv) {
-  const int lane = lane_id(), wv = threadIdx.x >> 6;
-  const int h = blockIdx.y * kWaves + wv;
-  if (h >= a.H) return;
+  constexpr int KT = kStateTiles<D>;
+  __shared__ floatx4 s_part[2][kWaves * KT * 64];  // partial S, z / dS, dz of a long window
+  __shared__ float s_tr[kWaves][D * kTrLd<D>];     // transposes, one tile per wave
+  const int lane = lane_id();
+  const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const PlanHeader* hdr = a.hdr;
   if (hdr->magic != kPlanMagic || hdr->n != a.n || hdr->num_windows != a.W) return;
-  const int32_t c = blockIdx.x;
-  if (c >= min(hdr->n_chunks, a.max_chunks)) return;
+  const Items it = work_items(a, hdr);
   const int32_t* perm = hdr->csr ? nullptr : a.perm;
   const int i = lane & 15, g = lane >> 4;
   const size_t rs = (size_t)a.H * D;
-  const int col = h * D;
-  const int32_t n = a.n;
+  const int32_t n = a.n, G = gridDim.x;
   const Sel<T, D> sel(i, g);
-  int32_t wb;
-  Stream str = chunk_stream<T, D>(a, c, wb, lane);
-  PermRegs pr;
-  pr.perm = perm;
-  pr.re = str.re;
-  pr.load(str.rb, lane);
-  auto load_job = [&](JobBuf<T, D>& jb, const Job& j) {
-    int32_t o[2];
-    bool ok[2];
-    job_rows(j, pr, lane, o, ok);
-    job_load<T, D>(jb, o, ok, j.phase == 1 ? q : k, j.phase == 1 ? dout : v, n, rs, col, g);
-  };
-
-  Job j0 = str.first(wb);
-  Job j1 = str.next<3>(j0);
-  Job j2 = str.next<3>(j1);
-  JobBuf<T, D> b0, b1, b2;
-  load_job(b0, j0);
-  load_job(b1, j1);
-  State<D> st;  // phase 0: S, z ; phase 1: beta dS, beta dz
-  __shared__ float s_tr[kWaves][D * kTrLd<D>];  // transposes, one tile per wave
   float* tile = s_tr[wv];
-  BwdOp<T, D> op;
-  auto step = [&](JobBuf<T, D>& cur, JobBuf<T, D>& nxt) {
-    load_job(nxt, j2);
-    job_arrange<T, D>(cur);
-    const bool first = j0.r0 == j0.ws, last = j0.r0 + kSliceRows >= j0.we;
-    if (j0.phase == 0) {
-      if (first) st.clear();
-      state_seg<T, D, 2>(cur, j0.r0, j0.ws, j0.we, i, g, sel, st);
-      if (last) make_state_op<T, D>(st, op, tile, i, g);
-    } else if (j0.phase == 1) {
-      if (first) st.clear();
-      qgrad_seg<T, D, 2, 0, 1>(cur, j0.r0, j0.ws, j0.we, i, g, sel, op, dq, rs, col, st);
-      if (last) make_grad_op<T, D>(st, op.inv_beta, op, tile, i, g);
-    } else {
-      kgrad_seg<T, D, 2>(cur, j0.r0, j0.ws, j0.we, i, g, op, dk, dv, rs, col);
+  const T* const mats[4] = {k, v, q, dout};
+  constexpr unsigned kKV = 3u, kQD = 12u, kAll = 15u;
+
+  int32_t item = blockIdx.x;
+  Pending cur;
+  {
+    const Slot sl = item_slot(it, item, wv);
+    pending_request(cur, a, sl, slot_entry(a, sl), wv, perm, lane);
+  }
+  Slot nsl = item_slot(it, item + G, wv);
+  int4 ne = slot_entry(a, nsl);
+  while (item < it.total) {
+    const WaveWork ww = cur.ww;
+    const int col = ww.h * D;
+    const bool resident = ww.rb - ww.ra <= kBlockRows;
+    const unsigned first = resident ? kAll : kKV;
+    Block<T, D, 4> bk;
+    if (ww.kind != 0) block_fetch<T, D, 4>(bk, cur.br, ww.ra, ww.rb, n, mats, first, rs, col, g);
+    Pending nxt;
+    pending_request(nxt, a, nsl, ne, wv, perm, lane);
+    nsl = item_slot(it, item + 2 * G, wv);
+    ne = slot_entry(a, nsl);
+
+    block_arrange<T, D, 4>(bk, first);
+    WinIter wi;
+    for (bool more = wi.first(ww, cur.str); more; more = wi.next(ww, cur.str)) {
+      const int32_t wa = wi.wc.ws, wb = wi.wc.we;
+      State<D> st;  // S, z ; then beta dS, beta dz
+      BwdOp<T, D> op;
+      // phase 0: S, z
+      st.clear();
+      for (int32_t base = ww.ra; base < ww.rb; base += kBlockRows) {
+        if (base != ww.ra) {
+          BlockRows br;
+          block_rows(br, base, ww.rb, perm, lane);
+          block_fetch<T, D, 4>(bk, br, base, ww.rb, n, mats, kKV, rs, col, g);
+          block_arrange<T, D, 4>(bk, kKV);
+        }
+#pragma unroll
+        for (int jj = 0; jj < kBlockJobs; ++jj) {
+          const int32_t r0 = base + kSliceRows * jj;
+          if (job_overlaps(r0, wa, wb)) state_seg<T, D, 4>(bk.j[jj], r0, wa, wb, i, g, sel, st);
+        }
+      }
+      if (wi.shared) {
+        publish<D>(st, s_part[0] + wv * KT * 64, lane);
+        lds_barrier();
+        combine<D>(st, s_part[0], lane);
+      }
+      make_state_op<T, D>(st, op, tile, i, g);
+      // phase 1: dq and beta dS, beta dz
+      st.clear();
+      for (int32_t base = ww.ra; base < ww.rb; base += kBlockRows) {
+        if (!resident) {
+          BlockRows br;
+          block_rows(br, base, ww.rb, perm, lane);
+          block_fetch<T, D, 4>(bk, br, base, ww.rb, n, mats, kQD, rs, col, g);
+          block_arrange<T, D, 4>(bk, kQD);
+        }
+#pragma unroll
+        for (int jj = 0; jj < kBlockJobs; ++jj) {
+          const int32_t r0 = base + kSliceRows * jj;
+          if (job_overlaps(r0, wa, wb))
+            qgrad_seg<T, D, 4, 2, 3>(bk.j[jj], r0, wa, wb, i, g, sel, op, dq, rs, col, st);
+        }
+      }
+      if (wi.shared) {
+        // slot set 1 is free: its last readers passed the barrier above before
+        // this item's set-0 reads ended (sets alternate within every long item)
+        publish<D>(st, s_part[1] + wv * KT * 64, lane);
+        lds_barrier();
+        combine<D>(st, s_part[1], lane);
+      }
+      make_grad_op<T, D>(st, op.inv_beta, op, tile, i, g);
+      // phase 2: dk, dv
+      for (int32_t base = ww.ra; base < ww.rb; base += kBlockRows) {
+        if (!resident) {
+          BlockRows br;
+          block_rows(br, base, ww.rb, perm, lane);
+          block_fetch<T, D, 4>(bk, br, base, ww.rb, n, mats, kKV, rs, col, g);
+          block_arrange<T, D, 4>(bk, kKV);
+        }
+#pragma unroll
+        for (int jj = 0; jj < kBlockJobs; ++jj) {
+          const int32_t r0 = base + kSliceRows * jj;
+          if (job_overlaps(r0, wa, wb)) kgrad_seg<T, D, 4>(bk.j[jj], r0, wa, wb, i, g, op, dk, dv, rs, col);
+        }
+      }
     }
-    j0 = j1;
-    j1 = j2;
-    j2 = str.next<3>(j2);
-  };
-  for (;;) {
-    if (j0.w < 0) break;
-    step(b0, b2);
-    if (j0.w < 0) break;
-    step(b1, b0);
-    if (j0.w < 0) break;
-    step(b2, b1);
+    item += G;
+    cur = nxt;
   }
 }
 
 // ------------------------------------------------------------ host launchers
-static inline int grid_x(int32_t max_chunks) {
-  return max_chunks < 1 ? 1 : max_chunks;
+// Workgroups of a launch: the resident capacity of the device for the kernel
+// (workgroups per CU x CUs, queried once per device and kernel), at most enough
+// for every item the plan can hold (long windows have more than kMinChunkRows
+// rows), a multiple of 8.
+static int resident_workgroups(const void* kernel) {
+  struct Entry {
+    const void* kernel;
+    int dev, cap;
+  };
+  static Entry cache[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) dev = 0;
+  for (const Entry& e : cache)
+    if (e.kernel == kernel && e.dev == dev) return e.cap;
+  int per_cu = 0, cus = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, 64 * kWaves, 0) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      per_cu < 1 || cus < 1) {
+    per_cu = 2;
+    cus = 256;
+  }
+  for (Entry& e : cache)
+    if (e.kernel == nullptr) {
+      e = Entry{kernel, dev, per_cu * cus};
+      break;
+    }
+  return per_cu * cus;
 }
 
-static KernelArgs kernel_args(const void* plan, int32_t n, int32_t W, int32_t H) {
-  const PlanLayout lay = plan_layout(n, W);
+// Workgroups of a launch: the resident capacity of the device for the kernel,
+// at most enough for every item the plan can hold (long windows have more than
+// kMinChunkRows rows), a multiple of 8.
+static int grid_size(const void* kernel, const PlanLayout& lay, int32_t H) {
+  const int c = resident_workgroups(kernel);
+  const int hw = H < 4 ? H : 4, cpw = 4 / hw, hg = (H + 3) / 4;
+  const int64_t itemsL = (int64_t)((lay.max_long + 7) & ~7) * H;
+  const int64_t itemsC = (int64_t)(lay.max_chunks + cpw - 1) / cpw * hg;
+  int64_t g = itemsL + itemsC;
+  if (g > c) g = c;
+  g = (g + 7) & ~7;
+  return (int)(g < 8 ? 8 : g);
+}
+
+static KernelArgs kernel_args(const void* plan, const PlanLayout& lay, int32_t n, int32_t W,
+                              int32_t H) {
   const char* base = static_cast<const char*>(plan);
   KernelArgs a;
   a.hdr = reinterpret_cast<const PlanHeader*>(base + lay.header);
   a.perm = reinterpret_cast<const int32_t*>(base + lay.perm);
   a.offs = reinterpret_cast<const int32_t*>(base + lay.offsets);
   a.chunks = reinterpret_cast<const Chunk*>(base + lay.chunks);
+  a.longs = reinterpret_cast<const LongWin*>(base + lay.longs);
   a.max_chunks = lay.max_chunks;
+  a.max_long = lay.max_long;
   a.n = n;
   a.W = W;
   a.H = H;
@@ -1049,11 +1312,11 @@ static KernelArgs kernel_args(const void* plan, int32_t n, int32_t W, int32_t H)
 template <typename T, int D>
 static hipError_t fwd_impl(const void* plan, int32_t n, int32_t W, int32_t H, const void* q,
                            const void* k, const void* v, void* o, hipStream_t stream) {
-  const KernelArgs a = kernel_args(plan, n, W, H);
-  const int waves = H < kWaves ? H : kWaves;
-  hipLaunchKernelGGL((k_sla_fwd<T, D>), dim3(grid_x(a.max_chunks), (H + kWaves - 1) / kWaves),
-                     dim3(64 * waves), 0, stream, a, static_cast<const T*>(q),
-                     static_cast<const T*>(k), static_cast<const T*>(v), static_cast<T*>(o));
+  const PlanLayout lay = plan_layout(n, W);
+  const KernelArgs a = kernel_args(plan, lay, n, W, H);
+  hipLaunchKernelGGL((k_sla_fwd<T, D>), dim3(grid_size(reinterpret_cast<const void*>(&k_sla_fwd<T, D>), lay, H)), dim3(64 * kWaves), 0, stream, a,
+                     static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v),
+                     static_cast<T*>(o));
   return hipGetLastError();
 }
 
@@ -1061,11 +1324,10 @@ template <typename T, int D>
 static hipError_t bwd_impl(const void* plan, int32_t n, int32_t W, int32_t H, const void* q,
                            const void* k, const void* v, const void* dout, void* dq, void* dk,
                            void* dv, hipStream_t stream) {
-  const KernelArgs a = kernel_args(plan, n, W, H);
-  const int waves = H < kWaves ? H : kWaves;
-  hipLaunchKernelGGL((k_sla_bwd<T, D>), dim3(grid_x(a.max_chunks), (H + kWaves - 1) / kWaves),
-                     dim3(64 * waves), 0, stream, a, static_cast<const T*>(q),
-                     static_cast<const T*>(k), static_cast<const T*>(v),
+  const PlanLayout lay = plan_layout(n, W);
+  const KernelArgs a = kernel_args(plan, lay, n, W, H);
+  hipLaunchKernelGGL((k_sla_bwd<T, D>), dim3(grid_size(reinterpret_cast<const void*>(&k_sla_bwd<T, D>), lay, H)), dim3(64 * kWaves), 0, stream, a,
+                     static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v),
                      static_cast<const T*>(dout), static_cast<T*>(dq), static_cast<T*>(dk),
                      static_cast<T*>(dv));
   return hipGetLastError();

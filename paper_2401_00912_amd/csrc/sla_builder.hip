@@ -84,67 +84,104 @@ __device__ V block_exscan(V x, V identity, Op op, V* s, V* total) {
   return r;
 }
 
-// ------------------------------------------------------------- chunk table
-// Chunk table from the offsets in LDS (page rule, pages of L/2 rows), in
-// sequence order.  s_aux: LDS scratch of at least W ints.  Every thread of the
-// block calls it; returns the number of chunks.
-__device__ int32_t build_chunks(const int32_t* s_off, int32_t* s_aux, int32_t W, int32_t L,
-                                Chunk* __restrict__ chunks, int32_t* s_scan) {
+// ------------------------------------------------------ chunk / long tables
+// Work tables from the offsets in LDS, in sequence order (pages of P = L/2 rows):
+// a window of more than L rows is "long" and goes to the long-window table; a
+// window of P+1..L rows is a chunk of its own; a window of 1..P rows opens a
+// chunk unless the previous non-empty window is short and starts in the same
+// page.  A chunk runs to the next event (chunk start or long window).  s_aux: LDS
+// scratch of at least W ints.  Every thread of the block calls it; returns the
+// number of chunks and sets *n_long.
+__device__ int32_t build_tables(const int32_t* s_off, int32_t* s_aux, int32_t W, int32_t L,
+                                Chunk* __restrict__ chunks, LongWin* __restrict__ longs,
+                                int32_t* s_scan, int32_t* n_long) {
   const int tid = threadIdx.x, T = blockDim.x;
   const int32_t page = L >> 1;
   const int P = (W + T - 1) / T;
   const int w0 = min(tid * P, W), w1 = min(w0 + P, W);
-  // the last non-empty window start and the end of the last long window before
-  // my range decide whether my first non-empty window starts a chunk
-  int32_t aggStart = -1, aggLong = -1;
+  // the start of the last non-empty window and the end of the last window of
+  // more than P rows before my range decide the kind of my first window
+  int32_t aggStart = -1, aggWide = -1;
   for (int w = w0; w < w1; ++w) {
     const int32_t len = s_off[w + 1] - s_off[w];
     if (len > 0) aggStart = s_off[w];
-    if (len > page) aggLong = s_off[w + 1];
+    if (len > page) aggWide = s_off[w + 1];
   }
   int32_t tmp;
   const int32_t lastStart = block_exscan(aggStart, -1, OpMax(), s_scan, &tmp);
-  const int32_t lastLongEnd = block_exscan(aggLong, -1, OpMax(), s_scan, &tmp);
-  auto starts = [&](int32_t& ls, int32_t& ll, int w) {
+  const int32_t lastWideEnd = block_exscan(aggWide, -1, OpMax(), s_scan, &tmp);
+  // 0: no event, 1: opens a chunk, 2: long window.  ls / ll: start of the previous
+  // non-empty window / end of the previous window of more than P rows (ll == a
+  // exactly when the previous non-empty window is not short).
+  auto kind = [&](int32_t& ls, int32_t& ll, int w) -> int {
     const int32_t a = s_off[w], len = s_off[w + 1] - a;
-    if (len <= 0) return false;
-    const bool is_long = len > page;
-    const bool st = is_long || ls < 0 || ll == a || (ls / page) != (a / page);
+    if (len <= 0) return 0;
+    int k = 0;
+    if (len > L) k = 2;
+    else if (len > page || ls < 0 || ll == a || (ls / page) != (a / page)) k = 1;
     ls = a;
-    if (is_long) ll = a + len;
-    return st;
+    if (len > page) ll = a + len;
+    return k;
   };
-  int32_t cnt = 0;
+  int32_t cs = 0, cl = 0;
   {
-    int32_t ls = lastStart, ll = lastLongEnd;
-    for (int w = w0; w < w1; ++w) cnt += starts(ls, ll, w);
+    int32_t ls = lastStart, ll = lastWideEnd;
+    for (int w = w0; w < w1; ++w) {
+      const int k = kind(ls, ll, w);
+      cs += k == 1;
+      cl += k == 2;
+    }
   }
-  int32_t n_chunks = 0;
-  int32_t c = block_exscan(cnt, 0, OpSum(), s_scan, &n_chunks);
+  // both counts in one scan: chunks in the low 16 bits, long windows above (W <= 16384)
+  int32_t tot = 0;
+  const int32_t ex = block_exscan(cs | (cl << 16), 0, OpSum(), s_scan, &tot);
+  const int32_t s0 = ex & 0xffff, l0 = ex >> 16;
+  const int32_t nC = tot & 0xffff, nL = tot >> 16;
   {
-    int32_t ls = lastStart, ll = lastLongEnd;
-    for (int w = w0; w < w1; ++w)
-      if (starts(ls, ll, w)) s_aux[c++] = w;   // first window of chunk c (sequence order)
+    // the event list in sequence order: s_aux[chunk index + long index] = window
+    int32_t ls = lastStart, ll = lastWideEnd, sc = s0, sl = l0;
+    for (int w = w0; w < w1; ++w) {
+      const int k = kind(ls, ll, w);
+      if (k) s_aux[sc + sl] = w;
+      sc += k == 1;
+      sl += k == 2;
+    }
   }
   __syncthreads();
-  for (int i = tid; i < n_chunks; i += T) {
-    Chunk ch;
-    ch.win_begin = s_aux[i];
-    ch.win_end = i + 1 < n_chunks ? s_aux[i + 1] : W;
-    ch.row_begin = s_off[ch.win_begin];
-    ch.row_end = s_off[ch.win_end];
-    chunks[i] = ch;
+  {
+    int32_t ls = lastStart, ll = lastWideEnd, sc = s0, sl = l0;
+    for (int w = w0; w < w1; ++w) {
+      const int k = kind(ls, ll, w);
+      if (k == 1) {
+        const int32_t e = sc + sl;
+        Chunk ch;
+        ch.win_begin = w;
+        ch.win_end = e + 1 < nC + nL ? s_aux[e + 1] : W;
+        ch.row_begin = s_off[w];
+        ch.row_end = s_off[ch.win_end];
+        chunks[sc++] = ch;
+      } else if (k == 2) {
+        LongWin lw;
+        lw.window = w;
+        lw.row_begin = s_off[w];
+        lw.row_end = s_off[w + 1];
+        lw.pad = 0;
+        longs[sl++] = lw;
+      }
+    }
   }
-  return n_chunks;
+  *n_long = nL;
+  return nC;
 }
 
 __device__ void write_header(PlanHeader* hdr, int32_t n, int32_t W, int32_t L, int32_t n_chunks,
-                             int32_t csr, int32_t invalid, int32_t* invalid_out) {
+                             int32_t n_long, int32_t csr, int32_t invalid, int32_t* invalid_out) {
   hdr->magic = kPlanMagic;
   hdr->n = n;
   hdr->num_windows = W;
   hdr->chunk_rows = L;
   hdr->n_chunks = n_chunks;
+  hdr->n_long = n_long;
   hdr->csr = csr;
   hdr->invalid = invalid;
   if (invalid_out) *invalid_out = invalid;
@@ -158,7 +195,8 @@ __global__ __launch_bounds__(kBuildThreads) void k_plan(int32_t csr, int32_t W, 
                                                         int32_t* __restrict__ invalid_out,
                                                         PlanHeader* __restrict__ hdr,
                                                         int32_t* __restrict__ plan_offsets,
-                                                        Chunk* __restrict__ chunks) {
+                                                        Chunk* __restrict__ chunks,
+                                                        LongWin* __restrict__ longs) {
   __shared__ int32_t s_off[kMaxWindows + 1];
   __shared__ int32_t s_aux[kMaxWindows + 1];
   __shared__ int32_t s_scan[33];
@@ -196,8 +234,9 @@ __global__ __launch_bounds__(kBuildThreads) void k_plan(int32_t csr, int32_t W, 
     plan_offsets[w] = s_off[w];
     if (!csr && offsets_io) offsets_io[w] = s_off[w];
   }
-  const int32_t n_chunks = build_chunks(s_off, s_aux, W, L, chunks, s_scan);
-  if (tid == 0) write_header(hdr, n, W, L, n_chunks, csr, invalid, invalid_out);
+  int32_t n_long = 0;
+  const int32_t n_chunks = build_tables(s_off, s_aux, W, L, chunks, longs, s_scan, &n_long);
+  if (tid == 0) write_header(hdr, n, W, L, n_chunks, n_long, csr, invalid, invalid_out);
 }
 
 // --------------------------------------------------------------- k_scatter
@@ -222,8 +261,8 @@ __global__ __launch_bounds__(kBuildThreads) void k_scatter(
     const int32_t* __restrict__ ids, int32_t n, int32_t W, int32_t L, int32_t E, int32_t nb,
     int32_t ld, int32_t nws, const int32_t* __restrict__ counts, int32_t* __restrict__ perm,
     int32_t* __restrict__ perm_out, int32_t* __restrict__ plan_offsets,
-    int32_t* __restrict__ offsets_out, Chunk* __restrict__ chunks, PlanHeader* __restrict__ hdr,
-    int32_t* __restrict__ invalid_out) {
+    int32_t* __restrict__ offsets_out, Chunk* __restrict__ chunks, LongWin* __restrict__ longs,
+    PlanHeader* __restrict__ hdr, int32_t* __restrict__ invalid_out) {
   extern __shared__ int32_t lds[];
   __shared__ int32_t s_scan[33];
   int32_t* base = lds;               // offsets[w] + rows of window w in earlier blocks
@@ -352,11 +391,12 @@ __global__ __launch_bounds__(kBuildThreads) void k_scatter(
     }
   }
 
-  // (4) block 0: chunk table and header (hist is free again)
+  // (4) block 0: chunk and long-window tables and header (hist is free again)
   if (blk == 0) {
     __syncthreads();
-    const int32_t n_chunks = build_chunks(base, hist, W, L, chunks, s_scan);
-    if (tid == 0) write_header(hdr, n, W, L, n_chunks, 0, invalid, invalid_out);
+    int32_t n_long = 0;
+    const int32_t n_chunks = build_tables(base, hist, W, L, chunks, longs, s_scan, &n_long);
+    if (tid == 0) write_header(hdr, n, W, L, n_chunks, n_long, 0, invalid, invalid_out);
   }
 }
 
@@ -383,11 +423,12 @@ hipError_t launch_build(const int32_t* ids, int32_t n, int32_t W, int32_t L, int
   int32_t* perm = reinterpret_cast<int32_t*>(base + lay.perm);
   int32_t* offs = reinterpret_cast<int32_t*>(base + lay.offsets);
   Chunk* chunks = reinterpret_cast<Chunk*>(base + lay.chunks);
+  LongWin* longs = reinterpret_cast<LongWin*>(base + lay.longs);
   int32_t* counts = reinterpret_cast<int32_t*>(base + lay.counts);
   const int csr = ids == nullptr;
   if (csr || lay.n_blocks == 0) {
     hipLaunchKernelGGL(k_plan, dim3(1), dim3(kBuildThreads), 0, stream, csr, W, n, L, offsets_io,
-                       invalid_out, hdr, offs, chunks);
+                       invalid_out, hdr, offs, chunks, longs);
     return hipGetLastError();
   }
   hipLaunchKernelGGL(k_count, dim3(lay.n_blocks), dim3(kBuildThreads), 0, stream, ids, n, W,
@@ -407,7 +448,7 @@ hipError_t launch_build(const int32_t* ids, int32_t n, int32_t W, int32_t L, int
   }
   hipLaunchKernelGGL(k_scatter, dim3(lay.n_blocks), dim3(kBuildThreads), lds, stream, ids, n, W, L,
                      lay.block_elems, lay.n_blocks, lay.counts_ld, nws, counts, perm, perm_out,
-                     offs, offsets_io, chunks, hdr, invalid_out);
+                     offs, offsets_io, chunks, longs, hdr, invalid_out);
   return hipGetLastError();
 }
 

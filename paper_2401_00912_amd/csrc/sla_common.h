@@ -16,33 +16,42 @@ namespace sla {
 // need (the window-sorted view of the rows and the chunk table) plus the
 // builder's scratch.  Section offsets are a pure function of (n, num_windows).
 // ----------------------------------------------------------------------------
-constexpr int32_t kPlanMagic = 0x534c4131;   // "SLA1"
+constexpr int32_t kPlanMagic = 0x534c4132;   // "SLA2"
 constexpr int32_t kMaxWindows = 16384;       // LDS-resident window tables
 constexpr int32_t kMinChunkRows = 32;
-constexpr int32_t kMaxChunkRows = 4096;
-constexpr int32_t kDefaultChunkRows = 128;
+constexpr int32_t kMaxChunkRows = 64;        // rows one wavefront holds in registers
+constexpr int32_t kDefaultChunkRows = 64;
 
 struct PlanHeader {
   int32_t magic;
   int32_t n;            // rows
   int32_t num_windows;  // window slots W
   int32_t chunk_rows;   // L
-  int32_t n_chunks;     // written by the builder
+  int32_t n_chunks;     // chunks of whole windows (written by the builder)
   int32_t csr;          // 1: rows already window-sorted (identity permutation)
   int32_t invalid;      // out-of-range ids / CSR violations seen by the builder
-  int32_t pad[9];
+  int32_t n_long;       // windows of more than L rows (written by the builder)
+  int32_t pad[8];
 };
 static_assert(sizeof(PlanHeader) == 64, "header is 64 bytes");
 
 // One chunk: rows [row_begin, row_end) of the window-sorted sequence, made of
-// windows [win_begin, win_end) (whole windows; empty windows may be included).
+// windows [win_begin, win_end) (whole windows of at most L rows; empty windows
+// may be included).
 struct Chunk {
   int32_t row_begin, row_end, win_begin, win_end;
 };
 
+// One window of more than L rows: its rows are split among the waves of a
+// workgroup, which add their partial states.
+struct LongWin {
+  int32_t window, row_begin, row_end, pad;
+};
+
 struct PlanLayout {
-  size_t header, perm, offsets, chunks, counts, total;
+  size_t header, perm, offsets, chunks, longs, counts, total;
   int32_t max_chunks;   // capacity of the chunk table
+  int32_t max_long;     // capacity of the long-window table
   int32_t n_blocks;     // builder blocks
   int32_t block_elems;  // rows per builder block
   int32_t counts_ld;    // row stride (ints) of the builder's count matrix
@@ -66,8 +75,11 @@ __host__ __device__ inline PlanLayout plan_layout(int64_t n, int32_t num_windows
   L.block_elems = builder_block_elems(n);
   L.n_blocks = (int32_t)((n + L.block_elems - 1) / L.block_elems);
   L.counts_ld = (int32_t)align_up((size_t)W + 1, 4);
-  // Every chunk holds at least one non-empty window, so W bounds the count.
+  // Every chunk holds at least one non-empty window, so min(W, n) bounds the
+  // count; a long window has more than kMinChunkRows rows.
   L.max_chunks = (int32_t)(W < n ? W : n);
+  const int64_t nl = n / (kMinChunkRows + 1);
+  L.max_long = (int32_t)(W < nl ? W : nl);
   size_t off = 0;
   L.header = off;
   off += 256;
@@ -77,6 +89,8 @@ __host__ __device__ inline PlanLayout plan_layout(int64_t n, int32_t num_windows
   off = align_up(off + (size_t)(W + 1) * 4, 256);
   L.chunks = off;
   off = align_up(off + (size_t)(L.max_chunks > 0 ? L.max_chunks : 1) * sizeof(Chunk), 256);
+  L.longs = off;
+  off = align_up(off + (size_t)(L.max_long > 0 ? L.max_long : 1) * sizeof(LongWin), 256);
   L.counts = off;
   off = align_up(off + (size_t)L.n_blocks * (size_t)L.counts_ld * 4, 256);
   L.total = off;

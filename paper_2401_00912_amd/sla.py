@@ -45,8 +45,10 @@ class PlanLayout(ctypes.Structure):
         ("perm", ctypes.c_size_t),
         ("offsets", ctypes.c_size_t),
         ("chunks", ctypes.c_size_t),
+        ("longs", ctypes.c_size_t),
         ("total", ctypes.c_size_t),
         ("max_chunks", ctypes.c_int32),
+        ("max_long", ctypes.c_int32),
     ]
 
 
@@ -129,7 +131,8 @@ def _dtype_code(dt) -> int:
 
 @dataclass
 class Plan:
-    """Device plan of one scene: window-sorted row order, offsets and chunks."""
+    """Device plan of one scene: window-sorted row order, offsets, chunks and
+    long windows."""
 
     buf: object          # torch uint8 tensor on the device (the plan bytes)
     n: int
@@ -226,16 +229,19 @@ def backward(plan: Plan, q, k, v, dout, dq=None, dk=None, dv=None):
 
 
 def read_plan(plan: Plan):
-    """Host copy of the plan's header, perm, offsets and chunk table (tests)."""
+    """Host copy of the plan's header, perm, offsets, chunk table and long-window
+    table (tests)."""
     import numpy as np
 
     lay = plan_layout(plan.n, plan.num_windows)
     raw = plan.buf.cpu().numpy()
     hdr = raw[lay.header: lay.header + 64].view(np.int32)
-    header = dict(zip(("magic", "n", "num_windows", "chunk_rows", "n_chunks", "csr", "invalid"),
-                      hdr[:7].tolist()))
+    header = dict(zip(("magic", "n", "num_windows", "chunk_rows", "n_chunks", "csr", "invalid",
+                       "n_long"), hdr[:8].tolist()))
     perm = raw[lay.perm: lay.perm + 4 * plan.n].view(np.int32)
     offs = raw[lay.offsets: lay.offsets + 4 * (plan.num_windows + 1)].view(np.int32)
     nc = max(0, min(header["n_chunks"], lay.max_chunks))
     chunks = raw[lay.chunks: lay.chunks + 16 * nc].view(np.int32).reshape(nc, 4)
-    return header, perm, offs, chunks
+    nl = max(0, min(header["n_long"], lay.max_long))
+    longs = raw[lay.longs: lay.longs + 16 * nl].view(np.int32).reshape(nl, 4)
+    return header, perm, offs, chunks, longs

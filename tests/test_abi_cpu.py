@@ -46,9 +46,9 @@ def test_only_the_abi_is_exported():
 
 
 def test_queries(L):
-    assert L.sla_abi_version() == 1
+    assert L.sla_abi_version() == 2
     assert L.sla_max_windows() == 16384
-    assert L.sla_default_chunk_rows() == 128
+    assert L.sla_default_chunk_rows() == 64
     for s in range(5):
         assert sla.status_string(s).startswith("SLA_")
     assert sla.plan_bytes(0, 1) > 0
@@ -61,6 +61,9 @@ def test_queries(L):
     assert lay.offsets >= lay.perm + 4 * 60000
     assert lay.chunks >= lay.offsets + 4 * 1522
     assert lay.max_chunks == 1521
+    assert lay.longs % 256 == 0 and lay.longs >= lay.chunks + 16 * 1521
+    assert lay.max_long == min(1521, 60000 // 33) and lay.total >= lay.longs + 16 * lay.max_long
+    assert sla.plan_layout(100, 8).max_long == 3 and sla.plan_layout(100, 2).max_long == 2
 
 
 FAKE = 1 << 20  # a 256-aligned fake device address: never dereferenced, every call below fails validation
@@ -110,7 +113,7 @@ def test_build_argument_errors(L):
         ids, n, W, L_, perm, off, None, plan, pb, None)
     assert b(FAKE, 100, 8, 33, None, None, FAKE, nb) == sla.SLA_E_ARG       # odd chunk rows
     assert b(FAKE, 100, 8, 16, None, None, FAKE, nb) == sla.SLA_E_ARG       # too small
-    assert b(FAKE, 100, 8, 8192, None, None, FAKE, nb) == sla.SLA_E_ARG     # too large
+    assert b(FAKE, 100, 8, 66, None, None, FAKE, nb) == sla.SLA_E_ARG       # too large
     assert b(FAKE, 100, 8, 0, None, None, FAKE, 64) == sla.SLA_E_WORKSPACE
     assert b(FAKE, 100, 8, 0, None, None, None, nb) == sla.SLA_E_ARG
     assert b(None, 100, 8, 0, None, None, FAKE, nb) == sla.SLA_E_ARG        # CSR mode needs offsets

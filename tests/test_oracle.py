@@ -51,35 +51,47 @@ def test_segments_vs_enumeration(seed):
 
 
 # ---------------------------------------------------------------- chunk plan
-def _check_plan_invariants(off, L, chunks):
+def _check_plan_invariants(off, L, chunks, longs):
     off = np.asarray(off)
     nw = len(off) - 1
     page = L // 2
     lengths = np.diff(off)
-    # covers [first non-empty start, N) exactly once, in order
     nonempty = np.nonzero(lengths > 0)[0]
-    if nonempty.size == 0:
-        assert len(chunks) == 0
-        return
-    assert chunks[0][0] == off[nonempty[0]]
-    assert chunks[-1][1] == off[-1]
-    assert chunks[-1][3] == nw
+    # every non-empty window is in exactly one chunk or in the long table
+    owner = np.zeros(nw, dtype=np.int64)
+    for rb, re, wb, we in chunks:
+        owner[wb:we][lengths[wb:we] > 0] += 1
+    owner[np.asarray(longs, dtype=np.int64)] += 1
+    assert np.array_equal(owner[nonempty], np.ones(nonempty.size, dtype=np.int64))
+    assert np.all(owner[lengths == 0] == 0)
+    # long windows: more than L rows, listed in order
+    assert all(lengths[w] > L for w in longs)
+    assert list(longs) == sorted(longs)
+    # chunks: whole windows, in order, disjoint, rows tiled by the long windows
+    covered = np.zeros(int(off[-1]), dtype=np.int64)
+    for w in longs:
+        covered[off[w]:off[w + 1]] += 1
     for a, b in zip(chunks[:-1], chunks[1:]):
-        assert a[1] == b[0] and a[3] == b[2]
+        assert a[3] <= b[2]
     for rb, re, wb, we in chunks:
         assert rb < re and wb < we
         assert off[wb] == rb and off[we] == re          # whole windows only
+        covered[rb:re] += 1
         inside = lengths[wb:we]
-        if (inside > page).any():                      # a long window is alone
+        assert inside[0] > 0                           # a chunk opens on a non-empty window
+        assert np.all(inside <= L)
+        if (inside > page).any():                      # a mid window is alone
             assert (inside > 0).sum() == 1
         else:
             assert re - rb <= L - 1                     # packs stay under L rows
             starts = off[wb:we][inside > 0]
             assert np.all(starts // page == starts[0] // page)
+    if nonempty.size:
+        assert np.all(covered[off[nonempty[0]]:] == 1)
 
 
 @pytest.mark.parametrize("seed", range(8))
-@pytest.mark.parametrize("L", [32, 64, 128, 256])
+@pytest.mark.parametrize("L", [8, 32, 48, 64])
 def test_chunk_plan_invariants(seed, L):
     rng = np.random.default_rng([seed, L])
     W = int(rng.integers(1, 200))
@@ -87,23 +99,29 @@ def test_chunk_plan_invariants(seed, L):
     if seed % 3 == 0:
         lengths = rng.integers(0, 8, size=W)
     off = workloads.offsets_from_lengths(lengths).astype(np.int64)
-    _check_plan_invariants(off, L, oracle.chunk_plan_ref(off, L).tolist())
+    chunks, longs = oracle.chunk_plan_ref(off, L)
+    _check_plan_invariants(off, L, chunks.tolist(), longs.tolist())
 
 
 def test_chunk_plan_hand_example():
-    # L = 8, pages of 4 rows.  Windows: 3, 0, 2, 5, 1, 1, 0, 2 rows.
-    # rows:  w0 [0,3)  w1 empty  w2 [3,5)  w3 [5,10) long  w4 [10,11)  w5 [11,12)
-    #        w6 empty  w7 [12,14)
-    # w0 opens; w2 starts at row 3 (page 0, same as w0) -> joins; w3 is long -> alone;
-    # w4 follows a long window -> opens; w5 starts at 11 (page 2, same as w4's 10) ->
-    # joins; w7 starts at 12 (page 3) -> opens.
-    off = workloads.offsets_from_lengths(np.array([3, 0, 2, 5, 1, 1, 0, 2]))
-    got = oracle.chunk_plan_ref(off, 8).tolist()
-    assert got == [[0, 5, 0, 3], [5, 10, 3, 4], [10, 12, 4, 7], [12, 14, 7, 8]]
+    # L = 8, pages of 4 rows.  Windows: 3, 0, 2, 5, 1, 1, 0, 2, 9, 4, 0 rows.
+    # rows:  w0 [0,3)  w1 empty  w2 [3,5)  w3 [5,10) mid  w4 [10,11)  w5 [11,12)
+    #        w6 empty  w7 [12,14)  w8 [14,23) long  w9 [23,27)  w10 empty
+    # w0 opens; w2 starts at row 3 (page 0, same as w0) -> joins; w3 has 5 > 4
+    # rows -> alone; w4 follows a mid window -> opens; w5 starts at 11 (page 2,
+    # same as w4's 10) -> joins; w7 starts at 12 (page 3) -> opens and ends where
+    # the long window w8 begins; w8 (9 > 8 rows) goes to the long table; w9
+    # follows a long window -> opens and runs to the last window slot.
+    off = workloads.offsets_from_lengths(np.array([3, 0, 2, 5, 1, 1, 0, 2, 9, 4, 0]))
+    chunks, longs = oracle.chunk_plan_ref(off, 8)
+    assert chunks.tolist() == [[0, 5, 0, 3], [5, 10, 3, 4], [10, 12, 4, 7], [12, 14, 7, 8],
+                               [23, 27, 9, 11]]
+    assert longs.tolist() == [8]
 
 
 def test_chunk_plan_empty():
-    assert oracle.chunk_plan_ref(np.zeros(5, dtype=np.int64), 64).shape == (0, 4)
+    chunks, longs = oracle.chunk_plan_ref(np.zeros(5, dtype=np.int64), 64)
+    assert chunks.shape == (0, 4) and longs.shape == (0,)
 
 
 # ------------------------------------------------------------------ forward pins
