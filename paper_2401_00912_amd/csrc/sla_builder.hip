@@ -20,7 +20,17 @@
 
 namespace sla {
 
-constexpr int kBuildThreads = 1024;  // threads of every builder workgroup
+#ifndef SLA_BUILD_THREADS
+#define SLA_BUILD_THREADS 1024
+#endif
+constexpr int kBuildThreads = SLA_BUILD_THREADS;  // threads of every builder workgroup
+
+// Workgroup barrier for LDS traffic only: this wave's LDS operations complete,
+// then every wave arrives.  Threads of a builder workgroup exchange data through
+// LDS alone, so global loads in flight (the next phase's inputs) stay in flight.
+__device__ __forceinline__ void lds_sync() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
 
 // ------------------------------------------------------------------ k_count
 __global__ __launch_bounds__(kBuildThreads) void k_count(const int32_t* __restrict__ ids, int32_t n,
@@ -28,14 +38,14 @@ __global__ __launch_bounds__(kBuildThreads) void k_count(const int32_t* __restri
                                                          int32_t* __restrict__ counts) {
   __shared__ int32_t hist[kMaxWindows + 1];
   for (int i = threadIdx.x; i <= W; i += blockDim.x) hist[i] = 0;
-  __syncthreads();
+  lds_sync();
   const int64_t base = (int64_t)blockIdx.x * E;
   const int64_t end = base + E < n ? base + E : n;
   for (int64_t i = base + threadIdx.x; i < end; i += blockDim.x) {
     const int32_t id = ids[i];
     atomicAdd(&hist[(uint32_t)id < (uint32_t)W ? id : W], 1);
   }
-  __syncthreads();
+  lds_sync();
   int32_t* row = counts + (size_t)blockIdx.x * ld;
   for (int i = threadIdx.x; i < ld; i += blockDim.x) row[i] = i <= W ? hist[i] : 0;
 }
@@ -46,6 +56,14 @@ struct OpSum {
 };
 struct OpMax {
   __device__ int32_t operator()(int32_t a, int32_t b) const { return a > b ? a : b; }
+};
+// Max of each 32-bit half of a packed pair.
+struct OpMax2 {
+  __device__ uint64_t operator()(uint64_t a, uint64_t b) const {
+    const uint32_t hi = max((uint32_t)(a >> 32), (uint32_t)(b >> 32));
+    const uint32_t lo = max((uint32_t)a, (uint32_t)b);
+    return ((uint64_t)hi << 32) | lo;
+  }
 };
 
 
@@ -61,7 +79,7 @@ __device__ V block_exscan(V x, V identity, Op op, V* s, V* total) {
     if (lane >= d) inc = op(inc, y);
   }
   if (lane == 63) s[wv] = inc;
-  __syncthreads();
+  lds_sync();
   if (wv == 0) {
     const V v = lane < nwv ? s[lane] : identity;
     V inc2 = v;
@@ -75,12 +93,12 @@ __device__ V block_exscan(V x, V identity, Op op, V* s, V* total) {
     if (lane < nwv) s[lane] = ex2;
     if (lane == nwv - 1) s[32] = inc2;
   }
-  __syncthreads();
+  lds_sync();
   V ex = __shfl_up(inc, 1, 64);
   if (lane == 0) ex = identity;
   const V r = op(s[wv], ex);
   *total = s[32];
-  __syncthreads();
+  lds_sync();
   return r;
 }
 
@@ -94,7 +112,7 @@ __device__ V block_exscan(V x, V identity, Op op, V* s, V* total) {
 // number of chunks and sets *n_long.
 __device__ int32_t build_tables(const int32_t* s_off, int32_t* s_aux, int32_t W, int32_t L,
                                 Chunk* __restrict__ chunks, LongWin* __restrict__ longs,
-                                int32_t* s_scan, int32_t* n_long) {
+                                int32_t* s_scan, uint64_t* s_scan2, int32_t* n_long) {
   const int tid = threadIdx.x, T = blockDim.x;
   const int32_t page = L >> 1;
   const int P = (W + T - 1) / T;
@@ -107,9 +125,13 @@ __device__ int32_t build_tables(const int32_t* s_off, int32_t* s_aux, int32_t W,
     if (len > 0) aggStart = s_off[w];
     if (len > page) aggWide = s_off[w + 1];
   }
-  int32_t tmp;
-  const int32_t lastStart = block_exscan(aggStart, -1, OpMax(), s_scan, &tmp);
-  const int32_t lastWideEnd = block_exscan(aggWide, -1, OpMax(), s_scan, &tmp);
+  // both maxima in one scan of (value + 1) pairs
+  uint64_t tmp;
+  const uint64_t both = block_exscan<OpMax2, uint64_t>(
+      ((uint64_t)(uint32_t)(aggStart + 1) << 32) | (uint32_t)(aggWide + 1), 0ull, OpMax2(), s_scan2,
+      &tmp);
+  const int32_t lastStart = (int32_t)(both >> 32) - 1;
+  const int32_t lastWideEnd = (int32_t)(uint32_t)both - 1;
   // 0: no event, 1: opens a chunk, 2: long window.  ls / ll: start of the previous
   // non-empty window / end of the previous window of more than P rows (ll == a
   // exactly when the previous non-empty window is not short).
@@ -147,7 +169,7 @@ __device__ int32_t build_tables(const int32_t* s_off, int32_t* s_aux, int32_t W,
       sl += k == 2;
     }
   }
-  __syncthreads();
+  lds_sync();
   {
     int32_t ls = lastStart, ll = lastWideEnd, sc = s0, sl = l0;
     for (int w = w0; w < w1; ++w) {
@@ -200,6 +222,7 @@ __global__ __launch_bounds__(kBuildThreads) void k_plan(int32_t csr, int32_t W, 
   __shared__ int32_t s_off[kMaxWindows + 1];
   __shared__ int32_t s_aux[kMaxWindows + 1];
   __shared__ int32_t s_scan[33];
+  __shared__ uint64_t s_scan2[33];
   const int tid = threadIdx.x, T = blockDim.x;
   int32_t invalid = 0, total = 0;
   if (csr) {
@@ -229,13 +252,13 @@ __global__ __launch_bounds__(kBuildThreads) void k_plan(int32_t csr, int32_t W, 
   } else {
     for (int w = tid; w <= W; w += T) s_off[w] = 0;
   }
-  __syncthreads();
+  lds_sync();
   for (int w = tid; w <= W; w += T) {
     plan_offsets[w] = s_off[w];
     if (!csr && offsets_io) offsets_io[w] = s_off[w];
   }
   int32_t n_long = 0;
-  const int32_t n_chunks = build_tables(s_off, s_aux, W, L, chunks, longs, s_scan, &n_long);
+  const int32_t n_chunks = build_tables(s_off, s_aux, W, L, chunks, longs, s_scan, s_scan2, &n_long);
   if (tid == 0) write_header(hdr, n, W, L, n_chunks, n_long, csr, invalid, invalid_out);
 }
 
@@ -256,113 +279,169 @@ __device__ __forceinline__ uint64_t lanemask_lt(int lane) {
   return lane == 0 ? 0ull : (~0ull >> (64 - lane));
 }
 
-// Dynamic LDS: base[W + 1] then hist[max(nws W, W + 1)], nws = waves that rank rows.
+// Dynamic LDS: base[W + 1], tot[W + 1], hist[max(nws W, W + 1)] (overlap) or
+// base[W + 1], hist[max(nws W, W + 1)] with tot = hist (no overlap, large W);
+// nws = waves that rank rows.  Blocks 0..nb-1 rank and scatter the rows of
+// builder block blockIdx.x; block nb publishes the offsets and builds the chunk
+// and long-window tables and the header, in parallel with the others.
+//
+// A ranking block requests its rows' window ids and its share of the count
+// matrix first; with `overlap` it counts its rows per wave (which needs only the
+// ids) while the matrix is in flight; then the column prefix and totals, the
+// offsets, the per-wave prefix and the scatter.
+constexpr int kMatBatch = 16;   // count-matrix rows a thread has in flight at once
+
 __global__ __launch_bounds__(kBuildThreads) void k_scatter(
     const int32_t* __restrict__ ids, int32_t n, int32_t W, int32_t L, int32_t E, int32_t nb,
-    int32_t ld, int32_t nws, const int32_t* __restrict__ counts, int32_t* __restrict__ perm,
-    int32_t* __restrict__ perm_out, int32_t* __restrict__ plan_offsets,
+    int32_t ld, int32_t nws, int32_t overlap, const int32_t* __restrict__ counts,
+    int32_t* __restrict__ perm, int32_t* __restrict__ perm_out, int32_t* __restrict__ plan_offsets,
     int32_t* __restrict__ offsets_out, Chunk* __restrict__ chunks, LongWin* __restrict__ longs,
     PlanHeader* __restrict__ hdr, int32_t* __restrict__ invalid_out) {
   extern __shared__ int32_t lds[];
   __shared__ int32_t s_scan[33];
-  int32_t* base = lds;               // offsets[w] + rows of window w in earlier blocks
-  int32_t* hist = lds + (W + 1);     // column totals, then the per-wave row counts
+  __shared__ uint64_t s_scan2[33];
+  int32_t* base = lds;                              // offsets[w] + rows of window w in earlier blocks
+  int32_t* tot = lds + (W + 1);                     // column totals
+  int32_t* hist = overlap ? tot + (W + 1) : tot;    // per-wave row counts (table block: scratch)
   const int tid = threadIdx.x, T = blockDim.x;
   const int lane = tid & 63, wv = tid >> 6;
   const int32_t blk = blockIdx.x;
+  const bool tables = blk == nb;
 
-  // (1) column prefix over the earlier blocks and column totals.  Thread (part,
-  // g) sums rows [part RP, part RP + RP) of column group g (4 columns, one 16-B
-  // load per row), so all of a thread's loads are in flight together.
+  // this wave's rows [rbeg, rend): ids of the first two 64-row groups
+  const int64_t span = E / nws;
+  const int64_t rbeg = (int64_t)blk * E + wv * span;
+  const int64_t rend = rbeg + span < n ? rbeg + span : n;
+  const bool ranks = !tables && wv < nws;
+  int32_t id0 = -1, id1 = -1;
+  if (ranks) {
+    if (rbeg + lane < rend) id0 = ids[rbeg + lane];
+    if (rbeg + 64 + lane < rend) id1 = ids[rbeg + 64 + lane];
+  }
+
+  // count-matrix shares: unit (part, g) sums rows [part RP, part RP + RP) of
+  // column group g (4 columns, one 16-B load per row); a thread takes units tid,
+  // tid + T, ...; the first kMatBatch rows of its first unit are requested now
+  const int G = ld >> 2;
+  const int R = max(1, min(T / G, nb));
+  const int RP = (nb + R - 1) / R;
+  const int NU = R * G;
+  int4 x[kMatBatch];
+  {
+    const int part = tid / G, cg = tid - part * G;
+    const int b0 = part * RP, b1 = min(b0 + RP, nb);
+#pragma unroll
+    for (int u = 0; u < kMatBatch; ++u)
+      x[u] = tid < NU && b0 + u < b1 ? reinterpret_cast<const int4*>(counts + (size_t)(b0 + u) * ld)[cg]
+                                     : make_int4(0, 0, 0, 0);
+  }
+
   for (int w = tid; w <= W; w += T) {
     base[w] = 0;
-    hist[w] = 0;
+    tot[w] = 0;
   }
-  __syncthreads();
-  {
-    const int G = ld >> 2;
-    const int R = G >= T ? 1 : min(T / G, nb);
-    const int RP = (nb + R - 1) / R;
-    for (int item = tid; item < R * G; item += T) {
-      const int part = item / G, g = item - part * G;
-      const int b0 = part * RP, b1 = min(b0 + RP, nb);
-      int4 pre = make_int4(0, 0, 0, 0), tot = make_int4(0, 0, 0, 0);
-      for (int b = b0; b < b1; b += 16) {
-        int4 x[16];
+  if (!tables && overlap)   // every thread of the block: the loop is strided over all of them
+    for (int i = tid; i < nws * W; i += T) hist[i] = 0;
+  lds_sync();
+
+  // (a) ranking blocks: per-wave window counts of the wave's rows
+  const int nbits = W > 1 ? 32 - __clz(W - 1) : 0;
+  int32_t* h = hist + wv * W;
+  const uint64_t lt = lanemask_lt(lane);
+  auto count_group = [&](int32_t id) {
+    const bool valid = (uint32_t)id < (uint32_t)W;
+    const uint64_t m = match_key(id, valid, nbits);
+    if (valid && (m & lt) == 0) h[id] += __popcll(m);
+  };
+  auto id_at = [&](int64_t r) -> int32_t { return r + lane < rend ? ids[r + lane] : -1; };
+  auto count_rows = [&]() {
+    if (ranks) {
+      count_group(id0);
+      if (rbeg + 64 < rend) count_group(id1);
+      for (int64_t r = rbeg + 128; r < rend; r += 64) count_group(id_at(r));
+    }
+  };
+  if (overlap) count_rows();
+
+  // (b) column prefix over the earlier blocks and column totals
+  for (int unit = tid; unit < NU; unit += T) {
+    const int part = unit / G, cg = unit - part * G;
+    const int b0 = part * RP, b1 = min(b0 + RP, nb);
+    int4 pre = make_int4(0, 0, 0, 0), sum = make_int4(0, 0, 0, 0);
+    for (int b = b0; b < b1; b += kMatBatch) {
+      if (unit != tid || b != b0) {
 #pragma unroll
-        for (int u = 0; u < 16; ++u)
-          x[u] = b + u < b1 ? reinterpret_cast<const int4*>(counts + (size_t)(b + u) * ld)[g]
+        for (int u = 0; u < kMatBatch; ++u)
+          x[u] = b + u < b1 ? reinterpret_cast<const int4*>(counts + (size_t)(b + u) * ld)[cg]
                             : make_int4(0, 0, 0, 0);
-#pragma unroll
-        for (int u = 0; u < 16; ++u) {
-          tot.x += x[u].x; tot.y += x[u].y; tot.z += x[u].z; tot.w += x[u].w;
-          if (b + u < blk) { pre.x += x[u].x; pre.y += x[u].y; pre.z += x[u].z; pre.w += x[u].w; }
-        }
       }
-      const int w = 4 * g;
-      const int32_t p4[4] = {pre.x, pre.y, pre.z, pre.w}, t4[4] = {tot.x, tot.y, tot.z, tot.w};
 #pragma unroll
-      for (int k = 0; k < 4; ++k) {
-        if (w + k <= W) {
-          if (R > 1) {
-            atomicAdd(&base[w + k], p4[k]);
-            atomicAdd(&hist[w + k], t4[k]);
-          } else {
-            base[w + k] = p4[k];
-            hist[w + k] = t4[k];
-          }
+      for (int u = 0; u < kMatBatch; ++u) {
+        sum.x += x[u].x; sum.y += x[u].y; sum.z += x[u].z; sum.w += x[u].w;
+        if (b + u < blk) { pre.x += x[u].x; pre.y += x[u].y; pre.z += x[u].z; pre.w += x[u].w; }
+      }
+    }
+    const int w = 4 * cg;
+    const int32_t p4[4] = {pre.x, pre.y, pre.z, pre.w}, t4[4] = {sum.x, sum.y, sum.z, sum.w};
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      if (w + k <= W) {
+        if (R > 1) {
+          atomicAdd(&base[w + k], p4[k]);
+          atomicAdd(&tot[w + k], t4[k]);
+        } else {
+          base[w + k] = p4[k];
+          tot[w + k] = t4[k];
         }
       }
     }
   }
-  __syncthreads();
-  const int32_t invalid = hist[W];   // column W counts the out-of-range ids
+  lds_sync();
+  const int32_t invalid = tot[W];   // column W counts the out-of-range ids
 
-  // (2) offsets = exclusive scan of the column totals; base += offsets
+  // (c) offsets = exclusive scan of the column totals; base += offsets
   {
     const int P = (W + T - 1) / T;
     const int w0 = min(tid * P, W), w1 = min(w0 + P, W);
     int32_t local = 0;
-    for (int w = w0; w < w1; ++w) local += hist[w];
+    for (int w = w0; w < w1; ++w) local += tot[w];
     int32_t total = 0;
     int32_t ex = block_exscan(local, 0, OpSum(), s_scan, &total);
+    if (tables) {
+      // the table block: base[0..W] become the offsets
+      for (int w = w0; w < w1; ++w) {
+        const int32_t t = tot[w];
+        base[w] = ex;
+        plan_offsets[w] = ex;
+        if (offsets_out) offsets_out[w] = ex;
+        ex += t;
+      }
+      if (tid == 0) {
+        base[W] = total;
+        plan_offsets[W] = total;
+        if (offsets_out) offsets_out[W] = total;
+      }
+      lds_sync();
+      int32_t n_long = 0;
+      const int32_t n_chunks = build_tables(base, hist, W, L, chunks, longs, s_scan, s_scan2, &n_long);
+      if (tid == 0) write_header(hdr, n, W, L, n_chunks, n_long, 0, invalid, invalid_out);
+      return;
+    }
     for (int w = w0; w < w1; ++w) {
-      const int32_t t = hist[w];
+      const int32_t t = tot[w];
       base[w] += ex;
       ex += t;
     }
-    if (tid == 0) base[W] = total;   // for block 0, base[0..W] are then the offsets
   }
-  __syncthreads();
-  if (blk == 0) {
-    for (int w = tid; w <= W; w += T) {
-      plan_offsets[w] = base[w];
-      if (offsets_out) offsets_out[w] = base[w];
-    }
+  if (!overlap) {
+    // hist takes the place of the totals now
+    lds_sync();
+    for (int i = tid; i < nws * W; i += T) hist[i] = 0;
+    lds_sync();
+    count_rows();
+    lds_sync();
   }
-
-  // (3) stable ranks: wave v of the first nws takes rows [v span, v span + span)
-  // of the block; per-wave window counts, their prefix over the waves, then the
-  // scatter with each wave's running counters.
-  for (int i = tid; i < nws * W; i += T) hist[i] = 0;
-  __syncthreads();
-  const int nbits = W > 1 ? 32 - __clz(W - 1) : 0;
-  const int64_t span = E / nws;
-  const int64_t rbeg = (int64_t)blk * E + wv * span;
-  const int64_t rend = rbeg + span < n ? rbeg + span : n;
-  int32_t* h = hist + wv * W;
-  const uint64_t lt = lanemask_lt(lane);
-  if (wv < nws) {
-    for (int64_t r = rbeg; r < rend; r += 64) {
-      const int64_t i = r + lane;
-      const bool in = i < rend;
-      const int32_t id = in ? ids[i] : -1;
-      const bool valid = in && (uint32_t)id < (uint32_t)W;
-      const uint64_t m = match_key(id, valid, nbits);
-      if (valid && (m & lt) == 0) h[id] += __popcll(m);
-    }
-  }
-  __syncthreads();
+  // (d) exclusive prefix of the per-wave counts over the waves
   for (int w = tid; w < W; w += T) {
     int32_t run = 0;
     for (int v = 0; v < nws; ++v) {
@@ -371,47 +450,49 @@ __global__ __launch_bounds__(kBuildThreads) void k_scatter(
       run += t;
     }
   }
-  __syncthreads();
-  if (wv < nws) {
-    for (int64_t r = rbeg; r < rend; r += 64) {
-      const int64_t i = r + lane;
-      const bool in = i < rend;
-      const int32_t id = in ? ids[i] : -1;
-      const bool valid = in && (uint32_t)id < (uint32_t)W;
-      const uint64_t m = match_key(id, valid, nbits);
-      if (valid) {
-        const int32_t hb = h[id];
-        const int32_t pos = base[id] + hb + __popcll(m & lt);
-        if ((uint32_t)pos < (uint32_t)n) {
-          perm[pos] = (int32_t)i;
-          if (perm_out) perm_out[pos] = (int32_t)i;
-        }
-        if ((m & lt) == 0) h[id] = hb + __popcll(m);
-      }
-    }
-  }
+  lds_sync();
 
-  // (4) block 0: chunk and long-window tables and header (hist is free again)
-  if (blk == 0) {
-    __syncthreads();
-    int32_t n_long = 0;
-    const int32_t n_chunks = build_tables(base, hist, W, L, chunks, longs, s_scan, &n_long);
-    if (tid == 0) write_header(hdr, n, W, L, n_chunks, n_long, 0, invalid, invalid_out);
+  // (e) scatter, each wave with its running counters
+  auto scatter_group = [&](int64_t r, int32_t id) {
+    const int64_t i = r + lane;
+    const bool valid = (uint32_t)id < (uint32_t)W;
+    const uint64_t m = match_key(id, valid, nbits);
+    if (valid) {
+      const int32_t hb = h[id];
+      const int32_t pos = base[id] + hb + __popcll(m & lt);
+      if ((uint32_t)pos < (uint32_t)n) {
+        perm[pos] = (int32_t)i;
+        if (perm_out) perm_out[pos] = (int32_t)i;
+      }
+      if ((m & lt) == 0) h[id] = hb + __popcll(m);
+    }
+  };
+  if (ranks) {
+    scatter_group(rbeg, id0);
+    if (rbeg + 64 < rend) scatter_group(rbeg + 64, id1);
+    for (int64_t r = rbeg + 128; r < rend; r += 64) scatter_group(r, id_at(r));
   }
 }
 
 // Waves of k_scatter that rank rows: as many as the LDS holds (<= 16), and at
 // most one per 64 rows of a block.
-static int scatter_waves(int32_t W, int32_t E, size_t* lds_bytes) {
+// Prefers the overlapped layout; large W falls back to the sequential one.
+static int scatter_waves(int32_t W, int32_t E, size_t* lds_bytes, int* overlap) {
   constexpr size_t kLds = 160 * 1024 - 1024;   // leave room for the static arrays
-  int nws = kBuildThreads / 64;
-  auto bytes = [&](int v) {
+  auto bytes = [&](int v, int ov) {
     const size_t h = (size_t)v * W > (size_t)W + 1 ? (size_t)v * W : (size_t)W + 1;
-    return ((size_t)W + 1 + h) * 4;
+    return ((ov ? 2 : 1) * ((size_t)W + 1) + h) * 4;
   };
-  while (nws > 1 && (bytes(nws) > kLds || (int64_t)nws * 64 > E)) nws >>= 1;
-  *lds_bytes = bytes(nws);
-  return nws;
+  for (int ov = 1; ov >= 0; --ov) {
+    int nws = kBuildThreads / 64;
+    while (nws > 1 && (bytes(nws, ov) > kLds || (int64_t)nws * 64 > E)) nws >>= 1;
+    if (bytes(nws, ov) <= kLds || ov == 0) {
+      *lds_bytes = bytes(nws, ov);
+      *overlap = ov;
+      return nws;
+    }
+  }
+  return 1;
 }
 
 // ------------------------------------------------------------ host launchers
@@ -434,7 +515,8 @@ hipError_t launch_build(const int32_t* ids, int32_t n, int32_t W, int32_t L, int
   hipLaunchKernelGGL(k_count, dim3(lay.n_blocks), dim3(kBuildThreads), 0, stream, ids, n, W,
                      lay.block_elems, lay.counts_ld, counts);
   size_t lds = 0;
-  const int nws = scatter_waves(W, lay.block_elems, &lds);
+  int overlap = 0;
+  const int nws = scatter_waves(W, lay.block_elems, &lds, &overlap);
   // the dynamic LDS of k_scatter exceeds the default limit: raise it once per device
   static bool lds_attr[64] = {};
   int dev = 0;
@@ -446,8 +528,8 @@ hipError_t launch_build(const int32_t* ids, int32_t n, int32_t W, int32_t L, int
     if (e != hipSuccess) return e;
     if (dev >= 0 && dev < 64) lds_attr[dev] = true;
   }
-  hipLaunchKernelGGL(k_scatter, dim3(lay.n_blocks), dim3(kBuildThreads), lds, stream, ids, n, W, L,
-                     lay.block_elems, lay.n_blocks, lay.counts_ld, nws, counts, perm, perm_out,
+  hipLaunchKernelGGL(k_scatter, dim3(lay.n_blocks + 1), dim3(kBuildThreads), lds, stream, ids, n, W, L,
+                     lay.block_elems, lay.n_blocks, lay.counts_ld, nws, overlap, counts, perm, perm_out,
                      offs, offsets_io, chunks, longs, hdr, invalid_out);
   return hipGetLastError();
 }
