@@ -1278,16 +1278,24 @@ static int resident_workgroups(const void* kernel) {
   return per_cu * cus;
 }
 
-// Workgroups of a launch: the resident capacity of the device for the kernel,
-// at most enough for every item the plan can hold (long windows have more than
-// kMinChunkRows rows), a multiple of 8.
-static int grid_size(const void* kernel, const PlanLayout& lay, int32_t H) {
-  const int c = resident_workgroups(kernel);
+// Workgroups of a launch: a whole number k of the device's resident capacity for
+// the kernel (a partial last round of workgroups would start late and set the
+// end), with k ~ (row-heads) / (300 x resident).  Small scenes (one Waymo-like
+// frame) get one persistent round whose waves prefetch item to item; large ones
+// (200k+ rows, several heads) get several rounds, so that the hardware
+// dispatcher balances items of very different cost.  At most enough workgroups
+// for every item the plan can hold; a multiple of 8.
+constexpr int64_t kRowHeadsPerWorkgroup = 300;
+
+static int grid_size(const void* kernel, const PlanLayout& lay, int32_t n, int32_t H) {
+  const int64_t c = resident_workgroups(kernel);
   const int hw = H < 4 ? H : 4, cpw = 4 / hw, hg = (H + 3) / 4;
   const int64_t itemsL = (int64_t)((lay.max_long + 7) & ~7) * H;
   const int64_t itemsC = (int64_t)(lay.max_chunks + cpw - 1) / cpw * hg;
-  int64_t g = itemsL + itemsC;
-  if (g > c) g = c;
+  int64_t k = ((int64_t)n * H + c * kRowHeadsPerWorkgroup / 2) / (c * kRowHeadsPerWorkgroup);
+  if (k < 1) k = 1;
+  int64_t g = k * c;
+  if (g > itemsL + itemsC) g = itemsL + itemsC;
   g = (g + 7) & ~7;
   return (int)(g < 8 ? 8 : g);
 }
@@ -1314,7 +1322,7 @@ static hipError_t fwd_impl(const void* plan, int32_t n, int32_t W, int32_t H, co
                            const void* k, const void* v, void* o, hipStream_t stream) {
   const PlanLayout lay = plan_layout(n, W);
   const KernelArgs a = kernel_args(plan, lay, n, W, H);
-  hipLaunchKernelGGL((k_sla_fwd<T, D>), dim3(grid_size(reinterpret_cast<const void*>(&k_sla_fwd<T, D>), lay, H)), dim3(64 * kWaves), 0, stream, a,
+  hipLaunchKernelGGL((k_sla_fwd<T, D>), dim3(grid_size(reinterpret_cast<const void*>(&k_sla_fwd<T, D>), lay, n, H)), dim3(64 * kWaves), 0, stream, a,
                      static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v),
                      static_cast<T*>(o));
   return hipGetLastError();
@@ -1326,7 +1334,7 @@ static hipError_t bwd_impl(const void* plan, int32_t n, int32_t W, int32_t H, co
                            void* dv, hipStream_t stream) {
   const PlanLayout lay = plan_layout(n, W);
   const KernelArgs a = kernel_args(plan, lay, n, W, H);
-  hipLaunchKernelGGL((k_sla_bwd<T, D>), dim3(grid_size(reinterpret_cast<const void*>(&k_sla_bwd<T, D>), lay, H)), dim3(64 * kWaves), 0, stream, a,
+  hipLaunchKernelGGL((k_sla_bwd<T, D>), dim3(grid_size(reinterpret_cast<const void*>(&k_sla_bwd<T, D>), lay, n, H)), dim3(64 * kWaves), 0, stream, a,
                      static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v),
                      static_cast<const T*>(dout), static_cast<T*>(dq), static_cast<T*>(dk),
                      static_cast<T*>(dv));
