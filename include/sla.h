@@ -91,8 +91,9 @@ typedef struct {
   int32_t max_long;
 } sla_plan_layout_t;
 /* Plan header (int32 fields in order): magic, n, num_windows, chunk_rows,
- * n_chunks, csr (1 = rows were already window-sorted), invalid, n_long, then
- * padding. */
+ * n_chunks, csr (1 = rows were already window-sorted), invalid, n_long, n_long4
+ * (long windows of more than 2 chunk_rows rows, listed first in the long table),
+ * then padding. */
 
 sla_status_t sla_plan_layout(int64_t n, int32_t num_windows, sla_plan_layout_t* out /* host */);
 
@@ -119,11 +120,13 @@ sla_status_t sla_plan_layout(int64_t n, int32_t num_windows, sla_plan_layout_t* 
  * Work tables (both modes), with L = chunk_rows (0 = default 64; else even,
  * 32..64) and pages of L/2 rows: a window of more than L rows is "long" and is
  * listed in the long-window table (the forward and backward split its rows among
- * the wavefronts of one workgroup, which add their partial window states); a
- * window of L/2 + 1 .. L rows is a chunk of its own; shorter windows are packed
- * into one chunk while they start in the same page, so a packed chunk never
- * splits a window and never exceeds L - 1 rows.  Empty windows get nothing.  Both
- * tables are in sequence order.
+ * four wavefronts of one workgroup if it has more than 2L rows, else among two,
+ * which add their partial window states; four-way windows are listed first,
+ * then two-way ones, each group in sequence order); a window of L/2 + 1 .. L
+ * rows is a chunk of its own; shorter windows are packed into one chunk while
+ * they start in the same page, so a packed chunk never splits a window and never
+ * exceeds L - 1 rows.  Empty windows get nothing.  The chunk table is in
+ * sequence order.
  *
  * invalid_count (device int32, may be NULL) receives the number of out-of-range
  * ids (mode A) or offset violations (mode B).  The plan must be at least

@@ -113,7 +113,8 @@ def chunk_plan_ref(offsets: np.ndarray, chunk_rows: int):
     rows, every non-empty window is exactly one of:
       * long  (more than L rows): listed in the long-window table and nowhere
         else (its rows are split among several workers, whose partial states are
-        added before the output is formed);
+        added before the output is formed): four ways if it has more than 2L
+        rows, two ways otherwise;
       * mid   (P < rows <= L): a chunk of its own;
       * short (1..P rows): opens a new chunk unless the previous non-empty window
         is short and starts in the same page (page = start_row // P); otherwise it
@@ -124,9 +125,10 @@ def chunk_plan_ref(offsets: np.ndarray, chunk_rows: int):
     num_windows), so empty windows between are included; its rows are
     [offsets[win_begin], offsets[win_end]).
 
-    Returns (chunks, longs): int64 [n_chunks, 4] of (row_begin, row_end,
-    win_begin, win_end) in sequence order, and int64 [n_long] window ids in
-    sequence order.
+    Returns (chunks, longs, n_four): chunks int64 [n_chunks, 4] of (row_begin,
+    row_end, win_begin, win_end) in sequence order; longs int64 [n_long] window
+    ids, the four-way windows first, then the two-way ones, each group in
+    sequence order; n_four the number of four-way windows.
     """
     off = [int(x) for x in offsets]
     nw = len(off) - 1
@@ -143,15 +145,15 @@ def chunk_plan_ref(offsets: np.ndarray, chunk_rows: int):
         elif not short or prev is None or not prev[1] or (prev[0] // page) != (off[w] // page):
             events.append((w, True))
         prev = (off[w], short)
-    chunks, longs = [], []
+    chunks, four, two = [], [], []
     for e, (w, is_chunk) in enumerate(events):
         if not is_chunk:
-            longs.append(w)
+            (four if off[w + 1] - off[w] > 2 * chunk_rows else two).append(w)
             continue
         we = events[e + 1][0] if e + 1 < len(events) else nw
         chunks.append((off[w], off[we], w, we))
     return (np.asarray(chunks, dtype=np.int64).reshape(-1, 4),
-            np.asarray(longs, dtype=np.int64))
+            np.asarray(four + two, dtype=np.int64), len(four))
 
 
 def _window_rows(offsets, perm, w):

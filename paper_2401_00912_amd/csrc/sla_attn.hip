@@ -753,35 +753,45 @@ __device__ __forceinline__ void kgrad_seg(const Slice<T, Geo<D>::KS, NM>& sb, in
 // in flight, so an item's row gathers start as soon as the previous item's rows
 // have been requested and its data path is one memory round trip long.
 struct Items {
-  int32_t nL, nC, H, hw, cpw, hg;
-  int32_t itemsL, total;
+  int32_t nL4, nL2, nC, H, hp, hw, cpw, hg;
+  int32_t itemsL4, itemsL, total;
 };
 
 __device__ __forceinline__ Items work_items(const KernelArgs& a, const PlanHeader* hdr) {
   Items it;
-  it.nL = max(0, min(hdr->n_long, a.max_long));
+  const int32_t nL = max(0, min(hdr->n_long, a.max_long));
+  it.nL4 = max(0, min(hdr->n_long4, nL));
+  it.nL2 = nL - it.nL4;
   it.nC = max(0, min(hdr->n_chunks, a.max_chunks));
   it.H = a.H;
+  it.hp = (a.H + 1) / 2;
   it.hw = min(a.H, 4);
   it.cpw = 4 / it.hw;
   it.hg = (a.H + 3) / 4;
-  it.itemsL = ((it.nL + 7) & ~7) * a.H;
+  it.itemsL4 = ((it.nL4 + 7) & ~7) * a.H;
+  it.itemsL = it.itemsL4 + ((it.nL2 + 7) & ~7) * it.hp;
   it.total = it.itemsL + (it.nC + it.cpw - 1) / it.cpw * it.hg;
   return it;
 }
 
 struct WaveWork {
-  int kind;        // 0: nothing, 1: a chunk, 2: a quarter of a long window
+  int kind;        // 0: nothing, 1: a chunk, 2: a share of a long window
   int h;           // head
   int32_t ra, rb;  // rows (sorted positions)
   int32_t wb, we;  // windows
+  int pair;        // long window: 0 = the four waves share it, 1 = waves 2m, 2m + 1 do
 };
 
 // Where item `item` puts wave wv (wave-uniform): table entry index (-1: none),
-// the table (0: long windows, 1: chunks) and the head.
+// the table (0: long windows, 1: chunks), the head, and for a long window how
+// many waves share it and which share is this wave's (-1: none, the wave only
+// takes part in the workgroup's partial-state exchange).
+//   four-way long items: one per (window, head), the four waves take quarters;
+//   two-way long items: one per (window, pair of heads), waves 2m and 2m + 1
+//     take the halves of head 2 x (item's pair) + m.
 struct Slot {
   int32_t idx;
-  int table, h;
+  int table, h, parts, piece;
 };
 
 __device__ __forceinline__ Slot item_slot(const Items& it, int32_t item, int wv) {
@@ -789,12 +799,22 @@ __device__ __forceinline__ Slot item_slot(const Items& it, int32_t item, int wv)
   sl.idx = -1;
   sl.table = 0;
   sl.h = 0;
+  sl.parts = 4;
+  sl.piece = wv;
   if (item >= it.total) return sl;
-  if (item < it.itemsL) {
+  if (item < it.itemsL4) {
     const int32_t r = item >> 3;
     const int32_t j = (r / it.H) * 8 + (item & 7);
     sl.h = r % it.H;
-    if (j < it.nL) sl.idx = j;
+    if (j < it.nL4) sl.idx = j;
+  } else if (item < it.itemsL) {
+    const int32_t r = (item - it.itemsL4) >> 3;   // itemsL4 is a multiple of 8
+    const int32_t j = (r / it.hp) * 8 + (item & 7);
+    const int h = (r % it.hp) * 2 + (wv >> 1);
+    sl.parts = 2;
+    sl.piece = h < it.H ? (wv & 1) : -1;
+    sl.h = h < it.H ? h : 0;
+    if (j < it.nL2) sl.idx = it.nL4 + j;
   } else {
     const int32_t b = item - it.itemsL;
     const int32_t grp = b / it.hg;
@@ -820,16 +840,19 @@ __device__ __forceinline__ WaveWork decode_work(const KernelArgs& a, const Slot&
   ww.kind = 0;
   ww.h = sl.h;
   ww.ra = ww.rb = ww.wb = ww.we = 0;
+  ww.pair = 0;
   if (sl.idx < 0) return ww;
   if (sl.table == 0) {  // LongWin: window, row_begin, row_end
     const int32_t rs = max(0, min(e.y, a.n));
     const int32_t re = max(rs, min(e.z, a.n));
     const int64_t len = re - rs;
-    ww.ra = rs + (int32_t)((len * wv) >> 2);
-    ww.rb = rs + (int32_t)((len * (wv + 1)) >> 2);
+    const int p = sl.piece < 0 ? 0 : sl.piece;
+    ww.ra = rs + (int32_t)(len * p / sl.parts);
+    ww.rb = sl.piece < 0 ? ww.ra : rs + (int32_t)(len * (p + 1) / sl.parts);
     ww.wb = e.x;
     ww.we = e.x + 1;
     ww.kind = 2;
+    ww.pair = sl.parts == 2;
   } else {  // Chunk: row_begin, row_end, win_begin, win_end
     ww.ra = max(0, min(e.x, a.n));
     ww.rb = max(ww.ra, min(min(e.y, a.n), ww.ra + kMaxChunkRows));
@@ -1003,13 +1026,15 @@ __device__ __forceinline__ void publish(const State<D>& st, floatx4* slot, int l
   for (int a = 0; a < NT; ++a) slot[(t++) * 64 + lane] = st.V[a];
 }
 
-// st = sum of the kWaves published states, in wave order.
+// st = sum of the published states of the waves that share this wave's long
+// window (all four, or the pair 2m, 2m + 1), in wave order.
 template <int D>
-__device__ __forceinline__ void combine(State<D>& st, const floatx4* slots, int lane) {
+__device__ __forceinline__ void combine(State<D>& st, const floatx4* slots, int lane, int wv,
+                                        bool pair) {
   constexpr int NT = Geo<D>::NT, KT = kStateTiles<D>;
   st.clear();
-#pragma unroll
-  for (int w = 0; w < kWaves; ++w) {
+  const int w0 = pair ? (wv & ~1) : 0, nw = pair ? 2 : kWaves;
+  for (int w = w0; w < w0 + nw; ++w) {
     const floatx4* sl = slots + w * KT * 64;
     int t = 0;
 #pragma unroll
@@ -1108,7 +1133,7 @@ void k_sla_fwd(KernelArgs a, const T* __restrict__ q, const T* __restrict__ k,
       if (wi.shared) {
         publish<D>(st, s_part + wv * KT * 64, lane);
         lds_barrier();
-        combine<D>(st, s_part, lane);
+        combine<D>(st, s_part, lane, wv, ww.pair);
         lds_barrier();  // the slots may be written by the next long item
       }
       FwdOp<T, D> op;
@@ -1201,7 +1226,7 @@ void k_sla_bwd(KernelArgs a, const T* __restrict__ q, const T* __restrict__ k,
       if (wi.shared) {
         publish<D>(st, s_part[0] + wv * KT * 64, lane);
         lds_barrier();
-        combine<D>(st, s_part[0], lane);
+        combine<D>(st, s_part[0], lane, wv, ww.pair);
       }
       make_state_op<T, D>(st, op, tile, i, g);
       // phase 1: dq and beta dS, beta dz
@@ -1225,7 +1250,7 @@ void k_sla_bwd(KernelArgs a, const T* __restrict__ q, const T* __restrict__ k,
         // this item's set-0 reads ended (sets alternate within every long item)
         publish<D>(st, s_part[1] + wv * KT * 64, lane);
         lds_barrier();
-        combine<D>(st, s_part[1], lane);
+        combine<D>(st, s_part[1], lane, wv, ww.pair);
       }
       make_grad_op<T, D>(st, op.inv_beta, op, tile, i, g);
       // phase 2: dk, dv
@@ -1290,7 +1315,7 @@ constexpr int64_t kRowHeadsPerWorkgroup = 300;
 static int grid_size(const void* kernel, const PlanLayout& lay, int32_t n, int32_t H) {
   const int64_t c = resident_workgroups(kernel);
   const int hw = H < 4 ? H : 4, cpw = 4 / hw, hg = (H + 3) / 4;
-  const int64_t itemsL = (int64_t)((lay.max_long + 7) & ~7) * H;
+  const int64_t itemsL = (int64_t)(((lay.max_long + 7) & ~7) + 8) * H;
   const int64_t itemsC = (int64_t)(lay.max_chunks + cpw - 1) / cpw * hg;
   int64_t k = ((int64_t)n * H + c * kRowHeadsPerWorkgroup / 2) / (c * kRowHeadsPerWorkgroup);
   if (k < 1) k = 1;

@@ -54,6 +54,9 @@ __global__ __launch_bounds__(kBuildThreads) void k_count(const int32_t* __restri
 struct OpSum {
   __device__ int32_t operator()(int32_t a, int32_t b) const { return a + b; }
 };
+struct OpSum64 {
+  __device__ uint64_t operator()(uint64_t a, uint64_t b) const { return a + b; }
+};
 struct OpMax {
   __device__ int32_t operator()(int32_t a, int32_t b) const { return a > b ? a : b; }
 };
@@ -104,15 +107,17 @@ __device__ V block_exscan(V x, V identity, Op op, V* s, V* total) {
 
 // ------------------------------------------------------ chunk / long tables
 // Work tables from the offsets in LDS, in sequence order (pages of P = L/2 rows):
-// a window of more than L rows is "long" and goes to the long-window table; a
-// window of P+1..L rows is a chunk of its own; a window of 1..P rows opens a
-// chunk unless the previous non-empty window is short and starts in the same
-// page.  A chunk runs to the next event (chunk start or long window).  s_aux: LDS
-// scratch of at least W ints.  Every thread of the block calls it; returns the
-// number of chunks and sets *n_long.
+// a window of more than L rows is "long" and goes to the long-window table
+// (four-way ones, of more than 2L rows, first, then two-way ones); a window of
+// P+1..L rows is a chunk of its own; a window of 1..P rows opens a chunk unless
+// the previous non-empty window is short and starts in the same page.  A chunk
+// runs to the next event (chunk start or long window).  s_aux: LDS scratch of at
+// least W ints.  Every thread of the block calls it; returns the number of
+// chunks and sets *n_long and *n_long4.
 __device__ int32_t build_tables(const int32_t* s_off, int32_t* s_aux, int32_t W, int32_t L,
                                 Chunk* __restrict__ chunks, LongWin* __restrict__ longs,
-                                int32_t* s_scan, uint64_t* s_scan2, int32_t* n_long) {
+                                int32_t* s_scan, uint64_t* s_scan2, int32_t* n_long,
+                                int32_t* n_long4) {
   const int tid = threadIdx.x, T = blockDim.x;
   const int32_t page = L >> 1;
   const int P = (W + T - 1) / T;
@@ -132,78 +137,80 @@ __device__ int32_t build_tables(const int32_t* s_off, int32_t* s_aux, int32_t W,
       &tmp);
   const int32_t lastStart = (int32_t)(both >> 32) - 1;
   const int32_t lastWideEnd = (int32_t)(uint32_t)both - 1;
-  // 0: no event, 1: opens a chunk, 2: long window.  ls / ll: start of the previous
-  // non-empty window / end of the previous window of more than P rows (ll == a
-  // exactly when the previous non-empty window is not short).
+  // 0: no event, 1: opens a chunk, 2: two-way long window, 3: four-way long
+  // window.  ls / ll: start of the previous non-empty window / end of the
+  // previous window of more than P rows (ll == a exactly when the previous
+  // non-empty window is not short).
   auto kind = [&](int32_t& ls, int32_t& ll, int w) -> int {
     const int32_t a = s_off[w], len = s_off[w + 1] - a;
     if (len <= 0) return 0;
     int k = 0;
-    if (len > L) k = 2;
+    if (len > L) k = len > 2 * L ? 3 : 2;
     else if (len > page || ls < 0 || ll == a || (ls / page) != (a / page)) k = 1;
     ls = a;
     if (len > page) ll = a + len;
     return k;
   };
-  int32_t cs = 0, cl = 0;
+  uint64_t cnt = 0;   // chunks, two-way, four-way: 21 bits each (W <= 16384)
   {
     int32_t ls = lastStart, ll = lastWideEnd;
     for (int w = w0; w < w1; ++w) {
       const int k = kind(ls, ll, w);
-      cs += k == 1;
-      cl += k == 2;
+      if (k) cnt += 1ull << (21 * (k - 1));
     }
   }
-  // both counts in one scan: chunks in the low 16 bits, long windows above (W <= 16384)
-  int32_t tot = 0;
-  const int32_t ex = block_exscan(cs | (cl << 16), 0, OpSum(), s_scan, &tot);
-  const int32_t s0 = ex & 0xffff, l0 = ex >> 16;
-  const int32_t nC = tot & 0xffff, nL = tot >> 16;
+  uint64_t tot = 0;
+  const uint64_t ex = block_exscan<OpSum64, uint64_t>(cnt, 0ull, OpSum64(), s_scan2, &tot);
+  constexpr uint64_t kMask = (1ull << 21) - 1;
+  const int32_t s0 = (int32_t)(ex & kMask), t0 = (int32_t)((ex >> 21) & kMask),
+                f0 = (int32_t)(ex >> 42);
+  const int32_t nC = (int32_t)(tot & kMask), n2 = (int32_t)((tot >> 21) & kMask),
+                n4 = (int32_t)(tot >> 42);
   {
-    // the event list in sequence order: s_aux[chunk index + long index] = window
-    int32_t ls = lastStart, ll = lastWideEnd, sc = s0, sl = l0;
-    for (int w = w0; w < w1; ++w) {
-      const int k = kind(ls, ll, w);
-      if (k) s_aux[sc + sl] = w;
-      sc += k == 1;
-      sl += k == 2;
-    }
+    // the event list in sequence order: s_aux[event index] = window
+    int32_t ls = lastStart, ll = lastWideEnd, e = s0 + t0 + f0;
+    for (int w = w0; w < w1; ++w)
+      if (kind(ls, ll, w)) s_aux[e++] = w;
   }
   lds_sync();
   {
-    int32_t ls = lastStart, ll = lastWideEnd, sc = s0, sl = l0;
+    int32_t ls = lastStart, ll = lastWideEnd, sc = s0, s2 = t0, s4 = f0;
+    const int32_t nE = nC + n2 + n4;
     for (int w = w0; w < w1; ++w) {
       const int k = kind(ls, ll, w);
       if (k == 1) {
-        const int32_t e = sc + sl;
+        const int32_t e = sc + s2 + s4;
         Chunk ch;
         ch.win_begin = w;
-        ch.win_end = e + 1 < nC + nL ? s_aux[e + 1] : W;
+        ch.win_end = e + 1 < nE ? s_aux[e + 1] : W;
         ch.row_begin = s_off[w];
         ch.row_end = s_off[ch.win_end];
         chunks[sc++] = ch;
-      } else if (k == 2) {
+      } else if (k >= 2) {
         LongWin lw;
         lw.window = w;
         lw.row_begin = s_off[w];
         lw.row_end = s_off[w + 1];
         lw.pad = 0;
-        longs[sl++] = lw;
+        longs[k == 3 ? s4++ : n4 + s2++] = lw;
       }
     }
   }
-  *n_long = nL;
+  *n_long = n2 + n4;
+  *n_long4 = n4;
   return nC;
 }
 
 __device__ void write_header(PlanHeader* hdr, int32_t n, int32_t W, int32_t L, int32_t n_chunks,
-                             int32_t n_long, int32_t csr, int32_t invalid, int32_t* invalid_out) {
+                             int32_t n_long, int32_t n_long4, int32_t csr, int32_t invalid,
+                             int32_t* invalid_out) {
   hdr->magic = kPlanMagic;
   hdr->n = n;
   hdr->num_windows = W;
   hdr->chunk_rows = L;
   hdr->n_chunks = n_chunks;
   hdr->n_long = n_long;
+  hdr->n_long4 = n_long4;
   hdr->csr = csr;
   hdr->invalid = invalid;
   if (invalid_out) *invalid_out = invalid;
@@ -257,9 +264,10 @@ __global__ __launch_bounds__(kBuildThreads) void k_plan(int32_t csr, int32_t W, 
     plan_offsets[w] = s_off[w];
     if (!csr && offsets_io) offsets_io[w] = s_off[w];
   }
-  int32_t n_long = 0;
-  const int32_t n_chunks = build_tables(s_off, s_aux, W, L, chunks, longs, s_scan, s_scan2, &n_long);
-  if (tid == 0) write_header(hdr, n, W, L, n_chunks, n_long, csr, invalid, invalid_out);
+  int32_t n_long = 0, n_long4 = 0;
+  const int32_t n_chunks =
+      build_tables(s_off, s_aux, W, L, chunks, longs, s_scan, s_scan2, &n_long, &n_long4);
+  if (tid == 0) write_header(hdr, n, W, L, n_chunks, n_long, n_long4, csr, invalid, invalid_out);
 }
 
 // --------------------------------------------------------------- k_scatter
@@ -422,9 +430,10 @@ __global__ __launch_bounds__(kBuildThreads) void k_scatter(
         if (offsets_out) offsets_out[W] = total;
       }
       lds_sync();
-      int32_t n_long = 0;
-      const int32_t n_chunks = build_tables(base, hist, W, L, chunks, longs, s_scan, s_scan2, &n_long);
-      if (tid == 0) write_header(hdr, n, W, L, n_chunks, n_long, 0, invalid, invalid_out);
+      int32_t n_long = 0, n_long4 = 0;
+      const int32_t n_chunks =
+          build_tables(base, hist, W, L, chunks, longs, s_scan, s_scan2, &n_long, &n_long4);
+      if (tid == 0) write_header(hdr, n, W, L, n_chunks, n_long, n_long4, 0, invalid, invalid_out);
       return;
     }
     for (int w = w0; w < w1; ++w) {

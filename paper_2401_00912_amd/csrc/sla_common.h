@@ -31,7 +31,8 @@ struct PlanHeader {
   int32_t csr;          // 1: rows already window-sorted (identity permutation)
   int32_t invalid;      // out-of-range ids / CSR violations seen by the builder
   int32_t n_long;       // windows of more than L rows (written by the builder)
-  int32_t pad[8];
+  int32_t n_long4;      // of which more than 2L rows (split four ways; listed first)
+  int32_t pad[7];
 };
 static_assert(sizeof(PlanHeader) == 64, "header is 64 bytes");
 
@@ -43,7 +44,8 @@ struct Chunk {
 };
 
 // One window of more than L rows: its rows are split among the waves of a
-// workgroup, which add their partial states.
+// workgroup (four ways above 2L rows, else two ways), which add their partial
+// states.
 struct LongWin {
   int32_t window, row_begin, row_end, pad;
 };

@@ -237,7 +237,7 @@ def read_plan(plan: Plan):
     raw = plan.buf.cpu().numpy()
     hdr = raw[lay.header: lay.header + 64].view(np.int32)
     header = dict(zip(("magic", "n", "num_windows", "chunk_rows", "n_chunks", "csr", "invalid",
-                       "n_long"), hdr[:8].tolist()))
+                       "n_long", "n_long4"), hdr[:9].tolist()))
     perm = raw[lay.perm: lay.perm + 4 * plan.n].view(np.int32)
     offs = raw[lay.offsets: lay.offsets + 4 * (plan.num_windows + 1)].view(np.int32)
     nc = max(0, min(header["n_chunks"], lay.max_chunks))

@@ -67,8 +67,9 @@ def check_plan(S, plan, ids, W, chunk_rows, offsets_in=None):
         o_ref = offsets_in.astype(np.int64)
         assert np.array_equal(offs.astype(np.int64), o_ref)
         assert header["csr"] == 1
-    ch_ref, lw_ref = oracle.chunk_plan_ref(o_ref, L)
+    ch_ref, lw_ref, n_four = oracle.chunk_plan_ref(o_ref, L)
     assert header["n_chunks"] == len(ch_ref) and header["n_long"] == len(lw_ref)
+    assert header["n_long4"] == n_four
     assert np.array_equal(chunks.astype(np.int64), ch_ref), "chunk table differs"
     assert np.array_equal(longs[:, 0].astype(np.int64), lw_ref), "long-window table differs"
     assert np.array_equal(longs[:, 1].astype(np.int64), o_ref[lw_ref])

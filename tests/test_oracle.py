@@ -51,7 +51,7 @@ def test_segments_vs_enumeration(seed):
 
 
 # ---------------------------------------------------------------- chunk plan
-def _check_plan_invariants(off, L, chunks, longs):
+def _check_plan_invariants(off, L, chunks, longs, n_four):
     off = np.asarray(off)
     nw = len(off) - 1
     page = L // 2
@@ -64,9 +64,12 @@ def _check_plan_invariants(off, L, chunks, longs):
     owner[np.asarray(longs, dtype=np.int64)] += 1
     assert np.array_equal(owner[nonempty], np.ones(nonempty.size, dtype=np.int64))
     assert np.all(owner[lengths == 0] == 0)
-    # long windows: more than L rows, listed in order
+    # long windows: more than L rows; four-way ones (more than 2L rows) first,
+    # then two-way ones, each group in sequence order
     assert all(lengths[w] > L for w in longs)
-    assert list(longs) == sorted(longs)
+    four, two = list(longs[:n_four]), list(longs[n_four:])
+    assert all(lengths[w] > 2 * L for w in four) and all(lengths[w] <= 2 * L for w in two)
+    assert four == sorted(four) and two == sorted(two)
     # chunks: whole windows, in order, disjoint, rows tiled by the long windows
     covered = np.zeros(int(off[-1]), dtype=np.int64)
     for w in longs:
@@ -99,29 +102,31 @@ def test_chunk_plan_invariants(seed, L):
     if seed % 3 == 0:
         lengths = rng.integers(0, 8, size=W)
     off = workloads.offsets_from_lengths(lengths).astype(np.int64)
-    chunks, longs = oracle.chunk_plan_ref(off, L)
-    _check_plan_invariants(off, L, chunks.tolist(), longs.tolist())
+    chunks, longs, n_four = oracle.chunk_plan_ref(off, L)
+    _check_plan_invariants(off, L, chunks.tolist(), longs.tolist(), n_four)
 
 
 def test_chunk_plan_hand_example():
-    # L = 8, pages of 4 rows.  Windows: 3, 0, 2, 5, 1, 1, 0, 2, 9, 4, 0 rows.
+    # L = 8, pages of 4 rows.  Windows: 3, 0, 2, 5, 1, 1, 0, 2, 9, 4, 0, 17 rows.
     # rows:  w0 [0,3)  w1 empty  w2 [3,5)  w3 [5,10) mid  w4 [10,11)  w5 [11,12)
     #        w6 empty  w7 [12,14)  w8 [14,23) long  w9 [23,27)  w10 empty
+    #        w11 [27,44) long
     # w0 opens; w2 starts at row 3 (page 0, same as w0) -> joins; w3 has 5 > 4
     # rows -> alone; w4 follows a mid window -> opens; w5 starts at 11 (page 2,
     # same as w4's 10) -> joins; w7 starts at 12 (page 3) -> opens and ends where
-    # the long window w8 begins; w8 (9 > 8 rows) goes to the long table; w9
-    # follows a long window -> opens and runs to the last window slot.
-    off = workloads.offsets_from_lengths(np.array([3, 0, 2, 5, 1, 1, 0, 2, 9, 4, 0]))
-    chunks, longs = oracle.chunk_plan_ref(off, 8)
+    # the long window w8 begins; w8 (9 rows: more than 8, at most 16) is a two-way
+    # long window; w9 follows a long window -> opens and ends where w11 begins;
+    # w11 (17 > 16 rows) is a four-way long window, listed first.
+    off = workloads.offsets_from_lengths(np.array([3, 0, 2, 5, 1, 1, 0, 2, 9, 4, 0, 17]))
+    chunks, longs, n_four = oracle.chunk_plan_ref(off, 8)
     assert chunks.tolist() == [[0, 5, 0, 3], [5, 10, 3, 4], [10, 12, 4, 7], [12, 14, 7, 8],
                                [23, 27, 9, 11]]
-    assert longs.tolist() == [8]
+    assert longs.tolist() == [11, 8] and n_four == 1
 
 
 def test_chunk_plan_empty():
-    chunks, longs = oracle.chunk_plan_ref(np.zeros(5, dtype=np.int64), 64)
-    assert chunks.shape == (0, 4) and longs.shape == (0,)
+    chunks, longs, n_four = oracle.chunk_plan_ref(np.zeros(5, dtype=np.int64), 64)
+    assert chunks.shape == (0, 4) and longs.shape == (0,) and n_four == 0
 
 
 # ------------------------------------------------------------------ forward pins
