@@ -46,6 +46,9 @@ def parse():
     p.add_argument("--cpu-seconds", type=float, default=12.0)
     p.add_argument("--copy-probe", action="store_true",
                    help="after timing, run plain copies of known size (calibrates PMC byte counters)")
+    p.add_argument("--compare-scatter", action="store_true",
+                   help="instead of the training step: forward time and memory of the chunk-wise path "
+                        "against the naive scatter-based one, as sequence length and window length grow")
     p.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                    help="no GPU work: summarise two rocprofv3 --pmc counter_collection.csv files "
                         "(FETCH_SIZE run, WRITE_SIZE run) of `bench.py --no-graph --copy-probe`")
@@ -154,6 +157,9 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     sla.lib()
+    if args.compare_scatter:
+        print(json.dumps(compare_scatter(torch, sla, workloads, dev)), flush=True)
+        return
 
     cfg = args.config
     training = cfg == 5
@@ -333,6 +339,61 @@ def main():
     if not args.no_cpu:
         out["cpu_baseline"] = cpu_baseline(base, training, args.cpu_seconds)
     print(json.dumps(out), flush=True)
+
+
+def compare_scatter(torch, sla, workloads, dev):
+    """Forward of the chunk-wise path (sla_forward) against the naive scatter-based
+    one (sla_forward_scatter: a cached kv matrix per voxel, summed per window), the
+    comparison of the paper's Fig. 4, on fp16 inputs with H = 4, d = 32:
+      * sequence length: 1, 2, 4 and 8 Waymo-like frames concatenated;
+      * window length: about 131k voxels in equal windows of 16 .. 1024 rows.
+    Each case: median of 20 timed calls (HIP events, inputs resident) after 3
+    warm-up calls; memory = the plan (chunk-wise) or the kv cache (scatter)."""
+    H, d = 4, 32
+
+    def time_call(fn, reps=20):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(reps):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            fn()
+            b.record()
+            torch.cuda.synchronize()
+            ts.append(a.elapsed_time(b) * 1e3)
+        return float(np.median(ts))
+
+    def case(ids, W, label):
+        rng = np.random.default_rng([99, ids.size])
+        n = ids.size
+        q, k, v = (torch.from_numpy(workloads.normal_values(rng, n, H, d, "f16")).to(dev)
+                   for _ in range(3))
+        plan = sla.build_segments(torch.from_numpy(ids).to(dev), num_windows=W)
+        o1, o2 = torch.empty_like(q), torch.empty_like(q)
+        ws = torch.empty(sla.scatter_workspace_bytes(n, H, d), dtype=torch.uint8, device=dev)
+        t_chunk = time_call(lambda: sla.forward(plan, q, k, v, out=o1))
+        t_scat = time_call(lambda: sla.forward_scatter(plan, q, k, v, out=o2, workspace=ws))
+        diff = float((o1.float() - o2.float()).abs().max() / o2.float().abs().max())
+        out = {"case": label, "n": n, "windows": W, "chunkwise_us": t_chunk, "scatter_us": t_scat,
+               "speedup": t_scat / t_chunk, "chunkwise_extra_bytes": sla.plan_bytes(n, W),
+               "scatter_extra_bytes": int(ws.numel()), "max_rel_diff": diff}
+        del ws, q, k, v, o1, o2
+        torch.cuda.synchronize()
+        return out
+
+    rows = []
+    for frames in (1, 2, 4, 8):
+        ids = np.concatenate([workloads.waymo_like_ids(np.random.default_rng([6, 0, f])) +
+                              f * workloads.FRAME_WINDOWS for f in range(frames)]).astype(np.int32)
+        rows.append(case(ids, frames * workloads.FRAME_WINDOWS, f"{frames} frame(s)"))
+    for wlen in (16, 64, 144, 512, 1024):
+        nw = 131072 // wlen
+        ids = workloads.ids_from_lengths(np.full(nw, wlen), np.random.default_rng([7, wlen]))
+        rows.append(case(ids, nw, f"windows of {wlen} rows"))
+    return {"metric": "SLA forward: chunk-wise vs naive scatter-based (time and extra memory)",
+            "dtype": "f16", "heads": H, "head_dim": d, "data": "synthetic", "comparison": rows}
 
 
 def cpu_baseline(base, training, budget_s):

@@ -162,6 +162,27 @@ sla_status_t sla_backward(const void* plan, size_t plan_bytes, int64_t n, int32_
                           const void* k, const void* v, const void* dout, void* dq, void* dk,
                           void* dv, sla_stream_t stream);
 
+/*
+ * The naive scatter-based forward that Sec. 3.2 ("Hardware Efficient
+ * Implementation") contrasts with the chunk-wise kernel, kept as a comparator
+ * for Fig. 4's time-and-memory comparison: the kv matrix phi(k)^T v of every
+ * voxel (with phi(k) as one more column) is cached in `workspace` (fp32,
+ * N x heads x head_dim x (head_dim + 1) floats, caller-owned, 16-byte aligned,
+ * at least sla_scatter_workspace_bytes() bytes), the cached matrices are summed
+ * per window in sorted-row order, and o = phi(q) S / (phi(q) . z) as in
+ * sla_forward.  Same plan, layouts, dtypes and errors as sla_forward, plus
+ * SLA_E_WORKSPACE for a short workspace and SLA_E_UNSUPPORTED for heads x
+ * head_dim above 2048.  All arithmetic is fp32 on the vector
+ * units.  It exists to be measured against sla_forward, not as a fast path.
+ */
+size_t sla_scatter_workspace_bytes(int64_t n, int32_t heads, int32_t head_dim);
+
+sla_status_t sla_forward_scatter(const void* plan, size_t plan_bytes, int64_t n,
+                                 int32_t num_windows, sla_dtype_t dtype, int32_t heads,
+                                 int32_t head_dim, const void* q, const void* k, const void* v,
+                                 void* o, void* workspace, size_t workspace_bytes,
+                                 sla_stream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

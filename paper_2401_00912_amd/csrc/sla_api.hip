@@ -14,11 +14,15 @@ hipError_t launch_forward(const void* plan, int32_t n, int32_t W, int dtype, int
 hipError_t launch_backward(const void* plan, int32_t n, int32_t W, int dtype, int32_t H,
                            int32_t d, const void* q, const void* k, const void* v,
                            const void* dout, void* dq, void* dk, void* dv, hipStream_t stream);
+size_t naive_workspace_bytes(int64_t n, int32_t H, int32_t d);
+hipError_t launch_forward_scatter(const void* plan, int32_t n, int32_t W, int dtype, int32_t H,
+                                  int32_t d, const void* q, const void* k, const void* v,
+                                  void* o, void* workspace, hipStream_t stream);
 }  // namespace sla
 
 namespace {
 
-constexpr int32_t kAbiVersion = 2;
+constexpr int32_t kAbiVersion = 3;
 
 bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
 
@@ -131,4 +135,28 @@ SLA_EXPORT sla_status_t sla_backward(const void* plan, size_t plan_bytes, int64_
   return hip_status(sla::launch_backward(plan, (int32_t)n, num_windows, (int)dtype, heads,
                                          head_dim, q, k, v, dout, dq, dk, dv,
                                          static_cast<hipStream_t>(stream)));
+}
+
+SLA_EXPORT size_t sla_scatter_workspace_bytes(int64_t n, int32_t heads, int32_t head_dim) {
+  if (n < 0 || heads < 1 || (head_dim != 16 && head_dim != 32)) return 0;
+  return sla::naive_workspace_bytes(n, heads, head_dim);
+}
+
+SLA_EXPORT sla_status_t sla_forward_scatter(const void* plan, size_t plan_bytes, int64_t n,
+                                            int32_t num_windows, sla_dtype_t dtype, int32_t heads,
+                                            int32_t head_dim, const void* q, const void* k,
+                                            const void* v, void* o, void* workspace,
+                                            size_t workspace_bytes, sla_stream_t stream) {
+  const sla_status_t st = check_tensor_args(n, num_windows, (int)dtype, heads, head_dim, plan, plan_bytes);
+  if (st != SLA_OK) return st;
+  if ((int64_t)heads * head_dim > 2048) return SLA_E_UNSUPPORTED;   // the kv kernel's LDS rows
+  if (n == 0) return SLA_OK;
+  if (!q || !k || !v || !o || !workspace) return SLA_E_ARG;
+  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(o, 16) ||
+      !aligned(workspace, 16))
+    return SLA_E_ARG;
+  if (workspace_bytes < sla::naive_workspace_bytes(n, heads, head_dim)) return SLA_E_WORKSPACE;
+  return hip_status(sla::launch_forward_scatter(plan, (int32_t)n, num_windows, (int)dtype, heads,
+                                                head_dim, q, k, v, o, workspace,
+                                                static_cast<hipStream_t>(stream)));
 }

@@ -9,6 +9,8 @@ Functions mirror the C ABI in include/sla.h:
     build_segments(ids | offsets, num_windows, chunk_rows=0) -> Plan
     forward(plan, q, k, v, out=None) -> o
     backward(plan, q, k, v, dout, dq=None, dk=None, dv=None) -> (dq, dk, dv)
+    scatter_workspace_bytes(n, heads, head_dim)
+    forward_scatter(plan, q, k, v, out=None, workspace=None) -> o   (naive comparator)
 """
 from __future__ import annotations
 
@@ -30,6 +32,8 @@ EXPORTED = (
     "sla_build_segments",
     "sla_forward",
     "sla_backward",
+    "sla_scatter_workspace_bytes",
+    "sla_forward_scatter",
 )
 
 
@@ -82,6 +86,10 @@ def lib() -> ctypes.CDLL:
     L.sla_forward.argtypes = [vp, sz, i64, i32, ctypes.c_int, i32, i32, vp, vp, vp, vp, vp]
     L.sla_backward.restype = ctypes.c_int
     L.sla_backward.argtypes = [vp, sz, i64, i32, ctypes.c_int, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp]
+    L.sla_scatter_workspace_bytes.restype = sz
+    L.sla_scatter_workspace_bytes.argtypes = [i64, i32, i32]
+    L.sla_forward_scatter.restype = ctypes.c_int
+    L.sla_forward_scatter.argtypes = [vp, sz, i64, i32, ctypes.c_int, i32, i32, vp, vp, vp, vp, vp, sz, vp]
     _lib = L
     return L
 
@@ -226,6 +234,32 @@ def backward(plan: Plan, q, k, v, dout, dq=None, dk=None, dv=None):
                             _stream(q.device))
     _check(st, "sla_backward")
     return dq, dk, dv
+
+
+def scatter_workspace_bytes(n: int, heads: int, head_dim: int) -> int:
+    return int(lib().sla_scatter_workspace_bytes(int(n), int(heads), int(head_dim)))
+
+
+def forward_scatter(plan: Plan, q, k, v, out=None, workspace=None):
+    """The naive scatter-based forward (per-voxel kv cache + per-window sums),
+    the comparator of the chunk-wise sla_forward."""
+    torch = _torch()
+    _check_rows("q", q, plan.n)
+    _check_rows("k", k, plan.n, q)
+    _check_rows("v", v, plan.n, q)
+    if out is None:
+        out = torch.empty_like(q)
+    _check_rows("out", out, plan.n, q)
+    H, d = q.shape[1], q.shape[2]
+    need = scatter_workspace_bytes(plan.n, H, d)
+    if workspace is None:
+        workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=q.device)
+    st = lib().sla_forward_scatter(_ptr(plan.buf), plan.nbytes, plan.n, plan.num_windows,
+                                   _dtype_code(q.dtype), H, d, _ptr(q), _ptr(k), _ptr(v), _ptr(out),
+                                   _ptr(workspace), int(workspace.numel() * workspace.element_size()),
+                                   _stream(q.device))
+    _check(st, "sla_forward_scatter")
+    return out
 
 
 def read_plan(plan: Plan):

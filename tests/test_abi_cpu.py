@@ -46,7 +46,7 @@ def test_only_the_abi_is_exported():
 
 
 def test_queries(L):
-    assert L.sla_abi_version() == 2
+    assert L.sla_abi_version() == 3
     assert L.sla_max_windows() == 16384
     assert L.sla_default_chunk_rows() == 64
     for s in range(5):
@@ -121,3 +121,23 @@ def test_build_argument_errors(L):
     assert b(FAKE + 1, 100, 8, 0, None, None, FAKE, nb) == sla.SLA_E_ARG    # misaligned ids
     assert b(FAKE, 100, 16385, 0, None, None, FAKE, 1 << 30) == sla.SLA_E_UNSUPPORTED
     assert b(FAKE, -5, 8, 0, None, None, FAKE, nb) == sla.SLA_E_ARG
+
+
+def test_scatter_argument_errors(L):
+    nb = sla.plan_bytes(100, 8)
+    need = sla.scatter_workspace_bytes(100, 4, 32)
+    assert need == 100 * 4 * 32 * 33 * 4
+    assert sla.scatter_workspace_bytes(100, 4, 24) == 0
+    assert sla.scatter_workspace_bytes(-1, 4, 32) == 0
+    call = lambda **kw: L.sla_forward_scatter(  # noqa: E731
+        kw.get("plan", FAKE), kw.get("pb", nb), kw.get("n", 100), 8, 1, 4, kw.get("d", 32), FAKE,
+        FAKE, FAKE, FAKE, kw.get("ws", FAKE), kw.get("wsb", need), None)
+    assert call(wsb=need - 1) == sla.SLA_E_WORKSPACE
+    assert call(ws=None) == sla.SLA_E_ARG
+    assert call(ws=FAKE + 4) == sla.SLA_E_ARG
+    assert call(d=24) == sla.SLA_E_UNSUPPORTED
+    assert call(pb=10) == sla.SLA_E_WORKSPACE
+    assert call(n=0) == sla.SLA_OK
+    big = L.sla_forward_scatter(FAKE, sla.plan_bytes(100, 8), 100, 8, 1, 128, 32, FAKE, FAKE, FAKE,
+                                FAKE, FAKE, sla.scatter_workspace_bytes(100, 128, 32), None)
+    assert big == sla.SLA_E_UNSUPPORTED

@@ -335,3 +335,44 @@ def test_backward_determinism(sla):
     torch.cuda.synchronize()
     for a, b in zip(r1, r2):
         assert torch.equal(a, b)
+
+
+# ------------------------------------------------------- naive comparator
+def scatter_parity(S, ids, offsets, n, W, q, k, v, dtype, label=""):
+    import torch
+
+    plan = build(S, ids=ids, W=W, offsets=offsets, n=n)
+    off, perm = check_plan(S, plan, ids, W, 0, offsets)
+    tq, tk, tv = to_dev(q, dtype), to_dev(k, dtype), to_dev(v, dtype)
+    o = torch.full_like(tq, float("nan"))
+    S.forward_scatter(plan, tq, tk, tv, out=o)
+    torch.cuda.synchronize()
+    got = to_host64(o, dtype)
+    w = lambda a: oracle.widen(a, dtype)  # noqa: E731
+    ref = oracle.sla_forward_ref(w(q), w(k), w(v), off, perm)
+    rows = ~np.isnan(ref[:, 0, 0])
+    floor = 1e-3 * max(float(np.abs(w(v)).max()) if v.size else 1.0, 1e-30)
+    err = rel_err_per_head(got, ref, floor, rows)
+    _say(f"[scatter {label}] n={n} W={W} dtype={dtype} rel_err={err:.3e}")
+    assert err <= TOL[dtype], f"{label}: scatter forward relative error {err:.3e}"
+    assert np.isnan(got[~rows]).all(), "rows outside every window were written"
+
+
+@pytest.mark.parametrize("cfg", [1, 2])
+def test_forward_scatter_config(sla, cfg):
+    wl = workloads.make_config(cfg)
+    scatter_parity(sla, wl["ids"], wl["offsets"], wl["n"], wl["num_windows"], wl["q"], wl["k"], wl["v"],
+                   wl["dtype"], label=f"cfg{cfg}")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "f16", "bf16"])
+@pytest.mark.parametrize("shape", [(2, 32), (8, 16), (3, 32)])
+def test_forward_scatter_shapes(sla, dtype, shape):
+    H, d = shape
+    rng = np.random.default_rng([31, H, d, len(dtype)])
+    lengths = _adversarial_lengths(rng, 128)
+    ids = workloads.ids_from_lengths(lengths, rng)
+    ids[rng.random(ids.size) < 0.01] = -1          # rows outside every window stay unwritten
+    n, W = ids.size, lengths.size
+    q, k, v = (workloads.normal_values(rng, n, H, d, dtype) for _ in range(3))
+    scatter_parity(sla, ids, None, n, W, q, k, v, dtype, label=f"shape{shape}")
