@@ -4,9 +4,13 @@ Only the test suite, the smoke check and the benchmark's CPU-baseline leg may us
 this package.  It shares no code with the HIP library and imports nothing from it.
 """
 from .sla_ref import (  # noqa: F401
+    FEATURE_MAPS,
     chunk_plan_ref,
     dphi,
+    dphi_relu,
+    feature_map,
     phi,
+    phi_relu,
     segments_ref,
     sla_backward_ref,
     sla_forward_ref,

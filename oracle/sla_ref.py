@@ -17,7 +17,16 @@ What is computed, and the passage it follows
 * ``phi`` / ``dphi``: the kernel feature map.  Sec. 3.2 (after Eq. (3)) only names
   "the kernel function" and attributes LA to the linear-transformer paper it cites,
   whose feature map is elu(x)+1.  Reading taken: phi(x) = x + 1 for x > 0 and
-  exp(x) otherwise.
+  exp(x) otherwise.  This is ``feature_map="elu1"``, the default.
+* ``phi_relu`` / ``dphi_relu``: the variant of Sec. 4.5 / Tab. 7, which trains
+  the model with other linear-attention designs; its "Efficient Attn" row cites a
+  ReLU-kernel linear attention, whose normaliser carries a small epsilon so that
+  rows with phi(q) . z = 0 stay finite.  Reading taken: phi(x) = max(x, 0),
+  phi'(x) = 1 for x > 0 and 0 otherwise (phi'(0) = 0).  This is
+  ``feature_map="relu"``.
+* ``eps``: Eq. (3) has no epsilon, so the default is 0.  For either map an
+  ``eps >= 0`` may be added to the normaliser, o_i = phi(q_i) S / (phi(q_i) . z +
+  eps); with eps = 0 a zero normaliser gives 0/0 = NaN, which is not masked.
 * ``segments_ref``: Sec. 3.2 orders all voxels of the scene by window so that each
   window is one contiguous sub-matrix of a single flattened matrix.  Read as a
   stable sort of rows by window id plus CSR offsets over the window slots; this
@@ -32,7 +41,7 @@ What is computed, and the passage it follows
   per-window linear attention) and Eq. (3) (per-window normalised linear
   attention), evaluated in the phi(Q)(phi(K)^T V) order of Sec. 3.1.  Non-causal:
   every row of a window sees the whole window (Eq. (3) sums over all m^j rows).
-  No 1/sqrt(d) scale and no epsilon in the denominator (Eq. (3) has neither).
+  No 1/sqrt(d) scale (Eq. (3) has none); epsilon as above.
 * ``sla_backward_ref``: the paper trains the model but does not write the
   backward pass; the gradients here are derived from Eq. (3) by the chain rule
   (derivation in the docstring).
@@ -45,6 +54,10 @@ __all__ = [
     "widen",
     "phi",
     "dphi",
+    "phi_relu",
+    "dphi_relu",
+    "feature_map",
+    "FEATURE_MAPS",
     "segments_ref",
     "chunk_plan_ref",
     "sla_forward_ref",
@@ -80,6 +93,37 @@ def dphi(x: np.ndarray) -> np.ndarray:
     """Derivative of phi: 1 for x > 0, exp(x) for x <= 0 (continuous at 0)."""
     x = np.asarray(x, dtype=np.float64)
     return np.where(x > 0.0, 1.0, np.exp(np.minimum(x, 0.0)))
+
+
+def phi_relu(x: np.ndarray) -> np.ndarray:
+    """ReLU feature map of the Tab. 7 variant: max(x, 0)."""
+    x = np.asarray(x, dtype=np.float64)
+    return np.where(x > 0.0, x, 0.0)
+
+
+def dphi_relu(x: np.ndarray) -> np.ndarray:
+    """Derivative of phi_relu: 1 for x > 0, 0 for x <= 0 (phi'(0) = 0)."""
+    x = np.asarray(x, dtype=np.float64)
+    return np.where(x > 0.0, 1.0, 0.0)
+
+
+FEATURE_MAPS = ("elu1", "relu")
+
+
+def feature_map(name: str):
+    """(phi, phi') of a feature map by name: "elu1" (Sec. 3.2) or "relu" (Tab. 7)."""
+    if name == "elu1":
+        return phi, dphi
+    if name == "relu":
+        return phi_relu, dphi_relu
+    raise ValueError(f"unknown feature map {name!r}")
+
+
+def _check_eps(eps) -> float:
+    eps = float(eps)
+    if not (np.isfinite(eps) and eps >= 0.0):
+        raise ValueError(f"eps must be finite and >= 0, not {eps!r}")
+    return eps
 
 
 # ------------------------------------------------------------------ segment builder
@@ -164,17 +208,20 @@ def _window_rows(offsets, perm, w):
 
 
 # -------------------------------------------------------------------------- forward
-def sla_forward_ref(q, k, v, offsets, perm=None):
+def sla_forward_ref(q, k, v, offsets, perm=None, feature_map_name="elu1", eps=0.0):
     """SLA forward, Eq. (2)-(3), per window and per head.
 
     q, k, v: float64 [n, H, d] in original row order.  offsets: [W + 1] CSR over
     sorted positions; perm: sorted position -> original row (None = identity,
     i.e. rows already window-sorted).  For window w with rows R and each head:
-        S = sum_{j in R} phi(k_j)^T v_j      (d x d)
-        z = sum_{j in R} phi(k_j)            (d)
-        o_i = (phi(q_i) S) / (phi(q_i) . z)  for every i in R.
-    Rows that belong to no window are NaN.
+        S = sum_{j in R} phi(k_j)^T v_j            (d x d)
+        z = sum_{j in R} phi(k_j)                  (d)
+        o_i = (phi(q_i) S) / (phi(q_i) . z + eps)  for every i in R.
+    phi is chosen by ``feature_map_name`` ("elu1" or "relu"); eps >= 0 (0 in
+    Eq. (3)).  Rows that belong to no window are NaN.
     """
+    fphi, _ = feature_map(feature_map_name)
+    eps = _check_eps(eps)
     q = np.asarray(q, dtype=np.float64)
     k = np.asarray(k, dtype=np.float64)
     v = np.asarray(v, dtype=np.float64)
@@ -183,32 +230,35 @@ def sla_forward_ref(q, k, v, offsets, perm=None):
         rows = _window_rows(offsets, perm, w)
         if rows.size == 0:
             continue
-        fq = phi(q[rows])  # [m, H, d]
-        fk = phi(k[rows])
+        fq = fphi(q[rows])  # [m, H, d]
+        fk = fphi(k[rows])
         vv = v[rows]
         S = np.einsum("mhe,mhc->hec", fk, vv)
         z = fk.sum(axis=0)  # [H, d]
         num = np.einsum("mhe,hec->mhc", fq, S)
-        den = np.einsum("mhe,he->mh", fq, z)
+        den = np.einsum("mhe,he->mh", fq, z) + eps
         out[rows] = num / den[:, :, None]
     return out
 
 
 # ------------------------------------------------------------------------- backward
-def sla_backward_ref(q, k, v, dout, offsets, perm=None):
+def sla_backward_ref(q, k, v, dout, offsets, perm=None, feature_map_name="elu1", eps=0.0):
     """Gradients of sum(dout * SLA(q, k, v)) with respect to q, k, v.
 
     Derived from Eq. (3) by the chain rule (the paper does not write them out).
     Per window and head, with fq_i = phi(q_i), fk_j = phi(k_j), S, z as in the
-    forward, den_i = fq_i . z and o_i = fq_i S / den_i:
+    forward, den_i = fq_i . z + eps and o_i = fq_i S / den_i:
         g_i   = dout_i / den_i                      d loss / d num_i
         s_i   = -(dout_i . o_i) / den_i             d loss / d den_i
         dfq_i = g_i S^T + s_i z                     d loss / d phi(q_i)
         dS    = sum_i fq_i^T g_i ,  dz = sum_i s_i fq_i
         dfk_j = v_j dS^T + dz ,     dv_j = fk_j dS
         dq = dfq * phi'(q) ,        dk = dfk * phi'(k)
-    Rows that belong to no window are NaN.
+    (eps is a constant, so it only enters through den.)  Rows that belong to no
+    window are NaN.
     """
+    fphi, fdphi = feature_map(feature_map_name)
+    eps = _check_eps(eps)
     q = np.asarray(q, dtype=np.float64)
     k = np.asarray(k, dtype=np.float64)
     v = np.asarray(v, dtype=np.float64)
@@ -221,10 +271,10 @@ def sla_backward_ref(q, k, v, dout, offsets, perm=None):
         if rows.size == 0:
             continue
         qq, kk, vv, do = q[rows], k[rows], v[rows], dout[rows]
-        fq, fk = phi(qq), phi(kk)
+        fq, fk = fphi(qq), fphi(kk)
         S = np.einsum("mhe,mhc->hec", fk, vv)
         z = fk.sum(axis=0)
-        den = np.einsum("mhe,he->mh", fq, z)
+        den = np.einsum("mhe,he->mh", fq, z) + eps
         o = np.einsum("mhe,hec->mhc", fq, S) / den[:, :, None]
         g = do / den[:, :, None]
         s = -np.einsum("mhc,mhc->mh", do, o) / den
@@ -233,6 +283,6 @@ def sla_backward_ref(q, k, v, dout, offsets, perm=None):
         dz = np.einsum("mh,mhe->he", s, fq)
         dfk = np.einsum("mhc,hec->mhe", vv, dS) + dz[None, :, :]
         dv[rows] = np.einsum("mhe,hec->mhc", fk, dS)
-        dq[rows] = dfq * dphi(qq)
-        dk[rows] = dfk * dphi(kk)
+        dq[rows] = dfq * fdphi(qq)
+        dk[rows] = dfk * fdphi(kk)
     return dq, dk, dv

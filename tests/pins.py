@@ -50,9 +50,14 @@ def _phi_scalar(x: float) -> float:
     return x + 1.0 if x > 0 else math.exp(x)
 
 
-def brute_forward(q, k, v, ids, num_windows):
-    """Quadratic form of Sec. 3.1: o_i = sum_j (phi(q_i).phi(k_j)) v_j / sum_j phi(q_i).phi(k_j),
+def _relu_scalar(x: float) -> float:
+    return x if x > 0 else 0.0
+
+
+def brute_forward(q, k, v, ids, num_windows, fmap="elu1", eps=0.0):
+    """Quadratic form of Sec. 3.1: o_i = sum_j (phi(q_i).phi(k_j)) v_j / (sum_j phi(q_i).phi(k_j) + eps),
     j over the rows with the same window id as i; plain Python loops."""
+    f = _phi_scalar if fmap == "elu1" else _relu_scalar
     n, H, d = q.shape
     out = np.full((n, H, d), np.nan)
     for i in range(n):
@@ -67,17 +72,19 @@ def brute_forward(q, k, v, ids, num_windows):
                     continue
                 a = 0.0
                 for e in range(d):
-                    a += _phi_scalar(q[i, h, e]) * _phi_scalar(k[j, h, e])
+                    a += f(q[i, h, e]) * f(k[j, h, e])
                 den += a
                 for c in range(d):
                     num[c] += a * v[j, h, c]
+            den += eps
             for c in range(d):
-                out[i, h, c] = num[c] / den
+                out[i, h, c] = num[c] / den if den != 0.0 else math.nan
     return out
 
 
-def exact_forward(qf, kf, vf, ids):
-    """Exact rational evaluation for inputs with q, k > 0 (phi(x) = x + 1 exactly)."""
+def exact_forward(qf, kf, vf, ids, shift=1, eps=Fraction(0)):
+    """Exact rational evaluation for inputs with q, k > 0, where phi(x) = x + shift
+    exactly (shift 1: elu + 1; shift 0: ReLU), with eps added to the normaliser."""
     n, H, d = len(qf), len(qf[0]), len(qf[0][0])
     out = np.zeros((n, H, d))
     for i in range(n):
@@ -87,18 +94,25 @@ def exact_forward(qf, kf, vf, ids):
             for j in range(n):
                 if ids[j] != ids[i]:
                     continue
-                a = sum((qf[i][h][e] + 1) * (kf[j][h][e] + 1) for e in range(d))
+                a = sum((qf[i][h][e] + shift) * (kf[j][h][e] + shift) for e in range(d))
                 den += a
                 for c in range(d):
                     num[c] += a * vf[j][h][c]
+            den += eps
             for c in range(d):
                 out[i, h, c] = float(num[c] / den)
     return out
 
 
 def rel_err(x, ref):
+    """max |x - ref| / max |ref| over the entries where ref is a number; inf if
+    x and ref are NaN in different places."""
     x = np.asarray(x, dtype=np.float64)
     ref = np.asarray(ref, dtype=np.float64)
+    if not np.array_equal(np.isnan(x), np.isnan(ref)):
+        return math.inf
+    if np.isnan(ref).all():
+        return 0.0
     scale = max(np.nanmax(np.abs(ref)), 1e-300)
     return float(np.nanmax(np.abs(x - ref)) / scale)
 
@@ -263,4 +277,187 @@ def backward_pin_failures(bwd, fwd, seg):
     a, b, c = bwd(q1, k1, v1, do1, off1, perm1)
     if rel_err(c, do1) > 1e-15 or np.abs(a).max() > 1e-13 or np.abs(b).max() > 1e-13:
         fails.append("singleton_grad")
+    return fails
+
+
+# ------------------------------------------- feature-map variants and epsilon
+# The ReLU feature map of the Tab. 7 variant (phi(x) = max(x, 0), phi'(0) = 0)
+# and an eps >= 0 added to the normaliser, for either map.  ``fwd`` and ``bwd``
+# take (..., offsets, perm, feature_map_name, eps).
+def _away_from_zero(x, gap=1e-3):
+    """Inputs kept at least `gap` from the ReLU kink (finite differences)."""
+    return np.where(np.abs(x) < gap, np.where(x < 0, -gap, gap), x)
+
+
+def variant_forward_pin_failures(fwd, seg):
+    fails = []
+
+    def run(ids, q, k, v, W, fmap, eps):
+        perm, off, _ = seg(ids, W)
+        return fwd(q, k, v, off, perm, fmap, eps)
+
+    # 1. quadratic form (brute force), both maps, with and without eps; with
+    #    eps = 0 some ReLU rows have a zero normaliser and are NaN on both sides
+    for fmap in ("relu", "elu1"):
+        for eps in (0.0, 0.3):
+            for seed in range(3):
+                ids, q, k, v, _ = tiny_case(40 + seed)
+                W = int(ids.max()) + 2
+                with np.errstate(invalid="ignore", divide="ignore"):
+                    got = run(ids, q, k, v, W, fmap, eps)
+                if rel_err(got, brute_forward(q, k, v, ids, W, fmap, eps)) > 1e-12:
+                    fails.append(f"bruteforce_{fmap}_eps{eps}[{seed}]")
+    # 2. exact rationals with positive q, k and eps = 1/4, both maps
+    rng = np.random.default_rng(8)
+    n, H, d = 9, 2, 3
+    ids = rng.integers(0, 3, size=n)
+    qi = rng.integers(1, 17, size=(n, H, d))
+    ki = rng.integers(1, 17, size=(n, H, d))
+    vi = rng.integers(-16, 17, size=(n, H, d))
+    qf = [[[Fraction(int(x), 8) for x in row] for row in r] for r in qi]
+    kf = [[[Fraction(int(x), 8) for x in row] for row in r] for r in ki]
+    vf = [[[Fraction(int(x), 8) for x in row] for row in r] for r in vi]
+    for fmap, shift in (("relu", 0), ("elu1", 1)):
+        exact = exact_forward(qf, kf, vf, ids, shift=shift, eps=Fraction(1, 4))
+        if rel_err(run(ids, qi / 8.0, ki / 8.0, vi / 8.0, 3, fmap, 0.25), exact) > 1e-14:
+            fails.append(f"exact_rational_{fmap}")
+    # 3. for x > 0, relu(x + 1) = elu(x) + 1: the ReLU path on q + 1, k + 1 is the
+    #    elu path on q, k (a cross-check against the pinned default map)
+    ids, q, k, v, _ = tiny_case(45)
+    qp, kp = np.abs(q) + 0.01, np.abs(k) + 0.01
+    W = int(ids.max()) + 1
+    for eps in (0.0, 0.5):
+        if rel_err(run(ids, qp + 1, kp + 1, v, W, "relu", eps), run(ids, qp, kp, v, W, "elu1", eps)) > 1e-14:
+            fails.append(f"relu_shift_is_elu_eps{eps}")
+    # 4. ReLU is positively homogeneous: scaling q (or every k) by t > 0 is the
+    #    same as dividing eps by t
+    ids, q, k, v, _ = tiny_case(46)
+    W = int(ids.max()) + 1
+    t = 2.5
+    base = run(ids, q, k, v, W, "relu", 0.8)
+    if rel_err(run(ids, t * q, k, v, W, "relu", 0.8 * t), base) > 1e-13:
+        fails.append("relu_q_homogeneous")
+    if rel_err(run(ids, q, t * k, v, W, "relu", 0.8 * t), base) > 1e-13:
+        fails.append("relu_k_homogeneous")
+    with np.errstate(invalid="ignore", divide="ignore"):
+        b0 = run(ids, q, k, v, W, "relu", 0.0)
+        if rel_err(run(ids, t * q, k / t, v, W, "relu", 0.0), b0) > 1e-13:
+            fails.append("relu_scale_invariant")
+    # 5. with eps the weights sum to s_i = o_i(v = 1) < 1: o(v + c) = o(v) + s c
+    for fmap in ("relu", "elu1"):
+        b = run(ids, q, k, v, W, fmap, 0.7)
+        s1 = run(ids, q, k, np.ones_like(v), W, fmap, 0.7)
+        c = np.linspace(-2, 2, v.shape[1] * v.shape[2]).reshape(v.shape[1:])
+        if rel_err(run(ids, q, k, v + c, W, fmap, 0.7), b + s1 * c) > 1e-13:
+            fails.append(f"affine_eps_{fmap}")
+        if not (np.all(s1 < 1.0) and np.all(s1 >= 0.0) and np.ptp(s1, axis=2).max() < 1e-14):
+            fails.append(f"weight_sum_eps_{fmap}")
+    # 6. ReLU zero cases with eps > 0: a query with no positive entry, and a
+    #    window whose keys have none, give o = 0 exactly (NaN when eps = 0)
+    ids = np.array([0, 0, 0, 1, 1])
+    rng = np.random.default_rng(9)
+    q, k, v = (rng.standard_normal((5, 1, 3)) for _ in range(3))
+    q[1] = -np.abs(q[1])
+    k[3:] = -np.abs(k[3:]) - 0.1
+    q[[0, 2, 3, 4]] = np.abs(q[[0, 2, 3, 4]]) + 0.1
+    k[:3] = np.abs(k[:3]) + 0.1
+    o = run(ids, q, k, v, 2, "relu", 0.25)
+    if not (np.all(o[1] == 0.0) and np.all(o[3:] == 0.0) and np.all(o[[0, 2]] != 0.0)):
+        fails.append("relu_zero_rows")
+    with np.errstate(invalid="ignore", divide="ignore"):
+        o0 = run(ids, q, k, v, 2, "relu", 0.0)
+    if not (np.isnan(o0[[1, 3, 4]]).all() and np.isfinite(o0[[0, 2]]).all()):
+        fails.append("relu_zero_rows_eps0_nan")
+    return fails
+
+
+def _loss_v(fwd, seg, ids, W, q, k, v, do, fmap, eps):
+    perm, off, _ = seg(ids, W)
+    return float(np.nansum(fwd(q, k, v, off, perm, fmap, eps) * do))
+
+
+def variant_backward_pin_failures(bwd, fwd, seg):
+    fails = []
+    # 1. central finite differences, both maps, eps = 0.3, inputs away from the kink
+    for fmap in ("relu", "elu1"):
+        ids, q, k, v, do = tiny_case(50, windows=3, max_len=5, d=3)
+        q, k = _away_from_zero(q), _away_from_zero(k)
+        W = 3
+        perm, off, _ = seg(ids, W)
+        grads = bwd(q, k, v, do, off, perm, fmap, 0.3)
+        h = 1e-6
+        for pos, name in enumerate(("dq", "dk", "dv")):
+            x = (q, k, v)[pos]
+            num = np.zeros_like(x)
+            for idx in np.ndindex(x.shape):
+                args_p, args_m = [q, k, v], [q, k, v]
+                xp, xm = x.copy(), x.copy()
+                xp[idx] += h
+                xm[idx] -= h
+                args_p[pos], args_m[pos] = xp, xm
+                num[idx] = (_loss_v(fwd, seg, ids, W, *args_p, do, fmap, 0.3)
+                            - _loss_v(fwd, seg, ids, W, *args_m, do, fmap, 0.3)) / (2 * h)
+            if rel_err(grads[pos], num) > 1e-6:
+                fails.append(f"finite_difference_{fmap}_{name}")
+    # 2. sum of dv over a window = sum_i s_i dout_i, s_i = o_i(v = 1)
+    ids, q, k, v, do = tiny_case(51, windows=4, max_len=8, d=4)
+    W = 4
+    perm, off, _ = seg(ids, W)
+    for fmap in ("relu", "elu1"):
+        _, _, dv = bwd(q, k, v, do, off, perm, fmap, 0.6)
+        s1 = fwd(q, k, np.ones_like(v), off, perm, fmap, 0.6)[:, :, :1]
+        for w in range(W):
+            rows = ids == w
+            if rows.any() and rel_err(dv[rows].sum(0), (s1[rows] * do[rows]).sum(0)) > 1e-12:
+                fails.append(f"sum_dv_eps_{fmap}")
+                break
+    # 3. ReLU, eps = 0, every normaliser positive: o is invariant to scaling one
+    #    query row, and to scaling every key of a window, so q . dq = 0 per row
+    #    and head, and sum_window k . dk = 0 per head (Euler)
+    ids, q, k, v, do = tiny_case(52, windows=4, max_len=8, d=4)
+    q[:, :, 0] = np.abs(q[:, :, 0]) + 0.1
+    k[:, :, 0] = np.abs(k[:, :, 0]) + 0.1
+    perm, off, _ = seg(ids, W)
+    dq, dk, _ = bwd(q, k, v, do, off, perm, "relu", 0.0)
+    scale = max(1.0, np.abs(dq).max(), np.abs(dk).max())
+    if np.abs((q * dq).sum(axis=2)).max() > 1e-12 * scale:
+        fails.append("relu_euler_q")
+    for w in range(W):
+        rows = ids == w
+        if rows.any() and np.abs((k[rows] * dk[rows]).sum(axis=(0, 2))).max() > 1e-12 * scale:
+            fails.append("relu_euler_k")
+            break
+    # 4. with eps > 0 the same scalings act as eps -> eps / t, so
+    #    sum q . dq = sum k . dk = -eps dL/deps (dL/deps by finite differences)
+    eps, h = 0.4, 1e-6
+    dq, dk, _ = bwd(q, k, v, do, off, perm, "relu", eps)
+    dl = (_loss_v(fwd, seg, ids, W, q, k, v, do, "relu", eps + h)
+          - _loss_v(fwd, seg, ids, W, q, k, v, do, "relu", eps - h)) / (2 * h)
+    if abs((q * dq).sum() + eps * dl) > 1e-7 * max(1.0, abs(eps * dl)):
+        fails.append("relu_euler_q_eps")
+    if abs((k * dk).sum() + eps * dl) > 1e-7 * max(1.0, abs(eps * dl)):
+        fails.append("relu_euler_k_eps")
+    # 5. phi'(0) = 0: entries at or below zero get no gradient under ReLU
+    ids, q, k, v, do = tiny_case(53, windows=3, max_len=6, d=4)
+    q[::2, :, 1] = 0.0
+    k[1::3, :, 2] = 0.0
+    W = 3
+    perm, off, _ = seg(ids, W)
+    dq, dk, _ = bwd(q, k, v, do, off, perm, "relu", 0.3)
+    if np.any(dq[q <= 0] != 0.0) or np.any(dk[k <= 0] != 0.0):
+        fails.append("relu_dphi_at_zero")
+    # (not vacuous: most positive entries do get a gradient; a feature e with
+    # z_e = 0 in its window legitimately gets none, as then S[e, :] = 0 too)
+    if (np.count_nonzero(dq[q > 0]) < 0.6 * np.count_nonzero(q > 0)
+            or np.count_nonzero(dk[k > 0]) < 0.6 * np.count_nonzero(k > 0)):
+        fails.append("relu_gradient_vanishes")
+    # 6. relu(x + 1) = elu(x) + 1 for x > 0: gradients agree as well
+    ids, q, k, v, do = tiny_case(54, windows=3, max_len=6, d=4)
+    qp, kp = np.abs(q) + 0.01, np.abs(k) + 0.01
+    perm, off, _ = seg(ids, W)
+    for eps in (0.0, 0.5):
+        a = bwd(qp + 1, kp + 1, v, do, off, perm, "relu", eps)
+        b = bwd(qp, kp, v, do, off, perm, "elu1", eps)
+        if max(rel_err(x, y) for x, y in zip(a, b)) > 1e-13:
+            fails.append(f"relu_shift_is_elu_grad_eps{eps}")
     return fails

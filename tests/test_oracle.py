@@ -2,6 +2,7 @@
 plausible mistake planted in a copy of the oracle fails at least one pin."""
 import importlib.util
 import os
+import types
 
 import numpy as np
 import pytest
@@ -248,3 +249,95 @@ def test_segments_mutant_is_caught():
     p1, _, _ = unstable(ids, 5)
     p2, _ = pins.segments_plain(ids, 5)
     assert not np.array_equal(p1, p2)
+
+
+# ------------------------------------------- feature-map variants and epsilon
+def test_phi_relu_values():
+    x = np.array([-2.0, -0.0, 0.0, 1e-300, 3.5])
+    assert oracle.phi_relu(x).tolist() == [0.0, 0.0, 0.0, 1e-300, 3.5]
+    assert oracle.dphi_relu(x).tolist() == [0.0, 0.0, 0.0, 1.0, 1.0]
+    with pytest.raises(ValueError):
+        oracle.feature_map("gelu")
+    with pytest.raises(ValueError):
+        oracle.sla_forward_ref(np.ones((1, 1, 1)), np.ones((1, 1, 1)), np.ones((1, 1, 1)),
+                               np.array([0, 1]), None, "relu", -1e-9)
+
+
+def test_variant_forward_pins():
+    assert pins.variant_forward_pin_failures(oracle.sla_forward_ref, oracle.segments_ref) == []
+
+
+def test_variant_backward_pins():
+    assert pins.variant_backward_pin_failures(oracle.sla_backward_ref, oracle.sla_forward_ref,
+                                              oracle.segments_ref) == []
+
+
+def test_default_map_and_eps_unchanged():
+    # the default call is Eq. (3) as before: elu + 1 and no epsilon
+    ids, q, k, v, do = pins.tiny_case(60)
+    perm, off, _ = oracle.segments_ref(ids, int(ids.max()) + 1)
+    assert np.array_equal(oracle.sla_forward_ref(q, k, v, off, perm),
+                          oracle.sla_forward_ref(q, k, v, off, perm, "elu1", 0.0))
+    a = oracle.sla_backward_ref(q, k, v, do, off, perm)
+    b = oracle.sla_backward_ref(q, k, v, do, off, perm, "elu1", 0.0)
+    assert all(np.array_equal(x, y) for x, y in zip(a, b))
+
+
+def _oracle_from_source(replacements):
+    """A copy of the oracle module with source edits: (old, new, occurrence), the
+    occurrence index counting from 0, or None for every occurrence."""
+    path = os.path.join(os.path.dirname(sla_ref.__file__), "sla_ref.py")
+    src = open(path).read()
+    for old, new, which in replacements:
+        count = src.count(old)
+        assert count > 0 and (which is None or which < count), f"mutation site {old!r} not found"
+        if which is None:
+            src = src.replace(old, new)
+        else:
+            at = -1
+            for _ in range(which + 1):
+                at = src.index(old, at + 1)
+            src = src[:at] + new + src[at + len(old):]
+    mod = types.ModuleType("sla_ref_mutant")
+    exec(compile(src, path, "exec"), mod.__dict__)
+    return mod
+
+
+_DEN = 'den = np.einsum("mhe,he->mh", fq, z) + eps'
+VARIANT_FWD_MUTANTS = {
+    "eps_dropped": [(_DEN, 'den = np.einsum("mhe,he->mh", fq, z)', 0)],
+    "eps_in_numerator": [('num = np.einsum("mhe,hec->mhc", fq, S)',
+                          'num = np.einsum("mhe,hec->mhc", fq, S) + eps', 0)],
+    "eps_scales_normaliser": [(_DEN, 'den = np.einsum("mhe,he->mh", fq, z) * (1.0 + eps)', 0)],
+    "eps_squared": [(_DEN, 'den = np.einsum("mhe,he->mh", fq, z) + eps * eps', 0)],
+    "relu_leaky": [("return np.where(x > 0.0, x, 0.0)", "return np.where(x > 0.0, x, 0.01 * x)", 0)],
+    "relu_offset": [("return np.where(x > 0.0, x, 0.0)", "return np.where(x > 0.0, x + 1e-9, 0.0)", 0)],
+    "relu_is_elu": [("return phi_relu, dphi_relu", "return phi, dphi", 0)],
+}
+
+VARIANT_BWD_MUTANTS = {
+    "bwd_eps_dropped": [(_DEN, 'den = np.einsum("mhe,he->mh", fq, z)', 1)],
+    "relu_dphi_one_at_zero": [("return np.where(x > 0.0, 1.0, 0.0)", "return np.where(x >= 0.0, 1.0, 0.0)", 0)],
+    "relu_dphi_ones": [("return np.where(x > 0.0, 1.0, 0.0)", "return np.where(x > 0.0, 1.0, 1.0)", 0)],
+    "relu_dq_elu_derivative": [("dq[rows] = dfq * fdphi(qq)", "dq[rows] = dfq * dphi(qq)", 0)],
+    "relu_dk_elu_derivative": [("dk[rows] = dfk * fdphi(kk)", "dk[rows] = dfk * dphi(kk)", 0)],
+    "bwd_eps_in_s_only": [('s = -np.einsum("mhc,mhc->mh", do, o) / den',
+                           's = -np.einsum("mhc,mhc->mh", do, o) / (den - eps)', 0)],
+}
+
+
+@pytest.mark.parametrize("name", sorted(VARIANT_FWD_MUTANTS))
+def test_variant_forward_mutant_is_caught(name):
+    mod = _oracle_from_source(VARIANT_FWD_MUTANTS[name])
+    with np.errstate(all="ignore"):
+        fails = pins.variant_forward_pin_failures(mod.sla_forward_ref, oracle.segments_ref)
+    assert fails, f"planted mistake {name} passed every variant forward pin"
+
+
+@pytest.mark.parametrize("name", sorted(VARIANT_BWD_MUTANTS))
+def test_variant_backward_mutant_is_caught(name):
+    mod = _oracle_from_source(VARIANT_BWD_MUTANTS[name])
+    with np.errstate(all="ignore"):
+        fails = pins.variant_backward_pin_failures(mod.sla_backward_ref, oracle.sla_forward_ref,
+                                                   oracle.segments_ref)
+    assert fails, f"planted mistake {name} passed every variant backward pin"
