@@ -42,6 +42,9 @@ def parse():
     p.add_argument("--config", type=int, default=5, choices=[1, 2, 3, 4, 5])
     p.add_argument("--chunk-rows", type=int, default=0)
     p.add_argument("--no-graph", action="store_true", help="time eager launches instead of graph replay")
+    p.add_argument("--feature-map", choices=["elu1", "relu"], default=None,
+                   help="time the sla_forward_ex / sla_backward_ex variant with this feature map")
+    p.add_argument("--eps", type=float, default=None, help="epsilon of the normaliser (with --feature-map)")
     p.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     p.add_argument("--cpu-seconds", type=float, default=12.0)
     p.add_argument("--copy-probe", action="store_true",
@@ -146,7 +149,7 @@ def main():
         return
     if args.gpus != 1:
         print(f"bench.py: this build measures one GPU only (asked for --gpus {args.gpus}); "
-              "SLA shards by window ranges with no exchange, see DESIGN.md", file=sys.stderr)
+              "SLA would shard by contiguous window ranges with no exchange between GPUs", file=sys.stderr)
         sys.exit(2)
     import torch
 
@@ -163,6 +166,9 @@ def main():
 
     cfg = args.config
     training = cfg == 5
+    variant = None
+    if args.feature_map is not None or args.eps is not None:
+        variant = (args.feature_map or "elu1", 0.0 if args.eps is None else args.eps)
     base = workloads.make_config(cfg, with_grad=training)
     n, H, d, W, dt = base["n"], base["heads"], base["head_dim"], base["num_windows"], base["dtype"]
     e = elem_size(dt)
@@ -217,11 +223,12 @@ def main():
             plan = plans[i % nsets]
         if ev is not None:
             ev[1].record()
-        sla.forward(plan, st["q"], st["k"], st["v"], out=st["o"])
+        sla.forward(plan, st["q"], st["k"], st["v"], out=st["o"], feature_map=args.feature_map, eps=args.eps)
         if ev is not None:
             ev[2].record()
         if training:
-            sla.backward(plan, st["q"], st["k"], st["v"], st["dout"], st["dq"], st["dk"], st["dv"])
+            sla.backward(plan, st["q"], st["k"], st["v"], st["dout"], st["dq"], st["dk"], st["dv"],
+                         feature_map=args.feature_map, eps=args.eps)
         if ev is not None:
             ev[3].record()
 
@@ -329,15 +336,18 @@ def main():
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": achieved / HBM_PEAK_GBS,
-            "traffic": stored_traffic(dom),
+            # the stored counters were taken for the default feature map
+            "traffic": stored_traffic(dom) if variant is None else None,
             "algorithmic_bytes": dom_bytes,
             "avg_ms": dom_ms,
         },
         "breakdown_ms": {"build": t_build, "forward": t_fwd, "backward": t_bwd},
         "step_roofline_frac": step_bytes / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS,
     }
+    if variant is not None:
+        out["config"]["feature_map"], out["config"]["eps"] = variant
     if not args.no_cpu:
-        out["cpu_baseline"] = cpu_baseline(base, training, args.cpu_seconds)
+        out["cpu_baseline"] = cpu_baseline(base, training, args.cpu_seconds, variant)
     print(json.dumps(out), flush=True)
 
 
@@ -396,7 +406,7 @@ def compare_scatter(torch, sla, workloads, dev):
             "dtype": "f16", "heads": H, "head_dim": d, "data": "synthetic", "comparison": rows}
 
 
-def cpu_baseline(base, training, budget_s):
+def cpu_baseline(base, training, budget_s, variant=None):
     """The CPU oracle as it stands, on whole frames of the same workload."""
     import oracle
 
@@ -413,9 +423,10 @@ def cpu_baseline(base, training, budget_s):
             perm, off, _ = oracle.segments_ref(base["ids"], base["num_windows"])
         else:
             perm, off = None, base["offsets"].astype(np.int64)
-        oracle.sla_forward_ref(q, k, v, off, perm)
+        extra = () if variant is None else variant
+        oracle.sla_forward_ref(q, k, v, off, perm, *extra)
         if training:
-            oracle.sla_backward_ref(q, k, v, do, off, perm)
+            oracle.sla_backward_ref(q, k, v, do, off, perm, *extra)
 
     ctx = threadpool_limits(limits=1) if threadpool_limits else None
     if ctx:

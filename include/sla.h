@@ -15,7 +15,8 @@
  *   phi(x) = elu(x) + 1 (x + 1 for x > 0, exp(x) otherwise): the feature map of
  *     the linear-attention paper Sec. 3.2 cites for LA;
  *   attention is non-causal inside a window (Eq. (3) sums over the whole window);
- *   no 1/sqrt(d) scale and no epsilon in the denominator (Eq. (3) has neither);
+ *   no 1/sqrt(d) scale and no epsilon in the denominator (Eq. (3) has neither;
+ *     sla_forward_ex / sla_backward_ex add an epsilon and a ReLU feature map);
  *   heads are independent; channel c of a row is head c / head_dim.
  *
  * Conventions shared by every entry point:
@@ -54,6 +55,12 @@ typedef enum {
 } sla_status_t;
 
 typedef enum { SLA_F32 = 0, SLA_F16 = 1, SLA_BF16 = 2 } sla_dtype_t;
+
+/* Kernel feature map phi of Eq. (3) (sla_forward_ex / sla_backward_ex). */
+typedef enum {
+  SLA_PHI_ELU1 = 0,  /* elu(x) + 1: x + 1 for x > 0, exp(x) otherwise (the default)     */
+  SLA_PHI_RELU = 1   /* max(x, 0), derivative 1 for x > 0 and 0 otherwise (phi'(0) = 0) */
+} sla_feature_map_t;
 
 typedef void* sla_stream_t; /* hipStream_t */
 
@@ -161,6 +168,33 @@ sla_status_t sla_backward(const void* plan, size_t plan_bytes, int64_t n, int32_
                           sla_dtype_t dtype, int32_t heads, int32_t head_dim, const void* q,
                           const void* k, const void* v, const void* dout, void* dq, void* dk,
                           void* dv, sla_stream_t stream);
+
+/*
+ * Linear-attention variants (Sec. 4.5 / Tab. 7 trains the model with other
+ * linear-attention designs; its "Efficient Attn" row is ReLU-kernel linear
+ * attention, whose normaliser carries a small epsilon): forward and backward as
+ * above with the feature map chosen by `feature_map` and eps added to the
+ * normaliser,
+ *     o_i = phi(q_i) S / (phi(q_i) . z + eps).
+ * sla_forward / sla_backward are these calls with SLA_PHI_ELU1 and eps = 0.
+ * eps must be finite and >= 0 and feature_map one of the enum values, else
+ * SLA_E_ARG.  With eps = 0 a zero normaliser (under ReLU: a query row with no
+ * positive entry, or one whose positive features are all absent from the
+ * window's keys) gives 0/0 = NaN in that row's output, and in the backward NaN
+ * in the gradients of that row and of its window's keys and values; with
+ * eps > 0 such a row's output is 0.  phi and eps are applied in fp32; the
+ * operands of the matrix cores are as in sla_forward.
+ */
+sla_status_t sla_forward_ex(const void* plan, size_t plan_bytes, int64_t n, int32_t num_windows,
+                            sla_dtype_t dtype, int32_t heads, int32_t head_dim,
+                            sla_feature_map_t feature_map, float eps, const void* q,
+                            const void* k, const void* v, void* o, sla_stream_t stream);
+
+sla_status_t sla_backward_ex(const void* plan, size_t plan_bytes, int64_t n, int32_t num_windows,
+                             sla_dtype_t dtype, int32_t heads, int32_t head_dim,
+                             sla_feature_map_t feature_map, float eps, const void* q,
+                             const void* k, const void* v, const void* dout, void* dq, void* dk,
+                             void* dv, sla_stream_t stream);
 
 /*
  * The naive scatter-based forward that Sec. 3.2 ("Hardware Efficient

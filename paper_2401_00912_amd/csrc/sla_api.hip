@@ -9,10 +9,10 @@ namespace sla {
 hipError_t launch_build(const int32_t* ids, int32_t n, int32_t W, int32_t L, int32_t* perm_out,
                         int32_t* offsets_io, int32_t* invalid_out, void* plan, hipStream_t stream);
 hipError_t launch_forward(const void* plan, int32_t n, int32_t W, int dtype, int32_t H, int32_t d,
-                          const void* q, const void* k, const void* v, void* o,
+                          int phi, float eps, const void* q, const void* k, const void* v, void* o,
                           hipStream_t stream);
-hipError_t launch_backward(const void* plan, int32_t n, int32_t W, int dtype, int32_t H,
-                           int32_t d, const void* q, const void* k, const void* v,
+hipError_t launch_backward(const void* plan, int32_t n, int32_t W, int dtype, int32_t H, int32_t d,
+                           int phi, float eps, const void* q, const void* k, const void* v,
                            const void* dout, void* dq, void* dk, void* dv, hipStream_t stream);
 size_t naive_workspace_bytes(int64_t n, int32_t H, int32_t d);
 hipError_t launch_forward_scatter(const void* plan, int32_t n, int32_t W, int dtype, int32_t H,
@@ -22,7 +22,7 @@ hipError_t launch_forward_scatter(const void* plan, int32_t n, int32_t W, int dt
 
 namespace {
 
-constexpr int32_t kAbiVersion = 3;
+constexpr int32_t kAbiVersion = 4;
 
 bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
 
@@ -45,6 +45,42 @@ sla_status_t check_tensor_args(int64_t n, int32_t W, int dtype, int32_t heads, i
 }
 
 sla_status_t hip_status(hipError_t e) { return e == hipSuccess ? SLA_OK : SLA_E_HIP; }
+
+// feature map known, eps finite and >= 0 (NaN fails both comparisons)
+bool variant_ok(int phi, float eps) {
+  return (phi == SLA_PHI_ELU1 || phi == SLA_PHI_RELU) && eps >= 0.f && eps <= 3.0e38f;
+}
+
+sla_status_t forward_impl(const void* plan, size_t plan_bytes, int64_t n, int32_t num_windows,
+                          sla_dtype_t dtype, int32_t heads, int32_t head_dim, int phi, float eps,
+                          const void* q, const void* k, const void* v, void* o,
+                          sla_stream_t stream) {
+  const sla_status_t st = check_tensor_args(n, num_windows, (int)dtype, heads, head_dim, plan, plan_bytes);
+  if (st != SLA_OK) return st;
+  if (!variant_ok(phi, eps)) return SLA_E_ARG;
+  if (n == 0) return SLA_OK;
+  if (!q || !k || !v || !o) return SLA_E_ARG;
+  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(o, 16)) return SLA_E_ARG;
+  return hip_status(sla::launch_forward(plan, (int32_t)n, num_windows, (int)dtype, heads, head_dim,
+                                        phi, eps, q, k, v, o, static_cast<hipStream_t>(stream)));
+}
+
+sla_status_t backward_impl(const void* plan, size_t plan_bytes, int64_t n, int32_t num_windows,
+                           sla_dtype_t dtype, int32_t heads, int32_t head_dim, int phi, float eps,
+                           const void* q, const void* k, const void* v, const void* dout,
+                           void* dq, void* dk, void* dv, sla_stream_t stream) {
+  const sla_status_t st = check_tensor_args(n, num_windows, (int)dtype, heads, head_dim, plan, plan_bytes);
+  if (st != SLA_OK) return st;
+  if (!variant_ok(phi, eps)) return SLA_E_ARG;
+  if (n == 0) return SLA_OK;
+  if (!q || !k || !v || !dout || !dq || !dk || !dv) return SLA_E_ARG;
+  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(dout, 16) ||
+      !aligned(dq, 16) || !aligned(dk, 16) || !aligned(dv, 16))
+    return SLA_E_ARG;
+  return hip_status(sla::launch_backward(plan, (int32_t)n, num_windows, (int)dtype, heads,
+                                         head_dim, phi, eps, q, k, v, dout, dq, dk, dv,
+                                         static_cast<hipStream_t>(stream)));
+}
 
 }  // namespace
 
@@ -111,13 +147,8 @@ SLA_EXPORT sla_status_t sla_forward(const void* plan, size_t plan_bytes, int64_t
                                     int32_t num_windows, sla_dtype_t dtype, int32_t heads,
                                     int32_t head_dim, const void* q, const void* k, const void* v,
                                     void* o, sla_stream_t stream) {
-  const sla_status_t st = check_tensor_args(n, num_windows, (int)dtype, heads, head_dim, plan, plan_bytes);
-  if (st != SLA_OK) return st;
-  if (n == 0) return SLA_OK;
-  if (!q || !k || !v || !o) return SLA_E_ARG;
-  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(o, 16)) return SLA_E_ARG;
-  return hip_status(sla::launch_forward(plan, (int32_t)n, num_windows, (int)dtype, heads, head_dim,
-                                        q, k, v, o, static_cast<hipStream_t>(stream)));
+  return forward_impl(plan, plan_bytes, n, num_windows, dtype, heads, head_dim, SLA_PHI_ELU1, 0.f,
+                      q, k, v, o, stream);
 }
 
 SLA_EXPORT sla_status_t sla_backward(const void* plan, size_t plan_bytes, int64_t n,
@@ -125,16 +156,27 @@ SLA_EXPORT sla_status_t sla_backward(const void* plan, size_t plan_bytes, int64_
                                      int32_t head_dim, const void* q, const void* k,
                                      const void* v, const void* dout, void* dq, void* dk, void* dv,
                                      sla_stream_t stream) {
-  const sla_status_t st = check_tensor_args(n, num_windows, (int)dtype, heads, head_dim, plan, plan_bytes);
-  if (st != SLA_OK) return st;
-  if (n == 0) return SLA_OK;
-  if (!q || !k || !v || !dout || !dq || !dk || !dv) return SLA_E_ARG;
-  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(dout, 16) ||
-      !aligned(dq, 16) || !aligned(dk, 16) || !aligned(dv, 16))
-    return SLA_E_ARG;
-  return hip_status(sla::launch_backward(plan, (int32_t)n, num_windows, (int)dtype, heads,
-                                         head_dim, q, k, v, dout, dq, dk, dv,
-                                         static_cast<hipStream_t>(stream)));
+  return backward_impl(plan, plan_bytes, n, num_windows, dtype, heads, head_dim, SLA_PHI_ELU1,
+                       0.f, q, k, v, dout, dq, dk, dv, stream);
+}
+
+SLA_EXPORT sla_status_t sla_forward_ex(const void* plan, size_t plan_bytes, int64_t n,
+                                       int32_t num_windows, sla_dtype_t dtype, int32_t heads,
+                                       int32_t head_dim, sla_feature_map_t feature_map, float eps,
+                                       const void* q, const void* k, const void* v, void* o,
+                                       sla_stream_t stream) {
+  return forward_impl(plan, plan_bytes, n, num_windows, dtype, heads, head_dim, (int)feature_map,
+                      eps, q, k, v, o, stream);
+}
+
+SLA_EXPORT sla_status_t sla_backward_ex(const void* plan, size_t plan_bytes, int64_t n,
+                                        int32_t num_windows, sla_dtype_t dtype, int32_t heads,
+                                        int32_t head_dim, sla_feature_map_t feature_map,
+                                        float eps, const void* q, const void* k, const void* v,
+                                        const void* dout, void* dq, void* dk, void* dv,
+                                        sla_stream_t stream) {
+  return backward_impl(plan, plan_bytes, n, num_windows, dtype, heads, head_dim, (int)feature_map,
+                       eps, q, k, v, dout, dq, dk, dv, stream);
 }
 
 SLA_EXPORT size_t sla_scatter_workspace_bytes(int64_t n, int32_t heads, int32_t head_dim) {

@@ -37,6 +37,11 @@
 // the matrix core (exact) gives lane (i, g) rows 4g..4g+3 of column i, and two
 // sub-tiles give the 8 rows.
 //
+// Feature maps (template parameter PHI): elu(x) + 1 (Eq. (3) as read from the
+// linear-transformer paper that Sec. 3.2 cites), or ReLU with phi'(0) = 0 (the
+// "Efficient Attn" variant of Sec. 4.5 / Tab. 7).  Either may add eps >= 0 to the
+// normaliser: o = phi(q) S / (phi(q) . z + eps).
+//
 // 16-bit storage: matrix-core operands are the stored values or values rounded to
 // the storage type.  Derived operands are scaled by a power of two into [1, 2)
 // (S, dS) or to at most 1 (phi(q)/den) before rounding and the scale is divided
@@ -50,6 +55,9 @@ constexpr int kWaves = 4;       // waves (heads) per workgroup
 constexpr int kSliceRows = 32;  // rows per job
 
 constexpr float kLog2e = 1.4426950408889634f;
+
+constexpr int kPhiElu1 = 0;  // phi(x) = elu(x) + 1
+constexpr int kPhiRelu = 1;  // phi(x) = max(x, 0), phi'(0) = 0
 
 // phi(x) = x + 1 for x > 0, exp(x) otherwise, and its derivative.  With 16-bit
 // storage the result is rounded to 16 bits for the matrix cores, so the
@@ -83,16 +91,17 @@ __device__ __forceinline__ float recip(float x) {
   }
 }
 
-// Power of two p with x * p in [1, 2) (1 for x = 0 or non-finite x).
+// Power of two p with x * p in [1, 2) (1 for x = 0 or non-finite x; at most
+// 2^126, so that p and 1 / p stay finite, for x below the normal range).
 __device__ __forceinline__ float pow2_scale_to_one(float x) {
   if (!(x > 0.f) || !(x < 3.0e38f)) return 1.f;
-  return ldexpf(1.f, -ilogbf(x));
+  return ldexpf(1.f, min(-ilogbf(x), 126));
 }
 
-// Power of two <= x (1 for x = 0 or non-finite x).
+// Power of two <= x (1 for x = 0 or non-finite x; at least 2^-126).
 __device__ __forceinline__ float pow2_floor(float x) {
   if (!(x > 0.f) || !(x < 3.0e38f)) return 1.f;
-  return ldexpf(1.f, ilogbf(x));
+  return ldexpf(1.f, max(ilogbf(x), -126));
 }
 
 // ---------------------------------------------------------- lane exchanges
@@ -249,6 +258,7 @@ struct KernelArgs {
   const Chunk* chunks;
   const LongWin* longs;
   int32_t max_chunks, max_long, n, W, H;
+  float eps;  // added to the normaliser phi(q) . z
 };
 
 // ------------------------------------------------------------------ jobs
@@ -311,13 +321,31 @@ struct Sel {
 };
 
 // phi of a fragment, rounded to the storage type; zero where !ok.  fp16 works on
-// packed halves, phi(x) = 2^(min(x, 0) log2 e) + max(x, 0), which equals the
-// definition on both branches.
+// packed halves, elu + 1 as phi(x) = 2^(min(x, 0) log2 e) + max(x, 0), which
+// equals the definition on both branches.
 typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
 
-template <typename T, int KS>
+template <typename T, int KS, int PHI>
 __device__ __forceinline__ Raw<T, KS> phi_frag(Raw<T, KS> x, bool ok) {
-  if constexpr (std::is_same<T, _Float16>::value) {
+  if constexpr (PHI == kPhiRelu && std::is_same<T, _Float16>::value) {
+    constexpr int NW = KS / 2;
+    using W = uint32_t __attribute__((ext_vector_type(NW)));
+    const W w = __builtin_bit_cast(W, x);
+    W out;
+    const half2_t zero = {0, 0};
+#pragma unroll
+    for (int k = 0; k < NW; ++k) {
+      const half2_t p = __builtin_bit_cast(half2_t, (uint32_t)w[k]);
+      out[k] = ok ? __builtin_bit_cast(uint32_t, __builtin_elementwise_max(p, zero)) : 0u;
+    }
+    return __builtin_bit_cast(Raw<T, KS>, out);
+  } else if constexpr (PHI == kPhiRelu) {
+    float f[KS];
+    Frag<T, KS>::to_f32(x, f);
+#pragma unroll
+    for (int r = 0; r < KS; ++r) f[r] = ok ? fmaxf(f[r], 0.f) : 0.f;
+    return Frag<T, KS>::from_f32(f);
+  } else if constexpr (std::is_same<T, _Float16>::value) {
     constexpr int NW = KS / 2;
     using W = uint32_t __attribute__((ext_vector_type(NW)));
     const W w = __builtin_bit_cast(W, x);
@@ -345,12 +373,19 @@ __device__ __forceinline__ Raw<T, KS> phi_frag(Raw<T, KS> x, bool ok) {
   }
 }
 
-// phi of a fragment (as phi_frag) and phi' at the same slots in fp32, sharing
-// the exponential: with e = exp(min(x, 0)), phi(x) = e + max(x, 0), phi'(x) = e.
-template <typename T, int KS>
+// phi of a fragment (as phi_frag) and phi' at the same slots in fp32.  elu + 1
+// shares the exponential: with e = exp(min(x, 0)), phi(x) = e + max(x, 0),
+// phi'(x) = e.
+template <typename T, int KS, int PHI>
 __device__ __forceinline__ void phi_dphi(Raw<T, KS> x, bool ok, Raw<T, KS>& phi,
                                          float (&dphi)[KS]) {
-  if constexpr (std::is_same<T, _Float16>::value) {
+  if constexpr (PHI == kPhiRelu) {
+    float f[KS];
+    Frag<T, KS>::to_f32(x, f);
+#pragma unroll
+    for (int r = 0; r < KS; ++r) dphi[r] = f[r] > 0.f ? 1.f : 0.f;
+    phi = phi_frag<T, KS, PHI>(x, ok);
+  } else if constexpr (std::is_same<T, _Float16>::value) {
     constexpr int NW = KS / 2;
     using W = uint32_t __attribute__((ext_vector_type(NW)));
     const W w = __builtin_bit_cast(W, x);
@@ -403,7 +438,7 @@ __device__ __forceinline__ bool sub_overlaps(int32_t r0, int s, int32_t a, int32
 
 // Rows [a, b) of one slice into the state: M += phi(K)^T V, V += phi(K)^T 1.
 // K is matrix 0, V matrix 1.
-template <typename T, int D, int NM>
+template <typename T, int D, int NM, int PHI>
 __device__ __forceinline__ void state_seg(const Slice<T, Geo<D>::KS, NM>& sb, int32_t r0,
                                           int32_t a, int32_t b, int i, int g,
                                           const Sel<T, D>& sel, State<D>& st) {
@@ -415,7 +450,7 @@ __device__ __forceinline__ void state_seg(const Slice<T, Geo<D>::KS, NM>& sb, in
   for (int s = 0; s < 2; ++s) {
     const int32_t row = r0 + 16 * s + i;
     const bool in = sb.ok[s] && row >= a && row < b;
-    const Raw<T, KS> fk = phi_frag<T, KS>(sb.x[0][s], in);
+    const Raw<T, KS> fk = phi_frag<T, KS, PHI>(sb.x[0][s], in);
     const Raw<T, KS> vv = in ? sb.x[1][s] : F::zero();
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
@@ -456,10 +491,12 @@ struct FwdOp {
   Raw<T, Geo<D>::KS> A[Geo<D>::NT];  // sig S as operand of result tile ct (contract e)
   Raw<T, Geo<D>::KS> Az;             // sig z in rows 0, 4, 8, 12: the normaliser of every
                                      // row lands in component 0 of every lane group
+  float seps;                        // sig eps
 };
 
 template <typename T, int D>
-__device__ __forceinline__ void make_fwd_op(const State<D>& st, FwdOp<T, D>& op, int i) {
+__device__ __forceinline__ void make_fwd_op(const State<D>& st, FwdOp<T, D>& op, int i,
+                                            float eps) {
   constexpr int KS = Geo<D>::KS, NT = Geo<D>::NT;
   const float sig = Ty<T>::kNarrow ? pow2_scale_to_one(st.absmax()) : 1.f;
 #pragma unroll
@@ -474,12 +511,13 @@ __device__ __forceinline__ void make_fwd_op(const State<D>& st, FwdOp<T, D>& op,
 #pragma unroll
   for (int r = 0; r < KS; ++r) zx[r] = st.V[r >> 2][r & 3] * zmul;
   op.Az = Frag<T, KS>::from_f32(zx);
+  op.seps = sig * eps;
 }
 
-// o = phi(q) S / (phi(q) . z) for rows [a, b) of one slice (Q is matrix QM):
-// numerator and normaliser both come from the matrix cores with the same
-// rounded phi(q) and the same scale sig, which cancels.
-template <typename T, int D, int NM, int QM>
+// o = phi(q) S / (phi(q) . z + eps) for rows [a, b) of one slice (Q is matrix
+// QM): numerator and normaliser both come from the matrix cores with the same
+// rounded phi(q) and the same scale sig, which cancels (eps is scaled by sig).
+template <typename T, int D, int NM, int QM, int PHI>
 __device__ __forceinline__ void apply_seg(const Slice<T, Geo<D>::KS, NM>& sb, int32_t r0,
                                           int32_t a, int32_t b, int i, int g,
                                           const FwdOp<T, D>& op, T* o, size_t rs, int col) {
@@ -491,9 +529,9 @@ __device__ __forceinline__ void apply_seg(const Slice<T, Geo<D>::KS, NM>& sb, in
     if (!sub_overlaps(r0, s, a, b)) continue;
     const int32_t row = r0 + 16 * s + i;
     const bool in = sb.ok[s] && row >= a && row < b;
-    const Raw<T, KS> bq = phi_frag<T, KS>(sb.x[QM][s], in);
+    const Raw<T, KS> bq = phi_frag<T, KS, PHI>(sb.x[QM][s], in);
     const floatx4 den = F::mma(op.Az, bq, zero);
-    const float scale = recip<T>(den[0]);
+    const float scale = recip<T>(den[0] + op.seps);
     float ox[KS];
 #pragma unroll
     for (int ct = 0; ct < NT; ++ct) {
@@ -517,6 +555,13 @@ template <typename T, int W16>
 constexpr int kWpe = sizeof(T) == 4 ? (W16 > 2 ? W16 / 2 : 1) : W16;
 
 // ----------------------------------------------------------- backward math
+// bf16 keeps 8 significant bits, so the backward carries two operands as a
+// sum of two bf16 values (high part and rounding residual, 16 bits together):
+// -dout.o in the dz accumulation and dS^T in dk = (v dS^T + dz) phi'(k), the
+// two terms that cancel there.  fp16 (11 bits) and fp32 need no split.
+template <typename T>
+constexpr bool kSplitGrad = std::is_same<T, bf16_t>::value;
+
 // Operands of the backward's head-dim contractions for one window.  The same
 // registers first hold the state operands (for the Q,dout rows) and are then
 // overwritten with the state-gradient operands (for the K,V gradient rows).
@@ -525,11 +570,13 @@ struct BwdOp {
   Raw<T, Geo<D>::KS> A[Geo<D>::NT];  // sig S   (o = phi(q) S, tile ct)  | rho dS^T (dfk = v dS^T, tile et)
   Raw<T, Geo<D>::KS> B[Geo<D>::NT];  // sig S^T (dfq = dout S^T, tile et) | rho dS  (dv = phi(k) dS, tile ct)
   Raw<T, Geo<D>::KS> Az;             // sig z in rows 0, 4, 8, 12 (normaliser) | unused
-  float z[Geo<D>::KS];               // sig z                             | dz
+  float z[Geo<D>::KS];               // sig z (as rounded in Az)          | dz
   float inv_scale;                   // unused                            | 1 / rho
   float bsig;                        // beta sig: phi(q) / den in the state gradients is
                                      // scaled by beta (<= min z, so beta phi(q) / den <= 1)
   float inv_beta;                    // 1 / beta
+  float seps;                        // sig eps
+  Raw<T, Geo<D>::KS> Al[kSplitGrad<T> ? Geo<D>::NT : 1];  // unused | residual of A (bf16)
 };
 
 // The transpose of a state as operands of a head-dim contraction: slot r of lane
@@ -538,10 +585,11 @@ struct BwdOp {
 template <int D>
 constexpr int kTrLd = D + 4;
 
-template <typename T, int D>
+template <typename T, int D, bool LO = false>
 __device__ __forceinline__ void transposed_operand(const State<D>& st, float mul, float* tile,
                                                    int i, int g,
-                                                   Raw<T, Geo<D>::KS> (&out)[Geo<D>::NT]) {
+                                                   Raw<T, Geo<D>::KS> (&out)[Geo<D>::NT],
+                                                   Raw<T, Geo<D>::KS>* out_lo = nullptr) {
   constexpr int KS = Geo<D>::KS, NT = Geo<D>::NT, LD = kTrLd<D>;
 #pragma unroll
   for (int et = 0; et < NT; ++et)
@@ -562,13 +610,24 @@ __device__ __forceinline__ void transposed_operand(const State<D>& st, float mul
       x[4 * ct + 3] = p.w * mul;
     }
     out[et] = Frag<T, KS>::from_f32(x);
+    if constexpr (LO) {
+      float hi[KS];
+      Frag<T, KS>::to_f32(out[et], hi);
+#pragma unroll
+      for (int r = 0; r < KS; ++r) x[r] -= hi[r];
+      out_lo[et] = Frag<T, KS>::from_f32(x);
+    }
   }
   wave_lds_sync();   // the tile may be written again by the next call
 }
 
-template <typename T, int D>
+// beta bounds phi(q)_e / den through 1 / z_e, for every e with z_e > 0.  Under
+// ReLU a feature with z_e = 0 has phi(k_j)_e = 0 for every row of the window, so
+// row e of dS and dz_e reach neither dk (phi'(k_j)_e = 0) nor dv (phi(k_j)_e =
+// 0): qgrad_seg leaves those features out of the state gradients.
+template <typename T, int D, int PHI>
 __device__ __forceinline__ void make_state_op(const State<D>& st, BwdOp<T, D>& op, float* tile,
-                                              int i, int g) {
+                                              int i, int g, float eps) {
   constexpr int KS = Geo<D>::KS, NT = Geo<D>::NT;
   const float sig = Ty<T>::kNarrow ? pow2_scale_to_one(st.absmax()) : 1.f;
 #pragma unroll
@@ -579,21 +638,25 @@ __device__ __forceinline__ void make_state_op(const State<D>& st, BwdOp<T, D>& o
     op.A[ct] = tiles_operand<T, D>(col, sig);
   }
   transposed_operand<T, D>(st, sig, tile, i, g, op.B);
+  // op.z holds sig z rounded exactly as in the normaliser operand Az: dq subtracts
+  // (dout.o) z from dout S^T, and for a row whose normaliser is mostly eps the two
+  // terms cancel to eps / den; the same z on both sides keeps that residual exact
   float zmin = 3.0e38f;
-  const float zmul = (i & 3) == 0 ? sig : 0.f;
   float zx[KS];
 #pragma unroll
   for (int r = 0; r < KS; ++r) {
     const float z = st.V[r >> 2][r & 3];
-    zmin = fminf(zmin, z);
-    op.z[r] = z * sig;
-    zx[r] = z * zmul;
+    if (PHI != kPhiRelu || z > 0.f) zmin = fminf(zmin, z);
+    const float zs = Ty<T>::kNarrow ? u16_to_f32<T>(f32_to_u16<T>(z * sig)) : z * sig;
+    op.z[r] = zs;
+    zx[r] = (i & 3) == 0 ? zs : 0.f;
   }
   op.Az = Frag<T, KS>::from_f32(zx);
   // phi(q)_e / den <= 1 / z_e <= 1 / min z, so beta phi(q) / den <= 1
   const float beta = Ty<T>::kNarrow ? pow2_floor(wave_reduce<false>(zmin)) : 1.f;
   op.bsig = beta * sig;
   op.inv_beta = 1.f / beta;
+  op.seps = sig * eps;
 }
 
 // From state-gradient tiles that carry a factor `1 / inv_beta`.
@@ -605,7 +668,7 @@ __device__ __forceinline__ void make_grad_op(const State<D>& st, float inv_beta,
   const float rho = Ty<T>::kNarrow ? pow2_scale_to_one(mx) : 1.f;
   op.inv_scale = 1.f / rho;
   const float mul = rho * inv_beta;
-  transposed_operand<T, D>(st, mul, tile, i, g, op.A);
+  transposed_operand<T, D, kSplitGrad<T>>(st, mul, tile, i, g, op.A, op.Al);
 #pragma unroll
   for (int ct = 0; ct < NT; ++ct) {
     floatx4 col[NT];
@@ -619,9 +682,9 @@ __device__ __forceinline__ void make_grad_op(const State<D>& st, float inv_beta,
 
 // Rows [a, b) of one slice: dq, and into gs: M += beta (phi(q)/den)^T dout,
 // V += beta (phi(q)/den)^T (-dout.o).  q is matrix QI, dout matrix DI.  The
-// normaliser comes from the matrix cores (den' = sig den); with sig folded into
-// z, dphi(q) = (sig dfq - dot sig z) / den'.
-template <typename T, int D, int NM, int QI, int DI>
+// normaliser comes from the matrix cores (den' = sig den, plus sig eps); with sig
+// folded into z, dphi(q) = (sig dfq - dot sig z) / den'.
+template <typename T, int D, int NM, int QI, int DI, int PHI>
 __device__ __forceinline__ void qgrad_seg(const Slice<T, Geo<D>::KS, NM>& sb, int32_t r0,
                                           int32_t a, int32_t b, int i, int g,
                                           const Sel<T, D>& sel, const BwdOp<T, D>& op, T* dq,
@@ -629,7 +692,8 @@ __device__ __forceinline__ void qgrad_seg(const Slice<T, Geo<D>::KS, NM>& sb, in
   constexpr int KS = Geo<D>::KS, NT = Geo<D>::NT;
   using F = Frag<T, KS>;
   const floatx4 zero = {0.f, 0.f, 0.f, 0.f};
-  Raw<T, KS> xr[2], dr[2], nd[2];
+  constexpr bool SP = kSplitGrad<T>;
+  Raw<T, KS> xr[2], dr[2], nd[2], nl[2];
 #pragma unroll
   for (int s = 0; s < 2; ++s) {
     const int32_t row = r0 + 16 * s + i;
@@ -637,14 +701,15 @@ __device__ __forceinline__ void qgrad_seg(const Slice<T, Geo<D>::KS, NM>& sb, in
     dr[s] = in ? sb.x[DI][s] : F::zero();
     xr[s] = F::zero();
     nd[s] = F::zero();
+    if constexpr (SP) nl[s] = F::zero();
     if (!sub_overlaps(r0, s, a, b)) continue;
     Raw<T, KS> bq;
     float dphq[KS], fq[KS], dox[KS];
-    phi_dphi<T, KS>(sb.x[QI][s], in, bq, dphq);
+    phi_dphi<T, KS, PHI>(sb.x[QI][s], in, bq, dphq);
     F::to_f32(bq, fq);
     F::to_f32(dr[s], dox);
     const floatx4 den4 = F::mma(op.Az, bq, zero);
-    const float rden = recip<T>(in ? den4[0] : 1.f);
+    const float rden = recip<T>(in ? den4[0] + op.seps : 1.f);
     float dot = 0.f;
 #pragma unroll
     for (int ct = 0; ct < NT; ++ct) {
@@ -669,13 +734,19 @@ __device__ __forceinline__ void qgrad_seg(const Slice<T, Geo<D>::KS, NM>& sb, in
     const float w = op.bsig * rden;
 #pragma unroll
     for (int r = 0; r < KS; ++r) {
-      xs[r] = fq[r] * w;
+      xs[r] = (PHI != kPhiRelu || op.z[r] > 0.f) ? fq[r] * w : 0.f;
       ns[r] = -dot;
     }
     xr[s] = F::from_f32(xs);
     nd[s] = F::from_f32(ns);
+    if constexpr (SP) {
+      const float res = -dot - u16_to_f32<T>(f32_to_u16<T>(-dot));
+#pragma unroll
+      for (int r = 0; r < KS; ++r) ns[r] = res;
+      nl[s] = F::from_f32(ns);
+    }
   }
-  floatx4 tx[2][NT], td[2][NT], tn[2];
+  floatx4 tx[2][NT], td[2][NT], tn[2], tl[2];
 #pragma unroll
   for (int s = 0; s < 2; ++s) {
 #pragma unroll
@@ -684,12 +755,16 @@ __device__ __forceinline__ void qgrad_seg(const Slice<T, Geo<D>::KS, NM>& sb, in
       td[s][t] = F::mma(dr[s], sel.m[t], zero);
     }
     tn[s] = F::mma(nd[s], sel.m[0], zero);
+    if constexpr (SP) tl[s] = F::mma(nl[s], sel.m[0], zero);
   }
   const Raw<T, 8> pn = pack_rows<T>(tn[0], tn[1]);
+  Raw<T, 8> pl;
+  if constexpr (SP) pl = pack_rows<T>(tl[0], tl[1]);
 #pragma unroll
   for (int et = 0; et < NT; ++et) {
     const Raw<T, 8> px = pack_rows<T>(tx[0][et], tx[1][et]);
     gs.V[et] = Frag<T, 8>::mma(px, pn, gs.V[et]);
+    if constexpr (SP) gs.V[et] = Frag<T, 8>::mma(px, pl, gs.V[et]);
 #pragma unroll
     for (int ct = 0; ct < NT; ++ct) {
       const Raw<T, 8> pd = pack_rows<T>(td[0][ct], td[1][ct]);
@@ -699,7 +774,7 @@ __device__ __forceinline__ void qgrad_seg(const Slice<T, Geo<D>::KS, NM>& sb, in
 }
 
 // Rows [a, b) of one slice: dk = (v dS^T + dz) phi'(k), dv = phi(k) dS.
-template <typename T, int D, int NM>
+template <typename T, int D, int NM, int PHI>
 __device__ __forceinline__ void kgrad_seg(const Slice<T, Geo<D>::KS, NM>& sb, int32_t r0,
                                           int32_t a, int32_t b, int i, int g,
                                           const BwdOp<T, D>& op, T* dk, T* dv, size_t rs,
@@ -714,11 +789,12 @@ __device__ __forceinline__ void kgrad_seg(const Slice<T, Geo<D>::KS, NM>& sb, in
     const bool in = sb.ok[s] && row >= a && row < b;
     Raw<T, KS> fk;
     float dphk[KS];
-    phi_dphi<T, KS>(sb.x[0][s], in, fk, dphk);
+    phi_dphi<T, KS, PHI>(sb.x[0][s], in, fk, dphk);
     float dkx[KS], dvx[KS];
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
-      const floatx4 a4 = F::mma(op.A[t], sb.x[1][s], zero);
+      floatx4 a4 = F::mma(op.A[t], sb.x[1][s], zero);
+      if constexpr (kSplitGrad<T>) a4 = F::mma(op.Al[t], sb.x[1][s], a4);
       const floatx4 b4 = F::mma(op.B[t], fk, zero);
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
@@ -1069,7 +1145,7 @@ struct WinIter {
 };
 
 // ------------------------------------------------------------------ forward
-template <typename T, int D>
+template <typename T, int D, int PHI>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(kWpe<T, SLA_FWD_WPE>)))
 void k_sla_fwd(KernelArgs a, const T* __restrict__ q, const T* __restrict__ k,
                const T* __restrict__ v, T* __restrict__ o) {
@@ -1127,7 +1203,7 @@ void k_sla_fwd(KernelArgs a, const T* __restrict__ q, const T* __restrict__ k,
 #pragma unroll
         for (int jj = 0; jj < kBlockJobs; ++jj) {
           const int32_t r0 = base + kSliceRows * jj;
-          if (job_overlaps(r0, wa, wb)) state_seg<T, D, 3>(bk.j[jj], r0, wa, wb, i, g, sel, st);
+          if (job_overlaps(r0, wa, wb)) state_seg<T, D, 3, PHI>(bk.j[jj], r0, wa, wb, i, g, sel, st);
         }
       }
       if (wi.shared) {
@@ -1137,7 +1213,7 @@ void k_sla_fwd(KernelArgs a, const T* __restrict__ q, const T* __restrict__ k,
         lds_barrier();  // the slots may be written by the next long item
       }
       FwdOp<T, D> op;
-      make_fwd_op<T, D>(st, op, i);
+      make_fwd_op<T, D>(st, op, i, a.eps);
       for (int32_t base = ww.ra; base < ww.rb; base += kBlockRows) {
         if (!resident) {
           BlockRows br;
@@ -1148,7 +1224,7 @@ void k_sla_fwd(KernelArgs a, const T* __restrict__ q, const T* __restrict__ k,
 #pragma unroll
         for (int jj = 0; jj < kBlockJobs; ++jj) {
           const int32_t r0 = base + kSliceRows * jj;
-          if (job_overlaps(r0, wa, wb)) apply_seg<T, D, 3, 2>(bk.j[jj], r0, wa, wb, i, g, op, o, rs, col);
+          if (job_overlaps(r0, wa, wb)) apply_seg<T, D, 3, 2, PHI>(bk.j[jj], r0, wa, wb, i, g, op, o, rs, col);
         }
       }
     }
@@ -1160,7 +1236,7 @@ void k_sla_fwd(KernelArgs a, const T* __restrict__ q, const T* __restrict__ k,
 // ----------------------------------------------------------------- backward
 // Per window: state S, z from K, V; then dq and the state gradients from Q, dout;
 // then dk, dv from K, V (held in registers since the first phase).
-template <typename T, int D>
+template <typename T, int D, int PHI>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(kWpe<T, SLA_BWD_WPE>)))
 void k_sla_bwd(KernelArgs a, const T* __restrict__ q, const T* __restrict__ k,
                const T* __restrict__ v, const T* __restrict__ dout, T* __restrict__ dq,
@@ -1220,7 +1296,7 @@ void k_sla_bwd(KernelArgs a, const T* __restrict__ q, const T* __restrict__ k,
 #pragma unroll
         for (int jj = 0; jj < kBlockJobs; ++jj) {
           const int32_t r0 = base + kSliceRows * jj;
-          if (job_overlaps(r0, wa, wb)) state_seg<T, D, 4>(bk.j[jj], r0, wa, wb, i, g, sel, st);
+          if (job_overlaps(r0, wa, wb)) state_seg<T, D, 4, PHI>(bk.j[jj], r0, wa, wb, i, g, sel, st);
         }
       }
       if (wi.shared) {
@@ -1228,7 +1304,7 @@ void k_sla_bwd(KernelArgs a, const T* __restrict__ q, const T* __restrict__ k,
         lds_barrier();
         combine<D>(st, s_part[0], lane, wv, ww.pair);
       }
-      make_state_op<T, D>(st, op, tile, i, g);
+      make_state_op<T, D, PHI>(st, op, tile, i, g, a.eps);
       // phase 1: dq and beta dS, beta dz
       st.clear();
       for (int32_t base = ww.ra; base < ww.rb; base += kBlockRows) {
@@ -1242,7 +1318,7 @@ void k_sla_bwd(KernelArgs a, const T* __restrict__ q, const T* __restrict__ k,
         for (int jj = 0; jj < kBlockJobs; ++jj) {
           const int32_t r0 = base + kSliceRows * jj;
           if (job_overlaps(r0, wa, wb))
-            qgrad_seg<T, D, 4, 2, 3>(bk.j[jj], r0, wa, wb, i, g, sel, op, dq, rs, col, st);
+            qgrad_seg<T, D, 4, 2, 3, PHI>(bk.j[jj], r0, wa, wb, i, g, sel, op, dq, rs, col, st);
         }
       }
       if (wi.shared) {
@@ -1264,7 +1340,7 @@ void k_sla_bwd(KernelArgs a, const T* __restrict__ q, const T* __restrict__ k,
 #pragma unroll
         for (int jj = 0; jj < kBlockJobs; ++jj) {
           const int32_t r0 = base + kSliceRows * jj;
-          if (job_overlaps(r0, wa, wb)) kgrad_seg<T, D, 4>(bk.j[jj], r0, wa, wb, i, g, op, dk, dv, rs, col);
+          if (job_overlaps(r0, wa, wb)) kgrad_seg<T, D, 4, PHI>(bk.j[jj], r0, wa, wb, i, g, op, dk, dv, rs, col);
         }
       }
     }
@@ -1326,7 +1402,7 @@ static int grid_size(const void* kernel, const PlanLayout& lay, int32_t n, int32
 }
 
 static KernelArgs kernel_args(const void* plan, const PlanLayout& lay, int32_t n, int32_t W,
-                              int32_t H) {
+                              int32_t H, float eps) {
   const char* base = static_cast<const char*>(plan);
   KernelArgs a;
   a.hdr = reinterpret_cast<const PlanHeader*>(base + lay.header);
@@ -1339,58 +1415,80 @@ static KernelArgs kernel_args(const void* plan, const PlanLayout& lay, int32_t n
   a.n = n;
   a.W = W;
   a.H = H;
+  a.eps = eps;
   return a;
 }
 
-template <typename T, int D>
-static hipError_t fwd_impl(const void* plan, int32_t n, int32_t W, int32_t H, const void* q,
-                           const void* k, const void* v, void* o, hipStream_t stream) {
+template <typename T, int D, int PHI>
+static hipError_t fwd_impl(const void* plan, int32_t n, int32_t W, int32_t H, float eps,
+                           const void* q, const void* k, const void* v, void* o,
+                           hipStream_t stream) {
   const PlanLayout lay = plan_layout(n, W);
-  const KernelArgs a = kernel_args(plan, lay, n, W, H);
-  hipLaunchKernelGGL((k_sla_fwd<T, D>), dim3(grid_size(reinterpret_cast<const void*>(&k_sla_fwd<T, D>), lay, n, H)), dim3(64 * kWaves), 0, stream, a,
-                     static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v),
-                     static_cast<T*>(o));
+  const KernelArgs a = kernel_args(plan, lay, n, W, H, eps);
+  const void* kern = reinterpret_cast<const void*>(&k_sla_fwd<T, D, PHI>);
+  hipLaunchKernelGGL((k_sla_fwd<T, D, PHI>), dim3(grid_size(kern, lay, n, H)), dim3(64 * kWaves), 0,
+                     stream, a, static_cast<const T*>(q), static_cast<const T*>(k),
+                     static_cast<const T*>(v), static_cast<T*>(o));
   return hipGetLastError();
 }
 
-template <typename T, int D>
-static hipError_t bwd_impl(const void* plan, int32_t n, int32_t W, int32_t H, const void* q,
-                           const void* k, const void* v, const void* dout, void* dq, void* dk,
-                           void* dv, hipStream_t stream) {
+template <typename T, int D, int PHI>
+static hipError_t bwd_impl(const void* plan, int32_t n, int32_t W, int32_t H, float eps,
+                           const void* q, const void* k, const void* v, const void* dout, void* dq,
+                           void* dk, void* dv, hipStream_t stream) {
   const PlanLayout lay = plan_layout(n, W);
-  const KernelArgs a = kernel_args(plan, lay, n, W, H);
-  hipLaunchKernelGGL((k_sla_bwd<T, D>), dim3(grid_size(reinterpret_cast<const void*>(&k_sla_bwd<T, D>), lay, n, H)), dim3(64 * kWaves), 0, stream, a,
-                     static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v),
-                     static_cast<const T*>(dout), static_cast<T*>(dq), static_cast<T*>(dk),
-                     static_cast<T*>(dv));
+  const KernelArgs a = kernel_args(plan, lay, n, W, H, eps);
+  const void* kern = reinterpret_cast<const void*>(&k_sla_bwd<T, D, PHI>);
+  hipLaunchKernelGGL((k_sla_bwd<T, D, PHI>), dim3(grid_size(kern, lay, n, H)), dim3(64 * kWaves), 0,
+                     stream, a, static_cast<const T*>(q), static_cast<const T*>(k),
+                     static_cast<const T*>(v), static_cast<const T*>(dout), static_cast<T*>(dq),
+                     static_cast<T*>(dk), static_cast<T*>(dv));
   return hipGetLastError();
 }
 
-// dtype: 0 f32, 1 f16, 2 bf16
-hipError_t launch_forward(const void* plan, int32_t n, int32_t W, int dtype, int32_t H, int32_t d,
-                          const void* q, const void* k, const void* v, void* o,
-                          hipStream_t stream) {
+template <int PHI>
+static hipError_t forward_phi(const void* plan, int32_t n, int32_t W, int dtype, int32_t H,
+                              int32_t d, float eps, const void* q, const void* k, const void* v,
+                              void* o, hipStream_t stream) {
   if (d == 32) {
-    if (dtype == 0) return fwd_impl<float, 32>(plan, n, W, H, q, k, v, o, stream);
-    if (dtype == 1) return fwd_impl<_Float16, 32>(plan, n, W, H, q, k, v, o, stream);
-    return fwd_impl<bf16_t, 32>(plan, n, W, H, q, k, v, o, stream);
+    if (dtype == 0) return fwd_impl<float, 32, PHI>(plan, n, W, H, eps, q, k, v, o, stream);
+    if (dtype == 1) return fwd_impl<_Float16, 32, PHI>(plan, n, W, H, eps, q, k, v, o, stream);
+    return fwd_impl<bf16_t, 32, PHI>(plan, n, W, H, eps, q, k, v, o, stream);
   }
-  if (dtype == 0) return fwd_impl<float, 16>(plan, n, W, H, q, k, v, o, stream);
-  if (dtype == 1) return fwd_impl<_Float16, 16>(plan, n, W, H, q, k, v, o, stream);
-  return fwd_impl<bf16_t, 16>(plan, n, W, H, q, k, v, o, stream);
+  if (dtype == 0) return fwd_impl<float, 16, PHI>(plan, n, W, H, eps, q, k, v, o, stream);
+  if (dtype == 1) return fwd_impl<_Float16, 16, PHI>(plan, n, W, H, eps, q, k, v, o, stream);
+  return fwd_impl<bf16_t, 16, PHI>(plan, n, W, H, eps, q, k, v, o, stream);
+}
+
+template <int PHI>
+static hipError_t backward_phi(const void* plan, int32_t n, int32_t W, int dtype, int32_t H,
+                               int32_t d, float eps, const void* q, const void* k, const void* v,
+                               const void* dout, void* dq, void* dk, void* dv,
+                               hipStream_t stream) {
+  if (d == 32) {
+    if (dtype == 0) return bwd_impl<float, 32, PHI>(plan, n, W, H, eps, q, k, v, dout, dq, dk, dv, stream);
+    if (dtype == 1) return bwd_impl<_Float16, 32, PHI>(plan, n, W, H, eps, q, k, v, dout, dq, dk, dv, stream);
+    return bwd_impl<bf16_t, 32, PHI>(plan, n, W, H, eps, q, k, v, dout, dq, dk, dv, stream);
+  }
+  if (dtype == 0) return bwd_impl<float, 16, PHI>(plan, n, W, H, eps, q, k, v, dout, dq, dk, dv, stream);
+  if (dtype == 1) return bwd_impl<_Float16, 16, PHI>(plan, n, W, H, eps, q, k, v, dout, dq, dk, dv, stream);
+  return bwd_impl<bf16_t, 16, PHI>(plan, n, W, H, eps, q, k, v, dout, dq, dk, dv, stream);
+}
+
+// dtype: 0 f32, 1 f16, 2 bf16; phi: 0 elu + 1, 1 ReLU
+hipError_t launch_forward(const void* plan, int32_t n, int32_t W, int dtype, int32_t H, int32_t d,
+                          int phi, float eps, const void* q, const void* k, const void* v, void* o,
+                          hipStream_t stream) {
+  if (phi == kPhiRelu) return forward_phi<kPhiRelu>(plan, n, W, dtype, H, d, eps, q, k, v, o, stream);
+  return forward_phi<kPhiElu1>(plan, n, W, dtype, H, d, eps, q, k, v, o, stream);
 }
 
 hipError_t launch_backward(const void* plan, int32_t n, int32_t W, int dtype, int32_t H, int32_t d,
-                           const void* q, const void* k, const void* v, const void* dout,
-                           void* dq, void* dk, void* dv, hipStream_t stream) {
-  if (d == 32) {
-    if (dtype == 0) return bwd_impl<float, 32>(plan, n, W, H, q, k, v, dout, dq, dk, dv, stream);
-    if (dtype == 1) return bwd_impl<_Float16, 32>(plan, n, W, H, q, k, v, dout, dq, dk, dv, stream);
-    return bwd_impl<bf16_t, 32>(plan, n, W, H, q, k, v, dout, dq, dk, dv, stream);
-  }
-  if (dtype == 0) return bwd_impl<float, 16>(plan, n, W, H, q, k, v, dout, dq, dk, dv, stream);
-  if (dtype == 1) return bwd_impl<_Float16, 16>(plan, n, W, H, q, k, v, dout, dq, dk, dv, stream);
-  return bwd_impl<bf16_t, 16>(plan, n, W, H, q, k, v, dout, dq, dk, dv, stream);
+                           int phi, float eps, const void* q, const void* k, const void* v,
+                           const void* dout, void* dq, void* dk, void* dv, hipStream_t stream) {
+  if (phi == kPhiRelu)
+    return backward_phi<kPhiRelu>(plan, n, W, dtype, H, d, eps, q, k, v, dout, dq, dk, dv, stream);
+  return backward_phi<kPhiElu1>(plan, n, W, dtype, H, d, eps, q, k, v, dout, dq, dk, dv, stream);
 }
 
 }  // namespace sla

@@ -7,8 +7,11 @@ Functions mirror the C ABI in include/sla.h:
     plan_bytes(n, num_windows)
     plan_layout(n, num_windows)
     build_segments(ids | offsets, num_windows, chunk_rows=0) -> Plan
-    forward(plan, q, k, v, out=None) -> o
-    backward(plan, q, k, v, dout, dq=None, dk=None, dv=None) -> (dq, dk, dv)
+    forward(plan, q, k, v, out=None, feature_map=None, eps=None) -> o
+    backward(plan, q, k, v, dout, dq=None, dk=None, dv=None, feature_map=None, eps=None)
+        -> (dq, dk, dv)
+        (feature_map "elu1" | "relu" and eps >= 0 select sla_forward_ex /
+        sla_backward_ex; leaving both None calls sla_forward / sla_backward)
     scatter_workspace_bytes(n, heads, head_dim)
     forward_scatter(plan, q, k, v, out=None, workspace=None) -> o   (naive comparator)
 """
@@ -22,6 +25,8 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsla.so")
 
 SLA_OK, SLA_E_ARG, SLA_E_UNSUPPORTED, SLA_E_WORKSPACE, SLA_E_HIP = range(5)
 
+FEATURE_MAPS = {"elu1": 0, "relu": 1}   # sla_feature_map_t
+
 EXPORTED = (
     "sla_abi_version",
     "sla_status_string",
@@ -32,6 +37,8 @@ EXPORTED = (
     "sla_build_segments",
     "sla_forward",
     "sla_backward",
+    "sla_forward_ex",
+    "sla_backward_ex",
     "sla_scatter_workspace_bytes",
     "sla_forward_scatter",
 )
@@ -86,6 +93,11 @@ def lib() -> ctypes.CDLL:
     L.sla_forward.argtypes = [vp, sz, i64, i32, ctypes.c_int, i32, i32, vp, vp, vp, vp, vp]
     L.sla_backward.restype = ctypes.c_int
     L.sla_backward.argtypes = [vp, sz, i64, i32, ctypes.c_int, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp]
+    f32, en = ctypes.c_float, ctypes.c_int
+    L.sla_forward_ex.restype = ctypes.c_int
+    L.sla_forward_ex.argtypes = [vp, sz, i64, i32, en, i32, i32, en, f32, vp, vp, vp, vp, vp]
+    L.sla_backward_ex.restype = ctypes.c_int
+    L.sla_backward_ex.argtypes = [vp, sz, i64, i32, en, i32, i32, en, f32, vp, vp, vp, vp, vp, vp, vp, vp]
     L.sla_scatter_workspace_bytes.restype = sz
     L.sla_scatter_workspace_bytes.argtypes = [i64, i32, i32]
     L.sla_forward_scatter.restype = ctypes.c_int
@@ -204,7 +216,17 @@ def _check_rows(name, t, n, like=None):
         raise ValueError(f"{name} must match q in shape, dtype and device")
 
 
-def forward(plan: Plan, q, k, v, out=None):
+def _variant(feature_map, eps):
+    """None for the plain Eq. (3) calls, else (sla_feature_map_t, eps)."""
+    if feature_map is None and eps is None:
+        return None
+    fm = "elu1" if feature_map is None else feature_map
+    if fm not in FEATURE_MAPS:
+        raise ValueError(f"feature_map must be one of {sorted(FEATURE_MAPS)}, not {fm!r}")
+    return FEATURE_MAPS[fm], float(0.0 if eps is None else eps)
+
+
+def forward(plan: Plan, q, k, v, out=None, feature_map=None, eps=None):
     torch = _torch()
     _check_rows("q", q, plan.n)
     _check_rows("k", k, plan.n, q)
@@ -213,13 +235,20 @@ def forward(plan: Plan, q, k, v, out=None):
         out = torch.empty_like(q)
     _check_rows("out", out, plan.n, q)
     H, d = q.shape[1], q.shape[2]
-    st = lib().sla_forward(_ptr(plan.buf), plan.nbytes, plan.n, plan.num_windows, _dtype_code(q.dtype),
-                           H, d, _ptr(q), _ptr(k), _ptr(v), _ptr(out), _stream(q.device))
-    _check(st, "sla_forward")
+    var = _variant(feature_map, eps)
+    if var is None:
+        st = lib().sla_forward(_ptr(plan.buf), plan.nbytes, plan.n, plan.num_windows, _dtype_code(q.dtype),
+                               H, d, _ptr(q), _ptr(k), _ptr(v), _ptr(out), _stream(q.device))
+        _check(st, "sla_forward")
+    else:
+        st = lib().sla_forward_ex(_ptr(plan.buf), plan.nbytes, plan.n, plan.num_windows,
+                                  _dtype_code(q.dtype), H, d, var[0], var[1], _ptr(q), _ptr(k), _ptr(v),
+                                  _ptr(out), _stream(q.device))
+        _check(st, "sla_forward_ex")
     return out
 
 
-def backward(plan: Plan, q, k, v, dout, dq=None, dk=None, dv=None):
+def backward(plan: Plan, q, k, v, dout, dq=None, dk=None, dv=None, feature_map=None, eps=None):
     torch = _torch()
     for name, t in (("q", q), ("k", k), ("v", v), ("dout", dout)):
         _check_rows(name, t, plan.n, q)
@@ -229,10 +258,17 @@ def backward(plan: Plan, q, k, v, dout, dq=None, dk=None, dv=None):
     for name, t in (("dq", dq), ("dk", dk), ("dv", dv)):
         _check_rows(name, t, plan.n, q)
     H, d = q.shape[1], q.shape[2]
-    st = lib().sla_backward(_ptr(plan.buf), plan.nbytes, plan.n, plan.num_windows, _dtype_code(q.dtype),
-                            H, d, _ptr(q), _ptr(k), _ptr(v), _ptr(dout), _ptr(dq), _ptr(dk), _ptr(dv),
-                            _stream(q.device))
-    _check(st, "sla_backward")
+    var = _variant(feature_map, eps)
+    if var is None:
+        st = lib().sla_backward(_ptr(plan.buf), plan.nbytes, plan.n, plan.num_windows, _dtype_code(q.dtype),
+                                H, d, _ptr(q), _ptr(k), _ptr(v), _ptr(dout), _ptr(dq), _ptr(dk), _ptr(dv),
+                                _stream(q.device))
+        _check(st, "sla_backward")
+    else:
+        st = lib().sla_backward_ex(_ptr(plan.buf), plan.nbytes, plan.n, plan.num_windows,
+                                   _dtype_code(q.dtype), H, d, var[0], var[1], _ptr(q), _ptr(k), _ptr(v),
+                                   _ptr(dout), _ptr(dq), _ptr(dk), _ptr(dv), _stream(q.device))
+        _check(st, "sla_backward_ex")
     return dq, dk, dv
 
 

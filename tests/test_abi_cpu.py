@@ -46,7 +46,7 @@ def test_only_the_abi_is_exported():
 
 
 def test_queries(L):
-    assert L.sla_abi_version() == 3
+    assert L.sla_abi_version() == 4
     assert L.sla_max_windows() == 16384
     assert L.sla_default_chunk_rows() == 64
     for s in range(5):
@@ -141,3 +141,26 @@ def test_scatter_argument_errors(L):
     big = L.sla_forward_scatter(FAKE, sla.plan_bytes(100, 8), 100, 8, 1, 128, 32, FAKE, FAKE, FAKE,
                                 FAKE, FAKE, sla.scatter_workspace_bytes(100, 128, 32), None)
     assert big == sla.SLA_E_UNSUPPORTED
+
+
+def test_variant_argument_errors(L):
+    nb = sla.plan_bytes(100, 8)
+    f = lambda fm, eps, **kw: L.sla_forward_ex(  # noqa: E731
+        FAKE, nb, kw.get("n", 100), 8, 1, 4, kw.get("d", 32), fm, eps, FAKE, FAKE, FAKE,
+        kw.get("o", FAKE), None)
+    b = lambda fm, eps: L.sla_backward_ex(FAKE, nb, 100, 8, 1, 4, 32, fm, eps,  # noqa: E731
+                                          *([FAKE] * 7), None)
+    for call in (f, b):
+        assert call(2, 0.0) == sla.SLA_E_ARG             # unknown feature map
+        assert call(-1, 0.0) == sla.SLA_E_ARG
+        assert call(1, -1e-6) == sla.SLA_E_ARG           # eps < 0
+        assert call(1, float("nan")) == sla.SLA_E_ARG
+        assert call(0, float("inf")) == sla.SLA_E_ARG
+    assert f(1, 1e-6, d=24) == sla.SLA_E_UNSUPPORTED     # the shared checks still apply
+    assert f(1, 1e-6, o=FAKE + 2) == sla.SLA_E_ARG
+    assert f(1, 1e-6, n=0) == sla.SLA_OK
+    assert f(0, 0.0, n=0) == sla.SLA_OK
+    with pytest.raises(ValueError):
+        sla._variant("gelu", 0.0)
+    assert sla._variant(None, None) is None
+    assert sla._variant("relu", None) == (1, 0.0) and sla._variant(None, 1e-3) == (0, 1e-3)

@@ -78,42 +78,61 @@ def check_plan(S, plan, ids, W, chunk_rows, offsets_in=None):
     return o_ref, (p_ref if ids is not None else None)
 
 
-def run_forward(S, plan, wl_q, wl_k, wl_v, dtype):
+def run_forward(S, plan, wl_q, wl_k, wl_v, dtype, fmap=None, eps=None):
     import torch
 
     q, k, v = to_dev(wl_q, dtype), to_dev(wl_k, dtype), to_dev(wl_v, dtype)
     o = torch.full_like(q, float("nan"))
-    S.forward(plan, q, k, v, out=o)
+    S.forward(plan, q, k, v, out=o, feature_map=fmap, eps=eps)
     torch.cuda.synchronize()
     return to_host64(o, dtype)
 
 
-def forward_parity(S, ids, offsets, n, W, q, k, v, dtype, chunk_rows=0, label=""):
+def _oracle_variant(fmap, eps):
+    return ("elu1" if fmap is None else fmap), (0.0 if eps is None else eps)
+
+
+def _match_nan(got, ref, rows, label):
+    """Rows of a window: NaN exactly where the oracle has NaN (a zero normaliser
+    with eps = 0); those entries are then left out of the error."""
+    bad = np.isnan(ref) & rows[:, None, None]
+    assert np.array_equal(np.isnan(got) & rows[:, None, None], bad), f"{label}: NaN positions differ"
+    if bad.any():
+        got, ref = np.where(bad, 0.0, got), np.where(bad, 0.0, ref)
+    return got, ref
+
+
+def forward_parity(S, ids, offsets, n, W, q, k, v, dtype, chunk_rows=0, label="", fmap=None, eps=None):
     plan = build(S, ids=ids, W=W, chunk_rows=chunk_rows, offsets=offsets, n=n)
     off, perm = check_plan(S, plan, ids, W, chunk_rows, offsets)
-    got = run_forward(S, plan, q, k, v, dtype)
+    got = run_forward(S, plan, q, k, v, dtype, fmap, eps)
     w = lambda a: oracle.widen(a, dtype)  # noqa: E731
-    ref = oracle.sla_forward_ref(w(q), w(k), w(v), off, perm)
-    rows = ~np.isnan(ref[:, 0, 0])
+    with np.errstate(invalid="ignore", divide="ignore"):
+        ref = oracle.sla_forward_ref(w(q), w(k), w(v), off, perm, *_oracle_variant(fmap, eps))
+    rows = np.zeros(n, dtype=bool)
+    rows[perm if perm is not None else np.arange(off[-1])] = True
+    assert np.isnan(ref[~rows]).all()
+    g0, r0 = _match_nan(got, ref, rows, label)
     floor = 1e-3 * max(float(np.abs(w(v)).max()) if v.size else 1.0, 1e-30)
-    err = rel_err_per_head(got, ref, floor, rows)
-    _say(f"[fwd {label}] n={n} W={W} dtype={dtype} rel_err={err:.3e} p99.9={p999(got[rows], ref[rows]):.3e}")
+    err = rel_err_per_head(g0, r0, floor, rows)
+    _say(f"[fwd {label}] n={n} W={W} dtype={dtype} rel_err={err:.3e} p99.9={p999(g0[rows], r0[rows]):.3e}")
     assert err <= TOL[dtype], f"{label}: forward relative error {err:.3e}"
     return got, ref
 
 
-def backward_parity(S, ids, offsets, n, W, q, k, v, do, dtype, chunk_rows=0, label=""):
+def backward_parity(S, ids, offsets, n, W, q, k, v, do, dtype, chunk_rows=0, label="", fmap=None,
+                    eps=None):
     import torch
 
     plan = build(S, ids=ids, W=W, chunk_rows=chunk_rows, offsets=offsets, n=n)
     off, perm = check_plan(S, plan, ids, W, chunk_rows, offsets)
     tq, tk, tv, tdo = (to_dev(a, dtype) for a in (q, k, v, do))
     outs = [torch.full_like(tq, float("nan")) for _ in range(3)]
-    S.backward(plan, tq, tk, tv, tdo, *outs)
+    S.backward(plan, tq, tk, tv, tdo, *outs, feature_map=fmap, eps=eps)
     torch.cuda.synchronize()
     got = [to_host64(t, dtype) for t in outs]
     w = lambda a: oracle.widen(a, dtype)  # noqa: E731
-    ref = oracle.sla_backward_ref(w(q), w(k), w(v), w(do), off, perm)
+    ref = oracle.sla_backward_ref(w(q), w(k), w(v), w(do), off, perm, *_oracle_variant(fmap, eps))
     rows = ~np.isnan(ref[0][:, 0, 0])
     mv, mdo = float(np.abs(w(v)).max()), float(np.abs(w(do)).max())
     floors = (1e-3 * mdo * mv, 1e-3 * mdo * mv, 1e-3 * mdo)
@@ -376,3 +395,108 @@ def test_forward_scatter_shapes(sla, dtype, shape):
     n, W = ids.size, lengths.size
     q, k, v = (workloads.normal_values(rng, n, H, d, dtype) for _ in range(3))
     scatter_parity(sla, ids, None, n, W, q, k, v, dtype, label=f"shape{shape}")
+
+
+# ------------------------------------------- feature-map variants and epsilon
+VARIANTS = [("relu", 0.0), ("relu", 1e-3), ("elu1", 0.5)]
+
+
+@pytest.mark.parametrize("fmap,eps", VARIANTS)
+@pytest.mark.parametrize("cfg", [1, 2, 3])
+def test_variant_forward_config(sla, cfg, fmap, eps):
+    # with eps = 0 some ReLU rows of config 3 (d = 16, singleton windows) have a
+    # zero normaliser: NaN on both sides, checked position by position
+    wl = workloads.make_config(cfg)
+    forward_parity(sla, wl["ids"], wl["offsets"], wl["n"], wl["num_windows"], wl["q"], wl["k"], wl["v"],
+                   wl["dtype"], label=f"cfg{cfg}-{fmap}-{eps}", fmap=fmap, eps=eps)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "f16", "bf16"])
+@pytest.mark.parametrize("shape", [(2, 32), (8, 16), (3, 32)])
+def test_variant_forward_shapes(sla, dtype, shape):
+    H, d = shape
+    rng = np.random.default_rng([41, H, d, len(dtype)])
+    lengths = _adversarial_lengths(rng, 128)
+    ids = workloads.ids_from_lengths(lengths, rng)
+    n, W = ids.size, lengths.size
+    q, k, v = (workloads.normal_values(rng, n, H, d, dtype) for _ in range(3))
+    for fmap, eps in (("relu", 1e-4), ("elu1", 0.25)):
+        forward_parity(sla, ids, None, n, W, q, k, v, dtype, label=f"shape{shape}-{fmap}", fmap=fmap, eps=eps)
+
+
+@pytest.mark.parametrize("fmap,eps", [("relu", 1e-6), ("relu", 0.05), ("elu1", 1e-3)])
+def test_variant_backward_config5(sla, fmap, eps):
+    wl = workloads.make_config(5)
+    backward_parity(sla, wl["ids"], None, wl["n"], wl["num_windows"], wl["q"], wl["k"], wl["v"], wl["dout"],
+                    wl["dtype"], label=f"cfg5-{fmap}-{eps}", fmap=fmap, eps=eps)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "f16", "bf16"])
+@pytest.mark.parametrize("shape", [(2, 32), (8, 16), (3, 32)])
+def test_variant_backward_shapes(sla, dtype, shape):
+    H, d = shape
+    rng = np.random.default_rng([42, H, d, len(dtype)])
+    lengths = _adversarial_lengths(rng, 128)
+    ids = workloads.ids_from_lengths(lengths, rng)
+    n, W = ids.size, lengths.size
+    q, k, v, do = (workloads.normal_values(rng, n, H, d, dtype) for _ in range(4))
+    for fmap, eps in (("relu", 1e-4), ("elu1", 0.25)):
+        backward_parity(sla, ids, None, n, W, q, k, v, do, dtype, label=f"shape{shape}-{fmap}", fmap=fmap,
+                        eps=eps)
+
+
+def test_variant_default_is_plain(sla):
+    # the _ex calls with elu + 1 and eps = 0 are the plain calls, bit for bit
+    import torch
+
+    wl = workloads.make_config(5)
+    plan = build(sla, ids=wl["ids"], W=wl["num_windows"])
+    tq, tk, tv, tdo = (to_dev(wl[x], "f16") for x in ("q", "k", "v", "dout"))
+    assert torch.equal(sla.forward(plan, tq, tk, tv), sla.forward(plan, tq, tk, tv, feature_map="elu1", eps=0.0))
+    a = sla.backward(plan, tq, tk, tv, tdo)
+    b = sla.backward(plan, tq, tk, tv, tdo, feature_map="elu1", eps=0.0)
+    torch.cuda.synchronize()
+    assert all(torch.equal(x, y) for x, y in zip(a, b))
+
+
+@pytest.mark.parametrize("dtype", ["f32", "f16", "bf16"])
+def test_variant_relu_zero_rows(sla, dtype):
+    # a query with no positive entry, and a window whose keys have none: o = 0
+    # exactly with eps > 0, NaN with eps = 0 (the oracle agrees position by position)
+    rng = np.random.default_rng([43, len(dtype)])
+    lengths = np.array([40, 1, 70, 5, 200, 1])
+    ids = workloads.ids_from_lengths(lengths, rng)
+    n, H, d = ids.size, 2, 32
+    q, k, v = (rng.standard_normal((n, H, d)).astype(np.float32) for _ in range(3))
+    zq = rng.random(n) < 0.1                                  # queries with no positive entry
+    q[zq] = -np.abs(q[zq])
+    zk = (ids == 1) | (ids == 3)                              # windows whose keys have none
+    k[zk] = -np.abs(k[zk])
+    q, k, v = (workloads.cast_values(x, dtype) for x in (q, k, v))
+    got, _ = forward_parity(sla, ids, None, n, lengths.size, q, k, v, dtype, label="relu-zero", fmap="relu",
+                            eps=1e-3)
+    assert np.all(got[zq] == 0.0) and np.all(got[zk] == 0.0)
+    got0, ref0 = forward_parity(sla, ids, None, n, lengths.size, q, k, v, dtype, label="relu-zero-eps0",
+                                fmap="relu", eps=0.0)
+    assert np.isnan(got0[zq | zk]).all() and np.isnan(ref0[zq | zk]).all()
+
+
+def test_variant_relu_absent_features(sla):
+    # features that no key of a window has (z_e = 0) while the queries are large
+    # on them and small elsewhere: the state-gradient operands must stay finite in
+    # fp16 (those features reach neither dk nor dv) and match the oracle
+    rng = np.random.default_rng(44)
+    lengths = np.array([300, 40, 3, 1, 65])
+    ids = workloads.ids_from_lengths(lengths, rng)
+    n, H, d = ids.size, 2, 32
+    q, k, v, do = (rng.standard_normal((n, H, d)).astype(np.float32) for _ in range(4))
+    k[:, :, :8] = -np.abs(k[:, :, :8]) - 0.01                 # features 0..7 absent from every key
+    q[:, :, :8] = np.abs(q[:, :, :8]) * 60 + 100
+    few = rng.random(n) < 0.3                                 # rows active on one tiny feature only
+    q[few, :, 8:] = -1.0
+    q[few, :, 8] = 1e-3
+    q, k, v, do = (workloads.cast_values(x, "f16") for x in (q, k, v, do))
+    W = lengths.size
+    for eps in (1e-6, 0.1):
+        forward_parity(sla, ids, None, n, W, q, k, v, "f16", label=f"absent-{eps}", fmap="relu", eps=eps)
+        backward_parity(sla, ids, None, n, W, q, k, v, do, "f16", label=f"absent-{eps}", fmap="relu", eps=eps)
