@@ -305,6 +305,7 @@ def main():
             torch.cuda.synchronize()
             del a, b
     step_bytes = (fwd_bytes + bwd_bytes + 8 * n) if training else fwd_bytes
+    copy_gbs = measure_copy(torch, dev)
 
     nonempty = int((np.diff(plans[0].offsets.cpu().numpy()) > 0).sum())
     frames = base.get("frames", 1)
@@ -340,6 +341,9 @@ def main():
             "traffic": stored_traffic(dom) if variant is None else None,
             "algorithmic_bytes": dom_bytes,
             "avg_ms": dom_ms,
+            # a plain device-to-device copy on the same GPU, for scale
+            "copy_gbs": copy_gbs,
+            "frac_of_copy": achieved / copy_gbs if copy_gbs else None,
         },
         "breakdown_ms": {"build": t_build, "forward": t_fwd, "backward": t_bwd},
         "step_roofline_frac": step_bytes / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS,
@@ -406,6 +410,35 @@ def compare_scatter(torch, sla, workloads, dev):
             "dtype": "f16", "heads": H, "head_dim": d, "data": "synthetic", "comparison": rows}
 
 
+def measure_copy(torch, dev, nbytes=COPY_PROBE_BYTES, reps=5):
+    """GB/s (read + write bytes) of a plain device-to-device copy of `nbytes`,
+    buffers rotated so that the Infinity Cache cannot serve repeats."""
+    bufs = [torch.empty(nbytes, dtype=torch.uint8, device=dev).fill_(1) for _ in range(3)]
+    dst = torch.empty_like(bufs[0])
+    dst.copy_(bufs[0])
+    torch.cuda.synchronize()
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for i in range(reps):
+        dst.copy_(bufs[i % 3])
+    t1.record()
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / reps
+    del bufs, dst
+    return 2 * nbytes / (ms * 1e-3) / 1e9
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(base, training, budget_s, variant=None):
     """The CPU oracle as it stands, on whole frames of the same workload."""
     import oracle
@@ -448,6 +481,7 @@ def cpu_baseline(base, training, budget_s, variant=None):
         "unit": "voxels/s",
         "cores": 1,
         "kind": "oracle",
+        "cpu_model": cpu_model(),
         "sample": f"{reps} whole frame(s) of N={base['n']} voxels, "
                   f"{'segments+forward+backward' if training else 'segments+forward'} in numpy float64, "
                   f"{el:.1f} s wall, 1 thread",

@@ -45,6 +45,12 @@ What is computed, and the passage it follows
 * ``sla_backward_ref``: the paper trains the model but does not write the
   backward pass; the gradients here are derived from Eq. (3) by the chain rule
   (derivation in the docstring).
+* ``sla_projected_forward_ref``: Sec. 3.2 maps every voxel of the scene to Q, K
+  and V with one shared projection layer before the attention, and the attention
+  block projects its output back.  Reading taken: linear layers with bias in the
+  usual [out, in] weight layout, Q = X W_q^T + b_q (likewise K, V) with
+  W_qkv = [W_q; W_k; W_v] stacked by rows, and Y = SLA(Q, K, V) W_o^T + b_o, heads
+  split from the C channels as in the plain path.
 """
 from __future__ import annotations
 
@@ -62,6 +68,7 @@ __all__ = [
     "chunk_plan_ref",
     "sla_forward_ref",
     "sla_backward_ref",
+    "sla_projected_forward_ref",
 ]
 
 
@@ -286,3 +293,31 @@ def sla_backward_ref(q, k, v, dout, offsets, perm=None, feature_map_name="elu1",
         dq[rows] = dfq * fdphi(qq)
         dk[rows] = dfk * fdphi(kk)
     return dq, dk, dv
+
+
+# ------------------------------------------------------------ projected forward
+def sla_projected_forward_ref(x, w_qkv, b_qkv, w_o, b_o, heads, offsets, perm=None,
+                              feature_map_name="elu1", eps=0.0):
+    """Projection layer, SLA and output projection (Sec. 3.2, reading above).
+
+    x: float64 [n, C] voxel features in original row order, C = heads * d.
+    w_qkv: [3C, C] (rows 0..C-1 give Q, C..2C-1 K, 2C..3C-1 V); b_qkv: [3C] or None.
+    w_o: [C, C]; b_o: [C] or None.  Returns (o, y): o [n, heads, d] the SLA output
+    (NaN for rows in no window) and y [n, C] = o W_o^T + b_o.
+    """
+    x = np.asarray(x, dtype=np.float64)
+    w_qkv = np.asarray(w_qkv, dtype=np.float64)
+    w_o = np.asarray(w_o, dtype=np.float64)
+    n, C = x.shape
+    if C % heads or w_qkv.shape != (3 * C, C) or w_o.shape != (C, C):
+        raise ValueError("shapes: x [n, C], w_qkv [3C, C], w_o [C, C], C a multiple of heads")
+    d = C // heads
+    qkv = x @ w_qkv.T
+    if b_qkv is not None:
+        qkv = qkv + np.asarray(b_qkv, dtype=np.float64)
+    q, k, v = (qkv[:, i * C:(i + 1) * C].reshape(n, heads, d) for i in range(3))
+    o = sla_forward_ref(q, k, v, offsets, perm, feature_map_name, eps)
+    y = o.reshape(n, C) @ w_o.T
+    if b_o is not None:
+        y = y + np.asarray(b_o, dtype=np.float64)
+    return o, y

@@ -461,3 +461,86 @@ def variant_backward_pin_failures(bwd, fwd, seg):
         if max(rel_err(x, y) for x, y in zip(a, b)) > 1e-13:
             fails.append(f"relu_shift_is_elu_grad_eps{eps}")
     return fails
+
+
+# ----------------------------------------------------------- projected forward
+# ``fwd_proj(x, w_qkv, b_qkv, w_o, b_o, heads, offsets, perm, fmap, eps) -> (o, y)``:
+# the projection layer of Sec. 3.2, SLA, and the output projection.
+def brute_projected(x, w_qkv, b_qkv, w_o, b_o, heads, ids, W, fmap="elu1", eps=0.0):
+    """Plain loops: every projection as a sum over input channels, the attention
+    as the quadratic form, then the output projection."""
+    n, C = x.shape
+    d = C // heads
+    qkv = np.zeros((n, 3 * C))
+    for r in range(n):
+        for j in range(3 * C):
+            acc = 0.0 if b_qkv is None else float(b_qkv[j])
+            for c in range(C):
+                acc += x[r, c] * w_qkv[j, c]
+            qkv[r, j] = acc
+    q = qkv[:, :C].reshape(n, heads, d)
+    k = qkv[:, C:2 * C].reshape(n, heads, d)
+    v = qkv[:, 2 * C:].reshape(n, heads, d)
+    o = brute_forward(q, k, v, ids, W, fmap, eps)
+    of = o.reshape(n, C)
+    y = np.full((n, C), np.nan)
+    for r in range(n):
+        if np.isnan(of[r]).any():
+            continue
+        for j in range(C):
+            acc = 0.0 if b_o is None else float(b_o[j])
+            for c in range(C):
+                acc += of[r, c] * w_o[j, c]
+            y[r, j] = acc
+    return o, y
+
+
+def projected_pin_failures(fwd_proj, seg, fwd):
+    fails = []
+    rng = np.random.default_rng(70)
+    # 1. brute force, heads in {1, 2, 3}, with and without biases, both maps
+    for seed, heads, d, bias, fmap, eps in ((0, 2, 2, True, "elu1", 0.0), (1, 1, 3, False, "elu1", 0.0),
+                                            (2, 3, 2, True, "relu", 0.2), (3, 2, 3, True, "elu1", 0.5)):
+        ids, _, _, _, _ = tiny_case(80 + seed, windows=4, max_len=5)
+        n, C = len(ids), heads * d
+        x = rng.standard_normal((n, C))
+        wq = rng.standard_normal((3 * C, C)) / np.sqrt(C)
+        wo = rng.standard_normal((C, C)) / np.sqrt(C)
+        bq = rng.standard_normal(3 * C) if bias else None
+        bo = rng.standard_normal(C) if bias else None
+        W = int(ids.max()) + 1
+        perm, off, _ = seg(ids, W)
+        with np.errstate(invalid="ignore", divide="ignore"):
+            o, y = fwd_proj(x, wq, bq, wo, bo, heads, off, perm, fmap, eps)
+            ob, yb = brute_projected(x, wq, bq, wo, bo, heads, ids, W, fmap, eps)
+        if rel_err(o, ob) > 1e-12 or rel_err(y, yb) > 1e-12:
+            fails.append(f"projected_bruteforce[{seed}]")
+    # 2. block structure: W_q = I, W_k = 2 I, W_v = a permutation, W_o = I, no bias
+    #    gives the plain SLA of (x, 2 x, x P^T)
+    ids, _, _, _, _ = tiny_case(90, windows=5, max_len=6)
+    heads, d = 2, 3
+    n, C = len(ids), heads * d
+    x = rng.standard_normal((n, C))
+    P = np.eye(C)[rng.permutation(C)]
+    wq = np.concatenate([np.eye(C), 2 * np.eye(C), P])
+    W = int(ids.max()) + 1
+    perm, off, _ = seg(ids, W)
+    o, y = fwd_proj(x, wq, None, np.eye(C), None, heads, off, perm, "elu1", 0.0)
+    ref = fwd(x.reshape(n, heads, d), 2 * x.reshape(n, heads, d), (x @ P.T).reshape(n, heads, d), off, perm)
+    if rel_err(o, ref) > 1e-14 or rel_err(y, ref.reshape(n, C)) > 1e-14:
+        fails.append("projected_blocks")
+    # 3. biases: b_v = c shifts every o by c (weights sum to 1), so y by W_o c;
+    #    b_o shifts y
+    wq = rng.standard_normal((3 * C, C)) / np.sqrt(C)
+    wo = rng.standard_normal((C, C)) / np.sqrt(C)
+    o0, y0 = fwd_proj(x, wq, None, wo, None, heads, off, perm, "elu1", 0.0)
+    c = rng.standard_normal(C)
+    bq = np.concatenate([np.zeros(2 * C), c])
+    o1, y1 = fwd_proj(x, wq, bq, wo, None, heads, off, perm, "elu1", 0.0)
+    if rel_err(o1, o0 + c.reshape(heads, d)) > 1e-13 or rel_err(y1, y0 + wo @ c) > 1e-13:
+        fails.append("projected_value_bias")
+    bo = rng.standard_normal(C)
+    _, y2 = fwd_proj(x, wq, None, wo, bo, heads, off, perm, "elu1", 0.0)
+    if rel_err(y2, y0 + bo) > 1e-13:
+        fails.append("projected_output_bias")
+    return fails

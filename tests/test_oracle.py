@@ -341,3 +341,28 @@ def test_variant_backward_mutant_is_caught(name):
         fails = pins.variant_backward_pin_failures(mod.sla_backward_ref, oracle.sla_forward_ref,
                                                    oracle.segments_ref)
     assert fails, f"planted mistake {name} passed every variant backward pin"
+
+
+# ------------------------------------------------------------ projected forward
+def test_projected_pins():
+    assert pins.projected_pin_failures(oracle.sla_projected_forward_ref, oracle.segments_ref,
+                                       oracle.sla_forward_ref) == []
+
+
+PROJECTED_MUTANTS = {
+    "q_k_blocks_swapped": [("q, k, v = (qkv[:, i * C:(i + 1) * C]", "k, q, v = (qkv[:, i * C:(i + 1) * C]", 0)],
+    "output_weight_not_transposed": [("y = o.reshape(n, C) @ w_o.T", "y = o.reshape(n, C) @ w_o", 0)],
+    "input_weight_not_transposed": [("qkv = x @ w_qkv.T", "qkv = x @ w_qkv.reshape(C, 3 * C)", 0)],
+    "heads_interleaved": [(".reshape(n, heads, d) for i in range(3))",
+                          ".reshape(n, d, heads).transpose(0, 2, 1) for i in range(3))", 0)],
+    "bias_dropped": [("qkv = qkv + np.asarray(b_qkv, dtype=np.float64)", "qkv = qkv", 0)],
+}
+
+
+@pytest.mark.parametrize("name", sorted(PROJECTED_MUTANTS))
+def test_projected_mutant_is_caught(name):
+    mod = _oracle_from_source(PROJECTED_MUTANTS[name])
+    with np.errstate(all="ignore"):
+        fails = pins.projected_pin_failures(mod.sla_projected_forward_ref, oracle.segments_ref,
+                                            oracle.sla_forward_ref)
+    assert fails, f"planted mistake {name} passed every projected pin"
