@@ -49,6 +49,9 @@ def parse():
     p.add_argument("--cpu-seconds", type=float, default=12.0)
     p.add_argument("--copy-probe", action="store_true",
                    help="after timing, run plain copies of known size (calibrates PMC byte counters)")
+    p.add_argument("--projected", action="store_true",
+                   help="time the projection fused into SLA (sla_forward_projected) against the unfused "
+                        "chain: torch linear, sla_forward, torch linear")
     p.add_argument("--compare-scatter", action="store_true",
                    help="instead of the training step: forward time and memory of the chunk-wise path "
                         "against the naive scatter-based one, as sequence length and window length grow")
@@ -162,6 +165,9 @@ def main():
     sla.lib()
     if args.compare_scatter:
         print(json.dumps(compare_scatter(torch, sla, workloads, dev)), flush=True)
+        return
+    if args.projected:
+        print(json.dumps(bench_projected(torch, sla, workloads, dev, args)), flush=True)
         return
 
     cfg = args.config
@@ -353,6 +359,88 @@ def main():
     if not args.no_cpu:
         out["cpu_baseline"] = cpu_baseline(base, training, args.cpu_seconds, variant)
     print(json.dumps(out), flush=True)
+
+
+def bench_projected(torch, sla, workloads, dev, args):
+    """Projection layer + SLA + output projection on one frame (plan built outside
+    the timed region): the fused path against the unfused chain, both timed with
+    graph replay over rotated buffer sets."""
+    import torch.nn.functional as Fn
+
+    cfg = args.config if args.config in (2, 3) else 2
+    base = workloads.make_config(cfg, with_grad=False)
+    n, H, d, W, dt = base["n"], base["heads"], base["head_dim"], base["num_windows"], base["dtype"]
+    C = H * d
+    tdt = {"f16": torch.float16, "bf16": torch.bfloat16}[dt]
+    e = 2
+    gen = torch.Generator(device="cpu").manual_seed(11)
+    w_qkv = (torch.randn(3 * C, C, generator=gen) / C ** 0.5).to(tdt).to(dev)
+    b_qkv = (0.1 * torch.randn(3 * C, generator=gen)).to(tdt).to(dev)
+    w_o = (torch.randn(C, C, generator=gen) / C ** 0.5).to(tdt).to(dev)
+    b_o = (0.1 * torch.randn(C, generator=gen)).to(tdt).to(dev)
+    per_set = 6 * n * C * e
+    nsets = max(3, int(np.ceil(2 * MALL_BYTES / per_set)) + 1)
+    sets = []
+    for s_ in range(nsets):
+        wl = workloads.shuffled(base, [cfg, 2, s_])
+        x = torch.randn(n, C, generator=gen).to(tdt).to(dev)
+        plan = sla.build_segments(torch.from_numpy(wl["ids"]).to(dev), num_windows=W, want_perm=False)
+        sets.append({"x": x, "plan": plan, "o": torch.empty(n, H, d, dtype=tdt, device=dev),
+                     "y": torch.empty(n, C, dtype=tdt, device=dev)})
+    torch.cuda.synchronize()
+
+    def fused(st):
+        sla.forward_projected(st["plan"], st["x"], w_qkv, w_o, H, b_qkv, b_o, st["o"], st["y"])
+
+    def unfused(st):
+        qkv = Fn.linear(st["x"], w_qkv, b_qkv)
+        q, k, v = (qkv[:, i * C:(i + 1) * C].contiguous().view(n, H, d) for i in range(3))
+        o = sla.forward(st["plan"], q, k, v, out=st["o"])
+        st["y"].copy_(Fn.linear(o.view(n, C), w_o, b_o))
+
+    def timed(fn, reps):
+        for i in range(args.warmup):
+            fn(sets[i % nsets])
+        torch.cuda.synchronize()
+        graphs = []
+        cap = torch.cuda.Stream(dev)
+        cap.wait_stream(torch.cuda.current_stream(dev))
+        with torch.cuda.stream(cap):
+            for s_ in range(nsets):
+                g = torch.cuda.CUDAGraph()
+                with torch.cuda.graph(g, stream=cap):
+                    fn(sets[s_])
+                graphs.append(g)
+        torch.cuda.current_stream(dev).wait_stream(cap)
+        for g in graphs:
+            g.replay()
+        torch.cuda.synchronize()
+        t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        t0.record()
+        for i in range(reps):
+            graphs[i % nsets].replay()
+        t1.record()
+        torch.cuda.synchronize()
+        return t0.elapsed_time(t1) / reps * 1e3
+
+    reps = max(50, args.steps)
+    t_fused = timed(fused, reps)
+    t_unfused = timed(unfused, reps)
+    fused_bytes = 4 * n * C * e     # x read, o written; o read, y written
+    unfused_bytes = 10 * n * C * e  # + q, k, v written and read, and their copies' extra pass
+    return {
+        "mode": "projected",
+        "workload": base["name"],
+        "n": n, "heads": H, "head_dim": d, "dtype": dt, "buffer_sets": nsets,
+        "fused_us": t_fused,
+        "unfused_us": t_unfused,
+        "speedup": t_unfused / t_fused,
+        "fused_algorithmic_bytes": fused_bytes,
+        "fused_gbs": fused_bytes / (t_fused * 1e-6) / 1e9,
+        "fused_frac_of_hbm_peak": fused_bytes / (t_fused * 1e-6) / 1e9 / HBM_PEAK_GBS,
+        "unfused_chain": "torch linear (x W_qkv^T + b), three contiguous q/k/v copies, sla_forward, "
+                         "torch linear (o W_o^T + b)",
+    }
 
 
 def compare_scatter(torch, sla, workloads, dev):

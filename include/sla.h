@@ -197,6 +197,33 @@ sla_status_t sla_backward_ex(const void* plan, size_t plan_bytes, int64_t n, int
                              void* dv, sla_stream_t stream);
 
 /*
+ * Projection layer, SLA and output projection in two launches, without q, k, v
+ * in memory.  Sec. 3.2 maps every voxel of the scene to Q, K and V with one
+ * shared projection layer before the attention; the attention block projects
+ * its output back.  Read as linear layers with bias in the [out, in] weight
+ * layout:
+ *     [q | k | v] = x W_qkv^T + b_qkv,   o = SLA(q, k, v)  (as sla_forward_ex),
+ *     y = o W_o^T + b_o.
+ *   x      [n, C] features in original row order, C = heads * head_dim;
+ *   w_qkv  [3C, C]: rows 0..C-1 give q, C..2C-1 k, 2C..3C-1 v (channel c of q,
+ *          k, v is head c / head_dim as everywhere);
+ *   b_qkv  [3C] or NULL (no bias);  w_o [C, C];  b_o [C] or NULL;
+ *   o      [n, C] output: SLA's output before the output projection;
+ *   y      [n, C] output.
+ * All in `dtype`, which must be SLA_F16 or SLA_BF16; C must be 64 or 128
+ * (else SLA_E_UNSUPPORTED).  x, w_qkv, w_o, o, y 16-byte aligned.  Rows in no
+ * window get neither o nor y.  The projections run on the matrix cores with
+ * fp32 accumulation; q, k, v are rounded to `dtype` (as if stored) before the
+ * attention, o is rounded before the output projection.
+ */
+sla_status_t sla_forward_projected(const void* plan, size_t plan_bytes, int64_t n,
+                                   int32_t num_windows, sla_dtype_t dtype, int32_t heads,
+                                   int32_t head_dim, sla_feature_map_t feature_map, float eps,
+                                   const void* x, const void* w_qkv, const void* b_qkv,
+                                   const void* w_o, const void* b_o, void* o, void* y,
+                                   sla_stream_t stream);
+
+/*
  * The naive scatter-based forward that Sec. 3.2 ("Hardware Efficient
  * Implementation") contrasts with the chunk-wise kernel, kept as a comparator
  * for Fig. 4's time-and-memory comparison: the kv matrix phi(k)^T v of every

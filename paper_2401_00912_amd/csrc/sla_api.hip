@@ -14,6 +14,10 @@ hipError_t launch_forward(const void* plan, int32_t n, int32_t W, int dtype, int
 hipError_t launch_backward(const void* plan, int32_t n, int32_t W, int dtype, int32_t H, int32_t d,
                            int phi, float eps, const void* q, const void* k, const void* v,
                            const void* dout, void* dq, void* dk, void* dv, hipStream_t stream);
+hipError_t launch_forward_projected(const void* plan, int32_t n, int32_t W, int dtype, int32_t H,
+                                    int32_t d, int phi, float eps, const void* x, const void* wqkv,
+                                    const void* bqkv, const void* wo, const void* bo, void* o,
+                                    void* y, hipStream_t stream);
 size_t naive_workspace_bytes(int64_t n, int32_t H, int32_t d);
 hipError_t launch_forward_scatter(const void* plan, int32_t n, int32_t W, int dtype, int32_t H,
                                   int32_t d, const void* q, const void* k, const void* v,
@@ -22,7 +26,7 @@ hipError_t launch_forward_scatter(const void* plan, int32_t n, int32_t W, int dt
 
 namespace {
 
-constexpr int32_t kAbiVersion = 4;
+constexpr int32_t kAbiVersion = 5;
 
 bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
 
@@ -177,6 +181,29 @@ SLA_EXPORT sla_status_t sla_backward_ex(const void* plan, size_t plan_bytes, int
                                         sla_stream_t stream) {
   return backward_impl(plan, plan_bytes, n, num_windows, dtype, heads, head_dim, (int)feature_map,
                        eps, q, k, v, dout, dq, dk, dv, stream);
+}
+
+SLA_EXPORT sla_status_t sla_forward_projected(const void* plan, size_t plan_bytes, int64_t n,
+                                              int32_t num_windows, sla_dtype_t dtype,
+                                              int32_t heads, int32_t head_dim,
+                                              sla_feature_map_t feature_map, float eps,
+                                              const void* x, const void* w_qkv, const void* b_qkv,
+                                              const void* w_o, const void* b_o, void* o, void* y,
+                                              sla_stream_t stream) {
+  const sla_status_t st = check_tensor_args(n, num_windows, (int)dtype, heads, head_dim, plan, plan_bytes);
+  if (st != SLA_OK) return st;
+  if (!variant_ok((int)feature_map, eps)) return SLA_E_ARG;
+  if (dtype != SLA_F16 && dtype != SLA_BF16) return SLA_E_UNSUPPORTED;
+  const int64_t C = (int64_t)heads * head_dim;
+  if (C != 64 && C != 128) return SLA_E_UNSUPPORTED;
+  if (n == 0) return SLA_OK;
+  if (!x || !w_qkv || !w_o || !o || !y) return SLA_E_ARG;
+  if (!aligned(x, 16) || !aligned(w_qkv, 16) || !aligned(w_o, 16) || !aligned(o, 16) ||
+      !aligned(y, 16) || !aligned(b_qkv, 2) || !aligned(b_o, 2))
+    return SLA_E_ARG;
+  return hip_status(sla::launch_forward_projected(plan, (int32_t)n, num_windows, (int)dtype, heads,
+                                                  head_dim, (int)feature_map, eps, x, w_qkv, b_qkv,
+                                                  w_o, b_o, o, y, static_cast<hipStream_t>(stream)));
 }
 
 SLA_EXPORT size_t sla_scatter_workspace_bytes(int64_t n, int32_t heads, int32_t head_dim) {

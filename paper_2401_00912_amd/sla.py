@@ -12,6 +12,8 @@ Functions mirror the C ABI in include/sla.h:
         -> (dq, dk, dv)
         (feature_map "elu1" | "relu" and eps >= 0 select sla_forward_ex /
         sla_backward_ex; leaving both None calls sla_forward / sla_backward)
+    forward_projected(plan, x, w_qkv, w_o, heads, b_qkv=None, b_o=None, o=None, y=None,
+                      feature_map="elu1", eps=0.0) -> (o, y)
     scatter_workspace_bytes(n, heads, head_dim)
     forward_scatter(plan, q, k, v, out=None, workspace=None) -> o   (naive comparator)
 """
@@ -39,6 +41,7 @@ EXPORTED = (
     "sla_backward",
     "sla_forward_ex",
     "sla_backward_ex",
+    "sla_forward_projected",
     "sla_scatter_workspace_bytes",
     "sla_forward_scatter",
 )
@@ -98,6 +101,8 @@ def lib() -> ctypes.CDLL:
     L.sla_forward_ex.argtypes = [vp, sz, i64, i32, en, i32, i32, en, f32, vp, vp, vp, vp, vp]
     L.sla_backward_ex.restype = ctypes.c_int
     L.sla_backward_ex.argtypes = [vp, sz, i64, i32, en, i32, i32, en, f32, vp, vp, vp, vp, vp, vp, vp, vp]
+    L.sla_forward_projected.restype = ctypes.c_int
+    L.sla_forward_projected.argtypes = [vp, sz, i64, i32, en, i32, i32, en, f32, vp, vp, vp, vp, vp, vp, vp, vp]
     L.sla_scatter_workspace_bytes.restype = sz
     L.sla_scatter_workspace_bytes.argtypes = [i64, i32, i32]
     L.sla_forward_scatter.restype = ctypes.c_int
@@ -270,6 +275,39 @@ def backward(plan: Plan, q, k, v, dout, dq=None, dk=None, dv=None, feature_map=N
                                    _ptr(dout), _ptr(dq), _ptr(dk), _ptr(dv), _stream(q.device))
         _check(st, "sla_backward_ex")
     return dq, dk, dv
+
+
+def forward_projected(plan: Plan, x, w_qkv, w_o, heads: int, b_qkv=None, b_o=None, o=None, y=None,
+                      feature_map="elu1", eps=0.0):
+    """Projection layer, SLA and output projection (sla_forward_projected):
+    x [n, C], w_qkv [3C, C], w_o [C, C], optional biases [3C], [C]; returns (o, y)
+    with o [n, heads, C // heads] and y [n, C]."""
+    torch = _torch()
+    if x.dim() != 2 or x.shape[0] != plan.n or not x.is_contiguous():
+        raise ValueError(f"x must be a contiguous [n, C] tensor with n={plan.n}")
+    n, C = x.shape
+    if C % heads:
+        raise ValueError("C must be a multiple of heads")
+    d = C // heads
+    for name, t, shape in (("w_qkv", w_qkv, (3 * C, C)), ("w_o", w_o, (C, C)),
+                           ("b_qkv", b_qkv, (3 * C,)), ("b_o", b_o, (C,))):
+        if t is None:
+            continue
+        if tuple(t.shape) != shape or t.dtype != x.dtype or t.device != x.device or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous {shape} tensor like x")
+    o = torch.empty((n, heads, d), dtype=x.dtype, device=x.device) if o is None else o
+    y = torch.empty_like(x) if y is None else y
+    _check_rows("o", o, n)
+    if y.shape != x.shape or y.dtype != x.dtype or not y.is_contiguous():
+        raise ValueError("y must be a contiguous tensor like x")
+    if feature_map not in FEATURE_MAPS:
+        raise ValueError(f"feature_map must be one of {sorted(FEATURE_MAPS)}, not {feature_map!r}")
+    st = lib().sla_forward_projected(_ptr(plan.buf), plan.nbytes, plan.n, plan.num_windows,
+                                     _dtype_code(x.dtype), heads, d, FEATURE_MAPS[feature_map], float(eps),
+                                     _ptr(x), _ptr(w_qkv), _ptr(b_qkv), _ptr(w_o), _ptr(b_o), _ptr(o), _ptr(y),
+                                     _stream(x.device))
+    _check(st, "sla_forward_projected")
+    return o, y
 
 
 def scatter_workspace_bytes(n: int, heads: int, head_dim: int) -> int:

@@ -46,7 +46,7 @@ def test_only_the_abi_is_exported():
 
 
 def test_queries(L):
-    assert L.sla_abi_version() == 4
+    assert L.sla_abi_version() == 5
     assert L.sla_max_windows() == 16384
     assert L.sla_default_chunk_rows() == 64
     for s in range(5):
@@ -164,3 +164,20 @@ def test_variant_argument_errors(L):
         sla._variant("gelu", 0.0)
     assert sla._variant(None, None) is None
     assert sla._variant("relu", None) == (1, 0.0) and sla._variant(None, 1e-3) == (0, 1e-3)
+
+
+def test_projected_argument_errors(L):
+    nb = sla.plan_bytes(100, 8)
+    def call(dtype=1, H=4, d=32, fm=0, eps=0.0, n=100, x=FAKE, y=FAKE, bq=None):
+        return L.sla_forward_projected(FAKE, nb, n, 8, dtype, H, d, fm, eps, x, FAKE, bq, FAKE, None,
+                                       FAKE, y, None)
+    assert call(dtype=0) == sla.SLA_E_UNSUPPORTED        # fp32 is not supported
+    assert call(H=3) == sla.SLA_E_UNSUPPORTED            # C = 96
+    assert call(H=8) == sla.SLA_E_UNSUPPORTED            # C = 256
+    assert call(d=24) == sla.SLA_E_UNSUPPORTED
+    assert call(fm=3) == sla.SLA_E_ARG
+    assert call(eps=-1.0) == sla.SLA_E_ARG
+    assert call(x=FAKE + 8) == sla.SLA_E_ARG
+    assert call(y=None) == sla.SLA_E_ARG
+    assert call(bq=FAKE + 1) == sla.SLA_E_ARG
+    assert call(n=0) == sla.SLA_OK

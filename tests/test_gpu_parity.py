@@ -15,7 +15,7 @@ import pytest
 
 import oracle
 import workloads
-from tests.gpu_util import TOL, p999, rel_err_per_head, to_dev, to_host64
+from tests.gpu_util import TOL, p999, rel_err_per_head, to_dev, to_host64, torch_dtype
 
 pytestmark = pytest.mark.gpu
 
@@ -500,3 +500,82 @@ def test_variant_relu_absent_features(sla):
     for eps in (1e-6, 0.1):
         forward_parity(sla, ids, None, n, W, q, k, v, "f16", label=f"absent-{eps}", fmap="relu", eps=eps)
         backward_parity(sla, ids, None, n, W, q, k, v, do, "f16", label=f"absent-{eps}", fmap="relu", eps=eps)
+
+
+# ------------------------------------------------- projection fused into SLA
+def projected_parity(S, ids, offsets, n, W, H, d, dtype, fmap="elu1", eps=0.0, bias=True, seed=0,
+                     label="", chunk_rows=0):
+    import torch
+
+    rng = np.random.default_rng([51, seed, H, d])
+    C = H * d
+    cast = lambda a: workloads.cast_values(np.asarray(a, dtype=np.float32), dtype)  # noqa: E731
+    x = cast(rng.standard_normal((n, C)))
+    wq = cast(rng.standard_normal((3 * C, C)) / np.sqrt(C))
+    wo = cast(rng.standard_normal((C, C)) / np.sqrt(C))
+    bq = cast(0.2 * rng.standard_normal(3 * C)) if bias else None
+    bo = cast(0.2 * rng.standard_normal(C)) if bias else None
+    plan = build(S, ids=ids, W=W, chunk_rows=chunk_rows, offsets=offsets, n=n)
+    off, perm = check_plan(S, plan, ids, W, chunk_rows, offsets)
+    dev = lambda a: None if a is None else to_dev(a, dtype)  # noqa: E731
+    o = torch.full((n, H, d), float("nan"), dtype=torch_dtype(dtype), device="cuda")
+    y = torch.full((n, C), float("nan"), dtype=torch_dtype(dtype), device="cuda")
+    S.forward_projected(plan, dev(x), dev(wq), dev(wo), H, dev(bq), dev(bo), o, y, fmap, eps)
+    torch.cuda.synchronize()
+    go, gy = to_host64(o, dtype), to_host64(y, dtype)
+    w = lambda a: None if a is None else oracle.widen(a, dtype)  # noqa: E731
+    with np.errstate(invalid="ignore", divide="ignore"):
+        ro, ry = oracle.sla_projected_forward_ref(w(x), w(wq), w(bq), w(wo), w(bo), H, off, perm, fmap, eps)
+    rows = np.zeros(n, dtype=bool)
+    rows[perm if perm is not None else np.arange(off[-1])] = True
+    assert np.isnan(go[~rows]).all() and np.isnan(gy[~rows]).all(), "rows in no window were written"
+    g0, r0 = _match_nan(go, ro, rows, label)
+    gy3, ry3 = _match_nan(gy.reshape(n, H, d), ry.reshape(n, H, d), rows, label)
+    eo = rel_err_per_head(g0, r0, 1e-3 * float(np.nanmax(np.abs(r0))) if rows.any() else 1.0, rows)
+    ey = rel_err_per_head(gy3, ry3, 1e-3 * float(np.nanmax(np.abs(ry3))) if rows.any() else 1.0, rows)
+    _say(f"[proj {label}] n={n} H={H} d={d} {dtype} {fmap} eps={eps} o rel_err={eo:.3e} y rel_err={ey:.3e}")
+    assert eo <= TOL[dtype], f"{label}: o relative error {eo:.3e}"
+    assert ey <= TOL[dtype], f"{label}: y relative error {ey:.3e}"
+
+
+@pytest.mark.parametrize("cfg", [2, 3, 5])
+def test_projected_config(sla, cfg):
+    # config 3 (bf16, H = 8, d = 16) has windows of up to 1,024 rows: quarters of
+    # more than 64 rows take the streamed path
+    wl = workloads.make_config(cfg, with_grad=False)
+    projected_parity(sla, wl["ids"], wl["offsets"], wl["n"], wl["num_windows"], wl["heads"], wl["head_dim"],
+                     wl["dtype"], label=f"cfg{cfg}")
+
+
+@pytest.mark.parametrize("dtype", ["f16", "bf16"])
+@pytest.mark.parametrize("shape", [(4, 32), (8, 16), (2, 32), (4, 16)])
+def test_projected_shapes(sla, dtype, shape):
+    H, d = shape
+    rng = np.random.default_rng([52, H, d, len(dtype)])
+    lengths = _adversarial_lengths(rng, 128)
+    ids = workloads.ids_from_lengths(lengths, rng)
+    ids[rng.random(ids.size) < 0.01] = -1          # rows outside every window stay unwritten
+    n, W = ids.size, lengths.size
+    projected_parity(sla, ids, None, n, W, H, d, dtype, seed=1, label=f"shape{shape}")
+    projected_parity(sla, ids, None, n, W, H, d, dtype, fmap="relu", eps=1e-3, bias=False, seed=2,
+                     label=f"shape{shape}-relu")
+
+
+def test_projected_csr_and_chunk_rows(sla):
+    wl = workloads.make_config(2, with_grad=False)
+    perm, off, _ = oracle.segments_ref(wl["ids"], wl["num_windows"])
+    # rows already window-sorted: CSR mode, no permutation
+    projected_parity(sla, None, off, wl["n"], wl["num_windows"], 4, 32, "f16", seed=3, label="csr")
+    projected_parity(sla, wl["ids"], None, wl["n"], wl["num_windows"], 4, 32, "f16", seed=4, label="L32",
+                     chunk_rows=32)
+
+
+def test_projected_long_windows(sla):
+    # four-way windows above 256 rows (streamed), two-way windows with an odd
+    # count (a pair whose second window is missing), and a one-window scene
+    rng = np.random.default_rng(53)
+    for lengths in (np.array([700, 300, 257, 256, 100, 90, 70, 3, 1]), np.array([2000]), np.array([65])):
+        ids = workloads.ids_from_lengths(lengths, rng)
+        for dtype in ("f16", "bf16"):
+            projected_parity(sla, ids, None, ids.size, lengths.size, 4, 32, dtype, seed=5,
+                             label=f"long{lengths.size}")
