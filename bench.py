@@ -66,7 +66,8 @@ def elem_size(dtype):
 
 
 COPY_PROBE_BYTES = 256 << 20   # per copy, 3 copies from distinct buffers
-KERNEL_SOURCES = ["paper_2401_00912_amd/csrc/sla_attn.hip", "paper_2401_00912_amd/csrc/sla_common.h"]
+KERNEL_SOURCES = ["paper_2401_00912_amd/csrc/sla_attn.hip", "paper_2401_00912_amd/csrc/sla_attn_core.h",
+                  "paper_2401_00912_amd/csrc/sla_common.h"]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_sla_bwd_training_step_pmc.txt")
 
 
