@@ -277,6 +277,32 @@ def main():
     torch.cuda.synchronize()
     ms_total = t0.elapsed_time(t1)
     ms_step = ms_total / args.steps
+    # four more loops of K steps, for the median of five (the first loop is `value`)
+    loops = [ms_step]
+    for _ in range(4):
+        t0.record()
+        for i in range(args.steps):
+            if graphs is not None:
+                graphs[i % nsets].replay()
+            else:
+                step(i)
+        t1.record()
+        torch.cuda.synchronize()
+        loops.append(t0.elapsed_time(t1) / args.steps)
+    e2e_ms = None
+    if not training:
+        # forward-only configs: end to end, segment build + forward, eager launches
+        for i in range(args.warmup):
+            sla.forward(build(sets[i % nsets]), sets[i % nsets]["q"], sets[i % nsets]["k"],
+                        sets[i % nsets]["v"], out=sets[i % nsets]["o"])
+        torch.cuda.synchronize()
+        t0.record()
+        for i in range(args.steps):
+            st = sets[i % nsets]
+            sla.forward(build(st), st["q"], st["k"], st["v"], out=st["o"])
+        t1.record()
+        torch.cuda.synchronize()
+        e2e_ms = t0.elapsed_time(t1) / args.steps
 
     # ---- per-kernel breakdown: eager launches bracketed by events on the launch stream.
     # A spin kernel first lets the host enqueue every step before the GPU reaches them,
@@ -354,11 +380,16 @@ def main():
         },
         "breakdown_ms": {"build": t_build, "forward": t_fwd, "backward": t_bwd},
         "step_roofline_frac": step_bytes / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS,
+        "ms_per_step_loops": loops,
+        "ms_per_step_median_of_5": float(np.median(loops)),
     }
+    if e2e_ms is not None:
+        out["build_plus_forward_ms"] = e2e_ms
     if variant is not None:
         out["config"]["feature_map"], out["config"]["eps"] = variant
     if not args.no_cpu:
         out["cpu_baseline"] = cpu_baseline(base, training, args.cpu_seconds, variant)
+        out["cpu_baseline"]["all_cores"] = cpu_baseline_pool(cfg, training, args.cpu_seconds, variant)
     print(json.dumps(out), flush=True)
 
 
@@ -526,6 +557,90 @@ def cpu_model():
     except OSError:
         pass
     return "unknown"
+
+
+# ---- the oracle on every host core: a process pool over contiguous window ranges
+_POOL_WL = {}
+
+
+def _pool_init(cfg, training):
+    import workloads
+    import oracle
+
+    wl = workloads.make_config(cfg, with_grad=training)
+    dt = wl["dtype"]
+    _POOL_WL["q"], _POOL_WL["k"], _POOL_WL["v"] = (oracle.widen(wl[x], dt) for x in ("q", "k", "v"))
+    _POOL_WL["do"] = oracle.widen(wl["dout"], dt) if training else None
+
+
+def _pool_work(job):
+    """The oracle on one contiguous range of windows: the range's rows (in window
+    order) with offsets local to them, a scene of its own."""
+    import oracle
+
+    rows, off, training, variant = job
+    extra = () if variant is None else variant
+    w = _POOL_WL
+    q, k, v = w["q"][rows], w["k"][rows], w["v"][rows]
+    oracle.sla_forward_ref(q, k, v, off, None, *extra)
+    if training:
+        oracle.sla_backward_ref(q, k, v, w["do"][rows], off, None, *extra)
+    return int(rows.size)
+
+
+def cpu_baseline_pool(cfg, training, budget_s, variant=None, max_procs=16):
+    """The same oracle calls split over contiguous window ranges of balanced row
+    counts, one range per process (at most the 16-core share of the GPU machine); the
+    segment build runs in the parent.  Workers start (and build their inputs)
+    before the clock starts."""
+    import multiprocessing as mp
+
+    import oracle
+    import workloads
+
+    procs = max(1, min(max_procs, len(os.sched_getaffinity(0))))
+    base = workloads.make_config(cfg, with_grad=False)
+    old = {k: os.environ.get(k) for k in ("OMP_NUM_THREADS", "OPENBLAS_NUM_THREADS", "MKL_NUM_THREADS")}
+    for k in old:
+        os.environ[k] = "1"
+    try:
+        ctx = mp.get_context("spawn")
+        with ctx.Pool(procs, initializer=_pool_init, initargs=(cfg, training)) as pool:
+            def one():
+                if base["ids"] is not None:
+                    perm, off, _ = oracle.segments_ref(base["ids"], base["num_windows"])
+                else:
+                    perm, off = None, base["offsets"].astype(np.int64)
+                W = len(off) - 1
+                cuts = np.searchsorted(off, np.linspace(0, off[-1], procs + 1)).clip(0, W)
+                cuts[0], cuts[-1] = 0, W
+                order = perm if perm is not None else np.arange(off[-1])
+                jobs = [(order[off[a]:off[b]], off[a:b + 1] - off[a], training, variant)
+                        for a, b in zip(cuts[:-1], cuts[1:]) if b > a]
+                assert sum(pool.map(_pool_work, jobs)) == off[-1]
+            one()                                   # untimed: workers warm
+            reps, t_start = 0, time.perf_counter()
+            while True:
+                one()
+                reps += 1
+                if time.perf_counter() - t_start >= budget_s:
+                    break
+            el = time.perf_counter() - t_start
+    finally:
+        for k, v in old.items():
+            if v is None:
+                os.environ.pop(k, None)
+            else:
+                os.environ[k] = v
+    per = el / reps
+    return {
+        "value": base["n"] / per,
+        "unit": "voxels/s",
+        "cores": procs,
+        "kind": "oracle",
+        "sample": f"{reps} whole frame(s), windows split over {procs} processes, {el:.1f} s wall",
+        "ms_per_frame": per * 1e3,
+    }
 
 
 def cpu_baseline(base, training, budget_s, variant=None):
