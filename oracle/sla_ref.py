@@ -51,6 +51,14 @@ What is computed, and the passage it follows
   usual [out, in] weight layout, Q = X W_q^T + b_q (likewise K, V) with
   W_qkv = [W_q; W_k; W_v] stacked by rows, and Y = SLA(Q, K, V) W_o^T + b_o, heads
   split from the C channels as in the plain path.
+* ``cwi_forward_ref``: the cross-window interaction of Sec. 3.3, Eq. (4)-(7): the
+  4c channels split into four quarters, two depthwise convolutions with long 1D
+  kernels along the two grid axes (window size + 1 taps), a depthwise 3 x 3 x 3
+  convolution and an identity, concatenated.  Read as submanifold (sparse)
+  convolutions, as on voxel sets: outputs only at the voxels, a tap whose cell
+  holds no voxel contributes zero; each tap a centred cross-correlation tap (the
+  deep-learning "convolution"); the first axis branch along x, the second along
+  y; no bias (the block's normalisation follows).
 """
 from __future__ import annotations
 
@@ -69,6 +77,7 @@ __all__ = [
     "sla_forward_ref",
     "sla_backward_ref",
     "sla_projected_forward_ref",
+    "cwi_forward_ref",
 ]
 
 
@@ -321,3 +330,59 @@ def sla_projected_forward_ref(x, w_qkv, b_qkv, w_o, b_o, heads, offsets, perm=No
     if b_o is not None:
         y = y + np.asarray(b_o, dtype=np.float64)
     return o, y
+
+
+# ---------------------------------------------------------- cross-window interaction
+def cwi_forward_ref(coords, x, w_x, w_y, w_3, grid):
+    """Cross-window interaction, Eq. (4)-(7) of Sec. 3.3, on sparse voxels.
+
+    coords: int [n, 3] cell (x, y, z) of every voxel, unique, inside grid
+    (gx, gy, gz).  x: float64 [n, 4c] features.  w_x [K_x, c] and w_y [K_y, c] (K
+    odd) the depthwise kernels of the two axis branches, w_3 [27, c] the 3 x 3 x 3
+    one, tap (dx + 1) + 3 (dy + 1) + 9 (dz + 1).  Returns [n, 4c]:
+        channels [0, c)    sum_t w_x[t] x[cell + (t - (K_x - 1) / 2) e_x]
+        channels [c, 2c)   sum_t w_y[t] x[cell + (t - (K_y - 1) / 2) e_y]
+        channels [2c, 3c)  sum over the 27 offsets of w_3[tap] x[cell + offset]
+        channels [3c, 4c)  x (identity)
+    where a cell holding no voxel (or outside the grid) contributes zero.
+    """
+    coords = np.asarray(coords, dtype=np.int64)
+    x = np.asarray(x, dtype=np.float64)
+    w_x, w_y, w_3 = (np.asarray(w, dtype=np.float64) for w in (w_x, w_y, w_3))
+    n, C = x.shape
+    c = C // 4
+    gx, gy, gz = (int(g) for g in grid)
+    if C % 4 or w_x.shape[1] != c or w_y.shape[1] != c or w_3.shape != (27, c):
+        raise ValueError("x [n, 4c], w_x [K_x, c], w_y [K_y, c], w_3 [27, c]")
+    if w_x.shape[0] % 2 == 0 or w_y.shape[0] % 2 == 0:
+        raise ValueError("axis kernels need an odd number of taps")
+    table = np.full(gx * gy * gz, -1, dtype=np.int64)  # cell -> voxel row
+    cell = (coords[:, 2] * gy + coords[:, 1]) * gx + coords[:, 0]
+    table[cell] = np.arange(n)
+
+    def neighbour(dx, dy, dz):
+        """Row of the voxel at cell + (dx, dy, dz), or -1."""
+        nx, ny, nz = coords[:, 0] + dx, coords[:, 1] + dy, coords[:, 2] + dz
+        inside = (nx >= 0) & (nx < gx) & (ny >= 0) & (ny < gy) & (nz >= 0) & (nz < gz)
+        rows = np.full(n, -1, dtype=np.int64)
+        rows[inside] = table[(nz[inside] * gy + ny[inside]) * gx + nx[inside]]
+        return rows
+
+    out = np.zeros((n, C))
+    out[:, 3 * c:] = x[:, 3 * c:]
+    for branch, w, axis in ((0, w_x, 0), (1, w_y, 1)):
+        half = (w.shape[0] - 1) // 2
+        for t in range(w.shape[0]):
+            off = [0, 0, 0]
+            off[axis] = t - half
+            rows = neighbour(*off)
+            ok = rows >= 0
+            lo = branch * c
+            out[ok, lo:lo + c] += w[t] * x[rows[ok], lo:lo + c]
+    for dz in (-1, 0, 1):
+        for dy in (-1, 0, 1):
+            for dx in (-1, 0, 1):
+                rows = neighbour(dx, dy, dz)
+                ok = rows >= 0
+                out[ok, 2 * c:3 * c] += w_3[(dx + 1) + 3 * (dy + 1) + 9 * (dz + 1)] * x[rows[ok], 2 * c:3 * c]
+    return out

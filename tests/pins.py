@@ -544,3 +544,59 @@ def projected_pin_failures(fwd_proj, seg, fwd):
     if rel_err(y2, y0 + bo) > 1e-13:
         fails.append("projected_output_bias")
     return fails
+
+
+# ------------------------------------------------------ cross-window interaction
+def cwi_pin_failures(cwi):
+    """Pins for ``cwi(coords, x, w_x, w_y, w_3, grid) -> [n, 4c]`` (Eq. (4)-(7))."""
+    from scipy import ndimage
+
+    fails = []
+    rng = np.random.default_rng(90)
+    c = 3
+    # 1. a sparse set is the dense grid with zeros in the empty cells, sampled at
+    #    the voxels: compare with scipy's zero-padded correlations on the grid
+    for seed, grid, fill, kx, ky in ((0, (9, 7, 3), 1.0, 5, 3), (1, (11, 10, 4), 0.35, 7, 9),
+                                     (2, (13, 6, 1), 0.6, 13, 5)):
+        r2 = np.random.default_rng([91, seed])
+        gx, gy, gz = grid
+        occ = r2.random((gz, gy, gx)) < fill
+        occ.flat[r2.integers(occ.size)] = True
+        zz, yy, xx = np.nonzero(occ)
+        order = r2.permutation(zz.size)
+        coords = np.stack([xx, yy, zz], axis=1)[order]
+        n = coords.shape[0]
+        x = r2.standard_normal((n, 4 * c))
+        w_x, w_y, w_3 = r2.standard_normal((kx, c)), r2.standard_normal((ky, c)), r2.standard_normal((27, c))
+        got = cwi(coords, x, w_x, w_y, w_3, grid)
+        dense = np.zeros((gz, gy, gx, 4 * c))
+        dense[coords[:, 2], coords[:, 1], coords[:, 0]] = x
+        exp = np.zeros((gz, gy, gx, 4 * c))
+        for ch in range(c):
+            exp[..., ch] = ndimage.correlate1d(dense[..., ch], w_x[:, ch], axis=2, mode="constant")
+            exp[..., c + ch] = ndimage.correlate1d(dense[..., c + ch], w_y[:, ch], axis=1, mode="constant")
+            k3 = w_3[:, ch].reshape(3, 3, 3)  # [dz][dy][dx]
+            exp[..., 2 * c + ch] = ndimage.correlate(dense[..., 2 * c + ch], k3, mode="constant")
+        exp[..., 3 * c:] = dense[..., 3 * c:]
+        ref = exp[coords[:, 2], coords[:, 1], coords[:, 0]]
+        if rel_err(got, ref) > 1e-12:
+            fails.append(f"cwi_dense_correlate[{seed}]")
+    # 2. a lone voxel: every branch is its centre tap times the input
+    x1 = rng.standard_normal((1, 4 * c))
+    w_x, w_y, w_3 = rng.standard_normal((5, c)), rng.standard_normal((3, c)), rng.standard_normal((27, c))
+    out1 = cwi(np.array([[2, 3, 1]]), x1, w_x, w_y, w_3, (6, 6, 3))
+    exp1 = np.concatenate([w_x[2] * x1[0, :c], w_y[1] * x1[0, c:2 * c], w_3[13] * x1[0, 2 * c:3 * c],
+                           x1[0, 3 * c:]])
+    if rel_err(out1[0], exp1) > 1e-15:
+        fails.append("cwi_single_voxel")
+    # 3. translating every voxel (inside the grid) leaves the outputs unchanged,
+    #    and permuting the rows permutes them
+    coords = np.array([[1, 1, 0], [2, 1, 0], [1, 2, 0], [4, 2, 0], [2, 2, 0], [3, 3, 0]])
+    x = rng.standard_normal((6, 4 * c))
+    base = cwi(coords, x, w_x, w_y, w_3, (8, 8, 2))
+    if rel_err(cwi(coords + np.array([3, 2, 1]), x, w_x, w_y, w_3, (8, 8, 2)), base) > 1e-15:
+        fails.append("cwi_translation")
+    p = rng.permutation(6)
+    if rel_err(cwi(coords[p], x[p], w_x, w_y, w_3, (8, 8, 2)), base[p]) > 1e-15:
+        fails.append("cwi_permutation")
+    return fails

@@ -366,3 +366,27 @@ def test_projected_mutant_is_caught(name):
         fails = pins.projected_pin_failures(mod.sla_projected_forward_ref, oracle.segments_ref,
                                             oracle.sla_forward_ref)
     assert fails, f"planted mistake {name} passed every projected pin"
+
+
+# ------------------------------------------------------ cross-window interaction
+def test_cwi_pins():
+    assert pins.cwi_pin_failures(oracle.cwi_forward_ref) == []
+
+
+CWI_MUTANTS = {
+    "kernel_flipped": [("off[axis] = t - half", "off[axis] = half - t", 0)],
+    "axes_swapped": [("for branch, w, axis in ((0, w_x, 0), (1, w_y, 1)):",
+                      "for branch, w, axis in ((0, w_x, 1), (1, w_y, 0)):", 0)],
+    "cube_taps_transposed": [("w_3[(dx + 1) + 3 * (dy + 1) + 9 * (dz + 1)]", "w_3[(dz + 1) + 3 * (dy + 1) + 9 * (dx + 1)]", 0)],
+    "identity_dropped": [("out[:, 3 * c:] = x[:, 3 * c:]", "out[:, 3 * c:] = 0.0", 0)],
+    "off_centre": [("half = (w.shape[0] - 1) // 2", "half = w.shape[0] // 2 - 1", 0)],
+    "branch_channels_shifted": [("lo = branch * c", "lo = (branch + 1) % 3 * c", 0)],
+}
+
+
+@pytest.mark.parametrize("name", sorted(CWI_MUTANTS))
+def test_cwi_mutant_is_caught(name):
+    mod = _oracle_from_source(CWI_MUTANTS[name])
+    with np.errstate(all="ignore"):
+        fails = pins.cwi_pin_failures(mod.cwi_forward_ref)
+    assert fails, f"planted mistake {name} passed every CWI pin"

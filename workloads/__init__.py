@@ -87,13 +87,13 @@ _R = None
 _C = None
 
 
-def waymo_like_ids(rng: np.random.Generator) -> np.ndarray:
-    """Window id of each occupied pillar of one synthetic frame, in raster order.
+def waymo_like_pillars(rng: np.random.Generator):
+    """(x, y) cell coordinates of the occupied pillars of one synthetic frame, in
+    raster order (y major).
 
     A cell at range r (cells) from the grid centre is occupied with probability
     min(1, c / r) inside the sensor range (r <= 234 cells), 0 beyond; c is set so
-    that the expected number of pillars is 60,000.  Window id = (y // 12) * 39 +
-    x // 12.  Raster order is NOT window-sorted.
+    that the expected number of pillars is 60,000.
     """
     global _R, _C
     if _R is None:
@@ -101,7 +101,39 @@ def waymo_like_ids(rng: np.random.Generator) -> np.ndarray:
         _C = _solve_density(FRAME_TARGET_N, _R)
     occ = rng.random((GRID, GRID)) < _occupancy_prob(_C, _R)
     y, x = np.nonzero(occ)
+    return x.astype(np.int32), y.astype(np.int32)
+
+
+def window_ids(x: np.ndarray, y: np.ndarray) -> np.ndarray:
+    """Window id of a cell: (y // 12) * 39 + x // 12."""
     return ((y // WIN) * WIN_PER_SIDE + x // WIN).astype(np.int32)
+
+
+def waymo_like_ids(rng: np.random.Generator) -> np.ndarray:
+    """Window id of each occupied pillar of one synthetic frame, in raster order
+    (not window-sorted)."""
+    x, y = waymo_like_pillars(rng)
+    return window_ids(x, y)
+
+
+def make_cwi_frame(seed=0, channels: int = 128, taps: int = 13, dtype: str = "f16") -> dict:
+    """One Waymo-like pillar frame for the cross-window interaction: coordinates
+    (x, y, 0) on the 468 x 468 grid, window ids, features x [n, channels] ~ N(0, 1),
+    and depthwise weights for the two axis branches (taps x channels / 4) and the
+    3 x 3 x 3 branch (27 x channels / 4), ~ N(0, 1 / taps).  Geometry seed
+    [6, 0, seed], values [6, 1, seed]."""
+    geo = np.random.default_rng([6, 0, seed])
+    val = np.random.default_rng([6, 1, seed])
+    x, y = waymo_like_pillars(geo)
+    n, c = x.size, channels // 4
+    coords = np.stack([x, y, np.zeros_like(x)], axis=1).astype(np.int32)
+    feats = cast_values(val.standard_normal((n, channels), dtype=np.float32), dtype)
+    w = lambda k: cast_values((val.standard_normal((k, c)) / np.sqrt(k)).astype(np.float32), dtype)  # noqa: E731
+    return {"name": f"waymo-like pillar frame for CWI: 468x468 grid, ~60k pillars, C={channels}, "
+                    f"{taps}-tap axis kernels, {dtype}",
+            "n": n, "grid": (GRID, GRID, 1), "coords": coords, "ids": window_ids(x, y),
+            "num_windows": FRAME_WINDOWS, "channels": channels, "taps": taps, "dtype": dtype,
+            "x": feats, "w_x": w(taps), "w_y": w(taps), "w_3": w(27)}
 
 
 def _lognormal_round_clip_mean(mu: float, sigma: float, lo: int, hi: int) -> float:
