@@ -52,6 +52,9 @@ def parse():
     p.add_argument("--projected", action="store_true",
                    help="time the projection fused into SLA (sla_forward_projected) against the unfused "
                         "chain: torch linear, sla_forward, torch linear")
+    p.add_argument("--cwi", action="store_true",
+                   help="time the cross-window interaction (cell table build + forward) on a Waymo-like "
+                        "pillar frame")
     p.add_argument("--compare-scatter", action="store_true",
                    help="instead of the training step: forward time and memory of the chunk-wise path "
                         "against the naive scatter-based one, as sequence length and window length grow")
@@ -166,6 +169,9 @@ def main():
     sla.lib()
     if args.compare_scatter:
         print(json.dumps(compare_scatter(torch, sla, workloads, dev)), flush=True)
+        return
+    if args.cwi:
+        print(json.dumps(bench_cwi(torch, sla, workloads, dev, args)), flush=True)
         return
     if args.projected:
         print(json.dumps(bench_projected(torch, sla, workloads, dev, args)), flush=True)
@@ -391,6 +397,86 @@ def main():
         out["cpu_baseline"] = cpu_baseline(base, training, args.cpu_seconds, variant)
         out["cpu_baseline"]["all_cores"] = cpu_baseline_pool(cfg, training, args.cpu_seconds, variant)
     print(json.dumps(out), flush=True)
+
+
+def bench_cwi(torch, sla, workloads, dev, args):
+    """Cross-window interaction on Waymo-like pillar frames (C = 128, 13-tap axis
+    kernels, fp16): the cell table build and the forward, rows visited in the
+    window order of the frame's SLA plan (and, for comparison, in row order);
+    buffer sets rotated, graph replay."""
+    import oracle  # only to derive the window order of the synthetic frames
+
+    nsets = 6
+    sets = []
+    for s_ in range(nsets):
+        f = workloads.make_cwi_frame(seed=s_)
+        perm, _, _ = oracle.segments_ref(f["ids"], f["num_windows"])
+        dt = {"f16": torch.float16}[f["dtype"]]
+        sets.append({
+            "coords": torch.from_numpy(f["coords"]).to(dev),
+            "order": torch.from_numpy(perm.astype(np.int32)).to(dev),
+            "x": torch.from_numpy(f["x"]).to(dev),
+            "w": [torch.from_numpy(f[k]).to(dev) for k in ("w_x", "w_y", "w_3")],
+            "y": torch.empty(f["n"], f["channels"], dtype=dt, device=dev),
+            "map": torch.empty(sla.cwi_map_bytes(*f["grid"]) // 4, dtype=torch.int32, device=dev),
+            "grid": f["grid"], "n": f["n"], "C": f["channels"],
+        })
+
+    def build(st):
+        sla.cwi_build_map(st["coords"], st["grid"], map=st["map"])
+
+    def fwd(st, ordered=True):
+        sla.cwi_forward(st["map"], st["grid"], st["coords"], st["x"], *st["w"],
+                        order=st["order"] if ordered else None, y=st["y"])
+
+    def timed(fn, reps):
+        for i in range(args.warmup):
+            fn(sets[i % nsets])
+        torch.cuda.synchronize()
+        graphs = []
+        cap = torch.cuda.Stream(dev)
+        cap.wait_stream(torch.cuda.current_stream(dev))
+        with torch.cuda.stream(cap):
+            for s_ in range(nsets):
+                g = torch.cuda.CUDAGraph()
+                with torch.cuda.graph(g, stream=cap):
+                    fn(sets[s_])
+                graphs.append(g)
+        torch.cuda.current_stream(dev).wait_stream(cap)
+        for g in graphs:
+            g.replay()
+        torch.cuda.synchronize()
+        t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        t0.record()
+        for i in range(reps):
+            graphs[i % nsets].replay()
+        t1.record()
+        torch.cuda.synchronize()
+        return t0.elapsed_time(t1) / reps * 1e3
+
+    reps = max(100, args.steps)
+    for st in sets:
+        build(st)
+    t_build = timed(build, reps)
+    t_fwd = timed(fwd, reps)
+    t_fwd_rows = timed(lambda st: fwd(st, ordered=False), reps)
+    n = int(np.mean([st["n"] for st in sets]))
+    C, e = sets[0]["C"], 2
+    cells = int(np.prod(sets[0]["grid"]))
+    fwd_bytes = n * (2 * C * e + 12 + 4)          # x read, y written, coordinates, visiting order
+    build_bytes = 4 * cells + n * (12 + 4)        # table cleared, coordinates read, rows written
+    return {
+        "mode": "cwi",
+        "workload": workloads.make_cwi_frame.__doc__.split(":")[0].strip().replace("\n", " "),
+        "n": n, "channels": C, "taps": 13, "grid": list(sets[0]["grid"]), "dtype": "f16", "buffer_sets": nsets,
+        "build_us": t_build,
+        "forward_us": t_fwd,
+        "forward_row_order_us": t_fwd_rows,
+        "forward_algorithmic_bytes": fwd_bytes,
+        "forward_gbs": fwd_bytes / (t_fwd * 1e-6) / 1e9,
+        "forward_frac_of_hbm_peak": fwd_bytes / (t_fwd * 1e-6) / 1e9 / HBM_PEAK_GBS,
+        "build_algorithmic_bytes": build_bytes,
+    }
 
 
 def bench_projected(torch, sla, workloads, dev, args):

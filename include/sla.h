@@ -224,6 +224,49 @@ sla_status_t sla_forward_projected(const void* plan, size_t plan_bytes, int64_t 
                                    sla_stream_t stream);
 
 /*
+ * Cross-window interaction (Sec. 3.3, Eq. (4)-(7)), the module that follows SLA
+ * in every block: the channels of each voxel, 4c of them, go through four
+ * branches whose outputs are concatenated,
+ *   [0, c)    depthwise convolution along x with taps_x taps (w_x [taps_x, c]),
+ *   [c, 2c)   depthwise convolution along y with taps_y taps (w_y [taps_y, c]),
+ *   [2c, 3c)  depthwise 3 x 3 x 3 convolution (w_3 [27, c], tap
+ *             (dx + 1) + 3 (dy + 1) + 9 (dz + 1)),
+ *   [3c, 4c)  identity;
+ * the paper's axis kernels have window size + 1 taps (13 for 12 x 12 windows).
+ * Read as submanifold convolutions on the voxel set: outputs only at the voxels,
+ * a tap whose cell holds no voxel contributes zero, each tap a centred
+ * cross-correlation tap (y[p] = sum_t w[t] x[p + t - (taps - 1) / 2]), no bias.
+ *
+ * Voxels are cells (x, y, z) of a gx x gy x gz grid (pillars: gz = 1), given as
+ * int32 coords [n, 3].  Neighbours are found through a dense cell -> row table
+ * (`map`, int32 [gx gy gz], caller-owned, sla_cwi_map_bytes() bytes), built per
+ * scene by sla_cwi_build_map: -1 in empty cells.  Coordinates must be unique and
+ * inside the grid; rows that are not are counted in *conflicts (device int32,
+ * may be NULL; a cell claimed twice keeps the larger row) and their outputs, and
+ * those of their neighbours, are undefined.
+ *
+ * sla_cwi_forward: x, y [n, channels] in original row order, `dtype` throughout
+ * (fp32 accumulation), channels = 4c with c * (element size) a multiple of 16
+ * bytes and 64 divisible by c * (element size) / 16 (fp16/bf16: channels 32 x 2^k
+ * up to 2048; fp32: 16 x 2^k up to 1024); taps odd, 1..63; else
+ * SLA_E_UNSUPPORTED.  `order` (int32
+ * [n], may be NULL = 0..n-1) is the order in which rows are visited, e.g. the
+ * SLA plan's permutation: rows of one window together keep the neighbours in
+ * cache.  x, y and the weights 16-byte aligned.
+ */
+size_t sla_cwi_map_bytes(int32_t gx, int32_t gy, int32_t gz);
+
+sla_status_t sla_cwi_build_map(const int32_t* coords, int64_t n, int32_t gx, int32_t gy,
+                               int32_t gz, int32_t* map, size_t map_bytes, int32_t* conflicts,
+                               sla_stream_t stream);
+
+sla_status_t sla_cwi_forward(const int32_t* map, int32_t gx, int32_t gy, int32_t gz,
+                             const int32_t* coords, int64_t n, const int32_t* order,
+                             sla_dtype_t dtype, int32_t channels, int32_t taps_x, int32_t taps_y,
+                             const void* x, const void* w_x, const void* w_y, const void* w_3,
+                             void* y, sla_stream_t stream);
+
+/*
  * The naive scatter-based forward that Sec. 3.2 ("Hardware Efficient
  * Implementation") contrasts with the chunk-wise kernel, kept as a comparator
  * for Fig. 4's time-and-memory comparison: the kv matrix phi(k)^T v of every

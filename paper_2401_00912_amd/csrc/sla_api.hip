@@ -19,6 +19,13 @@ hipError_t launch_forward_projected(const void* plan, int32_t n, int32_t W, int 
                                     const void* bqkv, const void* wo, const void* bo, void* o,
                                     void* y, hipStream_t stream);
 size_t naive_workspace_bytes(int64_t n, int32_t H, int32_t d);
+hipError_t launch_cwi_build_map(const int32_t* coords, int32_t n, int32_t gx, int32_t gy,
+                                int32_t gz, int32_t* map, int32_t* conflicts, hipStream_t stream);
+hipError_t launch_cwi_forward(const int32_t* map, int32_t gx, int32_t gy, int32_t gz,
+                              const int32_t* coords, int32_t n, const int32_t* order, int dtype,
+                              int32_t channels, int32_t kx, int32_t ky, const void* x,
+                              const void* w_x, const void* w_y, const void* w_3, void* y,
+                              hipStream_t stream);
 hipError_t launch_forward_scatter(const void* plan, int32_t n, int32_t W, int dtype, int32_t H,
                                   int32_t d, const void* q, const void* k, const void* v,
                                   void* o, void* workspace, hipStream_t stream);
@@ -26,7 +33,15 @@ hipError_t launch_forward_scatter(const void* plan, int32_t n, int32_t W, int dt
 
 namespace {
 
-constexpr int32_t kAbiVersion = 5;
+constexpr int32_t kAbiVersion = 6;
+
+// cells of a CWI grid, or -1 when a side is not positive or the grid has more
+// than INT32_MAX cells
+int64_t cwi_cells(int32_t gx, int32_t gy, int32_t gz) {
+  if (gx < 1 || gy < 1 || gz < 1) return -1;
+  const int64_t cells = (int64_t)gx * gy * gz;
+  return cells > INT32_MAX ? -1 : cells;
+}
 
 bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) & (a - 1)) == 0; }
 
@@ -228,4 +243,52 @@ SLA_EXPORT sla_status_t sla_forward_scatter(const void* plan, size_t plan_bytes,
   return hip_status(sla::launch_forward_scatter(plan, (int32_t)n, num_windows, (int)dtype, heads,
                                                 head_dim, q, k, v, o, workspace,
                                                 static_cast<hipStream_t>(stream)));
+}
+
+SLA_EXPORT size_t sla_cwi_map_bytes(int32_t gx, int32_t gy, int32_t gz) {
+  const int64_t cells = cwi_cells(gx, gy, gz);
+  return cells < 0 ? 0 : (size_t)cells * sizeof(int32_t);
+}
+
+SLA_EXPORT sla_status_t sla_cwi_build_map(const int32_t* coords, int64_t n, int32_t gx,
+                                          int32_t gy, int32_t gz, int32_t* map,
+                                          size_t map_bytes, int32_t* conflicts,
+                                          sla_stream_t stream) {
+  const int64_t cells = cwi_cells(gx, gy, gz);
+  if (cells < 0 || n < 0 || n >= INT32_MAX) return SLA_E_ARG;
+  if (map == nullptr || !aligned(map, 4)) return SLA_E_ARG;
+  if (map_bytes < (size_t)cells * sizeof(int32_t)) return SLA_E_WORKSPACE;
+  if (n > 0 && (coords == nullptr || !aligned(coords, 4))) return SLA_E_ARG;
+  if (conflicts && !aligned(conflicts, 4)) return SLA_E_ARG;
+  return hip_status(sla::launch_cwi_build_map(coords, (int32_t)n, gx, gy, gz, map, conflicts,
+                                              static_cast<hipStream_t>(stream)));
+}
+
+SLA_EXPORT sla_status_t sla_cwi_forward(const int32_t* map, int32_t gx, int32_t gy, int32_t gz,
+                                        const int32_t* coords, int64_t n, const int32_t* order,
+                                        sla_dtype_t dtype, int32_t channels, int32_t taps_x,
+                                        int32_t taps_y, const void* x, const void* w_x,
+                                        const void* w_y, const void* w_3, void* y,
+                                        sla_stream_t stream) {
+  if (cwi_cells(gx, gy, gz) < 0 || n < 0 || n >= INT32_MAX) return SLA_E_ARG;
+  if (dtype < 0 || dtype > 2) return SLA_E_ARG;
+  const int64_t esize = dtype == 0 ? 4 : 2;
+  // four branches of c channels; a branch row is a whole number of 16-byte
+  // pieces, and that number divides 64 (one wave holds whole rows)
+  if (channels < 4 || channels % 4) return SLA_E_UNSUPPORTED;
+  const int64_t piece_bytes = (int64_t)(channels / 4) * esize;
+  if (piece_bytes % 16) return SLA_E_UNSUPPORTED;
+  const int64_t pq = piece_bytes / 16;
+  if (pq > 64 || (64 % pq)) return SLA_E_UNSUPPORTED;
+  if (taps_x < 1 || taps_y < 1 || taps_x > 63 || taps_y > 63 || !(taps_x & 1) || !(taps_y & 1))
+    return SLA_E_UNSUPPORTED;
+  if (n > 0 && (int64_t)n * channels * esize > (int64_t)UINT32_MAX * 4) return SLA_E_UNSUPPORTED;
+  if (n == 0) return SLA_OK;
+  if (!map || !coords || !x || !w_x || !w_y || !w_3 || !y) return SLA_E_ARG;
+  if (!aligned(map, 4) || !aligned(coords, 4) || (order && !aligned(order, 4)) || !aligned(x, 16) ||
+      !aligned(w_x, 16) || !aligned(w_y, 16) || !aligned(w_3, 16) || !aligned(y, 16))
+    return SLA_E_ARG;
+  return hip_status(sla::launch_cwi_forward(map, gx, gy, gz, coords, (int32_t)n, order, (int)dtype,
+                                            channels, taps_x, taps_y, x, w_x, w_y, w_3, y,
+                                            static_cast<hipStream_t>(stream)));
 }

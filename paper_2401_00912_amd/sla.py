@@ -14,6 +14,9 @@ Functions mirror the C ABI in include/sla.h:
         sla_backward_ex; leaving both None calls sla_forward / sla_backward)
     forward_projected(plan, x, w_qkv, w_o, heads, b_qkv=None, b_o=None, o=None, y=None,
                       feature_map="elu1", eps=0.0) -> (o, y)
+    cwi_map_bytes(gx, gy, gz)
+    cwi_build_map(coords, grid, map=None) -> (map, conflicts)
+    cwi_forward(map, grid, coords, x, w_x, w_y, w_3, order=None, y=None) -> y
     scatter_workspace_bytes(n, heads, head_dim)
     forward_scatter(plan, q, k, v, out=None, workspace=None) -> o   (naive comparator)
 """
@@ -42,6 +45,9 @@ EXPORTED = (
     "sla_forward_ex",
     "sla_backward_ex",
     "sla_forward_projected",
+    "sla_cwi_map_bytes",
+    "sla_cwi_build_map",
+    "sla_cwi_forward",
     "sla_scatter_workspace_bytes",
     "sla_forward_scatter",
 )
@@ -103,6 +109,12 @@ def lib() -> ctypes.CDLL:
     L.sla_backward_ex.argtypes = [vp, sz, i64, i32, en, i32, i32, en, f32, vp, vp, vp, vp, vp, vp, vp, vp]
     L.sla_forward_projected.restype = ctypes.c_int
     L.sla_forward_projected.argtypes = [vp, sz, i64, i32, en, i32, i32, en, f32, vp, vp, vp, vp, vp, vp, vp, vp]
+    L.sla_cwi_map_bytes.restype = sz
+    L.sla_cwi_map_bytes.argtypes = [i32, i32, i32]
+    L.sla_cwi_build_map.restype = ctypes.c_int
+    L.sla_cwi_build_map.argtypes = [vp, i64, i32, i32, i32, vp, sz, vp, vp]
+    L.sla_cwi_forward.restype = ctypes.c_int
+    L.sla_cwi_forward.argtypes = [vp, i32, i32, i32, vp, i64, vp, en, i32, i32, i32, vp, vp, vp, vp, vp, vp]
     L.sla_scatter_workspace_bytes.restype = sz
     L.sla_scatter_workspace_bytes.argtypes = [i64, i32, i32]
     L.sla_forward_scatter.restype = ctypes.c_int
@@ -308,6 +320,57 @@ def forward_projected(plan: Plan, x, w_qkv, w_o, heads: int, b_qkv=None, b_o=Non
                                      _stream(x.device))
     _check(st, "sla_forward_projected")
     return o, y
+
+
+def cwi_map_bytes(gx: int, gy: int, gz: int) -> int:
+    return int(lib().sla_cwi_map_bytes(int(gx), int(gy), int(gz)))
+
+
+def cwi_build_map(coords, grid, map=None):
+    """Cell -> row table of a scene for the cross-window interaction: coords int32
+    [n, 3] (x, y, z) on the device, grid (gx, gy, gz).  Returns (map, conflicts),
+    conflicts an int32 [1] device tensor (rows outside the grid or on a taken cell)."""
+    torch = _torch()
+    gx, gy, gz = (int(g) for g in grid)
+    if coords.dtype != torch.int32 or coords.dim() != 2 or coords.shape[1] != 3 or not coords.is_contiguous():
+        raise ValueError("coords must be a contiguous int32 [n, 3] tensor")
+    nb = cwi_map_bytes(gx, gy, gz)
+    if nb == 0:
+        raise SlaError(SLA_E_ARG, "sla_cwi_map_bytes")
+    if map is None:
+        map = torch.empty(nb // 4, dtype=torch.int32, device=coords.device)
+    conflicts = torch.empty(1, dtype=torch.int32, device=coords.device)
+    n = coords.shape[0]
+    cptr = _ptr(coords) if n else ctypes.c_void_p(0)
+    st = lib().sla_cwi_build_map(cptr, n, gx, gy, gz, _ptr(map), int(map.numel() * 4), _ptr(conflicts),
+                                 _stream(coords.device))
+    _check(st, "sla_cwi_build_map")
+    return map, conflicts
+
+
+def cwi_forward(map, grid, coords, x, w_x, w_y, w_3, order=None, y=None):
+    """Cross-window interaction (sla_cwi_forward): x [n, 4c], w_x [K_x, c], w_y
+    [K_y, c], w_3 [27, c]; order an int32 [n] visiting order or None."""
+    torch = _torch()
+    gx, gy, gz = (int(g) for g in grid)
+    if x.dim() != 2 or not x.is_contiguous():
+        raise ValueError("x must be a contiguous [n, channels] tensor")
+    n, C = x.shape
+    c = C // 4
+    for name, t, rows in (("w_x", w_x, None), ("w_y", w_y, None), ("w_3", w_3, 27)):
+        if t.dim() != 2 or t.shape[1] != c or (rows and t.shape[0] != rows) or t.dtype != x.dtype \
+                or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous [taps, {c}] tensor like x")
+    if coords.shape != (n, 3) or coords.dtype != torch.int32:
+        raise ValueError("coords must be int32 [n, 3]")
+    if order is not None and (order.numel() < n or order.dtype != torch.int32):
+        raise ValueError("order must be int32 [n]")
+    y = torch.empty_like(x) if y is None else y
+    st = lib().sla_cwi_forward(_ptr(map), gx, gy, gz, _ptr(coords), n, _ptr(order), _dtype_code(x.dtype), C,
+                               int(w_x.shape[0]), int(w_y.shape[0]), _ptr(x), _ptr(w_x), _ptr(w_y), _ptr(w_3),
+                               _ptr(y), _stream(x.device))
+    _check(st, "sla_cwi_forward")
+    return y
 
 
 def scatter_workspace_bytes(n: int, heads: int, head_dim: int) -> int:

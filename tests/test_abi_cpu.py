@@ -46,7 +46,7 @@ def test_only_the_abi_is_exported():
 
 
 def test_queries(L):
-    assert L.sla_abi_version() == 5
+    assert L.sla_abi_version() == 6
     assert L.sla_max_windows() == 16384
     assert L.sla_default_chunk_rows() == 64
     for s in range(5):
@@ -181,3 +181,30 @@ def test_projected_argument_errors(L):
     assert call(y=None) == sla.SLA_E_ARG
     assert call(bq=FAKE + 1) == sla.SLA_E_ARG
     assert call(n=0) == sla.SLA_OK
+
+
+def test_cwi_argument_errors(L):
+    assert sla.cwi_map_bytes(468, 468, 1) == 4 * 468 * 468
+    assert sla.cwi_map_bytes(0, 4, 1) == 0 and sla.cwi_map_bytes(1 << 16, 1 << 16, 1) == 0
+    mb = sla.cwi_map_bytes(8, 8, 1)
+    bm = lambda **k: L.sla_cwi_build_map(k.get("coords", FAKE), k.get("n", 10), 8, 8, k.get("gz", 1),  # noqa: E731
+                                         k.get("map", FAKE), k.get("mb", mb), None, None)
+    assert bm(mb=mb - 4) == sla.SLA_E_WORKSPACE
+    assert bm(map=None) == sla.SLA_E_ARG
+    assert bm(coords=None) == sla.SLA_E_ARG
+    assert bm(gz=0) == sla.SLA_E_ARG
+    assert bm(n=-1) == sla.SLA_E_ARG
+
+    def fw(dtype=1, C=128, kx=13, ky=13, n=10, x=FAKE, order=None):
+        return L.sla_cwi_forward(FAKE, 8, 8, 1, FAKE, n, order, dtype, C, kx, ky, x, FAKE, FAKE, FAKE, FAKE,
+                                 None)
+    assert fw(kx=12) == sla.SLA_E_UNSUPPORTED        # even taps
+    assert fw(ky=65) == sla.SLA_E_UNSUPPORTED
+    assert fw(C=96) == sla.SLA_E_UNSUPPORTED         # 3 pieces of 16 bytes per branch row: 64 % 3 != 0
+    assert fw(C=48) == sla.SLA_E_UNSUPPORTED         # 24 bytes per branch row: not whole pieces
+    assert fw(C=4096) == sla.SLA_E_UNSUPPORTED       # 128 pieces per branch row: more than a wave
+    assert fw(dtype=0, C=48) == sla.SLA_E_UNSUPPORTED  # fp32: 48 bytes per branch row: 3 pieces
+    assert fw(dtype=5) == sla.SLA_E_ARG
+    assert fw(x=FAKE + 4) == sla.SLA_E_ARG
+    assert fw(order=FAKE + 2) == sla.SLA_E_ARG
+    assert fw(n=0) == sla.SLA_OK

@@ -579,3 +579,70 @@ def test_projected_long_windows(sla):
         for dtype in ("f16", "bf16"):
             projected_parity(sla, ids, None, ids.size, lengths.size, 4, 32, dtype, seed=5,
                              label=f"long{lengths.size}")
+
+
+# ---------------------------------------------------- cross-window interaction
+def cwi_parity(S, coords, grid, x, w_x, w_y, w_3, dtype, order=None, label=""):
+    import torch
+
+    cc = torch.from_numpy(np.ascontiguousarray(coords.astype(np.int32))).cuda()
+    m, conflicts = S.cwi_build_map(cc, grid)
+    tord = None if order is None else torch.from_numpy(np.ascontiguousarray(order.astype(np.int32))).cuda()
+    dev = lambda a: to_dev(a, dtype)  # noqa: E731
+    y = torch.full(x.shape, float("nan"), dtype=torch_dtype(dtype), device="cuda")
+    S.cwi_forward(m, grid, cc, dev(x), dev(w_x), dev(w_y), dev(w_3), order=tord, y=y)
+    torch.cuda.synchronize()
+    assert int(conflicts.cpu()[0]) == 0
+    got = to_host64(y, dtype)
+    w = lambda a: oracle.widen(a, dtype)  # noqa: E731
+    ref = oracle.cwi_forward_ref(coords, w(x), w(w_x), w(w_y), w(w_3), grid)
+    n, C = x.shape
+    err = rel_err_per_head(got.reshape(n, 4, C // 4), ref.reshape(n, 4, C // 4),
+                           1e-3 * float(np.abs(ref).max()) if n else 1.0)
+    _say(f"[cwi {label}] n={n} C={C} grid={grid} {dtype} rel_err={err:.3e}")
+    assert err <= TOL[dtype], f"{label}: CWI relative error {err:.3e}"
+    # the identity branch is a copy, bit for bit
+    assert np.array_equal(got[:, 3 * C // 4:], w(x)[:, 3 * C // 4:])
+    return m
+
+
+def test_cwi_frame(sla):
+    # a Waymo-like pillar frame, visited in the SLA plan's window order and in row order
+    f = workloads.make_cwi_frame()
+    perm, _, _ = oracle.segments_ref(f["ids"], f["num_windows"])
+    for order in (perm, None):
+        cwi_parity(sla, f["coords"], f["grid"], f["x"], f["w_x"], f["w_y"], f["w_3"], f["dtype"], order=order,
+                   label="frame" + ("-window-order" if order is not None else ""))
+
+
+@pytest.mark.parametrize("dtype", ["f32", "f16", "bf16"])
+@pytest.mark.parametrize("C,kx,ky", [(32, 13, 13), (64, 5, 31), (128, 1, 63), (256, 13, 3)])
+def test_cwi_voxels(sla, dtype, C, kx, ky):
+    # 3D voxel grids (the 3 x 3 x 3 branch sees all its z taps), random occupancy
+    # including runs along both axes, rows shuffled
+    if dtype == "f32" and C == 32:
+        C = 16
+    rng = np.random.default_rng([61, C, kx, len(dtype)])
+    grid = (37, 29, 5)
+    occ = rng.random(grid[::-1]) < 0.3
+    zz, yy, xx = np.nonzero(occ)
+    coords = np.stack([xx, yy, zz], axis=1)[rng.permutation(zz.size)]
+    n, c = coords.shape[0], C // 4
+    cast = lambda a: workloads.cast_values(a.astype(np.float32), dtype)  # noqa: E731
+    x = cast(rng.standard_normal((n, C)))
+    w_x, w_y, w_3 = (cast(rng.standard_normal((k, c)) / np.sqrt(k)) for k in (kx, ky, 27))
+    cwi_parity(sla, coords, grid, x, w_x, w_y, w_3, dtype, order=rng.permutation(n), label=f"vox{C}")
+
+
+def test_cwi_conflicts_and_empty(sla):
+    import torch
+
+    coords = np.array([[1, 1, 0], [2, 1, 0], [1, 1, 0], [9, 0, 0], [0, 7, 0]], dtype=np.int32)
+    m, conflicts = sla.cwi_build_map(torch.from_numpy(coords).cuda(), (8, 8, 1))
+    torch.cuda.synchronize()
+    assert int(conflicts.cpu()[0]) == 2                      # a taken cell, a cell outside the grid
+    table = m.cpu().numpy().reshape(8, 8)
+    assert table[1, 1] == 2 and table[1, 2] == 1 and table[7, 0] == 4 and (table >= 0).sum() == 3
+    m0, c0 = sla.cwi_build_map(torch.zeros((0, 3), dtype=torch.int32, device="cuda"), (4, 4, 2))
+    torch.cuda.synchronize()
+    assert int(c0.cpu()[0]) == 0 and bool((m0 == -1).all())
