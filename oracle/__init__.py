@@ -6,6 +6,7 @@ this package.  It shares no code with the HIP library and imports nothing from i
 from .sla_ref import (  # noqa: F401
     FEATURE_MAPS,
     chunk_plan_ref,
+    cwi_backward_ref,
     cwi_forward_ref,
     dphi,
     dphi_relu,

@@ -59,6 +59,9 @@ What is computed, and the passage it follows
   holds no voxel contributes zero; each tap a centred cross-correlation tap (the
   deep-learning "convolution"); the first axis branch along x, the second along
   y; no bias (the block's normalisation follows).
+* ``cwi_backward_ref``: the gradients of that module with respect to its input
+  and its three kernels, by the chain rule (the paper trains the model but does
+  not write them out).
 """
 from __future__ import annotations
 
@@ -78,6 +81,7 @@ __all__ = [
     "sla_backward_ref",
     "sla_projected_forward_ref",
     "cwi_forward_ref",
+    "cwi_backward_ref",
 ]
 
 
@@ -386,3 +390,61 @@ def cwi_forward_ref(coords, x, w_x, w_y, w_3, grid):
                 ok = rows >= 0
                 out[ok, 2 * c:3 * c] += w_3[(dx + 1) + 3 * (dy + 1) + 9 * (dz + 1)] * x[rows[ok], 2 * c:3 * c]
     return out
+
+
+def _cwi_neighbours(coords, grid):
+    """neighbour(dx, dy, dz) -> row of the voxel at cell + offset for every voxel,
+    or -1 (a dense cell table, as in cwi_forward_ref)."""
+    coords = np.asarray(coords, dtype=np.int64)
+    n = coords.shape[0]
+    gx, gy, gz = (int(g) for g in grid)
+    table = np.full(gx * gy * gz, -1, dtype=np.int64)
+    table[(coords[:, 2] * gy + coords[:, 1]) * gx + coords[:, 0]] = np.arange(n)
+
+    def neighbour(dx, dy, dz):
+        nx, ny, nz = coords[:, 0] + dx, coords[:, 1] + dy, coords[:, 2] + dz
+        inside = (nx >= 0) & (nx < gx) & (ny >= 0) & (ny < gy) & (nz >= 0) & (nz < gz)
+        rows = np.full(n, -1, dtype=np.int64)
+        rows[inside] = table[(nz[inside] * gy + ny[inside]) * gx + nx[inside]]
+        return rows
+
+    return neighbour
+
+
+def cwi_backward_ref(coords, x, w_x, w_y, w_3, dy, grid):
+    """Gradients of sum(dy * cwi_forward_ref(coords, x, w_x, w_y, w_3, grid)).
+
+    Every tap of the forward adds w[t] * x[q] to out[p] for the voxel q at p's
+    cell + offset_t.  So, per tap:  dx[q] += w[t] * dy[p]  and
+    dw[t] += dy[p] * x[q]  (elementwise over the branch's channels); the identity
+    quarter passes dy through.  Returns (dx [n, 4c], dw_x, dw_y, dw_3).
+    """
+    x = np.asarray(x, dtype=np.float64)
+    dy = np.asarray(dy, dtype=np.float64)
+    w_x, w_y, w_3 = (np.asarray(w, dtype=np.float64) for w in (w_x, w_y, w_3))
+    n, C = x.shape
+    c = C // 4
+    neighbour = _cwi_neighbours(coords, grid)
+    dx = np.zeros((n, C))
+    dx[:, 3 * c:] = dy[:, 3 * c:]
+    dws = [np.zeros_like(w_x), np.zeros_like(w_y), np.zeros_like(w_3)]
+
+    def tap(branch, t, w, off):
+        rows = neighbour(*off)
+        ok = np.nonzero(rows >= 0)[0]
+        lo = branch * c
+        q = rows[ok]
+        np.add.at(dx, (q, slice(lo, lo + c)), w[t] * dy[ok, lo:lo + c])
+        dws[branch][t] = (dy[ok, lo:lo + c] * x[q, lo:lo + c]).sum(axis=0)
+
+    for branch, w, axis in ((0, w_x, 0), (1, w_y, 1)):
+        half = (w.shape[0] - 1) // 2
+        for t in range(w.shape[0]):
+            off = [0, 0, 0]
+            off[axis] = t - half
+            tap(branch, t, w, off)
+    for dz in (-1, 0, 1):
+        for dy_ in (-1, 0, 1):
+            for dx_ in (-1, 0, 1):
+                tap(2, (dx_ + 1) + 3 * (dy_ + 1) + 9 * (dz + 1), w_3, (dx_, dy_, dz))
+    return dx, dws[0], dws[1], dws[2]

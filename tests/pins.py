@@ -600,3 +600,52 @@ def cwi_pin_failures(cwi):
     if rel_err(cwi(coords[p], x[p], w_x, w_y, w_3, (8, 8, 2)), base[p]) > 1e-15:
         fails.append("cwi_permutation")
     return fails
+
+
+def cwi_backward_pin_failures(cwi_bwd, cwi_fwd):
+    """Pins for ``cwi_bwd(coords, x, w_x, w_y, w_3, dy, grid) -> (dx, dw_x, dw_y, dw_3)``."""
+    fails = []
+    rng = np.random.default_rng(95)
+    c = 2
+    grid = (7, 6, 3)
+    occ = rng.random(grid[::-1]) < 0.45
+    zz, yy, xx = np.nonzero(occ)
+    coords = np.stack([xx, yy, zz], axis=1)[rng.permutation(zz.size)]
+    n = coords.shape[0]
+    x = rng.standard_normal((n, 4 * c))
+    dy = rng.standard_normal((n, 4 * c))
+    w_x, w_y, w_3 = rng.standard_normal((5, c)), rng.standard_normal((3, c)), rng.standard_normal((27, c))
+    dx, dwx, dwy, dw3 = cwi_bwd(coords, x, w_x, w_y, w_3, dy, grid)
+    out = cwi_fwd(coords, x, w_x, w_y, w_3, grid)
+    # 1. the module is linear in x: <dy, F(x)> = <dx, x> (adjoint / dot-product test)
+    if abs((dy * out).sum() - (dx * x).sum()) > 1e-12 * max(1.0, abs((dy * out).sum())):
+        fails.append("cwi_adjoint_x")
+    # 2. the convolution branches are linear in their kernels: <dw, w> recovers
+    #    each branch's share of <dy, F>
+    for b, (dw, w) in enumerate(((dwx, w_x), (dwy, w_y), (dw3, w_3))):
+        share = (dy[:, b * c:(b + 1) * c] * out[:, b * c:(b + 1) * c]).sum()
+        if abs((dw * w).sum() - share) > 1e-12 * max(1.0, abs(share)):
+            fails.append(f"cwi_adjoint_w{b}")
+    # 3. central finite differences on a few entries of x and of each kernel
+    h = 1e-6
+
+    def loss(x_, wx_, wy_, w3_):
+        return float((dy * cwi_fwd(coords, x_, wx_, wy_, w3_, grid)).sum())
+
+    for idx in ((0, 0), (n // 2, c + 1), (n - 1, 2 * c), (3, 3 * c)):
+        xp, xm = x.copy(), x.copy()
+        xp[idx] += h
+        xm[idx] -= h
+        fd = (loss(xp, w_x, w_y, w_3) - loss(xm, w_x, w_y, w_3)) / (2 * h)
+        if abs(fd - dx[idx]) > 1e-6 * max(1.0, abs(fd)):
+            fails.append(f"cwi_fd_dx{idx}")
+    for b, (w, dw) in enumerate(((w_x, dwx), (w_y, dwy), (w_3, dw3))):
+        idx = (w.shape[0] // 2 + 1, c - 1)
+        args_p = [w_x.copy(), w_y.copy(), w_3.copy()]
+        args_m = [w_x.copy(), w_y.copy(), w_3.copy()]
+        args_p[b][idx] += h
+        args_m[b][idx] -= h
+        fd = (loss(x, *args_p) - loss(x, *args_m)) / (2 * h)
+        if abs(fd - dw[idx]) > 1e-6 * max(1.0, abs(fd)):
+            fails.append(f"cwi_fd_dw{b}")
+    return fails

@@ -390,3 +390,26 @@ def test_cwi_mutant_is_caught(name):
     with np.errstate(all="ignore"):
         fails = pins.cwi_pin_failures(mod.cwi_forward_ref)
     assert fails, f"planted mistake {name} passed every CWI pin"
+
+
+def test_cwi_backward_pins():
+    assert pins.cwi_backward_pin_failures(oracle.cwi_backward_ref, oracle.cwi_forward_ref) == []
+
+
+CWI_BWD_MUTANTS = {
+    "dx_gathered_not_scattered": [("np.add.at(dx, (q, slice(lo, lo + c)), w[t] * dy[ok, lo:lo + c])",
+                                   "dx[ok, lo:lo + c] += w[t] * dy[q, lo:lo + c]", 0)],
+    "identity_grad_dropped": [("dx[:, 3 * c:] = dy[:, 3 * c:]", "dx[:, 3 * c:] = 0.0", 0)],
+    "dw_from_own_row": [("dws[branch][t] = (dy[ok, lo:lo + c] * x[q, lo:lo + c]).sum(axis=0)",
+                         "dws[branch][t] = (dy[ok, lo:lo + c] * x[ok, lo:lo + c]).sum(axis=0)", 0)],
+    "cube_grad_taps_flipped": [("tap(2, (dx_ + 1) + 3 * (dy_ + 1) + 9 * (dz + 1), w_3, (dx_, dy_, dz))",
+                                "tap(2, (1 - dx_) + 3 * (1 - dy_) + 9 * (1 - dz), w_3, (dx_, dy_, dz))", 0)],
+}
+
+
+@pytest.mark.parametrize("name", sorted(CWI_BWD_MUTANTS))
+def test_cwi_backward_mutant_is_caught(name):
+    mod = _oracle_from_source(CWI_BWD_MUTANTS[name])
+    with np.errstate(all="ignore"):
+        fails = pins.cwi_backward_pin_failures(mod.cwi_backward_ref, oracle.cwi_forward_ref)
+    assert fails, f"planted mistake {name} passed every CWI backward pin"
