@@ -418,6 +418,14 @@ def bench_cwi(torch, sla, workloads, dev, args):
             "x": torch.from_numpy(f["x"]).to(dev),
             "w": [torch.from_numpy(f[k]).to(dev) for k in ("w_x", "w_y", "w_3")],
             "y": torch.empty(f["n"], f["channels"], dtype=dt, device=dev),
+            "dy": torch.from_numpy(workloads.cast_values(
+                np.random.default_rng([7, s_]).standard_normal(f["x"].shape).astype(np.float32),
+                f["dtype"])).to(dev),
+            "dx": torch.empty(f["n"], f["channels"], dtype=dt, device=dev),
+            "dw": [torch.empty(f[k].shape, dtype=dt, device=dev) for k in ("w_x", "w_y", "w_3")],
+            "ws": torch.empty(sla.cwi_backward_workspace_bytes(f["n"], dt, f["channels"], f["w_x"].shape[0],
+                                                               f["w_y"].shape[0]),
+                              dtype=torch.uint8, device=dev),
             "map": torch.empty(sla.cwi_map_bytes(*f["grid"]) // 4, dtype=torch.int32, device=dev),
             "grid": f["grid"], "n": f["n"], "C": f["channels"],
         })
@@ -428,6 +436,10 @@ def bench_cwi(torch, sla, workloads, dev, args):
     def fwd(st, ordered=True):
         sla.cwi_forward(st["map"], st["grid"], st["coords"], st["x"], *st["w"],
                         order=st["order"] if ordered else None, y=st["y"])
+
+    def bwd(st):
+        sla.cwi_backward(st["map"], st["grid"], st["coords"], st["x"], *st["w"], st["dy"], order=st["order"],
+                         workspace=st["ws"], out=(st["dx"], *st["dw"]))
 
     def timed(fn, reps):
         for i in range(args.warmup):
@@ -460,10 +472,15 @@ def bench_cwi(torch, sla, workloads, dev, args):
     t_build = timed(build, reps)
     t_fwd = timed(fwd, reps)
     t_fwd_rows = timed(lambda st: fwd(st, ordered=False), reps)
+    t_bwd = timed(bwd, reps)
     n = int(np.mean([st["n"] for st in sets]))
     C, e = sets[0]["C"], 2
     cells = int(np.prod(sets[0]["grid"]))
     fwd_bytes = n * (2 * C * e + 12 + 4)          # x read, y written, coordinates, visiting order
+    # backward: dy read and dx written (the reversed-kernel pass), then x and dy
+    # of the three convolution quarters read again for the kernel gradients,
+    # coordinates and visiting order read by both passes
+    bwd_bytes = n * (2 * C * e + 2 * (3 * C // 4) * e + 2 * (12 + 4))
     build_bytes = 4 * cells + n * (12 + 4)        # table cleared, coordinates read, rows written
     return {
         "mode": "cwi",
@@ -476,6 +493,10 @@ def bench_cwi(torch, sla, workloads, dev, args):
         "forward_gbs": fwd_bytes / (t_fwd * 1e-6) / 1e9,
         "forward_frac_of_hbm_peak": fwd_bytes / (t_fwd * 1e-6) / 1e9 / HBM_PEAK_GBS,
         "build_algorithmic_bytes": build_bytes,
+        "backward_us": t_bwd,
+        "backward_algorithmic_bytes": bwd_bytes,
+        "backward_gbs": bwd_bytes / (t_bwd * 1e-6) / 1e9,
+        "backward_frac_of_hbm_peak": bwd_bytes / (t_bwd * 1e-6) / 1e9 / HBM_PEAK_GBS,
     }
 
 

@@ -267,6 +267,28 @@ sla_status_t sla_cwi_forward(const int32_t* map, int32_t gx, int32_t gy, int32_t
                              void* y, sla_stream_t stream);
 
 /*
+ * Backward of sla_cwi_forward (the chain rule; the paper does not write it out):
+ * given dy = dL/dy [n, channels], writes dx [n, channels] and the kernel
+ * gradients dw_x [taps_x, c], dw_y [taps_y, c], dw_3 [27, c], all in `dtype`
+ * (rounded from fp32 sums).  Same table, coordinates, order and shapes as the
+ * forward (the table must hold every voxel: no conflicts).  `workspace`
+ * (caller-owned, 16-byte aligned, at least sla_cwi_backward_workspace_bytes(),
+ * which returns 0 for an unsupported shape) receives fp32 partial sums of the
+ * kernel gradients, one set per block of rows (at most 512 sets); they are
+ * added in a fixed order, so the result is deterministic.  With n = 0 the
+ * kernel gradients are zero.
+ */
+size_t sla_cwi_backward_workspace_bytes(int64_t n, sla_dtype_t dtype, int32_t channels,
+                                        int32_t taps_x, int32_t taps_y);
+
+sla_status_t sla_cwi_backward(const int32_t* map, int32_t gx, int32_t gy, int32_t gz,
+                              const int32_t* coords, int64_t n, const int32_t* order,
+                              sla_dtype_t dtype, int32_t channels, int32_t taps_x, int32_t taps_y,
+                              const void* x, const void* w_x, const void* w_y, const void* w_3,
+                              const void* dy, void* dx, void* dw_x, void* dw_y, void* dw_3,
+                              void* workspace, size_t workspace_bytes, sla_stream_t stream);
+
+/*
  * The naive scatter-based forward that Sec. 3.2 ("Hardware Efficient
  * Implementation") contrasts with the chunk-wise kernel, kept as a comparator
  * for Fig. 4's time-and-memory comparison: the kv matrix phi(k)^T v of every

@@ -26,6 +26,13 @@ hipError_t launch_cwi_forward(const int32_t* map, int32_t gx, int32_t gy, int32_
                               int32_t channels, int32_t kx, int32_t ky, const void* x,
                               const void* w_x, const void* w_y, const void* w_3, void* y,
                               hipStream_t stream);
+size_t cwi_backward_workspace_bytes(int32_t n, int32_t channels, int32_t kx, int32_t ky, int esize);
+hipError_t launch_cwi_backward(const int32_t* map, int32_t gx, int32_t gy, int32_t gz,
+                               const int32_t* coords, int32_t n, const int32_t* order, int dtype,
+                               int32_t channels, int32_t kx, int32_t ky, const void* x,
+                               const void* w_x, const void* w_y, const void* w_3, const void* dy,
+                               void* dx, void* dw_x, void* dw_y, void* dw_3, void* workspace,
+                               hipStream_t stream);
 hipError_t launch_forward_scatter(const void* plan, int32_t n, int32_t W, int dtype, int32_t H,
                                   int32_t d, const void* q, const void* k, const void* v,
                                   void* o, void* workspace, hipStream_t stream);
@@ -33,7 +40,7 @@ hipError_t launch_forward_scatter(const void* plan, int32_t n, int32_t W, int dt
 
 namespace {
 
-constexpr int32_t kAbiVersion = 6;
+constexpr int32_t kAbiVersion = 7;
 
 // cells of a CWI grid, or -1 when a side is not positive or the grid has more
 // than INT32_MAX cells
@@ -264,25 +271,32 @@ SLA_EXPORT sla_status_t sla_cwi_build_map(const int32_t* coords, int64_t n, int3
                                               static_cast<hipStream_t>(stream)));
 }
 
+// shapes of sla_cwi_forward / sla_cwi_backward (see sla.h)
+static sla_status_t cwi_shape_ok(int64_t n, int dtype, int32_t channels, int32_t kx, int32_t ky) {
+  if (n < 0 || n >= INT32_MAX) return SLA_E_ARG;
+  if (dtype < 0 || dtype > 2) return SLA_E_ARG;
+  const int64_t esize = dtype == 0 ? 4 : 2;
+  if (channels < 4 || channels % 4) return SLA_E_UNSUPPORTED;
+  const int64_t piece_bytes = (int64_t)(channels / 4) * esize;
+  if (piece_bytes % 16) return SLA_E_UNSUPPORTED;
+  const int64_t pq = piece_bytes / 16;
+  if (pq > 64 || (64 % pq)) return SLA_E_UNSUPPORTED;
+  if (kx < 1 || ky < 1 || kx > 63 || ky > 63 || !(kx & 1) || !(ky & 1)) return SLA_E_UNSUPPORTED;
+  if (n > 0 && (int64_t)n * channels * esize > (int64_t)UINT32_MAX * 4) return SLA_E_UNSUPPORTED;
+  return SLA_OK;
+}
+
 SLA_EXPORT sla_status_t sla_cwi_forward(const int32_t* map, int32_t gx, int32_t gy, int32_t gz,
                                         const int32_t* coords, int64_t n, const int32_t* order,
                                         sla_dtype_t dtype, int32_t channels, int32_t taps_x,
                                         int32_t taps_y, const void* x, const void* w_x,
                                         const void* w_y, const void* w_3, void* y,
                                         sla_stream_t stream) {
-  if (cwi_cells(gx, gy, gz) < 0 || n < 0 || n >= INT32_MAX) return SLA_E_ARG;
-  if (dtype < 0 || dtype > 2) return SLA_E_ARG;
-  const int64_t esize = dtype == 0 ? 4 : 2;
+  if (cwi_cells(gx, gy, gz) < 0) return SLA_E_ARG;
   // four branches of c channels; a branch row is a whole number of 16-byte
   // pieces, and that number divides 64 (one wave holds whole rows)
-  if (channels < 4 || channels % 4) return SLA_E_UNSUPPORTED;
-  const int64_t piece_bytes = (int64_t)(channels / 4) * esize;
-  if (piece_bytes % 16) return SLA_E_UNSUPPORTED;
-  const int64_t pq = piece_bytes / 16;
-  if (pq > 64 || (64 % pq)) return SLA_E_UNSUPPORTED;
-  if (taps_x < 1 || taps_y < 1 || taps_x > 63 || taps_y > 63 || !(taps_x & 1) || !(taps_y & 1))
-    return SLA_E_UNSUPPORTED;
-  if (n > 0 && (int64_t)n * channels * esize > (int64_t)UINT32_MAX * 4) return SLA_E_UNSUPPORTED;
+  const sla_status_t st = cwi_shape_ok(n, (int)dtype, channels, taps_x, taps_y);
+  if (st != SLA_OK) return st;
   if (n == 0) return SLA_OK;
   if (!map || !coords || !x || !w_x || !w_y || !w_3 || !y) return SLA_E_ARG;
   if (!aligned(map, 4) || !aligned(coords, 4) || (order && !aligned(order, 4)) || !aligned(x, 16) ||
@@ -291,4 +305,41 @@ SLA_EXPORT sla_status_t sla_cwi_forward(const int32_t* map, int32_t gx, int32_t 
   return hip_status(sla::launch_cwi_forward(map, gx, gy, gz, coords, (int32_t)n, order, (int)dtype,
                                             channels, taps_x, taps_y, x, w_x, w_y, w_3, y,
                                             static_cast<hipStream_t>(stream)));
+}
+
+SLA_EXPORT size_t sla_cwi_backward_workspace_bytes(int64_t n, sla_dtype_t dtype, int32_t channels,
+                                                   int32_t taps_x, int32_t taps_y) {
+  if (cwi_shape_ok(n, (int)dtype, channels, taps_x, taps_y) != SLA_OK) return 0;
+  return sla::cwi_backward_workspace_bytes((int32_t)n, channels, taps_x, taps_y,
+                                           dtype == SLA_F32 ? 4 : 2);
+}
+
+SLA_EXPORT sla_status_t sla_cwi_backward(const int32_t* map, int32_t gx, int32_t gy, int32_t gz,
+                                         const int32_t* coords, int64_t n, const int32_t* order,
+                                         sla_dtype_t dtype, int32_t channels, int32_t taps_x,
+                                         int32_t taps_y, const void* x, const void* w_x,
+                                         const void* w_y, const void* w_3, const void* dy, void* dx,
+                                         void* dw_x, void* dw_y, void* dw_3, void* workspace,
+                                         size_t workspace_bytes, sla_stream_t stream) {
+  if (cwi_cells(gx, gy, gz) < 0) return SLA_E_ARG;
+  const sla_status_t st = cwi_shape_ok(n, (int)dtype, channels, taps_x, taps_y);
+  if (st != SLA_OK) return st;
+  if (!dw_x || !dw_y || !dw_3 || !w_x || !w_y || !w_3) return SLA_E_ARG;
+  if (!aligned(w_x, 16) || !aligned(w_y, 16) || !aligned(w_3, 16) || !aligned(dw_x, 4) ||
+      !aligned(dw_y, 4) || !aligned(dw_3, 4))
+    return SLA_E_ARG;
+  if (!workspace || !aligned(workspace, 16)) return SLA_E_ARG;
+  if (workspace_bytes < sla::cwi_backward_workspace_bytes((int32_t)n, channels, taps_x, taps_y,
+                                                          dtype == SLA_F32 ? 4 : 2))
+    return SLA_E_WORKSPACE;
+  if (n > 0) {
+    if (!map || !coords || !x || !dy || !dx) return SLA_E_ARG;
+    if (!aligned(map, 4) || !aligned(coords, 4) || (order && !aligned(order, 4)) || !aligned(x, 16) ||
+        !aligned(dy, 16) || !aligned(dx, 16))
+      return SLA_E_ARG;
+  }
+  // n = 0 still writes zero kernel gradients
+  return hip_status(sla::launch_cwi_backward(map, gx, gy, gz, coords, (int32_t)n, order, (int)dtype,
+                                             channels, taps_x, taps_y, x, w_x, w_y, w_3, dy, dx, dw_x,
+                                             dw_y, dw_3, workspace, static_cast<hipStream_t>(stream)));
 }

@@ -119,6 +119,7 @@ struct CwiArgs {
   int32_t pq;            // 16-byte pieces per branch row (divides 64)
   int32_t kx, ky;
   int32_t groups;        // row groups of 64 / pq rows
+  int32_t flip;          // 1: every kernel reversed (the input gradient)
 };
 
 // Workgroup b: the four branches (one wave each) of row group g(b); groups are
@@ -181,7 +182,8 @@ __global__ __launch_bounds__(256) void k_cwi_fwd(CwiArgs a, const T* __restrict_
     for (int u = 0; u < kCwiGroup; ++u) {
       const bool hit = (uint32_t)nb[u] < (uint32_t)a.n;
       xv[u] = hit ? *reinterpret_cast<const uint4*>(x + (size_t)nb[u] * C + col) : make_uint4(0, 0, 0, 0);
-      const int tap = branch == 2 ? (t0 + u + 9) % 27 : t0 + u;
+      int tap = branch == 2 ? (t0 + u + 9) % 27 : t0 + u;
+      if (a.flip) tap = (branch == 2 ? 26 : taps - 1) - tap;  // the mirrored offset's weight
       wv[u] = (hit && t0 + u < taps) ? *reinterpret_cast<const uint4*>(w + (size_t)tap * a.c + pc * E)
                                      : make_uint4(0, 0, 0, 0);
     }
@@ -204,12 +206,12 @@ hipError_t launch_cwi_build_map(const int32_t* coords, int32_t n, int32_t gx, in
   return hipGetLastError();
 }
 
-// dtype: 0 f32, 1 f16, 2 bf16
-hipError_t launch_cwi_forward(const int32_t* map, int32_t gx, int32_t gy, int32_t gz,
-                              const int32_t* coords, int32_t n, const int32_t* order, int dtype,
-                              int32_t channels, int32_t kx, int32_t ky, const void* x,
-                              const void* w_x, const void* w_y, const void* w_3, void* y,
-                              hipStream_t stream) {
+// dtype: 0 f32, 1 f16, 2 bf16; flip: every kernel reversed
+static hipError_t cwi_forward_launch(const int32_t* map, int32_t gx, int32_t gy, int32_t gz,
+                                     const int32_t* coords, int32_t n, const int32_t* order,
+                                     int dtype, int32_t channels, int32_t kx, int32_t ky,
+                                     const void* x, const void* w_x, const void* w_y,
+                                     const void* w_3, void* y, hipStream_t stream, int flip) {
   CwiArgs a;
   a.map = map;
   a.coords = coords;
@@ -223,6 +225,7 @@ hipError_t launch_cwi_forward(const int32_t* map, int32_t gx, int32_t gy, int32_
   a.pq = a.c * esize / 16;
   a.kx = kx;
   a.ky = ky;
+  a.flip = flip;
   const int rows_per = 64 / a.pq;
   a.groups = (n + rows_per - 1) / rows_per;
   const unsigned grid = (unsigned)(((int64_t)a.groups + 7) / 8 * 8);
@@ -242,6 +245,223 @@ hipError_t launch_cwi_forward(const int32_t* map, int32_t gx, int32_t gy, int32_
                        static_cast<const bf16_t*>(w_y), static_cast<const bf16_t*>(w_3),
                        static_cast<bf16_t*>(y));
   return hipGetLastError();
+}
+
+hipError_t launch_cwi_forward(const int32_t* map, int32_t gx, int32_t gy, int32_t gz,
+                              const int32_t* coords, int32_t n, const int32_t* order, int dtype,
+                              int32_t channels, int32_t kx, int32_t ky, const void* x,
+                              const void* w_x, const void* w_y, const void* w_3, void* y,
+                              hipStream_t stream) {
+  return cwi_forward_launch(map, gx, gy, gz, coords, n, order, dtype, channels, kx, ky, x, w_x, w_y,
+                            w_3, y, stream, 0);
+}
+
+// ------------------------------------------------------------------ backward
+// The chain rule of the module, per tap: dx[q] += w[t] dy[p] and
+// dw[t] += dy[p] x[q] for the voxel q at p's cell + offset_t.
+//  * dx: with unique voxels, q is p's neighbour at +o exactly when p is q's at -o,
+//    so dx is the forward applied to dy with every kernel reversed (flip); the
+//    identity quarter passes dy through.
+//  * dw: k_cwi_dw.  A lane owns one (tap, 16-byte piece) pair of a branch, so
+//    its fp32 sums are one piece (8 fp16 or 4 fp32 channels) and no sums are
+//    exchanged between lanes: a wave covers 64 pairs (the 13 taps x 4 pieces
+//    of a 32-channel fp16 branch fit one wave) and walks a contiguous range of
+//    rows, kDwBatch rows at a time with all their loads in flight (a row's
+//    index and cell are the same for the whole wave: fetched once per 64 rows,
+//    one per lane, and broadcast with readlane).  The four waves of a
+//    workgroup take adjacent row ranges; their sums are added in wave order
+//    and written as the workgroup's partial, and k_cwi_dw_reduce adds the
+//    partials in workgroup order.  Every order is fixed, so the result is
+//    deterministic.
+constexpr int kDwWaves = 4;          // waves per workgroup: adjacent row ranges
+constexpr int kDwBatch = 8;          // rows whose loads are in flight together
+#ifndef SLA_CWI_DW_ROWS
+#define SLA_CWI_DW_ROWS 64
+#endif
+constexpr int kDwRows = SLA_CWI_DW_ROWS;  // rows per wave, until kDwMaxBlocks is reached
+constexpr int kDwMaxBlocks = 512;    // workgroups per (branch, pair slice), at most
+
+struct DwGrid {
+  int32_t blocks;        // workgroups per (branch, pair slice)
+  int32_t rows;          // rows per wave
+  int32_t slices[3];     // pair slices (of 64) per branch
+};
+
+inline DwGrid cwi_dw_grid(int32_t n, int32_t c, int esize, int32_t kx, int32_t ky, int32_t gz) {
+  DwGrid g;
+  const int64_t waves = ((int64_t)n + kDwRows - 1) / kDwRows;
+  g.blocks = (int32_t)std::min<int64_t>(kDwMaxBlocks, std::max<int64_t>(1, (waves + kDwWaves - 1) / kDwWaves));
+  const int64_t per_block = (int64_t)g.blocks * kDwWaves;
+  g.rows = (int32_t)(((int64_t)n + per_block - 1) / per_block);
+  const int pq = c * esize / 16;
+  const int taps[3] = {kx, ky, gz == 1 ? 9 : 27};
+  for (int b = 0; b < 3; ++b) g.slices[b] = (taps[b] * pq + 63) / 64;
+  return g;
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_cwi_dw(CwiArgs a, DwGrid g, const T* __restrict__ x,
+                                                const T* __restrict__ dy,
+                                                float* __restrict__ partial) {
+  using P = CwiPiece<T>;
+  constexpr int E = P::kElems;
+  __shared__ float s_red[kDwWaves][64 * E];
+  // workgroups in [branch][pair slice][row block] order
+  int32_t b = (int32_t)blockIdx.x;
+  int branch = 0;
+  const int32_t n0 = g.slices[0] * g.blocks, n1 = n0 + g.slices[1] * g.blocks;
+  if (b >= n1) {
+    branch = 2;
+    b -= n1;
+  } else if (b >= n0) {
+    branch = 1;
+    b -= n0;
+  }
+  const int32_t slice = b / g.blocks, kb = b - slice * g.blocks;
+  const int wave = (int)(threadIdx.x >> 6), lane = lane_id();
+  const int taps = branch == 0 ? a.kx : (branch == 1 ? a.ky : (a.gz == 1 ? 9 : 27));
+  const int half = branch == 0 ? (a.kx - 1) / 2 : (branch == 1 ? (a.ky - 1) / 2 : 0);
+  const int base = branch == 0 ? 0 : (branch == 1 ? a.kx : a.kx + a.ky);
+  const int pair = slice * 64 + lane;
+  const bool valid = pair < taps * a.pq;
+  const int t = valid ? pair / a.pq : 0;
+  const int pc = valid ? pair - t * a.pq : 0;
+  const int C = 4 * a.c;
+  const int col = branch * a.c + pc * E;
+  const int k = branch == 2 ? (t + 9) % 27 : t;  // kernel tap; 3 x 3 x 3 visited in-plane first
+  const int ox = branch == 0 ? t - half : (branch == 2 ? k % 3 - 1 : 0);
+  const int oy = branch == 1 ? t - half : (branch == 2 ? (k / 3) % 3 - 1 : 0);
+  const int oz = branch == 2 ? k / 9 - 1 : 0;
+  const int32_t r0 = min(a.n, (kb * kDwWaves + wave) * g.rows), r1 = min(a.n, r0 + g.rows);
+  float acc[E];
+#pragma unroll
+  for (int e = 0; e < E; ++e) acc[e] = 0.f;
+  // 64 rows at a time: lane l fetches row l's index and cell once, and each
+  // batch reads them back with readlane (no memory round trip)
+  for (int32_t c0 = r0; c0 < r1; c0 += 64) {
+    const int32_t pl = c0 + lane;
+    const int32_t lrow = pl < r1 ? (a.order ? a.order[pl] : pl) : -1;
+    const bool lok = (uint32_t)lrow < (uint32_t)a.n;
+    const int32_t lcx = lok ? a.coords[3 * lrow] : 0, lcy = lok ? a.coords[3 * lrow + 1] : 0,
+                  lcz = lok ? a.coords[3 * lrow + 2] : 0;
+    const int cnt = min(64, r1 - c0);
+    for (int q0 = 0; q0 < cnt; q0 += kDwBatch) {
+      int32_t nb[kDwBatch];
+      uint4 dv[kDwBatch];
+#pragma unroll
+      for (int u = 0; u < kDwBatch; ++u) {
+        const int32_t row = __builtin_amdgcn_readlane(lrow, q0 + u);  // -1 past the range
+        const int32_t cx = __builtin_amdgcn_readlane(lcx, q0 + u), cy = __builtin_amdgcn_readlane(lcy, q0 + u),
+                      cz = __builtin_amdgcn_readlane(lcz, q0 + u);
+        const int32_t nx = cx + ox, ny = cy + oy, nz = cz + oz;
+        const bool in = valid && (uint32_t)row < (uint32_t)a.n && (uint32_t)nx < (uint32_t)a.gx &&
+                        (uint32_t)ny < (uint32_t)a.gy && (uint32_t)nz < (uint32_t)a.gz;
+        nb[u] = in ? a.map[((int64_t)nz * a.gy + ny) * a.gx + nx] : -1;
+        dv[u] = in ? *reinterpret_cast<const uint4*>(dy + (size_t)row * C + col) : make_uint4(0, 0, 0, 0);
+      }
+      uint4 xv[kDwBatch];
+#pragma unroll
+      for (int u = 0; u < kDwBatch; ++u)
+        xv[u] = (uint32_t)nb[u] < (uint32_t)a.n ? *reinterpret_cast<const uint4*>(x + (size_t)nb[u] * C + col)
+                                                 : make_uint4(0, 0, 0, 0);
+#pragma unroll
+      for (int u = 0; u < kDwBatch; ++u) P::add(acc, xv[u], dv[u]);  // += dy[row] * x[neighbour]
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < E; ++e) s_red[wave][lane * E + e] = acc[e];
+  __syncthreads();
+  if (wave != 0 || !valid) return;
+  const int32_t total = (a.kx + a.ky + 27) * a.c;
+  float* dst = partial + (size_t)kb * total + (size_t)(base + k) * a.c + pc * E;
+#pragma unroll
+  for (int e = 0; e < E; ++e)
+    dst[e] = ((s_red[0][lane * E + e] + s_red[1][lane * E + e]) + s_red[2][lane * E + e]) +
+             s_red[3][lane * E + e];
+}
+
+// dw[i] = sum of the workgroups' partials, in workgroup order (16 interleaved
+// slices, then the slices in order).  The 3 x 3 x 3 taps off the plane of a
+// one-cell-deep grid are never visited: their gradients are zero.
+template <typename T>
+__global__ __launch_bounds__(1024) void k_cwi_dw_reduce(const float* __restrict__ partial,
+                                                        int32_t blocks, int32_t kx, int32_t ky,
+                                                        int32_t c, int32_t gz,
+                                                        T* __restrict__ dw_x, T* __restrict__ dw_y,
+                                                        T* __restrict__ dw_3) {
+  __shared__ float s[16][64];
+  const int32_t total = (kx + ky + 27) * c;
+  const int e = (int)(threadIdx.x & 63), sl = (int)(threadIdx.x >> 6);
+  const int32_t i = (int32_t)blockIdx.x * 64 + e;
+  const int32_t i3 = i - (kx + ky) * c;
+  const bool unvisited = i3 >= 0 && gz == 1 && (i3 / c) / 9 != 1;
+  float acc = 0.f;
+  if (i < total && !unvisited) {
+#pragma unroll 4
+    for (int32_t b = sl; b < blocks; b += 16) acc += partial[(size_t)b * total + i];
+  }
+  s[sl][e] = acc;
+  __syncthreads();
+  if (sl != 0 || i >= total) return;
+  float r = 0.f;
+#pragma unroll
+  for (int k = 0; k < 16; ++k) r += s[k][e];
+  T* out = i < kx * c ? dw_x + i : (i < (kx + ky) * c ? dw_y + (i - kx * c) : dw_3 + i3);
+  if constexpr (std::is_same<T, float>::value) *out = r;
+  else *reinterpret_cast<unsigned short*>(out) = f32_to_u16<T>(r);
+}
+
+size_t cwi_backward_workspace_bytes(int32_t n, int32_t channels, int32_t kx, int32_t ky, int esize) {
+  const int c = channels / 4;
+  const DwGrid g = cwi_dw_grid(n, c, esize, kx, ky, 1);
+  return (size_t)g.blocks * (size_t)((kx + ky + 27) * c) * sizeof(float);
+}
+
+template <typename T>
+static hipError_t launch_dw(const CwiArgs& a, const DwGrid& g, const void* x, const void* dy,
+                            float* partial, void* dw_x, void* dw_y, void* dw_3, hipStream_t stream) {
+  const unsigned grid = (unsigned)((g.slices[0] + g.slices[1] + g.slices[2]) * g.blocks);
+  hipLaunchKernelGGL((k_cwi_dw<T>), dim3(grid), dim3(256), 0, stream, a, g, static_cast<const T*>(x),
+                     static_cast<const T*>(dy), partial);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const int32_t total = (a.kx + a.ky + 27) * a.c;
+  hipLaunchKernelGGL((k_cwi_dw_reduce<T>), dim3((unsigned)((total + 63) / 64)), dim3(1024), 0, stream,
+                     partial, g.blocks, a.kx, a.ky, a.c, a.gz, static_cast<T*>(dw_x),
+                     static_cast<T*>(dw_y), static_cast<T*>(dw_3));
+  return hipGetLastError();
+}
+
+hipError_t launch_cwi_backward(const int32_t* map, int32_t gx, int32_t gy, int32_t gz,
+                               const int32_t* coords, int32_t n, const int32_t* order, int dtype,
+                               int32_t channels, int32_t kx, int32_t ky, const void* x,
+                               const void* w_x, const void* w_y, const void* w_3, const void* dy,
+                               void* dx, void* dw_x, void* dw_y, void* dw_3, void* workspace,
+                               hipStream_t stream) {
+  hipError_t e = hipSuccess;
+  if (n > 0)
+    e = cwi_forward_launch(map, gx, gy, gz, coords, n, order, dtype, channels, kx, ky, dy, w_x, w_y,
+                           w_3, dx, stream, 1);
+  if (e != hipSuccess) return e;
+  CwiArgs a;
+  a.map = map;
+  a.coords = coords;
+  a.order = order;
+  a.n = n;
+  a.gx = gx;
+  a.gy = gy;
+  a.gz = gz;
+  a.c = channels / 4;
+  const int esize = dtype == 0 ? 4 : 2;
+  a.pq = a.c * esize / 16;
+  a.kx = kx;
+  a.ky = ky;
+  a.flip = 0;
+  const DwGrid g = cwi_dw_grid(n, a.c, esize, kx, ky, gz);
+  float* partial = static_cast<float*>(workspace);
+  if (dtype == 0) return launch_dw<float>(a, g, x, dy, partial, dw_x, dw_y, dw_3, stream);
+  if (dtype == 1) return launch_dw<_Float16>(a, g, x, dy, partial, dw_x, dw_y, dw_3, stream);
+  return launch_dw<bf16_t>(a, g, x, dy, partial, dw_x, dw_y, dw_3, stream);
 }
 
 }  // namespace sla

@@ -17,6 +17,7 @@ Functions mirror the C ABI in include/sla.h:
     cwi_map_bytes(gx, gy, gz)
     cwi_build_map(coords, grid, map=None) -> (map, conflicts)
     cwi_forward(map, grid, coords, x, w_x, w_y, w_3, order=None, y=None) -> y
+    cwi_backward(map, grid, coords, x, w_x, w_y, w_3, dy, order=None) -> (dx, dw_x, dw_y, dw_3)
     scatter_workspace_bytes(n, heads, head_dim)
     forward_scatter(plan, q, k, v, out=None, workspace=None) -> o   (naive comparator)
 """
@@ -48,6 +49,8 @@ EXPORTED = (
     "sla_cwi_map_bytes",
     "sla_cwi_build_map",
     "sla_cwi_forward",
+    "sla_cwi_backward_workspace_bytes",
+    "sla_cwi_backward",
     "sla_scatter_workspace_bytes",
     "sla_forward_scatter",
 )
@@ -115,6 +118,11 @@ def lib() -> ctypes.CDLL:
     L.sla_cwi_build_map.argtypes = [vp, i64, i32, i32, i32, vp, sz, vp, vp]
     L.sla_cwi_forward.restype = ctypes.c_int
     L.sla_cwi_forward.argtypes = [vp, i32, i32, i32, vp, i64, vp, en, i32, i32, i32, vp, vp, vp, vp, vp, vp]
+    L.sla_cwi_backward_workspace_bytes.restype = sz
+    L.sla_cwi_backward_workspace_bytes.argtypes = [i64, en, i32, i32, i32]
+    L.sla_cwi_backward.restype = ctypes.c_int
+    L.sla_cwi_backward.argtypes = [vp, i32, i32, i32, vp, i64, vp, en, i32, i32, i32, vp, vp, vp, vp, vp, vp,
+                                   vp, vp, vp, vp, sz, vp]
     L.sla_scatter_workspace_bytes.restype = sz
     L.sla_scatter_workspace_bytes.argtypes = [i64, i32, i32]
     L.sla_forward_scatter.restype = ctypes.c_int
@@ -371,6 +379,42 @@ def cwi_forward(map, grid, coords, x, w_x, w_y, w_3, order=None, y=None):
                                _ptr(y), _stream(x.device))
     _check(st, "sla_cwi_forward")
     return y
+
+
+def cwi_backward_workspace_bytes(n: int, dtype, channels: int, taps_x: int, taps_y: int) -> int:
+    """Workspace of cwi_backward (0: unsupported shape); dtype a torch dtype."""
+    return int(lib().sla_cwi_backward_workspace_bytes(int(n), _dtype_code(dtype), int(channels), int(taps_x),
+                                                      int(taps_y)))
+
+
+def cwi_backward(map, grid, coords, x, w_x, w_y, w_3, dy, order=None, workspace=None, out=None):
+    """Backward of cwi_forward (sla_cwi_backward): returns (dx, dw_x, dw_y, dw_3),
+    written into `out` when given (tensors shaped like x, w_x, w_y, w_3)."""
+    torch = _torch()
+    gx, gy, gz = (int(g) for g in grid)
+    n, C = x.shape
+    if dy.shape != x.shape or dy.dtype != x.dtype or not dy.is_contiguous():
+        raise ValueError("dy must be a contiguous tensor like x")
+    code = _dtype_code(x.dtype)
+    need = cwi_backward_workspace_bytes(n, x.dtype, C, w_x.shape[0], w_y.shape[0])
+    if need == 0:
+        raise SlaError(SLA_E_UNSUPPORTED, "sla_cwi_backward_workspace_bytes")
+    if workspace is None:
+        workspace = torch.empty(need, dtype=torch.uint8, device=x.device)
+    if out is None:
+        dx = torch.empty_like(x)
+        dws = [torch.empty_like(w) for w in (w_x, w_y, w_3)]
+    else:
+        dx, dws = out[0], list(out[1:])
+        for t, ref in zip(out, (x, w_x, w_y, w_3)):
+            if t.shape != ref.shape or t.dtype != ref.dtype or not t.is_contiguous():
+                raise ValueError("out tensors must be contiguous and shaped like x, w_x, w_y, w_3")
+    st = lib().sla_cwi_backward(_ptr(map), gx, gy, gz, _ptr(coords), n, _ptr(order), code, C,
+                                int(w_x.shape[0]), int(w_y.shape[0]), _ptr(x), _ptr(w_x), _ptr(w_y), _ptr(w_3),
+                                _ptr(dy), _ptr(dx), *(_ptr(t) for t in dws), _ptr(workspace),
+                                int(workspace.numel() * workspace.element_size()), _stream(x.device))
+    _check(st, "sla_cwi_backward")
+    return (dx, *dws)
 
 
 def scatter_workspace_bytes(n: int, heads: int, head_dim: int) -> int:

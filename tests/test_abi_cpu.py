@@ -46,7 +46,7 @@ def test_only_the_abi_is_exported():
 
 
 def test_queries(L):
-    assert L.sla_abi_version() == 6
+    assert L.sla_abi_version() == 7
     assert L.sla_max_windows() == 16384
     assert L.sla_default_chunk_rows() == 64
     for s in range(5):
@@ -208,3 +208,23 @@ def test_cwi_argument_errors(L):
     assert fw(x=FAKE + 4) == sla.SLA_E_ARG
     assert fw(order=FAKE + 2) == sla.SLA_E_ARG
     assert fw(n=0) == sla.SLA_OK
+
+
+def test_cwi_backward_argument_errors(L):
+    wb = L.sla_cwi_backward_workspace_bytes
+    # a workgroup per 256 rows (four waves of 64), at most 512
+    assert wb(60000, 1, 128, 13, 13) == 235 * 53 * 32 * 4
+    assert wb(100, 1, 128, 13, 13) == 1 * 53 * 32 * 4
+    assert wb(10 ** 6, 1, 128, 13, 13) == 512 * 53 * 32 * 4
+    assert wb(0, 1, 128, 13, 13) == 53 * 32 * 4                  # the zero gradients still go through it
+    assert wb(100, 1, 2048, 63, 63) == 153 * 512 * 4
+    assert wb(100, 1, 96, 13, 13) == 0
+    need = wb(100, 1, 128, 13, 13)
+
+    def bw(ws=FAKE, wsb=need, n=100, dx=FAKE, C=128):
+        return L.sla_cwi_backward(FAKE, 8, 8, 1, FAKE, n, None, 1, C, 13, 13, FAKE, FAKE, FAKE, FAKE, FAKE, dx,
+                                  FAKE, FAKE, FAKE, ws, wsb, None)
+    assert bw(wsb=need - 4) == sla.SLA_E_WORKSPACE
+    assert bw(ws=None) == sla.SLA_E_ARG
+    assert bw(dx=None) == sla.SLA_E_ARG
+    assert bw(C=96) == sla.SLA_E_UNSUPPORTED

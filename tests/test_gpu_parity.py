@@ -646,3 +646,90 @@ def test_cwi_conflicts_and_empty(sla):
     m0, c0 = sla.cwi_build_map(torch.zeros((0, 3), dtype=torch.int32, device="cuda"), (4, 4, 2))
     torch.cuda.synchronize()
     assert int(c0.cpu()[0]) == 0 and bool((m0 == -1).all())
+
+
+CWI_DW_TOL = {"f32": 1e-5, "f16": 2e-3, "bf16": 1e-2}   # fp32 sums rounded once to the storage type
+
+
+def cwi_backward_parity(S, coords, grid, x, w_x, w_y, w_3, dy, dtype, order=None, label="", repeat=False):
+    import torch
+
+    cc = torch.from_numpy(np.ascontiguousarray(coords.astype(np.int32))).cuda()
+    m, conflicts = S.cwi_build_map(cc, grid)
+    tord = None if order is None else torch.from_numpy(np.ascontiguousarray(order.astype(np.int32))).cuda()
+    dev = lambda a: to_dev(a, dtype)  # noqa: E731
+    args = (m, grid, cc, dev(x), dev(w_x), dev(w_y), dev(w_3), dev(dy))
+    got = S.cwi_backward(*args, order=tord)
+    torch.cuda.synchronize()
+    assert int(conflicts.cpu()[0]) == 0
+    got = [to_host64(t, dtype) for t in got]
+    w = lambda a: oracle.widen(a, dtype)  # noqa: E731
+    ref = oracle.cwi_backward_ref(coords, w(x), w(w_x), w(w_y), w(w_3), w(dy), grid)
+    n, C = x.shape
+    errs = []
+    if n:
+        errs.append(rel_err_per_head(got[0].reshape(n, 4, C // 4), ref[0].reshape(n, 4, C // 4),
+                                     1e-3 * float(np.abs(ref[0]).max())))
+        # the identity quarter passes dy through, bit for bit
+        assert np.array_equal(got[0][:, 3 * C // 4:], w(dy)[:, 3 * C // 4:])
+    else:
+        errs.append(0.0)
+    for g, r in zip(got[1:], ref[1:]):
+        scale = max(float(np.abs(r).max()), 1e-30)
+        errs.append(float(np.abs(g - r).max()) / scale if r.size else 0.0)
+        if n == 0:
+            assert not np.any(g), "kernel gradients of an empty set must be zero"
+    _say(f"[cwi-bwd {label}] n={n} C={C} grid={grid} {dtype} dx={errs[0]:.3e} "
+         f"dw_x={errs[1]:.3e} dw_y={errs[2]:.3e} dw_3={errs[3]:.3e}")
+    assert errs[0] <= TOL[dtype], f"{label}: dx relative error {errs[0]:.3e}"
+    assert max(errs[1:]) <= CWI_DW_TOL[dtype], f"{label}: kernel-gradient relative error {max(errs[1:]):.3e}"
+    if repeat:   # fixed reduction order: a second call (into given buffers) gives the same bits
+        out = tuple(torch.full_like(t, float("nan")) for t in (args[3], *args[4:7]))
+        ws = torch.empty(S.cwi_backward_workspace_bytes(n, args[3].dtype, C, w_x.shape[0], w_y.shape[0]),
+                         dtype=torch.uint8, device="cuda")
+        again = [to_host64(t, dtype) for t in S.cwi_backward(*args, order=tord, workspace=ws, out=out)]
+        torch.cuda.synchronize()
+        assert all(np.array_equal(a, b) for a, b in zip(got, again))
+
+
+def test_cwi_backward_frame(sla):
+    # the Waymo-like pillar frame, in the SLA plan's window order and in row order
+    f = workloads.make_cwi_frame()
+    perm, _, _ = oracle.segments_ref(f["ids"], f["num_windows"])
+    rng = np.random.default_rng(63)
+    dy = workloads.cast_values(rng.standard_normal(f["x"].shape).astype(np.float32), f["dtype"])
+    for order in (perm, None):
+        cwi_backward_parity(sla, f["coords"], f["grid"], f["x"], f["w_x"], f["w_y"], f["w_3"], dy, f["dtype"],
+                            order=order, label="frame" + ("-window-order" if order is not None else ""),
+                            repeat=order is not None)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "f16", "bf16"])
+@pytest.mark.parametrize("C,kx,ky", [(32, 13, 13), (64, 5, 31), (128, 1, 63), (256, 13, 3)])
+def test_cwi_backward_voxels(sla, dtype, C, kx, ky):
+    # 3D voxel grids (all 27 cube taps), random occupancy, rows shuffled
+    if dtype == "f32" and C == 32:
+        C = 16
+    rng = np.random.default_rng([64, C, kx, len(dtype)])
+    grid = (37, 29, 5)
+    occ = rng.random(grid[::-1]) < 0.3
+    zz, yy, xx = np.nonzero(occ)
+    coords = np.stack([xx, yy, zz], axis=1)[rng.permutation(zz.size)]
+    n, c = coords.shape[0], C // 4
+    cast = lambda a: workloads.cast_values(a.astype(np.float32), dtype)  # noqa: E731
+    x, dy = cast(rng.standard_normal((n, C))), cast(rng.standard_normal((n, C)))
+    w_x, w_y, w_3 = (cast(rng.standard_normal((k, c)) / np.sqrt(k)) for k in (kx, ky, 27))
+    cwi_backward_parity(sla, coords, grid, x, w_x, w_y, w_3, dy, dtype, order=rng.permutation(n),
+                        label=f"vox{C}")
+
+
+def test_cwi_backward_small_and_empty(sla):
+    # a handful of voxels (one row group, most lanes idle), a lone voxel, and none
+    rng = np.random.default_rng(65)
+    for n in (5, 1, 0):
+        cells = rng.choice(6 * 5 * 2, size=n, replace=False)
+        coords = np.stack([cells % 6, (cells // 6) % 5, cells // 30], axis=1)
+        x, dy = (workloads.cast_values(rng.standard_normal((n, 64)).astype(np.float32), "f16") for _ in range(2))
+        w_x, w_y, w_3 = (workloads.cast_values(rng.standard_normal((k, 16)).astype(np.float32), "f16")
+                         for k in (7, 3, 27))
+        cwi_backward_parity(sla, coords.reshape(n, 3), (6, 5, 2), x, w_x, w_y, w_3, dy, "f16", label=f"n{n}")
