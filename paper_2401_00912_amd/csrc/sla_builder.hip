@@ -70,37 +70,63 @@ struct OpMax2 {
 };
 
 
+// One step of a wave scan: v op (v moved by the DPP control CTRL into the rows
+// of ROWS); lanes the move does not reach take the identity.
+template <int CTRL, int ROWS, class Op, typename V>
+__device__ __forceinline__ V dpp_scan_step(V v, V identity, Op op) {
+  if constexpr (sizeof(V) == 4) {
+    return op(v, (V)__builtin_amdgcn_update_dpp((int)identity, (int)v, CTRL, ROWS, 0xf, false));
+  } else {
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp((int)(uint32_t)identity, (int)(uint32_t)v,
+                                                              CTRL, ROWS, 0xf, false);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp((int)(uint32_t)(identity >> 32),
+                                                              (int)(uint32_t)(v >> 32), CTRL, ROWS, 0xf,
+                                                              false);
+    return op(v, ((V)hi << 32) | lo);
+  }
+}
+
+// Inclusive scan over the 64 lanes in lane order: shifts by 1, 2, 4 and 8
+// lanes inside each row of 16, then lane 15 of rows 0 and 2 into rows 1 and 3,
+// then lane 31 into rows 2 and 3 (DPP moves, no LDS round trips).
+template <class Op, typename V>
+__device__ __forceinline__ V wave_inclusive_scan(V v, V identity, Op op) {
+  v = dpp_scan_step<0x111, 0xf>(v, identity, op);  // row_shr:1
+  v = dpp_scan_step<0x112, 0xf>(v, identity, op);  // row_shr:2
+  v = dpp_scan_step<0x114, 0xf>(v, identity, op);  // row_shr:4
+  v = dpp_scan_step<0x118, 0xf>(v, identity, op);  // row_shr:8
+  v = dpp_scan_step<0x142, 0xa>(v, identity, op);  // row_bcast:15
+  v = dpp_scan_step<0x143, 0xc>(v, identity, op);  // row_bcast:31
+  return v;
+}
+
+template <typename V>
+__device__ __forceinline__ V read_lane(V v, int lane) {
+  if constexpr (sizeof(V) == 4) {
+    return (V)__builtin_amdgcn_readlane((int)v, lane);
+  } else {
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)v, lane);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(v >> 32), lane);
+    return ((V)hi << 32) | lo;
+  }
+}
+
 // Exclusive scan of one value per thread in thread order; *total gets the
-// reduction of all values.  Uses s[0..32]; ends with a barrier so s can be reused.
+// reduction of all values.  Each wave scans its lanes, publishes its total in
+// s[0..15], and after one barrier every wave scans the wave totals itself.
+// Ends with a barrier so s can be reused.
 template <class Op, typename V = int32_t>
 __device__ V block_exscan(V x, V identity, Op op, V* s, V* total) {
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6, nwv = blockDim.x >> 6;
-  V inc = x;
-#pragma unroll
-  for (int d = 1; d < 64; d <<= 1) {
-    const V y = __shfl_up(inc, d, 64);
-    if (lane >= d) inc = op(inc, y);
-  }
+  const V inc = wave_inclusive_scan(x, identity, op);
   if (lane == 63) s[wv] = inc;
   lds_sync();
-  if (wv == 0) {
-    const V v = lane < nwv ? s[lane] : identity;
-    V inc2 = v;
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
-      const V y = __shfl_up(inc2, d, 64);
-      if (lane >= d) inc2 = op(inc2, y);
-    }
-    V ex2 = __shfl_up(inc2, 1, 64);
-    if (lane == 0) ex2 = identity;
-    if (lane < nwv) s[lane] = ex2;
-    if (lane == nwv - 1) s[32] = inc2;
-  }
-  lds_sync();
+  const V tinc = wave_inclusive_scan(lane < nwv ? s[lane] : identity, identity, op);
+  const V before = wv > 0 ? read_lane(tinc, wv - 1) : identity;
+  *total = read_lane(tinc, nwv - 1);
   V ex = __shfl_up(inc, 1, 64);
   if (lane == 0) ex = identity;
-  const V r = op(s[wv], ex);
-  *total = s[32];
+  const V r = op(before, ex);
   lds_sync();
   return r;
 }
@@ -356,16 +382,21 @@ __global__ __launch_bounds__(kBuildThreads) void k_scatter(
   const int nbits = W > 1 ? 32 - __clz(W - 1) : 0;
   int32_t* h = hist + wv * W;
   const uint64_t lt = lanemask_lt(lane);
-  auto count_group = [&](int32_t id) {
+  // returns the row's rank among this wave's rows of its window (-1: invalid id)
+  auto count_group = [&](int32_t id) -> int32_t {
     const bool valid = (uint32_t)id < (uint32_t)W;
     const uint64_t m = match_key(id, valid, nbits);
-    if (valid && (m & lt) == 0) h[id] += __popcll(m);
+    if (!valid) return -1;
+    const int32_t hb = h[id];
+    if ((m & lt) == 0) h[id] = hb + __popcll(m);
+    return hb + __popcll(m & lt);
   };
   auto id_at = [&](int64_t r) -> int32_t { return r + lane < rend ? ids[r + lane] : -1; };
+  int32_t rk0 = -1, rk1 = -1;   // ranks of the first two groups' rows
   auto count_rows = [&]() {
     if (ranks) {
-      count_group(id0);
-      if (rbeg + 64 < rend) count_group(id1);
+      rk0 = count_group(id0);
+      if (rbeg + 64 < rend) rk1 = count_group(id1);
       for (int64_t r = rbeg + 128; r < rend; r += 64) count_group(id_at(r));
     }
   };
@@ -450,13 +481,17 @@ __global__ __launch_bounds__(kBuildThreads) void k_scatter(
     count_rows();
     lds_sync();
   }
-  // (d) exclusive prefix of the per-wave counts over the waves
+  // (d) exclusive prefix of the per-wave counts over the waves (all of a
+  // window's counts are read before any is written back)
   for (int w = tid; w < W; w += T) {
+    int32_t t[kBuildThreads / 64];
+#pragma unroll
+    for (int v = 0; v < kBuildThreads / 64; ++v) t[v] = v < nws ? hist[v * W + w] : 0;
     int32_t run = 0;
-    for (int v = 0; v < nws; ++v) {
-      const int32_t t = hist[v * W + w];
-      hist[v * W + w] = run;
-      run += t;
+#pragma unroll
+    for (int v = 0; v < kBuildThreads / 64; ++v) {
+      if (v < nws) hist[v * W + w] = run;
+      run += t[v];
     }
   }
   lds_sync();
@@ -476,10 +511,24 @@ __global__ __launch_bounds__(kBuildThreads) void k_scatter(
       if ((m & lt) == 0) h[id] = hb + __popcll(m);
     }
   };
+  auto place = [&](int64_t r, int32_t id, int32_t rk) {
+    if (rk < 0) return;
+    const int32_t pos = base[id] + h[id] + rk;
+    if ((uint32_t)pos < (uint32_t)n) {
+      perm[pos] = (int32_t)(r + lane);
+      if (perm_out) perm_out[pos] = (int32_t)(r + lane);
+    }
+  };
   if (ranks) {
-    scatter_group(rbeg, id0);
-    if (rbeg + 64 < rend) scatter_group(rbeg + 64, id1);
-    for (int64_t r = rbeg + 128; r < rend; r += 64) scatter_group(r, id_at(r));
+    if (span <= 128) {
+      // every row of the wave was ranked by the counting pass
+      place(rbeg, id0, rk0);
+      if (rbeg + 64 < rend) place(rbeg + 64, id1, rk1);
+    } else {
+      scatter_group(rbeg, id0);
+      if (rbeg + 64 < rend) scatter_group(rbeg + 64, id1);
+      for (int64_t r = rbeg + 128; r < rend; r += 64) scatter_group(r, id_at(r));
+    }
   }
 }
 
