@@ -32,6 +32,10 @@ namespace sla {
 #define SLA_CWI_GROUP 8
 #endif
 constexpr int kCwiGroup = SLA_CWI_GROUP;  // taps whose loads are in flight together
+#ifndef SLA_CWI_TILED
+#define SLA_CWI_TILED 1
+#endif
+constexpr bool kCwiTiled = SLA_CWI_TILED != 0;  // pillar grids: the LDS-tiled kernel
 
 __global__ __launch_bounds__(256) void k_cwi_clear(int32_t* __restrict__ map, int64_t cells,
                                                    int32_t* __restrict__ conflicts) {
@@ -206,6 +210,197 @@ hipError_t launch_cwi_build_map(const int32_t* coords, int32_t n, int32_t gx, in
   return hipGetLastError();
 }
 
+// ------------------------------------------------------ tiled (pillar grids)
+// On a grid one cell deep every tap stays in the plane, and a tile of cells
+// with its halo holds all the neighbours its voxels read.  k_cwi_tiled gives
+// each convolution branch tiles of its own shape: kTileLen x kTileWid cells
+// along the branch's axis (the halo lies along the axis only), kCubeTile^2 for
+// the 3 x 3 taps.  A workgroup reads the table entries of its tile and halo
+// once, then the 16-byte pieces of those voxels (a slab of at most 64 bytes of
+// the branch's channels) into LDS, with the slab's weights, and computes every
+// voxel of the tile from LDS: each neighbour piece crosses L2 about once
+// instead of once per tap.  Taps are added in the same order as in k_cwi_fwd.
+// Row workgroups copy the identity quarter of every row and write zero branch
+// outputs for rows the table does not hold (conflicts).
+constexpr int kTileLen = 64;
+constexpr int kTileWid = 4;
+constexpr int kCubeTile = 16;
+constexpr int kSlabPieces = 4;
+constexpr int kBandLoads = 8;   // band pieces per thread: (64 + 63 - 1) x 4 cells x 4 pieces <= 8 x 256
+
+struct TileGrid {
+  int32_t ax, ay;       // x-axis branch tiles along x and across
+  int32_t bx, by;       // y-axis branch tiles across x and along y
+  int32_t cx, cy;       // 3 x 3 tiles
+  int32_t sp, slabs;    // pieces per slab, slabs per branch row
+  int32_t n_x, n_y, n_c, n_r;  // workgroups per role
+  int32_t max_cells, max_taps; // LDS sizing
+};
+
+inline TileGrid cwi_tile_grid(int32_t n, int32_t gx, int32_t gy, int32_t pq, int32_t kx, int32_t ky) {
+  TileGrid t;
+  t.ax = (gx + kTileLen - 1) / kTileLen;
+  t.ay = (gy + kTileWid - 1) / kTileWid;
+  t.bx = (gx + kTileWid - 1) / kTileWid;
+  t.by = (gy + kTileLen - 1) / kTileLen;
+  t.cx = (gx + kCubeTile - 1) / kCubeTile;
+  t.cy = (gy + kCubeTile - 1) / kCubeTile;
+  t.sp = pq < kSlabPieces ? pq : kSlabPieces;
+  t.slabs = pq / t.sp;
+  t.n_x = t.ax * t.ay * t.slabs;
+  t.n_y = t.bx * t.by * t.slabs;
+  t.n_c = t.cx * t.cy * t.slabs;
+  t.n_r = (n + 256 / pq - 1) / (256 / pq);   // 256 / pq rows per workgroup, one identity piece per thread
+  t.max_cells = std::max(std::max((kTileLen + kx - 1) * kTileWid, kTileWid * (kTileLen + ky - 1)),
+                         (kCubeTile + 2) * (kCubeTile + 2));
+  t.max_taps = std::max(std::max(kx, ky), 9);
+  return t;
+}
+
+inline size_t cwi_tile_lds(const TileGrid& t) {
+  const size_t rows = ((size_t)t.max_cells * 4 + 15) / 16 * 16;
+  return rows + ((size_t)t.max_cells + t.max_taps) * t.sp * 16;
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_cwi_tiled(CwiArgs a, TileGrid tg, const T* __restrict__ x,
+                                                   const T* __restrict__ w_x,
+                                                   const T* __restrict__ w_y,
+                                                   const T* __restrict__ w_3, T* __restrict__ y) {
+  using P = CwiPiece<T>;
+  constexpr int E = P::kElems;
+  const int tid = (int)threadIdx.x;
+  const int C = 4 * a.c;
+  const int pq = a.pq;
+  int32_t b = (int32_t)blockIdx.x;
+  const int32_t n_tiles = tg.n_x + tg.n_y + tg.n_c;
+  if (b >= n_tiles) {
+    // row workgroup, one (row, identity piece) per thread: the identity quarter,
+    // and zero branch outputs for a row the table does not hold
+    const int32_t p = (b - n_tiles) * (256 / pq) + tid / pq;
+    const int j = tid % pq;
+    if (p >= a.n) return;
+    const uint4 v = reinterpret_cast<const uint4*>(x + (size_t)p * C)[3 * pq + j];
+    const int32_t cx = a.coords[3 * p], cy = a.coords[3 * p + 1], cz = a.coords[3 * p + 2];
+    const bool inside = (uint32_t)cx < (uint32_t)a.gx && (uint32_t)cy < (uint32_t)a.gy && cz == 0;
+    const int32_t owner = inside ? a.map[(int64_t)cy * a.gx + cx] : -1;
+    uint4* dst = reinterpret_cast<uint4*>(y + (size_t)p * C);
+    dst[3 * pq + j] = v;
+    if (owner != p) {
+      dst[j] = make_uint4(0, 0, 0, 0);
+      dst[pq + j] = make_uint4(0, 0, 0, 0);
+      dst[2 * pq + j] = make_uint4(0, 0, 0, 0);
+    }
+    return;
+  }
+  int role = 0;
+  if (b >= tg.n_x + tg.n_y) {
+    role = 2;
+    b -= tg.n_x + tg.n_y;
+  } else if (b >= tg.n_x) {
+    role = 1;
+    b -= tg.n_x;
+  }
+  const int32_t slab = b % tg.slabs, tile = b / tg.slabs;
+  int TX, TY, hx, hy, tpr;
+  if (role == 0) { TX = kTileLen; TY = kTileWid; hx = (a.kx - 1) / 2; hy = 0; tpr = tg.ax; }
+  else if (role == 1) { TX = kTileWid; TY = kTileLen; hx = 0; hy = (a.ky - 1) / 2; tpr = tg.bx; }
+  else { TX = kCubeTile; TY = kCubeTile; hx = 1; hy = 1; tpr = tg.cx; }
+  const int32_t X0 = (tile % tpr) * TX, Y0 = (tile / tpr) * TY;
+  const int BW = TX + 2 * hx, BH = TY + 2 * hy, cells = BW * BH;
+  const int sp = tg.sp;
+  extern __shared__ uint4 s_dyn[];
+  int32_t* s_row = reinterpret_cast<int32_t*>(s_dyn);
+  uint4* s_x = s_dyn + (tg.max_cells * 4 + 15) / 16;
+  uint4* s_w = s_x + (size_t)tg.max_cells * sp;
+  // 1. table entries of the tile and its halo (at most 2 x 256 cells).  Every
+  // load is issued unconditionally from a clamped cell and the result is
+  // discarded afterwards: a load under a divergent branch would be waited for
+  // before the other branch may write its register.
+  bool any = false;
+  {
+    int32_t rw[2];
+    bool ok[2];
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+      const int i = tid + 256 * k;
+      const int bxx = i % BW, byy = i / BW;
+      const int32_t gxx = X0 - hx + bxx, gyy = Y0 - hy + byy;
+      ok[k] = i < cells && (uint32_t)gxx < (uint32_t)a.gx && (uint32_t)gyy < (uint32_t)a.gy;
+      const int32_t sx = min(max(gxx, 0), a.gx - 1), sy = min(max(gyy, 0), a.gy - 1);
+      rw[k] = a.map[(int64_t)sy * a.gx + sx];
+    }
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+      const int i = tid + 256 * k;
+      const int bxx = i % BW, byy = i / BW;
+      const int32_t row = ok[k] && (uint32_t)rw[k] < (uint32_t)a.n ? rw[k] : -1;
+      if (i < cells) s_row[i] = row;
+      any |= row >= 0 && bxx >= hx && bxx < hx + TX && byy >= hy && byy < hy + TY;
+    }
+  }
+  // the slab's weights in visiting order (the mirrored taps for flip)
+  const int taps = role == 0 ? a.kx : (role == 1 ? a.ky : 9);
+  const T* w = role == 0 ? w_x : (role == 1 ? w_y : w_3);
+  for (int i = tid; i < taps * sp; i += 256) {
+    const int t = i / sp, j = i - t * sp;
+    int k = role == 2 ? 9 + t : t;
+    if (a.flip) k = (role == 2 ? 26 : taps - 1) - k;
+    s_w[i] = *reinterpret_cast<const uint4*>(w + (size_t)k * a.c + (slab * sp + j) * E);
+  }
+  if (!__syncthreads_or(any)) return;
+  // 2. the slab's pieces of every voxel of the tile and its halo: a thread's
+  // pieces are all requested, then stored
+  const int col0 = role * a.c + slab * sp * E;
+  {
+    // as in step 1: loads of absent cells read row 0 (n > 0) and are dropped
+    const int nk = (cells * sp + 255) / 256;   // the same for the whole workgroup
+    int32_t rr[kBandLoads];
+#pragma unroll
+    for (int k = 0; k < kBandLoads; ++k) {
+      const int i = tid + 256 * k;
+      rr[k] = k < nk && i < cells * sp ? s_row[i / sp] : -1;
+    }
+    uint4 v[kBandLoads];
+#pragma unroll
+    for (int k = 0; k < kBandLoads; ++k) {
+      if (k >= nk) break;
+      const int i = tid + 256 * k;
+      const int j = i % sp;
+      v[k] = *reinterpret_cast<const uint4*>(x + (size_t)max(rr[k], 0) * C + col0 + j * E);
+    }
+#pragma unroll
+    for (int k = 0; k < kBandLoads; ++k) {
+      if (k >= nk) break;
+      const int i = tid + 256 * k;
+      if (i < cells * sp) s_x[i] = rr[k] >= 0 ? v[k] : make_uint4(0, 0, 0, 0);
+    }
+  }
+  __syncthreads();
+  // 3. the tile's voxels
+  for (int i = tid; i < TX * TY * sp; i += 256) {
+    const int u = i / sp, j = i - u * sp;
+    const int ux = u % TX, uy = u / TX;
+    const int cell = (uy + hy) * BW + ux + hx;
+    const int32_t row = s_row[cell];
+    if (row < 0) continue;
+    float acc[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) acc[e] = 0.f;
+    if (role == 2) {
+#pragma unroll
+      for (int t = 0; t < 9; ++t)  // kernel taps 9 .. 17: dx = t % 3 - 1, dy = t / 3 - 1
+        P::add(acc, s_x[(cell + (t / 3 - 1) * BW + t % 3 - 1) * sp + j], s_w[t * sp + j]);
+    } else {
+      const int step = role == 0 ? 1 : BW;
+      const int half = role == 0 ? hx : hy;
+      const int c0 = cell - half * step;
+      for (int t = 0; t < taps; ++t) P::add(acc, s_x[(c0 + t * step) * sp + j], s_w[t * sp + j]);
+    }
+    *reinterpret_cast<uint4*>(y + (size_t)row * C + col0 + j * E) = P::pack(acc);
+  }
+}
+
 // dtype: 0 f32, 1 f16, 2 bf16; flip: every kernel reversed
 static hipError_t cwi_forward_launch(const int32_t* map, int32_t gx, int32_t gy, int32_t gz,
                                      const int32_t* coords, int32_t n, const int32_t* order,
@@ -228,6 +423,27 @@ static hipError_t cwi_forward_launch(const int32_t* map, int32_t gx, int32_t gy,
   a.flip = flip;
   const int rows_per = 64 / a.pq;
   a.groups = (n + rows_per - 1) / rows_per;
+  if (gz == 1 && kCwiTiled) {
+    const TileGrid tg = cwi_tile_grid(n, gx, gy, a.pq, kx, ky);
+    const unsigned tgrid = (unsigned)(tg.n_x + tg.n_y + tg.n_c + tg.n_r);
+    const size_t lds = cwi_tile_lds(tg);
+    if (dtype == 0)
+      hipLaunchKernelGGL((k_cwi_tiled<float>), dim3(tgrid), dim3(256), lds, stream, a, tg,
+                         static_cast<const float*>(x), static_cast<const float*>(w_x),
+                         static_cast<const float*>(w_y), static_cast<const float*>(w_3),
+                         static_cast<float*>(y));
+    else if (dtype == 1)
+      hipLaunchKernelGGL((k_cwi_tiled<_Float16>), dim3(tgrid), dim3(256), lds, stream, a, tg,
+                         static_cast<const _Float16*>(x), static_cast<const _Float16*>(w_x),
+                         static_cast<const _Float16*>(w_y), static_cast<const _Float16*>(w_3),
+                         static_cast<_Float16*>(y));
+    else
+      hipLaunchKernelGGL((k_cwi_tiled<bf16_t>), dim3(tgrid), dim3(256), lds, stream, a, tg,
+                         static_cast<const bf16_t*>(x), static_cast<const bf16_t*>(w_x),
+                         static_cast<const bf16_t*>(w_y), static_cast<const bf16_t*>(w_3),
+                         static_cast<bf16_t*>(y));
+    return hipGetLastError();
+  }
   const unsigned grid = (unsigned)(((int64_t)a.groups + 7) / 8 * 8);
   if (dtype == 0)
     hipLaunchKernelGGL((k_cwi_fwd<float>), dim3(grid), dim3(256), 0, stream, a,

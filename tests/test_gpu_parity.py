@@ -733,3 +733,47 @@ def test_cwi_backward_small_and_empty(sla):
         w_x, w_y, w_3 = (workloads.cast_values(rng.standard_normal((k, 16)).astype(np.float32), "f16")
                          for k in (7, 3, 27))
         cwi_backward_parity(sla, coords.reshape(n, 3), (6, 5, 2), x, w_x, w_y, w_3, dy, "f16", label=f"n{n}")
+
+
+@pytest.mark.parametrize("dtype,C,kx,ky", [("f16", 128, 13, 13), ("bf16", 64, 5, 31), ("f32", 64, 1, 63),
+                                           ("f16", 512, 13, 3), ("f16", 32, 13, 13), ("f32", 16, 3, 3)])
+def test_cwi_tiled_matches_gather(sla, dtype, C, kx, ky):
+    # A pillar scene (one cell deep) takes the LDS-tiled kernel; the same scene in
+    # a grid two cells deep takes the gather kernel, whose extra 3 x 3 x 3 taps all
+    # land on empty cells.  Both add the same taps in the same order, so forward,
+    # dx and the kernel gradients agree bit for bit.  Occupancy: a dense block,
+    # random cells elsewhere, the grid's border rows and columns.
+    import torch
+
+    rng = np.random.default_rng([66, C, kx, ky, len(dtype)])
+    gx, gy = 150, 97
+    occ = rng.random((gy, gx)) < 0.35
+    occ[20:60, 30:90] = True
+    occ[0, :] |= rng.random(gx) < 0.7
+    occ[:, gx - 1] |= rng.random(gy) < 0.7
+    yy, xx = np.nonzero(occ)
+    perm = rng.permutation(yy.size)
+    coords = np.stack([xx, yy, np.zeros_like(xx)], axis=1)[perm].astype(np.int32)
+    n, c = coords.shape[0], C // 4
+    cast = lambda a: workloads.cast_values(a.astype(np.float32), dtype)  # noqa: E731
+    x, dy = cast(rng.standard_normal((n, C))), cast(rng.standard_normal((n, C)))
+    w_x, w_y, w_3 = (cast(rng.standard_normal((k, c)) / np.sqrt(k)) for k in (kx, ky, 27))
+    dev = lambda a: to_dev(a, dtype)  # noqa: E731
+    cc = torch.from_numpy(coords).cuda()
+    outs = []
+    for grid in ((gx, gy, 1), (gx, gy, 2)):
+        m, conflicts = sla.cwi_build_map(cc, grid)
+        y = sla.cwi_forward(m, grid, cc, dev(x), dev(w_x), dev(w_y), dev(w_3))
+        back = sla.cwi_backward(m, grid, cc, dev(x), dev(w_x), dev(w_y), dev(w_3), dev(dy))
+        torch.cuda.synchronize()
+        assert int(conflicts.cpu()[0]) == 0
+        outs.append([to_host64(t, dtype) for t in (y, *back)])
+    names = ("y", "dx", "dw_x", "dw_y", "dw_3")
+    for name, a, b in zip(names, *outs):
+        assert np.array_equal(a, b), f"{name}: tiled and gather paths differ"
+    # and the pair against the oracle, forward and dx
+    w = lambda a: oracle.widen(a, dtype)  # noqa: E731
+    ref = oracle.cwi_forward_ref(coords, w(x), w(w_x), w(w_y), w(w_3), (gx, gy, 1))
+    err = rel_err_per_head(outs[0][0].reshape(n, 4, c), ref.reshape(n, 4, c), 1e-3 * float(np.abs(ref).max()))
+    _say(f"[cwi-tiled] n={n} C={C} taps=({kx},{ky}) {dtype} rel_err={err:.3e}")
+    assert err <= TOL[dtype]
