@@ -250,9 +250,12 @@ sla_status_t sla_forward_projected(const void* plan, size_t plan_bytes, int64_t 
  * bytes and 64 divisible by c * (element size) / 16 (fp16/bf16: channels 32 x 2^k
  * up to 2048; fp32: 16 x 2^k up to 1024); taps odd, 1..63; else
  * SLA_E_UNSUPPORTED.  `order` (int32
- * [n], may be NULL = 0..n-1) is the order in which rows are visited, e.g. the
- * SLA plan's permutation: rows of one window together keep the neighbours in
- * cache.  x, y and the weights 16-byte aligned.
+ * [n], may be NULL = 0..n-1) is the order in which rows are visited on grids
+ * more than one cell deep, e.g. the SLA plan's permutation: rows of one window
+ * together keep the neighbours in cache.  Pillar grids (gz = 1) are processed
+ * in tiles of cells and ignore it; there a row the table does not hold gets
+ * zero branch outputs.  Results do not depend on `order`.  x, y and the
+ * weights 16-byte aligned.
  */
 size_t sla_cwi_map_bytes(int32_t gx, int32_t gy, int32_t gz);
 
