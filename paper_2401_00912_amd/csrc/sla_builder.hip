@@ -16,6 +16,8 @@
 //              chunk table and the header.
 // Mode B (CSR offsets given) and n = 0: one workgroup, k_plan, validates the
 // offsets and writes the chunk table and header.
+#include <atomic>
+
 #include "sla_common.h"
 
 namespace sla {
@@ -576,15 +578,16 @@ hipError_t launch_build(const int32_t* ids, int32_t n, int32_t W, int32_t L, int
   int overlap = 0;
   const int nws = scatter_waves(W, lay.block_elems, &lds, &overlap);
   // the dynamic LDS of k_scatter exceeds the default limit: raise it once per device
-  static bool lds_attr[64] = {};
+  // (atomic: host threads may build plans concurrently; setting it twice is harmless)
+  static std::atomic<bool> lds_attr[64] = {};
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return e;
-  if (dev < 0 || dev >= 64 || !lds_attr[dev]) {
+  if (dev < 0 || dev >= 64 || !lds_attr[dev].load(std::memory_order_acquire)) {
     e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_scatter),
                             hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024 - 1024);
     if (e != hipSuccess) return e;
-    if (dev >= 0 && dev < 64) lds_attr[dev] = true;
+    if (dev >= 0 && dev < 64) lds_attr[dev].store(true, std::memory_order_release);
   }
   hipLaunchKernelGGL(k_scatter, dim3(lay.n_blocks + 1), dim3(kBuildThreads), lds, stream, ids, n, W, L,
                      lay.block_elems, lay.n_blocks, lay.counts_ld, nws, overlap, counts, perm, perm_out,

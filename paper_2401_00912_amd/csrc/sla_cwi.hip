@@ -237,6 +237,16 @@ struct TileGrid {
   int32_t max_cells, max_taps; // LDS sizing
 };
 
+// Workgroups of the tiled launch, in 64 bits: a grid whose tiles do not fit one
+// launch (a degenerate shape such as 1 x 2^31 cells) takes the gather kernel.
+inline int64_t cwi_tile_workgroups(int32_t n, int32_t gx, int32_t gy, int32_t pq) {
+  const int64_t slabs = pq / (pq < kSlabPieces ? pq : kSlabPieces);
+  const int64_t ax = (gx + kTileLen - 1) / kTileLen, ay = (gy + kTileWid - 1) / kTileWid;
+  const int64_t bx = (gx + kTileWid - 1) / kTileWid, by = (gy + kTileLen - 1) / kTileLen;
+  const int64_t cx = (gx + kCubeTile - 1) / kCubeTile, cy = (gy + kCubeTile - 1) / kCubeTile;
+  return (ax * ay + bx * by + cx * cy) * slabs + (n + 256 / pq - 1) / (256 / pq);
+}
+
 inline TileGrid cwi_tile_grid(int32_t n, int32_t gx, int32_t gy, int32_t pq, int32_t kx, int32_t ky) {
   TileGrid t;
   t.ax = (gx + kTileLen - 1) / kTileLen;
@@ -423,7 +433,7 @@ static hipError_t cwi_forward_launch(const int32_t* map, int32_t gx, int32_t gy,
   a.flip = flip;
   const int rows_per = 64 / a.pq;
   a.groups = (n + rows_per - 1) / rows_per;
-  if (gz == 1 && kCwiTiled) {
+  if (gz == 1 && kCwiTiled && cwi_tile_workgroups(n, gx, gy, a.pq) <= INT32_MAX) {
     const TileGrid tg = cwi_tile_grid(n, gx, gy, a.pq, kx, ky);
     const unsigned tgrid = (unsigned)(tg.n_x + tg.n_y + tg.n_c + tg.n_r);
     const size_t lds = cwi_tile_lds(tg);

@@ -356,9 +356,9 @@ def cwi_build_map(coords, grid, map=None):
     return map, conflicts
 
 
-def cwi_forward(map, grid, coords, x, w_x, w_y, w_3, order=None, y=None):
-    """Cross-window interaction (sla_cwi_forward): x [n, 4c], w_x [K_x, c], w_y
-    [K_y, c], w_3 [27, c]; order an int32 [n] visiting order or None."""
+def _cwi_check(map, grid, coords, x, w_x, w_y, w_3, order, **like_x):
+    """Shapes, dtypes, devices and layouts of a cross-window interaction call (the
+    C entry points take the cell table without its size, so it is checked here)."""
     torch = _torch()
     gx, gy, gz = (int(g) for g in grid)
     if x.dim() != 2 or not x.is_contiguous():
@@ -367,12 +367,30 @@ def cwi_forward(map, grid, coords, x, w_x, w_y, w_3, order=None, y=None):
     c = C // 4
     for name, t, rows in (("w_x", w_x, None), ("w_y", w_y, None), ("w_3", w_3, 27)):
         if t.dim() != 2 or t.shape[1] != c or (rows and t.shape[0] != rows) or t.dtype != x.dtype \
-                or not t.is_contiguous():
+                or not t.is_contiguous() or t.device != x.device:
             raise ValueError(f"{name} must be a contiguous [taps, {c}] tensor like x")
-    if coords.shape != (n, 3) or coords.dtype != torch.int32:
-        raise ValueError("coords must be int32 [n, 3]")
-    if order is not None and (order.numel() < n or order.dtype != torch.int32):
-        raise ValueError("order must be int32 [n]")
+    if coords.shape != (n, 3) or coords.dtype != torch.int32 or not coords.is_contiguous() \
+            or coords.device != x.device:
+        raise ValueError("coords must be a contiguous int32 [n, 3] tensor on x's device")
+    need = cwi_map_bytes(gx, gy, gz)
+    if need == 0 or map.dtype != torch.int32 or map.numel() * 4 < need or not map.is_contiguous() \
+            or map.device != x.device:
+        raise ValueError("map must be the int32 cell table of this grid (cwi_build_map)")
+    if order is not None and (order.shape != (n,) or order.dtype != torch.int32 or not order.is_contiguous()
+                              or order.device != x.device):
+        raise ValueError("order must be a contiguous int32 [n] tensor on x's device")
+    for name, t in like_x.items():
+        if t is not None and (t.shape != x.shape or t.dtype != x.dtype or not t.is_contiguous()
+                              or t.device != x.device):
+            raise ValueError(f"{name} must be a contiguous tensor like x")
+    return gx, gy, gz, n, C
+
+
+def cwi_forward(map, grid, coords, x, w_x, w_y, w_3, order=None, y=None):
+    """Cross-window interaction (sla_cwi_forward): x [n, 4c], w_x [K_x, c], w_y
+    [K_y, c], w_3 [27, c]; order an int32 [n] visiting order or None."""
+    torch = _torch()
+    gx, gy, gz, n, C = _cwi_check(map, grid, coords, x, w_x, w_y, w_3, order, y=y)
     y = torch.empty_like(x) if y is None else y
     st = lib().sla_cwi_forward(_ptr(map), gx, gy, gz, _ptr(coords), n, _ptr(order), _dtype_code(x.dtype), C,
                                int(w_x.shape[0]), int(w_y.shape[0]), _ptr(x), _ptr(w_x), _ptr(w_y), _ptr(w_3),
@@ -391,10 +409,7 @@ def cwi_backward(map, grid, coords, x, w_x, w_y, w_3, dy, order=None, workspace=
     """Backward of cwi_forward (sla_cwi_backward): returns (dx, dw_x, dw_y, dw_3),
     written into `out` when given (tensors shaped like x, w_x, w_y, w_3)."""
     torch = _torch()
-    gx, gy, gz = (int(g) for g in grid)
-    n, C = x.shape
-    if dy.shape != x.shape or dy.dtype != x.dtype or not dy.is_contiguous():
-        raise ValueError("dy must be a contiguous tensor like x")
+    gx, gy, gz, n, C = _cwi_check(map, grid, coords, x, w_x, w_y, w_3, order, dy=dy)
     code = _dtype_code(x.dtype)
     need = cwi_backward_workspace_bytes(n, x.dtype, C, w_x.shape[0], w_y.shape[0])
     if need == 0:

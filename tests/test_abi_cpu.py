@@ -228,3 +228,31 @@ def test_cwi_backward_argument_errors(L):
     assert bw(ws=None) == sla.SLA_E_ARG
     assert bw(dx=None) == sla.SLA_E_ARG
     assert bw(C=96) == sla.SLA_E_UNSUPPORTED
+
+
+def test_cwi_binding_rejects_bad_tensors(L):
+    # the binding's checks run before the C call (CPU tensors never reach it)
+    import torch
+
+    n, c = 10, 8
+    grid = (8, 8, 1)
+    coords = torch.zeros((n, 3), dtype=torch.int32)
+    x = torch.zeros((n, 4 * c), dtype=torch.float16)
+    w = [torch.zeros((k, c), dtype=torch.float16) for k in (5, 3, 27)]
+    good_map = torch.zeros(64, dtype=torch.int32)
+    with pytest.raises(ValueError, match="map"):
+        sla.cwi_forward(torch.zeros(63, dtype=torch.int32), grid, coords, x, *w)   # one cell short
+    with pytest.raises(ValueError, match="map"):
+        sla.cwi_forward(good_map.float(), grid, coords, x, *w)
+    with pytest.raises(ValueError, match="y must"):
+        sla.cwi_forward(good_map, grid, coords, x, *w, y=torch.zeros((n, 4 * c + 8), dtype=torch.float16))
+    with pytest.raises(ValueError, match="order"):
+        sla.cwi_forward(good_map, grid, coords, x, *w, order=torch.zeros(n - 1, dtype=torch.int32))
+    with pytest.raises(ValueError, match="coords"):
+        sla.cwi_forward(good_map, grid, coords.t(), x, *w)
+    with pytest.raises(ValueError, match="w_3"):
+        sla.cwi_forward(good_map, grid, coords, x, w[0], w[1], torch.zeros((9, c), dtype=torch.float16))
+    with pytest.raises(ValueError, match="dy must"):
+        sla.cwi_backward(good_map, grid, coords, x, *w, x.float())
+    with pytest.raises(ValueError, match="map"):
+        sla.cwi_backward(torch.zeros(10, dtype=torch.int32), grid, coords, x, *w, x)
