@@ -571,9 +571,8 @@ __global__ __launch_bounds__(256) void k_cwi_dw(CwiArgs a, DwGrid g, const T* __
     const int32_t lcx = lok ? a.coords[3 * lrow] : 0, lcy = lok ? a.coords[3 * lrow + 1] : 0,
                   lcz = lok ? a.coords[3 * lrow + 2] : 0;
     const int cnt = min(64, r1 - c0);
-    for (int q0 = 0; q0 < cnt; q0 += kDwBatch) {
-      int32_t nb[kDwBatch];
-      uint4 dv[kDwBatch];
+    // table entries of the neighbours of rows q0 .. q0 + kDwBatch - 1 (-1: none)
+    auto entries = [&](int q0, int32_t (&nb)[kDwBatch]) {
 #pragma unroll
       for (int u = 0; u < kDwBatch; ++u) {
         const int32_t row = __builtin_amdgcn_readlane(lrow, q0 + u);  // -1 past the range
@@ -583,15 +582,32 @@ __global__ __launch_bounds__(256) void k_cwi_dw(CwiArgs a, DwGrid g, const T* __
         const bool in = valid && (uint32_t)row < (uint32_t)a.n && (uint32_t)nx < (uint32_t)a.gx &&
                         (uint32_t)ny < (uint32_t)a.gy && (uint32_t)nz < (uint32_t)a.gz;
         nb[u] = in ? a.map[((int64_t)nz * a.gy + ny) * a.gx + nx] : -1;
-        dv[u] = in ? *reinterpret_cast<const uint4*>(dy + (size_t)row * C + col) : make_uint4(0, 0, 0, 0);
       }
-      uint4 xv[kDwBatch];
+    };
+    // software pipeline: a batch's neighbour and dy pieces are requested with
+    // the next batch's table entries, so each batch waits one round trip
+    int32_t nb[kDwBatch];
+    entries(0, nb);
+    for (int q0 = 0; q0 < cnt; q0 += kDwBatch) {
+      uint4 xv[kDwBatch], dv[kDwBatch];
 #pragma unroll
-      for (int u = 0; u < kDwBatch; ++u)
-        xv[u] = (uint32_t)nb[u] < (uint32_t)a.n ? *reinterpret_cast<const uint4*>(x + (size_t)nb[u] * C + col)
-                                                 : make_uint4(0, 0, 0, 0);
+      for (int u = 0; u < kDwBatch; ++u) {
+        const bool hit = (uint32_t)nb[u] < (uint32_t)a.n;
+        const int32_t row = __builtin_amdgcn_readlane(lrow, q0 + u);
+        xv[u] = hit ? *reinterpret_cast<const uint4*>(x + (size_t)nb[u] * C + col) : make_uint4(0, 0, 0, 0);
+        dv[u] = hit ? *reinterpret_cast<const uint4*>(dy + (size_t)row * C + col) : make_uint4(0, 0, 0, 0);
+      }
+      int32_t nn[kDwBatch];
+      if (q0 + kDwBatch < cnt) {
+        entries(q0 + kDwBatch, nn);
+      } else {
+#pragma unroll
+        for (int u = 0; u < kDwBatch; ++u) nn[u] = -1;
+      }
 #pragma unroll
       for (int u = 0; u < kDwBatch; ++u) P::add(acc, xv[u], dv[u]);  // += dy[row] * x[neighbour]
+#pragma unroll
+      for (int u = 0; u < kDwBatch; ++u) nb[u] = nn[u];
     }
   }
 #pragma unroll
