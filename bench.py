@@ -63,6 +63,9 @@ def parse():
     p.add_argument("--pmc-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                    help="no GPU work: summarise two rocprofv3 --pmc counter_collection.csv files "
                         "(FETCH_SIZE run, WRITE_SIZE run) of `bench.py --no-graph --copy-probe`")
+    p.add_argument("--sq-summary", nargs="+", metavar="CSV",
+                   help="no GPU work: summarise rocprofv3 --pmc counter_collection.csv files of SQ "
+                        "counters (`bench.py --no-graph` runs): MFMA and VALU busy, LDS bank conflicts")
     return p.parse_args()
 
 
@@ -133,6 +136,61 @@ def pmc_summary(fetch_csv, write_csv):
     return "\n".join(lines)
 
 
+MI355X_CUS, MI355X_SIMDS, MI355X_XCDS = 256, 1024, 8
+
+
+def sq_summary(paths):
+    """Per-launch SQ counters of every kernel of the step (mean over dispatches)
+    and the derived figures rocprofv3 defines for gfx950: MfmaUtil = MFMA-busy
+    cycles / (GPU-active cycles x SIMDs), VALUBusy = VALU-active cycles / CUs /
+    GPU-active cycles, LDS bank-conflict ratio = conflict cycles / (LDS-active -
+    conflict cycles).  The counter file sums GRBM_GUI_ACTIVE over the 8 XCDs
+    while those definitions take its per-XCD maximum, so the sum is divided by 8.
+    One F16 MFMA "MOP" is 512 flops; TFLOP/s is over the dispatch's own duration
+    (its start and end timestamps)."""
+    import csv
+
+    acc, dur = {}, {}
+    for path in paths:
+        seen = set()
+        with open(path) as fh:
+            for r in csv.DictReader(fh):
+                k = short_kernel(r["Kernel_Name"])
+                if k is None or k == "copy":
+                    continue
+                acc.setdefault(k, {}).setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+                if r["Dispatch_Id"] not in seen:
+                    seen.add(r["Dispatch_Id"])
+                    dur.setdefault(k, []).append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-9)
+    lines = ["kernel      counter                          per_launch        dispatches"]
+    for k in ("k_count", "k_scatter", "k_sla_fwd", "k_sla_bwd"):
+        if k not in acc:
+            continue
+        c = {name: float(np.mean(v)) for name, v in acc[k].items()}
+        for name in sorted(c):
+            lines.append(f"{k:<11} {name:<32} {c[name]:>16.0f}  {len(acc[k][name]):>10}")
+        t = float(np.median(dur[k]))
+        lines.append(f"{k:<11} derived dispatch_us_median        {t * 1e6:>16.2f}")
+        g = c.get("GRBM_GUI_ACTIVE")
+        if g:
+            g /= MI355X_XCDS
+            if "SQ_VALU_MFMA_BUSY_CYCLES" in c:
+                lines.append(f"{k:<11} derived MfmaUtil_percent          "
+                             f"{100 * c['SQ_VALU_MFMA_BUSY_CYCLES'] / (g * MI355X_SIMDS):>16.2f}")
+            if "SQ_ACTIVE_INST_VALU" in c:
+                lines.append(f"{k:<11} derived VALUBusy_percent          "
+                             f"{100 * c['SQ_ACTIVE_INST_VALU'] / MI355X_CUS / g:>16.2f}")
+        if "SQ_LDS_BANK_CONFLICT" in c and "SQ_LDS_IDX_ACTIVE" in c:
+            den = c["SQ_LDS_IDX_ACTIVE"] - c["SQ_LDS_BANK_CONFLICT"]
+            if den > 0:
+                lines.append(f"{k:<11} derived LdsBankConflict_ratio     {c['SQ_LDS_BANK_CONFLICT'] / den:>16.4f}")
+        if "SQ_INSTS_VALU_MFMA_MOPS_F16" in c:
+            fl = 512 * c["SQ_INSTS_VALU_MFMA_MOPS_F16"]
+            lines.append(f"{k:<11} derived MFMA_F16_flops            {fl:>16.0f}")
+            lines.append(f"{k:<11} derived MFMA_F16_TFLOPs           {fl / t / 1e12:>16.1f}")
+    return "\n".join(lines)
+
+
 def stored_traffic(kernel):
     """Scaled HBM bytes per launch of `kernel` from the committed counter summary,
     or None when there is none or the kernel source changed since it was taken."""
@@ -155,6 +213,9 @@ def main():
     args = parse()
     if args.pmc_summary:
         print(pmc_summary(*args.pmc_summary))
+        return
+    if args.sq_summary:
+        print(sq_summary(args.sq_summary))
         return
     if args.gpus != 1:
         print(f"bench.py: this build measures one GPU only (asked for --gpus {args.gpus}); "
