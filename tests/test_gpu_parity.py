@@ -777,3 +777,23 @@ def test_cwi_tiled_matches_gather(sla, dtype, C, kx, ky):
     err = rel_err_per_head(outs[0][0].reshape(n, 4, c), ref.reshape(n, 4, c), 1e-3 * float(np.abs(ref).max()))
     _say(f"[cwi-tiled] n={n} C={C} taps=({kx},{ky}) {dtype} rel_err={err:.3e}")
     assert err <= TOL[dtype]
+
+
+@pytest.mark.parametrize("grid,density", [((1, 1, 1), 1.0), ((3, 70, 1), 0.5), ((70, 3, 1), 0.5),
+                                          ((65, 5, 1), 1.0), ((17, 17, 1), 0.2)])
+def test_cwi_tiled_edges(sla, grid, density):
+    # pillar grids smaller than a tile or its halo along one axis, partial tiles,
+    # a full grid and a lone voxel: forward and backward against the oracle
+    rng = np.random.default_rng([67, grid[0], grid[1]])
+    gx, gy, _ = grid
+    occ = rng.random((gy, gx)) < density
+    occ.flat[rng.integers(occ.size)] = True          # at least one voxel
+    yy, xx = np.nonzero(occ)
+    coords = np.stack([xx, yy, np.zeros_like(xx)], axis=1)[rng.permutation(yy.size)].astype(np.int32)
+    n, C = coords.shape[0], 64
+    c = C // 4
+    cast = lambda a: workloads.cast_values(a.astype(np.float32), "f16")  # noqa: E731
+    x, dy = cast(rng.standard_normal((n, C))), cast(rng.standard_normal((n, C)))
+    w_x, w_y, w_3 = (cast(rng.standard_normal((k, c)) / np.sqrt(k)) for k in (13, 13, 27))
+    cwi_parity(sla, coords, grid, x, w_x, w_y, w_3, "f16", label=f"edge{grid}")
+    cwi_backward_parity(sla, coords, grid, x, w_x, w_y, w_3, dy, "f16", label=f"edge{grid}")
