@@ -222,11 +222,25 @@ hipError_t launch_cwi_build_map(const int32_t* coords, int32_t n, int32_t gx, in
 // instead of once per tap.  Taps are added in the same order as in k_cwi_fwd.
 // Row workgroups copy the identity quarter of every row and write zero branch
 // outputs for rows the table does not hold (conflicts).
-constexpr int kTileLen = 64;
-constexpr int kTileWid = 4;
-constexpr int kCubeTile = 16;
+#ifndef SLA_CWI_TILE_LEN
+#define SLA_CWI_TILE_LEN 64
+#endif
+#ifndef SLA_CWI_TILE_WID
+#define SLA_CWI_TILE_WID 4
+#endif
+#ifndef SLA_CWI_CUBE_TILE
+#define SLA_CWI_CUBE_TILE 16
+#endif
+constexpr int kTileLen = SLA_CWI_TILE_LEN;
+constexpr int kTileWid = SLA_CWI_TILE_WID;
+constexpr int kCubeTile = SLA_CWI_CUBE_TILE;
 constexpr int kSlabPieces = 4;
-constexpr int kBandLoads = 8;   // band pieces per thread: (64 + 63 - 1) x 4 cells x 4 pieces <= 8 x 256
+// cells of the largest band (63 taps) and (cell, piece) loads per thread
+constexpr int kMaxBand = (kTileLen + 62) * kTileWid > (kCubeTile + 2) * (kCubeTile + 2)
+                             ? (kTileLen + 62) * kTileWid
+                             : (kCubeTile + 2) * (kCubeTile + 2);
+constexpr int kMapLoads = (kMaxBand + 255) / 256;
+constexpr int kBandLoads = (kMaxBand * kSlabPieces + 255) / 256;
 
 struct TileGrid {
   int32_t ax, ay;       // x-axis branch tiles along x and across
@@ -323,16 +337,16 @@ __global__ __launch_bounds__(256) void k_cwi_tiled(CwiArgs a, TileGrid tg, const
   int32_t* s_row = reinterpret_cast<int32_t*>(s_dyn);
   uint4* s_x = s_dyn + (tg.max_cells * 4 + 15) / 16;
   uint4* s_w = s_x + (size_t)tg.max_cells * sp;
-  // 1. table entries of the tile and its halo (at most 2 x 256 cells).  Every
+  // 1. table entries of the tile and its halo (at most kMapLoads x 256 cells).  Every
   // load is issued unconditionally from a clamped cell and the result is
   // discarded afterwards: a load under a divergent branch would be waited for
   // before the other branch may write its register.
   bool any = false;
   {
-    int32_t rw[2];
-    bool ok[2];
+    int32_t rw[kMapLoads];
+    bool ok[kMapLoads];
 #pragma unroll
-    for (int k = 0; k < 2; ++k) {
+    for (int k = 0; k < kMapLoads; ++k) {
       const int i = tid + 256 * k;
       const int bxx = i % BW, byy = i / BW;
       const int32_t gxx = X0 - hx + bxx, gyy = Y0 - hy + byy;
@@ -341,7 +355,7 @@ __global__ __launch_bounds__(256) void k_cwi_tiled(CwiArgs a, TileGrid tg, const
       rw[k] = a.map[(int64_t)sy * a.gx + sx];
     }
 #pragma unroll
-    for (int k = 0; k < 2; ++k) {
+    for (int k = 0; k < kMapLoads; ++k) {
       const int i = tid + 256 * k;
       const int bxx = i % BW, byy = i / BW;
       const int32_t row = ok[k] && (uint32_t)rw[k] < (uint32_t)a.n ? rw[k] : -1;
