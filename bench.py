@@ -609,7 +609,7 @@ def bench_projected(torch, sla, workloads, dev, args):
     graph replay over rotated buffer sets."""
     import torch.nn.functional as Fn
 
-    cfg = args.config if args.config in (2, 3) else 2
+    cfg = args.config if args.config in (2, 3, 4) else 2
     base = workloads.make_config(cfg, with_grad=False)
     n, H, d, W, dt = base["n"], base["heads"], base["head_dim"], base["num_windows"], base["dtype"]
     C = H * d

@@ -210,7 +210,7 @@ sla_status_t sla_backward_ex(const void* plan, size_t plan_bytes, int64_t n, int
  *   b_qkv  [3C] or NULL (no bias);  w_o [C, C];  b_o [C] or NULL;
  *   o      [n, C] output: SLA's output before the output projection;
  *   y      [n, C] output.
- * All in `dtype`, which must be SLA_F16 or SLA_BF16; C must be 64 or 128
+ * All in `dtype`, which must be SLA_F16 or SLA_BF16; C must be 64, 128 or 256
  * (else SLA_E_UNSUPPORTED).  x, w_qkv, w_o, o, y 16-byte aligned.  Rows in no
  * window get neither o nor y.  The projections run on the matrix cores with
  * fp32 accumulation; q, k, v are rounded to `dtype` (as if stored) before the

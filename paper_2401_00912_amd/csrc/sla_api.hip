@@ -217,7 +217,7 @@ SLA_EXPORT sla_status_t sla_forward_projected(const void* plan, size_t plan_byte
   if (!variant_ok((int)feature_map, eps)) return SLA_E_ARG;
   if (dtype != SLA_F16 && dtype != SLA_BF16) return SLA_E_UNSUPPORTED;
   const int64_t C = (int64_t)heads * head_dim;
-  if (C != 64 && C != 128) return SLA_E_UNSUPPORTED;
+  if (C != 64 && C != 128 && C != 256) return SLA_E_UNSUPPORTED;
   if (n == 0) return SLA_OK;
   if (!x || !w_qkv || !w_o || !o || !y) return SLA_E_ARG;
   if (!aligned(x, 16) || !aligned(w_qkv, 16) || !aligned(w_o, 16) || !aligned(o, 16) ||

@@ -24,7 +24,11 @@ namespace sla {
 //   chunk items  (four chunks, head): one chunk per wave.
 // The output o ([n, C], original row order) then goes through the output
 // projection, k_out_proj.
-constexpr int kProjMaxC = 128;
+constexpr int kProjMaxC = 256;
+// Above this many 32-channel blocks (C > 128) a block's features are fetched and
+// projected one 32-row job at a time, so that at most one job's features are
+// live (64 VGPRs for C = 256, as both jobs' for C = 128).
+constexpr int kProjBlockFetchMaxCB = 4;
 
 struct ProjArgs {
   const void* x;  // [n, C] features
@@ -159,6 +163,26 @@ __device__ __forceinline__ void project_job(Slice<T, Geo<D>::KS, 3>& sj, const R
   }
 }
 
+// One job's features (rows from the block's permutation entries).
+template <typename T, int CB>
+__device__ __forceinline__ void xjob_fetch(Raw<T, 8> (&xj)[2][CB], int32_t (&o)[2], bool (&ok)[2],
+                                           const BlockRows& br, int jj, int32_t base, int32_t end,
+                                           int32_t n, const T* x, int g) {
+  constexpr int C = 32 * CB;
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+    ok[s] = (uint32_t)br.o[jj][s] < (uint32_t)n;
+    o[s] = ok[s] ? br.o[jj][s] : 0;
+    const bool live = base + kSliceRows * jj + 16 * s < end;
+    const T* row = row_at(x, o[s], (size_t)C, 8 * g);
+#pragma unroll
+    for (int kb = 0; kb < CB; ++kb) {
+      if (live) xj[s][kb] = __builtin_bit_cast(Raw<T, 8>, *reinterpret_cast<const uint4*>(row + 32 * kb));
+      else xj[s][kb] = Frag<T, 8>::zero();
+    }
+  }
+}
+
 // All jobs of a block, job by job (a job's features are dead once its fragments
 // exist).
 template <typename T, int D, int CB>
@@ -269,8 +293,11 @@ void k_sla_fwd_proj(KernelArgs a, ProjArgs pa, T* __restrict__ o) {
     // streamed job by job: K, V for the state, then Q for the outputs.  The two
     // cases are separate branches, each with its own window loop, so that the
     // resident rows are not live in the streamed one.
-    XBlock<T, CB> xb;
-    if (ww.kind != 0 && resident) xblock_fetch<T, CB>(xb, cur.br, ww.ra, ww.rb, n, x, g);
+    constexpr bool kByJob = CB > kProjBlockFetchMaxCB;
+    XBlock<T, kByJob ? 1 : CB> xb;
+    if constexpr (!kByJob) {
+      if (ww.kind != 0 && resident) xblock_fetch<T, CB>(xb, cur.br, ww.ra, ww.rb, n, x, g);
+    }
     // the next item: its rows and windows are requested now, its successor's entry too
     Pending nxt;
     pending_request(nxt, a, nsl, ne, wv, perm, lane);
@@ -279,7 +306,19 @@ void k_sla_fwd_proj(KernelArgs a, ProjArgs pa, T* __restrict__ o) {
     WinIter wi;
     if (resident) {
       Block<T, D, 3> bk;
-      if (ww.kind != 0) project<T, D, CB>(bk, xb, kAll, s_w, s_b, i, g);
+      if constexpr (kByJob) {
+        if (ww.kind != 0) {
+#pragma unroll
+          for (int jj = 0; jj < kBlockJobs; ++jj) {
+            Raw<T, 8> xj[2][CB];
+            xjob_fetch<T, CB>(xj, bk.j[jj].o, bk.j[jj].ok, cur.br, jj, ww.ra, ww.rb, n, x, g);
+            project_job<T, D, CB>(bk.j[jj], xj, kAll, s_w, s_b, i, g);
+            __builtin_amdgcn_sched_barrier(0);
+          }
+        }
+      } else {
+        if (ww.kind != 0) project<T, D, CB>(bk, xb, kAll, s_w, s_b, i, g);
+      }
       for (bool more = wi.first(ww, cur.str); more; more = wi.next(ww, cur.str)) {
         const int32_t wa = wi.wc.ws, wb = wi.wc.we;
         State<D> st;
@@ -339,11 +378,18 @@ void k_sla_fwd_proj(KernelArgs a, ProjArgs pa, T* __restrict__ o) {
 // holds channels 32 kb + 8 g .. + 7 of row i as the second operand; output tile
 // t gives it y[i][16 t + 4 g + j], and two tiles are one 32-column block in the
 // slot order of the row stores.
+// C = 256: W_o takes 135 KB of LDS, one workgroup per CU, so that workgroup
+// has 16 waves (128 VGPRs per lane: the tiles below fit with the scheduling
+// fences between them).
+template <int CB>
+constexpr int kOutWaves = CB > 4 ? 16 : kWaves;
+
 template <typename T, int CB>
-__global__ __launch_bounds__(256) void k_out_proj(KernelArgs a, const T* __restrict__ o,
-                                                  const T* __restrict__ w, const T* __restrict__ b,
-                                                  T* __restrict__ y) {
-  constexpr int C = 32 * CB, LDW = C + 8;
+__global__ __launch_bounds__(64 * kOutWaves<CB>) void k_out_proj(KernelArgs a, const T* __restrict__ o,
+                                                                 const T* __restrict__ w,
+                                                                 const T* __restrict__ b,
+                                                                 T* __restrict__ y) {
+  constexpr int C = 32 * CB, LDW = C + 8, NW = kOutWaves<CB>;
   __shared__ __attribute__((aligned(16))) T s_w[C * LDW];
   __shared__ __attribute__((aligned(16))) float s_b[C];
   const PlanHeader* hdr = a.hdr;
@@ -360,8 +406,8 @@ __global__ __launch_bounds__(256) void k_out_proj(KernelArgs a, const T* __restr
   const int32_t nrows = max(0, min(a.offs[a.W], n));
   const int lane = lane_id(), wv = threadIdx.x >> 6;
   const int i = lane & 15, g = lane >> 4;
-  for (int32_t tile = (int32_t)blockIdx.x * kWaves + wv; tile * 16 < nrows;
-       tile += (int32_t)gridDim.x * kWaves) {
+  for (int32_t tile = (int32_t)blockIdx.x * NW + wv; tile * 16 < nrows;
+       tile += (int32_t)gridDim.x * NW) {
     const int32_t p = tile * 16 + i;
     const int32_t row = p < nrows ? (perm ? perm[p] : p) : -1;
     const bool ok = (uint32_t)row < (uint32_t)n;
@@ -388,6 +434,9 @@ __global__ __launch_bounds__(256) void k_out_proj(KernelArgs a, const T* __restr
         f[4 * tt + 1] = acc[1] + bias.y;
         f[4 * tt + 2] = acc[2] + bias.z;
         f[4 * tt + 3] = acc[3] + bias.w;
+        // C = 256: keep later tiles' weight reads from being hoisted here (all of
+        // them at once would not fit in the registers)
+        if constexpr (CB > 4) __builtin_amdgcn_sched_barrier(0);
       }
       RowIO<T, 32>::put(row_at(y, ok ? row : 0, (size_t)C, 32 * hb), g, F8::from_f32(f), ok);
     }
@@ -395,6 +444,20 @@ __global__ __launch_bounds__(256) void k_out_proj(KernelArgs a, const T* __restr
 }
 
 // ------------------------------------------------------------ host launchers
+// Resident workgroups of a launch of `threads`-thread workgroups (workgroups per
+// CU x CUs; queried per call, for the launches that are not 256 threads wide).
+inline int64_t resident_for(const void* kernel, int threads) {
+  int per_cu = 0, cus = 0, dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) dev = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, threads, 0) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      per_cu < 1 || cus < 1) {
+    per_cu = 1;
+    cus = 256;
+  }
+  return (int64_t)per_cu * cus;
+}
+
 // Projected forward: the fused projection + SLA kernel, then the output
 // projection.  Workgroups of the fused kernel: as grid_size, rounded up to a
 // multiple of 8 H (every workgroup keeps one head), at most enough for every item
@@ -422,11 +485,11 @@ static hipError_t proj_impl(const void* plan, int32_t n, int32_t W, int32_t H, f
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const void* kout = reinterpret_cast<const void*>(&k_out_proj<T, CB>);
-  int64_t go = resident_workgroups(kout);
-  const int64_t passes = ((int64_t)n + 16 * kWaves - 1) / (16 * kWaves);
+  int64_t go = kOutWaves<CB> == kWaves ? resident_workgroups(kout) : resident_for(kout, 64 * kOutWaves<CB>);
+  const int64_t passes = ((int64_t)n + 16 * kOutWaves<CB> - 1) / (16 * kOutWaves<CB>);
   if (go > passes) go = passes;
   if (go < 1) go = 1;
-  hipLaunchKernelGGL((k_out_proj<T, CB>), dim3((unsigned)go), dim3(64 * kWaves), 0, stream, a,
+  hipLaunchKernelGGL((k_out_proj<T, CB>), dim3((unsigned)go), dim3(64 * kOutWaves<CB>), 0, stream, a,
                      static_cast<const T*>(o), static_cast<const T*>(wo), static_cast<const T*>(bo),
                      static_cast<T*>(y));
   return hipGetLastError();
@@ -439,14 +502,16 @@ static hipError_t projected_t(const void* plan, int32_t n, int32_t W, int32_t H,
                               hipStream_t stream) {
   const int C = H * d;
   if (d == 32) {
+    if (C == 256) return proj_impl<T, 32, PHI, 8>(plan, n, W, H, eps, x, wqkv, bqkv, wo, bo, o, y, stream);
     if (C == 128) return proj_impl<T, 32, PHI, 4>(plan, n, W, H, eps, x, wqkv, bqkv, wo, bo, o, y, stream);
     return proj_impl<T, 32, PHI, 2>(plan, n, W, H, eps, x, wqkv, bqkv, wo, bo, o, y, stream);
   }
+  if (C == 256) return proj_impl<T, 16, PHI, 8>(plan, n, W, H, eps, x, wqkv, bqkv, wo, bo, o, y, stream);
   if (C == 128) return proj_impl<T, 16, PHI, 4>(plan, n, W, H, eps, x, wqkv, bqkv, wo, bo, o, y, stream);
   return proj_impl<T, 16, PHI, 2>(plan, n, W, H, eps, x, wqkv, bqkv, wo, bo, o, y, stream);
 }
 
-// dtype: 1 f16, 2 bf16; C = H d in {64, 128}; phi: 0 elu + 1, 1 ReLU
+// dtype: 1 f16, 2 bf16; C = H d in {64, 128, 256}; phi: 0 elu + 1, 1 ReLU
 hipError_t launch_forward_projected(const void* plan, int32_t n, int32_t W, int dtype, int32_t H,
                                     int32_t d, int phi, float eps, const void* x, const void* wqkv,
                                     const void* bqkv, const void* wo, const void* bo, void* o,

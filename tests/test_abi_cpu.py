@@ -173,7 +173,7 @@ def test_projected_argument_errors(L):
                                        FAKE, y, None)
     assert call(dtype=0) == sla.SLA_E_UNSUPPORTED        # fp32 is not supported
     assert call(H=3) == sla.SLA_E_UNSUPPORTED            # C = 96
-    assert call(H=8) == sla.SLA_E_UNSUPPORTED            # C = 256
+    assert call(H=16) == sla.SLA_E_UNSUPPORTED           # C = 512
     assert call(d=24) == sla.SLA_E_UNSUPPORTED
     assert call(fm=3) == sla.SLA_E_ARG
     assert call(eps=-1.0) == sla.SLA_E_ARG

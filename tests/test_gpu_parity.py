@@ -538,17 +538,18 @@ def projected_parity(S, ids, offsets, n, W, H, d, dtype, fmap="elu1", eps=0.0, b
     assert ey <= TOL[dtype], f"{label}: y relative error {ey:.3e}"
 
 
-@pytest.mark.parametrize("cfg", [2, 3, 5])
+@pytest.mark.parametrize("cfg", [2, 3, 4, 5])
 def test_projected_config(sla, cfg):
     # config 3 (bf16, H = 8, d = 16) has windows of up to 1,024 rows: quarters of
-    # more than 64 rows take the streamed path
+    # more than 64 rows take the streamed path; config 4 (bf16, H = 8, d = 32) has
+    # C = 256, whose features are fetched and projected one 32-row job at a time
     wl = workloads.make_config(cfg, with_grad=False)
     projected_parity(sla, wl["ids"], wl["offsets"], wl["n"], wl["num_windows"], wl["heads"], wl["head_dim"],
                      wl["dtype"], label=f"cfg{cfg}")
 
 
 @pytest.mark.parametrize("dtype", ["f16", "bf16"])
-@pytest.mark.parametrize("shape", [(4, 32), (8, 16), (2, 32), (4, 16)])
+@pytest.mark.parametrize("shape", [(4, 32), (8, 16), (2, 32), (4, 16), (8, 32), (16, 16)])
 def test_projected_shapes(sla, dtype, shape):
     H, d = shape
     rng = np.random.default_rng([52, H, d, len(dtype)])
