@@ -800,7 +800,7 @@ def _pool_work(job):
 
 def cpu_baseline_pool(cfg, training, budget_s, variant=None, max_procs=16):
     """The same oracle calls split over contiguous window ranges of balanced row
-    counts, one range per process (at most the 16-core share of the GPU machine); the
+    counts, one range per process (at most 16: one GPU's share of the host); the
     segment build runs in the parent.  Workers start (and build their inputs)
     before the clock starts."""
     import multiprocessing as mp
