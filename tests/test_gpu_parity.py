@@ -356,6 +356,42 @@ def test_backward_determinism(sla):
         assert torch.equal(a, b)
 
 
+def test_streams_share_a_plan(sla):
+    # the interface allows forward and backward calls on different streams to
+    # read one plan at the same time: two streams (default priority) run their
+    # own inputs through it, interleaved, and every result must equal the
+    # sequential one bit for bit
+    import torch
+
+    wl = workloads.make_config(5)
+    plan = build(sla, ids=wl["ids"], W=wl["num_windows"])
+    rng = np.random.default_rng(68)
+    sets = []
+    for _ in range(2):
+        q, k, v, do = (to_dev(workloads.cast_values(rng.standard_normal(wl["q"].shape).astype(np.float32), "f16"),
+                              "f16") for _ in range(4))
+        sets.append((q, k, v, do))
+    ref = []
+    for q, k, v, do in sets:
+        o = sla.forward(plan, q, k, v)
+        ref.append([o.clone()] + [t.clone() for t in sla.backward(plan, q, k, v, do)])
+    torch.cuda.synchronize()
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    outs = [[torch.empty_like(sets[i][0]) for _ in range(4)] for i in range(2)]
+    for s_ in streams:
+        s_.wait_stream(torch.cuda.current_stream())
+    for _ in range(3):
+        for i, s_ in enumerate(streams):
+            with torch.cuda.stream(s_):
+                q, k, v, do = sets[i]
+                sla.forward(plan, q, k, v, out=outs[i][0])
+                sla.backward(plan, q, k, v, do, outs[i][1], outs[i][2], outs[i][3])
+    torch.cuda.synchronize()
+    for i in range(2):
+        for a, b in zip(ref[i], outs[i]):
+            assert torch.equal(a, b)
+
+
 # ------------------------------------------------------- naive comparator
 def scatter_parity(S, ids, offsets, n, W, q, k, v, dtype, label=""):
     import torch
