@@ -392,6 +392,58 @@ def test_streams_share_a_plan(sla):
             assert torch.equal(a, b)
 
 
+def test_graph_replays(sla):
+    # the whole path captured in one HIP graph (segment build, forward, backward,
+    # cell table, cross-window interaction forward and backward), replayed three
+    # times; before each replay the outputs, the plan buffer and the cell table
+    # are scribbled over by eager work, and every replay must reproduce the eager
+    # results bit for bit
+    import torch
+
+    wl = workloads.make_config(5)
+    W = wl["num_windows"]
+    ids = to_dev(wl["ids"].astype(np.int32))
+    q, k, v, do = (to_dev(wl[x], "f16") for x in ("q", "k", "v", "dout"))
+    f = workloads.make_cwi_frame()
+    grid = f["grid"]
+    cc = torch.from_numpy(f["coords"]).cuda()
+    x = to_dev(f["x"], "f16")
+    w = [to_dev(f[key], "f16") for key in ("w_x", "w_y", "w_3")]
+    dy = to_dev(workloads.cast_values(np.random.default_rng(69).standard_normal(f["x"].shape).astype(np.float32),
+                                      "f16"), "f16")
+
+    def path():
+        plan = sla.build_segments(ids, num_windows=W)
+        o = sla.forward(plan, q, k, v)
+        grads = sla.backward(plan, q, k, v, do)
+        m, _ = sla.cwi_build_map(cc, grid)
+        y = sla.cwi_forward(m, grid, cc, x, *w)
+        back = sla.cwi_backward(m, grid, cc, x, *w, dy)
+        return plan, m, [o, *grads, y, *back]
+
+    _, _, eager = path()
+    eager = [t.clone() for t in eager]
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        with torch.cuda.graph(g, stream=side):
+            plan_g, map_g, outs = path()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    for rep in range(3):
+        for t in outs:
+            t.fill_(float("nan"))
+        plan_g.buf.fill_(0xA5)
+        map_g.fill_(-7)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        for i, (a, b) in enumerate(zip(eager, outs)):
+            assert torch.equal(a, b), f"replay {rep}: output {i} differs from the eager result"
+
+
 # ------------------------------------------------------- naive comparator
 def scatter_parity(S, ids, offsets, n, W, q, k, v, dtype, label=""):
     import torch
