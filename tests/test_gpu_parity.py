@@ -394,7 +394,8 @@ def test_streams_share_a_plan(sla):
 
 def test_graph_replays(sla):
     # the whole path captured in one HIP graph (segment build, forward, backward,
-    # cell table, cross-window interaction forward and backward), replayed three
+    # their ReLU / eps variants, the fused projection, cell table, cross-window
+    # interaction forward and backward), replayed three
     # times; before each replay the outputs, the plan buffer and the cell table
     # are scribbled over by eager work, and every replay must reproduce the eager
     # results bit for bit
@@ -412,14 +413,27 @@ def test_graph_replays(sla):
     dy = to_dev(workloads.cast_values(np.random.default_rng(69).standard_normal(f["x"].shape).astype(np.float32),
                                       "f16"), "f16")
 
+    n, H, d = q.shape
+    C = H * d
+    rng = np.random.default_rng(70)
+    xp = to_dev(workloads.cast_values(rng.standard_normal((n, C)).astype(np.float32), "f16"), "f16")
+    wq = to_dev(workloads.cast_values((rng.standard_normal((3 * C, C)) / np.sqrt(C)).astype(np.float32), "f16"),
+                "f16")
+    wo = to_dev(workloads.cast_values((rng.standard_normal((C, C)) / np.sqrt(C)).astype(np.float32), "f16"), "f16")
+
     def path():
         plan = sla.build_segments(ids, num_windows=W)
         o = sla.forward(plan, q, k, v)
         grads = sla.backward(plan, q, k, v, do)
+        o_relu = sla.forward(plan, q, k, v, feature_map="relu", eps=1e-3)
+        grads_relu = sla.backward(plan, q, k, v, do, feature_map="relu", eps=1e-3)
+        po = torch.empty((n, H, d), dtype=torch.float16, device="cuda")
+        py = torch.empty((n, C), dtype=torch.float16, device="cuda")
+        sla.forward_projected(plan, xp, wq, wo, H, None, None, po, py)
         m, _ = sla.cwi_build_map(cc, grid)
         y = sla.cwi_forward(m, grid, cc, x, *w)
         back = sla.cwi_backward(m, grid, cc, x, *w, dy)
-        return plan, m, [o, *grads, y, *back]
+        return plan, m, [o, *grads, o_relu, *grads_relu, po, py, y, *back]
 
     _, _, eager = path()
     eager = [t.clone() for t in eager]
