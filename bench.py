@@ -90,7 +90,8 @@ def kernel_source_hash():
 
 
 def short_kernel(name):
-    for k in ("k_sla_bwd", "k_sla_fwd", "k_count", "k_plan", "k_scatter"):
+    for k in ("k_sla_bwd", "k_sla_fwd", "k_count", "k_plan", "k_scatter", "k_cwi_tiled", "k_cwi_fwd",
+              "k_cwi_dw_reduce", "k_cwi_dw", "k_cwi_map", "k_cwi_clear"):
         if k in name:
             return k
     if "copyBuffer" in name:    # the runtime's device-to-device copy kernel
@@ -128,7 +129,8 @@ def pmc_summary(fetch_csv, write_csv):
         f"write_factor: {fw:.4f}   (WRITE_SIZE bytes by the copy / bytes it writes)",
         "kernel      dispatches  FETCH_raw_B   WRITE_raw_B   fetch_scaled_B  write_scaled_B  traffic_scaled_B",
     ]
-    for k in ("k_count", "k_plan", "k_scatter", "k_sla_fwd", "k_sla_bwd", "copy"):
+    for k in ("k_count", "k_plan", "k_scatter", "k_sla_fwd", "k_sla_bwd", "k_cwi_clear", "k_cwi_map",
+              "k_cwi_tiled", "k_cwi_fwd", "k_cwi_dw", "k_cwi_dw_reduce", "copy"):
         if k in f and k in w:
             fr, wr = f[k][0], w[k][0]
             lines.append(f"{k:<11} {f[k][1]:>10}  {fr:>12.0f}  {wr:>12.0f}  {fr / ff:>14.0f}  "
@@ -435,13 +437,7 @@ def main():
     achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
 
     if args.copy_probe:
-        for _ in range(3):
-            a = torch.empty(COPY_PROBE_BYTES, dtype=torch.uint8, device=dev).fill_(1)
-            b = torch.empty_like(a)
-            torch.cuda.synchronize()
-            b.copy_(a)
-            torch.cuda.synchronize()
-            del a, b
+        copy_probe(torch, dev)
     step_bytes = (fwd_bytes + bwd_bytes + 8 * n) if training else fwd_bytes
     copy_gbs = measure_copy(torch, dev)
 
@@ -507,17 +503,16 @@ def bench_cwi(torch, sla, workloads, dev, args):
     kernels, fp16): the cell table build and the forward, rows visited in the
     window order of the frame's SLA plan (and, for comparison, in row order);
     buffer sets rotated, graph replay."""
-    import oracle  # only to derive the window order of the synthetic frames
-
     nsets = 6
     sets = []
     for s_ in range(nsets):
         f = workloads.make_cwi_frame(seed=s_)
-        perm, _, _ = oracle.segments_ref(f["ids"], f["num_windows"])
+        # the window order comes from the library's own plan of the frame
+        plan = sla.build_segments(torch.from_numpy(f["ids"].astype(np.int32)).to(dev), f["num_windows"])
         dt = {"f16": torch.float16}[f["dtype"]]
         sets.append({
             "coords": torch.from_numpy(f["coords"]).to(dev),
-            "order": torch.from_numpy(perm.astype(np.int32)).to(dev),
+            "order": plan.perm,
             "x": torch.from_numpy(f["x"]).to(dev),
             "w": [torch.from_numpy(f[k]).to(dev) for k in ("w_x", "w_y", "w_3")],
             "y": torch.empty(f["n"], f["channels"], dtype=dt, device=dev),
@@ -548,6 +543,14 @@ def bench_cwi(torch, sla, workloads, dev, args):
         for i in range(args.warmup):
             fn(sets[i % nsets])
         torch.cuda.synchronize()
+        t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        if args.no_graph:   # eager launches (counter runs)
+            t0.record()
+            for i in range(reps):
+                fn(sets[i % nsets])
+            t1.record()
+            torch.cuda.synchronize()
+            return t0.elapsed_time(t1) / reps * 1e3
         graphs = []
         cap = torch.cuda.Stream(dev)
         cap.wait_stream(torch.cuda.current_stream(dev))
@@ -561,7 +564,6 @@ def bench_cwi(torch, sla, workloads, dev, args):
         for g in graphs:
             g.replay()
         torch.cuda.synchronize()
-        t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         t0.record()
         for i in range(reps):
             graphs[i % nsets].replay()
@@ -569,7 +571,7 @@ def bench_cwi(torch, sla, workloads, dev, args):
         torch.cuda.synchronize()
         return t0.elapsed_time(t1) / reps * 1e3
 
-    reps = max(100, args.steps)
+    reps = max(100, args.steps) if not args.no_graph else args.steps
     for st in sets:
         build(st)
     t_build = timed(build, reps)
@@ -585,7 +587,7 @@ def bench_cwi(torch, sla, workloads, dev, args):
     # coordinates and visiting order read by both passes
     bwd_bytes = n * (2 * C * e + 2 * (3 * C // 4) * e + 2 * (12 + 4))
     build_bytes = 4 * cells + n * (12 + 4)        # table cleared, coordinates read, rows written
-    return {
+    out = {
         "mode": "cwi",
         "workload": workloads.make_cwi_frame.__doc__.split(":")[0].strip().replace("\n", " "),
         "n": n, "channels": C, "taps": 13, "grid": list(sets[0]["grid"]), "dtype": "f16", "buffer_sets": nsets,
@@ -600,7 +602,11 @@ def bench_cwi(torch, sla, workloads, dev, args):
         "backward_algorithmic_bytes": bwd_bytes,
         "backward_gbs": bwd_bytes / (t_bwd * 1e-6) / 1e9,
         "backward_frac_of_hbm_peak": bwd_bytes / (t_bwd * 1e-6) / 1e9 / HBM_PEAK_GBS,
+        "graph_replay": not args.no_graph,
     }
+    if args.copy_probe:
+        copy_probe(torch, dev)
+    return out
 
 
 def bench_projected(torch, sla, workloads, dev, args):
@@ -738,6 +744,18 @@ def compare_scatter(torch, sla, workloads, dev):
         rows.append(case(ids, nw, f"windows of {wlen} rows"))
     return {"metric": "SLA forward: chunk-wise vs naive scatter-based (time and extra memory)",
             "dtype": "f16", "heads": H, "head_dim": d, "data": "synthetic", "comparison": rows}
+
+
+def copy_probe(torch, dev):
+    """Three plain device-to-device copies of COPY_PROBE_BYTES from distinct
+    buffers: the reference dispatches that scale the HBM byte counters."""
+    for _ in range(3):
+        a = torch.empty(COPY_PROBE_BYTES, dtype=torch.uint8, device=dev).fill_(1)
+        b = torch.empty_like(a)
+        torch.cuda.synchronize()
+        b.copy_(a)
+        torch.cuda.synchronize()
+        del a, b
 
 
 def measure_copy(torch, dev, nbytes=COPY_PROBE_BYTES, reps=5):

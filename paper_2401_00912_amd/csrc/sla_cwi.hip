@@ -512,14 +512,17 @@ hipError_t launch_cwi_forward(const int32_t* map, int32_t gx, int32_t gy, int32_
 //    workgroup take adjacent row ranges; their sums are added in wave order
 //    and written as the workgroup's partial, and k_cwi_dw_reduce adds the
 //    partials in workgroup order.  Every order is fixed, so the result is
-//    deterministic.
+//    deterministic.  XCD placement: the row blocks of a (branch, slice) are a
+//    multiple of 8 and workgroup j of it takes row block (j mod 8) B / 8 + j / 8
+//    (B blocks), so each XCD walks one contiguous eighth of the rows for every
+//    branch and slice, and its L2 serves the lines they share.
 constexpr int kDwWaves = 4;          // waves per workgroup: adjacent row ranges
 constexpr int kDwBatch = 8;          // rows whose loads are in flight together
 #ifndef SLA_CWI_DW_ROWS
 #define SLA_CWI_DW_ROWS 64
 #endif
 constexpr int kDwRows = SLA_CWI_DW_ROWS;  // rows per wave, until kDwMaxBlocks is reached
-constexpr int kDwMaxBlocks = 512;    // workgroups per (branch, pair slice), at most
+constexpr int kDwMaxBlocks = 512;    // workgroups per (branch, pair slice), at most (a multiple of 8)
 
 struct DwGrid {
   int32_t blocks;        // workgroups per (branch, pair slice)
@@ -530,7 +533,8 @@ struct DwGrid {
 inline DwGrid cwi_dw_grid(int32_t n, int32_t c, int esize, int32_t kx, int32_t ky, int32_t gz) {
   DwGrid g;
   const int64_t waves = ((int64_t)n + kDwRows - 1) / kDwRows;
-  g.blocks = (int32_t)std::min<int64_t>(kDwMaxBlocks, std::max<int64_t>(1, (waves + kDwWaves - 1) / kDwWaves));
+  const int64_t want = std::min<int64_t>(kDwMaxBlocks, std::max<int64_t>(1, (waves + kDwWaves - 1) / kDwWaves));
+  g.blocks = (int32_t)((want + 7) / 8 * 8);   // a multiple of 8: one eighth per XCD
   const int64_t per_block = (int64_t)g.blocks * kDwWaves;
   g.rows = (int32_t)(((int64_t)n + per_block - 1) / per_block);
   const int pq = c * esize / 16;
@@ -557,7 +561,8 @@ __global__ __launch_bounds__(256) void k_cwi_dw(CwiArgs a, DwGrid g, const T* __
     branch = 1;
     b -= n0;
   }
-  const int32_t slice = b / g.blocks, kb = b - slice * g.blocks;
+  const int32_t slice = b / g.blocks, j = b - slice * g.blocks;
+  const int32_t kb = (j & 7) * (g.blocks >> 3) + (j >> 3);
   const int wave = (int)(threadIdx.x >> 6), lane = lane_id();
   const int taps = branch == 0 ? a.kx : (branch == 1 ? a.ky : (a.gz == 1 ? 9 : 27));
   const int half = branch == 0 ? (a.kx - 1) / 2 : (branch == 1 ? (a.ky - 1) / 2 : 0);

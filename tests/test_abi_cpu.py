@@ -212,12 +212,12 @@ def test_cwi_argument_errors(L):
 
 def test_cwi_backward_argument_errors(L):
     wb = L.sla_cwi_backward_workspace_bytes
-    # a workgroup per 256 rows (four waves of 64), at most 512
-    assert wb(60000, 1, 128, 13, 13) == 235 * 53 * 32 * 4
-    assert wb(100, 1, 128, 13, 13) == 1 * 53 * 32 * 4
+    # a workgroup per 256 rows (four waves of 64), rounded up to a multiple of 8, at most 512
+    assert wb(60000, 1, 128, 13, 13) == 240 * 53 * 32 * 4
+    assert wb(100, 1, 128, 13, 13) == 8 * 53 * 32 * 4
     assert wb(10 ** 6, 1, 128, 13, 13) == 512 * 53 * 32 * 4
-    assert wb(0, 1, 128, 13, 13) == 53 * 32 * 4                  # the zero gradients still go through it
-    assert wb(100, 1, 2048, 63, 63) == 153 * 512 * 4
+    assert wb(0, 1, 128, 13, 13) == 8 * 53 * 32 * 4              # the zero gradients still go through it
+    assert wb(100, 1, 2048, 63, 63) == 8 * 153 * 512 * 4
     assert wb(100, 1, 96, 13, 13) == 0
     need = wb(100, 1, 128, 13, 13)
 
