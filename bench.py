@@ -440,6 +440,11 @@ def main():
         copy_probe(torch, dev)
     step_bytes = (fwd_bytes + bwd_bytes + 8 * n) if training else fwd_bytes
     copy_gbs = measure_copy(torch, dev)
+    perms = None
+    if "ids" in sets[0]:   # the plans' permutations (rows arrive unsorted)
+        lay = sla.plan_layout(n, W)
+        perms = [p.buf[lay.perm: lay.perm + 4 * n].view(torch.int32) for p in plans]
+    gather_gbs = measure_gather(torch, dev, sets, perms, ("q", "k", "v", "dout") if training else ("q", "k", "v"))
 
     nonempty = int((np.diff(plans[0].offsets.cpu().numpy()) > 0).sum())
     frames = base.get("frames", 1)
@@ -482,6 +487,10 @@ def main():
             # a plain device-to-device copy on the same GPU, for scale
             "copy_gbs": copy_gbs,
             "frac_of_copy": achieved / copy_gbs if copy_gbs else None,
+            # torch's index_select of the kernel's input rows through the same
+            # permutation (gathered reads, contiguous writes), for scale
+            "gather_gbs": gather_gbs,
+            "frac_of_gather": achieved / gather_gbs if gather_gbs else None,
         },
         "breakdown_ms": {"build": t_build, "forward": t_fwd, "backward": t_bwd},
         "step_roofline_frac": step_bytes / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS,
@@ -774,6 +783,42 @@ def measure_copy(torch, dev, nbytes=COPY_PROBE_BYTES, reps=5):
     ms = t0.elapsed_time(t1) / reps
     del bufs, dst
     return 2 * nbytes / (ms * 1e-3) / 1e9
+
+
+def measure_gather(torch, dev, sets, perms, names, reps=20):
+    """GB/s (read + write bytes) of torch's row gather (index_select through each
+    set's plan permutation into contiguous rows) over the matrices `names` of the
+    rotating buffer sets, in one graph: what a library gather reaches on the
+    same rows in the same order, for scale.  None without permutations."""
+    if perms is None:
+        return None
+    idx = [p.long() for p in perms]
+    outs = [[torch.empty_like(st[m]) for m in names] for st in sets]
+    def run():
+        for st, ix, o in zip(sets, idx, outs):
+            for m, dst in zip(names, o):
+                torch.index_select(st[m], 0, ix, out=dst)
+    run()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    cap = torch.cuda.Stream(dev)
+    cap.wait_stream(torch.cuda.current_stream(dev))
+    with torch.cuda.stream(cap):
+        with torch.cuda.graph(g, stream=cap):
+            run()
+    torch.cuda.current_stream(dev).wait_stream(cap)
+    g.replay()
+    torch.cuda.synchronize()
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for _ in range(reps):
+        g.replay()
+    t1.record()
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / reps
+    nbytes = sum(2 * st[m].numel() * st[m].element_size() for st in sets for m in names)
+    del g, outs
+    return nbytes / (ms * 1e-3) / 1e9
 
 
 def cpu_model():
