@@ -1,7 +1,7 @@
 // Segment builder: stable counting sort of rows by window id, CSR window offsets
 // and the chunk table (Sec. 3.2 / Fig. 3(a): voxels ordered by window into one
-// flattened matrix that is partitioned into chunks; Fig. 5 caption: "offsets
-// generation" computes the start of every chunk).
+// flattened matrix that is partitioned into chunks; the offset generation timed
+// in Fig. 5 computes the start of every chunk).
 //
 // Mode A (ids given), two launches over builder blocks of E rows:
 //   k_count    per block, a histogram of its rows' window ids (LDS atomics; the
@@ -12,8 +12,9 @@
 //              stable rank of every row among the rows of its window in this
 //              block (wave ballots on the id bits give the lanes sharing an id;
 //              waves take their bases in order) and perm[offsets[id] + block
-//              prefix + rank] = row.  Block 0 also publishes the offsets, the
-//              chunk table and the header.
+//              prefix + rank] = row.  One more workgroup (the last) computes the
+//              same totals and publishes the offsets, the chunk table and the
+//              header.
 // Mode B (CSR offsets given) and n = 0: one workgroup, k_plan, validates the
 // offsets and writes the chunk table and header.
 #include <atomic>
