@@ -18,4 +18,5 @@ from .sla_ref import (  # noqa: F401
     sla_forward_ref,
     sla_projected_forward_ref,
     widen,
+    xca_forward_ref,
 )

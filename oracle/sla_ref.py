@@ -14,8 +14,8 @@ Paper: "ScatterFormer: Efficient Voxel Transformer with Scattered Linear Attenti
 
 What is computed, and the passage it follows
 --------------------------------------------
-* ``phi`` / ``dphi``: the kernel feature map.  Sec. 3.2 (after Eq. (3)) only names
-  "the kernel function" and attributes LA to the linear-transformer paper it cites,
+* ``phi`` / ``dphi``: the kernel feature map.  Sec. 3.2 (after Eq. (3)) speaks
+  only of a kernel function and attributes LA to the linear-transformer paper it cites,
   whose feature map is elu(x)+1.  Reading taken: phi(x) = x + 1 for x > 0 and
   exp(x) otherwise.  This is ``feature_map="elu1"``, the default.
 * ``phi_relu`` / ``dphi_relu``: the variant of Sec. 4.5 / Tab. 7, which trains
@@ -32,8 +32,8 @@ What is computed, and the passage it follows
   stable sort of rows by window id plus CSR offsets over the window slots; this
   result is unique.
 * ``chunk_plan_ref``: Sec. 3.2 / Fig. 3(a) partition the flattened matrix into
-  chunks, and the Fig. 5 caption defines "offsets generation" as computing each
-  chunk's start row.  The packing rule written here (chunks of whole short
+  chunks, and the offset-generation step timed in Fig. 5 computes each chunk's
+  start row.  The packing rule written here (chunks of whole short
   windows, a table of long windows that are split among workers) is this
   library's own plan rule (the paper does not give one); it is pinned by its
   invariants.
@@ -59,6 +59,14 @@ What is computed, and the passage it follows
   holds no voxel contributes zero; each tap a centred cross-correlation tap (the
   deep-learning "convolution"); the first axis branch along x, the second along
   y; no bias (the block's normalisation follows).
+* ``xca_forward_ref``: the XCA row of the same ablation (Sec. 4.5, Tab. 7), which
+  cites cross-covariance attention (XCiT).  Reading taken: XCiT's operation
+  applied inside every window of the flattened matrix, per head: the window's
+  q and k columns are L2-normalised over the window's rows (a norm below 1e-12
+  counts as 1e-12), A = softmax over c of tau_h qhat[:, e] . khat[:, c] (a d x d
+  matrix per window and head; tau_h is the head's learned temperature, an
+  input here), and o_i[e] = sum_c A[e, c] v_i[c] for every row i of the window.
+  It needs the same per-window d x d reduction over the window's rows as Eq. (3).
 * ``cwi_backward_ref``: the gradients of that module with respect to its input
   and its three kernels, by the chain rule (the paper trains the model but does
   not write them out).
@@ -82,6 +90,7 @@ __all__ = [
     "sla_projected_forward_ref",
     "cwi_forward_ref",
     "cwi_backward_ref",
+    "xca_forward_ref",
 ]
 
 
@@ -448,3 +457,45 @@ def cwi_backward_ref(coords, x, w_x, w_y, w_3, dy, grid):
             for dx_ in (-1, 0, 1):
                 tap(2, (dx_ + 1) + 3 * (dy_ + 1) + 9 * (dz + 1), w_3, (dx_, dy_, dz))
     return dx, dws[0], dws[1], dws[2]
+
+
+# ---------------------------------------------------------------------- XCA variant
+XCA_NORM_FLOOR = 1e-12
+
+
+def xca_forward_ref(q, k, v, tau, offsets, perm=None):
+    """Cross-covariance attention inside every window (Sec. 4.5, Tab. 7, XCA row).
+
+    q, k, v: float64 [n, H, d] in original row order; tau: [H] temperatures;
+    offsets / perm as in ``sla_forward_ref``.  For window w with rows R and head h:
+        qhat[:, e] = q[R, h, e] / max(||q[R, h, e]||_2, 1e-12)      (likewise khat)
+        G[e, c]    = tau[h] * qhat[:, e] . khat[:, c]                (d x d)
+        A[e, :]    = softmax(G[e, :])                                 (over c)
+        o_i[e]     = sum_c A[e, c] v[i, h, c]                         for i in R.
+    Rows that belong to no window are NaN.
+    """
+    q = np.asarray(q, dtype=np.float64)
+    k = np.asarray(k, dtype=np.float64)
+    v = np.asarray(v, dtype=np.float64)
+    tau = np.asarray(tau, dtype=np.float64)
+    n, H, d = q.shape
+    if tau.shape != (H,):
+        raise ValueError("tau must hold one temperature per head")
+    out = np.full(q.shape, np.nan)
+    for w in range(len(offsets) - 1):
+        rows = _window_rows(offsets, perm, w)
+        if rows.size == 0:
+            continue
+        for h in range(H):
+            qw = q[rows, h, :]          # [m, d]
+            kw = k[rows, h, :]
+            qn = np.maximum(np.sqrt((qw * qw).sum(axis=0)), XCA_NORM_FLOOR)   # [d]
+            kn = np.maximum(np.sqrt((kw * kw).sum(axis=0)), XCA_NORM_FLOOR)
+            qhat = qw / qn
+            khat = kw / kn
+            G = tau[h] * (qhat.T @ khat)                 # [d, d]: row e, column c
+            G = G - G.max(axis=1, keepdims=True)
+            A = np.exp(G)
+            A = A / A.sum(axis=1, keepdims=True)
+            out[rows, h, :] = v[rows, h, :] @ A.T        # o_i[e] = sum_c A[e, c] v_i[c]
+    return out

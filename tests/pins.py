@@ -649,3 +649,94 @@ def cwi_backward_pin_failures(cwi_bwd, cwi_fwd):
         if abs(fd - dw[idx]) > 1e-6 * max(1.0, abs(fd)):
             fails.append(f"cwi_fd_dw{b}")
     return fails
+
+
+# ----------------------------------------------------------------- XCA variant
+def brute_xca(q, k, v, tau, ids, num_windows):
+    """XCA per window with plain Python loops, normalising after the dot product,
+    G[e][c] = tau (sum_j q_je k_jc) / (|q_e| |k_c|), and each softmax weight as
+    1 / sum_c' exp(G[e][c'] - G[e][c])."""
+    n, H, d = q.shape
+    out = np.full((n, H, d), np.nan)
+    for w in range(num_windows):
+        rows = [r for r in range(n) if ids[r] == w]
+        if not rows:
+            continue
+        for h in range(H):
+            nq = [max(math.sqrt(sum(q[r, h, e] ** 2 for r in rows)), 1e-12) for e in range(d)]
+            nk = [max(math.sqrt(sum(k[r, h, c] ** 2 for r in rows)), 1e-12) for c in range(d)]
+            G = [[tau[h] * sum(q[r, h, e] * k[r, h, c] for r in rows) / (nq[e] * nk[c]) for c in range(d)]
+                 for e in range(d)]
+            A = [[1.0 / sum(math.exp(G[e][c2] - G[e][c]) for c2 in range(d)) for c in range(d)]
+                 for e in range(d)]
+            for r in rows:
+                for e in range(d):
+                    out[r, h, e] = sum(A[e][c] * v[r, h, c] for c in range(d))
+    return out
+
+
+def xca_pin_failures(xca, seg):
+    """Pins for ``xca(q, k, v, tau, offsets, perm) -> [n, H, d]`` (Tab. 7, XCA row)."""
+    fails = []
+
+    def run(ids, q, k, v, tau, W):
+        perm, offs, _ = seg(ids, W)
+        return xca(q, k, v, tau, offs, perm)
+
+    # 1. brute force on tiny shuffled scenes
+    for seed in range(3):
+        ids, q, k, v, _ = tiny_case(seed, windows=4, max_len=6, heads=2, d=3)
+        tau = np.array([0.7, 2.5])
+        if rel_err(run(ids, q, k, v, tau, 4), brute_xca(q, k, v, tau, ids, 4)) > 1e-12:
+            fails.append(f"xca_brute[{seed}]")
+    # 2. tau = 0: every softmax row is uniform, o_i[e] = mean_c v_ic
+    ids, q, k, v, _ = tiny_case(7, windows=3, max_len=5, heads=2, d=4)
+    got = run(ids, q, k, v, np.zeros(2), 3)
+    ok = (ids >= 0) & (ids < 3)
+    exp = np.repeat(v.mean(axis=2, keepdims=True), 4, axis=2)
+    if rel_err(got[ok], exp[ok]) > 1e-14:
+        fails.append("xca_tau_zero")
+    # 3. v constant across channels: o_i[e] = v_i (each softmax row sums to 1 over c)
+    vc = np.repeat(v[:, :, :1], 4, axis=2)
+    if rel_err(run(ids, q, k, vc, np.array([1.5, -3.0]), 3)[ok], vc[ok]) > 1e-13:
+        fails.append("xca_rows_sum_to_one")
+    # 4. orthonormal structure: q columns s_e U_e and k columns with khat_{pi(e)} = U_e
+    #    (pi a 3-cycle on the first three channels), so G[e][c] = tau [c = pi(e)] and
+    #    o_i[e] = (e^tau v_i,pi(e) + sum_{c != pi(e)} v_ic) / (e^tau + d - 1)
+    rng = np.random.default_rng(5)
+    m, d, H = 6, 4, 2
+    pi = [1, 2, 0, 3]
+    qs = np.zeros((m, H, d))
+    ks = np.zeros((m, H, d))
+    tau = np.array([2.0, -1.25])
+    for h in range(H):
+        U, _ = np.linalg.qr(rng.standard_normal((m, d)))
+        s = rng.uniform(0.5, 3.0, size=d)
+        t = rng.uniform(0.5, 3.0, size=d)
+        for e in range(d):
+            qs[:, h, e] = s[e] * U[:, e]
+            ks[:, h, pi[e]] = t[pi[e]] * U[:, e]
+    vs = rng.standard_normal((m, H, d))
+    got = run(np.zeros(m, dtype=np.int64), qs, ks, vs, tau, 1)
+    exp = np.empty((m, H, d))
+    for h in range(H):
+        big = math.exp(tau[h])
+        for e in range(d):
+            rest = vs[:, h, :].sum(axis=1) - vs[:, h, pi[e]]
+            exp[:, h, e] = (big * vs[:, h, pi[e]] + rest) / (big + d - 1)
+    if rel_err(got, exp) > 1e-12:
+        fails.append("xca_orthonormal_closed_form")
+    # 5. a zero q column: its normalised column is zero, so its softmax row is uniform
+    q0 = q.copy()
+    q0[:, :, 2] = 0.0
+    got = run(ids, q0, k, v, np.array([1.5, -3.0]), 3)
+    if rel_err(got[ok][:, :, 2], v[ok].mean(axis=2)) > 1e-14:
+        fails.append("xca_zero_column")
+    # 6. windows are independent and rows may come in any order
+    p = np.random.default_rng(6).permutation(len(ids))
+    base = run(ids, q, k, v, np.array([1.5, -3.0]), 3)
+    if not np.array_equal(np.isnan(run(ids[p], q[p], k[p], v[p], np.array([1.5, -3.0]), 3)),
+                          np.isnan(base[p])) or \
+            rel_err(run(ids[p], q[p], k[p], v[p], np.array([1.5, -3.0]), 3)[ok[p]], base[p][ok[p]]) > 1e-13:
+        fails.append("xca_row_permutation")
+    return fails

@@ -413,3 +413,29 @@ def test_cwi_backward_mutant_is_caught(name):
     with np.errstate(all="ignore"):
         fails = pins.cwi_backward_pin_failures(mod.cwi_backward_ref, oracle.cwi_forward_ref)
     assert fails, f"planted mistake {name} passed every CWI backward pin"
+
+
+# ------------------------------------------------------------------ XCA variant
+def test_xca_pins():
+    assert pins.xca_pin_failures(oracle.xca_forward_ref, oracle.segments_ref) == []
+
+
+XCA_MUTANTS = {
+    "softmax_over_rows": [("G = G - G.max(axis=1, keepdims=True)", "G = G - G.max(axis=0, keepdims=True)", 0),
+                          ("A = A / A.sum(axis=1, keepdims=True)", "A = A / A.sum(axis=0, keepdims=True)", 0)],
+    "attention_transposed": [("out[rows, h, :] = v[rows, h, :] @ A.T", "out[rows, h, :] = v[rows, h, :] @ A", 0)],
+    "q_not_normalised": [("qhat = qw / qn", "qhat = qw", 0)],
+    "norm_over_channels": [("kn = np.maximum(np.sqrt((kw * kw).sum(axis=0)), XCA_NORM_FLOOR)",
+                            "kn = np.maximum(np.sqrt((kw * kw).sum(axis=1, keepdims=True)), XCA_NORM_FLOOR)", 0)],
+    "first_head_temperature": [("G = tau[h] * (qhat.T @ khat)", "G = tau[0] * (qhat.T @ khat)", 0)],
+    "no_norm_floor": [("qn = np.maximum(np.sqrt((qw * qw).sum(axis=0)), XCA_NORM_FLOOR)",
+                       "qn = np.sqrt((qw * qw).sum(axis=0))", 0)],
+}
+
+
+@pytest.mark.parametrize("name", sorted(XCA_MUTANTS))
+def test_xca_mutant_is_caught(name):
+    mod = _oracle_from_source(XCA_MUTANTS[name])
+    with np.errstate(all="ignore"):
+        fails = pins.xca_pin_failures(mod.xca_forward_ref, oracle.segments_ref)
+    assert fails, f"planted mistake {name} passed every XCA pin"
