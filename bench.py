@@ -57,6 +57,9 @@ def parse():
     p.add_argument("--cwi", action="store_true",
                    help="time the cross-window interaction (cell table build + forward) on a Waymo-like "
                         "pillar frame")
+    p.add_argument("--xca", action="store_true",
+                   help="time the XCA variant (sla_forward_xca) beside sla_forward on one frame, plan "
+                        "built outside the timed region")
     p.add_argument("--compare-scatter", action="store_true",
                    help="instead of the training step: forward time and memory of the chunk-wise path "
                         "against the naive scatter-based one, as sequence length and window length grow")
@@ -240,6 +243,9 @@ def main():
         return
     if args.projected:
         print(json.dumps(bench_projected(torch, sla, workloads, dev, args)), flush=True)
+        return
+    if args.xca:
+        print(json.dumps(bench_xca(torch, sla, workloads, dev, args)), flush=True)
         return
 
     cfg = args.config
@@ -616,6 +622,69 @@ def bench_cwi(torch, sla, workloads, dev, args):
     if args.copy_probe:
         copy_probe(torch, dev)
     return out
+
+
+def bench_xca(torch, sla, workloads, dev, args):
+    """The XCA variant on one frame (Waymo-like by default; --config 2, 3 or 4),
+    rows shuffled, plan built outside the timed region, beside sla_forward on the
+    same buffers; graph replay over rotated buffer sets."""
+    cfg = args.config if args.config in (2, 3, 4) else 2
+    base = workloads.make_config(cfg, with_grad=False)
+    n, H, d, W, dt = base["n"], base["heads"], base["head_dim"], base["num_windows"], base["dtype"]
+    tdt = {"f16": torch.float16, "bf16": torch.bfloat16}[dt]
+    e = 2
+    per_set = 4 * n * H * d * e
+    nsets = max(3, int(np.ceil(2 * MALL_BYTES / per_set)) + 1)
+    tau = torch.linspace(0.5, 3.0, H, dtype=torch.float32, device=dev)
+    sets = []
+    for s_ in range(nsets):
+        wl = workloads.shuffled(base, [cfg, 2, s_])
+        st = {key: torch.from_numpy(np.ascontiguousarray(wl[key])).view(tdt).to(dev) if dt == "bf16"
+              else torch.from_numpy(np.ascontiguousarray(wl[key])).to(dev) for key in ("q", "k", "v")}
+        st["plan"] = sla.build_segments(torch.from_numpy(wl["ids"]).to(dev), num_windows=W, want_perm=False)
+        st["o"] = torch.empty_like(st["q"])
+        sets.append(st)
+    torch.cuda.synchronize()
+
+    def timed(fn, reps):
+        for i in range(args.warmup):
+            fn(sets[i % nsets])
+        torch.cuda.synchronize()
+        graphs = []
+        cap = torch.cuda.Stream(dev)
+        cap.wait_stream(torch.cuda.current_stream(dev))
+        with torch.cuda.stream(cap):
+            for s_ in range(nsets):
+                g = torch.cuda.CUDAGraph()
+                with torch.cuda.graph(g, stream=cap):
+                    fn(sets[s_])
+                graphs.append(g)
+        torch.cuda.current_stream(dev).wait_stream(cap)
+        for g in graphs:
+            g.replay()
+        torch.cuda.synchronize()
+        t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        t0.record()
+        for i in range(reps):
+            graphs[i % nsets].replay()
+        t1.record()
+        torch.cuda.synchronize()
+        return t0.elapsed_time(t1) / reps * 1e3
+
+    reps = max(50, args.steps)
+    t_xca = timed(lambda st: sla.forward_xca(st["plan"], st["q"], st["k"], st["v"], tau, out=st["o"]), reps)
+    t_sla = timed(lambda st: sla.forward(st["plan"], st["q"], st["k"], st["v"], out=st["o"]), reps)
+    nbytes = 4 * n * H * d * e + 4 * n   # q, k, v read and o written once, plus the permutation
+    return {
+        "mode": "xca",
+        "workload": base["name"],
+        "n": n, "heads": H, "head_dim": d, "num_windows": W, "dtype": dt, "buffer_sets": nsets,
+        "xca_us": t_xca,
+        "sla_forward_us": t_sla,
+        "xca_algorithmic_bytes": nbytes,
+        "xca_gbs": nbytes / (t_xca * 1e-6) / 1e9,
+        "xca_frac_of_hbm_peak": nbytes / (t_xca * 1e-6) / 1e9 / HBM_PEAK_GBS,
+    }
 
 
 def bench_projected(torch, sla, workloads, dev, args):

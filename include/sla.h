@@ -312,6 +312,25 @@ sla_status_t sla_forward_scatter(const void* plan, size_t plan_bytes, int64_t n,
                                  void* o, void* workspace, size_t workspace_bytes,
                                  sla_stream_t stream);
 
+/*
+ * The XCA design of the linear-attention ablation (Sec. 4.5, Tab. 7), which
+ * cites cross-covariance attention (XCiT), applied inside every window of the
+ * plan.  For window w and head h, with the window's q and k columns normalised
+ * over the window's rows (qhat[:, e] = q[:, e] / max(|q[:, e]|_2, 1e-12), k
+ * likewise):
+ *     A[e][c] = softmax over c of  tau[h] qhat[:, e] . khat[:, c]   (d x d),
+ *     o_i[e]  = sum_c A[e][c] v_i[c]                               for i in w.
+ * tau: device float [heads], the per-head temperatures (4-byte aligned).  Same
+ * plan, row layouts, dtypes and errors as sla_forward (rows in no window are
+ * not written), plus SLA_E_UNSUPPORTED when num_windows x heads x 256 exceeds
+ * 2^32 - 1 (one 256-thread workgroup per window and head).  fp32 arithmetic on
+ * the vector units; outputs rounded to `dtype`.  Forward only.
+ */
+sla_status_t sla_forward_xca(const void* plan, size_t plan_bytes, int64_t n, int32_t num_windows,
+                             sla_dtype_t dtype, int32_t heads, int32_t head_dim, const float* tau,
+                             const void* q, const void* k, const void* v, void* o,
+                             sla_stream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

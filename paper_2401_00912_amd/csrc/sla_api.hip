@@ -36,11 +36,14 @@ hipError_t launch_cwi_backward(const int32_t* map, int32_t gx, int32_t gy, int32
 hipError_t launch_forward_scatter(const void* plan, int32_t n, int32_t W, int dtype, int32_t H,
                                   int32_t d, const void* q, const void* k, const void* v,
                                   void* o, void* workspace, hipStream_t stream);
+hipError_t launch_forward_xca(const void* plan, int32_t n, int32_t W, int dtype, int32_t H, int32_t d,
+                              const float* tau, const void* q, const void* k, const void* v, void* o,
+                              hipStream_t stream);
 }  // namespace sla
 
 namespace {
 
-constexpr int32_t kAbiVersion = 7;
+constexpr int32_t kAbiVersion = 8;
 
 // cells of a CWI grid, or -1 when a side is not positive or the grid has more
 // than INT32_MAX cells
@@ -250,6 +253,22 @@ SLA_EXPORT sla_status_t sla_forward_scatter(const void* plan, size_t plan_bytes,
   return hip_status(sla::launch_forward_scatter(plan, (int32_t)n, num_windows, (int)dtype, heads,
                                                 head_dim, q, k, v, o, workspace,
                                                 static_cast<hipStream_t>(stream)));
+}
+
+SLA_EXPORT sla_status_t sla_forward_xca(const void* plan, size_t plan_bytes, int64_t n,
+                                        int32_t num_windows, sla_dtype_t dtype, int32_t heads,
+                                        int32_t head_dim, const float* tau, const void* q,
+                                        const void* k, const void* v, void* o, sla_stream_t stream) {
+  const sla_status_t st = check_tensor_args(n, num_windows, (int)dtype, heads, head_dim, plan, plan_bytes);
+  if (st != SLA_OK) return st;
+  // one 256-thread workgroup per (window, head): the launch's work-items must fit 32 bits
+  if ((int64_t)num_windows * heads * 256 > (int64_t)UINT32_MAX) return SLA_E_UNSUPPORTED;
+  if (n == 0) return SLA_OK;
+  if (!tau || !q || !k || !v || !o) return SLA_E_ARG;
+  if (!aligned(tau, 4) || !aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(o, 16))
+    return SLA_E_ARG;
+  return hip_status(sla::launch_forward_xca(plan, (int32_t)n, num_windows, (int)dtype, heads, head_dim,
+                                            tau, q, k, v, o, static_cast<hipStream_t>(stream)));
 }
 
 SLA_EXPORT size_t sla_cwi_map_bytes(int32_t gx, int32_t gy, int32_t gz) {

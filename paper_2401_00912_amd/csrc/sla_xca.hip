@@ -1,0 +1,269 @@
+// Cross-covariance attention inside every window: the XCA design of the
+// linear-attention ablation (Sec. 4.5, Tab. 7), which cites XCiT, run on the
+// same window-sorted plan as SLA.  For window w and head h, with the window's q
+// and k columns L2-normalised over the window's rows (norms floored at 1e-12):
+//     A[e][c] = softmax over c of  tau_h qhat[:, e] . khat[:, c]     (d x d),
+//     o_i[e]  = sum_c A[e][c] v_i[c]                                 for i in w.
+// Like Eq. (3) it needs one d x d reduction over the window's rows per head,
+// here q^T k together with the column norms, and then one d x d product per row.
+//
+// k_xca_fwd: one workgroup per (window, head).
+//   1. 64 rows at a time, the window's q and k rows (this head's d columns)
+//      are gathered through the plan's permutation into LDS in fp32; thread
+//      (e, c-block) accumulates G[e][c] = sum_r q_re k_rc for its EPT columns,
+//      and the first wave the squared column norms.
+//   2. The logits tau G[e][c] / (|q_e| |k_c|) are bounded by |tau|, so the
+//      softmax needs no overflow guard beyond the usual max shift; the row max
+//      and sum are reduced over the CPR threads of a row with lane xors.
+//   3. Each thread keeps one row e of A in registers and, 64 rows at a time
+//      with the v rows in LDS, writes o_i[e] for its rows.  A window of at most
+//      64 rows gathers its v rows in step 1 already, into registers, so that
+//      their round trip overlaps the sums; longer windows gather v again here.
+// fp32 throughout; inputs widened from the storage type, outputs rounded to it.
+#include "sla_common.h"
+
+namespace sla {
+namespace {
+
+constexpr int kXcaThreads = 256;
+constexpr int kXcaRows = 64;   // rows staged in LDS at a time
+
+template <typename T>
+struct XcaIo;
+template <>
+struct XcaIo<float> {
+  static constexpr int kPiece = 4;   // elements per 16-byte piece
+  __device__ static void unpack(uint4 u, float (&x)[4]) {
+    x[0] = __uint_as_float(u.x); x[1] = __uint_as_float(u.y);
+    x[2] = __uint_as_float(u.z); x[3] = __uint_as_float(u.w);
+  }
+  __device__ static void store(float* p, float x) { *p = x; }
+};
+template <>
+struct XcaIo<_Float16> {
+  static constexpr int kPiece = 8;
+  __device__ static void unpack(uint4 u, float (&x)[8]) {
+    const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      x[2 * j] = (float)__builtin_bit_cast(_Float16, (unsigned short)(w[j] & 0xffffu));
+      x[2 * j + 1] = (float)__builtin_bit_cast(_Float16, (unsigned short)(w[j] >> 16));
+    }
+  }
+  __device__ static void store(_Float16* p, float x) { *p = (_Float16)x; }
+};
+template <>
+struct XcaIo<bf16_t> {
+  static constexpr int kPiece = 8;
+  __device__ static void unpack(uint4 u, float (&x)[8]) {
+    const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      x[2 * j] = __uint_as_float(w[j] << 16);
+      x[2 * j + 1] = __uint_as_float(w[j] & 0xffff0000u);
+    }
+  }
+  __device__ static void store(bf16_t* p, float x) {
+    p->bits = __builtin_bit_cast(unsigned short, (__bf16)x);
+  }
+};
+
+// LDS row stride of the staged rows: 16-byte aligned rows for float4 reads
+template <int D>
+constexpr int kXcaLd = D + 4;
+
+// 16-byte pieces of a staged block: piece j = (row r, piece pc); a thread takes
+// pieces tid, tid + 256 (at most two: 64 rows of 32 fp32 columns)
+template <typename T, int D>
+constexpr int kXcaPieces = kXcaRows * D / XcaIo<T>::kPiece;
+template <typename T, int D>
+constexpr int kXcaPerThread = (kXcaPieces<T, D> + kXcaThreads - 1) / kXcaThreads;
+
+// Gathers the raw pieces of rows [p0, p0 + nr) (sorted positions) of `x` into
+// registers (zero past nr or for an out-of-range row) and, when s_row is given,
+// records each row's original index there (-1 for none).
+template <typename T, int D>
+__device__ __forceinline__ void xca_fetch(const int32_t* pm, int32_t p0, int nr, int32_t n,
+                                          size_t rs, int col, const T* x,
+                                          uint4 (&raw)[kXcaPerThread<T, D>], int32_t* s_row) {
+  constexpr int PB = XcaIo<T>::kPiece, PR = D / PB;
+#pragma unroll
+  for (int u = 0; u < kXcaPerThread<T, D>; ++u) {
+    const int j = (int)threadIdx.x + u * kXcaThreads;
+    const int r = j / PR, pc = j - r * PR;
+    int32_t row = -1;
+    if (j < kXcaPieces<T, D> && r < nr) {
+      row = pm ? pm[p0 + r] : p0 + r;
+      if ((uint32_t)row >= (uint32_t)n) row = -1;
+    }
+    raw[u] = row >= 0 ? *reinterpret_cast<const uint4*>(x + (size_t)row * rs + col + pc * PB)
+                      : make_uint4(0, 0, 0, 0);
+    if (s_row && j < kXcaPieces<T, D> && pc == 0) s_row[r] = row;
+  }
+}
+
+// Raw pieces into an LDS block of fp32 rows.
+template <typename T, int D>
+__device__ __forceinline__ void xca_put(const uint4 (&raw)[kXcaPerThread<T, D>],
+                                        float (*a)[kXcaLd<D>]) {
+  constexpr int PB = XcaIo<T>::kPiece, PR = D / PB;
+#pragma unroll
+  for (int u = 0; u < kXcaPerThread<T, D>; ++u) {
+    const int j = (int)threadIdx.x + u * kXcaThreads;
+    if (j < kXcaPieces<T, D>) {
+      const int r = j / PR, pc = j - r * PR;
+      float x[PB];
+      XcaIo<T>::unpack(raw[u], x);
+#pragma unroll
+      for (int e = 0; e < PB; ++e) a[r][pc * PB + e] = x[e];
+    }
+  }
+}
+
+template <typename T, int D>
+__global__ __launch_bounds__(kXcaThreads) void k_xca_fwd(
+    const PlanHeader* __restrict__ hdr, const int32_t* __restrict__ perm,
+    const int32_t* __restrict__ offs, const float* __restrict__ tau, const T* __restrict__ q,
+    const T* __restrict__ k, const T* __restrict__ v, T* __restrict__ o, int32_t n, int32_t W,
+    int32_t H) {
+  constexpr int EPT = D * D / kXcaThreads;   // entries (e, c) per thread: 4 (d = 32) or 1 (d = 16)
+  constexpr int CPR = D / EPT;               // threads per row e of G
+  constexpr int RPP = kXcaThreads / D;       // output rows per pass of phase 3
+  static_assert(D * D % kXcaThreads == 0 && CPR <= 64 && (CPR & (CPR - 1)) == 0, "row groups");
+  constexpr int LD = kXcaLd<D>;
+  constexpr int NP = kXcaPerThread<T, D>;
+  __shared__ __align__(16) float s_a[kXcaRows][LD];   // q rows, then v rows
+  __shared__ __align__(16) float s_b[kXcaRows][LD];   // k rows
+  __shared__ float s_g[D][D + 1];          // softmax weights A
+  __shared__ float s_nrm[2 * D];           // |q_e|, then |k_c|
+  __shared__ int32_t s_row[kXcaRows];
+  if (hdr->magic != kPlanMagic || hdr->n != n || hdr->num_windows != W) return;
+  const int32_t w = (int32_t)(blockIdx.x / (uint32_t)H), h = (int32_t)(blockIdx.x - (uint32_t)w * H);
+  const int32_t* pm = hdr->csr ? nullptr : perm;
+  const int32_t rb = max(0, min(offs[w], n)), re = max(rb, min(offs[w + 1], n));
+  if (rb == re) return;
+  const int tid = (int)threadIdx.x;
+  const size_t rs = (size_t)H * D;
+  const int col = h * D;
+
+  // 1. G = q^T k over the window's rows, and the squared column norms
+  const int e = tid / CPR, c0 = (tid - e * CPR) * EPT;
+  float acc[EPT];
+#pragma unroll
+  for (int u = 0; u < EPT; ++u) acc[u] = 0.f;
+  float nrm = 0.f;
+  // a window of at most one block also gathers its v rows now, into registers,
+  // so that their round trip overlaps the q^T k sums
+  const bool one = re - rb <= kXcaRows;
+  uint4 vr[NP];
+  for (int32_t p0 = rb; p0 < re; p0 += kXcaRows) {
+    const int nr = min(kXcaRows, re - p0);
+    if (p0 != rb) __syncthreads();   // the previous block's readers are done
+    {
+      uint4 qr[NP], kr[NP];
+      xca_fetch<T, D>(pm, p0, nr, n, rs, col, q, qr, s_row);
+      xca_fetch<T, D>(pm, p0, nr, n, rs, col, k, kr, nullptr);
+      if (one) xca_fetch<T, D>(pm, p0, nr, n, rs, col, v, vr, nullptr);
+      xca_put<T, D>(qr, s_a);
+      xca_put<T, D>(kr, s_b);
+    }
+    __syncthreads();
+    for (int r = 0; r < nr; ++r) {
+      const float a = s_a[r][e];
+#pragma unroll
+      for (int u = 0; u < EPT; ++u) acc[u] += a * s_b[r][c0 + u];
+    }
+    // the first wave sums the squared columns (q in lanes 0..D-1, k after)
+    if (tid < D) {
+      for (int r = 0; r < nr; ++r) nrm += s_a[r][tid] * s_a[r][tid];
+    } else if (tid < 2 * D) {
+      for (int r = 0; r < nr; ++r) nrm += s_b[r][tid - D] * s_b[r][tid - D];
+    }
+  }
+  if (tid < 2 * D) s_nrm[tid] = fmaxf(sqrtf(nrm), 1e-12f);
+  __syncthreads();
+
+  // 2. softmax of each row e over c
+  const float t = tau[h];
+  float g[EPT];
+  float mx = -3.0e38f;
+#pragma unroll
+  for (int u = 0; u < EPT; ++u) {
+    g[u] = t * acc[u] / (s_nrm[e] * s_nrm[D + c0 + u]);
+    mx = fmaxf(mx, g[u]);
+  }
+#pragma unroll
+  for (int m = 1; m < CPR; m <<= 1) mx = fmaxf(mx, __shfl_xor(mx, m, 64));
+  float sum = 0.f;
+#pragma unroll
+  for (int u = 0; u < EPT; ++u) {
+    g[u] = expf(g[u] - mx);
+    sum += g[u];
+  }
+#pragma unroll
+  for (int m = 1; m < CPR; m <<= 1) sum += __shfl_xor(sum, m, 64);
+  const float inv = 1.f / sum;
+#pragma unroll
+  for (int u = 0; u < EPT; ++u) s_g[e][c0 + u] = g[u] * inv;
+  // s_a's last readers (the q^T k sums) passed the barrier above
+  if (one) xca_put<T, D>(vr, s_a);
+  __syncthreads();
+
+  // 3. o_i[e3] = sum_c A[e3][c] v_i[c]
+  const int e3 = tid % D, r3 = tid / D;
+  float arow[D];
+#pragma unroll
+  for (int c = 0; c < D; ++c) arow[c] = s_g[e3][c];
+  for (int32_t p0 = rb; p0 < re; p0 += kXcaRows) {
+    const int nr = min(kXcaRows, re - p0);
+    if (!one) {
+      __syncthreads();   // s_a and s_row are free
+      uint4 raw[NP];
+      xca_fetch<T, D>(pm, p0, nr, n, rs, col, v, raw, s_row);
+      xca_put<T, D>(raw, s_a);
+      __syncthreads();
+    }
+    for (int r = r3; r < nr; r += RPP) {
+      const int32_t row = s_row[r];
+      float s = 0.f;
+#pragma unroll
+      for (int c = 0; c < D; c += 4) {
+        const float4 x = *reinterpret_cast<const float4*>(&s_a[r][c]);
+        s += arow[c] * x.x + arow[c + 1] * x.y + arow[c + 2] * x.z + arow[c + 3] * x.w;
+      }
+      if (row >= 0) XcaIo<T>::store(o + (size_t)row * rs + col + e3, s);
+    }
+  }
+}
+
+template <typename T, int D>
+hipError_t xca_impl(const void* plan, int32_t n, int32_t W, int32_t H, const float* tau,
+                    const void* q, const void* k, const void* v, void* o, hipStream_t stream) {
+  const PlanLayout lay = plan_layout(n, W);
+  const char* base = static_cast<const char*>(plan);
+  hipLaunchKernelGGL((k_xca_fwd<T, D>), dim3((unsigned)((int64_t)W * H)), dim3(kXcaThreads), 0, stream,
+                     reinterpret_cast<const PlanHeader*>(base + lay.header),
+                     reinterpret_cast<const int32_t*>(base + lay.perm),
+                     reinterpret_cast<const int32_t*>(base + lay.offsets), tau,
+                     static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v),
+                     static_cast<T*>(o), n, W, H);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+// dtype: 0 f32, 1 f16, 2 bf16; d: 16 or 32
+hipError_t launch_forward_xca(const void* plan, int32_t n, int32_t W, int dtype, int32_t H, int32_t d,
+                              const float* tau, const void* q, const void* k, const void* v, void* o,
+                              hipStream_t stream) {
+  if (d == 32) {
+    if (dtype == 0) return xca_impl<float, 32>(plan, n, W, H, tau, q, k, v, o, stream);
+    if (dtype == 1) return xca_impl<_Float16, 32>(plan, n, W, H, tau, q, k, v, o, stream);
+    return xca_impl<bf16_t, 32>(plan, n, W, H, tau, q, k, v, o, stream);
+  }
+  if (dtype == 0) return xca_impl<float, 16>(plan, n, W, H, tau, q, k, v, o, stream);
+  if (dtype == 1) return xca_impl<_Float16, 16>(plan, n, W, H, tau, q, k, v, o, stream);
+  return xca_impl<bf16_t, 16>(plan, n, W, H, tau, q, k, v, o, stream);
+}
+
+}  // namespace sla

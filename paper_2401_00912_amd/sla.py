@@ -53,6 +53,7 @@ EXPORTED = (
     "sla_cwi_backward",
     "sla_scatter_workspace_bytes",
     "sla_forward_scatter",
+    "sla_forward_xca",
 )
 
 
@@ -127,6 +128,8 @@ def lib() -> ctypes.CDLL:
     L.sla_scatter_workspace_bytes.argtypes = [i64, i32, i32]
     L.sla_forward_scatter.restype = ctypes.c_int
     L.sla_forward_scatter.argtypes = [vp, sz, i64, i32, ctypes.c_int, i32, i32, vp, vp, vp, vp, vp, sz, vp]
+    L.sla_forward_xca.restype = ctypes.c_int
+    L.sla_forward_xca.argtypes = [vp, sz, i64, i32, ctypes.c_int, i32, i32, vp, vp, vp, vp, vp, vp]
     _lib = L
     return L
 
@@ -295,6 +298,25 @@ def backward(plan: Plan, q, k, v, dout, dq=None, dk=None, dv=None, feature_map=N
                                    _ptr(dout), _ptr(dq), _ptr(dk), _ptr(dv), _stream(q.device))
         _check(st, "sla_backward_ex")
     return dq, dk, dv
+
+
+def forward_xca(plan: Plan, q, k, v, tau, out=None):
+    """XCA inside every window (sla_forward_xca); tau: float32 [heads] on q's device."""
+    torch = _torch()
+    _check_rows("q", q, plan.n)
+    _check_rows("k", k, plan.n, q)
+    _check_rows("v", v, plan.n, q)
+    H, d = q.shape[1], q.shape[2]
+    if (tau.dtype != torch.float32 or tau.dim() != 1 or tau.shape[0] != H or not tau.is_contiguous()
+            or tau.device != q.device):
+        raise ValueError("tau must be a contiguous float32 [heads] tensor on q's device")
+    if out is None:
+        out = torch.empty_like(q)
+    _check_rows("out", out, plan.n, q)
+    st = lib().sla_forward_xca(_ptr(plan.buf), plan.nbytes, plan.n, plan.num_windows, _dtype_code(q.dtype),
+                               H, d, _ptr(tau), _ptr(q), _ptr(k), _ptr(v), _ptr(out), _stream(q.device))
+    _check(st, "sla_forward_xca")
+    return out
 
 
 def forward_projected(plan: Plan, x, w_qkv, w_o, heads: int, b_qkv=None, b_o=None, o=None, y=None,

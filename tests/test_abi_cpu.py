@@ -46,7 +46,7 @@ def test_only_the_abi_is_exported():
 
 
 def test_queries(L):
-    assert L.sla_abi_version() == 7
+    assert L.sla_abi_version() == 8
     assert L.sla_max_windows() == 16384
     assert L.sla_default_chunk_rows() == 64
     for s in range(5):
@@ -141,6 +141,25 @@ def test_scatter_argument_errors(L):
     big = L.sla_forward_scatter(FAKE, sla.plan_bytes(100, 8), 100, 8, 1, 128, 32, FAKE, FAKE, FAKE,
                                 FAKE, FAKE, sla.scatter_workspace_bytes(100, 128, 32), None)
     assert big == sla.SLA_E_UNSUPPORTED
+
+
+def test_xca_argument_errors(L):
+    nb = sla.plan_bytes(100, 8)
+    call = lambda **kw: L.sla_forward_xca(  # noqa: E731
+        kw.get("plan", FAKE), kw.get("pb", nb), kw.get("n", 100), kw.get("W", 8), kw.get("dt", 1),
+        kw.get("H", 4), kw.get("d", 32), kw.get("tau", FAKE), FAKE, FAKE, FAKE, kw.get("o", FAKE), None)
+    assert call(tau=None) == sla.SLA_E_ARG
+    assert call(tau=FAKE + 2) == sla.SLA_E_ARG      # tau is float32: 4-byte aligned
+    assert call(o=FAKE + 8) == sla.SLA_E_ARG
+    assert call(o=None) == sla.SLA_E_ARG
+    assert call(d=24) == sla.SLA_E_UNSUPPORTED
+    assert call(dt=3) == sla.SLA_E_ARG
+    assert call(pb=10) == sla.SLA_E_WORKSPACE
+    assert call(plan=FAKE + 64) == sla.SLA_E_ARG
+    assert call(n=0) == sla.SLA_OK
+    assert call(n=0, tau=None) == sla.SLA_OK          # nothing to do, nothing read
+    # one 256-thread workgroup per (window, head): 16384 windows x 1024 heads is too many
+    assert call(W=16384, H=1024, d=16, pb=sla.plan_bytes(100, 16384)) == sla.SLA_E_UNSUPPORTED
 
 
 def test_variant_argument_errors(L):

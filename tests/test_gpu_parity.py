@@ -900,3 +900,87 @@ def test_cwi_tiled_edges(sla, grid, density):
     w_x, w_y, w_3 = (cast(rng.standard_normal((k, c)) / np.sqrt(k)) for k in (13, 13, 27))
     cwi_parity(sla, coords, grid, x, w_x, w_y, w_3, "f16", label=f"edge{grid}")
     cwi_backward_parity(sla, coords, grid, x, w_x, w_y, w_3, dy, "f16", label=f"edge{grid}")
+
+
+# ------------------------------------------------------------------ XCA variant
+def xca_parity(S, ids, offsets, n, W, q, k, v, tau, dtype, label=""):
+    import torch
+
+    plan = build(S, ids=ids, W=W, offsets=offsets, n=n)
+    off, perm = check_plan(S, plan, ids, W, 0, offsets)
+    tq, tk, tv = (to_dev(a, dtype) for a in (q, k, v))
+    tau32 = np.asarray(tau, dtype=np.float32)
+    o = torch.full_like(tq, float("nan"))
+    S.forward_xca(plan, tq, tk, tv, torch.from_numpy(tau32).to(tq.device), out=o)
+    torch.cuda.synchronize()
+    got = to_host64(o, dtype)
+    w = lambda a: oracle.widen(a, dtype)  # noqa: E731
+    ref = oracle.xca_forward_ref(w(q), w(k), w(v), tau32.astype(np.float64), off, perm)
+    rows = np.zeros(n, dtype=bool)
+    rows[perm if perm is not None else np.arange(off[-1])] = True
+    assert np.isnan(got[~rows]).all(), f"{label}: a row in no window was written"
+    floor = 1e-3 * max(float(np.abs(w(v)).max()) if v.size else 1.0, 1e-30)
+    err = rel_err_per_head(got, ref, floor, rows)
+    _say(f"[xca {label}] n={n} W={W} dtype={dtype} rel_err={err:.3e}")
+    assert err <= TOL[dtype], f"{label}: XCA relative error {err:.3e}"
+    return got, ref
+
+
+def _xca_tau(H):
+    return np.linspace(-1.5, 4.0, H) if H > 1 else np.array([2.0])
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4])
+def test_xca_config(sla, cfg):
+    wl = workloads.make_config(cfg)
+    H = wl["q"].shape[1]
+    xca_parity(sla, wl["ids"], wl["offsets"], wl["n"], wl["num_windows"], wl["q"], wl["k"], wl["v"],
+               _xca_tau(H), wl["dtype"], label=f"cfg{cfg}")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "f16", "bf16"])
+@pytest.mark.parametrize("shape", [(2, 32), (8, 16), (3, 32), (1, 16)])
+def test_xca_shapes(sla, dtype, shape):
+    # empty windows, singletons, windows of 63/64/65 rows (one and two LDS
+    # blocks) and one of 1024 rows (16 blocks)
+    H, d = shape
+    rng = np.random.default_rng([43, H, d, len(dtype)])
+    lengths = _adversarial_lengths(rng, 64)
+    ids = workloads.ids_from_lengths(lengths, rng)
+    n, W = ids.size, lengths.size
+    q, k, v = (workloads.normal_values(rng, n, H, d, dtype) for _ in range(3))
+    xca_parity(sla, ids, None, n, W, q, k, v, _xca_tau(H), dtype, label=f"shape{shape}")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "f16"])
+def test_xca_degenerate(sla, dtype):
+    # a zero q column (its norm takes the floor: a uniform softmax row), a zero k
+    # column, tau = 0 in one head and a sharp softmax (tau = 40) in another, and
+    # rows with invalid window ids (in no window: left unwritten)
+    rng = np.random.default_rng([44, len(dtype)])
+    H, d = 4, 32
+    lengths = np.array([5, 1, 70, 0, 33, 2], dtype=np.int64)
+    ids = workloads.ids_from_lengths(lengths, rng)
+    ids = np.concatenate([ids, np.array([-1, 6, 99], dtype=ids.dtype)])
+    n, W = ids.size, lengths.size
+    q, k, v = (workloads.normal_values(rng, n, H, d, dtype) for _ in range(3))
+    q[:, 1, 7] = 0
+    k[:, 2, 30] = 0
+    xca_parity(sla, ids, None, n, W, q, k, v, np.array([0.0, 40.0, 1.0, -3.0]), dtype, label="degenerate")
+
+
+def test_xca_rows_in_order_and_csr(sla):
+    # CSR plan (rows already window-sorted, no permutation) against the same
+    # scene through ids: the same outputs, bit for bit
+    import torch
+
+    wl = workloads.make_config(1)
+    offs = wl["offsets"]
+    n, W = wl["n"], wl["num_windows"]
+    got_csr, _ = xca_parity(sla, None, offs, n, W, wl["q"], wl["k"], wl["v"], _xca_tau(wl["q"].shape[1]),
+                            wl["dtype"], label="csr")
+    ids = np.repeat(np.arange(W), np.diff(offs)).astype(np.int32)
+    got_ids, _ = xca_parity(sla, ids, None, n, W, wl["q"], wl["k"], wl["v"], _xca_tau(wl["q"].shape[1]),
+                            wl["dtype"], label="ids")
+    assert np.array_equal(got_csr, got_ids)
+    torch.cuda.synchronize()
