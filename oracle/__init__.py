@@ -18,5 +18,6 @@ from .sla_ref import (  # noqa: F401
     sla_forward_ref,
     sla_projected_forward_ref,
     widen,
+    xca_backward_ref,
     xca_forward_ref,
 )

@@ -67,6 +67,9 @@ What is computed, and the passage it follows
   matrix per window and head; tau_h is the head's learned temperature, an
   input here), and o_i[e] = sum_c A[e, c] v_i[c] for every row i of the window.
   It needs the same per-window d x d reduction over the window's rows as Eq. (3).
+* ``xca_backward_ref``: its gradients with respect to q, k, v and the
+  temperatures, by the chain rule (the paper trains the model with XCA but does
+  not write them out).
 * ``cwi_backward_ref``: the gradients of that module with respect to its input
   and its three kernels, by the chain rule (the paper trains the model but does
   not write them out).
@@ -91,6 +94,7 @@ __all__ = [
     "cwi_forward_ref",
     "cwi_backward_ref",
     "xca_forward_ref",
+    "xca_backward_ref",
 ]
 
 
@@ -499,3 +503,59 @@ def xca_forward_ref(q, k, v, tau, offsets, perm=None):
             A = A / A.sum(axis=1, keepdims=True)
             out[rows, h, :] = v[rows, h, :] @ A.T        # o_i[e] = sum_c A[e, c] v_i[c]
     return out
+
+
+def xca_backward_ref(q, k, v, tau, dout, offsets, perm=None):
+    """Gradients of ``xca_forward_ref``: (dq, dk, dv [n, H, d], dtau [H]).
+
+    Per window and head, with m rows, Qh = q / nq and Kh = k / nk column-wise
+    (nq_e = max(|q[:, e]|, 1e-12)), N = Qh^T Kh, G = tau N, A = softmax_c(G),
+    o_i = A v_i:
+        dv_i   = A^T do_i                     dA = sum_i do_i v_i^T
+        dG     = A * (dA - rowsum(A * dA))    (softmax backward, rows e)
+        dtau  += sum_{e,c} dG[e, c] N[e, c]   (over every window)
+        dQh    = tau Kh dG^T                  dKh = tau Qh dG
+        dq[:, e] = (dQh[:, e] - Qh[:, e] (Qh[:, e] . dQh[:, e])) / nq_e   when |q[:, e]| > 1e-12,
+                 = dQh[:, e] / 1e-12                                        otherwise (the floor
+                                                                            is a constant there);
+        likewise dk from dKh.
+    Rows that belong to no window are NaN in dq, dk, dv.
+    """
+    q = np.asarray(q, dtype=np.float64)
+    k = np.asarray(k, dtype=np.float64)
+    v = np.asarray(v, dtype=np.float64)
+    do = np.asarray(dout, dtype=np.float64)
+    tau = np.asarray(tau, dtype=np.float64)
+    n, H, d = q.shape
+    dq = np.full(q.shape, np.nan)
+    dk = np.full(q.shape, np.nan)
+    dv = np.full(q.shape, np.nan)
+    dtau = np.zeros(H)
+
+    def unnormalise(x, xh, nx, dxh):
+        raw = np.sqrt((x * x).sum(axis=0))
+        proj = dxh - xh * (xh * dxh).sum(axis=0)
+        return np.where(raw > XCA_NORM_FLOOR, proj, dxh) / nx
+
+    for w in range(len(offsets) - 1):
+        rows = _window_rows(offsets, perm, w)
+        if rows.size == 0:
+            continue
+        for h in range(H):
+            qw, kw, vw, dow = q[rows, h, :], k[rows, h, :], v[rows, h, :], do[rows, h, :]
+            nq = np.maximum(np.sqrt((qw * qw).sum(axis=0)), XCA_NORM_FLOOR)
+            nk = np.maximum(np.sqrt((kw * kw).sum(axis=0)), XCA_NORM_FLOOR)
+            qh, kh = qw / nq, kw / nk
+            N = qh.T @ kh
+            G = tau[h] * N
+            A = np.exp(G - G.max(axis=1, keepdims=True))
+            A = A / A.sum(axis=1, keepdims=True)
+            dv[rows, h, :] = dow @ A                   # dv_i[c] = sum_e A[e, c] do_i[e]
+            dA = dow.T @ vw                            # dA[e, c] = sum_i do_i[e] v_i[c]
+            dG = A * (dA - (A * dA).sum(axis=1, keepdims=True))
+            dtau[h] += (dG * N).sum()
+            dqh = tau[h] * (kh @ dG.T)                 # [m, d]: dqh[r, e] = tau sum_c dG[e, c] kh[r, c]
+            dkh = tau[h] * (qh @ dG)                   # dkh[r, c] = tau sum_e dG[e, c] qh[r, e]
+            dq[rows, h, :] = unnormalise(qw, qh, nq, dqh)
+            dk[rows, h, :] = unnormalise(kw, kh, nk, dkh)
+    return dq, dk, dv, dtau

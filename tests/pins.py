@@ -740,3 +740,64 @@ def xca_pin_failures(xca, seg):
             rel_err(run(ids[p], q[p], k[p], v[p], np.array([1.5, -3.0]), 3)[ok[p]], base[p][ok[p]]) > 1e-13:
         fails.append("xca_row_permutation")
     return fails
+
+
+def xca_backward_pin_failures(xca_bwd, xca_fwd, seg):
+    """Pins for ``xca_bwd(q, k, v, tau, dout, offsets, perm) -> (dq, dk, dv, dtau)``
+    against the pinned forward: central differences of L = <dout, o>, the adjoint
+    identity in v, and the invariance of o to a positive scale of any q or k
+    column within a window."""
+    fails = []
+    ids, q, k, v, do = tiny_case(11, windows=4, max_len=6, heads=2, d=3)
+    W = 4
+    tau = np.array([1.3, -2.1])
+    perm, offs, _ = seg(ids, W)
+    dq, dk, dv, dtau = xca_bwd(q, k, v, tau, do, offs, perm)
+
+    def loss(q_, k_, v_, t_):
+        o = xca_fwd(q_, k_, v_, t_, offs, perm)
+        ok = ~np.isnan(o[:, 0, 0])
+        return float((do[ok] * o[ok]).sum())
+
+    # 1. central differences on every entry of q, k, v (of rows in a window) and of tau
+    rows = np.nonzero((ids >= 0) & (ids < W))[0]
+    step = 1e-6
+    for name, arr, grad in (("q", q, dq), ("k", k, dk), ("v", v, dv)):
+        num = np.zeros_like(arr)
+        for r in rows:
+            for h in range(arr.shape[1]):
+                for e in range(arr.shape[2]):
+                    a1, a2 = arr.copy(), arr.copy()
+                    a1[r, h, e] += step
+                    a2[r, h, e] -= step
+                    args1 = {"q": q, "k": k, "v": v}
+                    args2 = dict(args1)
+                    args1[name], args2[name] = a1, a2
+                    num[r, h, e] = (loss(args1["q"], args1["k"], args1["v"], tau)
+                                    - loss(args2["q"], args2["k"], args2["v"], tau)) / (2 * step)
+        if rel_err(grad[rows], num[rows]) > 1e-6:
+            fails.append(f"xca_bwd_fd_{name}")
+    num_tau = np.array([(loss(q, k, v, tau + step * np.eye(2)[h]) - loss(q, k, v, tau - step * np.eye(2)[h]))
+                        / (2 * step) for h in range(2)])
+    if rel_err(dtau, num_tau) > 1e-6:
+        fails.append("xca_bwd_fd_tau")
+    # 2. o is linear in v: <dout, o> = <dv, v>
+    if abs(loss(q, k, v, tau) - float((dv[rows] * v[rows]).sum())) > 1e-12 * max(1.0, abs(loss(q, k, v, tau))):
+        fails.append("xca_bwd_adjoint_v")
+    # 3. scaling a q (or k) column of one window leaves o unchanged, so the
+    #    gradient along that column vanishes: sum_r dq[r, e] q[r, e] = 0 per window
+    worst = 0.0
+    for w in range(W):
+        rw = np.nonzero(ids == w)[0]
+        if rw.size == 0:
+            continue
+        for x, g in ((q, dq), (k, dk)):
+            dots = (g[rw] * x[rw]).sum(axis=0)
+            worst = max(worst, float(np.abs(dots).max()) / max(float(np.abs(g[rw]).max()), 1e-300))
+    if worst > 1e-12:
+        fails.append("xca_bwd_scale_invariance")
+    # 4. rows in no window get no gradient (NaN)
+    bad = np.nonzero((ids < 0) | (ids >= W))[0]
+    if bad.size and not all(np.isnan(g[bad]).all() for g in (dq, dk, dv)):
+        fails.append("xca_bwd_rows_outside")
+    return fails

@@ -439,3 +439,27 @@ def test_xca_mutant_is_caught(name):
     with np.errstate(all="ignore"):
         fails = pins.xca_pin_failures(mod.xca_forward_ref, oracle.segments_ref)
     assert fails, f"planted mistake {name} passed every XCA pin"
+
+
+def test_xca_backward_pins():
+    assert pins.xca_backward_pin_failures(oracle.xca_backward_ref, oracle.xca_forward_ref,
+                                          oracle.segments_ref) == []
+
+
+XCA_BWD_MUTANTS = {
+    "dv_transposed": [("dv[rows, h, :] = dow @ A", "dv[rows, h, :] = dow @ A.T", 0)],
+    "softmax_backward_without_row_term": [("dG = A * (dA - (A * dA).sum(axis=1, keepdims=True))",
+                                           "dG = A * dA", 0)],
+    "normalisation_backward_without_projection": [("proj = dxh - xh * (xh * dxh).sum(axis=0)",
+                                                   "proj = dxh", 0)],
+    "dtau_from_logits": [("dtau[h] += (dG * N).sum()", "dtau[h] += (dG * G).sum()", 0)],
+    "dkh_transposed": [("dkh = tau[h] * (qh @ dG)", "dkh = tau[h] * (qh @ dG.T)", 0)],
+}
+
+
+@pytest.mark.parametrize("name", sorted(XCA_BWD_MUTANTS))
+def test_xca_backward_mutant_is_caught(name):
+    mod = _oracle_from_source(XCA_BWD_MUTANTS[name])
+    with np.errstate(all="ignore"):
+        fails = pins.xca_backward_pin_failures(mod.xca_backward_ref, oracle.xca_forward_ref, oracle.segments_ref)
+    assert fails, f"planted mistake {name} passed every XCA backward pin"
