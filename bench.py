@@ -625,9 +625,10 @@ def bench_cwi(torch, sla, workloads, dev, args):
 
 
 def bench_xca(torch, sla, workloads, dev, args):
-    """The XCA variant on one frame (Waymo-like by default; --config 2, 3 or 4),
-    rows shuffled, plan built outside the timed region, beside sla_forward on the
-    same buffers; graph replay over rotated buffer sets."""
+    """The XCA variant, forward and backward, on one frame (Waymo-like by default;
+    --config 2, 3 or 4), rows shuffled, plan built outside the timed region,
+    beside sla_forward on the same buffers; graph replay over rotated buffer
+    sets."""
     cfg = args.config if args.config in (2, 3, 4) else 2
     base = workloads.make_config(cfg, with_grad=False)
     n, H, d, W, dt = base["n"], base["heads"], base["head_dim"], base["num_windows"], base["dtype"]
@@ -643,6 +644,10 @@ def bench_xca(torch, sla, workloads, dev, args):
               else torch.from_numpy(np.ascontiguousarray(wl[key])).to(dev) for key in ("q", "k", "v")}
         st["plan"] = sla.build_segments(torch.from_numpy(wl["ids"]).to(dev), num_windows=W, want_perm=False)
         st["o"] = torch.empty_like(st["q"])
+        st["do"] = torch.randn(st["q"].shape, device=dev).to(tdt)
+        st["grads"] = [torch.empty_like(st["q"]) for _ in range(3)]
+        st["dtau"] = torch.empty(H, dtype=torch.float32, device=dev)
+        st["ws"] = torch.empty(sla.lib().sla_xca_backward_workspace_bytes(W, H), dtype=torch.uint8, device=dev)
         sets.append(st)
     torch.cuda.synchronize()
 
@@ -674,7 +679,10 @@ def bench_xca(torch, sla, workloads, dev, args):
     reps = max(50, args.steps)
     t_xca = timed(lambda st: sla.forward_xca(st["plan"], st["q"], st["k"], st["v"], tau, out=st["o"]), reps)
     t_sla = timed(lambda st: sla.forward(st["plan"], st["q"], st["k"], st["v"], out=st["o"]), reps)
+    t_bwd = timed(lambda st: sla.backward_xca(st["plan"], st["q"], st["k"], st["v"], tau, st["do"], *st["grads"],
+                                              dtau=st["dtau"], workspace=st["ws"]), reps)
     nbytes = 4 * n * H * d * e + 4 * n   # q, k, v read and o written once, plus the permutation
+    bwd_bytes = 7 * n * H * d * e + 4 * n   # q, k, v, dout read and dq, dk, dv written once, plus the permutation
     return {
         "mode": "xca",
         "workload": base["name"],
@@ -684,6 +692,9 @@ def bench_xca(torch, sla, workloads, dev, args):
         "xca_algorithmic_bytes": nbytes,
         "xca_gbs": nbytes / (t_xca * 1e-6) / 1e9,
         "xca_frac_of_hbm_peak": nbytes / (t_xca * 1e-6) / 1e9 / HBM_PEAK_GBS,
+        "xca_backward_us": t_bwd,
+        "xca_backward_algorithmic_bytes": bwd_bytes,
+        "xca_backward_gbs": bwd_bytes / (t_bwd * 1e-6) / 1e9,
     }
 
 

@@ -331,6 +331,30 @@ sla_status_t sla_forward_xca(const void* plan, size_t plan_bytes, int64_t n, int
                              const void* q, const void* k, const void* v, void* o,
                              sla_stream_t stream);
 
+/*
+ * Backward of sla_forward_xca (the chain rule; the paper does not write it):
+ * given dout, writes dq, dk, dv for every row in a window and dtau[heads] (fp32,
+ * device, 4-byte aligned), the gradient of the temperatures summed over the
+ * windows.  With N = qhat^T khat and A the softmax of tau N, per window and head:
+ *     dv_i = A^T dout_i,   dA = sum_i dout_i v_i^T,
+ *     dG = A * (dA - rowsum(A * dA)),   dtau += sum dG * N,
+ *     dqhat = tau khat dG^T, dkhat = tau qhat dG, and through the
+ *     normalisation dq[:, e] = (dqhat[:, e] - qhat[:, e] (qhat[:, e] . dqhat[:, e])) / |q[:, e]|
+ *     (a column whose norm took the 1e-12 floor gets dqhat[:, e] / 1e-12), dk alike.
+ * `workspace` (caller-owned, 4-byte aligned, at least
+ * sla_xca_backward_workspace_bytes(num_windows, heads) bytes) receives one fp32
+ * partial of dtau per (window, head); the partials are then added in window
+ * order, so dtau is deterministic.  Errors as sla_forward_xca, plus
+ * SLA_E_WORKSPACE for a short workspace.  With n = 0, dtau is zero.
+ */
+size_t sla_xca_backward_workspace_bytes(int32_t num_windows, int32_t heads);
+
+sla_status_t sla_backward_xca(const void* plan, size_t plan_bytes, int64_t n, int32_t num_windows,
+                              sla_dtype_t dtype, int32_t heads, int32_t head_dim, const float* tau,
+                              const void* q, const void* k, const void* v, const void* dout,
+                              void* dq, void* dk, void* dv, float* dtau, void* workspace,
+                              size_t workspace_bytes, sla_stream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -236,6 +236,264 @@ __global__ __launch_bounds__(kXcaThreads) void k_xca_fwd(
   }
 }
 
+// ---------------------------------------------------------------- backward
+// Chain rule of the forward, per (window, head) workgroup, with
+// N = qhat^T khat, G = tau N and A = softmax_c(G):
+//   dv_i = A^T do_i,  dA = sum_i do_i v_i^T,  dG = A * (dA - rowsum(A * dA)),
+//   dtau partial = sum dG * N,
+//   dq[:, e] = (sum_c B_q[e][c] k[:, c] - q[:, e] s_e / nq_e) / nq_e with
+//   B_q[e][c] = tau dG[e][c] / nk_c and s_e = tau sum_c dG[e][c] N[e][c] (the
+//   projection of d qhat onto qhat, read off the d x d sums instead of a pass
+//   over the rows; zero where the norm took the floor), and likewise dk with
+//   B_k[e][c] = tau dG[e][c] / nq_e and t_c = tau sum_e dG[e][c] N[e][c].
+// Passes over the window's rows: q, k (N, as in the forward); dout, v (dA and
+// dv); q, k again (dq, dk).  The temperature gradient of every (window, head)
+// goes to `part`; k_xca_dtau adds the windows in order.
+template <typename T, int D>
+__global__ __launch_bounds__(kXcaThreads) void k_xca_bwd(
+    const PlanHeader* __restrict__ hdr, const int32_t* __restrict__ perm,
+    const int32_t* __restrict__ offs, const float* __restrict__ tau, const T* __restrict__ q,
+    const T* __restrict__ k, const T* __restrict__ v, const T* __restrict__ dout,
+    T* __restrict__ dq, T* __restrict__ dk, T* __restrict__ dv, float* __restrict__ part,
+    int32_t n, int32_t W, int32_t H) {
+  constexpr int EPT = D * D / kXcaThreads;
+  constexpr int CPR = D / EPT;
+  constexpr int RPP = kXcaThreads / D;
+  constexpr int LD = kXcaLd<D>;
+  constexpr int NP = kXcaPerThread<T, D>;
+  constexpr int NW = kXcaThreads / 64;
+  __shared__ __align__(16) float s_a[kXcaRows][LD];
+  __shared__ __align__(16) float s_b[kXcaRows][LD];
+  __shared__ float s_g[D][D + 1];    // A, then tau dG * N
+  __shared__ float s_dg[D][D + 1];   // dG
+  __shared__ float s_nrm[2 * D];     // nq, nk
+  __shared__ float s_st[2 * D];      // s_e, t_c
+  __shared__ float s_red[NW];
+  __shared__ int32_t s_row[kXcaRows];
+  const int tid = (int)threadIdx.x;
+  const int32_t b = (int32_t)blockIdx.x;
+  if (hdr->magic != kPlanMagic || hdr->n != n || hdr->num_windows != W) {
+    if (tid == 0) part[b] = 0.f;
+    return;
+  }
+  const int32_t w = (int32_t)((uint32_t)b / (uint32_t)H), h = b - w * H;
+  const int32_t* pm = hdr->csr ? nullptr : perm;
+  const int32_t rb = max(0, min(offs[w], n)), re = max(rb, min(offs[w + 1], n));
+  if (rb == re) {
+    if (tid == 0) part[b] = 0.f;
+    return;
+  }
+  const size_t rs = (size_t)H * D;
+  const int col = h * D;
+  const float t = tau[h];
+
+  // 1. N = qhat^T khat (raw sums and column norms), A
+  const int e = tid / CPR, c0 = (tid - e * CPR) * EPT;
+  float acc[EPT];
+#pragma unroll
+  for (int u = 0; u < EPT; ++u) acc[u] = 0.f;
+  float nrm = 0.f;
+  for (int32_t p0 = rb; p0 < re; p0 += kXcaRows) {
+    const int nr = min(kXcaRows, re - p0);
+    if (p0 != rb) __syncthreads();
+    {
+      uint4 qr[NP], kr[NP];
+      xca_fetch<T, D>(pm, p0, nr, n, rs, col, q, qr, s_row);
+      xca_fetch<T, D>(pm, p0, nr, n, rs, col, k, kr, nullptr);
+      xca_put<T, D>(qr, s_a);
+      xca_put<T, D>(kr, s_b);
+    }
+    __syncthreads();
+    for (int r = 0; r < nr; ++r) {
+      const float x = s_a[r][e];
+#pragma unroll
+      for (int u = 0; u < EPT; ++u) acc[u] += x * s_b[r][c0 + u];
+    }
+    if (tid < D) {
+      for (int r = 0; r < nr; ++r) nrm += s_a[r][tid] * s_a[r][tid];
+    } else if (tid < 2 * D) {
+      for (int r = 0; r < nr; ++r) nrm += s_b[r][tid - D] * s_b[r][tid - D];
+    }
+  }
+  if (tid < 2 * D) s_nrm[tid] = fmaxf(sqrtf(nrm), 1e-12f);
+  __syncthreads();
+  float nn[EPT], a[EPT];
+  float mx = -3.0e38f;
+#pragma unroll
+  for (int u = 0; u < EPT; ++u) {
+    nn[u] = acc[u] / (s_nrm[e] * s_nrm[D + c0 + u]);
+    a[u] = t * nn[u];
+    mx = fmaxf(mx, a[u]);
+  }
+#pragma unroll
+  for (int m = 1; m < CPR; m <<= 1) mx = fmaxf(mx, __shfl_xor(mx, m, 64));
+  float sum = 0.f;
+#pragma unroll
+  for (int u = 0; u < EPT; ++u) {
+    a[u] = expf(a[u] - mx);
+    sum += a[u];
+  }
+#pragma unroll
+  for (int m = 1; m < CPR; m <<= 1) sum += __shfl_xor(sum, m, 64);
+  const float inv = 1.f / sum;
+#pragma unroll
+  for (int u = 0; u < EPT; ++u) {
+    a[u] *= inv;
+    s_g[e][c0 + u] = a[u];
+  }
+  __syncthreads();
+
+  // 2. dA = sum_i do_i v_i^T, and dv_i[x3] = sum_e A[e][x3] do_i[e]
+  const int x3 = tid % D, r3 = tid / D;
+  float acl[D];
+#pragma unroll
+  for (int j = 0; j < D; ++j) acl[j] = s_g[j][x3];
+  float da[EPT];
+#pragma unroll
+  for (int u = 0; u < EPT; ++u) da[u] = 0.f;
+  for (int32_t p0 = rb; p0 < re; p0 += kXcaRows) {
+    const int nr = min(kXcaRows, re - p0);
+    __syncthreads();   // s_a, s_b, s_row (and s_g's column reads) are done with
+    {
+      uint4 dr[NP], vr[NP];
+      xca_fetch<T, D>(pm, p0, nr, n, rs, col, dout, dr, s_row);
+      xca_fetch<T, D>(pm, p0, nr, n, rs, col, v, vr, nullptr);
+      xca_put<T, D>(dr, s_a);
+      xca_put<T, D>(vr, s_b);
+    }
+    __syncthreads();
+    for (int r = 0; r < nr; ++r) {
+      const float x = s_a[r][e];
+#pragma unroll
+      for (int u = 0; u < EPT; ++u) da[u] += x * s_b[r][c0 + u];
+    }
+    for (int r = r3; r < nr; r += RPP) {
+      const int32_t row = s_row[r];
+      float s = 0.f;
+#pragma unroll
+      for (int j = 0; j < D; j += 4) {
+        const float4 x = *reinterpret_cast<const float4*>(&s_a[r][j]);
+        s += acl[j] * x.x + acl[j + 1] * x.y + acl[j + 2] * x.z + acl[j + 3] * x.w;
+      }
+      if (row >= 0) XcaIo<T>::store(dv + (size_t)row * rs + col + x3, s);
+    }
+  }
+
+  // 3. dG, the temperature partial, s_e and t_c
+  float rsum = 0.f;
+#pragma unroll
+  for (int u = 0; u < EPT; ++u) rsum += a[u] * da[u];
+#pragma unroll
+  for (int m = 1; m < CPR; m <<= 1) rsum += __shfl_xor(rsum, m, 64);
+  float dg[EPT], pt = 0.f, srow = 0.f;
+#pragma unroll
+  for (int u = 0; u < EPT; ++u) {
+    dg[u] = a[u] * (da[u] - rsum);
+    pt += dg[u] * nn[u];
+  }
+  srow = pt;
+#pragma unroll
+  for (int m = 1; m < CPR; m <<= 1) srow += __shfl_xor(srow, m, 64);   // sum_c dG N over row e
+  // the workgroup's sum of dG * N: the rows' sums, wave by wave, in order
+  float wsum = (tid - e * CPR) == 0 ? srow : 0.f;
+#pragma unroll
+  for (int m = 1; m < 64; m <<= 1) wsum += __shfl_xor(wsum, m, 64);
+  __syncthreads();   // the last block's readers of s_a, s_b and every reader of s_g are done
+  if ((tid & 63) == 0) s_red[tid >> 6] = wsum;
+  if (c0 == 0) s_st[e] = s_nrm[e] > 1e-12f ? t * srow : 0.f;
+#pragma unroll
+  for (int u = 0; u < EPT; ++u) {
+    s_dg[e][c0 + u] = dg[u];
+    s_g[e][c0 + u] = dg[u] * nn[u];
+  }
+  __syncthreads();
+  if (tid == 0) {
+    float tot = 0.f;
+#pragma unroll
+    for (int j = 0; j < NW; ++j) tot += s_red[j];
+    part[b] = tot;
+  }
+  if (tid < D) {
+    float cs = 0.f;
+    for (int j = 0; j < D; ++j) cs += s_g[j][tid];
+    s_st[D + tid] = s_nrm[D + tid] > 1e-12f ? t * cs : 0.f;
+  }
+  __syncthreads();
+
+  // 4. dq[:, x3] and dk[:, x3]
+  float bq[D], bk[D];
+#pragma unroll
+  for (int j = 0; j < D; ++j) {
+    bq[j] = t * s_dg[x3][j] / s_nrm[D + j];
+    bk[j] = t * s_dg[j][x3] / s_nrm[j];
+  }
+  const float iq = 1.f / s_nrm[x3], ik = 1.f / s_nrm[D + x3];
+  const float sq = s_st[x3] * iq, tk = s_st[D + x3] * ik;
+  for (int32_t p0 = rb; p0 < re; p0 += kXcaRows) {
+    const int nr = min(kXcaRows, re - p0);
+    __syncthreads();
+    {
+      uint4 qr[NP], kr[NP];
+      xca_fetch<T, D>(pm, p0, nr, n, rs, col, q, qr, s_row);
+      xca_fetch<T, D>(pm, p0, nr, n, rs, col, k, kr, nullptr);
+      xca_put<T, D>(qr, s_a);
+      xca_put<T, D>(kr, s_b);
+    }
+    __syncthreads();
+    for (int r = r3; r < nr; r += RPP) {
+      const int32_t row = s_row[r];
+      float gq = 0.f, gk = 0.f;
+#pragma unroll
+      for (int j = 0; j < D; j += 4) {
+        const float4 kx = *reinterpret_cast<const float4*>(&s_b[r][j]);
+        const float4 qx = *reinterpret_cast<const float4*>(&s_a[r][j]);
+        gq += bq[j] * kx.x + bq[j + 1] * kx.y + bq[j + 2] * kx.z + bq[j + 3] * kx.w;
+        gk += bk[j] * qx.x + bk[j + 1] * qx.y + bk[j + 2] * qx.z + bk[j + 3] * qx.w;
+      }
+      if (row >= 0) {
+        XcaIo<T>::store(dq + (size_t)row * rs + col + x3, (gq - s_a[r][x3] * sq) * iq);
+        XcaIo<T>::store(dk + (size_t)row * rs + col + x3, (gk - s_b[r][x3] * tk) * ik);
+      }
+    }
+  }
+}
+
+// dtau[h] = sum over windows, in window order, of the (window, head) partials:
+// 256 strided sums, then a fixed tree.
+__global__ __launch_bounds__(kXcaThreads) void k_xca_dtau(const float* __restrict__ part, int32_t W,
+                                                         int32_t H, float* __restrict__ dtau) {
+  __shared__ float s[kXcaThreads];
+  const int h = (int)blockIdx.x, tid = (int)threadIdx.x;
+  float x = 0.f;
+  for (int32_t w = tid; w < W; w += kXcaThreads) x += part[(size_t)w * H + h];
+  s[tid] = x;
+  __syncthreads();
+  for (int m = kXcaThreads / 2; m > 0; m >>= 1) {
+    if (tid < m) s[tid] += s[tid + m];
+    __syncthreads();
+  }
+  if (tid == 0) dtau[h] = s[0];
+}
+
+template <typename T, int D>
+hipError_t xca_bwd_impl(const void* plan, int32_t n, int32_t W, int32_t H, const float* tau,
+                        const void* q, const void* k, const void* v, const void* dout, void* dq,
+                        void* dk, void* dv, float* dtau, float* part, hipStream_t stream) {
+  const PlanLayout lay = plan_layout(n, W);
+  const char* base = static_cast<const char*>(plan);
+  hipLaunchKernelGGL((k_xca_bwd<T, D>), dim3((unsigned)((int64_t)W * H)), dim3(kXcaThreads), 0, stream,
+                     reinterpret_cast<const PlanHeader*>(base + lay.header),
+                     reinterpret_cast<const int32_t*>(base + lay.perm),
+                     reinterpret_cast<const int32_t*>(base + lay.offsets), tau,
+                     static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v),
+                     static_cast<const T*>(dout), static_cast<T*>(dq), static_cast<T*>(dk),
+                     static_cast<T*>(dv), part, n, W, H);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_xca_dtau, dim3((unsigned)H), dim3(kXcaThreads), 0, stream, part, W, H, dtau);
+  return hipGetLastError();
+}
+
 template <typename T, int D>
 hipError_t xca_impl(const void* plan, int32_t n, int32_t W, int32_t H, const float* tau,
                     const void* q, const void* k, const void* v, void* o, hipStream_t stream) {
@@ -264,6 +522,20 @@ hipError_t launch_forward_xca(const void* plan, int32_t n, int32_t W, int dtype,
   if (dtype == 0) return xca_impl<float, 16>(plan, n, W, H, tau, q, k, v, o, stream);
   if (dtype == 1) return xca_impl<_Float16, 16>(plan, n, W, H, tau, q, k, v, o, stream);
   return xca_impl<bf16_t, 16>(plan, n, W, H, tau, q, k, v, o, stream);
+}
+
+hipError_t launch_backward_xca(const void* plan, int32_t n, int32_t W, int dtype, int32_t H, int32_t d,
+                               const float* tau, const void* q, const void* k, const void* v,
+                               const void* dout, void* dq, void* dk, void* dv, float* dtau, float* part,
+                               hipStream_t stream) {
+  if (d == 32) {
+    if (dtype == 0) return xca_bwd_impl<float, 32>(plan, n, W, H, tau, q, k, v, dout, dq, dk, dv, dtau, part, stream);
+    if (dtype == 1) return xca_bwd_impl<_Float16, 32>(plan, n, W, H, tau, q, k, v, dout, dq, dk, dv, dtau, part, stream);
+    return xca_bwd_impl<bf16_t, 32>(plan, n, W, H, tau, q, k, v, dout, dq, dk, dv, dtau, part, stream);
+  }
+  if (dtype == 0) return xca_bwd_impl<float, 16>(plan, n, W, H, tau, q, k, v, dout, dq, dk, dv, dtau, part, stream);
+  if (dtype == 1) return xca_bwd_impl<_Float16, 16>(plan, n, W, H, tau, q, k, v, dout, dq, dk, dv, dtau, part, stream);
+  return xca_bwd_impl<bf16_t, 16>(plan, n, W, H, tau, q, k, v, dout, dq, dk, dv, dtau, part, stream);
 }
 
 }  // namespace sla

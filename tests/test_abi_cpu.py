@@ -162,6 +162,26 @@ def test_xca_argument_errors(L):
     assert call(W=16384, H=1024, d=16, pb=sla.plan_bytes(100, 16384)) == sla.SLA_E_UNSUPPORTED
 
 
+def test_xca_backward_argument_errors(L):
+    nb = sla.plan_bytes(100, 8)
+    assert L.sla_xca_backward_workspace_bytes(8, 4) == 8 * 4 * 4
+    assert L.sla_xca_backward_workspace_bytes(0, 4) == 0
+    need = 8 * 4 * 4
+    call = lambda **kw: L.sla_backward_xca(  # noqa: E731
+        FAKE, kw.get("pb", nb), kw.get("n", 100), 8, 1, 4, kw.get("d", 32), kw.get("tau", FAKE), FAKE, FAKE,
+        FAKE, FAKE, FAKE, FAKE, kw.get("dv", FAKE), kw.get("dtau", FAKE), kw.get("ws", FAKE),
+        kw.get("wsb", need), None)
+    assert call(wsb=need - 1) == sla.SLA_E_WORKSPACE
+    assert call(ws=None) == sla.SLA_E_ARG
+    assert call(dtau=None) == sla.SLA_E_ARG
+    assert call(dtau=FAKE + 2) == sla.SLA_E_ARG
+    assert call(tau=None) == sla.SLA_E_ARG
+    assert call(dv=FAKE + 8) == sla.SLA_E_ARG
+    assert call(dv=None) == sla.SLA_E_ARG
+    assert call(d=24) == sla.SLA_E_UNSUPPORTED
+    assert call(pb=10) == sla.SLA_E_WORKSPACE
+
+
 def test_variant_argument_errors(L):
     nb = sla.plan_bytes(100, 8)
     f = lambda fm, eps, **kw: L.sla_forward_ex(  # noqa: E731

@@ -986,3 +986,84 @@ def test_xca_rows_in_order_and_csr(sla):
                             wl["dtype"], label="ids")
     assert np.array_equal(got_csr, got_ids)
     torch.cuda.synchronize()
+
+
+# ------------------------------------------------------------ XCA backward
+# dq and dk pass through the softmax backward and the normalisation's projection,
+# two differences of nearly equal terms, so fp32 gets 1e-4 there (dv, a plain
+# product with A, keeps the forward's 1e-5); dtau sums signed terms over every
+# window and is held to 1e-3 of the largest head's value.
+XCA_BWD_TOL = {"f32": 1e-4, "f16": 2e-2, "bf16": 2e-2}
+
+
+def xca_backward_parity(S, ids, offsets, n, W, q, k, v, do, tau, dtype, label=""):
+    import torch
+
+    plan = build(S, ids=ids, W=W, offsets=offsets, n=n)
+    off, perm = check_plan(S, plan, ids, W, 0, offsets)
+    tq, tk, tv, tdo = (to_dev(a, dtype) for a in (q, k, v, do))
+    tau32 = np.asarray(tau, dtype=np.float32)
+    outs = [torch.full_like(tq, float("nan")) for _ in range(3)]
+    dq, dk, dv, dtau = S.backward_xca(plan, tq, tk, tv, torch.from_numpy(tau32).to(tq.device), tdo, *outs)
+    torch.cuda.synchronize()
+    got = [to_host64(t, dtype) for t in (dq, dk, dv)]
+    w = lambda a: oracle.widen(a, dtype)  # noqa: E731
+    ref = oracle.xca_backward_ref(w(q), w(k), w(v), tau32.astype(np.float64), w(do), off, perm)
+    rows = np.zeros(n, dtype=bool)
+    rows[perm if perm is not None else np.arange(off[-1])] = True
+    for name, x, r in zip(("dq", "dk", "dv"), got, ref[:3]):
+        assert np.isnan(x[~rows]).all(), f"{label}: {name} written outside every window"
+        err = rel_err_per_head(x, r, 1e-30, rows)
+        tol = TOL[dtype] if name == "dv" else XCA_BWD_TOL[dtype]
+        _say(f"[xca-bwd {label}] {name} n={n} dtype={dtype} rel_err={err:.3e}")
+        assert err <= tol, f"{label}: {name} relative error {err:.3e}"
+    dt = dtau.cpu().numpy().astype(np.float64)
+    derr = float(np.abs(dt - ref[3]).max()) / max(float(np.abs(ref[3]).max()), 1e-30)
+    _say(f"[xca-bwd {label}] dtau rel_err={derr:.3e}")
+    assert derr <= 1e-3, f"{label}: dtau relative error {derr:.3e}"
+    return got, dt
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3])
+def test_xca_backward_config(sla, cfg):
+    wl = workloads.make_config(cfg)
+    H = wl["q"].shape[1]
+    do = workloads.normal_values(np.random.default_rng([cfg, 9]), wl["n"], H, wl["q"].shape[2], wl["dtype"])
+    xca_backward_parity(sla, wl["ids"], wl["offsets"], wl["n"], wl["num_windows"], wl["q"], wl["k"], wl["v"],
+                        do, np.linspace(0.5, 3.0, H), wl["dtype"], label=f"cfg{cfg}")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "f16", "bf16"])
+@pytest.mark.parametrize("shape", [(2, 32), (8, 16), (3, 32)])
+def test_xca_backward_shapes(sla, dtype, shape):
+    H, d = shape
+    rng = np.random.default_rng([45, H, d, len(dtype)])
+    lengths = _adversarial_lengths(rng, 64)
+    ids = workloads.ids_from_lengths(lengths, rng)
+    n, W = ids.size, lengths.size
+    q, k, v, do = (workloads.normal_values(rng, n, H, d, dtype) for _ in range(4))
+    tau = np.linspace(-1.5, 4.0, H) + 0.25
+    xca_backward_parity(sla, ids, None, n, W, q, k, v, do, tau, dtype, label=f"shape{shape}")
+
+
+def test_xca_backward_deterministic_and_empty(sla):
+    import torch
+
+    rng = np.random.default_rng(46)
+    lengths = np.array([40, 0, 130, 1, 64], dtype=np.int64)
+    ids = workloads.ids_from_lengths(lengths, rng)
+    n, W, H, d = ids.size, lengths.size, 4, 32
+    q, k, v, do = (workloads.normal_values(rng, n, H, d, "f16") for _ in range(4))
+    tau = np.array([1.0, 2.0, -0.5, 3.0])
+    a = xca_backward_parity(sla, ids, None, n, W, q, k, v, do, tau, "f16", label="determinism")
+    b = xca_backward_parity(sla, ids, None, n, W, q, k, v, do, tau, "f16", label="determinism")
+    for x, y in zip(a[0], b[0]):
+        assert np.array_equal(x, y, equal_nan=True)
+    assert np.array_equal(a[1], b[1])
+    # n = 0: nothing to write, dtau is zero
+    plan = build(sla, ids=np.zeros(0, dtype=np.int32), W=3)
+    e = torch.zeros((0, 2, 16), dtype=torch.float16, device="cuda")
+    dtau = torch.full((2,), float("nan"), device="cuda")
+    sla.backward_xca(plan, e, e, e, torch.ones(2, device="cuda"), e, dtau=dtau)
+    torch.cuda.synchronize()
+    assert torch.equal(dtau.cpu(), torch.zeros(2))
