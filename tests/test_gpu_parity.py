@@ -394,7 +394,7 @@ def test_streams_share_a_plan(sla):
 
 def test_graph_replays(sla):
     # the whole path captured in one HIP graph (segment build, forward, backward,
-    # their ReLU / eps variants, the XCA variant, the fused projection, cell
+    # their ReLU / eps variants, the XCA forward and backward, the fused projection, cell
     # table, cross-window interaction forward and backward), replayed three
     # times; before each replay the outputs, the plan buffer and the cell table
     # are scribbled over by eager work, and every replay must reproduce the eager
@@ -429,13 +429,14 @@ def test_graph_replays(sla):
         o_relu = sla.forward(plan, q, k, v, feature_map="relu", eps=1e-3)
         grads_relu = sla.backward(plan, q, k, v, do, feature_map="relu", eps=1e-3)
         o_xca = sla.forward_xca(plan, q, k, v, tau)
+        g_xca = sla.backward_xca(plan, q, k, v, tau, do)
         po = torch.empty((n, H, d), dtype=torch.float16, device="cuda")
         py = torch.empty((n, C), dtype=torch.float16, device="cuda")
         sla.forward_projected(plan, xp, wq, wo, H, None, None, po, py)
         m, _ = sla.cwi_build_map(cc, grid)
         y = sla.cwi_forward(m, grid, cc, x, *w)
         back = sla.cwi_backward(m, grid, cc, x, *w, dy)
-        return plan, m, [o, *grads, o_relu, *grads_relu, o_xca, po, py, y, *back]
+        return plan, m, [o, *grads, o_relu, *grads_relu, o_xca, *g_xca, po, py, y, *back]
 
     _, _, eager = path()
     eager = [t.clone() for t in eager]
