@@ -323,7 +323,8 @@ sla_status_t sla_forward_scatter(const void* plan, size_t plan_bytes, int64_t n,
  * tau: device float [heads], the per-head temperatures (4-byte aligned).  Same
  * plan, row layouts, dtypes and errors as sla_forward (rows in no window are
  * not written), plus SLA_E_UNSUPPORTED when num_windows x heads x 256 exceeds
- * 2^32 - 1 (one 256-thread workgroup per window and head).  fp32 arithmetic on
+ * 2^32 - 1 (one 256-thread workgroup per window and head, windows padded
+ * to a multiple of 8).  fp32 arithmetic on
  * the vector units; outputs rounded to `dtype`.  Forward only.
  */
 sla_status_t sla_forward_xca(const void* plan, size_t plan_bytes, int64_t n, int32_t num_windows,

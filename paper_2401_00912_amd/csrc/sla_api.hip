@@ -265,8 +265,9 @@ SLA_EXPORT sla_status_t sla_forward_xca(const void* plan, size_t plan_bytes, int
                                         const void* k, const void* v, void* o, sla_stream_t stream) {
   const sla_status_t st = check_tensor_args(n, num_windows, (int)dtype, heads, head_dim, plan, plan_bytes);
   if (st != SLA_OK) return st;
-  // one 256-thread workgroup per (window, head): the launch's work-items must fit 32 bits
-  if ((int64_t)num_windows * heads * 256 > (int64_t)UINT32_MAX) return SLA_E_UNSUPPORTED;
+  // one 256-thread workgroup per (window, head), windows padded to a multiple of
+  // 8: the launch's work-items must fit 32 bits
+  if (((int64_t)num_windows + 7) / 8 * 8 * heads * 256 > (int64_t)UINT32_MAX) return SLA_E_UNSUPPORTED;
   if (n == 0) return SLA_OK;
   if (!tau || !q || !k || !v || !o) return SLA_E_ARG;
   if (!aligned(tau, 4) || !aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(o, 16))
@@ -288,7 +289,7 @@ SLA_EXPORT sla_status_t sla_backward_xca(const void* plan, size_t plan_bytes, in
                                          size_t workspace_bytes, sla_stream_t stream) {
   const sla_status_t st = check_tensor_args(n, num_windows, (int)dtype, heads, head_dim, plan, plan_bytes);
   if (st != SLA_OK) return st;
-  if ((int64_t)num_windows * heads * 256 > (int64_t)UINT32_MAX) return SLA_E_UNSUPPORTED;
+  if (((int64_t)num_windows + 7) / 8 * 8 * heads * 256 > (int64_t)UINT32_MAX) return SLA_E_UNSUPPORTED;
   if (!tau || !dtau || !workspace || !aligned(tau, 4) || !aligned(dtau, 4) || !aligned(workspace, 4))
     return SLA_E_ARG;
   if (workspace_bytes < sla_xca_backward_workspace_bytes(num_windows, heads)) return SLA_E_WORKSPACE;

@@ -7,7 +7,7 @@
 // Like Eq. (3) it needs one d x d reduction over the window's rows per head,
 // here q^T k together with the column norms, and then one d x d product per row.
 //
-// k_xca_fwd: one workgroup per (window, head).
+// k_xca_fwd: one workgroup per (window, head), the heads of a window on one XCD.
 //   1. 64 rows at a time, the window's q and k rows (this head's d columns)
 //      are gathered through the plan's permutation into LDS in fp32; thread
 //      (e, c-block) accumulates G[e][c] = sum_r q_re k_rc for its EPT columns,
@@ -67,6 +67,20 @@ struct XcaIo<bf16_t> {
     p->bits = __builtin_bit_cast(unsigned short, (__bf16)x);
   }
 };
+
+// Workgroup b -> (window, head) such that the heads of a window share b mod 8:
+// workgroups are dealt to the 8 XCDs round-robin, so the heads of a window run
+// on one XCD, whose L2 then serves the other heads' quarters of each row's
+// 128-byte lines.  The grid is 8 ceil(W / 8) H; workgroups past the last window
+// have nothing to do.
+__device__ __forceinline__ void xca_item(uint32_t b, int32_t H, int32_t& w, int32_t& h) {
+  const uint32_t per = 8u * (uint32_t)H;
+  const uint32_t g = b / per, r = b - g * per;
+  h = (int32_t)(r >> 3);
+  w = (int32_t)(g * 8u + (r & 7u));
+}
+
+inline unsigned xca_grid(int32_t W, int32_t H) { return (unsigned)(((int64_t)W + 7) / 8 * 8 * H); }
 
 // LDS row stride of the staged rows: 16-byte aligned rows for float4 reads
 template <int D>
@@ -137,8 +151,10 @@ __global__ __launch_bounds__(kXcaThreads) void k_xca_fwd(
   __shared__ float s_g[D][D + 1];          // softmax weights A
   __shared__ float s_nrm[2 * D];           // |q_e|, then |k_c|
   __shared__ int32_t s_row[kXcaRows];
+  int32_t w, h;
+  xca_item(blockIdx.x, H, w, h);
+  if (w >= W) return;
   if (hdr->magic != kPlanMagic || hdr->n != n || hdr->num_windows != W) return;
-  const int32_t w = (int32_t)(blockIdx.x / (uint32_t)H), h = (int32_t)(blockIdx.x - (uint32_t)w * H);
   const int32_t* pm = hdr->csr ? nullptr : perm;
   const int32_t rb = max(0, min(offs[w], n)), re = max(rb, min(offs[w + 1], n));
   if (rb == re) return;
@@ -271,12 +287,14 @@ __global__ __launch_bounds__(kXcaThreads) void k_xca_bwd(
   __shared__ float s_red[NW];
   __shared__ int32_t s_row[kXcaRows];
   const int tid = (int)threadIdx.x;
-  const int32_t b = (int32_t)blockIdx.x;
+  int32_t w, h;
+  xca_item(blockIdx.x, H, w, h);
+  if (w >= W) return;
+  const size_t b = (size_t)w * H + h;   // this (window, head)'s temperature partial
   if (hdr->magic != kPlanMagic || hdr->n != n || hdr->num_windows != W) {
     if (tid == 0) part[b] = 0.f;
     return;
   }
-  const int32_t w = (int32_t)((uint32_t)b / (uint32_t)H), h = b - w * H;
   const int32_t* pm = hdr->csr ? nullptr : perm;
   const int32_t rb = max(0, min(offs[w], n)), re = max(rb, min(offs[w + 1], n));
   if (rb == re) {
@@ -481,7 +499,7 @@ hipError_t xca_bwd_impl(const void* plan, int32_t n, int32_t W, int32_t H, const
                         void* dk, void* dv, float* dtau, float* part, hipStream_t stream) {
   const PlanLayout lay = plan_layout(n, W);
   const char* base = static_cast<const char*>(plan);
-  hipLaunchKernelGGL((k_xca_bwd<T, D>), dim3((unsigned)((int64_t)W * H)), dim3(kXcaThreads), 0, stream,
+  hipLaunchKernelGGL((k_xca_bwd<T, D>), dim3(xca_grid(W, H)), dim3(kXcaThreads), 0, stream,
                      reinterpret_cast<const PlanHeader*>(base + lay.header),
                      reinterpret_cast<const int32_t*>(base + lay.perm),
                      reinterpret_cast<const int32_t*>(base + lay.offsets), tau,
@@ -499,7 +517,7 @@ hipError_t xca_impl(const void* plan, int32_t n, int32_t W, int32_t H, const flo
                     const void* q, const void* k, const void* v, void* o, hipStream_t stream) {
   const PlanLayout lay = plan_layout(n, W);
   const char* base = static_cast<const char*>(plan);
-  hipLaunchKernelGGL((k_xca_fwd<T, D>), dim3((unsigned)((int64_t)W * H)), dim3(kXcaThreads), 0, stream,
+  hipLaunchKernelGGL((k_xca_fwd<T, D>), dim3(xca_grid(W, H)), dim3(kXcaThreads), 0, stream,
                      reinterpret_cast<const PlanHeader*>(base + lay.header),
                      reinterpret_cast<const int32_t*>(base + lay.perm),
                      reinterpret_cast<const int32_t*>(base + lay.offsets), tau,
