@@ -325,7 +325,7 @@ sla_status_t sla_forward_scatter(const void* plan, size_t plan_bytes, int64_t n,
  * not written), plus SLA_E_UNSUPPORTED when num_windows x heads x 256 exceeds
  * 2^32 - 1 (one 256-thread workgroup per window and head, windows padded
  * to a multiple of 8).  fp32 arithmetic on
- * the vector units; outputs rounded to `dtype`.  Forward only.
+ * the vector units; outputs rounded to `dtype`.  Its backward is sla_backward_xca.
  */
 sla_status_t sla_forward_xca(const void* plan, size_t plan_bytes, int64_t n, int32_t num_windows,
                              sla_dtype_t dtype, int32_t heads, int32_t head_dim, const float* tau,
