@@ -257,14 +257,21 @@ __global__ __launch_bounds__(kXcaThreads) void k_xca_fwd(
 // N = qhat^T khat, G = tau N and A = softmax_c(G):
 //   dv_i = A^T do_i,  dA = sum_i do_i v_i^T,  dG = A * (dA - rowsum(A * dA)),
 //   dtau partial = sum dG * N,
-//   dq[:, e] = (sum_c B_q[e][c] k[:, c] - q[:, e] s_e / nq_e) / nq_e with
-//   B_q[e][c] = tau dG[e][c] / nk_c and s_e = tau sum_c dG[e][c] N[e][c] (the
-//   projection of d qhat onto qhat, read off the d x d sums instead of a pass
-//   over the rows; zero where the norm took the floor), and likewise dk with
-//   B_k[e][c] = tau dG[e][c] / nq_e and t_c = tau sum_e dG[e][c] N[e][c].
+//   dqh[:, e] = sum_c B_q[e][c] k[:, c] with B_q[e][c] = tau dG[e][c] / nk_c,
+//   s_e = sum_r qhat_re dqh_re  (the projection of dqh onto qhat, summed over the
+//        window's rows; zero where the norm took the floor),
+//   dq[:, e] = (dqh[:, e] - qhat[:, e] s_e) / nq_e,
+// and likewise dk with B_k[e][c] = tau dG[e][c] / nq_e and t_c = sum_r khat_rc
+// dkh_rc.  s_e comes from the rows themselves, as qhat and dqh round, so that
+// the difference keeps the cancellation exact where it is exact in real
+// arithmetic: in a one-row window qhat = q / |q| is +-1 exactly (the square
+// root of a rounded square is the magnitude again in binary floating point), so
+// qhat s_e = dqh and dq = 0, as the chain rule gives.
 // Passes over the window's rows: q, k (N, as in the forward); dout, v (dA and
-// dv); q, k again (dq, dk).  The temperature gradient of every (window, head)
-// goes to `part`; k_xca_dtau adds the windows in order.
+// dv); q, k again (dqh, dkh and their projections; then dq, dk, from registers
+// for a window of one block, from a further pass over q, k otherwise).  The
+// temperature gradient of every (window, head) goes to `part`; k_xca_dtau adds
+// the windows in order.
 template <typename T, int D>
 __global__ __launch_bounds__(kXcaThreads) void k_xca_bwd(
     const PlanHeader* __restrict__ hdr, const int32_t* __restrict__ perm,
@@ -280,8 +287,9 @@ __global__ __launch_bounds__(kXcaThreads) void k_xca_bwd(
   constexpr int NW = kXcaThreads / 64;
   __shared__ __align__(16) float s_a[kXcaRows][LD];
   __shared__ __align__(16) float s_b[kXcaRows][LD];
-  __shared__ float s_g[D][D + 1];    // A, then tau dG * N
+  __shared__ float s_g[D][D + 1];    // A
   __shared__ float s_dg[D][D + 1];   // dG
+  __shared__ float s_sp[2 * RPP][D]; // shares of s_e and t_c
   __shared__ float s_nrm[2 * D];     // nq, nk
   __shared__ float s_st[2 * D];      // s_e, t_c
   __shared__ float s_red[NW];
@@ -397,7 +405,7 @@ __global__ __launch_bounds__(kXcaThreads) void k_xca_bwd(
     }
   }
 
-  // 3. dG, the temperature partial, s_e and t_c
+  // 3. dG and the temperature partial
   float rsum = 0.f;
 #pragma unroll
   for (int u = 0; u < EPT; ++u) rsum += a[u] * da[u];
@@ -418,12 +426,8 @@ __global__ __launch_bounds__(kXcaThreads) void k_xca_bwd(
   for (int m = 1; m < 64; m <<= 1) wsum += __shfl_xor(wsum, m, 64);
   __syncthreads();   // the last block's readers of s_a, s_b and every reader of s_g are done
   if ((tid & 63) == 0) s_red[tid >> 6] = wsum;
-  if (c0 == 0) s_st[e] = s_nrm[e] > 1e-12f ? t * srow : 0.f;
 #pragma unroll
-  for (int u = 0; u < EPT; ++u) {
-    s_dg[e][c0 + u] = dg[u];
-    s_g[e][c0 + u] = dg[u] * nn[u];
-  }
+  for (int u = 0; u < EPT; ++u) s_dg[e][c0 + u] = dg[u];
   __syncthreads();
   if (tid == 0) {
     float tot = 0.f;
@@ -431,46 +435,93 @@ __global__ __launch_bounds__(kXcaThreads) void k_xca_bwd(
     for (int j = 0; j < NW; ++j) tot += s_red[j];
     part[b] = tot;
   }
-  if (tid < D) {
-    float cs = 0.f;
-    for (int j = 0; j < D; ++j) cs += s_g[j][tid];
-    s_st[D + tid] = s_nrm[D + tid] > 1e-12f ? t * cs : 0.f;
-  }
-  __syncthreads();
 
-  // 4. dq[:, x3] and dk[:, x3]
+  // 4. dqh[:, x3], dkh[:, x3] for rows r3, r3 + RPP, ... of each block, and their
+  //    projections on qhat[:, x3], khat[:, x3]
   float bq[D], bk[D];
 #pragma unroll
   for (int j = 0; j < D; ++j) {
     bq[j] = t * s_dg[x3][j] / s_nrm[D + j];
     bk[j] = t * s_dg[j][x3] / s_nrm[j];
   }
-  const float iq = 1.f / s_nrm[x3], ik = 1.f / s_nrm[D + x3];
-  const float sq = s_st[x3] * iq, tk = s_st[D + x3] * ik;
+  const float nq = s_nrm[x3], nk = s_nrm[D + x3];
+  constexpr int RPT = kXcaRows / RPP;   // rows of a block per thread
+  float gqr[RPT], gkr[RPT];
+  // dqh and dkh of this thread's rows of the block in LDS
+  auto grads = [&](int nr) {
+#pragma unroll
+    for (int m = 0; m < RPT; ++m) {
+      const int r = r3 + RPP * m;
+      float gq = 0.f, gk = 0.f;
+      if (r < nr) {
+#pragma unroll
+        for (int j = 0; j < D; j += 4) {
+          const float4 kx = *reinterpret_cast<const float4*>(&s_b[r][j]);
+          const float4 qx = *reinterpret_cast<const float4*>(&s_a[r][j]);
+          gq += bq[j] * kx.x + bq[j + 1] * kx.y + bq[j + 2] * kx.z + bq[j + 3] * kx.w;
+          gk += bk[j] * qx.x + bk[j + 1] * qx.y + bk[j + 2] * qx.z + bk[j + 3] * qx.w;
+        }
+      }
+      gqr[m] = gq;
+      gkr[m] = gk;
+    }
+  };
+  auto fetch_qk = [&](int32_t p0, int nr) {
+    uint4 qr[NP], kr[NP];
+    xca_fetch<T, D>(pm, p0, nr, n, rs, col, q, qr, s_row);
+    xca_fetch<T, D>(pm, p0, nr, n, rs, col, k, kr, nullptr);
+    xca_put<T, D>(qr, s_a);
+    xca_put<T, D>(kr, s_b);
+  };
+  float ps = 0.f, pk = 0.f;   // this thread's share of s_x3 and t_x3, in row order
   for (int32_t p0 = rb; p0 < re; p0 += kXcaRows) {
     const int nr = min(kXcaRows, re - p0);
     __syncthreads();
-    {
-      uint4 qr[NP], kr[NP];
-      xca_fetch<T, D>(pm, p0, nr, n, rs, col, q, qr, s_row);
-      xca_fetch<T, D>(pm, p0, nr, n, rs, col, k, kr, nullptr);
-      xca_put<T, D>(qr, s_a);
-      xca_put<T, D>(kr, s_b);
-    }
+    fetch_qk(p0, nr);
     __syncthreads();
-    for (int r = r3; r < nr; r += RPP) {
-      const int32_t row = s_row[r];
-      float gq = 0.f, gk = 0.f;
+    grads(nr);
 #pragma unroll
-      for (int j = 0; j < D; j += 4) {
-        const float4 kx = *reinterpret_cast<const float4*>(&s_b[r][j]);
-        const float4 qx = *reinterpret_cast<const float4*>(&s_a[r][j]);
-        gq += bq[j] * kx.x + bq[j + 1] * kx.y + bq[j + 2] * kx.z + bq[j + 3] * kx.w;
-        gk += bk[j] * qx.x + bk[j + 1] * qx.y + bk[j + 2] * qx.z + bk[j + 3] * qx.w;
+    for (int m = 0; m < RPT; ++m) {
+      const int r = r3 + RPP * m;
+      if (r < nr) {
+        ps += (s_a[r][x3] / nq) * gqr[m];
+        pk += (s_b[r][x3] / nk) * gkr[m];
       }
+    }
+  }
+  // s_x3 = the RPP shares in order (the floor makes the norm a constant: no projection)
+  s_sp[r3][x3] = ps;
+  s_sp[RPP + r3][x3] = pk;
+  __syncthreads();
+  if (tid < 2 * D) {
+    const int c = tid & (D - 1), which = tid / D;
+    float x = 0.f;
+#pragma unroll
+    for (int j = 0; j < RPP; ++j) x += s_sp[which * RPP + j][c];
+    s_st[tid] = s_nrm[tid] > 1e-12f ? x : 0.f;
+  }
+  __syncthreads();
+  const float sq = s_st[x3], tk = s_st[D + x3];
+
+  // 5. dq[:, x3] and dk[:, x3]; a window of one block still has its q, k rows in
+  //    LDS and its dqh, dkh in registers
+  const bool one_block = re - rb <= kXcaRows;
+  for (int32_t p0 = rb; p0 < re; p0 += kXcaRows) {
+    const int nr = min(kXcaRows, re - p0);
+    if (!one_block) {
+      __syncthreads();
+      fetch_qk(p0, nr);
+      __syncthreads();
+      grads(nr);
+    }
+#pragma unroll
+    for (int m = 0; m < RPT; ++m) {
+      const int r = r3 + RPP * m;
+      if (r >= nr) continue;
+      const int32_t row = s_row[r];
       if (row >= 0) {
-        XcaIo<T>::store(dq + (size_t)row * rs + col + x3, (gq - s_a[r][x3] * sq) * iq);
-        XcaIo<T>::store(dk + (size_t)row * rs + col + x3, (gk - s_b[r][x3] * tk) * ik);
+        XcaIo<T>::store(dq + (size_t)row * rs + col + x3, (gqr[m] - (s_a[r][x3] / nq) * sq) / nq);
+        XcaIo<T>::store(dk + (size_t)row * rs + col + x3, (gkr[m] - (s_b[r][x3] / nk) * tk) / nk);
       }
     }
   }

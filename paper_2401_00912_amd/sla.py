@@ -251,6 +251,13 @@ def _check_rows(name, t, n, like=None):
         raise ValueError(f"{name} must match q in shape, dtype and device")
 
 
+def _check_workspace(ws, device):
+    """A caller's workspace: a contiguous tensor on the call's device (its size in
+    bytes, numel x element size, is checked by the library)."""
+    if ws.device != device or not ws.is_contiguous():
+        raise ValueError("workspace must be a contiguous tensor on the inputs' device")
+
+
 def _variant(feature_map, eps):
     """None for the plain Eq. (3) calls, else (sla_feature_map_t, eps)."""
     if feature_map is None and eps is None:
@@ -341,13 +348,17 @@ def backward_xca(plan: Plan, q, k, v, tau, dout, dq=None, dk=None, dv=None, dtau
     for name, t in (("dq", dq), ("dk", dk), ("dv", dv)):
         _check_rows(name, t, plan.n, q)
     dtau = torch.empty_like(tau) if dtau is None else dtau
+    if (dtau.dtype != torch.float32 or dtau.dim() != 1 or dtau.shape[0] != H or not dtau.is_contiguous()
+            or dtau.device != q.device):
+        raise ValueError("dtau must be a contiguous float32 [heads] tensor on q's device")
     need = int(lib().sla_xca_backward_workspace_bytes(plan.num_windows, H))
     if workspace is None:
         workspace = torch.empty(max(need, 4), dtype=torch.uint8, device=q.device)
+    _check_workspace(workspace, q.device)
     st = lib().sla_backward_xca(_ptr(plan.buf), plan.nbytes, plan.n, plan.num_windows, _dtype_code(q.dtype),
                                 H, d, _ptr(tau), _ptr(q), _ptr(k), _ptr(v), _ptr(dout), _ptr(dq), _ptr(dk),
-                                _ptr(dv), _ptr(dtau), _ptr(workspace), int(workspace.numel()),
-                                _stream(q.device))
+                                _ptr(dv), _ptr(dtau), _ptr(workspace),
+                                int(workspace.numel() * workspace.element_size()), _stream(q.device))
     _check(st, "sla_backward_xca")
     return dq, dk, dv, dtau
 
@@ -471,6 +482,7 @@ def cwi_backward(map, grid, coords, x, w_x, w_y, w_3, dy, order=None, workspace=
         raise SlaError(SLA_E_UNSUPPORTED, "sla_cwi_backward_workspace_bytes")
     if workspace is None:
         workspace = torch.empty(need, dtype=torch.uint8, device=x.device)
+    _check_workspace(workspace, x.device)
     if out is None:
         dx = torch.empty_like(x)
         dws = [torch.empty_like(w) for w in (w_x, w_y, w_3)]
@@ -505,6 +517,7 @@ def forward_scatter(plan: Plan, q, k, v, out=None, workspace=None):
     need = scatter_workspace_bytes(plan.n, H, d)
     if workspace is None:
         workspace = torch.empty(max(need, 16), dtype=torch.uint8, device=q.device)
+    _check_workspace(workspace, q.device)
     st = lib().sla_forward_scatter(_ptr(plan.buf), plan.nbytes, plan.n, plan.num_windows,
                                    _dtype_code(q.dtype), H, d, _ptr(q), _ptr(k), _ptr(v), _ptr(out),
                                    _ptr(workspace), int(workspace.numel() * workspace.element_size()),

@@ -295,3 +295,25 @@ def test_cwi_binding_rejects_bad_tensors(L):
         sla.cwi_backward(good_map, grid, coords, x, *w, x.float())
     with pytest.raises(ValueError, match="map"):
         sla.cwi_backward(torch.zeros(10, dtype=torch.int32), grid, coords, x, *w, x)
+
+
+def test_xca_backward_binding_rejects_bad_dtau_and_workspace(L):
+    # dtau and the workspace are checked before the C call: a short or 16-bit dtau
+    # would let the temperature kernel write past its end, and a workspace on
+    # another device would be handed over as a foreign pointer
+    import torch
+
+    n, H, d = 6, 4, 16
+    plan = sla.Plan(buf=torch.zeros(sla.plan_bytes(n, 2), dtype=torch.uint8), n=n, num_windows=2,
+                    chunk_rows=64, perm=None, offsets=None, invalid=None)
+    q = torch.zeros((n, H, d), dtype=torch.float16)
+    tau = torch.ones(H, dtype=torch.float32)
+    args = (plan, q, q, q, tau, q)
+    for bad in (torch.zeros(H, dtype=torch.float16), torch.zeros(H - 1), torch.zeros(2 * H)[::2],
+                torch.zeros((H, 1)), torch.zeros(H, device="meta")):
+        with pytest.raises(ValueError, match="dtau"):
+            sla.backward_xca(*args, dtau=bad)
+    with pytest.raises(ValueError, match="workspace"):
+        sla.backward_xca(*args, dtau=torch.zeros(H), workspace=torch.zeros(64, dtype=torch.uint8, device="meta"))
+    with pytest.raises(ValueError, match="workspace"):
+        sla.backward_xca(*args, dtau=torch.zeros(H), workspace=torch.zeros(64, dtype=torch.uint8)[::2])
