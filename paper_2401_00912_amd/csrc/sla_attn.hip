@@ -58,6 +58,7 @@ void k_sla_fwd(KernelArgs a, const T* __restrict__ q, const T* __restrict__ k,
                const T* __restrict__ v, T* __restrict__ o) {
   constexpr int KT = kStateTiles<D>;
   __shared__ floatx4 s_part[kWaves * KT * 64];  // partial states of a long window
+  __shared__ WaveMeta s_meta[kWaves];            // the items ahead (perm slices, offsets, entries)
   const int lane = lane_id();
   const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const PlanHeader* hdr = a.hdr;
@@ -71,32 +72,46 @@ void k_sla_fwd(KernelArgs a, const T* __restrict__ q, const T* __restrict__ k,
   const T* const mats[3] = {k, v, q};
   constexpr unsigned kKV = 3u, kQ = 4u, kAll = 7u;
 
+  WaveMeta& meta = s_meta[wv];
+  const bool csr = perm == nullptr;
   int32_t item = blockIdx.x;
-  Pending cur;
+  WaveWork wc, wn;
   {
-    const Slot sl = item_slot(it, item, wv);
-    pending_request(cur, a, sl, slot_entry(a, sl), wv, perm, lane);
+    const Slot s0 = item_slot(it, item, wv), s1 = item_slot(it, item + G, wv);
+    wc = decode_work(a, s0, slot_entry(a, s0), wv);
+    wn = decode_work(a, s1, slot_entry(a, s1), wv);
   }
-  Slot nsl = item_slot(it, item + G, wv);
-  int4 ne = slot_entry(a, nsl);
+  request_perm(wc, perm, meta.perm[0], lane);
+  request_perm(wn, perm, meta.perm[1], lane);
+  request_offs(wc, a, meta.offs[0], lane);
+  request_entry(a, item_slot(it, item + 2 * G, wv), &meta.ent[0], lane);
+  int par = 0;   // ring slot of the current item
   while (item < it.total) {
-    const WaveWork ww = cur.ww;
+    const WaveWork ww = wc;
     const int col = ww.h * D;
     // a range of more than kBlockRows rows (a quarter of a very long window) is
     // streamed through the block: K, V for the state, then Q for the outputs
     const bool resident = ww.rb - ww.ra <= kBlockRows;
     const unsigned first = resident ? kAll : kKV;
+    // the item's rows and windows, and the entry of the item after next, from LDS
+    wait_vm();
+    BlockRows br;
+    block_rows_lds(br, ww, meta.perm[par], csr, lane);
+    Stream str;
+    stream_lds(str, ww, a, meta.offs[par], lane);
+    const WaveWork wnn = decode_work(a, item_slot(it, item + 2 * G, wv), lds_entry(&meta.ent[par]), wv);
+    wait_lgkm();
+    // requests ahead: the slice of the item after next, the next item's windows,
+    // the entry after that; then this item's rows (whose wait covers these)
+    request_perm(wnn, perm, meta.perm[par], lane);
+    request_offs(wn, a, meta.offs[par ^ 1], lane);
+    request_entry(a, item_slot(it, item + 3 * G, wv), &meta.ent[par ^ 1], lane);
     Block<T, D, 3> bk;
-    if (ww.kind != 0) block_fetch<T, D, 3>(bk, cur.br, ww.ra, ww.rb, n, mats, first, rs, col, g);
-    // the next item: its rows and windows are requested now, its successor's entry too
-    Pending nxt;
-    pending_request(nxt, a, nsl, ne, wv, perm, lane);
-    nsl = item_slot(it, item + 2 * G, wv);
-    ne = slot_entry(a, nsl);
+    if (ww.kind != 0) block_fetch<T, D, 3>(bk, br, ww.ra, ww.rb, n, mats, first, rs, col, g);
 
     block_arrange<T, D, 3>(bk, first);
     WinIter wi;
-    for (bool more = wi.first(ww, cur.str); more; more = wi.next(ww, cur.str)) {
+    for (bool more = wi.first(ww, str); more; more = wi.next(ww, str)) {
       const int32_t wa = wi.wc.ws, wb = wi.wc.we;
       State<D> st;
       st.clear();
@@ -136,7 +151,9 @@ void k_sla_fwd(KernelArgs a, const T* __restrict__ q, const T* __restrict__ k,
       }
     }
     item += G;
-    cur = nxt;
+    wc = wn;
+    wn = wnn;
+    par ^= 1;
   }
 }
 
@@ -151,6 +168,7 @@ void k_sla_bwd(KernelArgs a, const T* __restrict__ q, const T* __restrict__ k,
   constexpr int KT = kStateTiles<D>;
   __shared__ floatx4 s_part[2][kWaves * KT * 64];  // partial S, z / dS, dz of a long window
   __shared__ float s_tr[kWaves][D * kTrLd<D>];     // transposes, one tile per wave
+  __shared__ WaveMeta s_meta[kWaves];              // the items ahead (perm slices, offsets, entries)
   const int lane = lane_id();
   const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const PlanHeader* hdr = a.hdr;
@@ -165,29 +183,43 @@ void k_sla_bwd(KernelArgs a, const T* __restrict__ q, const T* __restrict__ k,
   const T* const mats[4] = {k, v, q, dout};
   constexpr unsigned kKV = 3u, kQD = 12u, kAll = 15u;
 
+  WaveMeta& meta = s_meta[wv];
+  const bool csr = perm == nullptr;
   int32_t item = blockIdx.x;
-  Pending cur;
+  WaveWork wc, wn;
   {
-    const Slot sl = item_slot(it, item, wv);
-    pending_request(cur, a, sl, slot_entry(a, sl), wv, perm, lane);
+    const Slot s0 = item_slot(it, item, wv), s1 = item_slot(it, item + G, wv);
+    wc = decode_work(a, s0, slot_entry(a, s0), wv);
+    wn = decode_work(a, s1, slot_entry(a, s1), wv);
   }
-  Slot nsl = item_slot(it, item + G, wv);
-  int4 ne = slot_entry(a, nsl);
+  request_perm(wc, perm, meta.perm[0], lane);
+  request_perm(wn, perm, meta.perm[1], lane);
+  request_offs(wc, a, meta.offs[0], lane);
+  request_entry(a, item_slot(it, item + 2 * G, wv), &meta.ent[0], lane);
+  int par = 0;   // ring slot of the current item
   while (item < it.total) {
-    const WaveWork ww = cur.ww;
+    const WaveWork ww = wc;
     const int col = ww.h * D;
     const bool resident = ww.rb - ww.ra <= kBlockRows;
     const unsigned first = resident ? kAll : kKV;
+    // the item's rows and windows, and the entry of the item after next, from LDS
+    wait_vm();
+    BlockRows br;
+    block_rows_lds(br, ww, meta.perm[par], csr, lane);
+    Stream str;
+    stream_lds(str, ww, a, meta.offs[par], lane);
+    const WaveWork wnn = decode_work(a, item_slot(it, item + 2 * G, wv), lds_entry(&meta.ent[par]), wv);
+    wait_lgkm();
+    // requests ahead (see the forward); then this item's rows
+    request_perm(wnn, perm, meta.perm[par], lane);
+    request_offs(wn, a, meta.offs[par ^ 1], lane);
+    request_entry(a, item_slot(it, item + 3 * G, wv), &meta.ent[par ^ 1], lane);
     Block<T, D, 4> bk;
-    if (ww.kind != 0) block_fetch<T, D, 4>(bk, cur.br, ww.ra, ww.rb, n, mats, first, rs, col, g);
-    Pending nxt;
-    pending_request(nxt, a, nsl, ne, wv, perm, lane);
-    nsl = item_slot(it, item + 2 * G, wv);
-    ne = slot_entry(a, nsl);
+    if (ww.kind != 0) block_fetch<T, D, 4>(bk, br, ww.ra, ww.rb, n, mats, first, rs, col, g);
 
     block_arrange<T, D, 4>(bk, first);
     WinIter wi;
-    for (bool more = wi.first(ww, cur.str); more; more = wi.next(ww, cur.str)) {
+    for (bool more = wi.first(ww, str); more; more = wi.next(ww, str)) {
       const int32_t wa = wi.wc.ws, wb = wi.wc.we;
       State<D> st;  // S, z ; then beta dS, beta dz
       BwdOp<T, D> op;
@@ -252,7 +284,9 @@ void k_sla_bwd(KernelArgs a, const T* __restrict__ q, const T* __restrict__ k,
       }
     }
     item += G;
-    cur = nxt;
+    wc = wn;
+    wn = wnn;
+    par ^= 1;
   }
 }
 

@@ -1036,6 +1036,92 @@ __device__ __forceinline__ void pending_request(Pending& p, const KernelArgs& a,
   if (p.ww.kind == 1) p.str.request(p.ww.wb);
 }
 
+// ------------------------------------------------ the item stream, through LDS
+// A wave's view of the items ahead of it: the permutation slice of an item's
+// first block, the window offsets of a chunk and the plan entry of an item are
+// gathered into LDS by the memory system (global_load_lds: lane l's value lands
+// at the slot + 4 l) one or two items ahead, and read from LDS at the top of
+// the item that needs them.  Values prefetched into registers would have to be
+// carried from one item's registers to the next one's, and the copy, or a load
+// merged with a default value, waits for the load; through LDS the only wait of
+// an item is the one at its top.
+struct WaveMeta {
+  int32_t perm[2][kMaxChunkRows];   // permutation slices (ring by item parity)
+  int32_t offs[2][128];             // offs[wb + l] of a chunk's first 128 window slots
+  int4 ent[2];                      // plan entries
+};
+
+__device__ __forceinline__ int32_t first_block_rows(const WaveWork& w) {
+  return w.kind != 0 ? min(w.rb - w.ra, kMaxChunkRows) : 0;
+}
+
+// The permutation slice of an item's first block into `slot` (none in CSR mode).
+__device__ __forceinline__ void request_perm(const WaveWork& w, const int32_t* perm, int32_t* slot, int lane) {
+  if (perm != nullptr && lane < first_block_rows(w))
+    __builtin_amdgcn_global_load_lds(perm + w.ra + lane, (__attribute__((address_space(3))) void*)slot, 4, 0, 0);
+}
+
+// The offsets of a chunk's first 128 window slots into `slot` (indices clamped to
+// the table; windows past the chunk are ignored when the stream is built).
+__device__ __forceinline__ void request_offs(const WaveWork& w, const KernelArgs& a, int32_t* slot, int lane) {
+  if (w.kind != 1) return;
+  __builtin_amdgcn_global_load_lds(a.offs + min(w.wb + lane, a.W), (__attribute__((address_space(3))) void*)slot,
+                                   4, 0, 0);
+  __builtin_amdgcn_global_load_lds(a.offs + min(w.wb + 64 + lane, a.W),
+                                   (__attribute__((address_space(3))) void*)(slot + 64), 4, 0, 0);
+}
+
+// The plan entry of a slot into LDS (4 lanes of 4 bytes).
+__device__ __forceinline__ void request_entry(const KernelArgs& a, const Slot& sl, int4* slot, int lane) {
+  if (sl.idx < 0 || lane >= 4) return;
+  const int32_t* t = sl.table == 0 ? reinterpret_cast<const int32_t*>(a.longs) : reinterpret_cast<const int32_t*>(a.chunks);
+  __builtin_amdgcn_global_load_lds(t + 4 * sl.idx + lane, (__attribute__((address_space(3))) void*)slot, 4, 0, 0);
+}
+
+__device__ __forceinline__ int4 lds_entry(const int4* slot) {
+  typedef unsigned int u32x4v __attribute__((ext_vector_type(4)));
+  const u32x4v e = *(const __attribute__((address_space(3))) u32x4v*)slot;
+  return make_int4((int)__builtin_amdgcn_readfirstlane(e[0]), (int)__builtin_amdgcn_readfirstlane(e[1]),
+                   (int)__builtin_amdgcn_readfirstlane(e[2]), (int)__builtin_amdgcn_readfirstlane(e[3]));
+}
+
+// Original rows of an item's first block (the layout of block_rows) from its slice.
+__device__ __forceinline__ void block_rows_lds(BlockRows& br, const WaveWork& w, const int32_t* slot, bool csr,
+                                               int lane) {
+  const int i = lane & 15;
+  const int32_t nr = first_block_rows(w);
+#pragma unroll
+  for (int jj = 0; jj < kBlockJobs; ++jj)
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+      const int lr = kSliceRows * jj + 16 * s + i;
+      br.o[jj][s] = lr >= nr ? -1 : (csr ? w.ra + lr : *(const __attribute__((address_space(3))) int32_t*)(slot + lr));
+    }
+}
+
+// The window stream of a chunk from its offsets slot (page 0; later pages are
+// read from the plan as they are reached).
+__device__ __forceinline__ void stream_lds(Stream& str, const WaveWork& w, const KernelArgs& a, const int32_t* slot,
+                                           int lane) {
+  str.lane = lane;
+  str.offs = a.offs;
+  str.rb = w.ra;
+  str.re = w.rb;
+  str.wend = w.we;
+  str.wp = w.wb;
+  str.a = str.b = 0;
+  str.live = 0;
+  if (w.kind != 1) return;
+  const int32_t x0 = *(const __attribute__((address_space(3))) int32_t*)(slot + lane);
+  const int32_t x1 = *(const __attribute__((address_space(3))) int32_t*)(slot + lane + 1);
+  const bool has = w.wb + lane < w.we;
+  str.a = has ? max(x0, w.ra) : 0;
+  str.b = has ? min(x1, w.rb) : 0;
+}
+
+__device__ __forceinline__ void wait_vm() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+__device__ __forceinline__ void wait_lgkm() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+
 // Block until every wave of the workgroup gets here, with this wave's LDS writes
 // done (LDS only: loads in flight stay in flight).
 __device__ __forceinline__ void lds_barrier() {
