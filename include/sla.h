@@ -356,6 +356,28 @@ sla_status_t sla_backward_xca(const void* plan, size_t plan_bytes, int64_t n, in
                               void* dq, void* dk, void* dv, float* dtau, void* workspace,
                               size_t workspace_bytes, sla_stream_t stream);
 
+/*
+ * sla_backward_xca without a workspace argument, for callers that cannot
+ * allocate device memory: code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc.  The per-(window, head) partials of dtau go to
+ * a buffer of SLA_XCA_SCRATCH_FLOATS floats (1 MiB) that the library keeps in
+ * static device memory, one copy on every GPU it runs on, for the life of the
+ * process; the first call on a device looks its address up (no allocation, no
+ * hipMalloc / hipFree, no allocating library call).  Every partial is rewritten by
+ * every call, so the buffer needs no clearing and keeps the last call's values.
+ * num_windows * heads must not exceed SLA_XCA_SCRATCH_FLOATS (SLA_E_UNSUPPORTED
+ * otherwise, returned before anything is enqueued).  All calls on one GPU share
+ * the buffer: calls that may overlap on one GPU (different streams with no order
+ * between them) race and must not be issued.  Outputs equal those of
+ * sla_backward_xca bit for bit; other arguments and errors as sla_backward_xca.
+ */
+#define SLA_XCA_SCRATCH_FLOATS 262144
+
+sla_status_t sla_backward_xca_noalloc(const void* plan, size_t plan_bytes, int64_t n, int32_t num_windows,
+                                      sla_dtype_t dtype, int32_t heads, int32_t head_dim, const float* tau,
+                                      const void* q, const void* k, const void* v, const void* dout,
+                                      void* dq, void* dk, void* dv, float* dtau, sla_stream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

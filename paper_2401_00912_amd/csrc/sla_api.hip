@@ -43,6 +43,10 @@ hipError_t launch_backward_xca(const void* plan, int32_t n, int32_t W, int dtype
                                const float* tau, const void* q, const void* k, const void* v,
                                const void* dout, void* dq, void* dk, void* dv, float* dtau, float* part,
                                hipStream_t stream);
+hipError_t launch_backward_xca_noalloc(const void* plan, int32_t n, int32_t W, int dtype, int32_t H, int32_t d,
+                                       const float* tau, const void* q, const void* k, const void* v,
+                                       const void* dout, void* dq, void* dk, void* dv, float* dtau,
+                                       hipStream_t stream);
 }  // namespace sla
 
 namespace {
@@ -303,6 +307,27 @@ SLA_EXPORT sla_status_t sla_backward_xca(const void* plan, size_t plan_bytes, in
                                              tau, q, k, v, dout, dq, dk, dv, dtau,
                                              static_cast<float*>(workspace),
                                              static_cast<hipStream_t>(stream)));
+}
+
+SLA_EXPORT sla_status_t sla_backward_xca_noalloc(const void* plan, size_t plan_bytes, int64_t n,
+                                                 int32_t num_windows, sla_dtype_t dtype, int32_t heads,
+                                                 int32_t head_dim, const float* tau, const void* q,
+                                                 const void* k, const void* v, const void* dout, void* dq,
+                                                 void* dk, void* dv, float* dtau, sla_stream_t stream) {
+  const sla_status_t st = check_tensor_args(n, num_windows, (int)dtype, heads, head_dim, plan, plan_bytes);
+  if (st != SLA_OK) return st;
+  if (((int64_t)num_windows + 7) / 8 * 8 * heads * 256 > (int64_t)UINT32_MAX) return SLA_E_UNSUPPORTED;
+  if ((int64_t)num_windows * heads > (int64_t)SLA_XCA_SCRATCH_FLOATS) return SLA_E_UNSUPPORTED;
+  if (!tau || !dtau || !aligned(tau, 4) || !aligned(dtau, 4)) return SLA_E_ARG;
+  if (n > 0) {
+    if (!q || !k || !v || !dout || !dq || !dk || !dv) return SLA_E_ARG;
+    for (const void* p : {q, k, v, dout, static_cast<const void*>(dq), static_cast<const void*>(dk),
+                          static_cast<const void*>(dv)})
+      if (!aligned(p, 16)) return SLA_E_ARG;
+  }
+  return hip_status(sla::launch_backward_xca_noalloc(plan, (int32_t)n, num_windows, (int)dtype, heads,
+                                                     head_dim, tau, q, k, v, dout, dq, dk, dv, dtau,
+                                                     static_cast<hipStream_t>(stream)));
 }
 
 SLA_EXPORT size_t sla_cwi_map_bytes(int32_t gx, int32_t gy, int32_t gz) {

@@ -20,9 +20,21 @@
 //      64 rows gathers its v rows in step 1 already, into registers, so that
 //      their round trip overlaps the sums; longer windows gather v again here.
 // fp32 throughout; inputs widened from the storage type, outputs rounded to it.
+#include "sla.h"
 #include "sla_common.h"
 
+#include <mutex>
+
 namespace sla {
+
+// The dtau partials of the backward without a workspace (sla_backward_xca_noalloc):
+// one fp32 per (window, head), held in static device memory on every GPU the
+// library runs on.  In host code `scratch` only names the symbol; its address on
+// a device comes from hipGetSymbolAddress, looked up once per device.
+constexpr size_t kXcaScratchFloats = 262144;   // SLA_XCA_SCRATCH_FLOATS
+static_assert(kXcaScratchFloats == SLA_XCA_SCRATCH_FLOATS, "the header states the scratch size");
+static __device__ __align__(256) float scratch[kXcaScratchFloats];
+
 namespace {
 
 constexpr int kXcaThreads = 256;
@@ -605,6 +617,43 @@ hipError_t launch_backward_xca(const void* plan, int32_t n, int32_t W, int dtype
   if (dtype == 0) return xca_bwd_impl<float, 16>(plan, n, W, H, tau, q, k, v, dout, dq, dk, dv, dtau, part, stream);
   if (dtype == 1) return xca_bwd_impl<_Float16, 16>(plan, n, W, H, tau, q, k, v, dout, dq, dk, dv, dtau, part, stream);
   return xca_bwd_impl<bf16_t, 16>(plan, n, W, H, tau, q, k, v, dout, dq, dk, dv, dtau, part, stream);
+}
+
+// Device address of `scratch` on the current device (nullptr and the HIP error
+// if it cannot be looked up).  Looked up once per device, with that device current.
+static float* scratch_address(hipError_t& err) {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static float* addr[kMaxDevices] = {};
+  int dev = 0;
+  err = hipGetDevice(&dev);
+  if (err != hipSuccess) return nullptr;
+  if (dev < 0 || dev >= kMaxDevices) {
+    err = hipErrorInvalidDevice;
+    return nullptr;
+  }
+  std::lock_guard<std::mutex> lock(mu);
+  if (addr[dev] == nullptr) {
+    void* p = nullptr;
+    err = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (err != hipSuccess) return nullptr;
+    addr[dev] = static_cast<float*>(p);
+  }
+  err = hipSuccess;
+  return addr[dev];
+}
+
+// sla_backward_xca with the dtau partials in `scratch` (num_windows * heads <=
+// kXcaScratchFloats, checked by the caller).  Every partial is written by every
+// call, so nothing is cleared.
+hipError_t launch_backward_xca_noalloc(const void* plan, int32_t n, int32_t W, int dtype, int32_t H, int32_t d,
+                                       const float* tau, const void* q, const void* k, const void* v,
+                                       const void* dout, void* dq, void* dk, void* dv, float* dtau,
+                                       hipStream_t stream) {
+  hipError_t err;
+  float* part = scratch_address(err);
+  if (part == nullptr) return err;
+  return launch_backward_xca(plan, n, W, dtype, H, d, tau, q, k, v, dout, dq, dk, dv, dtau, part, stream);
 }
 
 }  // namespace sla

@@ -56,6 +56,7 @@ EXPORTED = (
     "sla_forward_xca",
     "sla_xca_backward_workspace_bytes",
     "sla_backward_xca",
+    "sla_backward_xca_noalloc",
 )
 
 
@@ -132,6 +133,8 @@ def lib() -> ctypes.CDLL:
     L.sla_forward_scatter.argtypes = [vp, sz, i64, i32, ctypes.c_int, i32, i32, vp, vp, vp, vp, vp, sz, vp]
     L.sla_forward_xca.restype = ctypes.c_int
     L.sla_forward_xca.argtypes = [vp, sz, i64, i32, ctypes.c_int, i32, i32, vp, vp, vp, vp, vp, vp]
+    L.sla_backward_xca_noalloc.restype = ctypes.c_int
+    L.sla_backward_xca_noalloc.argtypes = [vp, sz, i64, i32, en, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
     L.sla_xca_backward_workspace_bytes.restype = sz
     L.sla_xca_backward_workspace_bytes.argtypes = [i32, i32]
     L.sla_backward_xca.restype = ctypes.c_int
@@ -360,6 +363,32 @@ def backward_xca(plan: Plan, q, k, v, tau, dout, dq=None, dk=None, dv=None, dtau
                                 _ptr(dv), _ptr(dtau), _ptr(workspace),
                                 int(workspace.numel() * workspace.element_size()), _stream(q.device))
     _check(st, "sla_backward_xca")
+    return dq, dk, dv, dtau
+
+
+def backward_xca_noalloc(plan: Plan, q, k, v, tau, dout, dq=None, dk=None, dv=None, dtau=None):
+    """backward_xca through sla_backward_xca_noalloc: the dtau partials live in the
+    library's static device buffer (no workspace; calls on one GPU must not overlap)."""
+    torch = _torch()
+    for name, t in (("q", q), ("k", k), ("v", v), ("dout", dout)):
+        _check_rows(name, t, plan.n, q)
+    H, d = q.shape[1], q.shape[2]
+    if (tau.dtype != torch.float32 or tau.dim() != 1 or tau.shape[0] != H or not tau.is_contiguous()
+            or tau.device != q.device):
+        raise ValueError("tau must be a contiguous float32 [heads] tensor on q's device")
+    dq = torch.empty_like(q) if dq is None else dq
+    dk = torch.empty_like(q) if dk is None else dk
+    dv = torch.empty_like(q) if dv is None else dv
+    for name, t in (("dq", dq), ("dk", dk), ("dv", dv)):
+        _check_rows(name, t, plan.n, q)
+    dtau = torch.empty_like(tau) if dtau is None else dtau
+    if (dtau.dtype != torch.float32 or dtau.dim() != 1 or dtau.shape[0] != H or not dtau.is_contiguous()
+            or dtau.device != q.device):
+        raise ValueError("dtau must be a contiguous float32 [heads] tensor on q's device")
+    st = lib().sla_backward_xca_noalloc(_ptr(plan.buf), plan.nbytes, plan.n, plan.num_windows,
+                                        _dtype_code(q.dtype), H, d, _ptr(tau), _ptr(q), _ptr(k), _ptr(v),
+                                        _ptr(dout), _ptr(dq), _ptr(dk), _ptr(dv), _ptr(dtau), _stream(q.device))
+    _check(st, "sla_backward_xca_noalloc")
     return dq, dk, dv, dtau
 
 

@@ -317,3 +317,21 @@ def test_xca_backward_binding_rejects_bad_dtau_and_workspace(L):
         sla.backward_xca(*args, dtau=torch.zeros(H), workspace=torch.zeros(64, dtype=torch.uint8, device="meta"))
     with pytest.raises(ValueError, match="workspace"):
         sla.backward_xca(*args, dtau=torch.zeros(H), workspace=torch.zeros(64, dtype=torch.uint8)[::2])
+
+
+def test_xca_backward_noalloc_argument_errors(L):
+    # the size limit of the static buffer and the pointer checks are host-side:
+    # nothing is enqueued (and no device is touched) when they fail
+    assert L.sla_backward_xca_noalloc is not None
+    W = 16384
+    nb = sla.plan_bytes(100, W)
+    call = lambda **kw: L.sla_backward_xca_noalloc(  # noqa: E731
+        FAKE, kw.get("pb", nb), kw.get("n", 100), kw.get("W", W), 1, kw.get("H", 16), 32, kw.get("tau", FAKE),
+        FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, kw.get("dv", FAKE), kw.get("dtau", FAKE), None)
+    assert call(H=17) == sla.SLA_E_UNSUPPORTED          # 16384 x 17 partials > 262144
+    assert call(dtau=None) == sla.SLA_E_ARG
+    assert call(dtau=FAKE + 2) == sla.SLA_E_ARG
+    assert call(tau=None) == sla.SLA_E_ARG
+    assert call(dv=None) == sla.SLA_E_ARG
+    assert call(dv=FAKE + 8) == sla.SLA_E_ARG
+    assert call(pb=10) == sla.SLA_E_WORKSPACE
