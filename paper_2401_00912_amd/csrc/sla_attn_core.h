@@ -513,10 +513,11 @@ template <typename T, int W16>
 constexpr int kWpe = sizeof(T) == 4 ? (W16 > 2 ? W16 / 2 : 1) : W16;
 
 // ----------------------------------------------------------- backward math
-// bf16 keeps 8 significant bits, so the backward carries two operands as a
-// sum of two bf16 values (high part and rounding residual, 16 bits together):
-// -dout.o in the dz accumulation and dS^T in dk = (v dS^T + dz) phi'(k), the
-// two terms that cancel there.  fp16 (11 bits) and fp32 need no split.
+// bf16 keeps 8 significant bits, so the backward carries the operands of its
+// cancelling differences as a sum of two bf16 values (high part and rounding
+// residual, 16 bits together): S and S^T in dq = (dout S^T - (dout . o) z) / den
+// phi'(q) (o = phi(q) S / den), -dout.o in the dz accumulation, and dS^T in dk =
+// (v dS^T + dz) phi'(k).  fp16 (11 bits) and fp32 need no split.
 template <typename T>
 constexpr bool kSplitGrad = std::is_same<T, bf16_t>::value;
 
@@ -528,13 +529,15 @@ struct BwdOp {
   Raw<T, Geo<D>::KS> A[Geo<D>::NT];  // sig S   (o = phi(q) S, tile ct)  | rho dS^T (dfk = v dS^T, tile et)
   Raw<T, Geo<D>::KS> B[Geo<D>::NT];  // sig S^T (dfq = dout S^T, tile et) | rho dS  (dv = phi(k) dS, tile ct)
   Raw<T, Geo<D>::KS> Az;             // sig z in rows 0, 4, 8, 12 (normaliser) | unused
-  float z[Geo<D>::KS];               // sig z (as rounded in Az)          | dz
+  float z[Geo<D>::KS];               // sig z (as rounded in Az + Azl)    | dz
   float inv_scale;                   // unused                            | 1 / rho
   float bsig;                        // beta sig: phi(q) / den in the state gradients is
                                      // scaled by beta (<= min z, so beta phi(q) / den <= 1)
   float inv_beta;                    // 1 / beta
   float seps;                        // sig eps
-  Raw<T, Geo<D>::KS> Al[kSplitGrad<T> ? Geo<D>::NT : 1];  // unused | residual of A (bf16)
+  Raw<T, Geo<D>::KS> Al[kSplitGrad<T> ? Geo<D>::NT : 1];  // residual of A (bf16)
+  Raw<T, Geo<D>::KS> Bl[kSplitGrad<T> ? Geo<D>::NT : 1];  // residual of B (bf16) | unused
+  Raw<T, Geo<D>::KS> Azl;            // residual of Az (bf16)              | unused
 };
 
 // The transpose of a state as operands of a head-dim contraction: slot r of lane
@@ -594,22 +597,38 @@ __device__ __forceinline__ void make_state_op(const State<D>& st, BwdOp<T, D>& o
 #pragma unroll
     for (int et = 0; et < NT; ++et) col[et] = st.M[et][ct];
     op.A[ct] = tiles_operand<T, D>(col, sig);
+    if constexpr (kSplitGrad<T>) {
+      float x[KS], h[KS];
+      Frag<T, KS>::to_f32(op.A[ct], h);
+#pragma unroll
+      for (int r = 0; r < KS; ++r) x[r] = col[r >> 2][r & 3] * sig - h[r];
+      op.Al[ct] = Frag<T, KS>::from_f32(x);
+    }
   }
-  transposed_operand<T, D>(st, sig, tile, i, g, op.B);
-  // op.z holds sig z rounded exactly as in the normaliser operand Az: dq subtracts
+  transposed_operand<T, D, kSplitGrad<T>>(st, sig, tile, i, g, op.B, op.Bl);
+  // op.z holds sig z rounded exactly as in the normaliser operands: dq subtracts
   // (dout.o) z from dout S^T, and for a row whose normaliser is mostly eps the two
-  // terms cancel to eps / den; the same z on both sides keeps that residual exact
+  // terms cancel to eps / den; the same z on both sides keeps that residual exact.
+  // bf16 carries z as a pair (Az + Azl), as S is carried in A + Al: a z rounded
+  // to 8 bits against an S kept to 16 leaves the cancellation a 2^-9 remainder
   float zmin = 3.0e38f;
-  float zx[KS];
+  float zx[KS], zl[KS];
 #pragma unroll
   for (int r = 0; r < KS; ++r) {
     const float z = st.V[r >> 2][r & 3];
     if (PHI != kPhiRelu || z > 0.f) zmin = fminf(zmin, z);
-    const float zs = Ty<T>::kNarrow ? u16_to_f32<T>(f32_to_u16<T>(z * sig)) : z * sig;
+    const float zh = Ty<T>::kNarrow ? u16_to_f32<T>(f32_to_u16<T>(z * sig)) : z * sig;
+    float zs = zh;
+    if constexpr (kSplitGrad<T>) {
+      const float lo = u16_to_f32<T>(f32_to_u16<T>(z * sig - zh));
+      zs = zh + lo;
+      zl[r] = (i & 3) == 0 ? lo : 0.f;
+    }
     op.z[r] = zs;
-    zx[r] = (i & 3) == 0 ? zs : 0.f;
+    zx[r] = (i & 3) == 0 ? zh : 0.f;
   }
   op.Az = Frag<T, KS>::from_f32(zx);
+  if constexpr (kSplitGrad<T>) op.Azl = Frag<T, KS>::from_f32(zl);
   // phi(q)_e / den <= 1 / z_e <= 1 / min z, so beta phi(q) / den <= 1
   const float beta = Ty<T>::kNarrow ? pow2_floor(wave_reduce<false>(zmin)) : 1.f;
   op.bsig = beta * sig;
@@ -666,12 +685,14 @@ __device__ __forceinline__ void qgrad_seg(const Slice<T, Geo<D>::KS, NM>& sb, in
     phi_dphi<T, KS, PHI>(sb.x[QI][s], in, bq, dphq);
     F::to_f32(bq, fq);
     F::to_f32(dr[s], dox);
-    const floatx4 den4 = F::mma(op.Az, bq, zero);
+    floatx4 den4 = F::mma(op.Az, bq, zero);
+    if constexpr (SP) den4 = F::mma(op.Azl, bq, den4);
     const float rden = recip<T>(in ? den4[0] + op.seps : 1.f);
     float dot = 0.f;
 #pragma unroll
     for (int ct = 0; ct < NT; ++ct) {
-      const floatx4 d4 = F::mma(op.A[ct], bq, zero);
+      floatx4 d4 = F::mma(op.A[ct], bq, zero);
+      if constexpr (SP) d4 = F::mma(op.Al[ct], bq, d4);
 #pragma unroll
       for (int j = 0; j < 4; ++j) dot += dox[4 * ct + j] * d4[j];
     }
@@ -680,7 +701,8 @@ __device__ __forceinline__ void qgrad_seg(const Slice<T, Geo<D>::KS, NM>& sb, in
     float dqx[KS];
 #pragma unroll
     for (int et = 0; et < NT; ++et) {
-      const floatx4 d4 = F::mma(op.B[et], dr[s], zero);
+      floatx4 d4 = F::mma(op.B[et], dr[s], zero);
+      if constexpr (SP) d4 = F::mma(op.Bl[et], dr[s], d4);
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int r = 4 * et + j;

@@ -120,6 +120,12 @@ def forward_parity(S, ids, offsets, n, W, q, k, v, dtype, chunk_rows=0, label=""
     return got, ref
 
 
+# Gradients are held to half the 2e-2 bar in fp16 and bf16: the cancelling terms
+# of dq and dk (dout S^T against (dout.o) z, v dS^T against dz) run as hi/lo bf16
+# pairs, so what is left is the rounding of the stored inputs' images
+GRAD_TOL = {"f32": 1e-5, "f16": 1e-2, "bf16": 1e-2}
+
+
 def backward_parity(S, ids, offsets, n, W, q, k, v, do, dtype, chunk_rows=0, label="", fmap=None,
                     eps=None):
     import torch
@@ -139,7 +145,7 @@ def backward_parity(S, ids, offsets, n, W, q, k, v, do, dtype, chunk_rows=0, lab
     for name, x, r, fl in zip(("dq", "dk", "dv"), got, ref, floors):
         err = rel_err_per_head(x, r, fl, rows)
         _say(f"[bwd {label}] {name} n={n} dtype={dtype} rel_err={err:.3e}")
-        assert err <= TOL[dtype], f"{label}: {name} relative error {err:.3e}"
+        assert err <= GRAD_TOL[dtype], f"{label}: {name} relative error {err:.3e}"
     return got, ref
 
 
