@@ -1,17 +1,20 @@
 // SLA forward and backward on the gfx950 matrix cores.
 //
-// Work decomposition.  One wavefront per (chunk, head); a workgroup holds the
-// waves of up to four heads of one chunk, and the grid has one workgroup column
-// per chunk-table entry, so that every (chunk, head) of a scene is resident at
-// once (about 6 k waves for 1.5 k chunks and 4 heads) and the hardware
-// dispatcher balances them.  A chunk is a run of whole windows of the
-// window-sorted sequence (see the builder); its rows are read through the plan's
-// permutation, so q, k, v stay in the caller's order.
+// Work decomposition.  A persistent grid (about one workgroup per resident
+// slot, a multiple of 8) of four-wave workgroups walks a list of work items (see
+// item_slot in the core header): first one item per long window and head, whose
+// rows the four waves (or two, for windows of medium length) split between them
+// and whose partial states they add in LDS, then one item per chunk and group of
+// up to four heads, one wave per head.  A chunk is a run of whole short windows
+// of the window-sorted sequence (see the builder); its rows are read through the
+// plan's permutation, so q, k, v stay in the caller's order.
 //
-// A wave walks its chunk window by window as a stream of 32-row jobs (forward:
-// K,V rows into the state, then Q rows through it; backward: K,V, then Q,dout,
-// then K,V again) and keeps two jobs' rows in flight ahead of the one it
-// computes, so each wave has about three gathers outstanding at any time.
+// A wave holds its item's rows (up to kMaxChunkRows of q, k, v, and dout in the
+// backward) in registers for the whole item and walks its windows from there; a
+// share of a very long window that exceeds that is streamed through in blocks.
+// Items are software-pipelined per wave through an LDS ring: while item k
+// computes, the permutation slice and window offsets of item k + 1 and the plan
+// entry of item k + 2 are already in flight.
 //
 // Per window (Eq. (3); the chunk-wise state accumulation of Sec. 3.2 / Fig. 3(b)):
 //   state    S = phi(K)^T V and z = phi(K)^T 1 on the matrix cores over the
