@@ -138,7 +138,15 @@ sla_status_t sla_plan_layout(int64_t n, int32_t num_windows, sla_plan_layout_t* 
  * invalid_count (device int32, may be NULL) receives the number of out-of-range
  * ids (mode A) or offset violations (mode B).  The plan must be at least
  * sla_plan_bytes(n, num_windows) bytes, 256-byte aligned.  Valid for num_windows
- * in [1, sla_max_windows()].
+ * in [1, sla_max_windows()]; mode A also needs n <= 2^26 (SLA_E_UNSUPPORTED
+ * beyond).
+ *
+ * Plan scratch: mode A accumulates window totals in a region of the plan that
+ * must read zero when the build starts, and every build leaves it zero again.
+ * So zero-fill a plan buffer once after allocating it (hipMemset), before its
+ * first build; after that it can be rebuilt any number of times, for any n and
+ * num_windows it is large enough for.  Builds into one plan buffer must not
+ * overlap in time.
  */
 sla_status_t sla_build_segments(const int32_t* window_ids, int64_t n, int32_t num_windows,
                                 int32_t chunk_rows, int32_t* perm_out, int32_t* offsets,

@@ -174,6 +174,8 @@ SLA_EXPORT sla_status_t sla_build_segments(const int32_t* window_ids, int64_t n,
     if (offsets == nullptr || perm_out != nullptr) return SLA_E_ARG;  // CSR input mode
   } else if (n > 0 && !aligned(window_ids, 4)) {
     return SLA_E_ARG;
+  } else if (n > sla::kBuilderMaxRows) {
+    return SLA_E_UNSUPPORTED;
   }
   return hip_status(sla::launch_build(window_ids,
                                       (int32_t)n, num_windows, chunk_rows, perm_out, offsets,

@@ -3,18 +3,19 @@
 // flattened matrix that is partitioned into chunks; the offset generation timed
 // in Fig. 5 computes the start of every chunk).
 //
-// Mode A (ids given), two launches over builder blocks of E rows:
-//   k_count    per block, a histogram of its rows' window ids (LDS atomics; the
-//              counts are order-free, hence deterministic) -> count matrix;
-//   k_scatter  per block: the column prefix of the count matrix over the blocks
-//              before it and the column totals (read straight from the matrix),
-//              the exclusive scan of the totals (= offsets) in LDS, then the
-//              stable rank of every row among the rows of its window in this
-//              block (wave ballots on the id bits give the lanes sharing an id;
-//              waves take their bases in order) and perm[offsets[id] + block
-//              prefix + rank] = row.  One more workgroup (the last) computes the
-//              same totals and publishes the offsets, the chunk table and the
-//              header.
+// Mode A (ids given), two launches:
+//   k_sort   per builder block of E rows: a stable LSD radix sort of the block's
+//            rows by window id in LDS, and the exclusive prefix of the block's
+//            window counts (the start of every window's run in the block);
+//            it also adds the block's window counts to the plan's window totals;
+//   k_merge  one workgroup turns the totals into the offsets, the chunk and
+//            long-window tables and the header (and clears the totals); the
+//            others take a range of windows each: offsets from the blocks' prefix
+//            rows, and every sorted position of the range filled from the run of
+//            the block it falls in.
+// No workgroup waits on another, and every sum is an integer sum, so the result
+// is deterministic.  The totals must be zero when a build starts: a new plan
+// buffer is zero-filled once, and every build leaves them zero.
 // Mode B (CSR offsets given) and n = 0: one workgroup, k_plan, validates the
 // offsets and writes the chunk table and header.
 #include <atomic>
@@ -35,30 +36,16 @@ __device__ __forceinline__ void lds_sync() {
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
-// ------------------------------------------------------------------ k_count
-__global__ __launch_bounds__(kBuildThreads) void k_count(const int32_t* __restrict__ ids, int32_t n,
-                                                         int32_t W, int32_t E, int32_t ld,
-                                                         int32_t* __restrict__ counts) {
-  __shared__ int32_t hist[kMaxWindows + 1];
-  for (int i = threadIdx.x; i <= W; i += blockDim.x) hist[i] = 0;
-  lds_sync();
-  const int64_t base = (int64_t)blockIdx.x * E;
-  const int64_t end = base + E < n ? base + E : n;
-  for (int64_t i = base + threadIdx.x; i < end; i += blockDim.x) {
-    const int32_t id = ids[i];
-    atomicAdd(&hist[(uint32_t)id < (uint32_t)W ? id : W], 1);
-  }
-  lds_sync();
-  int32_t* row = counts + (size_t)blockIdx.x * ld;
-  for (int i = threadIdx.x; i < ld; i += blockDim.x) row[i] = i <= W ? hist[i] : 0;
-}
-
 // -------------------------------------------------------- block-wide scans
 struct OpSum {
   __device__ int32_t operator()(int32_t a, int32_t b) const { return a + b; }
 };
 struct OpSum64 {
   __device__ uint64_t operator()(uint64_t a, uint64_t b) const { return a + b; }
+};
+template <typename V>
+struct OpSumT {
+  __device__ V operator()(V a, V b) const { return a + b; }
 };
 struct OpMax {
   __device__ int32_t operator()(int32_t a, int32_t b) const { return a > b ? a : b; }
@@ -134,6 +121,37 @@ __device__ V block_exscan(V x, V identity, Op op, V* s, V* total) {
   return r;
 }
 
+// Exclusive scan of one value per thread in thread order with one barrier; *total
+// gets the reduction of all values.  The wave totals in s[0..15] must stay
+// untouched until the caller's next barrier.
+template <class Op, typename V>
+__device__ __forceinline__ V block_exscan1(V x, V identity, Op op, V* s, V* total) {
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6, nwv = blockDim.x >> 6;
+  const V inc = wave_inclusive_scan(x, identity, op);
+  if (lane == 63) s[wv] = inc;
+  // exclusive inside the wave: the inclusive value of the lane before (wave_shr:1)
+  V ex;
+  if constexpr (sizeof(V) == 4) {
+    ex = (V)__builtin_amdgcn_update_dpp((int)identity, (int)inc, 0x138, 0xf, 0xf, false);
+  } else {
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp((int)(uint32_t)identity, (int)(uint32_t)inc,
+                                                              0x138, 0xf, 0xf, false);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp((int)(uint32_t)(identity >> 32),
+                                                              (int)(uint32_t)(inc >> 32), 0x138, 0xf, 0xf,
+                                                              false);
+    ex = ((V)hi << 32) | lo;
+  }
+  lds_sync();
+  V before = identity, all = identity;
+  for (int u = 0; u < nwv; ++u) {
+    const V t = s[u];
+    if (u < wv) before = op(before, t);
+    all = op(all, t);
+  }
+  *total = all;
+  return op(before, ex);
+}
+
 // ------------------------------------------------------ chunk / long tables
 // Work tables from the offsets in LDS, in sequence order (pages of P = L/2 rows):
 // a window of more than L rows is "long" and goes to the long-window table
@@ -141,55 +159,58 @@ __device__ V block_exscan(V x, V identity, Op op, V* s, V* total) {
 // P+1..L rows is a chunk of its own; a window of 1..P rows opens a chunk unless
 // the previous non-empty window is short and starts in the same page.  A chunk
 // runs to the next event (chunk start or long window).  s_aux: LDS scratch of at
-// least W ints.  Every thread of the block calls it; returns the number of
-// chunks and sets *n_long and *n_long4.
+// least W ints.  Every thread of the block calls it (at most 32 windows a thread:
+// W <= 32 blockDim.x); returns the number of chunks and sets *n_long and
+// *n_long4.
 __device__ int32_t build_tables(const int32_t* s_off, int32_t* s_aux, int32_t W, int32_t L,
                                 Chunk* __restrict__ chunks, LongWin* __restrict__ longs,
                                 int32_t* s_scan, uint64_t* s_scan2, int32_t* n_long,
                                 int32_t* n_long4) {
   const int tid = threadIdx.x, T = blockDim.x;
   const int32_t page = L >> 1;
+  // x / page = (x m) >> 37 with m = ceil(2^37 / page), exact for 0 <= x < 2^31 and
+  // page <= 32 (the rounding error stays below 1/64, the distance of x / page to
+  // the next integer at least 1/32)
+  const uint64_t pm = ((1ull << 37) + (uint64_t)page - 1) / (uint64_t)page;
+  auto page_of = [&](int32_t x) -> uint32_t { return (uint32_t)(((uint64_t)(uint32_t)x * pm) >> 37); };
   const int P = (W + T - 1) / T;
   const int w0 = min(tid * P, W), w1 = min(w0 + P, W);
   // the start of the last non-empty window and the end of the last window of
   // more than P rows before my range decide the kind of my first window
   int32_t aggStart = -1, aggWide = -1;
   for (int w = w0; w < w1; ++w) {
-    const int32_t len = s_off[w + 1] - s_off[w];
-    if (len > 0) aggStart = s_off[w];
-    if (len > page) aggWide = s_off[w + 1];
+    const int32_t a = s_off[w], len = s_off[w + 1] - a;
+    if (len > 0) aggStart = a;
+    if (len > page) aggWide = a + len;
   }
   // both maxima in one scan of (value + 1) pairs
   uint64_t tmp;
-  const uint64_t both = block_exscan<OpMax2, uint64_t>(
+  const uint64_t both = block_exscan1<OpMax2, uint64_t>(
       ((uint64_t)(uint32_t)(aggStart + 1) << 32) | (uint32_t)(aggWide + 1), 0ull, OpMax2(), s_scan2,
       &tmp);
-  const int32_t lastStart = (int32_t)(both >> 32) - 1;
-  const int32_t lastWideEnd = (int32_t)(uint32_t)both - 1;
   // 0: no event, 1: opens a chunk, 2: two-way long window, 3: four-way long
-  // window.  ls / ll: start of the previous non-empty window / end of the
-  // previous window of more than P rows (ll == a exactly when the previous
-  // non-empty window is not short).
-  auto kind = [&](int32_t& ls, int32_t& ll, int w) -> int {
-    const int32_t a = s_off[w], len = s_off[w + 1] - a;
-    if (len <= 0) return 0;
-    int k = 0;
-    if (len > L) k = len > 2 * L ? 3 : 2;
-    else if (len > page || ls < 0 || ll == a || (ls / page) != (a / page)) k = 1;
-    ls = a;
-    if (len > page) ll = a + len;
-    return k;
-  };
+  // window; 2 bits a window in `codes`
+  uint64_t codes = 0;
   uint64_t cnt = 0;   // chunks, two-way, four-way: 21 bits each (W <= 16384)
   {
-    int32_t ls = lastStart, ll = lastWideEnd;
+    int32_t ls = (int32_t)(both >> 32) - 1;          // start of the previous non-empty window
+    int32_t ll = (int32_t)(uint32_t)both - 1;        // end of the previous window of > P rows
     for (int w = w0; w < w1; ++w) {
-      const int k = kind(ls, ll, w);
+      const int32_t a = s_off[w], len = s_off[w + 1] - a;
+      int k = 0;
+      if (len > 0) {
+        if (len > L) k = len > 2 * L ? 3 : 2;
+        else if (len > page || ls < 0 || ll == a || page_of(ls) != page_of(a)) k = 1;
+        ls = a;
+        if (len > page) ll = a + len;
+      }
+      codes |= (uint64_t)k << (2 * (w - w0));
       if (k) cnt += 1ull << (21 * (k - 1));
     }
   }
+  lds_sync();   // s_scan2 is reused
   uint64_t tot = 0;
-  const uint64_t ex = block_exscan<OpSum64, uint64_t>(cnt, 0ull, OpSum64(), s_scan2, &tot);
+  const uint64_t ex = block_exscan1<OpSum64, uint64_t>(cnt, 0ull, OpSum64(), s_scan2, &tot);
   constexpr uint64_t kMask = (1ull << 21) - 1;
   const int32_t s0 = (int32_t)(ex & kMask), t0 = (int32_t)((ex >> 21) & kMask),
                 f0 = (int32_t)(ex >> 42);
@@ -197,16 +218,16 @@ __device__ int32_t build_tables(const int32_t* s_off, int32_t* s_aux, int32_t W,
                 n4 = (int32_t)(tot >> 42);
   {
     // the event list in sequence order: s_aux[event index] = window
-    int32_t ls = lastStart, ll = lastWideEnd, e = s0 + t0 + f0;
+    int32_t e = s0 + t0 + f0;
     for (int w = w0; w < w1; ++w)
-      if (kind(ls, ll, w)) s_aux[e++] = w;
+      if ((codes >> (2 * (w - w0))) & 3u) s_aux[e++] = w;
   }
   lds_sync();
   {
-    int32_t ls = lastStart, ll = lastWideEnd, sc = s0, s2 = t0, s4 = f0;
+    int32_t sc = s0, s2 = t0, s4 = f0;
     const int32_t nE = nC + n2 + n4;
     for (int w = w0; w < w1; ++w) {
-      const int k = kind(ls, ll, w);
+      const int k = (int)((codes >> (2 * (w - w0))) & 3u);
       if (k == 1) {
         const int32_t e = sc + s2 + s4;
         Chunk ch;
@@ -299,7 +320,7 @@ __global__ __launch_bounds__(kBuildThreads) void k_plan(int32_t csr, int32_t W, 
   if (tid == 0) write_header(hdr, n, W, L, n_chunks, n_long, n_long4, csr, invalid, invalid_out);
 }
 
-// --------------------------------------------------------------- k_scatter
+// ------------------------------------------------------------ row ranking
 // Lanes whose (valid) key equals this lane's key; 0 for invalid lanes.  One
 // ballot per key bit: a lane matches iff it agrees with this lane on every bit.
 __device__ __forceinline__ uint64_t match_key(int32_t key, bool valid, int nbits) {
@@ -316,247 +337,274 @@ __device__ __forceinline__ uint64_t lanemask_lt(int lane) {
   return lane == 0 ? 0ull : (~0ull >> (64 - lane));
 }
 
-// Dynamic LDS: base[W + 1], tot[W + 1], hist[max(nws W, W + 1)] (overlap) or
-// base[W + 1], hist[max(nws W, W + 1)] with tot = hist (no overlap, large W);
-// nws = waves that rank rows.  Blocks 0..nb-1 rank and scatter the rows of
-// builder block blockIdx.x; block nb publishes the offsets and builds the chunk
-// and long-window tables and the header, in parallel with the others.
-//
-// A ranking block requests its rows' window ids and its share of the count
-// matrix first; with `overlap` it counts its rows per wave (which needs only the
-// ids) while the matrix is in flight; then the column prefix and totals, the
-// offsets, the per-wave prefix and the scatter.
-constexpr int kMatBatch = 16;   // count-matrix rows a thread has in flight at once
+// ------------------------------------------------------------------ k_sort
+// One workgroup per builder block of E = 1024 R rows.  Sorts the block's rows by
+// key (window id; W for an id outside [0, W); W + 1 for the padding after the
+// last row) with a stable LSD radix sort in LDS, 8 key bits per pass (at most two
+// passes, W <= 16384): a wave ranks its rows 64 at a time in row order (ballots
+// find the lanes with the same digit), a scan over (digit, wave) gives every row
+// its place.  Writes
+//   sorted[block E + p]   row at position p of the block's sorted order;
+//   counts[block][x]      rows of the block with key < x, x = 0..W (the start of
+//                         window x's run in the block's sorted order);
+// and adds its window counts (x = 0..W; x = W counts the ids outside [0, W)) to
+// the window totals, integer atomics, so the sums do not depend on their order.
+// Both go out as soon as the histogram is complete, under the radix passes.
+// LDS: hist[ld] | buf[2][E] | wcnt[2][256][16] (one count table when R = 8).
+constexpr int kSortThreads = 1024;
+constexpr int kSortWaves = kSortThreads / 64;
+constexpr int kDigits = 256;
+constexpr int kPosBits = 13;   // position of a row in its block (E <= 8192)
 
-__global__ __launch_bounds__(kBuildThreads) void k_scatter(
-    const int32_t* __restrict__ ids, int32_t n, int32_t W, int32_t L, int32_t E, int32_t nb,
-    int32_t ld, int32_t nws, int32_t overlap, const int32_t* __restrict__ counts,
-    int32_t* __restrict__ perm, int32_t* __restrict__ perm_out, int32_t* __restrict__ plan_offsets,
-    int32_t* __restrict__ offsets_out, Chunk* __restrict__ chunks, LongWin* __restrict__ longs,
-    PlanHeader* __restrict__ hdr, int32_t* __restrict__ invalid_out) {
+// Exclusive sum over the threads of the block in thread order, one barrier; the
+// wave totals in s[0..15] must stay untouched until the caller's next barrier.
+template <typename V>
+__device__ __forceinline__ V block_exsum(V x, V* s) {
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const V inc = wave_inclusive_scan(x, (V)0, OpSumT<V>());
+  if (lane == 63) s[wv] = inc;
+  lds_sync();
+  V before = 0;
+  for (int u = 0; u < wv; ++u) before += s[u];
+  return before + inc - x;
+}
+
+template <int R>
+__global__ __launch_bounds__(kSortThreads) void k_sort(const int32_t* __restrict__ ids, int32_t n,
+                                                      int32_t W, int32_t ld,
+                                                      int32_t* __restrict__ counts,
+                                                      int32_t* __restrict__ sorted,
+                                                      int32_t* __restrict__ totals) {
+  constexpr int E = kSortThreads * R;
+  constexpr bool kTwoTables = R <= 4;   // LDS budget at W = 16384
+  constexpr int kTable = kDigits * kSortWaves;
+  static_assert(E <= (1 << kPosBits), "row positions fit their field");
+  extern __shared__ int32_t lds[];
+  __shared__ uint64_t s_scan[kSortWaves];
+  int32_t* hist = lds;
+  uint32_t* buf = reinterpret_cast<uint32_t*>(lds + ld);   // buf[0..E) and buf[E..2E)
+  int32_t* wcnt = lds + ld + 2 * E;                         // table t at wcnt + t kTable
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int64_t base = (int64_t)blockIdx.x * E;
+  const int32_t rows = (int32_t)(n - base < E ? n - base : E);
+  // sub-group r of wave wv holds positions wv 64 R + 64 r + lane (row order)
+  uint32_t el[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const int pos = wv * 64 * R + 64 * r + lane;
+    uint32_t key = (uint32_t)W + 1u;
+    if (pos < rows) {
+      const int32_t id = ids[base + pos];
+      key = (uint32_t)id < (uint32_t)W ? (uint32_t)id : (uint32_t)W;
+    }
+    el[r] = (key << kPosBits) | (uint32_t)pos;
+  }
+  for (int i = tid; i < ld; i += kSortThreads) hist[i] = 0;
+  for (int i = tid; i < (kTwoTables ? 2 : 1) * kTable; i += kSortThreads) wcnt[i] = 0;
+  lds_sync();
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const uint32_t key = el[r] >> kPosBits;
+    if (key <= (uint32_t)W) atomicAdd(&hist[key], 1);
+  }
+
+  const int kbits = 32 - __clz(W + 1);   // bits of the largest key, W + 1
+  const int X = (W + 1 + kSortThreads - 1) / kSortThreads;
+  const int x0 = min(tid * X, W + 1), x1 = min(x0 + X, W + 1);
+  const uint64_t lt = lanemask_lt(lane);
+  for (int pass = 0, shift = 0; shift < kbits; ++pass, shift += 8) {
+    const int dbits = kbits - shift < 8 ? kbits - shift : 8;
+    int32_t* tab = wcnt + (kTwoTables ? pass * kTable : 0);
+    // (1) ranks inside the wave, sub-groups in row order
+    int32_t rk[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      const int32_t d = (int32_t)((el[r] >> (kPosBits + shift)) & 0xffu);
+      const uint64_t m = match_key(d, true, dbits);
+      int32_t* slot = &tab[d * kSortWaves + wv];
+      const int32_t before = *slot;   // a wave's LDS accesses complete in order
+      if ((m & lt) == 0) *slot = before + __popcll(m);
+      rk[r] = before + __popcll(m & lt);
+    }
+    lds_sync();
+    // (2) exclusive scan of the table in (digit, wave) order, four entries a
+    // thread; the first pass also scans the histogram (high half of the sum)
+    int32_t v[4], hsum = 0;
+    uint64_t sum = 0;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      v[k] = tab[4 * tid + k];
+      sum += (uint32_t)v[k];
+    }
+    if (pass == 0) {
+      for (int x = x0; x < x1; ++x) hsum += hist[x];
+      sum |= (uint64_t)(uint32_t)hsum << 32;
+    }
+    const uint64_t ex = block_exsum<uint64_t>(sum, s_scan);
+    int32_t e = (int32_t)(uint32_t)ex;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      tab[4 * tid + k] = e;
+      e += v[k];
+    }
+    if (pass == 0) {
+      // the block's prefix row and its share of the totals leave now
+      int32_t h = (int32_t)(ex >> 32);
+      int32_t* row = counts + (size_t)blockIdx.x * ld;
+      for (int x = x0; x < x1; ++x) {
+        const int32_t c = hist[x];
+        row[x] = h;
+        h += c;
+        if (c) __hip_atomic_fetch_add(totals + x, c, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+    }
+    lds_sync();
+    // (3) every row to its place
+    uint32_t* dst = buf + (pass & 1) * E;
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      const int32_t d = (int32_t)((el[r] >> (kPosBits + shift)) & 0xffu);
+      dst[tab[d * kSortWaves + wv] + rk[r]] = el[r];
+    }
+    lds_sync();
+#pragma unroll
+    for (int r = 0; r < R; ++r) el[r] = dst[wv * 64 * R + 64 * r + lane];
+    if (!kTwoTables && shift + 8 < kbits) {
+      for (int i = tid; i < kTable; i += kSortThreads) tab[i] = 0;
+      lds_sync();
+    }
+  }
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const int pos = wv * 64 * R + 64 * r + lane;
+    if (pos < rows) sorted[base + pos] = (int32_t)(base + (el[r] & ((1u << kPosBits) - 1u)));
+  }
+}
+
+// ------------------------------------------------------------------ k_merge
+// Workgroup 0 writes the offsets (the exclusive scan of the window totals), the
+// chunk and long-window tables and the header, and clears the totals for the next
+// build.  Workgroup 1 + r takes the range of ww windows [w0, w0 + nx): from the
+// blocks' prefix rows (counts[b][x], x = w0..w0 + nx) it forms, per column x, the
+// exclusive sum over blocks ex[x][b] = sum_{b' < b} counts[b'][x]; ex[x][nb] is
+// offsets[x] (rows with a window id below x, over all blocks), and the rows of
+// window w in block b follow those of blocks b' < b:
+//   sorted position offsets[w] + pre(b) + j, pre(b) = ex[w + 1][b] - ex[w][b],
+//   is row sorted[b E + counts[b][w] + j].
+// Every sorted position of the range finds its block by binary search over pre.
+// No workgroup waits for another.
+constexpr int kMergeThreads = 1024;
+
+__global__ __launch_bounds__(kMergeThreads) void k_merge(
+    int32_t n, int32_t W, int32_t L, int32_t E, int32_t nb, int32_t ld, int32_t ww,
+    const int32_t* __restrict__ counts, const int32_t* __restrict__ sorted,
+    int32_t* __restrict__ totals, int32_t* __restrict__ perm, int32_t* __restrict__ perm_out,
+    int32_t* __restrict__ plan_offsets, int32_t* __restrict__ offsets_out,
+    Chunk* __restrict__ chunks, LongWin* __restrict__ longs, PlanHeader* __restrict__ hdr,
+    int32_t* __restrict__ invalid_out) {
   extern __shared__ int32_t lds[];
   __shared__ int32_t s_scan[33];
   __shared__ uint64_t s_scan2[33];
-  int32_t* base = lds;                              // offsets[w] + rows of window w in earlier blocks
-  int32_t* tot = lds + (W + 1);                     // column totals
-  int32_t* hist = overlap ? tot + (W + 1) : tot;    // per-wave row counts (table block: scratch)
-  const int tid = threadIdx.x, T = blockDim.x;
-  const int lane = tid & 63, wv = tid >> 6;
-  const int32_t blk = blockIdx.x;
-  const bool tables = blk == nb;
-
-  // this wave's rows [rbeg, rend): ids of the first two 64-row groups
-  const int64_t span = E / nws;
-  const int64_t rbeg = (int64_t)blk * E + wv * span;
-  const int64_t rend = rbeg + span < n ? rbeg + span : n;
-  const bool ranks = !tables && wv < nws;
-  int32_t id0 = -1, id1 = -1;
-  if (ranks) {
-    if (rbeg + lane < rend) id0 = ids[rbeg + lane];
-    if (rbeg + 64 + lane < rend) id1 = ids[rbeg + 64 + lane];
-  }
-
-  // count-matrix shares: unit (part, g) sums rows [part RP, part RP + RP) of
-  // column group g (4 columns, one 16-B load per row); a thread takes units tid,
-  // tid + T, ...; the first kMatBatch rows of its first unit are requested now
-  const int G = ld >> 2;
-  const int R = max(1, min(T / G, nb));
-  const int RP = (nb + R - 1) / R;
-  const int NU = R * G;
-  int4 x[kMatBatch];
-  {
-    const int part = tid / G, cg = tid - part * G;
-    const int b0 = part * RP, b1 = min(b0 + RP, nb);
-#pragma unroll
-    for (int u = 0; u < kMatBatch; ++u)
-      x[u] = tid < NU && b0 + u < b1 ? reinterpret_cast<const int4*>(counts + (size_t)(b0 + u) * ld)[cg]
-                                     : make_int4(0, 0, 0, 0);
-  }
-
-  for (int w = tid; w <= W; w += T) {
-    base[w] = 0;
-    tot[w] = 0;
-  }
-  if (!tables && overlap)   // every thread of the block: the loop is strided over all of them
-    for (int i = tid; i < nws * W; i += T) hist[i] = 0;
-  lds_sync();
-
-  // (a) ranking blocks: per-wave window counts of the wave's rows
-  const int nbits = W > 1 ? 32 - __clz(W - 1) : 0;
-  int32_t* h = hist + wv * W;
-  const uint64_t lt = lanemask_lt(lane);
-  // returns the row's rank among this wave's rows of its window (-1: invalid id)
-  auto count_group = [&](int32_t id) -> int32_t {
-    const bool valid = (uint32_t)id < (uint32_t)W;
-    const uint64_t m = match_key(id, valid, nbits);
-    if (!valid) return -1;
-    const int32_t hb = h[id];
-    if ((m & lt) == 0) h[id] = hb + __popcll(m);
-    return hb + __popcll(m & lt);
-  };
-  auto id_at = [&](int64_t r) -> int32_t { return r + lane < rend ? ids[r + lane] : -1; };
-  int32_t rk0 = -1, rk1 = -1;   // ranks of the first two groups' rows
-  auto count_rows = [&]() {
-    if (ranks) {
-      rk0 = count_group(id0);
-      if (rbeg + 64 < rend) rk1 = count_group(id1);
-      for (int64_t r = rbeg + 128; r < rend; r += 64) count_group(id_at(r));
-    }
-  };
-  if (overlap) count_rows();
-
-  // (b) column prefix over the earlier blocks and column totals
-  for (int unit = tid; unit < NU; unit += T) {
-    const int part = unit / G, cg = unit - part * G;
-    const int b0 = part * RP, b1 = min(b0 + RP, nb);
-    int4 pre = make_int4(0, 0, 0, 0), sum = make_int4(0, 0, 0, 0);
-    for (int b = b0; b < b1; b += kMatBatch) {
-      if (unit != tid || b != b0) {
-#pragma unroll
-        for (int u = 0; u < kMatBatch; ++u)
-          x[u] = b + u < b1 ? reinterpret_cast<const int4*>(counts + (size_t)(b + u) * ld)[cg]
-                            : make_int4(0, 0, 0, 0);
-      }
-#pragma unroll
-      for (int u = 0; u < kMatBatch; ++u) {
-        sum.x += x[u].x; sum.y += x[u].y; sum.z += x[u].z; sum.w += x[u].w;
-        if (b + u < blk) { pre.x += x[u].x; pre.y += x[u].y; pre.z += x[u].z; pre.w += x[u].w; }
-      }
-    }
-    const int w = 4 * cg;
-    const int32_t p4[4] = {pre.x, pre.y, pre.z, pre.w}, t4[4] = {sum.x, sum.y, sum.z, sum.w};
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      if (w + k <= W) {
-        if (R > 1) {
-          atomicAdd(&base[w + k], p4[k]);
-          atomicAdd(&tot[w + k], t4[k]);
-        } else {
-          base[w + k] = p4[k];
-          tot[w + k] = t4[k];
-        }
-      }
-    }
-  }
-  lds_sync();
-  const int32_t invalid = tot[W];   // column W counts the out-of-range ids
-
-  // (c) offsets = exclusive scan of the column totals; base += offsets
-  {
-    const int P = (W + T - 1) / T;
-    const int w0 = min(tid * P, W), w1 = min(w0 + P, W);
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  if (blockIdx.x == 0) {
+    int32_t* s_off = lds;
+    int32_t* s_aux = lds + (W + 1);
+    const int P = (W + 1 + kMergeThreads - 1) / kMergeThreads;
+    const int x0 = min(tid * P, W + 1), x1 = min(x0 + P, W + 1);
     int32_t local = 0;
-    for (int w = w0; w < w1; ++w) local += tot[w];
+    for (int x = x0; x < x1; ++x) {
+      const int32_t t = totals[x];
+      s_off[x] = t;
+      local += x < W ? t : 0;
+      totals[x] = 0;
+    }
     int32_t total = 0;
     int32_t ex = block_exscan(local, 0, OpSum(), s_scan, &total);
-    if (tables) {
-      // the table block: base[0..W] become the offsets
-      for (int w = w0; w < w1; ++w) {
-        const int32_t t = tot[w];
-        base[w] = ex;
-        plan_offsets[w] = ex;
-        if (offsets_out) offsets_out[w] = ex;
-        ex += t;
-      }
-      if (tid == 0) {
-        base[W] = total;
-        plan_offsets[W] = total;
-        if (offsets_out) offsets_out[W] = total;
-      }
-      lds_sync();
-      int32_t n_long = 0, n_long4 = 0;
-      const int32_t n_chunks =
-          build_tables(base, hist, W, L, chunks, longs, s_scan, s_scan2, &n_long, &n_long4);
-      if (tid == 0) write_header(hdr, n, W, L, n_chunks, n_long, n_long4, 0, invalid, invalid_out);
-      return;
-    }
-    for (int w = w0; w < w1; ++w) {
-      const int32_t t = tot[w];
-      base[w] += ex;
+    const int32_t invalid = s_off[W];   // read before any thread overwrites it
+    lds_sync();
+    for (int x = x0; x < x1; ++x) {
+      const int32_t t = s_off[x];
+      s_off[x] = ex;
+      plan_offsets[x] = ex;
+      if (offsets_out) offsets_out[x] = ex;
       ex += t;
     }
+    lds_sync();
+    int32_t n_long = 0, n_long4 = 0;
+    const int32_t n_chunks =
+        build_tables(s_off, s_aux, W, L, chunks, longs, s_scan, s_scan2, &n_long, &n_long4);
+    if (tid == 0) write_header(hdr, n, W, L, n_chunks, n_long, n_long4, 0, invalid, invalid_out);
+    return;
   }
-  if (!overlap) {
-    // hist takes the place of the totals now
-    lds_sync();
-    for (int i = tid; i < nws * W; i += T) hist[i] = 0;
-    lds_sync();
-    count_rows();
-    lds_sync();
+  const int32_t w0 = ((int32_t)blockIdx.x - 1) * ww;
+  const int nx = min(ww, W - w0);
+  const int S = nb + 1;
+  int32_t* ex = lds;   // ex[xi S + b], xi = 0..nx, b = 0..nb
+  // (1) the tile, row by row of the matrix (nx + 1 consecutive ints per block)
+  for (int f = tid; f < nb * (nx + 1); f += kMergeThreads) {
+    const int b = f / (nx + 1), xi = f - b * (nx + 1);
+    ex[xi * S + b + 1] = counts[(size_t)b * ld + w0 + xi];
   }
-  // (d) exclusive prefix of the per-wave counts over the waves (all of a
-  // window's counts are read before any is written back)
-  for (int w = tid; w < W; w += T) {
-    int32_t t[kBuildThreads / 64];
-#pragma unroll
-    for (int v = 0; v < kBuildThreads / 64; ++v) t[v] = v < nws ? hist[v * W + w] : 0;
-    int32_t run = 0;
-#pragma unroll
-    for (int v = 0; v < kBuildThreads / 64; ++v) {
-      if (v < nws) hist[v * W + w] = run;
-      run += t[v];
+  if (tid <= nx) ex[tid * S] = 0;
+  lds_sync();
+  // (2) inclusive scan of every column over the blocks, one wave a column
+  for (int xi = wv; xi <= nx; xi += kMergeThreads / 64) {
+    int32_t carry = 0;
+    for (int b0 = 1; b0 <= nb; b0 += 64) {
+      const int b = b0 + lane;
+      const int32_t v = b <= nb ? ex[xi * S + b] : 0;
+      const int32_t inc = wave_inclusive_scan(v, 0, OpSum()) + carry;
+      if (b <= nb) ex[xi * S + b] = inc;
+      carry = __builtin_amdgcn_readlane(inc, 63);
     }
   }
   lds_sync();
-
-  // (e) scatter, each wave with its running counters
-  auto scatter_group = [&](int64_t r, int32_t id) {
-    const int64_t i = r + lane;
-    const bool valid = (uint32_t)id < (uint32_t)W;
-    const uint64_t m = match_key(id, valid, nbits);
-    if (valid) {
-      const int32_t hb = h[id];
-      const int32_t pos = base[id] + hb + __popcll(m & lt);
-      if ((uint32_t)pos < (uint32_t)n) {
-        perm[pos] = (int32_t)i;
-        if (perm_out) perm_out[pos] = (int32_t)i;
-      }
-      if ((m & lt) == 0) h[id] = hb + __popcll(m);
+  // (3) the range's sorted positions
+  const int32_t p0 = ex[nb], p1 = ex[nx * S + nb];
+  for (int32_t p = p0 + tid; p < p1; p += kMergeThreads) {
+    int lo = 0, hi = nx - 1;   // last window of the range starting at or before p
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (ex[mid * S + nb] <= p) lo = mid; else hi = mid - 1;
     }
-  };
-  auto place = [&](int64_t r, int32_t id, int32_t rk) {
-    if (rk < 0) return;
-    const int32_t pos = base[id] + h[id] + rk;
-    if ((uint32_t)pos < (uint32_t)n) {
-      perm[pos] = (int32_t)(r + lane);
-      if (perm_out) perm_out[pos] = (int32_t)(r + lane);
+    const int wi = lo;
+    const int32_t q = p - ex[wi * S + nb];
+    const int32_t* e0 = ex + wi * S;
+    const int32_t* e1 = e0 + S;
+    int bl = 0, bh = nb - 1;   // last block whose rows of window wi start at or before q
+    while (bl < bh) {
+      const int mid = (bl + bh + 1) >> 1;
+      if (e1[mid] - e0[mid] <= q) bl = mid; else bh = mid - 1;
     }
-  };
-  if (ranks) {
-    if (span <= 128) {
-      // every row of the wave was ranked by the counting pass
-      place(rbeg, id0, rk0);
-      if (rbeg + 64 < rend) place(rbeg + 64, id1, rk1);
-    } else {
-      scatter_group(rbeg, id0);
-      if (rbeg + 64 < rend) scatter_group(rbeg + 64, id1);
-      for (int64_t r = rbeg + 128; r < rend; r += 64) scatter_group(r, id_at(r));
+    const int32_t j = q - (e1[bl] - e0[bl]);
+    const int32_t start = e0[bl + 1] - e0[bl];
+    const int64_t at = (int64_t)bl * E + start + j;
+    const int32_t row = at < n ? sorted[at] : 0;
+    if (p < n) {
+      perm[p] = row;
+      if (perm_out) perm_out[p] = row;
     }
   }
-}
-
-// Waves of k_scatter that rank rows: as many as the LDS holds (<= 16), and at
-// most one per 64 rows of a block.
-// Prefers the overlapped layout; large W falls back to the sequential one.
-static int scatter_waves(int32_t W, int32_t E, size_t* lds_bytes, int* overlap) {
-  constexpr size_t kLds = 160 * 1024 - 1024;   // leave room for the static arrays
-  auto bytes = [&](int v, int ov) {
-    const size_t h = (size_t)v * W > (size_t)W + 1 ? (size_t)v * W : (size_t)W + 1;
-    return ((ov ? 2 : 1) * ((size_t)W + 1) + h) * 4;
-  };
-  for (int ov = 1; ov >= 0; --ov) {
-    int nws = kBuildThreads / 64;
-    while (nws > 1 && (bytes(nws, ov) > kLds || (int64_t)nws * 64 > E)) nws >>= 1;
-    if (bytes(nws, ov) <= kLds || ov == 0) {
-      *lds_bytes = bytes(nws, ov);
-      *overlap = ov;
-      return nws;
-    }
-  }
-  return 1;
 }
 
 // ------------------------------------------------------------ host launchers
+// Windows per merge workgroup: about 256 range workgroups, the tile within 96 KB.
+static int merge_windows(int32_t W, int32_t nb) {
+  const int by_lds = (24 * 1024) / (nb + 1) - 1;
+  int ww = (W + 255) / 256;
+  if (ww > by_lds) ww = by_lds;
+  return ww < 1 ? 1 : ww;
+}
+
+template <typename K>
+static hipError_t raise_lds_limit(K* kernel, std::atomic<bool>* done, int dev) {
+  if (dev >= 0 && dev < 64 && done[dev].load(std::memory_order_acquire)) return hipSuccess;
+  const hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kernel),
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024 - 1024);
+  if (e == hipSuccess && dev >= 0 && dev < 64) done[dev].store(true, std::memory_order_release);
+  return e;
+}
+
 hipError_t launch_build(const int32_t* ids, int32_t n, int32_t W, int32_t L, int32_t* perm_out,
                         int32_t* offsets_io, int32_t* invalid_out, void* plan, hipStream_t stream) {
   const PlanLayout lay = plan_layout(n, W);
@@ -567,32 +615,54 @@ hipError_t launch_build(const int32_t* ids, int32_t n, int32_t W, int32_t L, int
   Chunk* chunks = reinterpret_cast<Chunk*>(base + lay.chunks);
   LongWin* longs = reinterpret_cast<LongWin*>(base + lay.longs);
   int32_t* counts = reinterpret_cast<int32_t*>(base + lay.counts);
+  int32_t* sorted = reinterpret_cast<int32_t*>(base + lay.sorted);
+  int32_t* totals = reinterpret_cast<int32_t*>(base + lay.totals);
   const int csr = ids == nullptr;
   if (csr || lay.n_blocks == 0) {
     hipLaunchKernelGGL(k_plan, dim3(1), dim3(kBuildThreads), 0, stream, csr, W, n, L, offsets_io,
                        invalid_out, hdr, offs, chunks, longs);
     return hipGetLastError();
   }
-  hipLaunchKernelGGL(k_count, dim3(lay.n_blocks), dim3(kBuildThreads), 0, stream, ids, n, W,
-                     lay.block_elems, lay.counts_ld, counts);
-  size_t lds = 0;
-  int overlap = 0;
-  const int nws = scatter_waves(W, lay.block_elems, &lds, &overlap);
-  // the dynamic LDS of k_scatter exceeds the default limit: raise it once per device
-  // (atomic: host threads may build plans concurrently; setting it twice is harmless)
-  static std::atomic<bool> lds_attr[64] = {};
+  if (lay.n_blocks > kBuilderMaxBlocks) return hipErrorInvalidValue;
+  // the dynamic LDS of both kernels may exceed the default limit: raise it once per
+  // device (atomic: host threads may build plans concurrently; setting it twice is harmless)
+  static std::atomic<bool> attr_sort[4][64] = {}, attr_merge[64] = {};
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return e;
-  if (dev < 0 || dev >= 64 || !lds_attr[dev].load(std::memory_order_acquire)) {
-    e = hipFuncSetAttribute(reinterpret_cast<const void*>(&k_scatter),
-                            hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024 - 1024);
-    if (e != hipSuccess) return e;
-    if (dev >= 0 && dev < 64) lds_attr[dev].store(true, std::memory_order_release);
+  const int R = lay.block_elems / kSortThreads;
+  const size_t sort_lds =
+      ((size_t)lay.counts_ld + 2 * (size_t)lay.block_elems + (R <= 4 ? 2 : 1) * kDigits * kSortWaves) * 4;
+  const dim3 sg(lay.n_blocks), st(kSortThreads);
+  switch (R) {
+    case 1:
+      if ((e = raise_lds_limit(&k_sort<1>, attr_sort[0], dev)) != hipSuccess) return e;
+      hipLaunchKernelGGL(k_sort<1>, sg, st, sort_lds, stream, ids, n, W, lay.counts_ld, counts, sorted, totals);
+      break;
+    case 2:
+      if ((e = raise_lds_limit(&k_sort<2>, attr_sort[1], dev)) != hipSuccess) return e;
+      hipLaunchKernelGGL(k_sort<2>, sg, st, sort_lds, stream, ids, n, W, lay.counts_ld, counts, sorted, totals);
+      break;
+    case 4:
+      if ((e = raise_lds_limit(&k_sort<4>, attr_sort[2], dev)) != hipSuccess) return e;
+      hipLaunchKernelGGL(k_sort<4>, sg, st, sort_lds, stream, ids, n, W, lay.counts_ld, counts, sorted, totals);
+      break;
+    case 8:
+      if ((e = raise_lds_limit(&k_sort<8>, attr_sort[3], dev)) != hipSuccess) return e;
+      hipLaunchKernelGGL(k_sort<8>, sg, st, sort_lds, stream, ids, n, W, lay.counts_ld, counts, sorted, totals);
+      break;
+    default:
+      return hipErrorInvalidValue;
   }
-  hipLaunchKernelGGL(k_scatter, dim3(lay.n_blocks + 1), dim3(kBuildThreads), lds, stream, ids, n, W, L,
-                     lay.block_elems, lay.n_blocks, lay.counts_ld, nws, overlap, counts, perm, perm_out,
-                     offs, offsets_io, chunks, longs, hdr, invalid_out);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  const int ww = merge_windows(W, lay.n_blocks);
+  const int groups = (W + ww - 1) / ww;
+  const size_t tile = (size_t)(ww + 1) * (lay.n_blocks + 1), tables = 2 * ((size_t)W + 1);
+  const size_t merge_lds = (tile > tables ? tile : tables) * 4;
+  if ((e = raise_lds_limit(&k_merge, attr_merge, dev)) != hipSuccess) return e;
+  hipLaunchKernelGGL(k_merge, dim3(groups + 1), dim3(kMergeThreads), merge_lds, stream, n, W, L,
+                     lay.block_elems, lay.n_blocks, lay.counts_ld, ww, counts, sorted, totals, perm,
+                     perm_out, offs, offsets_io, chunks, longs, hdr, invalid_out);
   return hipGetLastError();
 }
 

@@ -51,30 +51,36 @@ struct LongWin {
 };
 
 struct PlanLayout {
-  size_t header, perm, offsets, chunks, longs, counts, total;
+  size_t header, totals, perm, offsets, chunks, longs, counts, sorted, total;
   int32_t max_chunks;   // capacity of the chunk table
   int32_t max_long;     // capacity of the long-window table
   int32_t n_blocks;     // builder blocks
   int32_t block_elems;  // rows per builder block
-  int32_t counts_ld;    // row stride (ints) of the builder's count matrix
+  int32_t counts_ld;    // row stride (ints) of the builder's prefix matrix
 };
 
 __host__ __device__ inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
-// Rows per builder block: a power of two >= 2048 chosen so that there are at most
-// 32 blocks (every block of the scatter reads the whole count matrix, at most
-// 32 * (W + 1) entries).
-constexpr int32_t kBuilderMaxBlocks = 32;
-__host__ __device__ inline int32_t builder_block_elems(int64_t n) {
-  int64_t e = 2048;
-  while (e * kBuilderMaxBlocks < n) e *= 2;
+// Rows per builder block: 1024 x 2^k, k <= 3, the smallest that keeps the
+// builder's prefix matrix (one row of num_windows + 1 ints per block) within 2^21
+// entries and the block count within kBuilderMaxBlocks, where possible.
+constexpr int32_t kBuilderMinBlockElems = 1024;
+constexpr int32_t kBuilderMaxBlockElems = 8192;
+constexpr int32_t kBuilderMaxBlocks = 8192;
+constexpr int64_t kBuilderMaxRows = (int64_t)kBuilderMaxBlockElems * kBuilderMaxBlocks;
+__host__ __device__ inline int32_t builder_block_elems(int64_t n, int32_t num_windows) {
+  int64_t e = kBuilderMinBlockElems;
+  while (e < kBuilderMaxBlockElems &&
+         (((n + e - 1) / e) * ((int64_t)num_windows + 1) > (int64_t)1 << 21 ||
+          (n + e - 1) / e > kBuilderMaxBlocks))
+    e *= 2;
   return (int32_t)e;
 }
 
 __host__ __device__ inline PlanLayout plan_layout(int64_t n, int32_t num_windows) {
   PlanLayout L;
   const int64_t W = num_windows;
-  L.block_elems = builder_block_elems(n);
+  L.block_elems = builder_block_elems(n, num_windows);
   L.n_blocks = (int32_t)((n + L.block_elems - 1) / L.block_elems);
   L.counts_ld = (int32_t)align_up((size_t)W + 1, 4);
   // Every chunk holds at least one non-empty window, so min(W, n) bounds the
@@ -85,6 +91,10 @@ __host__ __device__ inline PlanLayout plan_layout(int64_t n, int32_t num_windows
   size_t off = 0;
   L.header = off;
   off += 256;
+  // window totals of the build in progress: at a fixed place for every (n, W), and
+  // all zero between builds (the builder clears what it added)
+  L.totals = off;
+  off = align_up(off + ((size_t)kMaxWindows + 1) * 4, 256);
   L.perm = off;
   off = align_up(off + (size_t)n * 4, 256);
   L.offsets = off;
@@ -93,8 +103,12 @@ __host__ __device__ inline PlanLayout plan_layout(int64_t n, int32_t num_windows
   off = align_up(off + (size_t)(L.max_chunks > 0 ? L.max_chunks : 1) * sizeof(Chunk), 256);
   L.longs = off;
   off = align_up(off + (size_t)(L.max_long > 0 ? L.max_long : 1) * sizeof(LongWin), 256);
+  // builder scratch: per block, the exclusive prefix of its window counts; the
+  // rows of every block sorted by window
   L.counts = off;
   off = align_up(off + (size_t)L.n_blocks * (size_t)L.counts_ld * 4, 256);
+  L.sorted = off;
+  off = align_up(off + (size_t)n * 4, 256);
   L.total = off;
   return L;
 }

@@ -210,7 +210,8 @@ def new_plan_buffer(n: int, num_windows: int, device):
     nb = plan_bytes(n, num_windows)
     if nb == 0:
         raise SlaError(SLA_E_ARG, "sla_plan_bytes")
-    return torch.empty(nb, dtype=torch.uint8, device=device)
+    # zero-filled once: the builder keeps its window totals at zero between builds
+    return torch.zeros(nb, dtype=torch.uint8, device=device)
 
 
 def build_segments(ids=None, num_windows: int = 0, chunk_rows: int = 0, offsets=None,

@@ -176,8 +176,7 @@ def test_builder_random(sla, seed):
     check_plan(sla, plan, ids, W, L)
 
 
-# block sizes (2048 rows and up, at most 32 blocks), LDS limits of the scatter
-# (fewer ranking waves for large W) and the block prefix over many blocks
+# sort blocks of 1024, 2048 and 8192 rows, one to ~1000 blocks, already sorted ids
 @pytest.mark.parametrize("W,n,L,srt", [(16384, 1_000_000, 64, False), (8193, 100_000, 64, False),
                                        (6000, 65_536, 48, False), (1, 200_000, 32, False),
                                        (2, 65_537, 64, True), (1521, 2_000_000, 64, False),
@@ -190,6 +189,23 @@ def test_builder_shapes(sla, W, n, L, srt):
     _say(f"[builder shapes] n={n} W={W} L={L} sorted={srt}")
     plan = build(sla, ids=ids, W=W, chunk_rows=L)
     check_plan(sla, plan, ids, W, L)
+
+
+def test_builder_reuses_plan_buffer(sla):
+    # one zero-filled buffer rebuilt for other sizes: the builder's window totals sit
+    # at a fixed place and every build leaves them zero (block sizes 4096 and 1024)
+    import torch
+
+    rng = np.random.default_rng(9)
+    cases = [(500_000, 16384), (60_000, 1521), (5, 3), (200_000, 4096), (500_000, 16384), (777, 1)]
+    buf = sla.new_plan_buffer(max(n for n, _ in cases), 16384, "cuda")
+    for n, W in cases:
+        ids = rng.integers(0, W, size=n).astype(np.int32)
+        ids[rng.random(n) < 0.002] = W + 3
+        _say(f"[builder reuse] n={n} W={W}")
+        plan = sla.build_segments(to_dev(ids), num_windows=W, plan_buf=buf)
+        torch.cuda.synchronize()
+        check_plan(sla, plan, ids, W, 0)
 
 
 def test_builder_degenerate(sla):
