@@ -51,15 +51,21 @@ __device__ __forceinline__ float recip(float x) {
 
 // Power of two p with x * p in [1, 2) (1 for x = 0 or non-finite x; at most
 // 2^126, so that p and 1 / p stay finite, for x below the normal range).
+// Exponent of x > 0 from its bits; -127 for a subnormal x, which both callers
+// clamp to the same power of two as its true exponent.
+__device__ __forceinline__ int exponent_of(float x) {
+  return (int)((__float_as_uint(x) >> 23) & 0xffu) - 127;
+}
+
 __device__ __forceinline__ float pow2_scale_to_one(float x) {
   if (!(x > 0.f) || !(x < 3.0e38f)) return 1.f;
-  return ldexpf(1.f, min(-ilogbf(x), 126));
+  return ldexpf(1.f, min(-exponent_of(x), 126));
 }
 
 // Power of two <= x (1 for x = 0 or non-finite x; at least 2^-126).
 __device__ __forceinline__ float pow2_floor(float x) {
   if (!(x > 0.f) || !(x < 3.0e38f)) return 1.f;
-  return ldexpf(1.f, max(ilogbf(x), -126));
+  return ldexpf(1.f, max(exponent_of(x), -126));
 }
 
 // ---------------------------------------------------------- lane exchanges
@@ -403,31 +409,30 @@ __device__ __forceinline__ void state_seg(const Slice<T, Geo<D>::KS, NM>& sb, in
   constexpr int KS = Geo<D>::KS, NT = Geo<D>::NT;
   using F = Frag<T, KS>;
   const floatx4 zero = {0.f, 0.f, 0.f, 0.f};
-  floatx4 tk[2][NT], tv[2][NT];
+  Raw<T, KS> fk[2], vv[2];
 #pragma unroll
   for (int s = 0; s < 2; ++s) {
     const int32_t row = r0 + 16 * s + i;
     const bool in = sb.ok[s] && row >= a && row < b;
-    const Raw<T, KS> fk = phi_frag<T, KS, PHI>(sb.x[0][s], in);
-    const Raw<T, KS> vv = in ? sb.x[1][s] : F::zero();
-#pragma unroll
-    for (int t = 0; t < NT; ++t) {
-      tk[s][t] = F::mma(fk, sel.m[t], zero);
-      tv[s][t] = F::mma(vv, sel.m[t], zero);
-    }
+    fk[s] = phi_frag<T, KS, PHI>(sb.x[0][s], in);
+    vv[s] = in ? sb.x[1][s] : F::zero();
   }
+  // the row transposes, each packed into an operand as soon as it is formed
+  auto rows_of = [&](const Raw<T, KS>(&x)[2], int t) -> Raw<T, 8> {
+    return pack_rows<T>(F::mma(x[0], sel.m[t], zero), F::mma(x[1], sel.m[t], zero));
+  };
+  Raw<T, 8> pv[NT];
+#pragma unroll
+  for (int ct = 0; ct < NT; ++ct) pv[ct] = rows_of(vv, ct);
   // phi(K) is already zero outside [a, b), so z needs no row mask
   float one8[8] = {1.f, 1.f, 1.f, 1.f, 1.f, 1.f, 1.f, 1.f};
   const Raw<T, 8> ones = Frag<T, 8>::from_f32(one8);
 #pragma unroll
   for (int et = 0; et < NT; ++et) {
-    const Raw<T, 8> pk = pack_rows<T>(tk[0][et], tk[1][et]);
+    const Raw<T, 8> pk = rows_of(fk, et);
     st.V[et] = Frag<T, 8>::mma(pk, ones, st.V[et]);
 #pragma unroll
-    for (int ct = 0; ct < NT; ++ct) {
-      const Raw<T, 8> pv = pack_rows<T>(tv[0][ct], tv[1][ct]);
-      st.M[et][ct] = Frag<T, 8>::mma(pk, pv, st.M[et][ct]);
-    }
+    for (int ct = 0; ct < NT; ++ct) st.M[et][ct] = Frag<T, 8>::mma(pk, pv[ct], st.M[et][ct]);
   }
 }
 
@@ -726,30 +731,24 @@ __device__ __forceinline__ void qgrad_seg(const Slice<T, Geo<D>::KS, NM>& sb, in
       nl[s] = F::from_f32(ns);
     }
   }
-  floatx4 tx[2][NT], td[2][NT], tn[2], tl[2];
+  // the row transposes, each packed into an operand as soon as it is formed (the
+  // packed operand takes half the registers of its two result tiles)
+  auto rows_of = [&](const Raw<T, KS>(&x)[2], int t) -> Raw<T, 8> {
+    return pack_rows<T>(F::mma(x[0], sel.m[t], zero), F::mma(x[1], sel.m[t], zero));
+  };
+  Raw<T, 8> pd[NT];
 #pragma unroll
-  for (int s = 0; s < 2; ++s) {
-#pragma unroll
-    for (int t = 0; t < NT; ++t) {
-      tx[s][t] = F::mma(xr[s], sel.m[t], zero);
-      td[s][t] = F::mma(dr[s], sel.m[t], zero);
-    }
-    tn[s] = F::mma(nd[s], sel.m[0], zero);
-    if constexpr (SP) tl[s] = F::mma(nl[s], sel.m[0], zero);
-  }
-  const Raw<T, 8> pn = pack_rows<T>(tn[0], tn[1]);
+  for (int ct = 0; ct < NT; ++ct) pd[ct] = rows_of(dr, ct);
+  const Raw<T, 8> pn = rows_of(nd, 0);
   Raw<T, 8> pl;
-  if constexpr (SP) pl = pack_rows<T>(tl[0], tl[1]);
+  if constexpr (SP) pl = rows_of(nl, 0);
 #pragma unroll
   for (int et = 0; et < NT; ++et) {
-    const Raw<T, 8> px = pack_rows<T>(tx[0][et], tx[1][et]);
+    const Raw<T, 8> px = rows_of(xr, et);
     gs.V[et] = Frag<T, 8>::mma(px, pn, gs.V[et]);
     if constexpr (SP) gs.V[et] = Frag<T, 8>::mma(px, pl, gs.V[et]);
 #pragma unroll
-    for (int ct = 0; ct < NT; ++ct) {
-      const Raw<T, 8> pd = pack_rows<T>(td[0][ct], td[1][ct]);
-      gs.M[et][ct] = Frag<T, 8>::mma(px, pd, gs.M[et][ct]);
-    }
+    for (int ct = 0; ct < NT; ++ct) gs.M[et][ct] = Frag<T, 8>::mma(px, pd[ct], gs.M[et][ct]);
   }
 }
 
