@@ -16,6 +16,7 @@ from .sla_ref import (  # noqa: F401
     segments_ref,
     sla_backward_ref,
     sla_forward_ref,
+    sla_projected_backward_ref,
     sla_projected_forward_ref,
     widen,
     xca_backward_ref,

@@ -51,6 +51,10 @@ What is computed, and the passage it follows
   usual [out, in] weight layout, Q = X W_q^T + b_q (likewise K, V) with
   W_qkv = [W_q; W_k; W_v] stacked by rows, and Y = SLA(Q, K, V) W_o^T + b_o, heads
   split from the C channels as in the plain path.
+* ``sla_projected_backward_ref``: the gradients of that chain (input, both
+  weights, both biases) by the chain rule, for the loss sum(y . dy) over the rows
+  that lie in a window (the paper trains the projections but does not write the
+  gradients out).
 * ``cwi_forward_ref``: the cross-window interaction of Sec. 3.3, Eq. (4)-(7): the
   4c channels split into four quarters, two depthwise convolutions with long 1D
   kernels along the two grid axes (window size + 1 taps), a depthwise 3 x 3 x 3
@@ -347,6 +351,59 @@ def sla_projected_forward_ref(x, w_qkv, b_qkv, w_o, b_o, heads, offsets, perm=No
     if b_o is not None:
         y = y + np.asarray(b_o, dtype=np.float64)
     return o, y
+
+
+def _rows_in_windows(offsets, perm, n):
+    """Boolean [n]: rows that belong to a window (the first offsets[-1] sorted
+    positions)."""
+    offsets = np.asarray(offsets, dtype=np.int64)
+    pos = np.arange(int(offsets[-1]))
+    rows = pos if perm is None else np.asarray(perm, dtype=np.int64)[pos]
+    mask = np.zeros(n, dtype=bool)
+    mask[rows] = True
+    return mask
+
+
+def sla_projected_backward_ref(x, w_qkv, b_qkv, w_o, b_o, dy, heads, offsets, perm=None,
+                               feature_map_name="elu1", eps=0.0):
+    """Gradients of the projected forward (``sla_projected_forward_ref``) by the
+    chain rule, for the loss L = sum over rows in windows of y . dy.
+
+    dy: [n, C] gradient of y.  Rows in no window produce no y, so they take no
+    part: their dy is ignored and their dx is 0.  Returns float64
+    (dx [n, C], dw_qkv [3C, C], db_qkv [3C], dw_o [C, C], db_o [C]):
+        do = dy W_o                                  (y = o W_o^T + b_o)
+        dW_o = dy^T o,  db_o = sum_rows dy
+        dq, dk, dv = SLA backward of do              (``sla_backward_ref``)
+        dqkv = [dq | dk | dv]                        ([q | k | v] = x W_qkv^T + b_qkv)
+        dx = dqkv W_qkv,  dW_qkv = dqkv^T x,  db_qkv = sum_rows dqkv
+    """
+    x = np.asarray(x, dtype=np.float64)
+    w_qkv = np.asarray(w_qkv, dtype=np.float64)
+    w_o = np.asarray(w_o, dtype=np.float64)
+    dy = np.asarray(dy, dtype=np.float64)
+    n, C = x.shape
+    if C % heads or w_qkv.shape != (3 * C, C) or w_o.shape != (C, C) or dy.shape != (n, C):
+        raise ValueError("shapes: x, dy [n, C], w_qkv [3C, C], w_o [C, C], C a multiple of heads")
+    d = C // heads
+    qkv = x @ w_qkv.T
+    if b_qkv is not None:
+        qkv = qkv + np.asarray(b_qkv, dtype=np.float64)
+    q, k, v = (qkv[:, i * C:(i + 1) * C].reshape(n, heads, d) for i in range(3))
+    inside = _rows_in_windows(offsets, perm, n)
+    o = sla_forward_ref(q, k, v, offsets, perm, feature_map_name, eps).reshape(n, C)
+    o = np.where(inside[:, None], o, 0.0)
+    g = np.where(inside[:, None], dy, 0.0)
+    dw_o = g.T @ o
+    db_o = g.sum(axis=0)
+    do = (g @ w_o).reshape(n, heads, d)
+    dq, dk, dv = sla_backward_ref(q, k, v, do, offsets, perm, feature_map_name, eps)
+    dqkv = np.concatenate([t.reshape(n, C) for t in (dq, dk, dv)], axis=1)
+    dqkv = np.where(inside[:, None], dqkv, 0.0)
+    dx = dqkv @ w_qkv
+    dw_qkv = dqkv.T @ x
+    db_qkv = dqkv.sum(axis=0)
+    return dx, dw_qkv, db_qkv, dw_o, db_o
 
 
 # ---------------------------------------------------------- cross-window interaction

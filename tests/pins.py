@@ -546,6 +546,100 @@ def projected_pin_failures(fwd_proj, seg, fwd):
     return fails
 
 
+# ---------------------------------------------------------- projected backward
+# ``bwd_proj(x, w_qkv, b_qkv, w_o, b_o, dy, heads, offsets, perm, fmap, eps)
+#   -> (dx, dw_qkv, db_qkv, dw_o, db_o)``: gradients of sum(y . dy) over the rows
+# in windows.  Pinned against central differences of the plain-loop forward
+# (``brute_projected``), which shares nothing with the backward.
+def _proj_loss(x, wq, bq, wo, bo, dy, heads, ids, W, fmap, eps):
+    _, y = brute_projected(x, wq, bq, wo, bo, heads, ids, W, fmap, eps)
+    inside = ~np.isnan(y).any(axis=1)
+    return float((y[inside] * dy[inside]).sum())
+
+
+def projected_backward_pin_failures(bwd_proj, seg, bwd):
+    fails = []
+    rng = np.random.default_rng(71)
+    h = 1e-5
+    # 1. every entry of every gradient against a central difference of the loss
+    #    (both maps, with and without biases, a row in no window)
+    for seed, heads, d, bias, fmap, eps in ((0, 2, 2, True, "elu1", 0.0), (1, 1, 3, False, "relu", 0.3),
+                                            (2, 2, 2, True, "relu", 0.5)):
+        ids, _, _, _, _ = tiny_case(180 + seed, windows=3, max_len=4)
+        W = int(ids.max()) + 1
+        ids = np.concatenate([ids, [W + 2]])      # one row outside every window
+        n, C = len(ids), heads * d
+        x = rng.standard_normal((n, C))
+        wq = rng.standard_normal((3 * C, C)) / np.sqrt(C)
+        wo = rng.standard_normal((C, C)) / np.sqrt(C)
+        bq = rng.standard_normal(3 * C) if bias else None
+        bo = rng.standard_normal(C) if bias else None
+        dy = rng.standard_normal((n, C))
+        perm, off, _ = seg(ids, W)
+        got = bwd_proj(x, wq, bq, wo, bo, dy, heads, off, perm, fmap, eps)
+        # without a bias its gradient is still defined: the derivative at a zero bias
+        params = [x, wq, np.zeros(3 * C) if bq is None else bq, wo, np.zeros(C) if bo is None else bo]
+        for which, g in zip(range(5), got):
+            fd = np.zeros_like(params[which])
+            for idx in np.ndindex(params[which].shape):
+                args = [None if t is None else t.copy() for t in params]
+                args[which][idx] += h
+                lp = _proj_loss(*args, dy, heads, ids, W, fmap, eps)
+                args[which][idx] -= 2 * h
+                lm = _proj_loss(*args, dy, heads, ids, W, fmap, eps)
+                fd[idx] = (lp - lm) / (2 * h)
+            if g.shape != fd.shape or rel_err(g, fd) > 1e-6:
+                fails.append(f"projected_bwd_fd[{seed}][{which}]")
+        # the row in no window gets no input gradient
+        if np.any(got[0][-1] != 0.0):
+            fails.append(f"projected_bwd_outside_row[{seed}]")
+        # bias gradients are the row sums of dy and of [dq | dk | dv]
+        if rel_err(got[4], dy[:-1].sum(axis=0)) > 1e-13:
+            fails.append(f"projected_bwd_db_o[{seed}]")
+    # 2. W_qkv = [I; I; I], W_o = I, no biases: the plain SLA backward of (x, x, x),
+    #    dx = dq + dk + dv and dW_qkv = [dq | dk | dv]^T x
+    ids, _, _, _, _ = tiny_case(190, windows=5, max_len=6)
+    heads, d = 2, 3
+    n, C = len(ids), heads * d
+    W = int(ids.max()) + 1
+    perm, off, _ = seg(ids, W)
+    x = rng.standard_normal((n, C))
+    dy = rng.standard_normal((n, C))
+    wq = np.concatenate([np.eye(C)] * 3)
+    dx, dwq, dbq, dwo, dbo = bwd_proj(x, wq, None, np.eye(C), None, dy, heads, off, perm, "elu1", 0.0)
+    x3, dy3 = x.reshape(n, heads, d), dy.reshape(n, heads, d)
+    dq, dk, dv = bwd(x3, x3, x3, dy3, off, perm)
+    ref = (dq + dk + dv).reshape(n, C)
+    dqkv = np.concatenate([t.reshape(n, C) for t in (dq, dk, dv)], axis=1)
+    if rel_err(dx, ref) > 1e-13 or rel_err(dwq, dqkv.T @ x) > 1e-13 or rel_err(dbq, dqkv.sum(axis=0)) > 1e-13:
+        fails.append("projected_bwd_identity")
+    # 3. directional derivatives on a larger case (adjoint identities): for a random
+    #    direction t of each argument, <grad, t> = d/ds L(arg + s t) at s = 0
+    ids, _, _, _, _ = tiny_case(191, windows=6, max_len=8)
+    heads, d = 2, 3
+    n, C = len(ids), heads * d
+    W = int(ids.max()) + 1
+    perm, off, _ = seg(ids, W)
+    x = rng.standard_normal((n, C))
+    wq = rng.standard_normal((3 * C, C)) / np.sqrt(C)
+    wo = rng.standard_normal((C, C)) / np.sqrt(C)
+    bq, bo = rng.standard_normal(3 * C), rng.standard_normal(C)
+    dy = rng.standard_normal((n, C))
+    got = bwd_proj(x, wq, bq, wo, bo, dy, heads, off, perm, "elu1", 0.0)
+    params = [x, wq, bq, wo, bo]
+    for which in range(5):
+        t = rng.standard_normal(params[which].shape)
+        args_p = [a.copy() for a in params]
+        args_m = [a.copy() for a in params]
+        args_p[which] += h * t
+        args_m[which] -= h * t
+        dd = (_proj_loss(*args_p, dy, heads, ids, W, "elu1", 0.0)
+              - _proj_loss(*args_m, dy, heads, ids, W, "elu1", 0.0)) / (2 * h)
+        if abs(float((got[which] * t).sum()) - dd) > 1e-6 * max(1.0, abs(dd)):
+            fails.append(f"projected_bwd_direction[{which}]")
+    return fails
+
+
 # ------------------------------------------------------ cross-window interaction
 def cwi_pin_failures(cwi):
     """Pins for ``cwi(coords, x, w_x, w_y, w_3, grid) -> [n, 4c]`` (Eq. (4)-(7))."""

@@ -368,6 +368,33 @@ def test_projected_mutant_is_caught(name):
     assert fails, f"planted mistake {name} passed every projected pin"
 
 
+# ----------------------------------------------------------- projected backward
+def test_projected_backward_pins():
+    assert pins.projected_backward_pin_failures(oracle.sla_projected_backward_ref, oracle.segments_ref,
+                                                oracle.sla_backward_ref) == []
+
+
+PROJECTED_BWD_MUTANTS = {
+    "dw_o_transposed": [("dw_o = g.T @ o", "dw_o = o.T @ g", 0)],
+    "do_weight_transposed": [("do = (g @ w_o).reshape(n, heads, d)", "do = (g @ w_o.T).reshape(n, heads, d)", 0)],
+    "dx_weight_transposed_blocks": [("dx = dqkv @ w_qkv", "dx = dqkv @ w_qkv[np.r_[C:2 * C, 0:C, 2 * C:3 * C]]", 0)],
+    "dw_qkv_from_projected_rows": [("dw_qkv = dqkv.T @ x", "dw_qkv = dqkv.T @ qkv[:, :C]", 0)],
+    "outside_dy_counted": [("g = np.where(inside[:, None], dy, 0.0)", "g = dy", 0)],
+    "outside_dqkv_zeroed_late": [("dqkv = np.where(inside[:, None], dqkv, 0.0)",
+                                  "dqkv = np.where(np.isnan(dqkv), 1.0, dqkv)", 0)],
+    "db_qkv_dropped_v": [("db_qkv = dqkv.sum(axis=0)", "db_qkv = np.concatenate([dqkv[:, :2 * C].sum(axis=0), np.zeros(C)])", 0)],
+}
+
+
+@pytest.mark.parametrize("name", sorted(PROJECTED_BWD_MUTANTS))
+def test_projected_backward_mutant_is_caught(name):
+    mod = _oracle_from_source(PROJECTED_BWD_MUTANTS[name])
+    with np.errstate(all="ignore"):
+        fails = pins.projected_backward_pin_failures(mod.sla_projected_backward_ref, oracle.segments_ref,
+                                                     oracle.sla_backward_ref)
+    assert fails, f"planted mistake {name} passed every projected backward pin"
+
+
 # ------------------------------------------------------ cross-window interaction
 def test_cwi_pins():
     assert pins.cwi_pin_failures(oracle.cwi_forward_ref) == []
