@@ -115,8 +115,10 @@ sla_status_t sla_plan_layout(int64_t n, int32_t num_windows, sla_plan_layout_t* 
  *   offsets[w]  first sorted position of window w (empty windows allowed);
  * and the chunk table.  If perm_out / offsets are not NULL they receive copies
  * (int32[n] / int32[num_windows + 1]).  Rows whose id is outside
- * [0, num_windows) are counted and left out of every window; their output rows
- * are then never written.
+ * [0, num_windows) are counted and left out of every window (their output rows
+ * are then never written); perm lists them after every window, at sorted
+ * positions offsets[num_windows] .. n - 1 in row order, so perm is a permutation
+ * of all n rows.
  *
  * Mode B, window_ids == NULL: rows are already window-sorted and `offsets`
  * (int32[num_windows + 1], device) is an INPUT: offsets[0] = 0, non-decreasing,
@@ -230,6 +232,40 @@ sla_status_t sla_forward_projected(const void* plan, size_t plan_bytes, int64_t 
                                    const void* x, const void* w_qkv, const void* b_qkv,
                                    const void* w_o, const void* b_o, void* o, void* y,
                                    sla_stream_t stream);
+
+/*
+ * Backward of sla_forward_projected: the projection layer and output projection
+ * of Sec. 3.2 are trained with the attention; their gradients follow from the
+ * forward by the chain rule.  For dy = dL/dy [n, C] over the rows in windows:
+ *     do = dy W_o,   dW_o = dy^T o,   db_o = sum over rows of dy,
+ *     dq, dk, dv = SLA backward of do (as sla_backward_ex, same feature map, eps),
+ *     dx = [dq | dk | dv] W_qkv,   dW_qkv = [dq | dk | dv]^T x,
+ *     db_qkv = sum over rows of [dq | dk | dv].
+ *   x, w_qkv, b_qkv, w_o: the forward's inputs (layouts as there; b_o takes no
+ *          part); o [n, C]: the forward's o output; dy [n, C]; all in `dtype`.
+ *   dx     [n, C] in `dtype`: every row is written, zero for rows in no window.
+ *   dw_qkv [3C, C], dw_o [C, C] (fp32, required); db_qkv [3C], db_o [C] (fp32,
+ *          may be NULL).  Rows in no window take no part in these sums.
+ *   workspace: device, 256-byte aligned, at least
+ *          sla_backward_projected_workspace_bytes(n, heads, head_dim) bytes
+ *          (else SLA_E_WORKSPACE): the recomputed q, k, v, do, dq, dk, dv, the
+ *          weights as rows and the weight-gradient partials.
+ * q, k, v are recomputed from x (rounded to `dtype`, as in the forward); do, dq,
+ * dk, dv are rounded to `dtype` as stored; all products accumulate in fp32 on the
+ * matrix cores.  The sums over rows run over the plan's sorted rows in groups
+ * whose partials are added in group order: the results are deterministic.
+ * Same dtype, C and alignment rules as sla_forward_projected; dy and dx 16-byte
+ * aligned, the fp32 outputs 4-byte aligned.
+ */
+size_t sla_backward_projected_workspace_bytes(int64_t n, int32_t heads, int32_t head_dim);
+
+sla_status_t sla_backward_projected(const void* plan, size_t plan_bytes, int64_t n,
+                                    int32_t num_windows, sla_dtype_t dtype, int32_t heads,
+                                    int32_t head_dim, sla_feature_map_t feature_map, float eps,
+                                    const void* x, const void* w_qkv, const void* b_qkv,
+                                    const void* w_o, const void* o, const void* dy, void* dx,
+                                    float* dw_qkv, float* db_qkv, float* dw_o, float* db_o,
+                                    void* workspace, size_t workspace_bytes, sla_stream_t stream);
 
 /*
  * Cross-window interaction (Sec. 3.3, Eq. (4)-(7)), the module that follows SLA

@@ -18,7 +18,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libsla.so")
-SOURCES = ["sla_builder.hip", "sla_attn.hip", "sla_proj.hip", "sla_cwi.hip", "sla_naive.hip", "sla_xca.hip", "sla_api.hip"]
+SOURCES = ["sla_builder.hip", "sla_attn.hip", "sla_proj.hip", "sla_proj_bwd.hip", "sla_cwi.hip", "sla_naive.hip", "sla_xca.hip", "sla_api.hip"]
 ARCH = "gfx950"
 
 HIPCC_FLAGS = [

@@ -585,6 +585,26 @@ __global__ __launch_bounds__(kMergeThreads) void k_merge(
       if (perm_out) perm_out[p] = row;
     }
   }
+  // (4) the last range also lists the rows whose ids are out of range, after every
+  // window (sorted positions offsets[W] .. n - 1), in row order: in block b they
+  // follow its rows in windows, and blocks before b hold pre(b) = b E - ex[W][b]
+  if (w0 + nx == W) {
+    const int32_t* eW = ex + nx * S;
+    const int32_t q0 = eW[nb];
+    for (int32_t p = q0 + tid; p < n; p += kMergeThreads) {
+      const int32_t q = p - q0;
+      int bl = 0, bh = nb - 1;
+      while (bl < bh) {
+        const int mid = (bl + bh + 1) >> 1;
+        if ((int64_t)mid * E - eW[mid] <= q) bl = mid; else bh = mid - 1;
+      }
+      const int64_t j = q - ((int64_t)bl * E - eW[bl]);
+      const int64_t at = (int64_t)bl * E + (eW[bl + 1] - eW[bl]) + j;
+      const int32_t row = at < n ? sorted[at] : 0;
+      perm[p] = row;
+      if (perm_out) perm_out[p] = row;
+    }
+  }
 }
 
 // ------------------------------------------------------------ host launchers

@@ -1,0 +1,470 @@
+// Backward of the projection layer, SLA and output projection.
+//
+// Sec. 3.2 trains the shared projection layer that maps every voxel to Q, K and V,
+// and the block's output projection; the gradients follow from the forward
+//     [q | k | v] = x W_qkv^T + b_qkv,  o = SLA(q, k, v),  y = o W_o^T + b_o
+// by the chain rule, for dy = dL/dy over the rows that lie in a window:
+//     do = dy W_o,                      dW_o = dy^T o,       db_o = sum_rows dy,
+//     dq, dk, dv = SLA backward of do,
+//     dx = [dq | dk | dv] W_qkv,        dW_qkv = [dq | dk | dv]^T x,
+//     db_qkv = sum_rows [dq | dk | dv].
+// q, k, v are recomputed from x (they never reach HBM in the forward), o is the
+// forward's output.  Six launches:
+//   k_transpose     W_qkv^T and W_o^T into the workspace, so that every product
+//                   below reads its weights as rows;
+//   k_rows_gemm     q | k | v = x W_qkv^T + b_qkv, and do = dy W_o: a row of the
+//                   output is a row of the input times a weight matrix held in LDS;
+//   (SLA backward)  dq, dk, dv;
+//   k_rows_gemm     dx = [dq | dk | dv] W_qkv (zero for rows in no window);
+//   k_wgrad         per group of sorted rows, partial dW_qkv, dW_o and the bias
+//                   gradients: sums over rows on the matrix cores, after the rows
+//                   are turned into contraction operands (0/1 selection products);
+//   k_wgrad_reduce  the groups' partials summed in group order.
+// Rows are visited in the plan's sorted order, so every sum has a fixed order and
+// the results do not depend on scheduling.
+#include "sla_attn_core.h"
+
+namespace sla {
+
+// ------------------------------------------------------------ weights as rows
+// dst[j][k] = src[k][j] for src [K, N] (row-major), dst [N, K].
+template <typename T>
+__global__ __launch_bounds__(256) void k_transpose(const T* __restrict__ src, T* __restrict__ dst,
+                                                   int32_t K, int32_t N) {
+  __shared__ unsigned short tile[32][33];
+  const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;   // 32 x 8
+  const int32_t k0 = blockIdx.y * 32, j0 = blockIdx.x * 32;
+  const unsigned short* s = reinterpret_cast<const unsigned short*>(src);
+  unsigned short* d = reinterpret_cast<unsigned short*>(dst);
+  for (int r = ty; r < 32; r += 8)
+    if (k0 + r < K && j0 + tx < N) tile[r][tx] = s[(size_t)(k0 + r) * N + j0 + tx];
+  __syncthreads();
+  for (int r = ty; r < 32; r += 8)
+    if (j0 + r < N && k0 + tx < K) d[(size_t)(j0 + r) * K + k0 + tx] = tile[tx][r];
+}
+
+// ------------------------------------------------------------ row products
+// out[row][n0 + j] = sum_k A(row, k) Wr[n0 + j][k] + bias[n0 + j], j < 16 NBT, for
+// the rows at sorted positions [0, npos) (row = perm[p], or p without one).
+// A(row, k) = a[k / C][row][k % C] over nseg segments [n, C] (K = nseg C); Wr is
+// [N, K] row-major (a weight in the [out, in] layout); output column j goes to
+// out[j / C][row][j % C].  Positions at or after *nvalid (rows in no window) get
+// zero input, so their outputs are the bias (zero when there is none).
+//
+// One workgroup keeps the weight rows of its 16 NBT output columns in LDS (padded
+// rows of K + 8 elements) and walks 16-row tiles, one per wave: with the weight
+// rows as the first matrix-core operand and the input rows (16-byte pieces of 8
+// channels) as the second, lane (i, g) receives columns 16 t + 4 g .. + 3 of the
+// tile's row i, stored as one 4-element piece.
+struct RowGemmArgs {
+  const void* a[3];
+  void* out[3];
+  const void* w;             // Wr [N, K]
+  const void* bias;          // [N] or null
+  const PlanHeader* hdr;     // the plan: a CSR plan's rows are its positions
+  const int32_t* perm;       // the plan's permutation (read for plans built from ids)
+  const int32_t* nvalid;     // the plan's offsets[W]: rows in windows
+  int32_t C, K, N, npos, n, W;
+};
+
+template <typename T, int NBT>
+__global__ __launch_bounds__(256) void k_rows_gemm(RowGemmArgs ga) {
+  constexpr int NB = 16 * NBT;
+  if (ga.hdr->magic != kPlanMagic || ga.hdr->n != ga.n || ga.hdr->num_windows != ga.W) return;
+  const int32_t* perm = ga.hdr->csr ? nullptr : ga.perm;
+  extern __shared__ __attribute__((aligned(16))) unsigned char lds_raw[];
+  const int K = ga.K, LDW = K + 8, C = ga.C;
+  T* s_w = reinterpret_cast<T*>(lds_raw);
+  float* s_b = reinterpret_cast<float*>(s_w + NB * LDW);
+  const int32_t n0 = (int32_t)blockIdx.y * NB;
+  {
+    const int pieces = K / 8;
+    const T* w = static_cast<const T*>(ga.w);
+    for (int idx = threadIdx.x; idx < NB * pieces; idx += blockDim.x) {
+      const int jj = idx / pieces, pc = idx - jj * pieces;
+      *reinterpret_cast<uint4*>(s_w + jj * LDW + 8 * pc) =
+          *reinterpret_cast<const uint4*>(w + (size_t)(n0 + jj) * K + 8 * pc);
+    }
+    const unsigned short* b = static_cast<const unsigned short*>(ga.bias);
+    for (int jj = threadIdx.x; jj < NB; jj += blockDim.x) s_b[jj] = b ? u16_to_f32<T>(b[n0 + jj]) : 0.f;
+  }
+  __syncthreads();
+  using F8 = Frag<T, 8>;
+  const floatx4 zero = {0.f, 0.f, 0.f, 0.f};
+  const int lane = lane_id(), wv = threadIdx.x >> 6;
+  const int i = lane & 15, g = lane >> 4;
+  const int32_t nvalid = min(*ga.nvalid, ga.npos);
+  const int nseg = K / C;
+  T* outp = static_cast<T*>(ga.out[n0 / C]);
+  const int ocol = n0 % C;
+  for (int32_t tile = (int32_t)blockIdx.x * 4 + wv; tile * 16 < ga.npos; tile += (int32_t)gridDim.x * 4) {
+    const int32_t p = tile * 16 + i;
+    const bool inside = p < ga.npos;
+    const bool valid = p < nvalid;
+    int32_t row = inside ? (perm ? perm[p] : p) : 0;
+    if ((uint32_t)row >= (uint32_t)ga.n) row = 0;
+    floatx4 acc[NBT];
+#pragma unroll
+    for (int t = 0; t < NBT; ++t) acc[t] = zero;
+    for (int s = 0; s < nseg; ++s) {
+      const T* src = static_cast<const T*>(ga.a[s]) + (size_t)row * C + 8 * g;
+      for (int kb = 0; kb < C / 32; ++kb) {
+        Raw<T, 8> xo = __builtin_bit_cast(Raw<T, 8>, *reinterpret_cast<const uint4*>(src + 32 * kb));
+        if (!valid) xo = F8::zero();
+        const T* wr = s_w + i * LDW + s * C + 32 * kb + 8 * g;
+#pragma unroll
+        for (int t = 0; t < NBT; ++t) {
+          const Raw<T, 8> wo = *reinterpret_cast<const Raw<T, 8>*>(wr + 16 * t * LDW);
+          acc[t] = F8::mma(wo, xo, acc[t]);
+        }
+      }
+    }
+    if (!inside) continue;
+    T* dst = outp + (size_t)row * C + ocol + 4 * g;
+#pragma unroll
+    for (int t = 0; t < NBT; ++t) {
+      const float4 bias = *reinterpret_cast<const float4*>(s_b + 16 * t + 4 * g);
+      float f[4] = {acc[t][0] + bias.x, acc[t][1] + bias.y, acc[t][2] + bias.z, acc[t][3] + bias.w};
+      u16x4 pk;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) pk[j] = f32_to_u16<T>(f[j]);
+      *reinterpret_cast<u16x4*>(dst + 16 * t) = pk;
+    }
+  }
+}
+
+// ------------------------------------------------------------ weight gradients
+// Unit (problem, 32-row slab m0 of the gradient, column chunk n0 of up to 128,
+// row group): partial[group][m0 + e][n0 + c] = sum over the group's rows of
+// A(row, m0 + e) B(row, n0 + c), and, for n0 = 0, the bias partial
+// sum_rows A(row, m0 + e).  Problem 0: A = [dq | dk | dv] (3C columns), B = x;
+// problem 1: A = dy, B = o.  Rows are the sorted positions [0, nvalid) of the
+// plan, split into `groups` contiguous ranges; a wave takes one unit and walks its
+// rows 32 at a time: each 32-column block of a row is fetched as a row fragment
+// and turned into the operand of a contraction over rows (as the attention's
+// state sums), then the slab's 2 x 2 tiles per column block accumulate.
+struct WgradArgs {
+  const void* a0[3];     // dq, dk, dv [n, C]
+  const void* b0;        // x [n, C]
+  const void* a1;        // dy [n, C]
+  const void* b1;        // o [n, C]
+  const PlanHeader* hdr;
+  const int32_t* perm;
+  const int32_t* nvalid;
+  float* part;           // [groups][total]: dW_qkv [3C][C], dW_o [C][C], db_qkv [3C], db_o [C]
+  int32_t C, n, W, groups, units0, units1, chunks;
+};
+
+constexpr int kWgradChunkBlocks = 4;   // 32-column blocks per column chunk
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_wgrad(WgradArgs wa) {
+  using F = Frag<T, 8>;
+  constexpr int NCB = kWgradChunkBlocks;
+  const floatx4 zero = {0.f, 0.f, 0.f, 0.f};
+  if (wa.hdr->magic != kPlanMagic || wa.hdr->n != wa.n || wa.hdr->num_windows != wa.W) return;
+  const int32_t* perm = wa.hdr->csr ? nullptr : wa.perm;
+  const int lane = lane_id();
+  const int i = lane & 15, g = lane >> 4;
+  const int C = wa.C;
+  const int32_t unit = (int32_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int32_t per_group = wa.units0 + wa.units1;
+  const int32_t grp = unit / per_group;
+  if (grp >= wa.groups) return;
+  int32_t u = unit - grp * per_group;
+  const int prob = u < wa.units0 ? 0 : 1;
+  if (prob) u -= wa.units0;
+  const int slab = u / wa.chunks, chunk = u - slab * wa.chunks;
+  const int m0 = 32 * slab;
+  const int n0 = 32 * NCB * chunk;
+  const int ncb = min(NCB, (C - n0) / 32);
+  const T* A = prob ? static_cast<const T*>(wa.a1) : static_cast<const T*>(wa.a0[m0 / C]);
+  const int acol = m0 % C;
+  const T* B = static_cast<const T*>(prob ? wa.b1 : wa.b0);
+  const int32_t nvalid = max(0, min(*wa.nvalid, wa.n));
+  const int32_t p0 = (int32_t)((int64_t)nvalid * grp / wa.groups);
+  const int32_t p1 = (int32_t)((int64_t)nvalid * (grp + 1) / wa.groups);
+  const Sel<T, 32> sel(i, g);
+  float one8[8] = {1.f, 1.f, 1.f, 1.f, 1.f, 1.f, 1.f, 1.f};
+  const Raw<T, 8> ones = F::from_f32(one8);
+  floatx4 acc[2][2 * NCB], bacc[2];
+#pragma unroll
+  for (int et = 0; et < 2; ++et) {
+    bacc[et] = zero;
+#pragma unroll
+    for (int ct = 0; ct < 2 * NCB; ++ct) acc[et][ct] = zero;
+  }
+  auto rows_of = [&](const Raw<T, 8>(&x)[2], int t) -> Raw<T, 8> {
+    return pack_rows<T>(F::mma(x[0], sel.m[t], zero), F::mma(x[1], sel.m[t], zero));
+  };
+  // one job = 32 sorted positions; the next job's rows are fetched while this one
+  // is summed (fragments in memory order until used)
+  struct Job {
+    Raw<T, 8> a[2], b[NCB][2];
+    bool ok[2];
+  };
+  auto fetch = [&](Job& jb, int32_t base) {
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+      const int32_t p = base + 16 * s + i;
+      bool ok = p < p1;
+      int32_t r = ok ? (perm ? perm[p] : p) : 0;
+      if ((uint32_t)r >= (uint32_t)wa.n) {
+        r = 0;
+        ok = false;
+      }
+      jb.ok[s] = ok;
+      jb.a[s] = RowIO<T, 32>::fetch(A + (size_t)r * C + acol, g);
+#pragma unroll
+      for (int cb = 0; cb < NCB; ++cb)
+        if (cb < ncb) jb.b[cb][s] = RowIO<T, 32>::fetch(B + (size_t)r * C + n0 + 32 * cb, g);
+    }
+  };
+  Job cur;
+  if (p0 < p1) fetch(cur, p0);
+  for (int32_t base = p0; base < p1; base += 32) {
+    Job nxt;
+    const bool more = base + 32 < p1;
+    if (more) fetch(nxt, base + 32);
+    Raw<T, 8> fa[2];
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+      RowIO<T, 32>::arrange(cur.a[s]);
+      fa[s] = cur.ok[s] ? cur.a[s] : F::zero();
+    }
+    Raw<T, 8> pa[2];
+#pragma unroll
+    for (int et = 0; et < 2; ++et) {
+      pa[et] = rows_of(fa, et);
+      bacc[et] = F::mma(pa[et], ones, bacc[et]);
+    }
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb) {
+      if (cb >= ncb) break;
+      Raw<T, 8> fb[2];
+#pragma unroll
+      for (int s = 0; s < 2; ++s) {
+        RowIO<T, 32>::arrange(cur.b[cb][s]);
+        fb[s] = cur.ok[s] ? cur.b[cb][s] : F::zero();
+      }
+#pragma unroll
+      for (int ct = 0; ct < 2; ++ct) {
+        const Raw<T, 8> pb = rows_of(fb, ct);
+#pragma unroll
+        for (int et = 0; et < 2; ++et) acc[et][2 * cb + ct] = F::mma(pa[et], pb, acc[et][2 * cb + ct]);
+      }
+    }
+    if (more) cur = nxt;
+  }
+  // tile (et, ct): lane (c, g) component j is gradient entry
+  // [m0 + 16 et + 4 g + j][n0 + 16 ct + c]; the bias tile holds the row sums
+  const size_t total = (size_t)4 * C * C + 4 * (size_t)C;
+  float* part = wa.part + (size_t)grp * total;
+  float* dw = prob ? part + (size_t)3 * C * C : part;
+  float* db = prob ? part + (size_t)4 * C * C + 3 * C : part + (size_t)4 * C * C;
+#pragma unroll
+  for (int et = 0; et < 2; ++et) {
+#pragma unroll
+    for (int ct = 0; ct < 2 * NCB; ++ct) {
+      if (ct >= 2 * ncb) break;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) dw[(size_t)(m0 + 16 * et + 4 * g + j) * C + n0 + 16 * ct + i] = acc[et][ct][j];
+    }
+    if (chunk == 0 && i == 0) {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) db[m0 + 16 * et + 4 * g + j] = bacc[et][j];
+    }
+  }
+}
+
+// Sum of the groups' partials in group order: dW_qkv, dW_o, db_qkv, db_o (fp32).
+__global__ __launch_bounds__(256) void k_wgrad_reduce(const float* __restrict__ part, int32_t groups,
+                                                      int32_t C, float* __restrict__ dw_qkv,
+                                                      float* __restrict__ dw_o,
+                                                      float* __restrict__ db_qkv,
+                                                      float* __restrict__ db_o) {
+  const size_t total = (size_t)4 * C * C + 4 * (size_t)C;
+  for (size_t e = (size_t)blockIdx.x * blockDim.x + threadIdx.x; e < total;
+       e += (size_t)gridDim.x * blockDim.x) {
+    float s = 0.f;
+    for (int32_t gi = 0; gi < groups; ++gi) s += part[(size_t)gi * total + e];
+    const size_t cc = (size_t)C * C;
+    if (e < 3 * cc) dw_qkv[e] = s;
+    else if (e < 4 * cc) dw_o[e - 3 * cc] = s;
+    else if (e < 4 * cc + 3 * (size_t)C) { if (db_qkv) db_qkv[e - 4 * cc] = s; }
+    else if (db_o) db_o[e - 4 * cc - 3 * (size_t)C] = s;
+  }
+}
+
+// ------------------------------------------------------------ host side
+// Workspace: W_qkv^T [C][3C], W_o^T [C][C] (dtype); q, k, v, do, dq, dk, dv
+// [n][C] (dtype); the weight-gradient partials [groups][4 C^2 + 4 C] (fp32), with
+// one group per 512 rows, the partials held within 32 MiB.
+static int32_t wgrad_groups(int64_t n, int32_t C) {
+  const int64_t per = ((int64_t)4 * C * C + 4 * (int64_t)C) * 4;
+  int64_t g = (n + 511) / 512;
+  const int64_t cap = ((int64_t)32 << 20) / per;
+  if (g > cap) g = cap;
+  if (g < 1) g = 1;
+  return (int32_t)g;
+}
+
+struct ProjBwdLayout {
+  size_t wt_qkv, wt_o, act, act_stride, part, total;
+  int32_t groups;
+};
+
+static ProjBwdLayout proj_bwd_layout(int64_t n, int32_t C) {
+  ProjBwdLayout L;
+  size_t off = 0;
+  L.wt_qkv = off;
+  off = align_up(off + (size_t)3 * C * C * 2, 256);
+  L.wt_o = off;
+  off = align_up(off + (size_t)C * C * 2, 256);
+  L.act = off;
+  L.act_stride = align_up((size_t)n * C * 2, 256);
+  off += 7 * L.act_stride;
+  L.groups = wgrad_groups(n, C);
+  L.part = off;
+  off = align_up(off + (size_t)L.groups * ((size_t)4 * C * C + 4 * (size_t)C) * 4, 256);
+  L.total = off;
+  return L;
+}
+
+size_t projected_backward_workspace_bytes(int64_t n, int32_t C) { return proj_bwd_layout(n, C).total; }
+
+hipError_t launch_backward(const void* plan, int32_t n, int32_t W, int dtype, int32_t H, int32_t d,
+                           int phi, float eps, const void* q, const void* k, const void* v,
+                           const void* dout, void* dq, void* dk, void* dv, hipStream_t stream);
+
+template <typename T>
+static hipError_t rows_gemm(const RowGemmArgs& ga, hipStream_t stream) {
+  // 128 output columns a workgroup when its weight rows fit in 100 KB of LDS and
+  // the column blocks stay inside one output segment, else 64
+  const bool wide = ga.C % 128 == 0 && (size_t)128 * (ga.K + 8) * 2 <= 100 * 1024;
+  const int nb = wide ? 128 : 64;
+  const size_t lds = (size_t)nb * (ga.K + 8) * 2 + (size_t)nb * 4;
+  const int cols = ga.N / nb;
+  const int64_t tiles = ((int64_t)ga.npos + 63) / 64;
+  int64_t gx = 1024 / cols;
+  if (gx > tiles) gx = tiles;
+  if (gx < 1) gx = 1;
+  const void* kern = wide ? reinterpret_cast<const void*>(&k_rows_gemm<T, 8>)
+                          : reinterpret_cast<const void*>(&k_rows_gemm<T, 4>);
+  hipError_t e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024 - 1024);
+  if (e != hipSuccess) return e;
+  if (wide)
+    hipLaunchKernelGGL((k_rows_gemm<T, 8>), dim3((unsigned)gx, cols), dim3(256), lds, stream, ga);
+  else
+    hipLaunchKernelGGL((k_rows_gemm<T, 4>), dim3((unsigned)gx, cols), dim3(256), lds, stream, ga);
+  return hipGetLastError();
+}
+
+template <typename T>
+static hipError_t projected_backward_t(const void* plan, int32_t n, int32_t W, int dtype, int32_t H,
+                                       int32_t d, int phi, float eps, const void* x,
+                                       const void* wqkv, const void* bqkv, const void* wo,
+                                       const void* o, const void* dy, void* dx, float* dw_qkv,
+                                       float* db_qkv, float* dw_o, float* db_o, void* workspace,
+                                       hipStream_t stream) {
+  const int32_t C = H * d;
+  const PlanLayout lay = plan_layout(n, W);
+  const char* pb = static_cast<const char*>(plan);
+  const PlanHeader* hdr = reinterpret_cast<const PlanHeader*>(pb + lay.header);
+  const int32_t* offs = reinterpret_cast<const int32_t*>(pb + lay.offsets);
+  const int32_t* perm = reinterpret_cast<const int32_t*>(pb + lay.perm);
+  const ProjBwdLayout L = proj_bwd_layout(n, C);
+  char* ws = static_cast<char*>(workspace);
+  T* wt_qkv = reinterpret_cast<T*>(ws + L.wt_qkv);
+  T* wt_o = reinterpret_cast<T*>(ws + L.wt_o);
+  T* act[7];
+  for (int m = 0; m < 7; ++m) act[m] = reinterpret_cast<T*>(ws + L.act + m * L.act_stride);
+  T *q = act[0], *k = act[1], *v = act[2], *dov = act[3], *dq = act[4], *dk = act[5], *dv = act[6];
+  float* part = reinterpret_cast<float*>(ws + L.part);
+  hipError_t e;
+  // the weights as rows of the products below: W_qkv^T for dx, W_o^T for do
+  hipLaunchKernelGGL((k_transpose<T>), dim3((C + 31) / 32, (3 * C + 31) / 32), dim3(256), 0, stream,
+                     static_cast<const T*>(wqkv), wt_qkv, 3 * C, C);
+  hipLaunchKernelGGL((k_transpose<T>), dim3((C + 31) / 32, (C + 31) / 32), dim3(256), 0, stream,
+                     static_cast<const T*>(wo), wt_o, C, C);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  const int32_t* nvalid = offs + W;
+  // q | k | v = x W_qkv^T + b_qkv (the rows in windows)
+  RowGemmArgs ga{};
+  ga.hdr = hdr;
+  ga.perm = perm;
+  ga.nvalid = nvalid;
+  ga.C = C;
+  ga.n = n;
+  ga.W = W;
+  ga.npos = n;
+  ga.a[0] = x;
+  ga.out[0] = q;
+  ga.out[1] = k;
+  ga.out[2] = v;
+  ga.w = wqkv;
+  ga.bias = bqkv;
+  ga.K = C;
+  ga.N = 3 * C;
+  if ((e = rows_gemm<T>(ga, stream)) != hipSuccess) return e;
+  // do = dy W_o
+  ga.a[0] = dy;
+  ga.out[0] = dov;
+  ga.w = wt_o;
+  ga.bias = nullptr;
+  ga.N = C;
+  if ((e = rows_gemm<T>(ga, stream)) != hipSuccess) return e;
+  // dq, dk, dv
+  if ((e = launch_backward(plan, n, W, dtype, H, d, phi, eps, q, k, v, dov, dq, dk, dv, stream)) != hipSuccess)
+    return e;
+  // dx = [dq | dk | dv] W_qkv, zero for rows in no window
+  ga.a[0] = dq;
+  ga.a[1] = dk;
+  ga.a[2] = dv;
+  ga.out[0] = dx;
+  ga.w = wt_qkv;
+  ga.K = 3 * C;
+  ga.N = C;
+  if ((e = rows_gemm<T>(ga, stream)) != hipSuccess) return e;
+  // weight and bias gradients: partials per row group, then their ordered sum
+  WgradArgs wa{};
+  wa.a0[0] = dq;
+  wa.a0[1] = dk;
+  wa.a0[2] = dv;
+  wa.b0 = x;
+  wa.a1 = dy;
+  wa.b1 = o;
+  wa.hdr = hdr;
+  wa.perm = perm;
+  wa.nvalid = nvalid;
+  wa.part = part;
+  wa.C = C;
+  wa.n = n;
+  wa.W = W;
+  wa.groups = L.groups;
+  wa.chunks = (C + 32 * kWgradChunkBlocks - 1) / (32 * kWgradChunkBlocks);
+  wa.units0 = (3 * C / 32) * wa.chunks;
+  wa.units1 = (C / 32) * wa.chunks;
+  const int64_t waves = (int64_t)L.groups * (wa.units0 + wa.units1);
+  hipLaunchKernelGGL((k_wgrad<T>), dim3((unsigned)((waves + 3) / 4)), dim3(256), 0, stream, wa);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  const int64_t total = (int64_t)4 * C * C + 4 * (int64_t)C;
+  hipLaunchKernelGGL(k_wgrad_reduce, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, stream,
+                     static_cast<const float*>(part), L.groups, C, dw_qkv, dw_o, db_qkv, db_o);
+  return hipGetLastError();
+}
+
+// dtype: 1 f16, 2 bf16; C = H d in {64, 128, 256}; phi: 0 elu + 1, 1 ReLU
+hipError_t launch_backward_projected(const void* plan, int32_t n, int32_t W, int dtype, int32_t H,
+                                     int32_t d, int phi, float eps, const void* x, const void* wqkv,
+                                     const void* bqkv, const void* wo, const void* o, const void* dy,
+                                     void* dx, float* dw_qkv, float* db_qkv, float* dw_o,
+                                     float* db_o, void* workspace, hipStream_t stream) {
+  if (dtype == 1)
+    return projected_backward_t<_Float16>(plan, n, W, dtype, H, d, phi, eps, x, wqkv, bqkv, wo, o, dy, dx,
+                                          dw_qkv, db_qkv, dw_o, db_o, workspace, stream);
+  return projected_backward_t<bf16_t>(plan, n, W, dtype, H, d, phi, eps, x, wqkv, bqkv, wo, o, dy, dx,
+                                      dw_qkv, db_qkv, dw_o, db_o, workspace, stream);
+}
+
+}  // namespace sla

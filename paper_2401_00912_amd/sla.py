@@ -46,6 +46,8 @@ EXPORTED = (
     "sla_forward_ex",
     "sla_backward_ex",
     "sla_forward_projected",
+    "sla_backward_projected_workspace_bytes",
+    "sla_backward_projected",
     "sla_cwi_map_bytes",
     "sla_cwi_build_map",
     "sla_cwi_forward",
@@ -116,6 +118,10 @@ def lib() -> ctypes.CDLL:
     L.sla_backward_ex.argtypes = [vp, sz, i64, i32, en, i32, i32, en, f32, vp, vp, vp, vp, vp, vp, vp, vp]
     L.sla_forward_projected.restype = ctypes.c_int
     L.sla_forward_projected.argtypes = [vp, sz, i64, i32, en, i32, i32, en, f32, vp, vp, vp, vp, vp, vp, vp, vp]
+    L.sla_backward_projected_workspace_bytes.restype = sz
+    L.sla_backward_projected_workspace_bytes.argtypes = [i64, i32, i32]
+    L.sla_backward_projected.restype = ctypes.c_int
+    L.sla_backward_projected.argtypes = [vp, sz, i64, i32, en, i32, i32, en, f32] + [vp] * 11 + [vp, sz, vp]
     L.sla_cwi_map_bytes.restype = sz
     L.sla_cwi_map_bytes.argtypes = [i32, i32, i32]
     L.sla_cwi_build_map.restype = ctypes.c_int
@@ -424,6 +430,53 @@ def forward_projected(plan: Plan, x, w_qkv, w_o, heads: int, b_qkv=None, b_o=Non
                                      _stream(x.device))
     _check(st, "sla_forward_projected")
     return o, y
+
+
+def backward_projected_workspace_bytes(n: int, heads: int, head_dim: int) -> int:
+    return int(lib().sla_backward_projected_workspace_bytes(int(n), int(heads), int(head_dim)))
+
+
+def backward_projected(plan: Plan, x, w_qkv, w_o, o, dy, heads: int, b_qkv=None, feature_map="elu1", eps=0.0,
+                       dx=None, workspace=None, bias_grads=True):
+    """Gradients of sla_forward_projected (sla_backward_projected): x, dy [n, C],
+    w_qkv [3C, C], w_o [C, C], o the forward's SLA output ([n, heads, d] or [n, C]),
+    optional b_qkv [3C].  Returns (dx, dw_qkv, db_qkv, dw_o, db_o): dx like x, the
+    weight and bias gradients float32 (the bias ones None with bias_grads=False)."""
+    torch = _torch()
+    if x.dim() != 2 or x.shape[0] != plan.n or not x.is_contiguous():
+        raise ValueError(f"x must be a contiguous [n, C] tensor with n={plan.n}")
+    n, C = x.shape
+    if C % heads:
+        raise ValueError("C must be a multiple of heads")
+    d = C // heads
+    for name, t, shape in (("w_qkv", w_qkv, (3 * C, C)), ("w_o", w_o, (C, C)), ("b_qkv", b_qkv, (3 * C,)),
+                           ("dy", dy, (n, C))):
+        if t is None:
+            continue
+        if tuple(t.shape) != shape or t.dtype != x.dtype or t.device != x.device or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous {shape} tensor like x")
+    if o.dtype != x.dtype or o.device != x.device or not o.is_contiguous() or o.numel() != n * C:
+        raise ValueError("o must be the forward's contiguous [n, C] output, like x")
+    dx = torch.empty_like(x) if dx is None else dx
+    if dx.shape != x.shape or dx.dtype != x.dtype or not dx.is_contiguous() or dx.device != x.device:
+        raise ValueError("dx must be a contiguous tensor like x")
+    f32 = dict(dtype=torch.float32, device=x.device)
+    dw_qkv, dw_o = torch.empty((3 * C, C), **f32), torch.empty((C, C), **f32)
+    db_qkv = torch.empty(3 * C, **f32) if bias_grads else None
+    db_o = torch.empty(C, **f32) if bias_grads else None
+    need = backward_projected_workspace_bytes(n, heads, d)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=x.device)
+    _check_workspace(workspace, x.device)
+    if feature_map not in FEATURE_MAPS:
+        raise ValueError(f"feature_map must be one of {sorted(FEATURE_MAPS)}, not {feature_map!r}")
+    st = lib().sla_backward_projected(_ptr(plan.buf), plan.nbytes, plan.n, plan.num_windows,
+                                      _dtype_code(x.dtype), heads, d, FEATURE_MAPS[feature_map], float(eps),
+                                      _ptr(x), _ptr(w_qkv), _ptr(b_qkv), _ptr(w_o), _ptr(o), _ptr(dy), _ptr(dx),
+                                      _ptr(dw_qkv), _ptr(db_qkv), _ptr(dw_o), _ptr(db_o), _ptr(workspace),
+                                      workspace.numel() * workspace.element_size(), _stream(x.device))
+    _check(st, "sla_backward_projected")
+    return dx, dw_qkv, db_qkv, dw_o, db_o
 
 
 def cwi_map_bytes(gx: int, gy: int, gz: int) -> int:

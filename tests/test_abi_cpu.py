@@ -222,6 +222,35 @@ def test_projected_argument_errors(L):
     assert call(n=0) == sla.SLA_OK
 
 
+def test_projected_backward_argument_errors(L):
+    nb = sla.plan_bytes(100, 8)
+    need = sla.backward_projected_workspace_bytes(100, 4, 32)
+    assert need > 0
+    assert sla.backward_projected_workspace_bytes(100, 3, 32) == 0            # C = 96
+    assert sla.backward_projected_workspace_bytes(-1, 4, 32) == 0
+    # the workspace grows with n
+    assert sla.backward_projected_workspace_bytes(1000, 4, 32) > need
+
+    def call(dtype=1, H=4, d=32, fm=0, eps=0.0, x=FAKE, dy=FAKE, dx=FAKE, dwq=FAKE, dwo=FAKE, dbq=None,
+             ws=FAKE, wsb=None):
+        return L.sla_backward_projected(FAKE, nb, 100, 8, dtype, H, d, fm, eps, x, FAKE, None, FAKE, FAKE,
+                                        dy, dx, dwq, dbq, dwo, None, ws, need if wsb is None else wsb, None)
+    assert call(dtype=0) == sla.SLA_E_UNSUPPORTED        # fp32 is not supported
+    assert call(H=3) == sla.SLA_E_UNSUPPORTED            # C = 96
+    assert call(d=24) == sla.SLA_E_UNSUPPORTED
+    assert call(fm=3) == sla.SLA_E_ARG
+    assert call(eps=-1.0) == sla.SLA_E_ARG
+    assert call(x=FAKE + 8) == sla.SLA_E_ARG
+    assert call(dy=None) == sla.SLA_E_ARG
+    assert call(dx=FAKE + 4) == sla.SLA_E_ARG
+    assert call(dwq=None) == sla.SLA_E_ARG
+    assert call(dwo=FAKE + 2) == sla.SLA_E_ARG
+    assert call(dbq=FAKE + 1) == sla.SLA_E_ARG
+    assert call(ws=None) == sla.SLA_E_ARG
+    assert call(ws=FAKE + 16) == sla.SLA_E_ARG
+    assert call(wsb=need - 1) == sla.SLA_E_WORKSPACE
+
+
 def test_cwi_argument_errors(L):
     assert sla.cwi_map_bytes(468, 468, 1) == 4 * 468 * 468
     assert sla.cwi_map_bytes(0, 4, 1) == 0 and sla.cwi_map_bytes(1 << 16, 1 << 16, 1) == 0

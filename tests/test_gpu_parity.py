@@ -60,6 +60,9 @@ def check_plan(S, plan, ids, W, chunk_rows, offsets_in=None):
         assert int(plan.invalid.cpu()[0]) == inv
         assert np.array_equal(offs.astype(np.int64), o_ref), "offsets differ"
         assert np.array_equal(perm[:nvalid].astype(np.int64), p_ref), "perm differs"
+        # rows outside every window follow, in row order
+        outside = np.flatnonzero((ids < 0) | (ids >= W))
+        assert np.array_equal(perm[nvalid:].astype(np.int64), outside), "perm tail differs"
         assert np.array_equal(plan.perm.cpu().numpy()[:nvalid].astype(np.int64), p_ref)
         assert np.array_equal(plan.offsets.cpu().numpy().astype(np.int64), o_ref)
         assert header["csr"] == 0
@@ -707,6 +710,83 @@ def test_projected_long_windows(sla):
         for dtype in ("f16", "bf16"):
             projected_parity(sla, ids, None, ids.size, lengths.size, 4, 32, dtype, seed=5,
                              label=f"long{lengths.size}")
+
+
+# ---------------------------------------------------------- projected backward
+def projected_backward_parity(S, ids, offsets, n, W, H, d, dtype, fmap="elu1", eps=0.0, bias=True, seed=0,
+                              label=""):
+    import torch
+
+    rng = np.random.default_rng([57, seed, H, d])
+    C = H * d
+    cast = lambda a: workloads.cast_values(np.asarray(a, dtype=np.float32), dtype)  # noqa: E731
+    x = cast(rng.standard_normal((n, C)))
+    wq = cast(rng.standard_normal((3 * C, C)) / np.sqrt(C))
+    wo = cast(rng.standard_normal((C, C)) / np.sqrt(C))
+    bq = cast(0.2 * rng.standard_normal(3 * C)) if bias else None
+    bo = cast(0.2 * rng.standard_normal(C)) if bias else None
+    dy = cast(rng.standard_normal((n, C)))
+    plan = build(S, ids=ids, W=W, offsets=offsets, n=n)
+    off, perm = check_plan(S, plan, ids, W, 0, offsets)
+    dev = lambda a: None if a is None else to_dev(a, dtype)  # noqa: E731
+    tx, twq, two, tbq, tdy = dev(x), dev(wq), dev(wo), dev(bq), dev(dy)
+    o, _ = S.forward_projected(plan, tx, twq, two, H, tbq, dev(bo), None, None, fmap, eps)
+    dx = torch.full((n, C), float("nan"), dtype=torch_dtype(dtype), device="cuda")
+    got = S.backward_projected(plan, tx, twq, two, o, tdy, H, tbq, fmap, eps, dx=dx)
+    torch.cuda.synchronize()
+    gdx = to_host64(got[0], dtype)
+    gw = [t.cpu().numpy().astype(np.float64) for t in got[1:]]
+    w = lambda a: None if a is None else oracle.widen(a, dtype)  # noqa: E731
+    ref = oracle.sla_projected_backward_ref(w(x), w(wq), w(bq), w(wo), w(bo), w(dy), H, off, perm, fmap, eps)
+    rows = np.zeros(n, dtype=bool)
+    rows[perm if perm is not None else np.arange(off[-1])] = True
+    assert np.all(gdx[~rows] == 0.0), f"{label}: dx of rows in no window is not zero"
+    edx = rel_err_per_head(gdx.reshape(n, H, d), ref[0].reshape(n, H, d), 1e-3 * float(np.abs(ref[0]).max()),
+                           rows)
+    names = ("dw_qkv", "db_qkv", "dw_o", "db_o")
+    errs = []
+    for name, g, r in zip(names, gw, ref[1:]):
+        assert np.all(np.isfinite(g)), f"{label}: {name} not finite"
+        errs.append(float(np.abs(g - r).max()) / max(float(np.abs(r).max()), 1e-30))
+    _say(f"[proj-bwd {label}] n={n} H={H} d={d} {dtype} {fmap} eps={eps} dx {edx:.3e} "
+         + " ".join(f"{nm} {e:.3e}" for nm, e in zip(names, errs)))
+    assert edx <= TOL[dtype], f"{label}: dx relative error {edx:.3e}"
+    for nm, e in zip(names, errs):
+        assert e <= TOL[dtype], f"{label}: {nm} relative error {e:.3e}"
+    return got
+
+
+@pytest.mark.parametrize("cfg", [2, 3, 4])
+def test_projected_backward_config(sla, cfg):
+    wl = workloads.make_config(cfg, with_grad=False)
+    projected_backward_parity(sla, wl["ids"], None, wl["n"], wl["num_windows"], wl["heads"], wl["head_dim"],
+                              wl["dtype"], label=f"cfg{cfg}")
+
+
+@pytest.mark.parametrize("dtype", ["f16", "bf16"])
+@pytest.mark.parametrize("shape", [(2, 32), (8, 16), (4, 16), (16, 16)])
+def test_projected_backward_shapes(sla, dtype, shape):
+    # adversarial window lengths, 1% of the rows in no window, both maps
+    H, d = shape
+    rng = np.random.default_rng([58, H, d, len(dtype)])
+    lengths = _adversarial_lengths(rng, 128)
+    ids = workloads.ids_from_lengths(lengths, rng)
+    ids[rng.random(ids.size) < 0.01] = -1
+    n, W = ids.size, lengths.size
+    projected_backward_parity(sla, ids, None, n, W, H, d, dtype, seed=1, label=f"shape{shape}")
+    projected_backward_parity(sla, ids, None, n, W, H, d, dtype, fmap="relu", eps=1e-3, bias=False, seed=2,
+                              label=f"shape{shape}-relu")
+
+
+def test_projected_backward_csr_and_determinism(sla):
+    import torch
+
+    wl = workloads.make_config(2, with_grad=False)
+    perm, off, _ = oracle.segments_ref(wl["ids"], wl["num_windows"])
+    a = projected_backward_parity(sla, None, off, wl["n"], wl["num_windows"], 4, 32, "f16", seed=3, label="csr")
+    b = projected_backward_parity(sla, None, off, wl["n"], wl["num_windows"], 4, 32, "f16", seed=3, label="csr")
+    for x, y in zip(a, b):
+        assert torch.equal(x, y), "two runs differ"
 
 
 # ---------------------------------------------------- cross-window interaction
