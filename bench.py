@@ -723,11 +723,18 @@ def bench_projected(torch, sla, workloads, dev, args):
         x = torch.randn(n, C, generator=gen).to(tdt).to(dev)
         plan = sla.build_segments(torch.from_numpy(wl["ids"]).to(dev), num_windows=W, want_perm=False)
         sets.append({"x": x, "plan": plan, "o": torch.empty(n, H, d, dtype=tdt, device=dev),
-                     "y": torch.empty(n, C, dtype=tdt, device=dev)})
+                     "y": torch.empty(n, C, dtype=tdt, device=dev),
+                     "dy": torch.randn(n, C, generator=gen).to(tdt).to(dev),
+                     "dx": torch.empty(n, C, dtype=tdt, device=dev)})
+    ws = torch.empty(sla.backward_projected_workspace_bytes(n, H, d), dtype=torch.uint8, device=dev)
     torch.cuda.synchronize()
 
     def fused(st):
         sla.forward_projected(st["plan"], st["x"], w_qkv, w_o, H, b_qkv, b_o, st["o"], st["y"])
+
+    def backward(st):
+        sla.backward_projected(st["plan"], st["x"], w_qkv, w_o, st["o"], st["dy"], H, b_qkv, dx=st["dx"],
+                               workspace=ws)
 
     def unfused(st):
         qkv = Fn.linear(st["x"], w_qkv, b_qkv)
@@ -763,8 +770,14 @@ def bench_projected(torch, sla, workloads, dev, args):
     reps = max(50, args.steps)
     t_fused = timed(fused, reps)
     t_unfused = timed(unfused, reps)
+    for st in sets:     # the forward's o of every set, for the backward
+        fused(st)
+    t_backward = timed(backward, reps)
     fused_bytes = 4 * n * C * e     # x read, o written; o read, y written
     unfused_bytes = 10 * n * C * e  # + q, k, v written and read, and their copies' extra pass
+    # backward, least traffic: x, o, dy read and dx written (q, k, v, do, dq, dk, dv
+    # are intermediates), plus the SLA backward's own 7 n C e
+    backward_bytes = (4 + 7) * n * C * e
     return {
         "mode": "projected",
         "workload": base["name"],
@@ -777,6 +790,12 @@ def bench_projected(torch, sla, workloads, dev, args):
         "fused_frac_of_hbm_peak": fused_bytes / (t_fused * 1e-6) / 1e9 / HBM_PEAK_GBS,
         "unfused_chain": "torch linear (x W_qkv^T + b), three contiguous q/k/v copies, sla_forward, "
                          "torch linear (o W_o^T + b)",
+        "backward_us": t_backward,
+        "backward_algorithmic_bytes": backward_bytes,
+        "backward_gbs": backward_bytes / (t_backward * 1e-6) / 1e9,
+        "backward_frac_of_hbm_peak": backward_bytes / (t_backward * 1e-6) / 1e9 / HBM_PEAK_GBS,
+        "backward_path": "sla_backward_projected: q, k, v recomputed, do, SLA backward, dx, "
+                         "weight and bias gradients (fp32, fixed-order sums)",
     }
 
 

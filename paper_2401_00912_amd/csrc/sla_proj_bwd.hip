@@ -9,9 +9,10 @@
 //     dx = [dq | dk | dv] W_qkv,        dW_qkv = [dq | dk | dv]^T x,
 //     db_qkv = sum_rows [dq | dk | dv].
 // q, k, v are recomputed from x (they never reach HBM in the forward), o is the
-// forward's output.  Six launches:
+// forward's output.  The launches:
 //   k_transpose     W_qkv^T and W_o^T into the workspace, so that every product
 //                   below reads its weights as rows;
+//   k_row_mask      which rows lie in a window (from the plan's permutation);
 //   k_rows_gemm     q | k | v = x W_qkv^T + b_qkv, and do = dy W_o: a row of the
 //                   output is a row of the input times a weight matrix held in LDS;
 //   (SLA backward)  dq, dk, dv;
@@ -20,8 +21,10 @@
 //                   gradients: sums over rows on the matrix cores, after the rows
 //                   are turned into contraction operands (0/1 selection products);
 //   k_wgrad_reduce  the groups' partials summed in group order.
-// Rows are visited in the plan's sorted order, so every sum has a fixed order and
-// the results do not depend on scheduling.
+// Rows are visited in their own order, rows in no window masked out; every sum
+// over rows has a fixed order, so the results do not depend on scheduling.
+#include <algorithm>
+
 #include "sla_attn_core.h"
 
 namespace sla {
@@ -43,35 +46,52 @@ __global__ __launch_bounds__(256) void k_transpose(const T* __restrict__ src, T*
     if (j0 + r < N && k0 + tx < K) d[(size_t)(j0 + r) * K + k0 + tx] = tile[tx][r];
 }
 
+// ------------------------------------------------------------ rows in windows
+// mask[row] = 1 for the rows in a window, 0 for the others: the plan's sorted
+// positions [0, offsets[W]) hold the rows in windows and, for a plan built from
+// window ids, positions [offsets[W], n) the others, so every row is written once.
+__global__ __launch_bounds__(256) void k_row_mask(const PlanHeader* __restrict__ hdr,
+                                                  const int32_t* __restrict__ perm,
+                                                  const int32_t* __restrict__ nvalid_p, int32_t n,
+                                                  int32_t W, uint8_t* __restrict__ mask) {
+  if (hdr->magic != kPlanMagic || hdr->n != n || hdr->num_windows != W) return;
+  const bool csr = hdr->csr != 0;
+  const int32_t nvalid = max(0, min(*nvalid_p, n));
+  for (int32_t p = (int32_t)(blockIdx.x * blockDim.x + threadIdx.x); p < n;
+       p += (int32_t)(gridDim.x * blockDim.x)) {
+    const int32_t row = csr ? p : perm[p];
+    if ((uint32_t)row < (uint32_t)n) mask[row] = p < nvalid ? 1 : 0;
+  }
+}
+
 // ------------------------------------------------------------ row products
 // out[row][n0 + j] = sum_k A(row, k) Wr[n0 + j][k] + bias[n0 + j], j < 16 NBT, for
-// the rows at sorted positions [0, npos) (row = perm[p], or p without one).
-// A(row, k) = a[k / C][row][k % C] over nseg segments [n, C] (K = nseg C); Wr is
-// [N, K] row-major (a weight in the [out, in] layout); output column j goes to
-// out[j / C][row][j % C].  Positions at or after *nvalid (rows in no window) get
-// zero input, so their outputs are the bias (zero when there is none).
+// every row.  A(row, k) = a[k / C][row][k % C] over nseg segments [n, C] (K =
+// nseg C); Wr is [N, K] row-major (a weight in the [out, in] layout); output
+// column j goes to out[j / C][row][j % C].  Rows in no window (mask 0) get zero
+// input, so their outputs are the bias (zero when there is none).
 //
-// One workgroup keeps the weight rows of its 16 NBT output columns in LDS (padded
-// rows of K + 8 elements) and walks 16-row tiles, one per wave: with the weight
-// rows as the first matrix-core operand and the input rows (16-byte pieces of 8
-// channels) as the second, lane (i, g) receives columns 16 t + 4 g .. + 3 of the
-// tile's row i, stored as one 4-element piece.
+// One workgroup of 16 waves keeps the weight rows of its 16 NBT output columns in
+// LDS (padded rows of K + 8 elements) and walks 16-row tiles, one per wave: with
+// the weight rows as the first matrix-core operand and the input rows (16-byte
+// pieces of 8 channels) as the second, lane (i, g) receives columns
+// 16 t + 4 g .. + 3 of the tile's row i, stored as one 4-element piece.
+constexpr int kRowGemmThreads = 1024;
+
 struct RowGemmArgs {
   const void* a[3];
   void* out[3];
   const void* w;             // Wr [N, K]
   const void* bias;          // [N] or null
-  const PlanHeader* hdr;     // the plan: a CSR plan's rows are its positions
-  const int32_t* perm;       // the plan's permutation (read for plans built from ids)
-  const int32_t* nvalid;     // the plan's offsets[W]: rows in windows
-  int32_t C, K, N, npos, n, W;
+  const PlanHeader* hdr;
+  const uint8_t* mask;       // rows in windows
+  int32_t C, K, N, n, W;
 };
 
 template <typename T, int NBT>
-__global__ __launch_bounds__(256) void k_rows_gemm(RowGemmArgs ga) {
+__global__ __launch_bounds__(kRowGemmThreads) void k_rows_gemm(RowGemmArgs ga) {
   constexpr int NB = 16 * NBT;
   if (ga.hdr->magic != kPlanMagic || ga.hdr->n != ga.n || ga.hdr->num_windows != ga.W) return;
-  const int32_t* perm = ga.hdr->csr ? nullptr : ga.perm;
   extern __shared__ __attribute__((aligned(16))) unsigned char lds_raw[];
   const int K = ga.K, LDW = K + 8, C = ga.C;
   T* s_w = reinterpret_cast<T*>(lds_raw);
@@ -93,16 +113,15 @@ __global__ __launch_bounds__(256) void k_rows_gemm(RowGemmArgs ga) {
   const floatx4 zero = {0.f, 0.f, 0.f, 0.f};
   const int lane = lane_id(), wv = threadIdx.x >> 6;
   const int i = lane & 15, g = lane >> 4;
-  const int32_t nvalid = min(*ga.nvalid, ga.npos);
   const int nseg = K / C;
   T* outp = static_cast<T*>(ga.out[n0 / C]);
   const int ocol = n0 % C;
-  for (int32_t tile = (int32_t)blockIdx.x * 4 + wv; tile * 16 < ga.npos; tile += (int32_t)gridDim.x * 4) {
+  constexpr int NW = kRowGemmThreads / 64;
+  for (int32_t tile = (int32_t)blockIdx.x * NW + wv; tile * 16 < ga.n; tile += (int32_t)gridDim.x * NW) {
     const int32_t p = tile * 16 + i;
-    const bool inside = p < ga.npos;
-    const bool valid = p < nvalid;
-    int32_t row = inside ? (perm ? perm[p] : p) : 0;
-    if ((uint32_t)row >= (uint32_t)ga.n) row = 0;
+    const bool inside = p < ga.n;
+    const int32_t row = inside ? p : 0;
+    const bool valid = inside && ga.mask[row] != 0;
     floatx4 acc[NBT];
 #pragma unroll
     for (int t = 0; t < NBT; ++t) acc[t] = zero;
@@ -134,12 +153,12 @@ __global__ __launch_bounds__(256) void k_rows_gemm(RowGemmArgs ga) {
 }
 
 // ------------------------------------------------------------ weight gradients
-// Unit (problem, 32-row slab m0 of the gradient, column chunk n0 of up to 128,
-// row group): partial[group][m0 + e][n0 + c] = sum over the group's rows of
-// A(row, m0 + e) B(row, n0 + c), and, for n0 = 0, the bias partial
+// Unit (problem, 32-row slab m0 of the gradient, column chunk n0 of 64 columns,
+// row group): partial[group][m0 + e][n0 + c] = sum over the group's rows in
+// windows of A(row, m0 + e) B(row, n0 + c), and, for n0 = 0, the bias partial
 // sum_rows A(row, m0 + e).  Problem 0: A = [dq | dk | dv] (3C columns), B = x;
-// problem 1: A = dy, B = o.  Rows are the sorted positions [0, nvalid) of the
-// plan, split into `groups` contiguous ranges; a wave takes one unit and walks its
+// problem 1: A = dy, B = o.  The rows 0..n-1 are split into `groups` contiguous
+// ranges (rows in no window are masked out); a wave takes one unit and walks its
 // rows 32 at a time: each 32-column block of a row is fetched as a row fragment
 // and turned into the operand of a contraction over rows (as the attention's
 // state sums), then the slab's 2 x 2 tiles per column block accumulate.
@@ -149,13 +168,12 @@ struct WgradArgs {
   const void* a1;        // dy [n, C]
   const void* b1;        // o [n, C]
   const PlanHeader* hdr;
-  const int32_t* perm;
-  const int32_t* nvalid;
+  const uint8_t* mask;   // rows in windows
   float* part;           // [groups][total]: dW_qkv [3C][C], dW_o [C][C], db_qkv [3C], db_o [C]
   int32_t C, n, W, groups, units0, units1, chunks;
 };
 
-constexpr int kWgradChunkBlocks = 4;   // 32-column blocks per column chunk
+constexpr int kWgradChunkBlocks = 2;   // 32-column blocks per column chunk
 
 template <typename T>
 __global__ __launch_bounds__(256) void k_wgrad(WgradArgs wa) {
@@ -163,7 +181,6 @@ __global__ __launch_bounds__(256) void k_wgrad(WgradArgs wa) {
   constexpr int NCB = kWgradChunkBlocks;
   const floatx4 zero = {0.f, 0.f, 0.f, 0.f};
   if (wa.hdr->magic != kPlanMagic || wa.hdr->n != wa.n || wa.hdr->num_windows != wa.W) return;
-  const int32_t* perm = wa.hdr->csr ? nullptr : wa.perm;
   const int lane = lane_id();
   const int i = lane & 15, g = lane >> 4;
   const int C = wa.C;
@@ -181,9 +198,8 @@ __global__ __launch_bounds__(256) void k_wgrad(WgradArgs wa) {
   const T* A = prob ? static_cast<const T*>(wa.a1) : static_cast<const T*>(wa.a0[m0 / C]);
   const int acol = m0 % C;
   const T* B = static_cast<const T*>(prob ? wa.b1 : wa.b0);
-  const int32_t nvalid = max(0, min(*wa.nvalid, wa.n));
-  const int32_t p0 = (int32_t)((int64_t)nvalid * grp / wa.groups);
-  const int32_t p1 = (int32_t)((int64_t)nvalid * (grp + 1) / wa.groups);
+  const int32_t p0 = (int32_t)((int64_t)wa.n * grp / wa.groups);
+  const int32_t p1 = (int32_t)((int64_t)wa.n * (grp + 1) / wa.groups);
   const Sel<T, 32> sel(i, g);
   float one8[8] = {1.f, 1.f, 1.f, 1.f, 1.f, 1.f, 1.f, 1.f};
   const Raw<T, 8> ones = F::from_f32(one8);
@@ -207,13 +223,8 @@ __global__ __launch_bounds__(256) void k_wgrad(WgradArgs wa) {
 #pragma unroll
     for (int s = 0; s < 2; ++s) {
       const int32_t p = base + 16 * s + i;
-      bool ok = p < p1;
-      int32_t r = ok ? (perm ? perm[p] : p) : 0;
-      if ((uint32_t)r >= (uint32_t)wa.n) {
-        r = 0;
-        ok = false;
-      }
-      jb.ok[s] = ok;
+      const int32_t r = p < p1 ? p : p0;
+      jb.ok[s] = p < p1 && wa.mask[r] != 0;
       jb.a[s] = RowIO<T, 32>::fetch(A + (size_t)r * C + acol, g);
 #pragma unroll
       for (int cb = 0; cb < NCB; ++cb)
@@ -286,8 +297,17 @@ __global__ __launch_bounds__(256) void k_wgrad_reduce(const float* __restrict__ 
   const size_t total = (size_t)4 * C * C + 4 * (size_t)C;
   for (size_t e = (size_t)blockIdx.x * blockDim.x + threadIdx.x; e < total;
        e += (size_t)gridDim.x * blockDim.x) {
+    // eight loads in flight, added in group order
     float s = 0.f;
-    for (int32_t gi = 0; gi < groups; ++gi) s += part[(size_t)gi * total + e];
+    int32_t gi = 0;
+    for (; gi + 8 <= groups; gi += 8) {
+      float v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = part[(size_t)(gi + u) * total + e];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) s += v[u];
+    }
+    for (; gi < groups; ++gi) s += part[(size_t)gi * total + e];
     const size_t cc = (size_t)C * C;
     if (e < 3 * cc) dw_qkv[e] = s;
     else if (e < 4 * cc) dw_o[e - 3 * cc] = s;
@@ -310,7 +330,7 @@ static int32_t wgrad_groups(int64_t n, int32_t C) {
 }
 
 struct ProjBwdLayout {
-  size_t wt_qkv, wt_o, act, act_stride, part, total;
+  size_t wt_qkv, wt_o, mask, act, act_stride, part, total;
   int32_t groups;
 };
 
@@ -321,6 +341,8 @@ static ProjBwdLayout proj_bwd_layout(int64_t n, int32_t C) {
   off = align_up(off + (size_t)3 * C * C * 2, 256);
   L.wt_o = off;
   off = align_up(off + (size_t)C * C * 2, 256);
+  L.mask = off;
+  off = align_up(off + (size_t)n, 256);
   L.act = off;
   L.act_stride = align_up((size_t)n * C * 2, 256);
   off += 7 * L.act_stride;
@@ -345,8 +367,9 @@ static hipError_t rows_gemm(const RowGemmArgs& ga, hipStream_t stream) {
   const int nb = wide ? 128 : 64;
   const size_t lds = (size_t)nb * (ga.K + 8) * 2 + (size_t)nb * 4;
   const int cols = ga.N / nb;
-  const int64_t tiles = ((int64_t)ga.npos + 63) / 64;
-  int64_t gx = 1024 / cols;
+  // about one workgroup per CU, each walking many tiles with its staged weights
+  const int64_t tiles = ((int64_t)ga.n + 16 * (kRowGemmThreads / 64) - 1) / (16 * (kRowGemmThreads / 64));
+  int64_t gx = (256 + cols - 1) / cols;
   if (gx > tiles) gx = tiles;
   if (gx < 1) gx = 1;
   const void* kern = wide ? reinterpret_cast<const void*>(&k_rows_gemm<T, 8>)
@@ -354,9 +377,9 @@ static hipError_t rows_gemm(const RowGemmArgs& ga, hipStream_t stream) {
   hipError_t e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024 - 1024);
   if (e != hipSuccess) return e;
   if (wide)
-    hipLaunchKernelGGL((k_rows_gemm<T, 8>), dim3((unsigned)gx, cols), dim3(256), lds, stream, ga);
+    hipLaunchKernelGGL((k_rows_gemm<T, 8>), dim3((unsigned)gx, cols), dim3(kRowGemmThreads), lds, stream, ga);
   else
-    hipLaunchKernelGGL((k_rows_gemm<T, 4>), dim3((unsigned)gx, cols), dim3(256), lds, stream, ga);
+    hipLaunchKernelGGL((k_rows_gemm<T, 4>), dim3((unsigned)gx, cols), dim3(kRowGemmThreads), lds, stream, ga);
   return hipGetLastError();
 }
 
@@ -381,6 +404,7 @@ static hipError_t projected_backward_t(const void* plan, int32_t n, int32_t W, i
   for (int m = 0; m < 7; ++m) act[m] = reinterpret_cast<T*>(ws + L.act + m * L.act_stride);
   T *q = act[0], *k = act[1], *v = act[2], *dov = act[3], *dq = act[4], *dk = act[5], *dv = act[6];
   float* part = reinterpret_cast<float*>(ws + L.part);
+  uint8_t* mask = reinterpret_cast<uint8_t*>(ws + L.mask);
   hipError_t e;
   // the weights as rows of the products below: W_qkv^T for dx, W_o^T for do
   hipLaunchKernelGGL((k_transpose<T>), dim3((C + 31) / 32, (3 * C + 31) / 32), dim3(256), 0, stream,
@@ -388,16 +412,18 @@ static hipError_t projected_backward_t(const void* plan, int32_t n, int32_t W, i
   hipLaunchKernelGGL((k_transpose<T>), dim3((C + 31) / 32, (C + 31) / 32), dim3(256), 0, stream,
                      static_cast<const T*>(wo), wt_o, C, C);
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  const int32_t* nvalid = offs + W;
-  // q | k | v = x W_qkv^T + b_qkv (the rows in windows)
+  // which rows lie in a window
+  const int64_t mblocks = std::min<int64_t>(1024, std::max<int64_t>(1, ((int64_t)n + 255) / 256));
+  hipLaunchKernelGGL(k_row_mask, dim3((unsigned)mblocks), dim3(256), 0, stream, hdr, perm, offs + W, n, W,
+                     mask);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  // q | k | v = x W_qkv^T + b_qkv
   RowGemmArgs ga{};
   ga.hdr = hdr;
-  ga.perm = perm;
-  ga.nvalid = nvalid;
+  ga.mask = mask;
   ga.C = C;
   ga.n = n;
   ga.W = W;
-  ga.npos = n;
   ga.a[0] = x;
   ga.out[0] = q;
   ga.out[1] = k;
@@ -435,8 +461,7 @@ static hipError_t projected_backward_t(const void* plan, int32_t n, int32_t W, i
   wa.a1 = dy;
   wa.b1 = o;
   wa.hdr = hdr;
-  wa.perm = perm;
-  wa.nvalid = nvalid;
+  wa.mask = mask;
   wa.part = part;
   wa.C = C;
   wa.n = n;
