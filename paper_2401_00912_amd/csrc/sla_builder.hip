@@ -251,6 +251,161 @@ __device__ int32_t build_tables(const int32_t* s_off, int32_t* s_aux, int32_t W,
   return nC;
 }
 
+// -------------------------------------------- tables straight from the totals
+// The same tables as build_tables, from window lengths (the totals) rather than
+// offsets, with one scan fewer: a segment of windows is summarised by the rows
+// it holds, the start of its last non-empty window and the end of its last
+// window of more than P rows (both relative to the segment's first row, -1 for
+// none).  Joining two segments adds rows and shifts the second one's positions
+// by the first one's rows, so one scan over the threads' segments gives each
+// thread its first offset and the two positions the chunk rule needs.
+struct WinSeg {
+  int32_t rows, last_start, wide_end;
+};
+
+__device__ __forceinline__ WinSeg seg_join(WinSeg a, WinSeg b) {
+  WinSeg r;
+  r.rows = a.rows + b.rows;
+  r.last_start = b.last_start >= 0 ? a.rows + b.last_start : a.last_start;
+  r.wide_end = b.wide_end >= 0 ? a.rows + b.wide_end : a.wide_end;
+  return r;
+}
+
+// v joined after the value CTRL moves in (the identity where nothing moves in)
+template <int CTRL, int ROWS>
+__device__ __forceinline__ WinSeg seg_step(WinSeg v) {
+  WinSeg m;
+  m.rows = __builtin_amdgcn_update_dpp(0, v.rows, CTRL, ROWS, 0xf, false);
+  m.last_start = __builtin_amdgcn_update_dpp(-1, v.last_start, CTRL, ROWS, 0xf, false);
+  m.wide_end = __builtin_amdgcn_update_dpp(-1, v.wide_end, CTRL, ROWS, 0xf, false);
+  return seg_join(m, v);
+}
+
+// Exclusive join over the threads of the block, in thread order (one barrier;
+// s[0..15] must stay untouched until the caller's next barrier).
+__device__ __forceinline__ WinSeg seg_exscan(WinSeg v, WinSeg* s) {
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  WinSeg inc = v;
+  inc = seg_step<0x111, 0xf>(inc);  // row_shr:1
+  inc = seg_step<0x112, 0xf>(inc);  // row_shr:2
+  inc = seg_step<0x114, 0xf>(inc);  // row_shr:4
+  inc = seg_step<0x118, 0xf>(inc);  // row_shr:8
+  inc = seg_step<0x142, 0xa>(inc);  // row_bcast:15
+  inc = seg_step<0x143, 0xc>(inc);  // row_bcast:31
+  if (lane == 63) s[wv] = inc;
+  WinSeg ex;   // the inclusive value of the lane before (wave_shr:1)
+  ex.rows = __builtin_amdgcn_update_dpp(0, inc.rows, 0x138, 0xf, 0xf, false);
+  ex.last_start = __builtin_amdgcn_update_dpp(-1, inc.last_start, 0x138, 0xf, 0xf, false);
+  ex.wide_end = __builtin_amdgcn_update_dpp(-1, inc.wide_end, 0x138, 0xf, 0xf, false);
+  lds_sync();
+  WinSeg before = {0, -1, -1};
+  for (int u = 0; u < wv; ++u) before = seg_join(before, s[u]);
+  return seg_join(before, ex);
+}
+
+// Reads (and clears) the window totals totals[0..W], writes the offsets (to the
+// plan, to offsets_out when given, and to s_off[0..W]), the chunk and
+// long-window tables; returns the chunk count, sets *n_long, *n_long4 and
+// *invalid (rows with an out-of-range id).  LDS: s_off[W + 1], s_aux[W].  At
+// most 32 windows a thread.
+__device__ int32_t tables_from_totals(int32_t* __restrict__ totals, int32_t W, int32_t L,
+                                      int32_t* __restrict__ plan_offsets,
+                                      int32_t* __restrict__ offsets_out, int32_t* s_off,
+                                      int32_t* s_aux, Chunk* __restrict__ chunks,
+                                      LongWin* __restrict__ longs, WinSeg* s_seg, uint64_t* s_scan2,
+                                      int32_t* n_long, int32_t* n_long4, int32_t* invalid) {
+  const int tid = threadIdx.x, T = blockDim.x;
+  const int32_t page = L >> 1;
+  // x / page = (x m) >> 37 with m = ceil(2^37 / page) (as in build_tables)
+  const uint64_t pm = ((1ull << 37) + (uint64_t)page - 1) / (uint64_t)page;
+  auto page_of = [&](int32_t x) -> uint32_t { return (uint32_t)(((uint64_t)(uint32_t)x * pm) >> 37); };
+  const int P = (W + T - 1) / T;
+  const int w0 = min(tid * P, W), w1 = min(w0 + P, W);
+  // this thread's windows as a segment; their lengths stay in LDS
+  WinSeg own = {0, -1, -1};
+  for (int w = w0; w < w1; ++w) {
+    const int32_t len = totals[w];
+    totals[w] = 0;
+    s_aux[w] = len;
+    if (len > 0) own.last_start = own.rows;
+    if (len > page) own.wide_end = own.rows + len;
+    own.rows += len;
+  }
+  if (tid == 0) {
+    *invalid = totals[W];
+    totals[W] = 0;
+  }
+  const WinSeg ex = seg_exscan(own, s_seg);
+  // 0: no event, 1: opens a chunk, 2: two-way long window, 3: four-way long
+  // window; 2 bits a window in `codes`
+  uint64_t codes = 0;
+  uint64_t cnt = 0;   // chunks, two-way, four-way: 21 bits each (W <= 16384)
+  {
+    int32_t a = ex.rows, ls = ex.last_start, ll = ex.wide_end;
+    for (int w = w0; w < w1; ++w) {
+      const int32_t len = s_aux[w];
+      int k = 0;
+      if (len > 0) {
+        if (len > L) k = len > 2 * L ? 3 : 2;
+        else if (len > page || ls < 0 || ll == a || page_of(ls) != page_of(a)) k = 1;
+        ls = a;
+        if (len > page) ll = a + len;
+      }
+      codes |= (uint64_t)k << (2 * (w - w0));
+      if (k) cnt += 1ull << (21 * (k - 1));
+      s_off[w] = a;
+      plan_offsets[w] = a;
+      if (offsets_out) offsets_out[w] = a;
+      a += len;
+    }
+    if (w1 == W && w0 < w1) {
+      s_off[W] = a;
+      plan_offsets[W] = a;
+      if (offsets_out) offsets_out[W] = a;
+    }
+  }
+  uint64_t tot = 0;
+  const uint64_t exc = block_exscan1<OpSum64, uint64_t>(cnt, 0ull, OpSum64(), s_scan2, &tot);
+  constexpr uint64_t kMask = (1ull << 21) - 1;
+  const int32_t s0 = (int32_t)(exc & kMask), t0 = (int32_t)((exc >> 21) & kMask),
+                f0 = (int32_t)(exc >> 42);
+  const int32_t nC = (int32_t)(tot & kMask), n2 = (int32_t)((tot >> 21) & kMask),
+                n4 = (int32_t)(tot >> 42);
+  lds_sync();   // every window's length has been read from s_aux
+  {
+    int32_t e = s0 + t0 + f0;
+    for (int w = w0; w < w1; ++w)
+      if ((codes >> (2 * (w - w0))) & 3u) s_aux[e++] = w;
+  }
+  lds_sync();   // the event list and s_off
+  {
+    int32_t sc = s0, s2 = t0, s4 = f0;
+    const int32_t nE = nC + n2 + n4;
+    for (int w = w0; w < w1; ++w) {
+      const int k = (int)((codes >> (2 * (w - w0))) & 3u);
+      if (k == 1) {
+        const int32_t e = sc + s2 + s4;
+        Chunk ch;
+        ch.win_begin = w;
+        ch.win_end = e + 1 < nE ? s_aux[e + 1] : W;
+        ch.row_begin = s_off[w];
+        ch.row_end = s_off[ch.win_end];
+        chunks[sc++] = ch;
+      } else if (k >= 2) {
+        LongWin lw;
+        lw.window = w;
+        lw.row_begin = s_off[w];
+        lw.row_end = s_off[w + 1];
+        lw.pad = 0;
+        longs[k == 3 ? s4++ : n4 + s2++] = lw;
+      }
+    }
+  }
+  *n_long = n2 + n4;
+  *n_long4 = n4;
+  return nC;
+}
+
 __device__ void write_header(PlanHeader* hdr, int32_t n, int32_t W, int32_t L, int32_t n_chunks,
                              int32_t n_long, int32_t n_long4, int32_t csr, int32_t invalid,
                              int32_t* invalid_out) {
@@ -507,33 +662,15 @@ __global__ __launch_bounds__(kMergeThreads) void k_merge(
   __shared__ uint64_t s_scan2[33];
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   if (blockIdx.x == 0) {
+    __shared__ WinSeg s_seg[kMergeThreads / 64];
+    __shared__ int32_t s_invalid;
     int32_t* s_off = lds;
     int32_t* s_aux = lds + (W + 1);
-    const int P = (W + 1 + kMergeThreads - 1) / kMergeThreads;
-    const int x0 = min(tid * P, W + 1), x1 = min(x0 + P, W + 1);
-    int32_t local = 0;
-    for (int x = x0; x < x1; ++x) {
-      const int32_t t = totals[x];
-      s_off[x] = t;
-      local += x < W ? t : 0;
-      totals[x] = 0;
-    }
-    int32_t total = 0;
-    int32_t ex = block_exscan(local, 0, OpSum(), s_scan, &total);
-    const int32_t invalid = s_off[W];   // read before any thread overwrites it
-    lds_sync();
-    for (int x = x0; x < x1; ++x) {
-      const int32_t t = s_off[x];
-      s_off[x] = ex;
-      plan_offsets[x] = ex;
-      if (offsets_out) offsets_out[x] = ex;
-      ex += t;
-    }
-    lds_sync();
     int32_t n_long = 0, n_long4 = 0;
-    const int32_t n_chunks =
-        build_tables(s_off, s_aux, W, L, chunks, longs, s_scan, s_scan2, &n_long, &n_long4);
-    if (tid == 0) write_header(hdr, n, W, L, n_chunks, n_long, n_long4, 0, invalid, invalid_out);
+    const int32_t n_chunks = tables_from_totals(totals, W, L, plan_offsets, offsets_out, s_off, s_aux, chunks,
+                                                longs, s_seg, s_scan2, &n_long, &n_long4, &s_invalid);
+    lds_sync();
+    if (tid == 0) write_header(hdr, n, W, L, n_chunks, n_long, n_long4, 0, s_invalid, invalid_out);
     return;
   }
   const int32_t w0 = ((int32_t)blockIdx.x - 1) * ww;
