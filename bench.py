@@ -93,7 +93,7 @@ def kernel_source_hash():
 
 
 def short_kernel(name):
-    for k in ("k_sla_bwd", "k_sla_fwd", "k_count", "k_plan", "k_scatter", "k_cwi_tiled", "k_cwi_fwd",
+    for k in ("k_sla_bwd", "k_sla_fwd", "k_sort", "k_merge", "k_plan", "k_cwi_tiled", "k_cwi_fwd",
               "k_cwi_dw_reduce", "k_cwi_dw", "k_cwi_map", "k_cwi_clear"):
         if k in name:
             return k
@@ -132,7 +132,7 @@ def pmc_summary(fetch_csv, write_csv):
         f"write_factor: {fw:.4f}   (WRITE_SIZE bytes by the copy / bytes it writes)",
         "kernel      dispatches  FETCH_raw_B   WRITE_raw_B   fetch_scaled_B  write_scaled_B  traffic_scaled_B",
     ]
-    for k in ("k_count", "k_plan", "k_scatter", "k_sla_fwd", "k_sla_bwd", "k_cwi_clear", "k_cwi_map",
+    for k in ("k_sort", "k_merge", "k_plan", "k_sla_fwd", "k_sla_bwd", "k_cwi_clear", "k_cwi_map",
               "k_cwi_tiled", "k_cwi_fwd", "k_cwi_dw", "k_cwi_dw_reduce", "copy"):
         if k in f and k in w:
             fr, wr = f[k][0], w[k][0]
@@ -168,7 +168,7 @@ def sq_summary(paths):
                     seen.add(r["Dispatch_Id"])
                     dur.setdefault(k, []).append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-9)
     lines = ["kernel      counter                          per_launch        dispatches"]
-    for k in ("k_count", "k_scatter", "k_sla_fwd", "k_sla_bwd"):
+    for k in ("k_sort", "k_merge", "k_sla_fwd", "k_sla_bwd"):
         if k not in acc:
             continue
         c = {name: float(np.mean(v)) for name, v in acc[k].items()}
