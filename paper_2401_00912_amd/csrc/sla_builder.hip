@@ -505,10 +505,13 @@ __device__ __forceinline__ uint64_t lanemask_lt(int lane) {
 // and adds its window counts (x = 0..W; x = W counts the ids outside [0, W)) to
 // the window totals, integer atomics, so the sums do not depend on their order.
 // Both go out as soon as the histogram is complete, under the radix passes.
-// LDS: hist[ld] | buf[2][E] | wcnt[2][256][16] (one count table when R = 8).
+// LDS: hist[ld] | buf[2][E] | wcnt[2][256][17] (one count table when R = 8).
 constexpr int kSortThreads = 1024;
 constexpr int kSortWaves = kSortThreads / 64;
 constexpr int kDigits = 256;
+// (digit, wave) counters kCountLd ints apart per digit: with 16 the 64 lanes of a
+// wave, each on its own digit, would all fall in two LDS banks
+constexpr int kCountLd = kSortWaves + 1;
 constexpr int kPosBits = 13;   // position of a row in its block (E <= 8192)
 
 // Exclusive sum over the threads of the block in thread order, one barrier; the
@@ -532,7 +535,7 @@ __global__ __launch_bounds__(kSortThreads) void k_sort(const int32_t* __restrict
                                                       int32_t* __restrict__ totals) {
   constexpr int E = kSortThreads * R;
   constexpr bool kTwoTables = R <= 4;   // LDS budget at W = 16384
-  constexpr int kTable = kDigits * kSortWaves;
+  constexpr int kTable = kDigits * kCountLd;
   static_assert(E <= (1 << kPosBits), "row positions fit their field");
   extern __shared__ int32_t lds[];
   __shared__ uint64_t s_scan[kSortWaves];
@@ -576,7 +579,7 @@ __global__ __launch_bounds__(kSortThreads) void k_sort(const int32_t* __restrict
     for (int r = 0; r < R; ++r) {
       const int32_t d = (int32_t)((el[r] >> (kPosBits + shift)) & 0xffu);
       const uint64_t m = match_key(d, true, dbits);
-      int32_t* slot = &tab[d * kSortWaves + wv];
+      int32_t* slot = &tab[d * kCountLd + wv];
       const int32_t before = *slot;   // a wave's LDS accesses complete in order
       if ((m & lt) == 0) *slot = before + __popcll(m);
       rk[r] = before + __popcll(m & lt);
@@ -586,9 +589,12 @@ __global__ __launch_bounds__(kSortThreads) void k_sort(const int32_t* __restrict
     // thread; the first pass also scans the histogram (high half of the sum)
     int32_t v[4], hsum = 0;
     uint64_t sum = 0;
+    // entries 4 tid .. 4 tid + 3 of the (digit, wave) order: digit tid / 4, waves
+    // 4 (tid % 4) .. + 3
+    int32_t* ent = tab + (tid >> 2) * kCountLd + 4 * (tid & 3);
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
-      v[k] = tab[4 * tid + k];
+      v[k] = ent[k];
       sum += (uint32_t)v[k];
     }
     if (pass == 0) {
@@ -599,7 +605,7 @@ __global__ __launch_bounds__(kSortThreads) void k_sort(const int32_t* __restrict
     int32_t e = (int32_t)(uint32_t)ex;
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
-      tab[4 * tid + k] = e;
+      ent[k] = e;
       e += v[k];
     }
     if (pass == 0) {
@@ -619,7 +625,7 @@ __global__ __launch_bounds__(kSortThreads) void k_sort(const int32_t* __restrict
 #pragma unroll
     for (int r = 0; r < R; ++r) {
       const int32_t d = (int32_t)((el[r] >> (kPosBits + shift)) & 0xffu);
-      dst[tab[d * kSortWaves + wv] + rk[r]] = el[r];
+      dst[tab[d * kCountLd + wv] + rk[r]] = el[r];
     }
     lds_sync();
 #pragma unroll
@@ -789,7 +795,7 @@ hipError_t launch_build(const int32_t* ids, int32_t n, int32_t W, int32_t L, int
   if (e != hipSuccess) return e;
   const int R = lay.block_elems / kSortThreads;
   const size_t sort_lds =
-      ((size_t)lay.counts_ld + 2 * (size_t)lay.block_elems + (R <= 4 ? 2 : 1) * kDigits * kSortWaves) * 4;
+      ((size_t)lay.counts_ld + 2 * (size_t)lay.block_elems + (R <= 4 ? 2 : 1) * kDigits * kCountLd) * 4;
   const dim3 sg(lay.n_blocks), st(kSortThreads);
   switch (R) {
     case 1:
