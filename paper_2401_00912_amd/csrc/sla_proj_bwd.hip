@@ -153,51 +153,58 @@ __global__ __launch_bounds__(kRowGemmThreads) void k_rows_gemm(RowGemmArgs ga) {
 }
 
 // ------------------------------------------------------------ weight gradients
-// Unit (problem, 32-row slab m0 of the gradient, column chunk n0 of 64 columns,
-// row group): partial[group][m0 + e][n0 + c] = sum over the group's rows in
+// For one row group, four kinds of workgroup: A = dq, dk, dv (with B = x: rows
+// 0..C-1, C..2C-1, 2C..3C-1 of dW_qkv and of db_qkv) and A = dy (with B = o:
+// dW_o, db_o).  A unit is a 32-row slab m0 of A's gradient rows and a 64-column
+// chunk n0 of B's: partial[group][m0 + e][n0 + c] = sum over the group's rows in
 // windows of A(row, m0 + e) B(row, n0 + c), and, for n0 = 0, the bias partial
-// sum_rows A(row, m0 + e).  Problem 0: A = [dq | dk | dv] (3C columns), B = x;
-// problem 1: A = dy, B = o.  The rows 0..n-1 are split into `groups` contiguous
-// ranges (rows in no window are masked out); a wave takes one unit and walks its
-// rows 32 at a time: each 32-column block of a row is fetched as a row fragment
-// and turned into the operand of a contraction over rows (as the attention's
-// state sums), then the slab's 2 x 2 tiles per column block accumulate.
+// sum_rows A(row, m0 + e).  The rows 0..n-1 are split into `groups` contiguous
+// ranges.
+//
+// A workgroup of 8 waves takes 8 units of one kind (C / 32 x C / 64 of them per
+// kind) and walks its rows 32 at a time: the rows of A and B are staged in LDS
+// once (rows in no window stored as zeros), the next job's rows loaded into
+// registers while this one is summed; each wave reads its 32-column blocks as
+// row fragments, turns them into operands of a contraction over rows (0/1
+// selection products, as the attention's state sums) and accumulates its 2 x 4
+// result tiles.
 struct WgradArgs {
-  const void* a0[3];     // dq, dk, dv [n, C]
-  const void* b0;        // x [n, C]
-  const void* a1;        // dy [n, C]
-  const void* b1;        // o [n, C]
+  const void* mats[6];   // dq, dk, dv, x, dy, o [n, C]
   const PlanHeader* hdr;
   const uint8_t* mask;   // rows in windows
   float* part;           // [groups][total]: dW_qkv [3C][C], dW_o [C][C], db_qkv [3C], db_o [C]
-  int32_t C, n, W, groups, units0, units1, chunks;
+  int32_t C, n, W, groups, wgs_per_kind;
 };
 
-constexpr int kWgradChunkBlocks = 2;   // 32-column blocks per column chunk
+constexpr int kWgradThreads = 512;
+constexpr int kWgradChunk = 64;    // gradient columns per unit
 
-template <typename T>
-__global__ __launch_bounds__(256) void k_wgrad(WgradArgs wa) {
+// SP: 16-byte pieces a thread stages per job, 32 x 2C / 8 / 512 (C = 64, 128, 256)
+template <typename T, int SP>
+__global__ __launch_bounds__(kWgradThreads) void k_wgrad(WgradArgs wa) {
   using F = Frag<T, 8>;
-  constexpr int NCB = kWgradChunkBlocks;
+  constexpr int NCB = kWgradChunk / 32;
+  constexpr int NWV = kWgradThreads / 64;
   const floatx4 zero = {0.f, 0.f, 0.f, 0.f};
   if (wa.hdr->magic != kPlanMagic || wa.hdr->n != wa.n || wa.hdr->num_windows != wa.W) return;
-  const int lane = lane_id();
-  const int i = lane & 15, g = lane >> 4;
+  extern __shared__ __attribute__((aligned(16))) unsigned char lds_raw[];
   const int C = wa.C;
-  const int32_t unit = (int32_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  const int32_t per_group = wa.units0 + wa.units1;
-  const int32_t grp = unit / per_group;
-  if (grp >= wa.groups) return;
-  int32_t u = unit - grp * per_group;
-  const int prob = u < wa.units0 ? 0 : 1;
-  if (prob) u -= wa.units0;
-  const int slab = u / wa.chunks, chunk = u - slab * wa.chunks;
-  const int m0 = 32 * slab;
-  const int n0 = 32 * NCB * chunk;
-  const int ncb = min(NCB, (C - n0) / 32);
-  const T* A = prob ? static_cast<const T*>(wa.a1) : static_cast<const T*>(wa.a0[m0 / C]);
-  const int acol = m0 % C;
-  const T* B = static_cast<const T*>(prob ? wa.b1 : wa.b0);
+  const int LDR = 2 * C + 8;                 // staged row: A then B, padded
+  T* stage = reinterpret_cast<T*>(lds_raw);   // [2][32][LDR]
+  const int tid = threadIdx.x, lane = lane_id(), wv = tid >> 6;
+  const int i = lane & 15, g = lane >> 4;
+  const int32_t per_group = 4 * wa.wgs_per_kind;
+  const int32_t grp = (int32_t)blockIdx.x / per_group;
+  const int kind = ((int32_t)blockIdx.x % per_group) / wa.wgs_per_kind;
+  const int part_of_kind = ((int32_t)blockIdx.x % per_group) % wa.wgs_per_kind;
+  const int chunks = C / kWgradChunk;
+  const int units = (C / 32) * chunks;
+  const int unit = part_of_kind * NWV + wv;
+  const bool active = unit < units;
+  const int slab = active ? unit / chunks : 0, chunk = active ? unit % chunks : 0;
+  const int m0 = 32 * slab, n0 = kWgradChunk * chunk;
+  const T* A = static_cast<const T*>(wa.mats[kind == 3 ? 4 : kind]);
+  const T* B = static_cast<const T*>(wa.mats[kind == 3 ? 5 : 3]);
   const int32_t p0 = (int32_t)((int64_t)wa.n * grp / wa.groups);
   const int32_t p1 = (int32_t)((int64_t)wa.n * (grp + 1) / wa.groups);
   const Sel<T, 32> sel(i, g);
@@ -213,74 +220,97 @@ __global__ __launch_bounds__(256) void k_wgrad(WgradArgs wa) {
   auto rows_of = [&](const Raw<T, 8>(&x)[2], int t) -> Raw<T, 8> {
     return pack_rows<T>(F::mma(x[0], sel.m[t], zero), F::mma(x[1], sel.m[t], zero));
   };
-  // one job = 32 sorted positions; the next job's rows are fetched while this one
-  // is summed (fragments in memory order until used)
-  struct Job {
-    Raw<T, 8> a[2], b[NCB][2];
-    bool ok[2];
-  };
-  auto fetch = [&](Job& jb, int32_t base) {
+  // staging: 32 rows x 2C / 8 pieces of 16 bytes, SP a thread
+  const int per_mat = C / 8, pieces_per_row = 2 * per_mat;
+  const int npieces = 32 * pieces_per_row;
+  // the data and the row's mask byte are loaded together; rows in no window
+  // are zeroed when stored
+  uint4 held[SP];
+  int keep[SP];
+  auto load_job = [&](int32_t base) {
 #pragma unroll
-    for (int s = 0; s < 2; ++s) {
-      const int32_t p = base + 16 * s + i;
-      const int32_t r = p < p1 ? p : p0;
-      jb.ok[s] = p < p1 && wa.mask[r] != 0;
-      jb.a[s] = RowIO<T, 32>::fetch(A + (size_t)r * C + acol, g);
-#pragma unroll
-      for (int cb = 0; cb < NCB; ++cb)
-        if (cb < ncb) jb.b[cb][s] = RowIO<T, 32>::fetch(B + (size_t)r * C + n0 + 32 * cb, g);
+    for (int k = 0; k < SP; ++k) {
+      const int idx = tid + k * kWgradThreads;
+      held[k] = make_uint4(0, 0, 0, 0);
+      keep[k] = 0;
+      if (idx < npieces) {
+        const int r = idx / pieces_per_row, pc = idx - r * pieces_per_row;
+        const int32_t row = base + r;
+        const T* src = pc < per_mat ? A + 8 * pc : B + 8 * (pc - per_mat);
+        if (row < p1) {
+          keep[k] = wa.mask[row];
+          held[k] = *reinterpret_cast<const uint4*>(src + (size_t)row * C);
+        }
+      }
     }
   };
-  Job cur;
-  if (p0 < p1) fetch(cur, p0);
+  auto store_job = [&](T* buf) {
+#pragma unroll
+    for (int k = 0; k < SP; ++k) {
+      const int idx = tid + k * kWgradThreads;
+      if (idx < npieces) {
+        const int r = idx / pieces_per_row, pc = idx - r * pieces_per_row;
+        *reinterpret_cast<uint4*>(buf + r * LDR + 8 * pc) = keep[k] != 0 ? held[k] : make_uint4(0, 0, 0, 0);
+      }
+    }
+  };
+  int buf = 0;
+  if (p0 < p1) {
+    load_job(p0);
+    store_job(stage);
+  }
+  __syncthreads();
   for (int32_t base = p0; base < p1; base += 32) {
-    Job nxt;
     const bool more = base + 32 < p1;
-    if (more) fetch(nxt, base + 32);
-    Raw<T, 8> fa[2];
-#pragma unroll
-    for (int s = 0; s < 2; ++s) {
-      RowIO<T, 32>::arrange(cur.a[s]);
-      fa[s] = cur.ok[s] ? cur.a[s] : F::zero();
-    }
-    Raw<T, 8> pa[2];
-#pragma unroll
-    for (int et = 0; et < 2; ++et) {
-      pa[et] = rows_of(fa, et);
-      bacc[et] = F::mma(pa[et], ones, bacc[et]);
-    }
-#pragma unroll
-    for (int cb = 0; cb < NCB; ++cb) {
-      if (cb >= ncb) break;
-      Raw<T, 8> fb[2];
+    if (more) load_job(base + 32);
+    const T* cur = stage + buf * 32 * LDR;
+    if (active) {
+      Raw<T, 8> fa[2];
 #pragma unroll
       for (int s = 0; s < 2; ++s) {
-        RowIO<T, 32>::arrange(cur.b[cb][s]);
-        fb[s] = cur.ok[s] ? cur.b[cb][s] : F::zero();
+        fa[s] = *reinterpret_cast<const Raw<T, 8>*>(cur + (16 * s + i) * LDR + m0 + 8 * g);
+        RowIO<T, 32>::arrange(fa[s]);
+      }
+      Raw<T, 8> pa[2];
+#pragma unroll
+      for (int et = 0; et < 2; ++et) {
+        pa[et] = rows_of(fa, et);
+        bacc[et] = F::mma(pa[et], ones, bacc[et]);
       }
 #pragma unroll
-      for (int ct = 0; ct < 2; ++ct) {
-        const Raw<T, 8> pb = rows_of(fb, ct);
+      for (int cb = 0; cb < NCB; ++cb) {
+        Raw<T, 8> fb[2];
 #pragma unroll
-        for (int et = 0; et < 2; ++et) acc[et][2 * cb + ct] = F::mma(pa[et], pb, acc[et][2 * cb + ct]);
+        for (int s = 0; s < 2; ++s) {
+          fb[s] = *reinterpret_cast<const Raw<T, 8>*>(cur + (16 * s + i) * LDR + C + n0 + 32 * cb + 8 * g);
+          RowIO<T, 32>::arrange(fb[s]);
+        }
+#pragma unroll
+        for (int ct = 0; ct < 2; ++ct) {
+          const Raw<T, 8> pb = rows_of(fb, ct);
+#pragma unroll
+          for (int et = 0; et < 2; ++et) acc[et][2 * cb + ct] = F::mma(pa[et], pb, acc[et][2 * cb + ct]);
+        }
       }
     }
-    if (more) cur = nxt;
+    if (more) store_job(stage + (buf ^ 1) * 32 * LDR);
+    buf ^= 1;
+    __syncthreads();
   }
+  if (!active) return;
   // tile (et, ct): lane (c, g) component j is gradient entry
-  // [m0 + 16 et + 4 g + j][n0 + 16 ct + c]; the bias tile holds the row sums
+  // [m0 + 16 et + 4 g + j][n0 + 16 ct + c] of this kind's block; the bias tile
+  // holds the row sums
   const size_t total = (size_t)4 * C * C + 4 * (size_t)C;
   float* part = wa.part + (size_t)grp * total;
-  float* dw = prob ? part + (size_t)3 * C * C : part;
-  float* db = prob ? part + (size_t)4 * C * C + 3 * C : part + (size_t)4 * C * C;
+  float* dw = kind == 3 ? part + (size_t)3 * C * C : part + (size_t)kind * C * C;
+  float* db = kind == 3 ? part + (size_t)4 * C * C + 3 * C : part + (size_t)4 * C * C + (size_t)kind * C;
 #pragma unroll
   for (int et = 0; et < 2; ++et) {
 #pragma unroll
-    for (int ct = 0; ct < 2 * NCB; ++ct) {
-      if (ct >= 2 * ncb) break;
+    for (int ct = 0; ct < 2 * NCB; ++ct)
 #pragma unroll
       for (int j = 0; j < 4; ++j) dw[(size_t)(m0 + 16 * et + 4 * g + j) * C + n0 + 16 * ct + i] = acc[et][ct][j];
-    }
     if (chunk == 0 && i == 0) {
 #pragma unroll
       for (int j = 0; j < 4; ++j) db[m0 + 16 * et + 4 * g + j] = bacc[et][j];
@@ -319,10 +349,10 @@ __global__ __launch_bounds__(256) void k_wgrad_reduce(const float* __restrict__ 
 // ------------------------------------------------------------ host side
 // Workspace: W_qkv^T [C][3C], W_o^T [C][C] (dtype); q, k, v, do, dq, dk, dv
 // [n][C] (dtype); the weight-gradient partials [groups][4 C^2 + 4 C] (fp32), with
-// one group per 512 rows, the partials held within 32 MiB.
+// one group per 256 rows, the partials held within 32 MiB.
 static int32_t wgrad_groups(int64_t n, int32_t C) {
   const int64_t per = ((int64_t)4 * C * C + 4 * (int64_t)C) * 4;
-  int64_t g = (n + 511) / 512;
+  int64_t g = (n + 255) / 256;
   const int64_t cap = ((int64_t)32 << 20) / per;
   if (g > cap) g = cap;
   if (g < 1) g = 1;
@@ -454,12 +484,12 @@ static hipError_t projected_backward_t(const void* plan, int32_t n, int32_t W, i
   if ((e = rows_gemm<T>(ga, stream)) != hipSuccess) return e;
   // weight and bias gradients: partials per row group, then their ordered sum
   WgradArgs wa{};
-  wa.a0[0] = dq;
-  wa.a0[1] = dk;
-  wa.a0[2] = dv;
-  wa.b0 = x;
-  wa.a1 = dy;
-  wa.b1 = o;
+  wa.mats[0] = dq;
+  wa.mats[1] = dk;
+  wa.mats[2] = dv;
+  wa.mats[3] = x;
+  wa.mats[4] = dy;
+  wa.mats[5] = o;
   wa.hdr = hdr;
   wa.mask = mask;
   wa.part = part;
@@ -467,11 +497,18 @@ static hipError_t projected_backward_t(const void* plan, int32_t n, int32_t W, i
   wa.n = n;
   wa.W = W;
   wa.groups = L.groups;
-  wa.chunks = (C + 32 * kWgradChunkBlocks - 1) / (32 * kWgradChunkBlocks);
-  wa.units0 = (3 * C / 32) * wa.chunks;
-  wa.units1 = (C / 32) * wa.chunks;
-  const int64_t waves = (int64_t)L.groups * (wa.units0 + wa.units1);
-  hipLaunchKernelGGL((k_wgrad<T>), dim3((unsigned)((waves + 3) / 4)), dim3(256), 0, stream, wa);
+  const int units = (C / 32) * (C / kWgradChunk);
+  wa.wgs_per_kind = (units + kWgradThreads / 64 - 1) / (kWgradThreads / 64);
+  const size_t wlds = (size_t)2 * 32 * (2 * C + 8) * 2;
+  const void* wk = C == 256 ? reinterpret_cast<const void*>(&k_wgrad<T, 4>)
+                  : C == 128 ? reinterpret_cast<const void*>(&k_wgrad<T, 2>)
+                             : reinterpret_cast<const void*>(&k_wgrad<T, 1>);
+  if ((e = hipFuncSetAttribute(wk, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024 - 1024)) != hipSuccess)
+    return e;
+  const dim3 wg((unsigned)((int64_t)L.groups * 4 * wa.wgs_per_kind));
+  if (C == 256) hipLaunchKernelGGL((k_wgrad<T, 4>), wg, dim3(kWgradThreads), wlds, stream, wa);
+  else if (C == 128) hipLaunchKernelGGL((k_wgrad<T, 2>), wg, dim3(kWgradThreads), wlds, stream, wa);
+  else hipLaunchKernelGGL((k_wgrad<T, 1>), wg, dim3(kWgradThreads), wlds, stream, wa);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   const int64_t total = (int64_t)4 * C * C + 4 * (int64_t)C;
   hipLaunchKernelGGL(k_wgrad_reduce, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, stream,
