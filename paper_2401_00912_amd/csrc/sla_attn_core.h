@@ -520,18 +520,19 @@ constexpr int kWpe = sizeof(T) == 4 ? (W16 > 2 ? W16 / 2 : 1) : W16;
 // ----------------------------------------------------------- backward math
 // bf16 keeps 8 significant bits, so the backward carries the operands of its
 // cancelling differences as a sum of two bf16 values (high part and rounding
-// residual, 16 bits together): S and S^T in dq = (dout S^T - (dout . o) z) / den
-// phi'(q) (o = phi(q) S / den), -dout.o in the dz accumulation, and dS^T in dk =
-// (v dS^T + dz) phi'(k).  fp16 (11 bits) and fp32 need no split.
+// residual, 16 bits together): S^T in dq = (dout S^T - (dout . o) z) / den phi'(q)
+// (o = phi(q) S / den, so dout . o = phi(q) . (dout S^T) / den), -dout.o in the dz
+// accumulation, and dS^T in dk = (v dS^T + dz) phi'(k).  fp16 (11 bits) and fp32
+// need no split.
 template <typename T>
 constexpr bool kSplitGrad = std::is_same<T, bf16_t>::value;
 
-// Operands of the backward's head-dim contractions for one window.  The same
-// registers first hold the state operands (for the Q,dout rows) and are then
-// overwritten with the state-gradient operands (for the K,V gradient rows).
+// Operands of the backward's head-dim contractions for one window.  B first holds
+// the state operand (for the Q,dout rows) and is then overwritten with a
+// state-gradient operand (for the K,V gradient rows).
 template <typename T, int D>
 struct BwdOp {
-  Raw<T, Geo<D>::KS> A[Geo<D>::NT];  // sig S   (o = phi(q) S, tile ct)  | rho dS^T (dfk = v dS^T, tile et)
+  Raw<T, Geo<D>::KS> A[Geo<D>::NT];  // unused                           | rho dS^T (dfk = v dS^T, tile et)
   Raw<T, Geo<D>::KS> B[Geo<D>::NT];  // sig S^T (dfq = dout S^T, tile et) | rho dS  (dv = phi(k) dS, tile ct)
   Raw<T, Geo<D>::KS> Az;             // sig z in rows 0, 4, 8, 12 (normaliser) | unused
   float z[Geo<D>::KS];               // sig z (as rounded in Az + Azl)    | dz
@@ -540,7 +541,7 @@ struct BwdOp {
                                      // scaled by beta (<= min z, so beta phi(q) / den <= 1)
   float inv_beta;                    // 1 / beta
   float seps;                        // sig eps
-  Raw<T, Geo<D>::KS> Al[kSplitGrad<T> ? Geo<D>::NT : 1];  // residual of A (bf16)
+  Raw<T, Geo<D>::KS> Al[kSplitGrad<T> ? Geo<D>::NT : 1];  // unused | residual of A (bf16)
   Raw<T, Geo<D>::KS> Bl[kSplitGrad<T> ? Geo<D>::NT : 1];  // residual of B (bf16) | unused
   Raw<T, Geo<D>::KS> Azl;            // residual of Az (bf16)              | unused
 };
@@ -596,25 +597,11 @@ __device__ __forceinline__ void make_state_op(const State<D>& st, BwdOp<T, D>& o
                                               int i, int g, float eps) {
   constexpr int KS = Geo<D>::KS, NT = Geo<D>::NT;
   const float sig = Ty<T>::kNarrow ? pow2_scale_to_one(st.absmax()) : 1.f;
-#pragma unroll
-  for (int ct = 0; ct < NT; ++ct) {
-    floatx4 col[NT];
-#pragma unroll
-    for (int et = 0; et < NT; ++et) col[et] = st.M[et][ct];
-    op.A[ct] = tiles_operand<T, D>(col, sig);
-    if constexpr (kSplitGrad<T>) {
-      float x[KS], h[KS];
-      Frag<T, KS>::to_f32(op.A[ct], h);
-#pragma unroll
-      for (int r = 0; r < KS; ++r) x[r] = col[r >> 2][r & 3] * sig - h[r];
-      op.Al[ct] = Frag<T, KS>::from_f32(x);
-    }
-  }
   transposed_operand<T, D, kSplitGrad<T>>(st, sig, tile, i, g, op.B, op.Bl);
   // op.z holds sig z rounded exactly as in the normaliser operands: dq subtracts
   // (dout.o) z from dout S^T, and for a row whose normaliser is mostly eps the two
   // terms cancel to eps / den; the same z on both sides keeps that residual exact.
-  // bf16 carries z as a pair (Az + Azl), as S is carried in A + Al: a z rounded
+  // bf16 carries z as a pair (Az + Azl), as S^T is carried in B + Bl: a z rounded
   // to 8 bits against an S kept to 16 leaves the cancellation a 2^-9 remainder
   float zmin = 3.0e38f;
   float zx[KS], zl[KS];
@@ -686,34 +673,32 @@ __device__ __forceinline__ void qgrad_seg(const Slice<T, Geo<D>::KS, NM>& sb, in
     if constexpr (SP) nl[s] = F::zero();
     if (!sub_overlaps(r0, s, a, b)) continue;
     Raw<T, KS> bq;
-    float dphq[KS], fq[KS], dox[KS];
+    float dphq[KS], fq[KS];
     phi_dphi<T, KS, PHI>(sb.x[QI][s], in, bq, dphq);
     F::to_f32(bq, fq);
-    F::to_f32(dr[s], dox);
     floatx4 den4 = F::mma(op.Az, bq, zero);
     if constexpr (SP) den4 = F::mma(op.Azl, bq, den4);
     const float rden = recip<T>(in ? den4[0] + op.seps : 1.f);
+    // dfq = sig dout S^T; dout.o = phi(q) S dout^T / den = phi(q).dfq / den'
+    floatx4 dfq[NT];
     float dot = 0.f;
 #pragma unroll
-    for (int ct = 0; ct < NT; ++ct) {
-      floatx4 d4 = F::mma(op.A[ct], bq, zero);
-      if constexpr (SP) d4 = F::mma(op.Al[ct], bq, d4);
+    for (int et = 0; et < NT; ++et) {
+      dfq[et] = F::mma(op.B[et], dr[s], zero);
+      if constexpr (SP) dfq[et] = F::mma(op.Bl[et], dr[s], dfq[et]);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) dot += dox[4 * ct + j] * d4[j];
+      for (int j = 0; j < 4; ++j) dot += fq[4 * et + j] * dfq[et][j];
     }
     dot = sum_groups(dot) * rden;  // lane exchange: every lane takes part
     if (!in) dot = 0.f;
     float dqx[KS];
 #pragma unroll
-    for (int et = 0; et < NT; ++et) {
-      floatx4 d4 = F::mma(op.B[et], dr[s], zero);
-      if constexpr (SP) d4 = F::mma(op.Bl[et], dr[s], d4);
+    for (int et = 0; et < NT; ++et)
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int r = 4 * et + j;
-        dqx[r] = (d4[j] - dot * op.z[r]) * rden * dphq[r];
+        dqx[r] = (dfq[et][j] - dot * op.z[r]) * rden * dphq[r];
       }
-    }
     RowIO<T, D>::put(row_at(dq, sb.o[s], rs, col), g, F::from_f32(dqx), in);
     float xs[KS], ns[KS];
     const float w = op.bsig * rden;
