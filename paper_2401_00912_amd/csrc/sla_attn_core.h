@@ -110,6 +110,23 @@ struct Geo {
 };
 
 // ----------------------------------------------------------- row fragments
+// Element `e` of a tensor: byte offsets fit in 32 bits (the host checks that
+// every tensor is smaller than 4 GiB), so the address is a uniform base plus one
+// 32-bit lane offset, which the memory instructions take as such.
+template <typename T>
+__device__ __forceinline__ T* elem_at(T* base, uint32_t e) {
+  return reinterpret_cast<T*>(reinterpret_cast<char*>(base) + (uint64_t)(e * (uint32_t)sizeof(T)));
+}
+template <typename T>
+__device__ __forceinline__ const T* elem_at(const T* base, uint32_t e) {
+  return reinterpret_cast<const T*>(reinterpret_cast<const char*>(base) + (uint64_t)(e * (uint32_t)sizeof(T)));
+}
+// Element offset of head `col` of row o of a [n, H, d] tensor (row stride rs).
+__device__ __forceinline__ uint32_t row_off(int32_t o, size_t rs, int col) {
+  return (uint32_t)o * (uint32_t)rs + (uint32_t)col;
+}
+
+
 // A row fragment (KS elements of one head of one row, in slot order E) moves
 // between registers and memory.  16-bit types with head_dim 32: each lane group
 // g reads / writes the 8 contiguous elements 8g..8g+7 as one 16-byte access,
@@ -135,19 +152,21 @@ struct RowIO {
     x = r[0];
     y = r[1];
   }
-  // `row` points at the head's first element.  The load is unconditional (the
-  // caller passes a valid row for rows past a job and masks them in the math):
+  // `off` is the element offset of the head's first element from `base` (see
+  // elem_at: the lane's part is added in 32 bits, so the access is a uniform
+  // base plus one 32-bit lane offset).  The load is unconditional (the caller
+  // passes a valid row for rows past a job and masks them in the math):
   // merging a guarded load with a default would wait for the load right here.
   // The result is in memory order until arrange() puts it into slot order (kept
   // apart so that a prefetched fragment is not waited for at load time).
-  __device__ static R fetch(const T* row, int g) {
+  __device__ static R fetch(const T* base, uint32_t off, int g) {
     if constexpr (kSwizzle) {
-      return __builtin_bit_cast(R, *reinterpret_cast<const uint4*>(row + 8 * g));
+      return __builtin_bit_cast(R, *reinterpret_cast<const uint4*>(elem_at(base, off + 8 * g)));
     } else if constexpr (Ty<T>::kNarrow) {
       R r;
 #pragma unroll
       for (int t = 0; t < NT; ++t) {
-        const u16x4 p = *reinterpret_cast<const u16x4*>(row + 16 * t + 4 * g);
+        const u16x4 p = *reinterpret_cast<const u16x4*>(elem_at(base, off + 16 * t + 4 * g));
 #pragma unroll
         for (int j = 0; j < 4; ++j) r[4 * t + j] = p[j];
       }
@@ -156,7 +175,7 @@ struct RowIO {
       R r;
 #pragma unroll
       for (int t = 0; t < NT; ++t) {
-        const float4 p = *reinterpret_cast<const float4*>(row + 16 * t + 4 * g);
+        const float4 p = *reinterpret_cast<const float4*>(elem_at(base, off + 16 * t + 4 * g));
         r[4 * t + 0] = p.x;
         r[4 * t + 1] = p.y;
         r[4 * t + 2] = p.z;
@@ -175,27 +194,27 @@ struct RowIO {
       r = __builtin_bit_cast(R, w);
     }
   }
-  __device__ static void put(T* row, int g, R r, bool ok) {
+  __device__ static void put(T* base, uint32_t off, int g, R r, bool ok) {
     if constexpr (kSwizzle) {
       uint4 w = __builtin_bit_cast(uint4, r);
       swap32(w.x, w.z);
       swap32(w.y, w.w);
       swap16(w.x, w.z);
       swap16(w.y, w.w);
-      if (ok) *reinterpret_cast<uint4*>(row + 8 * g) = w;
+      if (ok) *reinterpret_cast<uint4*>(elem_at(base, off + 8 * g)) = w;
     } else if constexpr (Ty<T>::kNarrow) {
 #pragma unroll
       for (int t = 0; t < NT; ++t) {
         u16x4 p;
 #pragma unroll
         for (int j = 0; j < 4; ++j) p[j] = r[4 * t + j];
-        if (ok) *reinterpret_cast<u16x4*>(row + 16 * t + 4 * g) = p;
+        if (ok) *reinterpret_cast<u16x4*>(elem_at(base, off + 16 * t + 4 * g)) = p;
       }
     } else {
 #pragma unroll
       for (int t = 0; t < NT; ++t)
         if (ok)
-          *reinterpret_cast<float4*>(row + 16 * t + 4 * g) =
+          *reinterpret_cast<float4*>(elem_at(base, off + 16 * t + 4 * g)) =
               make_float4(r[4 * t], r[4 * t + 1], r[4 * t + 2], r[4 * t + 3]);
     }
   }
@@ -502,7 +521,7 @@ __device__ __forceinline__ void apply_seg(const Slice<T, Geo<D>::KS, NM>& sb, in
 #pragma unroll
       for (int j = 0; j < 4; ++j) ox[4 * ct + j] = d4[j] * scale;
     }
-    RowIO<T, D>::put(row_at(o, sb.o[s], rs, col), g, F::from_f32(ox), in);
+    RowIO<T, D>::put(o, row_off(sb.o[s], rs, col), g, F::from_f32(ox), in);
   }
 }
 
@@ -699,7 +718,7 @@ __device__ __forceinline__ void qgrad_seg(const Slice<T, Geo<D>::KS, NM>& sb, in
         const int r = 4 * et + j;
         dqx[r] = (dfq[et][j] - dot * op.z[r]) * rden * dphq[r];
       }
-    RowIO<T, D>::put(row_at(dq, sb.o[s], rs, col), g, F::from_f32(dqx), in);
+    RowIO<T, D>::put(dq, row_off(sb.o[s], rs, col), g, F::from_f32(dqx), in);
     float xs[KS], ns[KS];
     const float w = op.bsig * rden;
 #pragma unroll
@@ -767,8 +786,8 @@ __device__ __forceinline__ void kgrad_seg(const Slice<T, Geo<D>::KS, NM>& sb, in
         dvx[r] = b4[j] * op.inv_scale;
       }
     }
-    RowIO<T, D>::put(row_at(dk, sb.o[s], rs, col), g, F::from_f32(dkx), in);
-    RowIO<T, D>::put(row_at(dv, sb.o[s], rs, col), g, F::from_f32(dvx), in);
+    RowIO<T, D>::put(dk, row_off(sb.o[s], rs, col), g, F::from_f32(dkx), in);
+    RowIO<T, D>::put(dv, row_off(sb.o[s], rs, col), g, F::from_f32(dvx), in);
   }
 }
 
@@ -999,7 +1018,7 @@ __device__ __forceinline__ void block_fetch(Block<T, D, NM>& bk, const BlockRows
 #pragma unroll
       for (int m = 0; m < NM; ++m) {
         if (!(which & (1u << m))) continue;
-        if (live) bk.j[jj].x[m][s] = RowIO<T, D>::fetch(row_at(mats[m], bk.j[jj].o[s], rs, col), g);
+        if (live) bk.j[jj].x[m][s] = RowIO<T, D>::fetch(mats[m], row_off(bk.j[jj].o[s], rs, col), g);
         else bk.j[jj].x[m][s] = F::zero();
       }
     }

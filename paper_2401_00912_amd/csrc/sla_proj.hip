@@ -438,7 +438,7 @@ __global__ __launch_bounds__(64 * kOutWaves<CB>) void k_out_proj(KernelArgs a, c
         // them at once would not fit in the registers)
         if constexpr (CB > 4) __builtin_amdgcn_sched_barrier(0);
       }
-      RowIO<T, 32>::put(row_at(y, ok ? row : 0, (size_t)C, 32 * hb), g, F8::from_f32(f), ok);
+      RowIO<T, 32>::put(y, row_off(ok ? row : 0, (size_t)C, 32 * hb), g, F8::from_f32(f), ok);
     }
   }
 }
