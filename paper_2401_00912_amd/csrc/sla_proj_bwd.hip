@@ -65,17 +65,20 @@ __global__ __launch_bounds__(256) void k_row_mask(const PlanHeader* __restrict__
 }
 
 // ------------------------------------------------------------ row products
-// out[row][n0 + j] = sum_k A(row, k) Wr[n0 + j][k] + bias[n0 + j], j < 16 NBT, for
-// every row.  A(row, k) = a[k / C][row][k % C] over nseg segments [n, C] (K =
-// nseg C); Wr is [N, K] row-major (a weight in the [out, in] layout); output
-// column j goes to out[j / C][row][j % C].  Rows in no window (mask 0) get zero
-// input, so their outputs are the bias (zero when there is none).
+// out[row][j] = sum_k A(row, k) Wr[j][k] + bias[j] for every row.  A(row, k) =
+// a[k / C][row][k % C] over nseg segments [n, C] (K = nseg C); Wr is [N, K]
+// row-major (a weight in the [out, in] layout); output column j goes to
+// out[j / C][row][j % C].  Rows in no window (mask 0) get zero input, so their
+// outputs are the bias (zero when there is none).
 //
-// One workgroup of 16 waves keeps the weight rows of its 16 NBT output columns in
-// LDS (padded rows of K + 8 elements) and walks 16-row tiles, one per wave: with
-// the weight rows as the first matrix-core operand and the input rows (16-byte
-// pieces of 8 channels) as the second, lane (i, g) receives columns
-// 16 t + 4 g .. + 3 of the tile's row i, stored as one 4-element piece.
+// A workgroup of 16 waves keeps the weight rows of NB output columns (blockIdx.y
+// selects them; all N when they fit) in LDS, padded rows of K + 8 elements, and
+// walks 16-row tiles, one per wave.  When K <= 32 KBH a wave reads its tile's
+// input once into registers and forms every 16 NBT-column sub-block from them;
+// otherwise it reads the input again per sub-block.  With the weight rows as the
+// first matrix-core operand and the input rows (16-byte pieces of 8 channels) as
+// the second, lane (i, g) receives columns 16 t + 4 g .. + 3 of the tile's row i,
+// stored as one 4-element piece.
 constexpr int kRowGemmThreads = 1024;
 
 struct RowGemmArgs {
@@ -86,14 +89,15 @@ struct RowGemmArgs {
   const PlanHeader* hdr;
   const uint8_t* mask;       // rows in windows
   int32_t C, K, N, n, W;
+  int32_t NB;                // columns a workgroup holds (a multiple of 16 NBT dividing N)
 };
 
-template <typename T, int NBT>
+template <typename T, int NBT, int KBH>
 __global__ __launch_bounds__(kRowGemmThreads) void k_rows_gemm(RowGemmArgs ga) {
-  constexpr int NB = 16 * NBT;
+  constexpr int SB = 16 * NBT;
   if (ga.hdr->magic != kPlanMagic || ga.hdr->n != ga.n || ga.hdr->num_windows != ga.W) return;
   extern __shared__ __attribute__((aligned(16))) unsigned char lds_raw[];
-  const int K = ga.K, LDW = K + 8, C = ga.C;
+  const int K = ga.K, LDW = K + 8, C = ga.C, NB = ga.NB;
   T* s_w = reinterpret_cast<T*>(lds_raw);
   float* s_b = reinterpret_cast<float*>(s_w + NB * LDW);
   const int32_t n0 = (int32_t)blockIdx.y * NB;
@@ -114,40 +118,72 @@ __global__ __launch_bounds__(kRowGemmThreads) void k_rows_gemm(RowGemmArgs ga) {
   const int lane = lane_id(), wv = threadIdx.x >> 6;
   const int i = lane & 15, g = lane >> 4;
   const int nseg = K / C;
-  T* outp = static_cast<T*>(ga.out[n0 / C]);
-  const int ocol = n0 % C;
+  const bool held = K <= 32 * KBH;
   constexpr int NW = kRowGemmThreads / 64;
   for (int32_t tile = (int32_t)blockIdx.x * NW + wv; tile * 16 < ga.n; tile += (int32_t)gridDim.x * NW) {
     const int32_t p = tile * 16 + i;
     const bool inside = p < ga.n;
     const int32_t row = inside ? p : 0;
     const bool valid = inside && ga.mask[row] != 0;
-    floatx4 acc[NBT];
+    // the tile's input, when it fits in registers: k block kb is channels
+    // 32 kb .. + 31 of A, in segment 32 kb / C
+    Raw<T, 8> xh[KBH];
+    if (held) {
 #pragma unroll
-    for (int t = 0; t < NBT; ++t) acc[t] = zero;
-    for (int s = 0; s < nseg; ++s) {
-      const T* src = static_cast<const T*>(ga.a[s]) + (size_t)row * C + 8 * g;
-      for (int kb = 0; kb < C / 32; ++kb) {
-        Raw<T, 8> xo = __builtin_bit_cast(Raw<T, 8>, *reinterpret_cast<const uint4*>(src + 32 * kb));
-        if (!valid) xo = F8::zero();
-        const T* wr = s_w + i * LDW + s * C + 32 * kb + 8 * g;
-#pragma unroll
-        for (int t = 0; t < NBT; ++t) {
-          const Raw<T, 8> wo = *reinterpret_cast<const Raw<T, 8>*>(wr + 16 * t * LDW);
-          acc[t] = F8::mma(wo, xo, acc[t]);
+      for (int kb = 0; kb < KBH; ++kb) {
+        xh[kb] = F8::zero();
+        if (32 * kb < K) {
+          const int s = (32 * kb) / C, c0 = (32 * kb) % C;
+          const T* src = static_cast<const T*>(ga.a[s]);
+          const Raw<T, 8> xo = __builtin_bit_cast(
+              Raw<T, 8>, *reinterpret_cast<const uint4*>(elem_at(src, (uint32_t)row * (uint32_t)C + c0 + 8 * g)));
+          if (valid) xh[kb] = xo;
         }
       }
     }
-    if (!inside) continue;
-    T* dst = outp + (size_t)row * C + ocol + 4 * g;
+    for (int sb = 0; sb < NB; sb += SB) {
+      floatx4 acc[NBT];
 #pragma unroll
-    for (int t = 0; t < NBT; ++t) {
-      const float4 bias = *reinterpret_cast<const float4*>(s_b + 16 * t + 4 * g);
-      float f[4] = {acc[t][0] + bias.x, acc[t][1] + bias.y, acc[t][2] + bias.z, acc[t][3] + bias.w};
-      u16x4 pk;
+      for (int t = 0; t < NBT; ++t) acc[t] = zero;
+      const T* wsb = s_w + (sb + i) * LDW + 8 * g;
+      if (held) {
 #pragma unroll
-      for (int j = 0; j < 4; ++j) pk[j] = f32_to_u16<T>(f[j]);
-      *reinterpret_cast<u16x4*>(dst + 16 * t) = pk;
+        for (int kb = 0; kb < KBH; ++kb) {
+          if (32 * kb >= K) break;
+#pragma unroll
+          for (int t = 0; t < NBT; ++t) {
+            const Raw<T, 8> wo = *reinterpret_cast<const Raw<T, 8>*>(wsb + 16 * t * LDW + 32 * kb);
+            acc[t] = F8::mma(wo, xh[kb], acc[t]);
+          }
+        }
+      } else {
+        for (int s = 0; s < nseg; ++s) {
+          const T* src = static_cast<const T*>(ga.a[s]);
+          for (int kb = 0; kb < C / 32; ++kb) {
+            Raw<T, 8> xo = __builtin_bit_cast(
+                Raw<T, 8>, *reinterpret_cast<const uint4*>(elem_at(src, (uint32_t)row * (uint32_t)C + 32 * kb + 8 * g)));
+            if (!valid) xo = F8::zero();
+#pragma unroll
+            for (int t = 0; t < NBT; ++t) {
+              const Raw<T, 8> wo = *reinterpret_cast<const Raw<T, 8>*>(wsb + 16 * t * LDW + s * C + 32 * kb);
+              acc[t] = F8::mma(wo, xo, acc[t]);
+            }
+          }
+        }
+      }
+      if (!inside) continue;
+      const int32_t j0 = n0 + sb;   // a sub-block lies in one output segment (C % SB == 0)
+      T* outp = static_cast<T*>(ga.out[j0 / C]);
+      T* dst = elem_at(outp, (uint32_t)row * (uint32_t)C + (uint32_t)(j0 % C) + 4 * g);
+#pragma unroll
+      for (int t = 0; t < NBT; ++t) {
+        const float4 bias = *reinterpret_cast<const float4*>(s_b + sb + 16 * t + 4 * g);
+        float f[4] = {acc[t][0] + bias.x, acc[t][1] + bias.y, acc[t][2] + bias.z, acc[t][3] + bias.w};
+        u16x4 pk;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) pk[j] = f32_to_u16<T>(f[j]);
+        *reinterpret_cast<u16x4*>(dst + 16 * t) = pk;
+      }
     }
   }
 }
@@ -390,26 +426,41 @@ hipError_t launch_backward(const void* plan, int32_t n, int32_t W, int dtype, in
                            const void* dout, void* dq, void* dk, void* dv, hipStream_t stream);
 
 template <typename T>
-static hipError_t rows_gemm(const RowGemmArgs& ga, hipStream_t stream) {
-  // 128 output columns a workgroup when its weight rows fit in 100 KB of LDS and
-  // the column blocks stay inside one output segment, else 64
-  const bool wide = ga.C % 128 == 0 && (size_t)128 * (ga.K + 8) * 2 <= 100 * 1024;
-  const int nb = wide ? 128 : 64;
-  const size_t lds = (size_t)nb * (ga.K + 8) * 2 + (size_t)nb * 4;
+static hipError_t rows_gemm(RowGemmArgs ga, hipStream_t stream) {
+  // sub-blocks of 128 output columns when they stay inside one output segment and
+  // 128 weight rows fit in LDS, else 64; a workgroup holds the most columns that
+  // fit in 150 KB of LDS and divide N
+  constexpr size_t kLdsCap = 150 * 1024;
+  const auto lds_of = [&](int nb) { return (size_t)nb * (ga.K + 8) * 2 + (size_t)nb * 4; };
+  const bool wide = ga.C % 128 == 0 && lds_of(128) <= kLdsCap;
+  const int sb = wide ? 128 : 64;
+  int nb = sb;
+  for (int m = ga.N / sb; m >= 1; --m)
+    if (ga.N % (m * sb) == 0 && lds_of(m * sb) <= kLdsCap) {
+      nb = m * sb;
+      break;
+    }
+  if (lds_of(nb) > kLdsCap) return hipErrorInvalidValue;
+  ga.NB = nb;
+  const size_t lds = lds_of(nb);
   const int cols = ga.N / nb;
+  const bool small_k = ga.K <= 32 * 4;
   // about one workgroup per CU, each walking many tiles with its staged weights
   const int64_t tiles = ((int64_t)ga.n + 16 * (kRowGemmThreads / 64) - 1) / (16 * (kRowGemmThreads / 64));
   int64_t gx = (256 + cols - 1) / cols;
   if (gx > tiles) gx = tiles;
   if (gx < 1) gx = 1;
-  const void* kern = wide ? reinterpret_cast<const void*>(&k_rows_gemm<T, 8>)
-                          : reinterpret_cast<const void*>(&k_rows_gemm<T, 4>);
+  const void* kern = wide ? (small_k ? reinterpret_cast<const void*>(&k_rows_gemm<T, 8, 4>)
+                                     : reinterpret_cast<const void*>(&k_rows_gemm<T, 8, 12>))
+                          : (small_k ? reinterpret_cast<const void*>(&k_rows_gemm<T, 4, 4>)
+                                     : reinterpret_cast<const void*>(&k_rows_gemm<T, 4, 12>));
   hipError_t e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024 - 1024);
   if (e != hipSuccess) return e;
-  if (wide)
-    hipLaunchKernelGGL((k_rows_gemm<T, 8>), dim3((unsigned)gx, cols), dim3(kRowGemmThreads), lds, stream, ga);
-  else
-    hipLaunchKernelGGL((k_rows_gemm<T, 4>), dim3((unsigned)gx, cols), dim3(kRowGemmThreads), lds, stream, ga);
+  const dim3 grid((unsigned)gx, (unsigned)cols);
+  if (wide && small_k) hipLaunchKernelGGL((k_rows_gemm<T, 8, 4>), grid, dim3(kRowGemmThreads), lds, stream, ga);
+  else if (wide) hipLaunchKernelGGL((k_rows_gemm<T, 8, 12>), grid, dim3(kRowGemmThreads), lds, stream, ga);
+  else if (small_k) hipLaunchKernelGGL((k_rows_gemm<T, 4, 4>), grid, dim3(kRowGemmThreads), lds, stream, ga);
+  else hipLaunchKernelGGL((k_rows_gemm<T, 4, 12>), grid, dim3(kRowGemmThreads), lds, stream, ga);
   return hipGetLastError();
 }
 
