@@ -10,9 +10,9 @@
 //     db_qkv = sum_rows [dq | dk | dv].
 // q, k, v are recomputed from x (they never reach HBM in the forward), o is the
 // forward's output.  The launches:
-//   k_transpose     W_qkv^T and W_o^T into the workspace, so that every product
-//                   below reads its weights as rows;
-//   k_row_mask      which rows lie in a window (from the plan's permutation);
+//   k_prep          W_qkv^T and W_o^T into the workspace, so that every product
+//                   below reads its weights as rows, and which rows lie in a
+//                   window (from the plan's permutation), in one launch;
 //   k_rows_gemm     q | k | v = x W_qkv^T + b_qkv, and do = dy W_o: a row of the
 //                   output is a row of the input times a weight matrix held in LDS;
 //   (SLA backward)  dq, dk, dv;
@@ -29,14 +29,17 @@
 
 namespace sla {
 
-// ------------------------------------------------------------ weights as rows
-// dst[j][k] = src[k][j] for src [K, N] (row-major), dst [N, K].
+// ------------------------------------------------------------ preparation
+// One launch before the products: the weights as rows (W_qkv^T and W_o^T, in
+// 32 x 32 tiles, one a workgroup) and the row mask (the other workgroups).
+//
+// Tile (bx, by) of dst[j][k] = src[k][j] for src [K, N] (row-major), dst [N, K].
 template <typename T>
-__global__ __launch_bounds__(256) void k_transpose(const T* __restrict__ src, T* __restrict__ dst,
-                                                   int32_t K, int32_t N) {
-  __shared__ unsigned short tile[32][33];
+__device__ __forceinline__ void transpose_tile(const T* __restrict__ src, T* __restrict__ dst, int32_t K,
+                                               int32_t N, int32_t bx, int32_t by,
+                                               unsigned short (&tile)[32][33]) {
   const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;   // 32 x 8
-  const int32_t k0 = blockIdx.y * 32, j0 = blockIdx.x * 32;
+  const int32_t k0 = by * 32, j0 = bx * 32;
   const unsigned short* s = reinterpret_cast<const unsigned short*>(src);
   unsigned short* d = reinterpret_cast<unsigned short*>(dst);
   for (int r = ty; r < 32; r += 8)
@@ -46,21 +49,44 @@ __global__ __launch_bounds__(256) void k_transpose(const T* __restrict__ src, T*
     if (j0 + r < N && k0 + tx < K) d[(size_t)(j0 + r) * K + k0 + tx] = tile[tx][r];
 }
 
-// ------------------------------------------------------------ rows in windows
 // mask[row] = 1 for the rows in a window, 0 for the others: the plan's sorted
 // positions [0, offsets[W]) hold the rows in windows and, for a plan built from
 // window ids, positions [offsets[W], n) the others, so every row is written once.
-__global__ __launch_bounds__(256) void k_row_mask(const PlanHeader* __restrict__ hdr,
-                                                  const int32_t* __restrict__ perm,
-                                                  const int32_t* __restrict__ nvalid_p, int32_t n,
-                                                  int32_t W, uint8_t* __restrict__ mask) {
-  if (hdr->magic != kPlanMagic || hdr->n != n || hdr->num_windows != W) return;
+struct PrepArgs {
+  const void* wqkv;          // [3C, C]
+  void* wt_qkv;              // [C, 3C]
+  const void* wo;            // [C, C]
+  void* wt_o;                // [C, C]
+  const PlanHeader* hdr;
+  const int32_t* perm;
+  const int32_t* nvalid;     // offsets[W]
+  uint8_t* mask;
+  int32_t C, n, W, mask_blocks;
+};
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_prep(PrepArgs pa) {
+  __shared__ unsigned short tile[32][33];
+  const int32_t cb = pa.C / 32, tq = cb * 3 * cb, to = cb * cb;
+  const int32_t b = (int32_t)blockIdx.x;
+  if (b < tq) {
+    transpose_tile(static_cast<const T*>(pa.wqkv), static_cast<T*>(pa.wt_qkv), 3 * pa.C, pa.C, b % cb, b / cb,
+                   tile);
+    return;
+  }
+  if (b < tq + to) {
+    transpose_tile(static_cast<const T*>(pa.wo), static_cast<T*>(pa.wt_o), pa.C, pa.C, (b - tq) % cb,
+                   (b - tq) / cb, tile);
+    return;
+  }
+  const PlanHeader* hdr = pa.hdr;
+  if (hdr->magic != kPlanMagic || hdr->n != pa.n || hdr->num_windows != pa.W) return;
   const bool csr = hdr->csr != 0;
-  const int32_t nvalid = max(0, min(*nvalid_p, n));
-  for (int32_t p = (int32_t)(blockIdx.x * blockDim.x + threadIdx.x); p < n;
-       p += (int32_t)(gridDim.x * blockDim.x)) {
-    const int32_t row = csr ? p : perm[p];
-    if ((uint32_t)row < (uint32_t)n) mask[row] = p < nvalid ? 1 : 0;
+  const int32_t n = pa.n;
+  const int32_t nvalid = max(0, min(*pa.nvalid, n));
+  for (int32_t p = (b - tq - to) * 256 + (int32_t)threadIdx.x; p < n; p += pa.mask_blocks * 256) {
+    const int32_t row = csr ? p : pa.perm[p];
+    if ((uint32_t)row < (uint32_t)n) pa.mask[row] = p < nvalid ? 1 : 0;
   }
 }
 
@@ -487,16 +513,23 @@ static hipError_t projected_backward_t(const void* plan, int32_t n, int32_t W, i
   float* part = reinterpret_cast<float*>(ws + L.part);
   uint8_t* mask = reinterpret_cast<uint8_t*>(ws + L.mask);
   hipError_t e;
-  // the weights as rows of the products below: W_qkv^T for dx, W_o^T for do
-  hipLaunchKernelGGL((k_transpose<T>), dim3((C + 31) / 32, (3 * C + 31) / 32), dim3(256), 0, stream,
-                     static_cast<const T*>(wqkv), wt_qkv, 3 * C, C);
-  hipLaunchKernelGGL((k_transpose<T>), dim3((C + 31) / 32, (C + 31) / 32), dim3(256), 0, stream,
-                     static_cast<const T*>(wo), wt_o, C, C);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
-  // which rows lie in a window
-  const int64_t mblocks = std::min<int64_t>(1024, std::max<int64_t>(1, ((int64_t)n + 255) / 256));
-  hipLaunchKernelGGL(k_row_mask, dim3((unsigned)mblocks), dim3(256), 0, stream, hdr, perm, offs + W, n, W,
-                     mask);
+  // the weights as rows of the products below (W_qkv^T for dx, W_o^T for do),
+  // and which rows lie in a window
+  PrepArgs pa{};
+  pa.wqkv = wqkv;
+  pa.wt_qkv = wt_qkv;
+  pa.wo = wo;
+  pa.wt_o = wt_o;
+  pa.hdr = hdr;
+  pa.perm = perm;
+  pa.nvalid = offs + W;
+  pa.mask = mask;
+  pa.C = C;
+  pa.n = n;
+  pa.W = W;
+  pa.mask_blocks = (int32_t)std::min<int64_t>(1024, std::max<int64_t>(1, ((int64_t)n + 255) / 256));
+  const int32_t tiles = (C / 32) * (3 * C / 32) + (C / 32) * (C / 32);
+  hipLaunchKernelGGL((k_prep<T>), dim3((unsigned)(tiles + pa.mask_blocks)), dim3(256), 0, stream, pa);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   // q | k | v = x W_qkv^T + b_qkv
   RowGemmArgs ga{};
