@@ -300,7 +300,8 @@ __global__ __launch_bounds__(kXcaThreads) void k_xca_bwd(
   __shared__ __align__(16) float s_a[kXcaRows][LD];
   __shared__ __align__(16) float s_b[kXcaRows][LD];
   __shared__ float s_g[D][D + 1];    // A
-  __shared__ float s_dg[D][D + 1];   // dG
+  __shared__ __align__(16) float s_bq[D][LD];   // B_q[e][c] = tau dG[e][c] / nk_c
+  __shared__ __align__(16) float s_bk[D][LD];   // B_k[c][e] = tau dG[e][c] / nq_e
   __shared__ float s_sp[2 * RPP][D]; // shares of s_e and t_c
   __shared__ float s_nrm[2 * D];     // nq, nk
   __shared__ float s_st[2 * D];      // s_e, t_c
@@ -439,7 +440,10 @@ __global__ __launch_bounds__(kXcaThreads) void k_xca_bwd(
   __syncthreads();   // the last block's readers of s_a, s_b and every reader of s_g are done
   if ((tid & 63) == 0) s_red[tid >> 6] = wsum;
 #pragma unroll
-  for (int u = 0; u < EPT; ++u) s_dg[e][c0 + u] = dg[u];
+  for (int u = 0; u < EPT; ++u) {
+    s_bq[e][c0 + u] = t * dg[u] / s_nrm[D + c0 + u];
+    s_bk[c0 + u][e] = t * dg[u] / s_nrm[e];
+  }
   __syncthreads();
   if (tid == 0) {
     float tot = 0.f;
@@ -450,32 +454,32 @@ __global__ __launch_bounds__(kXcaThreads) void k_xca_bwd(
 
   // 4. dqh[:, x3], dkh[:, x3] for rows r3, r3 + RPP, ... of each block, and their
   //    projections on qhat[:, x3], khat[:, x3]
-  float bq[D], bk[D];
-#pragma unroll
-  for (int j = 0; j < D; ++j) {
-    bq[j] = t * s_dg[x3][j] / s_nrm[D + j];
-    bk[j] = t * s_dg[j][x3] / s_nrm[j];
-  }
   const float nq = s_nrm[x3], nk = s_nrm[D + x3];
   constexpr int RPT = kXcaRows / RPP;   // rows of a block per thread
   float gqr[RPT], gkr[RPT];
-  // dqh and dkh of this thread's rows of the block in LDS
+  // dqh and dkh of this thread's rows of the block in LDS: rows B_q[x3] and
+  // B_k[x3] are read 4 columns at a time, outside the loop over the rows, so
+  // that only one slice of them is held in registers
   auto grads = [&](int nr) {
 #pragma unroll
     for (int m = 0; m < RPT; ++m) {
-      const int r = r3 + RPP * m;
-      float gq = 0.f, gk = 0.f;
-      if (r < nr) {
+      gqr[m] = 0.f;
+      gkr[m] = 0.f;
+    }
 #pragma unroll
-        for (int j = 0; j < D; j += 4) {
+    for (int j = 0; j < D; j += 4) {
+      const float4 bq = *reinterpret_cast<const float4*>(&s_bq[x3][j]);
+      const float4 bk = *reinterpret_cast<const float4*>(&s_bk[x3][j]);
+#pragma unroll
+      for (int m = 0; m < RPT; ++m) {
+        const int r = r3 + RPP * m;
+        if (r < nr) {
           const float4 kx = *reinterpret_cast<const float4*>(&s_b[r][j]);
           const float4 qx = *reinterpret_cast<const float4*>(&s_a[r][j]);
-          gq += bq[j] * kx.x + bq[j + 1] * kx.y + bq[j + 2] * kx.z + bq[j + 3] * kx.w;
-          gk += bk[j] * qx.x + bk[j + 1] * qx.y + bk[j + 2] * qx.z + bk[j + 3] * qx.w;
+          gqr[m] += bq.x * kx.x + bq.y * kx.y + bq.z * kx.z + bq.w * kx.w;
+          gkr[m] += bk.x * qx.x + bk.y * qx.y + bk.z * qx.z + bk.w * qx.w;
         }
       }
-      gqr[m] = gq;
-      gkr[m] = gk;
     }
   };
   auto fetch_qk = [&](int32_t p0, int nr) {
