@@ -285,7 +285,7 @@ __global__ __launch_bounds__(kXcaThreads) void k_xca_fwd(
 // temperature gradient of every (window, head) goes to `part`; k_xca_dtau adds
 // the windows in order.
 template <typename T, int D>
-__global__ __launch_bounds__(kXcaThreads) void k_xca_bwd(
+__global__ __launch_bounds__(kXcaThreads) __attribute__((amdgpu_waves_per_eu(sizeof(T) == 4 ? 4 : 5))) void k_xca_bwd(
     const PlanHeader* __restrict__ hdr, const int32_t* __restrict__ perm,
     const int32_t* __restrict__ offs, const float* __restrict__ tau, const T* __restrict__ q,
     const T* __restrict__ k, const T* __restrict__ v, const T* __restrict__ dout,
@@ -299,8 +299,11 @@ __global__ __launch_bounds__(kXcaThreads) void k_xca_bwd(
   constexpr int NW = kXcaThreads / 64;
   __shared__ __align__(16) float s_a[kXcaRows][LD];
   __shared__ __align__(16) float s_b[kXcaRows][LD];
-  __shared__ float s_g[D][D + 1];    // A
-  __shared__ __align__(16) float s_bq[D][LD];   // B_q[e][c] = tau dG[e][c] / nk_c
+  // A (rows of D + 1) until pass 2 ends, then B_q[e][c] = tau dG[e][c] / nk_c
+  // (rows of LD) in the same place
+  __shared__ __align__(16) float s_ab[D * LD];
+  float (*const s_g)[D + 1] = reinterpret_cast<float (*)[D + 1]>(s_ab);
+  float (*const s_bq)[LD] = reinterpret_cast<float (*)[LD]>(s_ab);
   __shared__ __align__(16) float s_bk[D][LD];   // B_k[c][e] = tau dG[e][c] / nq_e
   __shared__ float s_sp[2 * RPP][D]; // shares of s_e and t_c
   __shared__ float s_nrm[2 * D];     // nq, nk
@@ -437,7 +440,8 @@ __global__ __launch_bounds__(kXcaThreads) void k_xca_bwd(
   float wsum = (tid - e * CPR) == 0 ? srow : 0.f;
 #pragma unroll
   for (int m = 1; m < 64; m <<= 1) wsum += __shfl_xor(wsum, m, 64);
-  __syncthreads();   // the last block's readers of s_a, s_b and every reader of s_g are done
+  __syncthreads();   // the last block's readers of s_a, s_b and every reader of s_g (A,
+                     // whose place B_q takes) are done
   if ((tid & 63) == 0) s_red[tid >> 6] = wsum;
 #pragma unroll
   for (int u = 0; u < EPT; ++u) {
