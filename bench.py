@@ -214,6 +214,43 @@ def stored_traffic(kernel):
     return None
 
 
+def time_rotating(torch, dev, fn, sets, reps, warmup, eager=False):
+    """Average microseconds of one call of fn over the buffer sets in rotation:
+    one HIP graph holding one call per set, replayed under events on the current
+    stream (a graph per call would time the host's graph launches for short calls),
+    or eager launches."""
+    nsets = len(sets)
+    for i in range(warmup):
+        fn(sets[i % nsets])
+    torch.cuda.synchronize()
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    if eager:
+        t0.record()
+        for i in range(reps):
+            fn(sets[i % nsets])
+        t1.record()
+        torch.cuda.synchronize()
+        return t0.elapsed_time(t1) / reps * 1e3
+    cur = torch.cuda.current_stream(dev)
+    cap = torch.cuda.Stream(dev)
+    cap.wait_stream(cur)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(cap):
+        with torch.cuda.graph(g, stream=cap):
+            for st in sets:
+                fn(st)
+    cur.wait_stream(cap)
+    g.replay()
+    torch.cuda.synchronize()
+    rounds = max(1, reps // nsets)
+    t0.record()
+    for _ in range(rounds):
+        g.replay()
+    t1.record()
+    torch.cuda.synchronize()
+    return t0.elapsed_time(t1) / (rounds * nsets) * 1e3
+
+
 def main():
     args = parse()
     if args.pmc_summary:
@@ -555,36 +592,7 @@ def bench_cwi(torch, sla, workloads, dev, args):
                          workspace=st["ws"], out=(st["dx"], *st["dw"]))
 
     def timed(fn, reps):
-        for i in range(args.warmup):
-            fn(sets[i % nsets])
-        torch.cuda.synchronize()
-        t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        if args.no_graph:   # eager launches (counter runs)
-            t0.record()
-            for i in range(reps):
-                fn(sets[i % nsets])
-            t1.record()
-            torch.cuda.synchronize()
-            return t0.elapsed_time(t1) / reps * 1e3
-        graphs = []
-        cap = torch.cuda.Stream(dev)
-        cap.wait_stream(torch.cuda.current_stream(dev))
-        with torch.cuda.stream(cap):
-            for s_ in range(nsets):
-                g = torch.cuda.CUDAGraph()
-                with torch.cuda.graph(g, stream=cap):
-                    fn(sets[s_])
-                graphs.append(g)
-        torch.cuda.current_stream(dev).wait_stream(cap)
-        for g in graphs:
-            g.replay()
-        torch.cuda.synchronize()
-        t0.record()
-        for i in range(reps):
-            graphs[i % nsets].replay()
-        t1.record()
-        torch.cuda.synchronize()
-        return t0.elapsed_time(t1) / reps * 1e3
+        return time_rotating(torch, dev, fn, sets, reps, args.warmup, eager=args.no_graph)
 
     reps = max(100, args.steps) if not args.no_graph else args.steps
     for st in sets:
@@ -652,29 +660,7 @@ def bench_xca(torch, sla, workloads, dev, args):
     torch.cuda.synchronize()
 
     def timed(fn, reps):
-        for i in range(args.warmup):
-            fn(sets[i % nsets])
-        torch.cuda.synchronize()
-        graphs = []
-        cap = torch.cuda.Stream(dev)
-        cap.wait_stream(torch.cuda.current_stream(dev))
-        with torch.cuda.stream(cap):
-            for s_ in range(nsets):
-                g = torch.cuda.CUDAGraph()
-                with torch.cuda.graph(g, stream=cap):
-                    fn(sets[s_])
-                graphs.append(g)
-        torch.cuda.current_stream(dev).wait_stream(cap)
-        for g in graphs:
-            g.replay()
-        torch.cuda.synchronize()
-        t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        t0.record()
-        for i in range(reps):
-            graphs[i % nsets].replay()
-        t1.record()
-        torch.cuda.synchronize()
-        return t0.elapsed_time(t1) / reps * 1e3
+        return time_rotating(torch, dev, fn, sets, reps, args.warmup, eager=args.no_graph)
 
     reps = max(50, args.steps)
     t_xca = timed(lambda st: sla.forward_xca(st["plan"], st["q"], st["k"], st["v"], tau, out=st["o"]), reps)
@@ -743,29 +729,7 @@ def bench_projected(torch, sla, workloads, dev, args):
         st["y"].copy_(Fn.linear(o.view(n, C), w_o, b_o))
 
     def timed(fn, reps):
-        for i in range(args.warmup):
-            fn(sets[i % nsets])
-        torch.cuda.synchronize()
-        graphs = []
-        cap = torch.cuda.Stream(dev)
-        cap.wait_stream(torch.cuda.current_stream(dev))
-        with torch.cuda.stream(cap):
-            for s_ in range(nsets):
-                g = torch.cuda.CUDAGraph()
-                with torch.cuda.graph(g, stream=cap):
-                    fn(sets[s_])
-                graphs.append(g)
-        torch.cuda.current_stream(dev).wait_stream(cap)
-        for g in graphs:
-            g.replay()
-        torch.cuda.synchronize()
-        t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        t0.record()
-        for i in range(reps):
-            graphs[i % nsets].replay()
-        t1.record()
-        torch.cuda.synchronize()
-        return t0.elapsed_time(t1) / reps * 1e3
+        return time_rotating(torch, dev, fn, sets, reps, args.warmup, eager=args.no_graph)
 
     reps = max(50, args.steps)
     t_fused = timed(fused, reps)
