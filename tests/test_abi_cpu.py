@@ -120,6 +120,8 @@ def test_build_argument_errors(L):
     assert b(None, 100, 8, 0, FAKE, FAKE, FAKE, nb) == sla.SLA_E_ARG        # CSR mode has no perm
     assert b(FAKE + 1, 100, 8, 0, None, None, FAKE, nb) == sla.SLA_E_ARG    # misaligned ids
     assert b(FAKE, 100, 16385, 0, None, None, FAKE, 1 << 30) == sla.SLA_E_UNSUPPORTED
+    # window ids (mode A) for at most 2^26 rows: 8,192 sort blocks of 8,192
+    assert b(FAKE, (1 << 26) + 1, 8, 0, None, None, FAKE, 1 << 40) == sla.SLA_E_UNSUPPORTED
     assert b(FAKE, -5, 8, 0, None, None, FAKE, nb) == sla.SLA_E_ARG
 
 

@@ -194,6 +194,20 @@ def test_builder_shapes(sla, W, n, L, srt):
     check_plan(sla, plan, ids, W, L)
 
 
+# the most rows mode A takes (2^26: 8,192 sort blocks of 8,192 rows), with the most
+# windows and out-of-range ids, and all rows in one window
+@pytest.mark.parametrize("W,bad", [(16384, 0.001), (1, 0.0)])
+def test_builder_max_rows(sla, W, bad):
+    n = 1 << 26
+    rng = np.random.default_rng([10, W])
+    ids = rng.integers(0, W, size=n, dtype=np.int32)
+    if bad:
+        ids[rng.random(n) < bad] = W
+    _say(f"[builder max rows] n={n} W={W}")
+    plan = build(sla, ids=ids, W=W)
+    check_plan(sla, plan, ids, W, 0)
+
+
 def test_builder_reuses_plan_buffer(sla):
     # one zero-filled buffer rebuilt for other sizes: the builder's window totals sit
     # at a fixed place and every build leaves them zero (block sizes 4096 and 1024)
