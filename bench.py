@@ -94,7 +94,8 @@ def kernel_source_hash():
 
 def short_kernel(name):
     for k in ("k_sla_bwd", "k_sla_fwd", "k_sort", "k_merge", "k_plan", "k_cwi_tiled", "k_cwi_fwd",
-              "k_cwi_dw_reduce", "k_cwi_dw", "k_cwi_map", "k_cwi_clear"):
+              "k_cwi_dw_reduce", "k_cwi_dw", "k_cwi_map", "k_cwi_clear", "k_xca_fwd", "k_xca_bwd",
+              "k_xca_dtau"):
         if k in name:
             return k
     if "copyBuffer" in name:    # the runtime's device-to-device copy kernel
@@ -149,7 +150,7 @@ def sq_summary(paths):
     and the derived figures rocprofv3 defines for gfx950: MfmaUtil = MFMA-busy
     cycles / (GPU-active cycles x SIMDs), VALUBusy = VALU-active cycles / CUs /
     GPU-active cycles, LDS bank-conflict ratio = conflict cycles / (LDS-active -
-    conflict cycles).  The counter file sums GRBM_GUI_ACTIVE over the 8 XCDs
+    conflict cycles), and LDS-active cycles per CU over GPU-active cycles.  The counter file sums GRBM_GUI_ACTIVE over the 8 XCDs
     while those definitions take its per-XCD maximum, so the sum is divided by 8.
     One F16 MFMA "MOP" is 512 flops; TFLOP/s is over the dispatch's own duration
     (its start and end timestamps)."""
@@ -168,9 +169,8 @@ def sq_summary(paths):
                     seen.add(r["Dispatch_Id"])
                     dur.setdefault(k, []).append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) * 1e-9)
     lines = ["kernel      counter                          per_launch        dispatches"]
-    for k in ("k_sort", "k_merge", "k_sla_fwd", "k_sla_bwd"):
-        if k not in acc:
-            continue
+    step = ("k_sort", "k_merge", "k_sla_fwd", "k_sla_bwd")
+    for k in [x for x in step if x in acc] + sorted(set(acc) - set(step)):
         c = {name: float(np.mean(v)) for name, v in acc[k].items()}
         for name in sorted(c):
             lines.append(f"{k:<11} {name:<32} {c[name]:>16.0f}  {len(acc[k][name]):>10}")
@@ -185,6 +185,9 @@ def sq_summary(paths):
             if "SQ_ACTIVE_INST_VALU" in c:
                 lines.append(f"{k:<11} derived VALUBusy_percent          "
                              f"{100 * c['SQ_ACTIVE_INST_VALU'] / MI355X_CUS / g:>16.2f}")
+            if "SQ_LDS_IDX_ACTIVE" in c:   # as VALUBusy: LDS-active cycles per CU over GPU-active cycles
+                lines.append(f"{k:<11} derived LdsActive_percent         "
+                             f"{100 * c['SQ_LDS_IDX_ACTIVE'] / MI355X_CUS / g:>16.2f}")
         if "SQ_LDS_BANK_CONFLICT" in c and "SQ_LDS_IDX_ACTIVE" in c:
             den = c["SQ_LDS_IDX_ACTIVE"] - c["SQ_LDS_BANK_CONFLICT"]
             if den > 0:

@@ -264,6 +264,200 @@ __global__ __launch_bounds__(kXcaThreads) void k_xca_fwd(
   }
 }
 
+// ----------------------------------------------- forward on the matrix cores
+// 16-bit storage, d = 32: the same three steps with both d x d contractions on
+// the matrix cores and the rows staged in LDS in their storage format.
+//   1. Wave w forms tile (w / 2, w % 2) of G = sum_r q_r^T k_r.  The contraction
+//      runs over rows, so both operands are columns of the staged rows, read
+//      with the LDS transpose load: in a group of 16 lanes, lane i of group g
+//      addresses row 8g + 4h + i / 4, columns 16t + 4 (i % 4) .. + 3, and
+//      receives (the probed lane layout of ds_read_b64_tr_b16) the four
+//      elements of column 16t + i in rows 8g + 4h .. + 3: operand slot 4h + j
+//      holds row 8g + 4h + j, for A (q) and B (k) alike.  The column norms are
+//      summed from the staged rows as in the fp32 path.
+//   2. The softmax as before, in fp32 from G in LDS; A is rounded to the storage
+//      type (bf16: as a pair of high part and residual, 16 bits together).
+//   3. o = v A^T: slot j of lane (i, g) is channel c = 8g + j, so A's row e and
+//      v's row r are read as they lie (16 bytes a lane); wave w forms the 16-row
+//      tile w of a 64-row block for both halves of d, and lane (i, g) receives
+//      o[row 16w + i][16t + 4g .. + 3].
+template <typename T>
+struct XcaTr;
+template <>
+struct XcaTr<_Float16> {
+  typedef short v4s __attribute__((ext_vector_type(4)));
+};
+template <>
+struct XcaTr<bf16_t> {
+  typedef short v4s __attribute__((ext_vector_type(4)));
+};
+
+// Columns 16t .. 16t + 15 of rows base .. base + 31 of a staged block as an
+// operand of a contraction over the rows (slot r of lane (i, g): row base + 8g + r,
+// column 16t + i).
+template <typename T, int LDH>
+__device__ __forceinline__ Raw<T, 8> xca_cols(const unsigned short (*s)[LDH], int base, int t, int i,
+                                              int g) {
+  using V = typename XcaTr<T>::v4s;
+  const int c = 16 * t + 4 * (i & 3);
+  const V a = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) V*)(&s[base + 8 * g + (i >> 2)][c]));
+  const V b = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) V*)(&s[base + 8 * g + 4 + (i >> 2)][c]));
+  Raw<T, 8> r;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    r[j] = (unsigned short)a[j];
+    r[4 + j] = (unsigned short)b[j];
+  }
+  return r;
+}
+
+template <typename T>
+__global__ __launch_bounds__(kXcaThreads) void k_xca_fwd_mma(
+    const PlanHeader* __restrict__ hdr, const int32_t* __restrict__ perm,
+    const int32_t* __restrict__ offs, const float* __restrict__ tau, const T* __restrict__ q,
+    const T* __restrict__ k, const T* __restrict__ v, T* __restrict__ o, int32_t n, int32_t W,
+    int32_t H) {
+  constexpr int D = 32;
+  constexpr int LDH = D + 8;                 // staged 16-bit rows: 80 bytes, 16-byte aligned
+  constexpr int EPT = D * D / kXcaThreads;   // softmax: entries (e, c) per thread
+  constexpr int CPR = D / EPT;
+  constexpr int NP = kXcaPerThread<T, D>;    // one 16-byte piece a thread
+  constexpr bool kPair = std::is_same<T, bf16_t>::value;
+  using F = Frag<T, 8>;
+  static_assert(NP == 1 && kXcaPieces<T, D> == kXcaThreads, "one piece a thread");
+  __shared__ __align__(16) unsigned short s_q[kXcaRows][LDH];
+  __shared__ __align__(16) unsigned short s_k[kXcaRows][LDH];
+  __shared__ __align__(16) unsigned short s_v[kXcaRows][LDH];
+  __shared__ __align__(16) unsigned short s_p[kPair ? 2 : 1][D][LDH];   // A (and its residual)
+  __shared__ float s_g[D][D + 1];
+  __shared__ float s_nrm[2 * D];
+  __shared__ int32_t s_row[kXcaRows];
+  int32_t w, h;
+  xca_item(blockIdx.x, H, w, h);
+  if (w >= W) return;
+  if (hdr->magic != kPlanMagic || hdr->n != n || hdr->num_windows != W) return;
+  const int32_t* pm = hdr->csr ? nullptr : perm;
+  const int32_t rb = max(0, min(offs[w], n)), re = max(rb, min(offs[w + 1], n));
+  if (rb == re) return;
+  const int tid = (int)threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int i = lane & 15, g = lane >> 4;
+  const size_t rs = (size_t)H * D;
+  const int col = h * D;
+  const floatx4 zero = {0.f, 0.f, 0.f, 0.f};
+  // piece tid of a block: row tid / 4, channels 8 (tid % 4) .. + 7
+  const int pr = tid >> 2, pc = tid & 3;
+  auto put = [&](unsigned short (*s)[LDH], uint4 x) { *reinterpret_cast<uint4*>(&s[pr][8 * pc]) = x; };
+
+  // 1. G tile (et, ct) of this wave, and the squared column norms
+  const int et = wv >> 1, ct = wv & 1;
+  floatx4 acc = zero;
+  float nrm = 0.f;
+  const bool one = re - rb <= kXcaRows;
+  uint4 vr[NP];
+  for (int32_t p0 = rb; p0 < re; p0 += kXcaRows) {
+    const int nr = min(kXcaRows, re - p0);
+    if (p0 != rb) __syncthreads();   // the previous block's readers are done
+    {
+      uint4 qr[NP], kr[NP];
+      xca_fetch<T, D>(pm, p0, nr, n, rs, col, q, qr, s_row);
+      xca_fetch<T, D>(pm, p0, nr, n, rs, col, k, kr, nullptr);
+      if (one) xca_fetch<T, D>(pm, p0, nr, n, rs, col, v, vr, nullptr);
+      put(s_q, qr[0]);
+      put(s_k, kr[0]);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      if (32 * ks >= nr) break;   // rows past nr are zero
+      acc = F::mma(xca_cols<T, LDH>(s_q, 32 * ks, et, i, g), xca_cols<T, LDH>(s_k, 32 * ks, ct, i, g), acc);
+    }
+    if (tid < D) {
+      for (int r = 0; r < nr; ++r) {
+        const float x = u16_to_f32<T>(s_q[r][tid]);
+        nrm += x * x;
+      }
+    } else if (tid < 2 * D) {
+      for (int r = 0; r < nr; ++r) {
+        const float x = u16_to_f32<T>(s_k[r][tid - D]);
+        nrm += x * x;
+      }
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < 4; ++j) s_g[16 * et + 4 * g + j][16 * ct + i] = acc[j];
+  if (tid < 2 * D) s_nrm[tid] = fmaxf(sqrtf(nrm), 1e-12f);
+  __syncthreads();
+
+  // 2. softmax of each row e over c, A to the storage type
+  {
+    const int e = tid / CPR, c0 = (tid - e * CPR) * EPT;
+    const float t = tau[h];
+    float gv[EPT];
+    float mx = -3.0e38f;
+#pragma unroll
+    for (int u = 0; u < EPT; ++u) {
+      gv[u] = t * s_g[e][c0 + u] / (s_nrm[e] * s_nrm[D + c0 + u]);
+      mx = fmaxf(mx, gv[u]);
+    }
+#pragma unroll
+    for (int m = 1; m < CPR; m <<= 1) mx = fmaxf(mx, __shfl_xor(mx, m, 64));
+    float sum = 0.f;
+#pragma unroll
+    for (int u = 0; u < EPT; ++u) {
+      gv[u] = expf(gv[u] - mx);
+      sum += gv[u];
+    }
+#pragma unroll
+    for (int m = 1; m < CPR; m <<= 1) sum += __shfl_xor(sum, m, 64);
+    const float inv = 1.f / sum;
+#pragma unroll
+    for (int u = 0; u < EPT; ++u) {
+      const float a = gv[u] * inv;
+      const unsigned short hi = f32_to_u16<T>(a);
+      s_p[0][e][c0 + u] = hi;
+      if constexpr (kPair) s_p[kPair ? 1 : 0][e][c0 + u] = f32_to_u16<T>(a - u16_to_f32<T>(hi));
+    }
+  }
+  // s_q's last readers (the norms) passed the barrier above; s_v is unused so far
+  if (one) put(s_v, vr[0]);
+  __syncthreads();
+
+  // 3. o = v A^T, tile wv of each 64-row block
+  Raw<T, 8> pa[2], pl[2];
+#pragma unroll
+  for (int t2 = 0; t2 < 2; ++t2) {
+    pa[t2] = *reinterpret_cast<const Raw<T, 8>*>(&s_p[0][16 * t2 + i][8 * g]);
+    if constexpr (kPair) pl[t2] = *reinterpret_cast<const Raw<T, 8>*>(&s_p[kPair ? 1 : 0][16 * t2 + i][8 * g]);
+  }
+  for (int32_t p0 = rb; p0 < re; p0 += kXcaRows) {
+    const int nr = min(kXcaRows, re - p0);
+    if (!one) {
+      __syncthreads();   // s_v and s_row are free
+      uint4 raw[NP];
+      xca_fetch<T, D>(pm, p0, nr, n, rs, col, v, raw, s_row);
+      put(s_v, raw[0]);
+      __syncthreads();
+    }
+    const int r = 16 * wv + i;
+    if (16 * wv >= nr) continue;   // the whole tile is past the block's rows
+    const Raw<T, 8> vb = *reinterpret_cast<const Raw<T, 8>*>(&s_v[r][8 * g]);
+    const int32_t row = r < nr ? s_row[r] : -1;
+#pragma unroll
+    for (int t2 = 0; t2 < 2; ++t2) {
+      floatx4 d4 = F::mma(pa[t2], vb, zero);
+      if constexpr (kPair) d4 = F::mma(pl[t2], vb, d4);
+      if (row >= 0) {
+        u16x4 pk;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) pk[j] = f32_to_u16<T>(d4[j]);
+        *reinterpret_cast<u16x4*>(o + (size_t)row * rs + col + 16 * t2 + 4 * g) = pk;
+      }
+    }
+  }
+}
+
 // ---------------------------------------------------------------- backward
 // Chain rule of the forward, per (window, head) workgroup, with
 // N = qhat^T khat, G = tau N and A = softmax_c(G):
@@ -588,6 +782,15 @@ hipError_t xca_impl(const void* plan, int32_t n, int32_t W, int32_t H, const flo
                     const void* q, const void* k, const void* v, void* o, hipStream_t stream) {
   const PlanLayout lay = plan_layout(n, W);
   const char* base = static_cast<const char*>(plan);
+  if constexpr (Ty<T>::kNarrow && D == 32) {
+    hipLaunchKernelGGL((k_xca_fwd_mma<T>), dim3(xca_grid(W, H)), dim3(kXcaThreads), 0, stream,
+                       reinterpret_cast<const PlanHeader*>(base + lay.header),
+                       reinterpret_cast<const int32_t*>(base + lay.perm),
+                       reinterpret_cast<const int32_t*>(base + lay.offsets), tau,
+                       static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v),
+                       static_cast<T*>(o), n, W, H);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL((k_xca_fwd<T, D>), dim3(xca_grid(W, H)), dim3(kXcaThreads), 0, stream,
                      reinterpret_cast<const PlanHeader*>(base + lay.header),
                      reinterpret_cast<const int32_t*>(base + lay.perm),
