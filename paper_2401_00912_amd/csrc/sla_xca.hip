@@ -741,6 +741,413 @@ __global__ __launch_bounds__(kXcaThreads) __attribute__((amdgpu_waves_per_eu(siz
   }
 }
 
+// ---------------------------------------------- backward on the matrix cores
+// 16-bit storage, d = 32: the chain rule of k_xca_bwd with its contractions on
+// the matrix cores, the rows staged in LDS in their storage format, and the same
+// three passes (a window of one block stages all four matrices in the first).
+//   1. G tile (w / 2, w % 2) of wave w from transpose reads, as the forward;
+//      the norms and the softmax in fp32; A rounded to the storage type (bf16:
+//      high part and residual).
+//   2. dA = sum_r dout_r^T v_r, tile (w / 2, w % 2), from transpose reads; dv =
+//      dout A (dv[r][c] = sum_e A[e][c] dout[r][e]): A's columns by transpose
+//      reads, dout's rows as they lie; wave w forms rows 16w .. 16w + 15.
+//   3. dG and the temperature share in fp32 as before.  B_q[e][c] = tau dG[e][c]
+//      / nk_c spans the range of 1 / nk, which a floored norm (a zero column)
+//      makes 10^12 times wider than the rest, so the column factor is split:
+//      B_q[e][c] k[r][c] = (tau dG[e][c] s_c / nk_c) (k[r][c] / s_c) with s_c =
+//      2^floor(log2 nk_c).  The first factor (within [1/2, 1] of tau dG) is
+//      scaled by one power of two into [1, 2) and stored as high part and
+//      residual (16 bits in bf16, 22 in fp16, no overflow); the second is the
+//      staged row rescaled by a power of two (exact, |k / s_c| < 2).  B_k^T
+//      (B_k[c][e] = tau dG[e][c] / nq_e) alike with nq_e.
+//   4. dqh = k B_q^T and dkh = q B_k^T for rows 16w + i from row reads; the
+//      projections s_e and t_c summed from the same fp32 values over the rows
+//      (lanes, then waves, in a fixed order), so the one-row window's exact
+//      cancellation holds as in k_xca_bwd; then dq, dk.
+__device__ __forceinline__ float xca_pow2_scale(float x) {
+  if (!(x > 0.f) || !(x < 3.0e38f)) return 1.f;
+  const int ex = (int)((__float_as_uint(x) >> 23) & 0xffu) - 127;
+  return ldexpf(1.f, min(-ex, 126));
+}
+
+// 2^floor(log2 x) for a normal x > 0 (the norms: at least 1e-12)
+__device__ __forceinline__ float xca_pow2_floor(float x) {
+  return __uint_as_float(__float_as_uint(x) & 0x7f800000u);
+}
+
+// A staged row's 8 channels 8g .. 8g + 7, each times a power of two (exact)
+template <typename T>
+__device__ __forceinline__ Raw<T, 8> xca_rescale(Raw<T, 8> x, const float (&m)[8]) {
+  Raw<T, 8> r;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) r[j] = f32_to_u16<T>(u16_to_f32<T>(x[j]) * m[j]);
+  return r;
+}
+
+template <typename T>
+__global__ __launch_bounds__(kXcaThreads) __attribute__((amdgpu_waves_per_eu(5))) void k_xca_bwd_mma(
+    const PlanHeader* __restrict__ hdr, const int32_t* __restrict__ perm,
+    const int32_t* __restrict__ offs, const float* __restrict__ tau, const T* __restrict__ q,
+    const T* __restrict__ k, const T* __restrict__ v, const T* __restrict__ dout,
+    T* __restrict__ dq, T* __restrict__ dk, T* __restrict__ dv, float* __restrict__ part,
+    int32_t n, int32_t W, int32_t H) {
+  constexpr int D = 32;
+  constexpr int LDH = D + 8;
+  constexpr int EPT = D * D / kXcaThreads;
+  constexpr int CPR = D / EPT;
+  constexpr int NP = kXcaPerThread<T, D>;
+  constexpr int NW = kXcaThreads / 64;
+  constexpr bool kPair = std::is_same<T, bf16_t>::value;
+  using F = Frag<T, 8>;
+  static_assert(NP == 1 && kXcaPieces<T, D> == kXcaThreads, "one piece a thread");
+  __shared__ __align__(16) unsigned short s_q[kXcaRows][LDH];
+  __shared__ __align__(16) unsigned short s_k[kXcaRows][LDH];
+  __shared__ __align__(16) unsigned short s_d[kXcaRows][LDH];   // dout
+  __shared__ __align__(16) unsigned short s_v[kXcaRows][LDH];
+  // pass 2: [0] A, [1] its residual; from step 3: B_q and its residual
+  __shared__ __align__(16) unsigned short s_m[2][D][LDH];
+  // from step 3, in the place of the v rows (read last in pass 2): B_k^T and its
+  // residual
+  unsigned short (*const s_bk)[D][LDH] = reinterpret_cast<unsigned short (*)[D][LDH]>(&s_v[0][0]);
+  __shared__ float s_g[D][D + 1];     // G, then dA
+  __shared__ float s_nrm[2 * D];
+  __shared__ float s_sp[NW][2 * D];   // the waves' shares of s_e and t_c
+  __shared__ float s_st[2 * D];       // s_e, t_c
+  __shared__ float s_red[3][NW];      // temperature shares; maxima of |B_q|, |B_k|
+  __shared__ int32_t s_row[kXcaRows];
+  const int tid = (int)threadIdx.x;
+  int32_t w, h;
+  xca_item(blockIdx.x, H, w, h);
+  if (w >= W) return;
+  const size_t b = (size_t)w * H + h;   // this (window, head)'s temperature partial
+  if (hdr->magic != kPlanMagic || hdr->n != n || hdr->num_windows != W) {
+    if (tid == 0) part[b] = 0.f;
+    return;
+  }
+  const int32_t* pm = hdr->csr ? nullptr : perm;
+  const int32_t rb = max(0, min(offs[w], n)), re = max(rb, min(offs[w + 1], n));
+  if (rb == re) {
+    if (tid == 0) part[b] = 0.f;
+    return;
+  }
+  const int lane = tid & 63, wv = tid >> 6;
+  const int i = lane & 15, g = lane >> 4;
+  const size_t rs = (size_t)H * D;
+  const int col = h * D;
+  const float t = tau[h];
+  const floatx4 zero = {0.f, 0.f, 0.f, 0.f};
+  const int pr = tid >> 2, pc = tid & 3;   // piece tid of a block: row tid / 4, channels 8 (tid % 4) ..
+  auto put = [&](unsigned short (*s)[LDH], uint4 x) { *reinterpret_cast<uint4*>(&s[pr][8 * pc]) = x; };
+  auto row_op = [&](const unsigned short (*s)[LDH], int r) {
+    return *reinterpret_cast<const Raw<T, 8>*>(&s[r][8 * g]);
+  };
+  const bool one = re - rb <= kXcaRows;
+  const int et = wv >> 1, ct = wv & 1;
+
+  // 1. G (raw sums) and the column norms
+  floatx4 gacc = zero;
+  float nrm = 0.f;
+  for (int32_t p0 = rb; p0 < re; p0 += kXcaRows) {
+    const int nr = min(kXcaRows, re - p0);
+    if (p0 != rb) __syncthreads();
+    {
+      uint4 qr[NP], kr[NP];
+      xca_fetch<T, D>(pm, p0, nr, n, rs, col, q, qr, s_row);
+      xca_fetch<T, D>(pm, p0, nr, n, rs, col, k, kr, nullptr);
+      if (one) {
+        uint4 dr[NP], vr[NP];
+        xca_fetch<T, D>(pm, p0, nr, n, rs, col, dout, dr, nullptr);
+        xca_fetch<T, D>(pm, p0, nr, n, rs, col, v, vr, nullptr);
+        put(s_d, dr[0]);
+        put(s_v, vr[0]);
+      }
+      put(s_q, qr[0]);
+      put(s_k, kr[0]);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      if (32 * ks >= nr) break;
+      gacc = F::mma(xca_cols<T, LDH>(s_q, 32 * ks, et, i, g), xca_cols<T, LDH>(s_k, 32 * ks, ct, i, g), gacc);
+    }
+    if (tid < D) {
+      for (int r = 0; r < nr; ++r) {
+        const float x = u16_to_f32<T>(s_q[r][tid]);
+        nrm += x * x;
+      }
+    } else if (tid < 2 * D) {
+      for (int r = 0; r < nr; ++r) {
+        const float x = u16_to_f32<T>(s_k[r][tid - D]);
+        nrm += x * x;
+      }
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < 4; ++j) s_g[16 * et + 4 * g + j][16 * ct + i] = gacc[j];
+  if (tid < 2 * D) s_nrm[tid] = fmaxf(sqrtf(nrm), 1e-12f);
+  __syncthreads();
+  // N = G / (nq nk), A = softmax of tau N over c, thread (e, c0 .. c0 + EPT - 1)
+  const int e = tid / CPR, c0 = (tid - e * CPR) * EPT;
+  float nn[EPT], a[EPT];
+  {
+    float mx = -3.0e38f;
+#pragma unroll
+    for (int u = 0; u < EPT; ++u) {
+      nn[u] = s_g[e][c0 + u] / (s_nrm[e] * s_nrm[D + c0 + u]);
+      a[u] = t * nn[u];
+      mx = fmaxf(mx, a[u]);
+    }
+#pragma unroll
+    for (int m = 1; m < CPR; m <<= 1) mx = fmaxf(mx, __shfl_xor(mx, m, 64));
+    float sum = 0.f;
+#pragma unroll
+    for (int u = 0; u < EPT; ++u) {
+      a[u] = expf(a[u] - mx);
+      sum += a[u];
+    }
+#pragma unroll
+    for (int m = 1; m < CPR; m <<= 1) sum += __shfl_xor(sum, m, 64);
+    const float inv = 1.f / sum;
+#pragma unroll
+    for (int u = 0; u < EPT; ++u) {
+      a[u] *= inv;
+      const unsigned short hi = f32_to_u16<T>(a[u]);
+      s_m[0][e][c0 + u] = hi;
+      if constexpr (kPair) s_m[1][e][c0 + u] = f32_to_u16<T>(a[u] - u16_to_f32<T>(hi));
+    }
+  }
+  __syncthreads();
+
+  // 2. dA, and dv = dout A for rows 16 wv + i of each block
+  Raw<T, 8> at[2], atl[2];
+#pragma unroll
+  for (int t2 = 0; t2 < 2; ++t2) {
+    at[t2] = xca_cols<T, LDH>(s_m[0], 0, t2, i, g);
+    if constexpr (kPair) atl[t2] = xca_cols<T, LDH>(s_m[1], 0, t2, i, g);
+  }
+  floatx4 dacc = zero;
+  for (int32_t p0 = rb; p0 < re; p0 += kXcaRows) {
+    const int nr = min(kXcaRows, re - p0);
+    if (!one) {
+      __syncthreads();   // the previous block's readers of s_d, s_v, s_row are done
+      uint4 dr[NP], vr[NP];
+      xca_fetch<T, D>(pm, p0, nr, n, rs, col, dout, dr, s_row);
+      xca_fetch<T, D>(pm, p0, nr, n, rs, col, v, vr, nullptr);
+      put(s_d, dr[0]);
+      put(s_v, vr[0]);
+      __syncthreads();
+    }
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      if (32 * ks >= nr) break;
+      dacc = F::mma(xca_cols<T, LDH>(s_d, 32 * ks, et, i, g), xca_cols<T, LDH>(s_v, 32 * ks, ct, i, g), dacc);
+    }
+    if (16 * wv < nr) {
+      const int r = 16 * wv + i;
+      const Raw<T, 8> db = row_op(s_d, r);
+      const int32_t row = r < nr ? s_row[r] : -1;
+#pragma unroll
+      for (int t2 = 0; t2 < 2; ++t2) {
+        floatx4 d4 = F::mma(at[t2], db, zero);
+        if constexpr (kPair) d4 = F::mma(atl[t2], db, d4);
+        if (row >= 0) {
+          u16x4 pk;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) pk[j] = f32_to_u16<T>(d4[j]);
+          *reinterpret_cast<u16x4*>(dv + (size_t)row * rs + col + 16 * t2 + 4 * g) = pk;
+        }
+      }
+    }
+  }
+  // s_g's readers (the softmax) passed the barrier after it
+#pragma unroll
+  for (int j = 0; j < 4; ++j) s_g[16 * et + 4 * g + j][16 * ct + i] = dacc[j];
+  __syncthreads();   // also: every reader of A in s_m and of the v rows is done
+
+  // 3. dG, the temperature share, B_q and B_k^T
+  float bq[EPT], bk[EPT];
+  {
+    float da[EPT], rsum = 0.f;
+#pragma unroll
+    for (int u = 0; u < EPT; ++u) {
+      da[u] = s_g[e][c0 + u];
+      rsum += a[u] * da[u];
+    }
+#pragma unroll
+    for (int m = 1; m < CPR; m <<= 1) rsum += __shfl_xor(rsum, m, 64);
+    float pt = 0.f, mq = 0.f, mk = 0.f;
+    const float nqe = s_nrm[e];
+#pragma unroll
+    for (int u = 0; u < EPT; ++u) {
+      const float dg = a[u] * (da[u] - rsum);
+      const float nkc = s_nrm[D + c0 + u];
+      pt += dg * nn[u];
+      bq[u] = t * dg * (xca_pow2_floor(nkc) / nkc);
+      bk[u] = t * dg * (xca_pow2_floor(nqe) / nqe);
+      mq = fmaxf(mq, fabsf(bq[u]));
+      mk = fmaxf(mk, fabsf(bk[u]));
+    }
+    float srow = pt;
+#pragma unroll
+    for (int m = 1; m < CPR; m <<= 1) srow += __shfl_xor(srow, m, 64);   // sum_c dG N over row e
+    float wsum = (tid - e * CPR) == 0 ? srow : 0.f;
+#pragma unroll
+    for (int m = 1; m < 64; m <<= 1) {
+      wsum += __shfl_xor(wsum, m, 64);
+      mq = fmaxf(mq, __shfl_xor(mq, m, 64));
+      mk = fmaxf(mk, __shfl_xor(mk, m, 64));
+    }
+    if (lane == 0) {
+      s_red[0][wv] = wsum;
+      s_red[1][wv] = mq;
+      s_red[2][wv] = mk;
+    }
+  }
+  __syncthreads();
+  float mq = 0.f, mk = 0.f;
+#pragma unroll
+  for (int j = 0; j < NW; ++j) {
+    mq = fmaxf(mq, s_red[1][j]);
+    mk = fmaxf(mk, s_red[2][j]);
+  }
+  const float sq_ = xca_pow2_scale(mq), sk_ = xca_pow2_scale(mk);
+  if (tid == 0) {
+    float tot = 0.f;
+#pragma unroll
+    for (int j = 0; j < NW; ++j) tot += s_red[0][j];
+    part[b] = tot;
+  }
+#pragma unroll
+  for (int u = 0; u < EPT; ++u) {
+    const float xq = bq[u] * sq_, xk = bk[u] * sk_;
+    const unsigned short hq = f32_to_u16<T>(xq), hk = f32_to_u16<T>(xk);
+    s_m[0][e][c0 + u] = hq;
+    s_m[1][e][c0 + u] = f32_to_u16<T>(xq - u16_to_f32<T>(hq));
+    s_bk[0][c0 + u][e] = hk;
+    s_bk[1][c0 + u][e] = f32_to_u16<T>(xk - u16_to_f32<T>(hk));
+  }
+  __syncthreads();
+
+  // 4. dqh, dkh of rows 16 wv + i, their projections, then dq, dk
+  const float iq = 1.f / sq_, ik = 1.f / sk_;
+  float gq[2][4], gk[2][4];   // dqh[r][16 t2 + 4 g + j], dkh[r][16 t2 + 4 g + j]
+  // (the B operands, the norms and the column scales are read from LDS where they
+  // are used: held in registers they cost a fourth workgroup per CU)
+  auto grads = [&](int r) {
+    float ik8[8], iq8[8];   // 1 / s_c for this lane's channels 8g .. 8g + 7
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      ik8[j] = 1.f / xca_pow2_floor(s_nrm[D + 8 * g + j]);
+      iq8[j] = 1.f / xca_pow2_floor(s_nrm[8 * g + j]);
+    }
+    const Raw<T, 8> kb = xca_rescale<T>(row_op(s_k, r), ik8), qb = xca_rescale<T>(row_op(s_q, r), iq8);
+#pragma unroll
+    for (int t2 = 0; t2 < 2; ++t2) {
+      const floatx4 x = F::mma(row_op(s_m[1], 16 * t2 + i), kb, F::mma(row_op(s_m[0], 16 * t2 + i), kb, zero));
+      const floatx4 y = F::mma(row_op(s_bk[1], 16 * t2 + i), qb, F::mma(row_op(s_bk[0], 16 * t2 + i), qb, zero));
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        gq[t2][j] = x[j] * iq;
+        gk[t2][j] = y[j] * ik;
+      }
+    }
+  };
+  auto fetch_qk = [&](int32_t p0, int nr) {
+    uint4 qr[NP], kr[NP];
+    xca_fetch<T, D>(pm, p0, nr, n, rs, col, q, qr, s_row);
+    xca_fetch<T, D>(pm, p0, nr, n, rs, col, k, kr, nullptr);
+    put(s_q, qr[0]);
+    put(s_k, kr[0]);
+  };
+  float ps[2][4] = {}, pk[2][4] = {};
+  for (int32_t p0 = rb; p0 < re; p0 += kXcaRows) {
+    const int nr = min(kXcaRows, re - p0);
+    if (!one) {
+      __syncthreads();
+      fetch_qk(p0, nr);
+      __syncthreads();
+    }
+    const int r = 16 * wv + i;
+    if (16 * wv < nr) {
+      grads(r);
+      if (r < nr) {
+#pragma unroll
+        for (int t2 = 0; t2 < 2; ++t2) {
+          const u16x4 qx = *reinterpret_cast<const u16x4*>(&s_q[r][16 * t2 + 4 * g]);
+          const u16x4 kx = *reinterpret_cast<const u16x4*>(&s_k[r][16 * t2 + 4 * g]);
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            ps[t2][j] += (u16_to_f32<T>(qx[j]) / s_nrm[16 * t2 + 4 * g + j]) * gq[t2][j];
+            pk[t2][j] += (u16_to_f32<T>(kx[j]) / s_nrm[D + 16 * t2 + 4 * g + j]) * gk[t2][j];
+          }
+        }
+      }
+    }
+  }
+  // the rows' shares: over the 16 lanes of a group (rows 16 wv + i), then the waves
+#pragma unroll
+  for (int m = 1; m < 16; m <<= 1)
+#pragma unroll
+    for (int t2 = 0; t2 < 2; ++t2)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        ps[t2][j] += __shfl_xor(ps[t2][j], m, 64);
+        pk[t2][j] += __shfl_xor(pk[t2][j], m, 64);
+      }
+  if (i == 0) {
+#pragma unroll
+    for (int t2 = 0; t2 < 2; ++t2)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        s_sp[wv][16 * t2 + 4 * g + j] = ps[t2][j];
+        s_sp[wv][D + 16 * t2 + 4 * g + j] = pk[t2][j];
+      }
+  }
+  __syncthreads();
+  if (tid < 2 * D) {
+    float x = 0.f;
+#pragma unroll
+    for (int j = 0; j < NW; ++j) x += s_sp[j][tid];
+    s_st[tid] = s_nrm[tid] > 1e-12f ? x : 0.f;   // a floored norm is a constant: no projection
+  }
+  __syncthreads();
+  float sv[2][4], tv[2][4];
+#pragma unroll
+  for (int t2 = 0; t2 < 2; ++t2)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      sv[t2][j] = s_st[16 * t2 + 4 * g + j];
+      tv[t2][j] = s_st[D + 16 * t2 + 4 * g + j];
+    }
+  for (int32_t p0 = rb; p0 < re; p0 += kXcaRows) {
+    const int nr = min(kXcaRows, re - p0);
+    if (!one) {
+      __syncthreads();
+      fetch_qk(p0, nr);
+      __syncthreads();
+    }
+    const int r = 16 * wv + i;
+    if (16 * wv >= nr) continue;
+    if (!one) grads(r);
+    const int32_t row = r < nr ? s_row[r] : -1;
+    if (row < 0) continue;
+#pragma unroll
+    for (int t2 = 0; t2 < 2; ++t2) {
+      const u16x4 qx = *reinterpret_cast<const u16x4*>(&s_q[r][16 * t2 + 4 * g]);
+      const u16x4 kx = *reinterpret_cast<const u16x4*>(&s_k[r][16 * t2 + 4 * g]);
+      u16x4 oq, ok;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const float nq = s_nrm[16 * t2 + 4 * g + j], nk = s_nrm[D + 16 * t2 + 4 * g + j];
+        oq[j] = f32_to_u16<T>((gq[t2][j] - (u16_to_f32<T>(qx[j]) / nq) * sv[t2][j]) / nq);
+        ok[j] = f32_to_u16<T>((gk[t2][j] - (u16_to_f32<T>(kx[j]) / nk) * tv[t2][j]) / nk);
+      }
+      *reinterpret_cast<u16x4*>(dq + (size_t)row * rs + col + 16 * t2 + 4 * g) = oq;
+      *reinterpret_cast<u16x4*>(dk + (size_t)row * rs + col + 16 * t2 + 4 * g) = ok;
+    }
+  }
+}
+
 // dtau[h] = sum over windows, in window order, of the (window, head) partials:
 // 256 strided sums, then a fixed tree.
 __global__ __launch_bounds__(kXcaThreads) void k_xca_dtau(const float* __restrict__ part, int32_t W,
@@ -764,6 +1171,15 @@ hipError_t xca_bwd_impl(const void* plan, int32_t n, int32_t W, int32_t H, const
                         void* dk, void* dv, float* dtau, float* part, hipStream_t stream) {
   const PlanLayout lay = plan_layout(n, W);
   const char* base = static_cast<const char*>(plan);
+  if constexpr (Ty<T>::kNarrow && D == 32)
+    hipLaunchKernelGGL((k_xca_bwd_mma<T>), dim3(xca_grid(W, H)), dim3(kXcaThreads), 0, stream,
+                       reinterpret_cast<const PlanHeader*>(base + lay.header),
+                       reinterpret_cast<const int32_t*>(base + lay.perm),
+                       reinterpret_cast<const int32_t*>(base + lay.offsets), tau,
+                       static_cast<const T*>(q), static_cast<const T*>(k), static_cast<const T*>(v),
+                       static_cast<const T*>(dout), static_cast<T*>(dq), static_cast<T*>(dk),
+                       static_cast<T*>(dv), part, n, W, H);
+  else
   hipLaunchKernelGGL((k_xca_bwd<T, D>), dim3(xca_grid(W, H)), dim3(kXcaThreads), 0, stream,
                      reinterpret_cast<const PlanHeader*>(base + lay.header),
                      reinterpret_cast<const int32_t*>(base + lay.perm),
