@@ -93,9 +93,10 @@ def kernel_source_hash():
 
 
 def short_kernel(name):
-    for k in ("k_sla_bwd", "k_sla_fwd", "k_sort", "k_merge", "k_plan", "k_cwi_tiled", "k_cwi_fwd",
-              "k_cwi_dw_reduce", "k_cwi_dw", "k_cwi_map", "k_cwi_clear", "k_xca_fwd", "k_xca_bwd",
-              "k_xca_dtau"):
+    for k in ("k_sla_bwd", "k_sla_fwd_proj", "k_sla_fwd", "k_sort", "k_merge", "k_plan", "k_cwi_tiled",
+              "k_cwi_fwd", "k_cwi_dw_reduce", "k_cwi_dw", "k_cwi_map", "k_cwi_clear", "k_xca_fwd_mma",
+              "k_xca_bwd_mma", "k_xca_fwd", "k_xca_bwd", "k_xca_dtau", "k_out_proj", "k_rows_gemm",
+              "k_wgrad_reduce", "k_wgrad", "k_prep"):
         if k in name:
             return k
     if "copyBuffer" in name:    # the runtime's device-to-device copy kernel

@@ -229,6 +229,28 @@ struct Frag {
   }
 };
 
+// Columns c0 .. c0 + 15 of 32 consecutive 16-bit rows in LDS (`rows` points at
+// the first, row stride `ld` elements, 8-byte aligned rows) as the operand of a
+// contraction over the rows: slot r of lane (i, g) holds row 8g + r, column
+// c0 + i.  Two LDS transpose loads (ds_read_b64_tr_b16): in each group of 16
+// lanes, lane i addresses row 8g + 4h + i / 4 at columns c0 + 4 (i % 4) .. + 3
+// and receives column c0 + i of rows 8g + 4h .. 8g + 4h + 3 (the lane layout
+// measured by an in-bounds probe of the instruction).
+template <typename T>
+__device__ __forceinline__ Raw<T, 8> lds_cols(const unsigned short* rows, int ld, int c0, int i, int g) {
+  typedef short v4s __attribute__((ext_vector_type(4)));
+  const unsigned short* p = rows + (8 * g + (i >> 2)) * ld + c0 + 4 * (i & 3);
+  const v4s a = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4s*)(p));
+  const v4s b = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4s*)(p + 4 * ld));
+  Raw<T, 8> r;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    r[j] = (unsigned short)a[j];
+    r[4 + j] = (unsigned short)b[j];
+  }
+  return r;
+}
+
 // 8-slot operand from two 4-row result tiles (rows 4g..4g+3 of two sub-tiles).
 template <typename T>
 __device__ __forceinline__ Raw<T, 8> pack_rows(floatx4 lo, floatx4 hi) {

@@ -17,9 +17,9 @@
 //                   output is a row of the input times a weight matrix held in LDS;
 //   (SLA backward)  dq, dk, dv;
 //   k_rows_gemm     dx = [dq | dk | dv] W_qkv (zero for rows in no window);
-//   k_wgrad         per group of sorted rows, partial dW_qkv, dW_o and the bias
-//                   gradients: sums over rows on the matrix cores, after the rows
-//                   are turned into contraction operands (0/1 selection products);
+//   k_wgrad         per group of rows, partial dW_qkv, dW_o and the bias
+//                   gradients: sums over rows on the matrix cores, the staged rows
+//                   read as contraction operands by LDS transpose loads;
 //   k_wgrad_reduce  the groups' partials summed in group order.
 // Rows are visited in their own order, rows in no window masked out; every sum
 // over rows has a fixed order, so the results do not depend on scheduling.
@@ -226,10 +226,9 @@ __global__ __launch_bounds__(kRowGemmThreads) void k_rows_gemm(RowGemmArgs ga) {
 // A workgroup of 8 waves takes 8 units of one kind (C / 32 x C / 64 of them per
 // kind) and walks its rows 32 at a time: the rows of A and B are staged in LDS
 // once (rows in no window stored as zeros), the next job's rows loaded into
-// registers while this one is summed; each wave reads its 32-column blocks as
-// row fragments, turns them into operands of a contraction over rows (0/1
-// selection products, as the attention's state sums) and accumulates its 2 x 4
-// result tiles.
+// registers while this one is summed; each wave reads its columns as operands of
+// a contraction over the job's rows with LDS transpose loads and accumulates its
+// 2 x 4 result tiles.
 struct WgradArgs {
   const void* mats[6];   // dq, dk, dv, x, dy, o [n, C]
   const PlanHeader* hdr;
@@ -269,7 +268,6 @@ __global__ __launch_bounds__(kWgradThreads) void k_wgrad(WgradArgs wa) {
   const T* B = static_cast<const T*>(wa.mats[kind == 3 ? 5 : 3]);
   const int32_t p0 = (int32_t)((int64_t)wa.n * grp / wa.groups);
   const int32_t p1 = (int32_t)((int64_t)wa.n * (grp + 1) / wa.groups);
-  const Sel<T, 32> sel(i, g);
   float one8[8] = {1.f, 1.f, 1.f, 1.f, 1.f, 1.f, 1.f, 1.f};
   const Raw<T, 8> ones = F::from_f32(one8);
   floatx4 acc[2][2 * NCB], bacc[2];
@@ -279,9 +277,6 @@ __global__ __launch_bounds__(kWgradThreads) void k_wgrad(WgradArgs wa) {
 #pragma unroll
     for (int ct = 0; ct < 2 * NCB; ++ct) acc[et][ct] = zero;
   }
-  auto rows_of = [&](const Raw<T, 8>(&x)[2], int t) -> Raw<T, 8> {
-    return pack_rows<T>(F::mma(x[0], sel.m[t], zero), F::mma(x[1], sel.m[t], zero));
-  };
   // staging: 32 rows x 2C / 8 pieces of 16 bytes, SP a thread
   const int per_mat = C / 8, pieces_per_row = 2 * per_mat;
   const int npieces = 32 * pieces_per_row;
@@ -327,33 +322,23 @@ __global__ __launch_bounds__(kWgradThreads) void k_wgrad(WgradArgs wa) {
     if (more) load_job(base + 32);
     const T* cur = stage + buf * 32 * LDR;
     if (active) {
-      Raw<T, 8> fa[2];
-#pragma unroll
-      for (int s = 0; s < 2; ++s) {
-        fa[s] = *reinterpret_cast<const Raw<T, 8>*>(cur + (16 * s + i) * LDR + m0 + 8 * g);
-        RowIO<T, 32>::arrange(fa[s]);
-      }
+      // the job's columns as operands of the contraction over its 32 rows,
+      // straight from the staged rows (LDS transpose loads)
+      const unsigned short* cu = reinterpret_cast<const unsigned short*>(cur);
       Raw<T, 8> pa[2];
 #pragma unroll
       for (int et = 0; et < 2; ++et) {
-        pa[et] = rows_of(fa, et);
+        pa[et] = lds_cols<T>(cu, LDR, m0 + 16 * et, i, g);
         bacc[et] = F::mma(pa[et], ones, bacc[et]);
       }
 #pragma unroll
-      for (int cb = 0; cb < NCB; ++cb) {
-        Raw<T, 8> fb[2];
-#pragma unroll
-        for (int s = 0; s < 2; ++s) {
-          fb[s] = *reinterpret_cast<const Raw<T, 8>*>(cur + (16 * s + i) * LDR + C + n0 + 32 * cb + 8 * g);
-          RowIO<T, 32>::arrange(fb[s]);
-        }
+      for (int cb = 0; cb < NCB; ++cb)
 #pragma unroll
         for (int ct = 0; ct < 2; ++ct) {
-          const Raw<T, 8> pb = rows_of(fb, ct);
+          const Raw<T, 8> pb = lds_cols<T>(cu, LDR, C + n0 + 32 * cb + 16 * ct, i, g);
 #pragma unroll
           for (int et = 0; et < 2; ++et) acc[et][2 * cb + ct] = F::mma(pa[et], pb, acc[et][2 * cb + ct]);
         }
-      }
     }
     if (more) store_job(stage + (buf ^ 1) * 32 * LDR);
     buf ^= 1;

@@ -281,36 +281,13 @@ __global__ __launch_bounds__(kXcaThreads) void k_xca_fwd(
 //      v's row r are read as they lie (16 bytes a lane); wave w forms the 16-row
 //      tile w of a 64-row block for both halves of d, and lane (i, g) receives
 //      o[row 16w + i][16t + 4g .. + 3].
-template <typename T>
-struct XcaTr;
-template <>
-struct XcaTr<_Float16> {
-  typedef short v4s __attribute__((ext_vector_type(4)));
-};
-template <>
-struct XcaTr<bf16_t> {
-  typedef short v4s __attribute__((ext_vector_type(4)));
-};
-
 // Columns 16t .. 16t + 15 of rows base .. base + 31 of a staged block as an
 // operand of a contraction over the rows (slot r of lane (i, g): row base + 8g + r,
-// column 16t + i).
+// column 16t + i), by LDS transpose loads.
 template <typename T, int LDH>
 __device__ __forceinline__ Raw<T, 8> xca_cols(const unsigned short (*s)[LDH], int base, int t, int i,
                                               int g) {
-  using V = typename XcaTr<T>::v4s;
-  const int c = 16 * t + 4 * (i & 3);
-  const V a = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-      (__attribute__((address_space(3))) V*)(&s[base + 8 * g + (i >> 2)][c]));
-  const V b = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-      (__attribute__((address_space(3))) V*)(&s[base + 8 * g + 4 + (i >> 2)][c]));
-  Raw<T, 8> r;
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    r[j] = (unsigned short)a[j];
-    r[4 + j] = (unsigned short)b[j];
-  }
-  return r;
+  return lds_cols<T>(&s[base][0], LDH, 16 * t, i, g);
 }
 
 template <typename T>
