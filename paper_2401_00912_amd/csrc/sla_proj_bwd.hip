@@ -255,9 +255,14 @@ __global__ __launch_bounds__(kWgradThreads) void k_wgrad(WgradArgs wa) {
   const int tid = threadIdx.x, lane = lane_id(), wv = tid >> 6;
   const int i = lane & 15, g = lane >> 4;
   const int32_t per_group = 4 * wa.wgs_per_kind;
-  const int32_t grp = (int32_t)blockIdx.x / per_group;
-  const int kind = ((int32_t)blockIdx.x % per_group) / wa.wgs_per_kind;
-  const int part_of_kind = ((int32_t)blockIdx.x % per_group) % wa.wgs_per_kind;
+  // the workgroups of one group are 8 ids apart: workgroups are dealt to the 8
+  // XCDs in turn, so they share one XCD and its L2, which serves x to the three
+  // kinds that read it (the grid is padded to whole blocks of 8 groups)
+  const int32_t hi = (int32_t)blockIdx.x >> 3;
+  const int32_t grp = (hi / per_group) * 8 + ((int32_t)blockIdx.x & 7);
+  if (grp >= wa.groups) return;
+  const int kind = (hi % per_group) / wa.wgs_per_kind;
+  const int part_of_kind = (hi % per_group) % wa.wgs_per_kind;
   const int chunks = C / kWgradChunk;
   const int units = (C / 32) * chunks;
   const int unit = part_of_kind * NWV + wv;
@@ -574,7 +579,7 @@ static hipError_t projected_backward_t(const void* plan, int32_t n, int32_t W, i
                              : reinterpret_cast<const void*>(&k_wgrad<T, 1>);
   if ((e = hipFuncSetAttribute(wk, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024 - 1024)) != hipSuccess)
     return e;
-  const dim3 wg((unsigned)((int64_t)L.groups * 4 * wa.wgs_per_kind));
+  const dim3 wg((unsigned)(((int64_t)L.groups + 7) / 8 * 8 * 4 * wa.wgs_per_kind));
   if (C == 256) hipLaunchKernelGGL((k_wgrad<T, 4>), wg, dim3(kWgradThreads), wlds, stream, wa);
   else if (C == 128) hipLaunchKernelGGL((k_wgrad<T, 2>), wg, dim3(kWgradThreads), wlds, stream, wa);
   else hipLaunchKernelGGL((k_wgrad<T, 1>), wg, dim3(kWgradThreads), wlds, stream, wa);
