@@ -225,10 +225,10 @@ __global__ __launch_bounds__(kRowGemmThreads) void k_rows_gemm(RowGemmArgs ga) {
 //
 // A workgroup of 8 waves takes 8 units of one kind (C / 32 x C / 64 of them per
 // kind) and walks its rows 32 at a time: the rows of A and B are staged in LDS
-// once (rows in no window stored as zeros), the next job's rows loaded into
-// registers while this one is summed; each wave reads its columns as operands of
-// a contraction over the job's rows with LDS transpose loads and accumulates its
-// 2 x 4 result tiles.
+// once (rows in no window stored as zeros), the next two jobs' rows (one for
+// C = 256) loaded into registers while this one is summed; each wave reads its
+// columns as operands of a contraction over the job's rows with LDS transpose
+// loads and accumulates its 2 x 4 result tiles.
 struct WgradArgs {
   const void* mats[6];   // dq, dk, dv, x, dy, o [n, C]
   const PlanHeader* hdr;
@@ -286,68 +286,100 @@ __global__ __launch_bounds__(kWgradThreads) void k_wgrad(WgradArgs wa) {
   const int per_mat = C / 8, pieces_per_row = 2 * per_mat;
   const int npieces = 32 * pieces_per_row;
   // the data and the row's mask byte are loaded together; rows in no window
-  // are zeroed when stored
-  uint4 held[SP];
-  int keep[SP];
-  auto load_job = [&](int32_t base) {
+  // are zeroed when stored.  For C <= 128 two jobs are in flight in registers
+  // (sets a and b) while a third is summed from LDS; for C = 256 one.
+  struct Held {
+    uint4 v[SP];
+    int keep[SP];
+  };
+  auto load_job = [&](Held& h, int32_t base) {
 #pragma unroll
     for (int k = 0; k < SP; ++k) {
       const int idx = tid + k * kWgradThreads;
-      held[k] = make_uint4(0, 0, 0, 0);
-      keep[k] = 0;
+      h.v[k] = make_uint4(0, 0, 0, 0);
+      h.keep[k] = 0;
       if (idx < npieces) {
         const int r = idx / pieces_per_row, pc = idx - r * pieces_per_row;
         const int32_t row = base + r;
         const T* src = pc < per_mat ? A + 8 * pc : B + 8 * (pc - per_mat);
         if (row < p1) {
-          keep[k] = wa.mask[row];
-          held[k] = *reinterpret_cast<const uint4*>(src + (size_t)row * C);
+          h.keep[k] = wa.mask[row];
+          h.v[k] = *reinterpret_cast<const uint4*>(src + (size_t)row * C);
         }
       }
     }
   };
-  auto store_job = [&](T* buf) {
+  auto store_job = [&](const Held& h, T* buf) {
 #pragma unroll
     for (int k = 0; k < SP; ++k) {
       const int idx = tid + k * kWgradThreads;
       if (idx < npieces) {
         const int r = idx / pieces_per_row, pc = idx - r * pieces_per_row;
-        *reinterpret_cast<uint4*>(buf + r * LDR + 8 * pc) = keep[k] != 0 ? held[k] : make_uint4(0, 0, 0, 0);
+        *reinterpret_cast<uint4*>(buf + r * LDR + 8 * pc) = h.keep[k] != 0 ? h.v[k] : make_uint4(0, 0, 0, 0);
       }
     }
   };
-  int buf = 0;
-  if (p0 < p1) {
-    load_job(p0);
-    store_job(stage);
-  }
-  __syncthreads();
-  for (int32_t base = p0; base < p1; base += 32) {
-    const bool more = base + 32 < p1;
-    if (more) load_job(base + 32);
-    const T* cur = stage + buf * 32 * LDR;
-    if (active) {
-      // the job's columns as operands of the contraction over its 32 rows,
-      // straight from the staged rows (LDS transpose loads)
-      const unsigned short* cu = reinterpret_cast<const unsigned short*>(cur);
-      Raw<T, 8> pa[2];
+  // one job's contraction over its 32 rows, its columns read straight from the
+  // staged rows (LDS transpose loads)
+  auto sum_job = [&](const T* cur) {
+    if (!active) return;
+    const unsigned short* cu = reinterpret_cast<const unsigned short*>(cur);
+    Raw<T, 8> pa[2];
 #pragma unroll
-      for (int et = 0; et < 2; ++et) {
-        pa[et] = lds_cols<T>(cu, LDR, m0 + 16 * et, i, g);
-        bacc[et] = F::mma(pa[et], ones, bacc[et]);
-      }
-#pragma unroll
-      for (int cb = 0; cb < NCB; ++cb)
-#pragma unroll
-        for (int ct = 0; ct < 2; ++ct) {
-          const Raw<T, 8> pb = lds_cols<T>(cu, LDR, C + n0 + 32 * cb + 16 * ct, i, g);
-#pragma unroll
-          for (int et = 0; et < 2; ++et) acc[et][2 * cb + ct] = F::mma(pa[et], pb, acc[et][2 * cb + ct]);
-        }
+    for (int et = 0; et < 2; ++et) {
+      pa[et] = lds_cols<T>(cu, LDR, m0 + 16 * et, i, g);
+      bacc[et] = F::mma(pa[et], ones, bacc[et]);
     }
-    if (more) store_job(stage + (buf ^ 1) * 32 * LDR);
-    buf ^= 1;
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb)
+#pragma unroll
+      for (int ct = 0; ct < 2; ++ct) {
+        const Raw<T, 8> pb = lds_cols<T>(cu, LDR, C + n0 + 32 * cb + 16 * ct, i, g);
+#pragma unroll
+        for (int et = 0; et < 2; ++et) acc[et][2 * cb + ct] = F::mma(pa[et], pb, acc[et][2 * cb + ct]);
+      }
+  };
+  T* const st0 = stage;
+  T* const st1 = stage + 32 * LDR;
+  if constexpr (SP <= 2) {
+    Held ha, hb;
+    if (p0 < p1) {
+      load_job(ha, p0);
+      store_job(ha, st0);
+    }
+    // a job past the group's rows loads nothing
+    load_job(ha, p0 + 32);
+    load_job(hb, p0 + 64);
     __syncthreads();
+    // jobs base (in st0), base + 32 (set a), base + 64 (set b)
+    for (int32_t base = p0; base < p1; base += 64) {
+      sum_job(st0);
+      if (base + 32 < p1) store_job(ha, st1);
+      load_job(ha, base + 96);
+      __syncthreads();
+      if (base + 32 >= p1) break;
+      sum_job(st1);
+      if (base + 64 < p1) store_job(hb, st0);
+      load_job(hb, base + 128);
+      __syncthreads();
+    }
+  } else {
+    // C = 256: a second set would cost a workgroup per CU; one job in flight
+    Held ha;
+    int buf = 0;
+    if (p0 < p1) {
+      load_job(ha, p0);
+      store_job(ha, st0);
+    }
+    __syncthreads();
+    for (int32_t base = p0; base < p1; base += 32) {
+      const bool more = base + 32 < p1;
+      if (more) load_job(ha, base + 32);
+      sum_job(buf ? st1 : st0);
+      if (more) store_job(ha, buf ? st0 : st1);
+      buf ^= 1;
+      __syncthreads();
+    }
   }
   if (!active) return;
   // tile (et, ct): lane (c, g) component j is gradient entry
