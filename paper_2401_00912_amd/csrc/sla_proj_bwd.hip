@@ -240,7 +240,13 @@ struct WgradArgs {
 constexpr int kWgradThreads = 512;
 constexpr int kWgradChunk = 64;    // gradient columns per unit
 
-// SP: 16-byte pieces a thread stages per job, 32 x 2C / 8 / 512 (C = 64, 128, 256)
+// A columns a workgroup stages: its 8 units span 8 / (C / 64) slabs of 32.
+__host__ __device__ constexpr int wgrad_a_cols(int C) {
+  return C < (kWgradThreads / 64) * 32 * kWgradChunk / C ? C : (kWgradThreads / 64) * 32 * kWgradChunk / C;
+}
+
+// SP: 16-byte pieces a thread stages per job, at most 32 (na + C) / 8 / 512:
+// 1, 2, 3 for C = 64, 128, 256
 template <typename T, int SP>
 __global__ __launch_bounds__(kWgradThreads) void k_wgrad(WgradArgs wa) {
   using F = Frag<T, 8>;
@@ -250,8 +256,6 @@ __global__ __launch_bounds__(kWgradThreads) void k_wgrad(WgradArgs wa) {
   if (wa.hdr->magic != kPlanMagic || wa.hdr->n != wa.n || wa.hdr->num_windows != wa.W) return;
   extern __shared__ __attribute__((aligned(16))) unsigned char lds_raw[];
   const int C = wa.C;
-  const int LDR = 2 * C + 8;                 // staged row: A then B, padded
-  T* stage = reinterpret_cast<T*>(lds_raw);   // [2][32][LDR]
   const int tid = threadIdx.x, lane = lane_id(), wv = tid >> 6;
   const int i = lane & 15, g = lane >> 4;
   const int32_t per_group = 4 * wa.wgs_per_kind;
@@ -269,6 +273,12 @@ __global__ __launch_bounds__(kWgradThreads) void k_wgrad(WgradArgs wa) {
   const bool active = unit < units;
   const int slab = active ? unit / chunks : 0, chunk = active ? unit % chunks : 0;
   const int m0 = 32 * slab, n0 = kWgradChunk * chunk;
+  // the workgroup's units cover A's columns a0 .. a0 + na - 1 (all of them for
+  // C <= 128, a quarter for C = 256) and all of B's: only those are staged
+  const int na = wgrad_a_cols(C);
+  const int a0 = (part_of_kind * NWV / chunks) * 32;
+  const int LDR = na + C + 8;                // staged row: A's columns then B's, padded
+  T* stage = reinterpret_cast<T*>(lds_raw);   // [2][32][LDR]
   const T* A = static_cast<const T*>(wa.mats[kind == 3 ? 4 : kind]);
   const T* B = static_cast<const T*>(wa.mats[kind == 3 ? 5 : 3]);
   const int32_t p0 = (int32_t)((int64_t)wa.n * grp / wa.groups);
@@ -282,8 +292,8 @@ __global__ __launch_bounds__(kWgradThreads) void k_wgrad(WgradArgs wa) {
 #pragma unroll
     for (int ct = 0; ct < 2 * NCB; ++ct) acc[et][ct] = zero;
   }
-  // staging: 32 rows x 2C / 8 pieces of 16 bytes, SP a thread
-  const int per_mat = C / 8, pieces_per_row = 2 * per_mat;
+  // staging: 32 rows x (na + C) / 8 pieces of 16 bytes, at most SP a thread
+  const int per_mat = na / 8, pieces_per_row = per_mat + C / 8;
   const int npieces = 32 * pieces_per_row;
   // the data and the row's mask byte are loaded together; rows in no window
   // are zeroed when stored.  For C <= 128 two jobs are in flight in registers
@@ -301,7 +311,7 @@ __global__ __launch_bounds__(kWgradThreads) void k_wgrad(WgradArgs wa) {
       if (idx < npieces) {
         const int r = idx / pieces_per_row, pc = idx - r * pieces_per_row;
         const int32_t row = base + r;
-        const T* src = pc < per_mat ? A + 8 * pc : B + 8 * (pc - per_mat);
+        const T* src = pc < per_mat ? A + a0 + 8 * pc : B + 8 * (pc - per_mat);
         if (row < p1) {
           h.keep[k] = wa.mask[row];
           h.v[k] = *reinterpret_cast<const uint4*>(src + (size_t)row * C);
@@ -327,14 +337,14 @@ __global__ __launch_bounds__(kWgradThreads) void k_wgrad(WgradArgs wa) {
     Raw<T, 8> pa[2];
 #pragma unroll
     for (int et = 0; et < 2; ++et) {
-      pa[et] = lds_cols<T>(cu, LDR, m0 + 16 * et, i, g);
+      pa[et] = lds_cols<T>(cu, LDR, m0 - a0 + 16 * et, i, g);
       bacc[et] = F::mma(pa[et], ones, bacc[et]);
     }
 #pragma unroll
     for (int cb = 0; cb < NCB; ++cb)
 #pragma unroll
       for (int ct = 0; ct < 2; ++ct) {
-        const Raw<T, 8> pb = lds_cols<T>(cu, LDR, C + n0 + 32 * cb + 16 * ct, i, g);
+        const Raw<T, 8> pb = lds_cols<T>(cu, LDR, na + n0 + 32 * cb + 16 * ct, i, g);
 #pragma unroll
         for (int et = 0; et < 2; ++et) acc[et][2 * cb + ct] = F::mma(pa[et], pb, acc[et][2 * cb + ct]);
       }
@@ -605,14 +615,14 @@ static hipError_t projected_backward_t(const void* plan, int32_t n, int32_t W, i
   wa.groups = L.groups;
   const int units = (C / 32) * (C / kWgradChunk);
   wa.wgs_per_kind = (units + kWgradThreads / 64 - 1) / (kWgradThreads / 64);
-  const size_t wlds = (size_t)2 * 32 * (2 * C + 8) * 2;
-  const void* wk = C == 256 ? reinterpret_cast<const void*>(&k_wgrad<T, 4>)
+  const size_t wlds = (size_t)2 * 32 * (wgrad_a_cols(C) + C + 8) * 2;
+  const void* wk = C == 256 ? reinterpret_cast<const void*>(&k_wgrad<T, 3>)
                   : C == 128 ? reinterpret_cast<const void*>(&k_wgrad<T, 2>)
                              : reinterpret_cast<const void*>(&k_wgrad<T, 1>);
   if ((e = hipFuncSetAttribute(wk, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024 - 1024)) != hipSuccess)
     return e;
   const dim3 wg((unsigned)(((int64_t)L.groups + 7) / 8 * 8 * 4 * wa.wgs_per_kind));
-  if (C == 256) hipLaunchKernelGGL((k_wgrad<T, 4>), wg, dim3(kWgradThreads), wlds, stream, wa);
+  if (C == 256) hipLaunchKernelGGL((k_wgrad<T, 3>), wg, dim3(kWgradThreads), wlds, stream, wa);
   else if (C == 128) hipLaunchKernelGGL((k_wgrad<T, 2>), wg, dim3(kWgradThreads), wlds, stream, wa);
   else hipLaunchKernelGGL((k_wgrad<T, 1>), wg, dim3(kWgradThreads), wlds, stream, wa);
   if ((e = hipGetLastError()) != hipSuccess) return e;
