@@ -97,9 +97,12 @@ __global__ __launch_bounds__(256) void k_prep(PrepArgs pa) {
 // out[j / C][row][j % C].  Rows in no window (mask 0) get zero input, so their
 // outputs are the bias (zero when there is none).
 //
-// A workgroup of 16 waves keeps the weight rows of NB output columns (blockIdx.y
-// selects them; all N when they fit) in LDS, padded rows of K + 8 elements, and
-// walks 16-row tiles, one per wave.  When K <= 32 KBH a wave reads its tile's
+// A workgroup of 16 waves keeps the weight rows of NB output columns (all N when
+// they fit) in LDS, padded rows of K + 8 elements, and walks 16-row tiles, one
+// per wave.  When N takes several column blocks, the workgroups of one row range
+// sit 8 ids apart: workgroups are dealt to the 8 XCDs in turn, so the column
+// blocks of a row range share one XCD, and its L2 serves their common input
+// rows (with several column blocks the grid's row ranges are a multiple of 8).  When K <= 32 KBH a wave reads its tile's
 // input once into registers and forms every 16 NBT-column sub-block from them;
 // otherwise it reads the input again per sub-block.  With the weight rows as the
 // first matrix-core operand and the input rows (16-byte pieces of 8 channels) as
@@ -126,7 +129,11 @@ __global__ __launch_bounds__(kRowGemmThreads) void k_rows_gemm(RowGemmArgs ga) {
   const int K = ga.K, LDW = K + 8, C = ga.C, NB = ga.NB;
   T* s_w = reinterpret_cast<T*>(lds_raw);
   float* s_b = reinterpret_cast<float*>(s_w + NB * LDW);
-  const int32_t n0 = (int32_t)blockIdx.y * NB;
+  const int32_t cols = ga.N / NB;
+  const int32_t hi = (int32_t)blockIdx.x >> 3;
+  const int32_t rb = (hi / cols) * 8 + ((int32_t)blockIdx.x & 7);   // row range
+  const int32_t ranges = (int32_t)gridDim.x / cols;
+  const int32_t n0 = (hi % cols) * NB;
   {
     const int pieces = K / 8;
     const T* w = static_cast<const T*>(ga.w);
@@ -146,7 +153,7 @@ __global__ __launch_bounds__(kRowGemmThreads) void k_rows_gemm(RowGemmArgs ga) {
   const int nseg = K / C;
   const bool held = K <= 32 * KBH;
   constexpr int NW = kRowGemmThreads / 64;
-  for (int32_t tile = (int32_t)blockIdx.x * NW + wv; tile * 16 < ga.n; tile += (int32_t)gridDim.x * NW) {
+  for (int32_t tile = rb * NW + wv; tile * 16 < ga.n; tile += ranges * NW) {
     const int32_t p = tile * 16 + i;
     const bool inside = p < ga.n;
     const int32_t row = inside ? p : 0;
@@ -503,18 +510,27 @@ static hipError_t rows_gemm(RowGemmArgs ga, hipStream_t stream) {
   const size_t lds = lds_of(nb);
   const int cols = ga.N / nb;
   const bool small_k = ga.K <= 32 * 4;
-  // about one workgroup per CU, each walking many tiles with its staged weights
+  // at most one workgroup per CU, each walking many tiles with its staged
+  // weights: row ranges a multiple of 8 (see the kernel), and no more
+  // workgroups than CUs, since a workgroup that waits for a free CU would start
+  // its fixed share of the tiles a whole launch late
   const int64_t tiles = ((int64_t)ga.n + 16 * (kRowGemmThreads / 64) - 1) / (16 * (kRowGemmThreads / 64));
-  int64_t gx = (256 + cols - 1) / cols;
-  if (gx > tiles) gx = tiles;
-  if (gx < 1) gx = 1;
+  int64_t gx;
+  if (cols == 1) {
+    gx = tiles < 256 ? tiles : 256;   // one column block: any number of row ranges
+    if (gx < 1) gx = 1;
+  } else {
+    gx = 256 / cols / 8 * 8;
+    if (gx > tiles) gx = (tiles + 7) / 8 * 8;
+    if (gx < 8) gx = 8;
+  }
   const void* kern = wide ? (small_k ? reinterpret_cast<const void*>(&k_rows_gemm<T, 8, 4>)
                                      : reinterpret_cast<const void*>(&k_rows_gemm<T, 8, 12>))
                           : (small_k ? reinterpret_cast<const void*>(&k_rows_gemm<T, 4, 4>)
                                      : reinterpret_cast<const void*>(&k_rows_gemm<T, 4, 12>));
   hipError_t e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024 - 1024);
   if (e != hipSuccess) return e;
-  const dim3 grid((unsigned)gx, (unsigned)cols);
+  const dim3 grid((unsigned)(gx * cols));
   if (wide && small_k) hipLaunchKernelGGL((k_rows_gemm<T, 8, 4>), grid, dim3(kRowGemmThreads), lds, stream, ga);
   else if (wide) hipLaunchKernelGGL((k_rows_gemm<T, 8, 12>), grid, dim3(kRowGemmThreads), lds, stream, ga);
   else if (small_k) hipLaunchKernelGGL((k_rows_gemm<T, 4, 4>), grid, dim3(kRowGemmThreads), lds, stream, ga);
