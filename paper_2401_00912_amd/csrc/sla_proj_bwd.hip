@@ -99,15 +99,16 @@ __global__ __launch_bounds__(256) void k_prep(PrepArgs pa) {
 //
 // A workgroup of 16 waves keeps the weight rows of NB output columns (all N when
 // they fit) in LDS, padded rows of K + 8 elements, and walks 16-row tiles, one
-// per wave.  When N takes several column blocks, the workgroups of one row range
-// sit 8 ids apart: workgroups are dealt to the 8 XCDs in turn, so the column
-// blocks of a row range share one XCD, and its L2 serves their common input
-// rows (with several column blocks the grid's row ranges are a multiple of 8).  When K <= 32 KBH a wave reads its tile's
-// input once into registers and forms every 16 NBT-column sub-block from them;
-// otherwise it reads the input again per sub-block.  With the weight rows as the
-// first matrix-core operand and the input rows (16-byte pieces of 8 channels) as
-// the second, lane (i, g) receives columns 16 t + 4 g .. + 3 of the tile's row i,
-// stored as one 4-element piece.
+// per wave.  When K <= 32 KBH a wave reads its tile's input once into registers
+// and forms every 16 NBT-column sub-block from them; otherwise it reads the
+// input again per sub-block.  With the weight rows as the first matrix-core
+// operand and the input rows (16-byte pieces of 8 channels) as the second, lane
+// (i, g) receives columns 16 t + 4 g .. + 3 of the tile's row i, stored as one
+// 4-element piece.
+// When N takes several column blocks, the workgroups of one row range sit 8 ids
+// apart: workgroups are dealt to the 8 XCDs in turn, so the column blocks of a
+// row range share one XCD, and its L2 serves their common input rows (the
+// grid's row ranges are then a multiple of 8).
 constexpr int kRowGemmThreads = 1024;
 
 struct RowGemmArgs {
@@ -247,9 +248,10 @@ struct WgradArgs {
 constexpr int kWgradThreads = 512;
 constexpr int kWgradChunk = 64;    // gradient columns per unit
 
-// A columns a workgroup stages: its 8 units span 8 / (C / 64) slabs of 32.
+// A columns a workgroup stages: its 8 units (one a wave) cover 8 / (C / 64)
+// slabs of 32 A columns, each with all C / 64 chunks of B's; at most C.
 __host__ __device__ constexpr int wgrad_a_cols(int C) {
-  return C < (kWgradThreads / 64) * 32 * kWgradChunk / C ? C : (kWgradThreads / 64) * 32 * kWgradChunk / C;
+  return (kWgradThreads / 64) / (C / kWgradChunk) * 32 < C ? (kWgradThreads / 64) / (C / kWgradChunk) * 32 : C;
 }
 
 // SP: 16-byte pieces a thread stages per job, at most 32 (na + C) / 8 / 512:
