@@ -101,7 +101,9 @@ __global__ __launch_bounds__(256) void k_prep(PrepArgs pa) {
 // they fit) in LDS, padded rows of K + 8 elements, and walks 16-row tiles, one
 // per wave.  When K <= 32 KBH a wave reads its tile's input once into registers
 // and forms every 16 NBT-column sub-block from them; otherwise it reads the
-// input again per sub-block.  With the weight rows as the first matrix-core
+// input again per sub-block (KBH = 0, for C = 256: a 256-channel segment at a
+// time, the next segment's pieces in flight while one is formed).  With the
+// weight rows as the first matrix-core
 // operand and the input rows (16-byte pieces of 8 channels) as the second, lane
 // (i, g) receives columns 16 t + 4 g .. + 3 of the tile's row i, stored as one
 // 4-element piece.
@@ -161,7 +163,7 @@ __global__ __launch_bounds__(kRowGemmThreads) void k_rows_gemm(RowGemmArgs ga) {
     const bool valid = inside && ga.mask[row] != 0;
     // the tile's input, when it fits in registers: k block kb is channels
     // 32 kb .. + 31 of A, in segment 32 kb / C
-    Raw<T, 8> xh[KBH];
+    Raw<T, 8> xh[KBH > 0 ? KBH : 1];
     if (held) {
 #pragma unroll
       for (int kb = 0; kb < KBH; ++kb) {
@@ -189,6 +191,39 @@ __global__ __launch_bounds__(kRowGemmThreads) void k_rows_gemm(RowGemmArgs ga) {
             const Raw<T, 8> wo = *reinterpret_cast<const Raw<T, 8>*>(wsb + 16 * t * LDW + 32 * kb);
             acc[t] = F8::mma(wo, xh[kb], acc[t]);
           }
+        }
+      } else if constexpr (KBH == 0) {
+        // the input one C-channel segment (C = 256) at a time: all of a
+        // segment's pieces are requested together, the next segment's while
+        // this one is formed
+        constexpr int KS = 8;
+        Raw<T, 8> xs[KS], xn[KS];
+        const T* src0 = static_cast<const T*>(ga.a[0]);
+#pragma unroll
+        for (int kb = 0; kb < KS; ++kb) {
+          xs[kb] = F8::zero();
+          if (valid)
+            xs[kb] = __builtin_bit_cast(
+                Raw<T, 8>, *reinterpret_cast<const uint4*>(elem_at(src0, (uint32_t)row * (uint32_t)C + 32 * kb + 8 * g)));
+        }
+        for (int s = 0; s < nseg; ++s) {
+          const T* srcn = static_cast<const T*>(ga.a[s + 1 < nseg ? s + 1 : s]);
+#pragma unroll
+          for (int kb = 0; kb < KS; ++kb) {
+            xn[kb] = F8::zero();
+            if (valid && s + 1 < nseg)
+              xn[kb] = __builtin_bit_cast(
+                  Raw<T, 8>, *reinterpret_cast<const uint4*>(elem_at(srcn, (uint32_t)row * (uint32_t)C + 32 * kb + 8 * g)));
+          }
+#pragma unroll
+          for (int kb = 0; kb < KS; ++kb)
+#pragma unroll
+            for (int t = 0; t < NBT; ++t) {
+              const Raw<T, 8> wo = *reinterpret_cast<const Raw<T, 8>*>(wsb + 16 * t * LDW + s * C + 32 * kb);
+              acc[t] = F8::mma(wo, xs[kb], acc[t]);
+            }
+#pragma unroll
+          for (int kb = 0; kb < KS; ++kb) xs[kb] = xn[kb];
         }
       } else {
         for (int s = 0; s < nseg; ++s) {
@@ -526,17 +561,20 @@ static hipError_t rows_gemm(RowGemmArgs ga, hipStream_t stream) {
     if (gx > tiles) gx = (tiles + 7) / 8 * 8;
     if (gx < 8) gx = 8;
   }
-  const void* kern = wide ? (small_k ? reinterpret_cast<const void*>(&k_rows_gemm<T, 8, 4>)
-                                     : reinterpret_cast<const void*>(&k_rows_gemm<T, 8, 12>))
-                          : (small_k ? reinterpret_cast<const void*>(&k_rows_gemm<T, 4, 4>)
-                                     : reinterpret_cast<const void*>(&k_rows_gemm<T, 4, 12>));
-  hipError_t e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024 - 1024);
+  // the input held in registers for K <= 128 or K <= 384, else streamed a
+  // segment at a time (K = 3C with C = 256)
+  // (128 weight rows of K > 592 exceed the LDS cap, so a streamed product is
+  // never wide)
+  const bool streamed = ga.K > 32 * 12;
+  if (streamed && (wide || ga.C > 256 || ga.C % 32 != 0)) return hipErrorInvalidValue;
+  void (*kern)(RowGemmArgs) =
+      streamed ? &k_rows_gemm<T, 4, 0>
+      : wide ? (small_k ? &k_rows_gemm<T, 8, 4> : &k_rows_gemm<T, 8, 12>)
+             : (small_k ? &k_rows_gemm<T, 4, 4> : &k_rows_gemm<T, 4, 12>);
+  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024 - 1024);
   if (e != hipSuccess) return e;
-  const dim3 grid((unsigned)(gx * cols));
-  if (wide && small_k) hipLaunchKernelGGL((k_rows_gemm<T, 8, 4>), grid, dim3(kRowGemmThreads), lds, stream, ga);
-  else if (wide) hipLaunchKernelGGL((k_rows_gemm<T, 8, 12>), grid, dim3(kRowGemmThreads), lds, stream, ga);
-  else if (small_k) hipLaunchKernelGGL((k_rows_gemm<T, 4, 4>), grid, dim3(kRowGemmThreads), lds, stream, ga);
-  else hipLaunchKernelGGL((k_rows_gemm<T, 4, 12>), grid, dim3(kRowGemmThreads), lds, stream, ga);
+  hipLaunchKernelGGL(kern, dim3((unsigned)(gx * cols)), dim3(kRowGemmThreads), lds, stream, ga);
   return hipGetLastError();
 }
 
