@@ -105,8 +105,9 @@ __global__ __launch_bounds__(256) void k_prep(PrepArgs pa) {
 // time, the next segment's pieces in flight while one is formed).  With the
 // weight rows as the first matrix-core
 // operand and the input rows (16-byte pieces of 8 channels) as the second, lane
-// (i, g) receives columns 16 t + 4 g .. + 3 of the tile's row i, stored as one
-// 4-element piece.
+// (i, g) receives 4 columns of the tile's row i from each tile; the weight rows
+// are staged in an order that makes a tile pair's 8 columns of a lane
+// consecutive, stored as one 16-byte piece.
 // When N takes several column blocks, the workgroups of one row range sit 8 ids
 // apart: workgroups are dealt to the 8 XCDs in turn, so the column blocks of a
 // row range share one XCD, and its L2 serves their common input rows (the
@@ -138,15 +139,20 @@ __global__ __launch_bounds__(kRowGemmThreads) void k_rows_gemm(RowGemmArgs ga) {
   const int32_t ranges = (int32_t)gridDim.x / cols;
   const int32_t n0 = (hi % cols) * NB;
   {
+    // output column jj of the block is matrix-core row pi(jj): within each 32
+    // columns, column 8 g + 4 v + j is row 16 v + 4 g + j (tile v of the pair),
+    // so that lane (i, g) receives columns 8 g .. 8 g + 7 of a tile pair and
+    // stores them as one 16-byte piece
+    auto pi = [](int jj) { return (jj & ~31) | ((jj & 4) << 2) | ((jj & 24) >> 1) | (jj & 3); };
     const int pieces = K / 8;
     const T* w = static_cast<const T*>(ga.w);
     for (int idx = threadIdx.x; idx < NB * pieces; idx += blockDim.x) {
       const int jj = idx / pieces, pc = idx - jj * pieces;
-      *reinterpret_cast<uint4*>(s_w + jj * LDW + 8 * pc) =
+      *reinterpret_cast<uint4*>(s_w + pi(jj) * LDW + 8 * pc) =
           *reinterpret_cast<const uint4*>(w + (size_t)(n0 + jj) * K + 8 * pc);
     }
     const unsigned short* b = static_cast<const unsigned short*>(ga.bias);
-    for (int jj = threadIdx.x; jj < NB; jj += blockDim.x) s_b[jj] = b ? u16_to_f32<T>(b[n0 + jj]) : 0.f;
+    for (int jj = threadIdx.x; jj < NB; jj += blockDim.x) s_b[pi(jj)] = b ? u16_to_f32<T>(b[n0 + jj]) : 0.f;
   }
   __syncthreads();
   using F8 = Frag<T, 8>;
@@ -243,15 +249,19 @@ __global__ __launch_bounds__(kRowGemmThreads) void k_rows_gemm(RowGemmArgs ga) {
       if (!inside) continue;
       const int32_t j0 = n0 + sb;   // a sub-block lies in one output segment (C % SB == 0)
       T* outp = static_cast<T*>(ga.out[j0 / C]);
-      T* dst = elem_at(outp, (uint32_t)row * (uint32_t)C + (uint32_t)(j0 % C) + 4 * g);
+      T* dst = elem_at(outp, (uint32_t)row * (uint32_t)C + (uint32_t)(j0 % C) + 8 * g);
 #pragma unroll
-      for (int t = 0; t < NBT; ++t) {
-        const float4 bias = *reinterpret_cast<const float4*>(s_b + sb + 16 * t + 4 * g);
-        float f[4] = {acc[t][0] + bias.x, acc[t][1] + bias.y, acc[t][2] + bias.z, acc[t][3] + bias.w};
-        u16x4 pk;
+      for (int u = 0; u < NBT / 2; ++u) {
+        float f[8];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) pk[j] = f32_to_u16<T>(f[j]);
-        *reinterpret_cast<u16x4*>(dst + 16 * t) = pk;
+        for (int v = 0; v < 2; ++v) {
+          const float4 bias = *reinterpret_cast<const float4*>(s_b + sb + 16 * (2 * u + v) + 4 * g);
+          f[4 * v + 0] = acc[2 * u + v][0] + bias.x;
+          f[4 * v + 1] = acc[2 * u + v][1] + bias.y;
+          f[4 * v + 2] = acc[2 * u + v][2] + bias.z;
+          f[4 * v + 3] = acc[2 * u + v][3] + bias.w;
+        }
+        *reinterpret_cast<Raw<T, 8>*>(dst + 32 * u) = F8::from_f32(f);
       }
     }
   }
