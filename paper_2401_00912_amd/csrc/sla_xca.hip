@@ -402,11 +402,15 @@ __global__ __launch_bounds__(kXcaThreads) void k_xca_fwd_mma(
   __syncthreads();
 
   // 3. o = v A^T, tile wv of each 64-row block
+  // tile t2's operand row i is A's row 8 (i / 4) + 4 t2 + i % 4, so that lane
+  // (i, g) receives columns 8 g .. 8 g + 7 of o over the two tiles and stores
+  // them as one 16-byte piece
   Raw<T, 8> pa[2], pl[2];
 #pragma unroll
   for (int t2 = 0; t2 < 2; ++t2) {
-    pa[t2] = *reinterpret_cast<const Raw<T, 8>*>(&s_p[0][16 * t2 + i][8 * g]);
-    if constexpr (kPair) pl[t2] = *reinterpret_cast<const Raw<T, 8>*>(&s_p[kPair ? 1 : 0][16 * t2 + i][8 * g]);
+    const int e = 8 * (i >> 2) + 4 * t2 + (i & 3);
+    pa[t2] = *reinterpret_cast<const Raw<T, 8>*>(&s_p[0][e][8 * g]);
+    if constexpr (kPair) pl[t2] = *reinterpret_cast<const Raw<T, 8>*>(&s_p[kPair ? 1 : 0][e][8 * g]);
   }
   for (int32_t p0 = rb; p0 < re; p0 += kXcaRows) {
     const int nr = min(kXcaRows, re - p0);
@@ -421,17 +425,15 @@ __global__ __launch_bounds__(kXcaThreads) void k_xca_fwd_mma(
     if (16 * wv >= nr) continue;   // the whole tile is past the block's rows
     const Raw<T, 8> vb = *reinterpret_cast<const Raw<T, 8>*>(&s_v[r][8 * g]);
     const int32_t row = r < nr ? s_row[r] : -1;
+    float f[8];
 #pragma unroll
     for (int t2 = 0; t2 < 2; ++t2) {
       floatx4 d4 = F::mma(pa[t2], vb, zero);
       if constexpr (kPair) d4 = F::mma(pl[t2], vb, d4);
-      if (row >= 0) {
-        u16x4 pk;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) pk[j] = f32_to_u16<T>(d4[j]);
-        *reinterpret_cast<u16x4*>(o + (size_t)row * rs + col + 16 * t2 + 4 * g) = pk;
-      }
+      for (int j = 0; j < 4; ++j) f[4 * t2 + j] = d4[j];
     }
+    if (row >= 0) *reinterpret_cast<Raw<T, 8>*>(o + (size_t)row * rs + col + 8 * g) = F::from_f32(f);
   }
 }
 
