@@ -792,6 +792,16 @@ def test_projected_backward_shapes(sla, dtype, shape):
                               label=f"shape{shape}-relu")
 
 
+@pytest.mark.parametrize("dtype,shape", [("f16", (2, 32)), ("bf16", (8, 32))])
+def test_projected_backward_tiny(sla, dtype, shape):
+    # fewer rows than one 16-row tile: the row products' and the weight
+    # gradients' grids are mostly idle (padded to whole blocks of 8 row ranges
+    # or groups), one row lies in no window
+    H, d = shape
+    ids = np.array([1, 0, -1, 1, 1], dtype=np.int32)
+    projected_backward_parity(sla, ids, None, ids.size, 3, H, d, dtype, seed=3, label=f"tiny{shape}")
+
+
 def test_projected_backward_csr_and_determinism(sla):
     import torch
 
