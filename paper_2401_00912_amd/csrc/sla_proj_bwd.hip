@@ -107,7 +107,8 @@ __global__ __launch_bounds__(256) void k_prep(PrepArgs pa) {
 // operand and the input rows (16-byte pieces of 8 channels) as the second, lane
 // (i, g) receives 4 columns of the tile's row i from each tile; the weight rows
 // are staged in an order that makes a tile pair's 8 columns of a lane
-// consecutive, stored as one 16-byte piece.
+// consecutive (one 16-byte piece), and lanes i and i ^ 8 trade pieces so that
+// each store writes 8 rows x 128 bytes.
 // When N takes several column blocks, the workgroups of one row range sit 8 ids
 // apart: workgroups are dealt to the 8 XCDs in turn, so the column blocks of a
 // row range share one XCD, and its L2 serves their common input rows (the
@@ -246,22 +247,40 @@ __global__ __launch_bounds__(kRowGemmThreads) void k_rows_gemm(RowGemmArgs ga) {
           }
         }
       }
-      if (!inside) continue;
       const int32_t j0 = n0 + sb;   // a sub-block lies in one output segment (C % SB == 0)
       T* outp = static_cast<T*>(ga.out[j0 / C]);
-      T* dst = elem_at(outp, (uint32_t)row * (uint32_t)C + (uint32_t)(j0 % C) + 8 * g);
+      // tile pairs 2w and 2w + 1 (64 columns): lanes i and i ^ 8 swap one
+      // piece (row rotation by 8 lanes), so that each store writes 8 rows x 128
+      // bytes: rows 0-7 of the tile first, then rows 8-15
+      const int32_t pa = tile * 16 + (i & 7), pb = pa + 8;
+      const uint32_t ccol = (uint32_t)(j0 % C) + (i < 8 ? 8 * g : 32 + 8 * g);
 #pragma unroll
-      for (int u = 0; u < NBT / 2; ++u) {
-        float f[8];
+      for (int w = 0; w < NBT / 4; ++w) {
+        Raw<T, 8> pk[2];
 #pragma unroll
-        for (int v = 0; v < 2; ++v) {
-          const float4 bias = *reinterpret_cast<const float4*>(s_b + sb + 16 * (2 * u + v) + 4 * g);
-          f[4 * v + 0] = acc[2 * u + v][0] + bias.x;
-          f[4 * v + 1] = acc[2 * u + v][1] + bias.y;
-          f[4 * v + 2] = acc[2 * u + v][2] + bias.z;
-          f[4 * v + 3] = acc[2 * u + v][3] + bias.w;
+        for (int u = 0; u < 2; ++u) {
+          float f[8];
+#pragma unroll
+          for (int v = 0; v < 2; ++v) {
+            const int t = 4 * w + 2 * u + v;
+            const float4 bias = *reinterpret_cast<const float4*>(s_b + sb + 16 * t + 4 * g);
+            f[4 * v + 0] = acc[t][0] + bias.x;
+            f[4 * v + 1] = acc[t][1] + bias.y;
+            f[4 * v + 2] = acc[t][2] + bias.z;
+            f[4 * v + 3] = acc[t][3] + bias.w;
+          }
+          pk[u] = F8::from_f32(f);
         }
-        *reinterpret_cast<Raw<T, 8>*>(dst + 32 * u) = F8::from_f32(f);
+        const uint4 snd = __builtin_bit_cast(uint4, i < 8 ? pk[1] : pk[0]);
+        uint4 rcv;
+        rcv.x = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)snd.x, 0x128, 0xf, 0xf, false);   // row_ror:8
+        rcv.y = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)snd.y, 0x128, 0xf, 0xf, false);
+        rcv.z = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)snd.z, 0x128, 0xf, 0xf, false);
+        rcv.w = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)snd.w, 0x128, 0xf, 0xf, false);
+        const uint4 da = i < 8 ? __builtin_bit_cast(uint4, pk[0]) : rcv;
+        const uint4 db = i < 8 ? rcv : __builtin_bit_cast(uint4, pk[1]);
+        if (pa < ga.n) *reinterpret_cast<uint4*>(elem_at(outp, (uint32_t)pa * (uint32_t)C + ccol + 64 * w)) = da;
+        if (pb < ga.n) *reinterpret_cast<uint4*>(elem_at(outp, (uint32_t)pb * (uint32_t)C + ccol + 64 * w)) = db;
       }
     }
   }
