@@ -99,16 +99,16 @@ __global__ __launch_bounds__(256) void k_prep(PrepArgs pa) {
 //
 // A workgroup of 16 waves keeps the weight rows of NB output columns (all N when
 // they fit) in LDS, padded rows of K + 8 elements, and walks 16-row tiles, one
-// per wave.  When K <= 32 KBH a wave reads its tile's input once into registers
-// and forms every 16 NBT-column sub-block from them; otherwise it reads the
-// input again per sub-block (KBH = 0, for C = 256: a 256-channel segment at a
-// time, the next segment's pieces in flight while one is formed).  With the
-// weight rows as the first matrix-core
-// operand and the input rows (16-byte pieces of 8 channels) as the second, lane
-// (i, g) receives 4 columns of the tile's row i from each tile; the weight rows
-// are staged in an order that makes a tile pair's 8 columns of a lane
-// consecutive (one 16-byte piece), and lanes i and i ^ 8 trade pieces so that
-// each store writes 8 rows x 128 bytes.
+// per wave.  With KBH > 0 (K <= 32 KBH) a wave reads its tile's input once into
+// registers and forms every 16 NBT-column sub-block from them; with KBH = 0 (K
+// = 3C for C = 256) it reads the input again per sub-block, a 256-channel
+// segment at a time, the next segment's pieces in flight while one is formed.
+// With the weight rows as the first matrix-core operand and the input rows
+// (16-byte pieces of 8 channels) as the second, lane (i, g) receives 4 columns
+// of the tile's row i from each tile; the weight rows are staged in an order
+// that makes a tile pair's 8 columns of a lane consecutive (one 16-byte piece),
+// and lanes i and i ^ 8 trade pieces so that each store writes 8 rows x 128
+// bytes.
 // When N takes several column blocks, the workgroups of one row range sit 8 ids
 // apart: workgroups are dealt to the 8 XCDs in turn, so the column blocks of a
 // row range share one XCD, and its L2 serves their common input rows (the
@@ -161,7 +161,7 @@ __global__ __launch_bounds__(kRowGemmThreads) void k_rows_gemm(RowGemmArgs ga) {
   const int lane = lane_id(), wv = threadIdx.x >> 6;
   const int i = lane & 15, g = lane >> 4;
   const int nseg = K / C;
-  const bool held = K <= 32 * KBH;
+  constexpr bool held = KBH > 0;   // the host picks KBH > 0 only when K <= 32 KBH
   constexpr int NW = kRowGemmThreads / 64;
   for (int32_t tile = rb * NW + wv; tile * 16 < ga.n; tile += ranges * NW) {
     const int32_t p = tile * 16 + i;
@@ -171,7 +171,7 @@ __global__ __launch_bounds__(kRowGemmThreads) void k_rows_gemm(RowGemmArgs ga) {
     // the tile's input, when it fits in registers: k block kb is channels
     // 32 kb .. + 31 of A, in segment 32 kb / C
     Raw<T, 8> xh[KBH > 0 ? KBH : 1];
-    if (held) {
+    if constexpr (held) {
 #pragma unroll
       for (int kb = 0; kb < KBH; ++kb) {
         xh[kb] = F8::zero();
@@ -189,7 +189,7 @@ __global__ __launch_bounds__(kRowGemmThreads) void k_rows_gemm(RowGemmArgs ga) {
 #pragma unroll
       for (int t = 0; t < NBT; ++t) acc[t] = zero;
       const T* wsb = s_w + (sb + i) * LDW + 8 * g;
-      if (held) {
+      if constexpr (held) {
 #pragma unroll
         for (int kb = 0; kb < KBH; ++kb) {
           if (32 * kb >= K) break;
@@ -199,7 +199,7 @@ __global__ __launch_bounds__(kRowGemmThreads) void k_rows_gemm(RowGemmArgs ga) {
             acc[t] = F8::mma(wo, xh[kb], acc[t]);
           }
         }
-      } else if constexpr (KBH == 0) {
+      } else {
         // the input one C-channel segment (C = 256) at a time: all of a
         // segment's pieces are requested together, the next segment's while
         // this one is formed
@@ -231,20 +231,6 @@ __global__ __launch_bounds__(kRowGemmThreads) void k_rows_gemm(RowGemmArgs ga) {
             }
 #pragma unroll
           for (int kb = 0; kb < KS; ++kb) xs[kb] = xn[kb];
-        }
-      } else {
-        for (int s = 0; s < nseg; ++s) {
-          const T* src = static_cast<const T*>(ga.a[s]);
-          for (int kb = 0; kb < C / 32; ++kb) {
-            Raw<T, 8> xo = __builtin_bit_cast(
-                Raw<T, 8>, *reinterpret_cast<const uint4*>(elem_at(src, (uint32_t)row * (uint32_t)C + 32 * kb + 8 * g)));
-            if (!valid) xo = F8::zero();
-#pragma unroll
-            for (int t = 0; t < NBT; ++t) {
-              const Raw<T, 8> wo = *reinterpret_cast<const Raw<T, 8>*>(wsb + 16 * t * LDW + s * C + 32 * kb);
-              acc[t] = F8::mma(wo, xo, acc[t]);
-            }
-          }
         }
       }
       const int32_t j0 = n0 + sb;   // a sub-block lies in one output segment (C % SB == 0)
@@ -591,9 +577,8 @@ static hipError_t rows_gemm(RowGemmArgs ga, hipStream_t stream) {
     if (gx < 8) gx = 8;
   }
   // the input held in registers for K <= 128 or K <= 384, else streamed a
-  // segment at a time (K = 3C with C = 256)
-  // (128 weight rows of K > 592 exceed the LDS cap, so a streamed product is
-  // never wide)
+  // segment at a time (K = 3C with C = 256; 128 weight rows of such K exceed the
+  // LDS cap, so a streamed product is never wide)
   const bool streamed = ga.K > 32 * 12;
   if (streamed && (wide || ga.C > 256 || ga.C % 32 != 0)) return hipErrorInvalidValue;
   void (*kern)(RowGemmArgs) =
