@@ -715,7 +715,8 @@ def bench_projected(torch, sla, workloads, dev, args):
         sets.append({"x": x, "plan": plan, "o": torch.empty(n, H, d, dtype=tdt, device=dev),
                      "y": torch.empty(n, C, dtype=tdt, device=dev),
                      "dy": torch.randn(n, C, generator=gen).to(tdt).to(dev),
-                     "dx": torch.empty(n, C, dtype=tdt, device=dev)})
+                     "dx": torch.empty(n, C, dtype=tdt, device=dev),
+                     "qkv": torch.empty(3, n, C, dtype=tdt, device=dev)})
     ws = torch.empty(sla.backward_projected_workspace_bytes(n, H, d), dtype=torch.uint8, device=dev)
     torch.cuda.synchronize()
 
@@ -725,6 +726,15 @@ def bench_projected(torch, sla, workloads, dev, args):
     def backward(st):
         sla.backward_projected(st["plan"], st["x"], w_qkv, w_o, st["o"], st["dy"], H, b_qkv, dx=st["dx"],
                                workspace=ws)
+
+    # the forward saving q, k, v, and the backward reading them
+    def fused_save(st):
+        sla.forward_projected(st["plan"], st["x"], w_qkv, w_o, H, b_qkv, b_o, st["o"], st["y"],
+                              qkv_out=st["qkv"])
+
+    def backward_saved(st):
+        sla.backward_projected(st["plan"], st["x"], w_qkv, w_o, st["o"], st["dy"], H, b_qkv, dx=st["dx"],
+                               workspace=ws, qkv=st["qkv"])
 
     def unfused(st):
         qkv = Fn.linear(st["x"], w_qkv, b_qkv)
@@ -741,6 +751,10 @@ def bench_projected(torch, sla, workloads, dev, args):
     for st in sets:     # the forward's o of every set, for the backward
         fused(st)
     t_backward = timed(backward, reps)
+    t_fused_save = timed(fused_save, reps)
+    for st in sets:     # the saved q, k, v of every set
+        fused_save(st)
+    t_backward_saved = timed(backward_saved, reps)
     fused_bytes = 4 * n * C * e     # x read, o written; o read, y written
     unfused_bytes = 10 * n * C * e  # + q, k, v written and read, and their copies' extra pass
     # backward, least traffic: x, o, dy read and dx written (q, k, v, do, dq, dk, dv
@@ -764,6 +778,12 @@ def bench_projected(torch, sla, workloads, dev, args):
         "backward_frac_of_hbm_peak": backward_bytes / (t_backward * 1e-6) / 1e9 / HBM_PEAK_GBS,
         "backward_path": "sla_backward_projected: q, k, v recomputed, do, SLA backward, dx, "
                          "weight and bias gradients (fp32, fixed-order sums)",
+        "fused_save_us": t_fused_save,
+        "backward_saved_us": t_backward_saved,
+        "saved_qkv_path": "the forward also stores q, k, v (3 n C e bytes more), the backward reads them "
+                          "instead of recomputing them",
+        "train_pair_us": t_fused + t_backward,
+        "train_pair_saved_us": t_fused_save + t_backward_saved,
     }
 
 

@@ -207,8 +207,8 @@ sla_status_t sla_backward_ex(const void* plan, size_t plan_bytes, int64_t n, int
                              void* dv, sla_stream_t stream);
 
 /*
- * Projection layer, SLA and output projection in two launches, without q, k, v
- * in memory.  Sec. 3.2 maps every voxel of the scene to Q, K and V with one
+ * Projection layer, SLA and output projection in two launches, q, k, v kept in
+ * registers.  Sec. 3.2 maps every voxel of the scene to Q, K and V with one
  * shared projection layer before the attention; the attention block projects
  * its output back.  Read as linear layers with bias in the [out, in] weight
  * layout:
@@ -219,19 +219,23 @@ sla_status_t sla_backward_ex(const void* plan, size_t plan_bytes, int64_t n, int
  *          k, v is head c / head_dim as everywhere);
  *   b_qkv  [3C] or NULL (no bias);  w_o [C, C];  b_o [C] or NULL;
  *   o      [n, C] output: SLA's output before the output projection;
- *   y      [n, C] output.
+ *   y      [n, C] output;
+ *   qkv_out [3][n][C] output or NULL: q, k, v (three consecutive [n, C]
+ *          tensors, q first) as projected, for sla_backward_projected to use
+ *          instead of recomputing them; rows in no window are not written.
+ *          It costs the forward the stores of 3 n C values.
  * All in `dtype`, which must be SLA_F16 or SLA_BF16; C must be 64, 128 or 256
- * (else SLA_E_UNSUPPORTED).  x, w_qkv, w_o, o, y 16-byte aligned.  Rows in no
- * window get neither o nor y.  The projections run on the matrix cores with
- * fp32 accumulation; q, k, v are rounded to `dtype` (as if stored) before the
- * attention, o is rounded before the output projection.
+ * (else SLA_E_UNSUPPORTED).  x, w_qkv, w_o, o, y, qkv_out 16-byte aligned.  Rows
+ * in no window get neither o nor y.  The projections run on the matrix cores
+ * with fp32 accumulation; q, k, v are rounded to `dtype` (as if stored) before
+ * the attention, o is rounded before the output projection.
  */
 sla_status_t sla_forward_projected(const void* plan, size_t plan_bytes, int64_t n,
                                    int32_t num_windows, sla_dtype_t dtype, int32_t heads,
                                    int32_t head_dim, sla_feature_map_t feature_map, float eps,
                                    const void* x, const void* w_qkv, const void* b_qkv,
                                    const void* w_o, const void* b_o, void* o, void* y,
-                                   sla_stream_t stream);
+                                   void* qkv_out, sla_stream_t stream);
 
 /*
  * Backward of sla_forward_projected: the projection layer and output projection
@@ -246,16 +250,19 @@ sla_status_t sla_forward_projected(const void* plan, size_t plan_bytes, int64_t 
  *   dx     [n, C] in `dtype`: every row is written, zero for rows in no window.
  *   dw_qkv [3C, C], dw_o [C, C] (fp32, required); db_qkv [3C], db_o [C] (fp32,
  *          may be NULL).  Rows in no window take no part in these sums.
+ *   qkv    [3][n][C] or NULL: the forward's qkv_out, for the same x, weights and
+ *          plan; given, q, k, v are read from it instead of being recomputed.
  *   workspace: device, 256-byte aligned, at least
  *          sla_backward_projected_workspace_bytes(n, heads, head_dim) bytes
  *          (else SLA_E_WORKSPACE): the recomputed q, k, v, do, dq, dk, dv, the
  *          weights as rows and the weight-gradient partials.
- * q, k, v are recomputed from x (rounded to `dtype`, as in the forward); do, dq,
+ * Without qkv, q, k, v are recomputed from x (rounded to `dtype`, as in the
+ * forward; the same products in the same order, so the same values); do, dq,
  * dk, dv are rounded to `dtype` as stored; all products accumulate in fp32 on the
  * matrix cores.  The sums over rows run over the plan's sorted rows in groups
  * whose partials are added in group order: the results are deterministic.
- * Same dtype, C and alignment rules as sla_forward_projected; dy and dx 16-byte
- * aligned, the fp32 outputs 4-byte aligned.
+ * Same dtype, C and alignment rules as sla_forward_projected; dy, dx and qkv
+ * 16-byte aligned, the fp32 outputs 4-byte aligned.
  */
 size_t sla_backward_projected_workspace_bytes(int64_t n, int32_t heads, int32_t head_dim);
 
@@ -265,7 +272,8 @@ sla_status_t sla_backward_projected(const void* plan, size_t plan_bytes, int64_t
                                     const void* x, const void* w_qkv, const void* b_qkv,
                                     const void* w_o, const void* o, const void* dy, void* dx,
                                     float* dw_qkv, float* db_qkv, float* dw_o, float* db_o,
-                                    void* workspace, size_t workspace_bytes, sla_stream_t stream);
+                                    const void* qkv, void* workspace, size_t workspace_bytes,
+                                    sla_stream_t stream);
 
 /*
  * Cross-window interaction (Sec. 3.3, Eq. (4)-(7)), the module that follows SLA

@@ -17,12 +17,13 @@ hipError_t launch_backward(const void* plan, int32_t n, int32_t W, int dtype, in
 hipError_t launch_forward_projected(const void* plan, int32_t n, int32_t W, int dtype, int32_t H,
                                     int32_t d, int phi, float eps, const void* x, const void* wqkv,
                                     const void* bqkv, const void* wo, const void* bo, void* o,
-                                    void* y, hipStream_t stream);
+                                    void* y, void* qkv, hipStream_t stream);
 hipError_t launch_backward_projected(const void* plan, int32_t n, int32_t W, int dtype, int32_t H,
                                      int32_t d, int phi, float eps, const void* x, const void* wqkv,
                                      const void* bqkv, const void* wo, const void* o, const void* dy,
                                      void* dx, float* dw_qkv, float* db_qkv, float* dw_o,
-                                     float* db_o, void* workspace, hipStream_t stream);
+                                     float* db_o, const void* qkv, void* workspace,
+                                     hipStream_t stream);
 size_t projected_backward_workspace_bytes(int64_t n, int32_t C);
 size_t naive_workspace_bytes(int64_t n, int32_t H, int32_t d);
 hipError_t launch_cwi_build_map(const int32_t* coords, int32_t n, int32_t gx, int32_t gy,
@@ -230,7 +231,7 @@ SLA_EXPORT sla_status_t sla_forward_projected(const void* plan, size_t plan_byte
                                               sla_feature_map_t feature_map, float eps,
                                               const void* x, const void* w_qkv, const void* b_qkv,
                                               const void* w_o, const void* b_o, void* o, void* y,
-                                              sla_stream_t stream) {
+                                              void* qkv_out, sla_stream_t stream) {
   const sla_status_t st = check_tensor_args(n, num_windows, (int)dtype, heads, head_dim, plan, plan_bytes);
   if (st != SLA_OK) return st;
   if (!variant_ok((int)feature_map, eps)) return SLA_E_ARG;
@@ -240,11 +241,12 @@ SLA_EXPORT sla_status_t sla_forward_projected(const void* plan, size_t plan_byte
   if (n == 0) return SLA_OK;
   if (!x || !w_qkv || !w_o || !o || !y) return SLA_E_ARG;
   if (!aligned(x, 16) || !aligned(w_qkv, 16) || !aligned(w_o, 16) || !aligned(o, 16) ||
-      !aligned(y, 16) || !aligned(b_qkv, 2) || !aligned(b_o, 2))
+      !aligned(y, 16) || !aligned(b_qkv, 2) || !aligned(b_o, 2) || !aligned(qkv_out, 16))
     return SLA_E_ARG;
   return hip_status(sla::launch_forward_projected(plan, (int32_t)n, num_windows, (int)dtype, heads,
                                                   head_dim, (int)feature_map, eps, x, w_qkv, b_qkv,
-                                                  w_o, b_o, o, y, static_cast<hipStream_t>(stream)));
+                                                  w_o, b_o, o, y, qkv_out,
+                                                  static_cast<hipStream_t>(stream)));
 }
 
 SLA_EXPORT size_t sla_backward_projected_workspace_bytes(int64_t n, int32_t heads, int32_t head_dim) {
@@ -261,8 +263,8 @@ SLA_EXPORT sla_status_t sla_backward_projected(const void* plan, size_t plan_byt
                                                const void* x, const void* w_qkv, const void* b_qkv,
                                                const void* w_o, const void* o, const void* dy,
                                                void* dx, float* dw_qkv, float* db_qkv, float* dw_o,
-                                               float* db_o, void* workspace, size_t workspace_bytes,
-                                               sla_stream_t stream) {
+                                               float* db_o, const void* qkv, void* workspace,
+                                               size_t workspace_bytes, sla_stream_t stream) {
   const sla_status_t st = check_tensor_args(n, num_windows, (int)dtype, heads, head_dim, plan, plan_bytes);
   if (st != SLA_OK) return st;
   if (!variant_ok((int)feature_map, eps)) return SLA_E_ARG;
@@ -272,13 +274,13 @@ SLA_EXPORT sla_status_t sla_backward_projected(const void* plan, size_t plan_byt
   if (!x || !w_qkv || !w_o || !o || !dy || !dx || !dw_qkv || !dw_o) return SLA_E_ARG;
   if (!aligned(x, 16) || !aligned(w_qkv, 16) || !aligned(w_o, 16) || !aligned(o, 16) ||
       !aligned(dy, 16) || !aligned(dx, 16) || !aligned(b_qkv, 2) || !aligned(dw_qkv, 4) ||
-      !aligned(dw_o, 4) || !aligned(db_qkv, 4) || !aligned(db_o, 4))
+      !aligned(dw_o, 4) || !aligned(db_qkv, 4) || !aligned(db_o, 4) || !aligned(qkv, 16))
     return SLA_E_ARG;
   if (workspace == nullptr || !aligned(workspace, 256)) return SLA_E_ARG;
   if (workspace_bytes < sla::projected_backward_workspace_bytes(n, (int32_t)C)) return SLA_E_WORKSPACE;
   return hip_status(sla::launch_backward_projected(plan, (int32_t)n, num_windows, (int)dtype, heads,
                                                    head_dim, (int)feature_map, eps, x, w_qkv, b_qkv,
-                                                   w_o, o, dy, dx, dw_qkv, db_qkv, dw_o, db_o,
+                                                   w_o, o, dy, dx, dw_qkv, db_qkv, dw_o, db_o, qkv,
                                                    workspace, static_cast<hipStream_t>(stream)));
 }
 

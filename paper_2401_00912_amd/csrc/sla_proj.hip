@@ -34,6 +34,7 @@ struct ProjArgs {
   const void* x;  // [n, C] features
   const void* w;  // [3C, C]: the rows of W_q, W_k, W_v
   const void* b;  // [3C] or null
+  void* qkv;      // [3][n][C]: q, k, v as projected, when they are saved
 };
 
 struct ProjItems {
@@ -163,6 +164,21 @@ __device__ __forceinline__ void project_job(Slice<T, Geo<D>::KS, 3>& sj, const R
   }
 }
 
+// The matrices selected by `which` (bit 0: K, 1: V, 2: Q) of one job, as
+// projected, to the saved q, k, v ([3][n][C], q first) at their rows' head
+// columns; lanes past the job's rows store nothing.
+template <typename T, int D>
+__device__ __forceinline__ void save_job(const Slice<T, Geo<D>::KS, 3>& sj, unsigned which, T* qkv,
+                                         size_t nC, size_t rs, int col, int g) {
+#pragma unroll
+  for (int m = 0; m < 3; ++m) {
+    if (!(which & (1u << m))) continue;
+    T* base = qkv + (m == 2 ? 0 : (m == 0 ? nC : 2 * nC));
+#pragma unroll
+    for (int s = 0; s < 2; ++s) RowIO<T, D>::put(base, row_off(sj.o[s], rs, col), g, sj.x[m][s], sj.ok[s]);
+  }
+}
+
 // One job's features (rows from the block's permutation entries).
 template <typename T, int CB>
 __device__ __forceinline__ void xjob_fetch(Raw<T, 8> (&xj)[2][CB], int32_t (&o)[2], bool (&ok)[2],
@@ -250,7 +266,9 @@ __device__ __forceinline__ void stage_rows(T* s_w, float* s_b, const T* w, const
 #define SLA_PROJ_WPE 2
 #endif
 
-template <typename T, int D, int PHI, int CB>
+// SAVE: q, k, v also go to pa.qkv as they are projected (for a backward that
+// does not recompute them).
+template <typename T, int D, int PHI, int CB, bool SAVE>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(SLA_PROJ_WPE)))
 void k_sla_fwd_proj(KernelArgs a, ProjArgs pa, T* __restrict__ o) {
   constexpr int KT = kStateTiles<D>, C = 32 * CB, LDW = C + 8;
@@ -275,6 +293,8 @@ void k_sla_fwd_proj(KernelArgs a, ProjArgs pa, T* __restrict__ o) {
   const int32_t n = a.n, G = gridDim.x;
   const Sel<T, D> sel(i, g);
   constexpr unsigned kKV = 3u, kQ = 4u, kAll = 7u;
+  T* const qkv = static_cast<T*>(pa.qkv);
+  const size_t nC = (size_t)n * rs;
 
   int32_t item = blockIdx.x;
   Pending cur;
@@ -313,11 +333,18 @@ void k_sla_fwd_proj(KernelArgs a, ProjArgs pa, T* __restrict__ o) {
             Raw<T, 8> xj[2][CB];
             xjob_fetch<T, CB>(xj, bk.j[jj].o, bk.j[jj].ok, cur.br, jj, ww.ra, ww.rb, n, x, g);
             project_job<T, D, CB>(bk.j[jj], xj, kAll, s_w, s_b, i, g);
+            if constexpr (SAVE) save_job<T, D>(bk.j[jj], kAll, qkv, nC, rs, col, g);
             __builtin_amdgcn_sched_barrier(0);
           }
         }
       } else {
-        if (ww.kind != 0) project<T, D, CB>(bk, xb, kAll, s_w, s_b, i, g);
+        if (ww.kind != 0) {
+          project<T, D, CB>(bk, xb, kAll, s_w, s_b, i, g);
+          if constexpr (SAVE) {
+#pragma unroll
+            for (int jj = 0; jj < kBlockJobs; ++jj) save_job<T, D>(bk.j[jj], kAll, qkv, nC, rs, col, g);
+          }
+        }
       }
       for (bool more = wi.first(ww, cur.str); more; more = wi.next(ww, cur.str)) {
         const int32_t wa = wi.wc.ws, wb = wi.wc.we;
@@ -350,6 +377,7 @@ void k_sla_fwd_proj(KernelArgs a, ProjArgs pa, T* __restrict__ o) {
         for (int32_t r0 = ww.ra; r0 < ww.rb; r0 += kSliceRows) {
           Slice<T, Geo<D>::KS, 3> sj;
           stream_job<T, D, CB>(sj, r0, ww.rb, perm, n, x, kKV, s_w, s_b, i, g);
+          if constexpr (SAVE) save_job<T, D>(sj, kKV, qkv, nC, rs, col, g);
           state_seg<T, D, 3, PHI>(sj, r0, wa, wb, i, g, sel, st);
         }
         if (wi.shared) {
@@ -363,6 +391,7 @@ void k_sla_fwd_proj(KernelArgs a, ProjArgs pa, T* __restrict__ o) {
         for (int32_t r0 = ww.ra; r0 < ww.rb; r0 += kSliceRows) {
           Slice<T, Geo<D>::KS, 3> sj;
           stream_job<T, D, CB>(sj, r0, ww.rb, perm, n, x, kQ, s_w, s_b, i, g);
+          if constexpr (SAVE) save_job<T, D>(sj, kQ, qkv, nC, rs, col, g);
           apply_seg<T, D, 3, 2, PHI>(sj, r0, wa, wb, i, g, op, o, rs, col);
         }
       }
@@ -465,10 +494,12 @@ inline int64_t resident_for(const void* kernel, int threads) {
 template <typename T, int D, int PHI, int CB>
 static hipError_t proj_impl(const void* plan, int32_t n, int32_t W, int32_t H, float eps,
                             const void* x, const void* wqkv, const void* bqkv, const void* wo,
-                            const void* bo, void* o, void* y, hipStream_t stream) {
+                            const void* bo, void* o, void* y, void* qkv, hipStream_t stream) {
   const PlanLayout lay = plan_layout(n, W);
   const KernelArgs a = kernel_args(plan, lay, n, W, H, eps);
-  const void* kern = reinterpret_cast<const void*>(&k_sla_fwd_proj<T, D, PHI, CB>);
+  void (*fk)(KernelArgs, ProjArgs, T*) =
+      qkv ? &k_sla_fwd_proj<T, D, PHI, CB, true> : &k_sla_fwd_proj<T, D, PHI, CB, false>;
+  const void* kern = reinterpret_cast<const void*>(fk);
   const int64_t c = resident_workgroups(kern);
   const int64_t unit = 8 * (int64_t)H;
   const int64_t ml = lay.max_long, mc = lay.max_chunks;
@@ -479,9 +510,8 @@ static hipError_t proj_impl(const void* plan, int32_t n, int32_t W, int32_t H, f
   if (g > items) g = items;
   g = (g + unit - 1) / unit * unit;
   if (g < unit) g = unit;
-  const ProjArgs pa{x, wqkv, bqkv};
-  hipLaunchKernelGGL((k_sla_fwd_proj<T, D, PHI, CB>), dim3((unsigned)g), dim3(64 * kWaves), 0, stream,
-                     a, pa, static_cast<T*>(o));
+  const ProjArgs pa{x, wqkv, bqkv, qkv};
+  hipLaunchKernelGGL(fk, dim3((unsigned)g), dim3(64 * kWaves), 0, stream, a, pa, static_cast<T*>(o));
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   const void* kout = reinterpret_cast<const void*>(&k_out_proj<T, CB>);
@@ -498,32 +528,32 @@ static hipError_t proj_impl(const void* plan, int32_t n, int32_t W, int32_t H, f
 template <typename T, int PHI>
 static hipError_t projected_t(const void* plan, int32_t n, int32_t W, int32_t H, int32_t d,
                               float eps, const void* x, const void* wqkv, const void* bqkv,
-                              const void* wo, const void* bo, void* o, void* y,
+                              const void* wo, const void* bo, void* o, void* y, void* qkv,
                               hipStream_t stream) {
   const int C = H * d;
   if (d == 32) {
-    if (C == 256) return proj_impl<T, 32, PHI, 8>(plan, n, W, H, eps, x, wqkv, bqkv, wo, bo, o, y, stream);
-    if (C == 128) return proj_impl<T, 32, PHI, 4>(plan, n, W, H, eps, x, wqkv, bqkv, wo, bo, o, y, stream);
-    return proj_impl<T, 32, PHI, 2>(plan, n, W, H, eps, x, wqkv, bqkv, wo, bo, o, y, stream);
+    if (C == 256) return proj_impl<T, 32, PHI, 8>(plan, n, W, H, eps, x, wqkv, bqkv, wo, bo, o, y, qkv, stream);
+    if (C == 128) return proj_impl<T, 32, PHI, 4>(plan, n, W, H, eps, x, wqkv, bqkv, wo, bo, o, y, qkv, stream);
+    return proj_impl<T, 32, PHI, 2>(plan, n, W, H, eps, x, wqkv, bqkv, wo, bo, o, y, qkv, stream);
   }
-  if (C == 256) return proj_impl<T, 16, PHI, 8>(plan, n, W, H, eps, x, wqkv, bqkv, wo, bo, o, y, stream);
-  if (C == 128) return proj_impl<T, 16, PHI, 4>(plan, n, W, H, eps, x, wqkv, bqkv, wo, bo, o, y, stream);
-  return proj_impl<T, 16, PHI, 2>(plan, n, W, H, eps, x, wqkv, bqkv, wo, bo, o, y, stream);
+  if (C == 256) return proj_impl<T, 16, PHI, 8>(plan, n, W, H, eps, x, wqkv, bqkv, wo, bo, o, y, qkv, stream);
+  if (C == 128) return proj_impl<T, 16, PHI, 4>(plan, n, W, H, eps, x, wqkv, bqkv, wo, bo, o, y, qkv, stream);
+  return proj_impl<T, 16, PHI, 2>(plan, n, W, H, eps, x, wqkv, bqkv, wo, bo, o, y, qkv, stream);
 }
 
 // dtype: 1 f16, 2 bf16; C = H d in {64, 128, 256}; phi: 0 elu + 1, 1 ReLU
 hipError_t launch_forward_projected(const void* plan, int32_t n, int32_t W, int dtype, int32_t H,
                                     int32_t d, int phi, float eps, const void* x, const void* wqkv,
                                     const void* bqkv, const void* wo, const void* bo, void* o,
-                                    void* y, hipStream_t stream) {
+                                    void* y, void* qkv, hipStream_t stream) {
   if (dtype == 1) {
     if (phi == kPhiRelu)
-      return projected_t<_Float16, kPhiRelu>(plan, n, W, H, d, eps, x, wqkv, bqkv, wo, bo, o, y, stream);
-    return projected_t<_Float16, kPhiElu1>(plan, n, W, H, d, eps, x, wqkv, bqkv, wo, bo, o, y, stream);
+      return projected_t<_Float16, kPhiRelu>(plan, n, W, H, d, eps, x, wqkv, bqkv, wo, bo, o, y, qkv, stream);
+    return projected_t<_Float16, kPhiElu1>(plan, n, W, H, d, eps, x, wqkv, bqkv, wo, bo, o, y, qkv, stream);
   }
   if (phi == kPhiRelu)
-    return projected_t<bf16_t, kPhiRelu>(plan, n, W, H, d, eps, x, wqkv, bqkv, wo, bo, o, y, stream);
-  return projected_t<bf16_t, kPhiElu1>(plan, n, W, H, d, eps, x, wqkv, bqkv, wo, bo, o, y, stream);
+    return projected_t<bf16_t, kPhiRelu>(plan, n, W, H, d, eps, x, wqkv, bqkv, wo, bo, o, y, qkv, stream);
+  return projected_t<bf16_t, kPhiElu1>(plan, n, W, H, d, eps, x, wqkv, bqkv, wo, bo, o, y, qkv, stream);
 }
 
 }  // namespace sla

@@ -597,8 +597,8 @@ static hipError_t projected_backward_t(const void* plan, int32_t n, int32_t W, i
                                        int32_t d, int phi, float eps, const void* x,
                                        const void* wqkv, const void* bqkv, const void* wo,
                                        const void* o, const void* dy, void* dx, float* dw_qkv,
-                                       float* db_qkv, float* dw_o, float* db_o, void* workspace,
-                                       hipStream_t stream) {
+                                       float* db_qkv, float* dw_o, float* db_o, const void* qkv,
+                                       void* workspace, hipStream_t stream) {
   const int32_t C = H * d;
   const PlanLayout lay = plan_layout(n, W);
   const char* pb = static_cast<const char*>(plan);
@@ -611,7 +611,14 @@ static hipError_t projected_backward_t(const void* plan, int32_t n, int32_t W, i
   T* wt_o = reinterpret_cast<T*>(ws + L.wt_o);
   T* act[7];
   for (int m = 0; m < 7; ++m) act[m] = reinterpret_cast<T*>(ws + L.act + m * L.act_stride);
-  T *q = act[0], *k = act[1], *v = act[2], *dov = act[3], *dq = act[4], *dk = act[5], *dv = act[6];
+  T *dov = act[3], *dq = act[4], *dk = act[5], *dv = act[6];
+  // q, k, v: as the forward saved them ([3][n][C]), else recomputed into the
+  // workspace below
+  const T* saved = static_cast<const T*>(qkv);
+  const size_t nC = (size_t)n * C;
+  const T* q = saved ? saved : act[0];
+  const T* k = saved ? saved + nC : act[1];
+  const T* v = saved ? saved + 2 * nC : act[2];
   float* part = reinterpret_cast<float*>(ws + L.part);
   uint8_t* mask = reinterpret_cast<uint8_t*>(ws + L.mask);
   hipError_t e;
@@ -641,14 +648,14 @@ static hipError_t projected_backward_t(const void* plan, int32_t n, int32_t W, i
   ga.n = n;
   ga.W = W;
   ga.a[0] = x;
-  ga.out[0] = q;
-  ga.out[1] = k;
-  ga.out[2] = v;
+  ga.out[0] = act[0];
+  ga.out[1] = act[1];
+  ga.out[2] = act[2];
   ga.w = wqkv;
   ga.bias = bqkv;
   ga.K = C;
   ga.N = 3 * C;
-  if ((e = rows_gemm<T>(ga, stream)) != hipSuccess) return e;
+  if (!saved && (e = rows_gemm<T>(ga, stream)) != hipSuccess) return e;
   // do = dy W_o
   ga.a[0] = dy;
   ga.out[0] = dov;
@@ -707,12 +714,12 @@ hipError_t launch_backward_projected(const void* plan, int32_t n, int32_t W, int
                                      int32_t d, int phi, float eps, const void* x, const void* wqkv,
                                      const void* bqkv, const void* wo, const void* o, const void* dy,
                                      void* dx, float* dw_qkv, float* db_qkv, float* dw_o,
-                                     float* db_o, void* workspace, hipStream_t stream) {
+                                     float* db_o, const void* qkv, void* workspace, hipStream_t stream) {
   if (dtype == 1)
     return projected_backward_t<_Float16>(plan, n, W, dtype, H, d, phi, eps, x, wqkv, bqkv, wo, o, dy, dx,
-                                          dw_qkv, db_qkv, dw_o, db_o, workspace, stream);
+                                          dw_qkv, db_qkv, dw_o, db_o, qkv, workspace, stream);
   return projected_backward_t<bf16_t>(plan, n, W, dtype, H, d, phi, eps, x, wqkv, bqkv, wo, o, dy, dx,
-                                      dw_qkv, db_qkv, dw_o, db_o, workspace, stream);
+                                      dw_qkv, db_qkv, dw_o, db_o, qkv, workspace, stream);
 }
 
 }  // namespace sla

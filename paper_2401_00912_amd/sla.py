@@ -117,11 +117,11 @@ def lib() -> ctypes.CDLL:
     L.sla_backward_ex.restype = ctypes.c_int
     L.sla_backward_ex.argtypes = [vp, sz, i64, i32, en, i32, i32, en, f32, vp, vp, vp, vp, vp, vp, vp, vp]
     L.sla_forward_projected.restype = ctypes.c_int
-    L.sla_forward_projected.argtypes = [vp, sz, i64, i32, en, i32, i32, en, f32, vp, vp, vp, vp, vp, vp, vp, vp]
+    L.sla_forward_projected.argtypes = [vp, sz, i64, i32, en, i32, i32, en, f32] + [vp] * 9
     L.sla_backward_projected_workspace_bytes.restype = sz
     L.sla_backward_projected_workspace_bytes.argtypes = [i64, i32, i32]
     L.sla_backward_projected.restype = ctypes.c_int
-    L.sla_backward_projected.argtypes = [vp, sz, i64, i32, en, i32, i32, en, f32] + [vp] * 11 + [vp, sz, vp]
+    L.sla_backward_projected.argtypes = [vp, sz, i64, i32, en, i32, i32, en, f32] + [vp] * 12 + [vp, sz, vp]
     L.sla_cwi_map_bytes.restype = sz
     L.sla_cwi_map_bytes.argtypes = [i32, i32, i32]
     L.sla_cwi_build_map.restype = ctypes.c_int
@@ -400,10 +400,11 @@ def backward_xca_noalloc(plan: Plan, q, k, v, tau, dout, dq=None, dk=None, dv=No
 
 
 def forward_projected(plan: Plan, x, w_qkv, w_o, heads: int, b_qkv=None, b_o=None, o=None, y=None,
-                      feature_map="elu1", eps=0.0):
+                      feature_map="elu1", eps=0.0, qkv_out=None):
     """Projection layer, SLA and output projection (sla_forward_projected):
     x [n, C], w_qkv [3C, C], w_o [C, C], optional biases [3C], [C]; returns (o, y)
-    with o [n, heads, C // heads] and y [n, C]."""
+    with o [n, heads, C // heads] and y [n, C].  qkv_out, a contiguous [3, n, C]
+    tensor like x, also receives q, k, v for backward_projected(qkv=...)."""
     torch = _torch()
     if x.dim() != 2 or x.shape[0] != plan.n or not x.is_contiguous():
         raise ValueError(f"x must be a contiguous [n, C] tensor with n={plan.n}")
@@ -424,12 +425,21 @@ def forward_projected(plan: Plan, x, w_qkv, w_o, heads: int, b_qkv=None, b_o=Non
         raise ValueError("y must be a contiguous tensor like x")
     if feature_map not in FEATURE_MAPS:
         raise ValueError(f"feature_map must be one of {sorted(FEATURE_MAPS)}, not {feature_map!r}")
+    _check_qkv("qkv_out", qkv_out, x)
     st = lib().sla_forward_projected(_ptr(plan.buf), plan.nbytes, plan.n, plan.num_windows,
                                      _dtype_code(x.dtype), heads, d, FEATURE_MAPS[feature_map], float(eps),
                                      _ptr(x), _ptr(w_qkv), _ptr(b_qkv), _ptr(w_o), _ptr(b_o), _ptr(o), _ptr(y),
-                                     _stream(x.device))
+                                     _ptr(qkv_out), _stream(x.device))
     _check(st, "sla_forward_projected")
     return o, y
+
+
+def _check_qkv(name, t, x):
+    if t is None:
+        return
+    n, C = x.shape
+    if tuple(t.shape) != (3, n, C) or t.dtype != x.dtype or t.device != x.device or not t.is_contiguous():
+        raise ValueError(f"{name} must be a contiguous (3, {n}, {C}) tensor like x")
 
 
 def backward_projected_workspace_bytes(n: int, heads: int, head_dim: int) -> int:
@@ -437,11 +447,13 @@ def backward_projected_workspace_bytes(n: int, heads: int, head_dim: int) -> int
 
 
 def backward_projected(plan: Plan, x, w_qkv, w_o, o, dy, heads: int, b_qkv=None, feature_map="elu1", eps=0.0,
-                       dx=None, workspace=None, bias_grads=True):
+                       dx=None, workspace=None, bias_grads=True, qkv=None):
     """Gradients of sla_forward_projected (sla_backward_projected): x, dy [n, C],
     w_qkv [3C, C], w_o [C, C], o the forward's SLA output ([n, heads, d] or [n, C]),
-    optional b_qkv [3C].  Returns (dx, dw_qkv, db_qkv, dw_o, db_o): dx like x, the
-    weight and bias gradients float32 (the bias ones None with bias_grads=False)."""
+    optional b_qkv [3C], optional qkv (the forward's qkv_out, [3, n, C]; q, k, v
+    are recomputed without it).  Returns (dx, dw_qkv, db_qkv, dw_o, db_o): dx like
+    x, the weight and bias gradients float32 (the bias ones None with
+    bias_grads=False)."""
     torch = _torch()
     if x.dim() != 2 or x.shape[0] != plan.n or not x.is_contiguous():
         raise ValueError(f"x must be a contiguous [n, C] tensor with n={plan.n}")
@@ -470,11 +482,13 @@ def backward_projected(plan: Plan, x, w_qkv, w_o, o, dy, heads: int, b_qkv=None,
     _check_workspace(workspace, x.device)
     if feature_map not in FEATURE_MAPS:
         raise ValueError(f"feature_map must be one of {sorted(FEATURE_MAPS)}, not {feature_map!r}")
+    _check_qkv("qkv", qkv, x)
     st = lib().sla_backward_projected(_ptr(plan.buf), plan.nbytes, plan.n, plan.num_windows,
                                       _dtype_code(x.dtype), heads, d, FEATURE_MAPS[feature_map], float(eps),
                                       _ptr(x), _ptr(w_qkv), _ptr(b_qkv), _ptr(w_o), _ptr(o), _ptr(dy), _ptr(dx),
-                                      _ptr(dw_qkv), _ptr(db_qkv), _ptr(dw_o), _ptr(db_o), _ptr(workspace),
-                                      workspace.numel() * workspace.element_size(), _stream(x.device))
+                                      _ptr(dw_qkv), _ptr(db_qkv), _ptr(dw_o), _ptr(db_o), _ptr(qkv),
+                                      _ptr(workspace), workspace.numel() * workspace.element_size(),
+                                      _stream(x.device))
     _check(st, "sla_backward_projected")
     return dx, dw_qkv, db_qkv, dw_o, db_o
 

@@ -209,9 +209,9 @@ def test_variant_argument_errors(L):
 
 def test_projected_argument_errors(L):
     nb = sla.plan_bytes(100, 8)
-    def call(dtype=1, H=4, d=32, fm=0, eps=0.0, n=100, x=FAKE, y=FAKE, bq=None):
+    def call(dtype=1, H=4, d=32, fm=0, eps=0.0, n=100, x=FAKE, y=FAKE, bq=None, qkv=None):
         return L.sla_forward_projected(FAKE, nb, n, 8, dtype, H, d, fm, eps, x, FAKE, bq, FAKE, None,
-                                       FAKE, y, None)
+                                       FAKE, y, qkv, None)
     assert call(dtype=0) == sla.SLA_E_UNSUPPORTED        # fp32 is not supported
     assert call(H=3) == sla.SLA_E_UNSUPPORTED            # C = 96
     assert call(H=16) == sla.SLA_E_UNSUPPORTED           # C = 512
@@ -221,6 +221,7 @@ def test_projected_argument_errors(L):
     assert call(x=FAKE + 8) == sla.SLA_E_ARG
     assert call(y=None) == sla.SLA_E_ARG
     assert call(bq=FAKE + 1) == sla.SLA_E_ARG
+    assert call(qkv=FAKE + 8) == sla.SLA_E_ARG          # q, k, v saved at a 16-byte boundary
     assert call(n=0) == sla.SLA_OK
 
 
@@ -234,9 +235,10 @@ def test_projected_backward_argument_errors(L):
     assert sla.backward_projected_workspace_bytes(1000, 4, 32) > need
 
     def call(dtype=1, H=4, d=32, fm=0, eps=0.0, x=FAKE, dy=FAKE, dx=FAKE, dwq=FAKE, dwo=FAKE, dbq=None,
-             ws=FAKE, wsb=None):
+             ws=FAKE, wsb=None, qkv=None):
         return L.sla_backward_projected(FAKE, nb, 100, 8, dtype, H, d, fm, eps, x, FAKE, None, FAKE, FAKE,
-                                        dy, dx, dwq, dbq, dwo, None, ws, need if wsb is None else wsb, None)
+                                        dy, dx, dwq, dbq, dwo, None, qkv, ws, need if wsb is None else wsb,
+                                        None)
     assert call(dtype=0) == sla.SLA_E_UNSUPPORTED        # fp32 is not supported
     assert call(H=3) == sla.SLA_E_UNSUPPORTED            # C = 96
     assert call(d=24) == sla.SLA_E_UNSUPPORTED
@@ -248,6 +250,7 @@ def test_projected_backward_argument_errors(L):
     assert call(dwq=None) == sla.SLA_E_ARG
     assert call(dwo=FAKE + 2) == sla.SLA_E_ARG
     assert call(dbq=FAKE + 1) == sla.SLA_E_ARG
+    assert call(qkv=FAKE + 4) == sla.SLA_E_ARG
     assert call(ws=None) == sla.SLA_E_ARG
     assert call(ws=FAKE + 16) == sla.SLA_E_ARG
     assert call(wsb=need - 1) == sla.SLA_E_WORKSPACE

@@ -792,6 +792,54 @@ def test_projected_backward_shapes(sla, dtype, shape):
                               label=f"shape{shape}-relu")
 
 
+@pytest.mark.parametrize("dtype,shape,long", [("f16", (4, 32), False), ("bf16", (8, 32), False),
+                                              ("f16", (2, 32), True)])
+def test_projected_saved_qkv(sla, dtype, shape, long):
+    # the forward's saved q, k, v: the projection of x (checked against float64
+    # from the same rounded inputs), o and y unchanged by saving, and the
+    # backward that reads them equal, bit for bit, to the one that recomputes
+    # them (the same products in the same order).  `long` adds a window of 1,024
+    # rows, whose shares are projected job by job (streamed).
+    import torch
+
+    H, d = shape
+    C = H * d
+    rng = np.random.default_rng([59, H, d, int(long)])
+    lengths = _adversarial_lengths(rng, 64) if long else rng.integers(1, 90, size=48)
+    ids = workloads.ids_from_lengths(np.asarray(lengths, dtype=np.int64), rng)
+    ids[rng.random(ids.size) < 0.01] = -1
+    n, W = ids.size, len(lengths)
+    cast = lambda a: workloads.cast_values(np.asarray(a, dtype=np.float32), dtype)  # noqa: E731
+    x = cast(rng.standard_normal((n, C)))
+    wq = cast(rng.standard_normal((3 * C, C)) / np.sqrt(C))
+    wo = cast(rng.standard_normal((C, C)) / np.sqrt(C))
+    bq = cast(0.2 * rng.standard_normal(3 * C))
+    dy = cast(rng.standard_normal((n, C)))
+    plan = build(sla, ids=ids, W=W)
+    off, perm = check_plan(sla, plan, ids, W, 0)
+    tx, twq, two, tbq, tdy = (to_dev(a, dtype) for a in (x, wq, wo, bq, dy))
+    zeros = lambda *shape: torch.zeros(shape, dtype=torch_dtype(dtype), device="cuda")  # noqa: E731
+    o0, y0 = sla.forward_projected(plan, tx, twq, two, H, tbq, None, zeros(n, H, d), zeros(n, C))
+    qkv = torch.full((3, n, C), float("nan"), dtype=torch_dtype(dtype), device="cuda")
+    o1, y1 = sla.forward_projected(plan, tx, twq, two, H, tbq, None, zeros(n, H, d), zeros(n, C), qkv_out=qkv)
+    torch.cuda.synchronize()
+    assert torch.equal(o0, o1) and torch.equal(y0, y1), "saving q, k, v changed o or y"
+    rows = np.zeros(n, dtype=bool)
+    rows[perm[: off[-1]] if perm is not None else np.arange(off[-1])] = True
+    w = lambda a: oracle.widen(a, dtype)  # noqa: E731
+    ref = w(x) @ w(wq).T + w(bq)
+    got = to_host64(qkv, dtype)
+    for m, name in enumerate("qkv"):
+        e = rel_err_per_head(got[m].reshape(n, H, d), ref[:, m * C:(m + 1) * C].reshape(n, H, d),
+                             1e-3 * float(np.abs(ref).max()), rows)
+        assert e <= (2e-3 if dtype == "f16" else 1e-2), f"saved {name}: {e:.2e}"
+    a = sla.backward_projected(plan, tx, twq, two, o1, tdy, H, tbq)
+    b = sla.backward_projected(plan, tx, twq, two, o1, tdy, H, tbq, qkv=qkv)
+    torch.cuda.synchronize()
+    for name, ta, tb in zip(("dx", "dw_qkv", "db_qkv", "dw_o", "db_o"), a, b):
+        assert torch.equal(ta, tb), f"{name} differs between recomputed and saved q, k, v"
+
+
 @pytest.mark.parametrize("dtype,shape", [("f16", (2, 32)), ("bf16", (8, 32))])
 def test_projected_backward_tiny(sla, dtype, shape):
     # fewer rows than one 16-row tile: the row products' and the weight
