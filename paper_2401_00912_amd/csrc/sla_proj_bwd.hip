@@ -281,12 +281,15 @@ __global__ __launch_bounds__(kRowGemmThreads) void k_rows_gemm(RowGemmArgs ga) {
 // sum_rows A(row, m0 + e).  The rows 0..n-1 are split into `groups` contiguous
 // ranges.
 //
-// A workgroup of 8 waves takes 8 units of one kind (C / 32 x C / 64 of them per
-// kind) and walks its rows 32 at a time: the rows of A and B are staged in LDS
-// once (rows in no window stored as zeros), the next two jobs' rows (one for
-// C = 256) loaded into registers while this one is summed; each wave reads its
-// columns as operands of a contraction over the job's rows with LDS transpose
-// loads and accumulates its 2 x 4 result tiles.
+// A workgroup of NT / 64 waves (8, or 16 for C = 256) takes as many units of
+// one kind (C / 32 x C / 64 of them per kind) and walks its rows 32 at a time:
+// the rows of A and B are staged in LDS once (rows in no window stored as
+// zeros), the next two jobs' rows loaded into registers while this one is
+// summed; each wave reads its columns as operands of a contraction over the
+// job's rows with LDS transpose loads and accumulates its 2 x 4 result tiles.
+// Every workgroup stages all of B's columns, so fewer, wider workgroups per
+// kind stage less: 16 waves for C = 256 (128 A columns and 256 B columns a row,
+// twice per kind, against 64 and 256 four times with 8 waves).
 struct WgradArgs {
   const void* mats[6];   // dq, dk, dv, x, dy, o [n, C]
   const PlanHeader* hdr;
@@ -295,22 +298,25 @@ struct WgradArgs {
   int32_t C, n, W, groups, wgs_per_kind;
 };
 
-constexpr int kWgradThreads = 512;
 constexpr int kWgradChunk = 64;    // gradient columns per unit
 
-// A columns a workgroup stages: its 8 units (one a wave) cover 8 / (C / 64)
-// slabs of 32 A columns, each with all C / 64 chunks of B's; at most C.
-__host__ __device__ constexpr int wgrad_a_cols(int C) {
-  return (kWgradThreads / 64) / (C / kWgradChunk) * 32 < C ? (kWgradThreads / 64) / (C / kWgradChunk) * 32 : C;
+// threads of a k_wgrad workgroup for a given C
+__host__ __device__ constexpr int wgrad_threads(int C) { return C == 256 ? 1024 : 512; }
+
+// A columns a workgroup stages: its NT / 64 units (one a wave) cover
+// (NT / 64) / (C / 64) slabs of 32 A columns, each with all C / 64 chunks of
+// B's; at most C.
+__host__ __device__ constexpr int wgrad_a_cols(int C, int NT) {
+  return (NT / 64) / (C / kWgradChunk) * 32 < C ? (NT / 64) / (C / kWgradChunk) * 32 : C;
 }
 
-// SP: 16-byte pieces a thread stages per job, at most 32 (na + C) / 8 / 512:
-// 1, 2, 3 for C = 64, 128, 256
-template <typename T, int SP>
-__global__ __launch_bounds__(kWgradThreads) void k_wgrad(WgradArgs wa) {
+// SP: 16-byte pieces a thread stages per job, at most 32 (na + C) / 8 / NT:
+// 1, 2, 2 for C = 64, 128 (512 threads), 256 (1,024 threads)
+template <typename T, int SP, int NT>
+__global__ __launch_bounds__(NT) void k_wgrad(WgradArgs wa) {
   using F = Frag<T, 8>;
   constexpr int NCB = kWgradChunk / 32;
-  constexpr int NWV = kWgradThreads / 64;
+  constexpr int NWV = NT / 64;
   const floatx4 zero = {0.f, 0.f, 0.f, 0.f};
   if (wa.hdr->magic != kPlanMagic || wa.hdr->n != wa.n || wa.hdr->num_windows != wa.W) return;
   extern __shared__ __attribute__((aligned(16))) unsigned char lds_raw[];
@@ -333,8 +339,8 @@ __global__ __launch_bounds__(kWgradThreads) void k_wgrad(WgradArgs wa) {
   const int slab = active ? unit / chunks : 0, chunk = active ? unit % chunks : 0;
   const int m0 = 32 * slab, n0 = kWgradChunk * chunk;
   // the workgroup's units cover A's columns a0 .. a0 + na - 1 (all of them for
-  // C <= 128, a quarter for C = 256) and all of B's: only those are staged
-  const int na = wgrad_a_cols(C);
+  // C <= 128, half for C = 256) and all of B's: only those are staged
+  const int na = wgrad_a_cols(C, NT);
   const int a0 = (part_of_kind * NWV / chunks) * 32;
   const int LDR = na + C + 8;                // staged row: A's columns then B's, padded
   T* stage = reinterpret_cast<T*>(lds_raw);   // [2][32][LDR]
@@ -355,8 +361,8 @@ __global__ __launch_bounds__(kWgradThreads) void k_wgrad(WgradArgs wa) {
   const int per_mat = na / 8, pieces_per_row = per_mat + C / 8;
   const int npieces = 32 * pieces_per_row;
   // the data and the row's mask byte are loaded together; rows in no window
-  // are zeroed when stored.  For C <= 128 two jobs are in flight in registers
-  // (sets a and b) while a third is summed from LDS; for C = 256 one.
+  // are zeroed when stored.  With SP <= 2 two jobs are in flight in registers
+  // (sets a and b) while a third is summed from LDS; otherwise one.
   struct Held {
     uint4 v[SP];
     int keep[SP];
@@ -364,7 +370,7 @@ __global__ __launch_bounds__(kWgradThreads) void k_wgrad(WgradArgs wa) {
   auto load_job = [&](Held& h, int32_t base) {
 #pragma unroll
     for (int k = 0; k < SP; ++k) {
-      const int idx = tid + k * kWgradThreads;
+      const int idx = tid + k * NT;
       h.v[k] = make_uint4(0, 0, 0, 0);
       h.keep[k] = 0;
       if (idx < npieces) {
@@ -381,7 +387,7 @@ __global__ __launch_bounds__(kWgradThreads) void k_wgrad(WgradArgs wa) {
   auto store_job = [&](const Held& h, T* buf) {
 #pragma unroll
     for (int k = 0; k < SP; ++k) {
-      const int idx = tid + k * kWgradThreads;
+      const int idx = tid + k * NT;
       if (idx < npieces) {
         const int r = idx / pieces_per_row, pc = idx - r * pieces_per_row;
         *reinterpret_cast<uint4*>(buf + r * LDR + 8 * pc) = h.keep[k] != 0 ? h.v[k] : make_uint4(0, 0, 0, 0);
@@ -433,7 +439,7 @@ __global__ __launch_bounds__(kWgradThreads) void k_wgrad(WgradArgs wa) {
       __syncthreads();
     }
   } else {
-    // C = 256: a second set would cost a workgroup per CU; one job in flight
+    // one job in flight
     Held ha;
     int buf = 0;
     if (p0 < p1) {
@@ -691,17 +697,18 @@ static hipError_t projected_backward_t(const void* plan, int32_t n, int32_t W, i
   wa.W = W;
   wa.groups = L.groups;
   const int units = (C / 32) * (C / kWgradChunk);
-  wa.wgs_per_kind = (units + kWgradThreads / 64 - 1) / (kWgradThreads / 64);
-  const size_t wlds = (size_t)2 * 32 * (wgrad_a_cols(C) + C + 8) * 2;
-  const void* wk = C == 256 ? reinterpret_cast<const void*>(&k_wgrad<T, 3>)
-                  : C == 128 ? reinterpret_cast<const void*>(&k_wgrad<T, 2>)
-                             : reinterpret_cast<const void*>(&k_wgrad<T, 1>);
+  const int wnt = wgrad_threads(C);
+  wa.wgs_per_kind = (units + wnt / 64 - 1) / (wnt / 64);
+  const size_t wlds = (size_t)2 * 32 * (wgrad_a_cols(C, wnt) + C + 8) * 2;
+  const void* wk = C == 256 ? reinterpret_cast<const void*>(&k_wgrad<T, 2, 1024>)
+                  : C == 128 ? reinterpret_cast<const void*>(&k_wgrad<T, 2, 512>)
+                             : reinterpret_cast<const void*>(&k_wgrad<T, 1, 512>);
   if ((e = hipFuncSetAttribute(wk, hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024 - 1024)) != hipSuccess)
     return e;
   const dim3 wg((unsigned)(((int64_t)L.groups + 7) / 8 * 8 * 4 * wa.wgs_per_kind));
-  if (C == 256) hipLaunchKernelGGL((k_wgrad<T, 3>), wg, dim3(kWgradThreads), wlds, stream, wa);
-  else if (C == 128) hipLaunchKernelGGL((k_wgrad<T, 2>), wg, dim3(kWgradThreads), wlds, stream, wa);
-  else hipLaunchKernelGGL((k_wgrad<T, 1>), wg, dim3(kWgradThreads), wlds, stream, wa);
+  if (C == 256) hipLaunchKernelGGL((k_wgrad<T, 2, 1024>), wg, dim3(1024), wlds, stream, wa);
+  else if (C == 128) hipLaunchKernelGGL((k_wgrad<T, 2, 512>), wg, dim3(512), wlds, stream, wa);
+  else hipLaunchKernelGGL((k_wgrad<T, 1, 512>), wg, dim3(512), wlds, stream, wa);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   const int64_t total = (int64_t)4 * C * C + 4 * (int64_t)C;
   hipLaunchKernelGGL(k_wgrad_reduce, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, stream,
