@@ -102,7 +102,8 @@ __global__ __launch_bounds__(256) void k_prep(PrepArgs pa) {
 // per wave.  With KBH > 0 (K <= 32 KBH) a wave reads its tile's input once into
 // registers and forms every 16 NBT-column sub-block from them; with KBH = 0 (K
 // = 3C for C = 256) it reads the input again per sub-block, a 256-channel
-// segment at a time, the next segment's pieces in flight while one is formed.
+// segment at a time, the next segment's pieces (or the next tile's first
+// segment) in flight while one is formed.
 // With the weight rows as the first matrix-core operand and the input rows
 // (16-byte pieces of 8 channels) as the second, lane (i, g) receives 4 columns
 // of the tile's row i from each tile; the weight rows are staged in an order
@@ -160,18 +161,56 @@ __global__ __launch_bounds__(kRowGemmThreads) void k_rows_gemm(RowGemmArgs ga) {
   const floatx4 zero = {0.f, 0.f, 0.f, 0.f};
   const int lane = lane_id(), wv = threadIdx.x >> 6;
   const int i = lane & 15, g = lane >> 4;
-  const int nseg = K / C;
   constexpr bool held = KBH > 0;   // the host picks KBH > 0 only when K <= 32 KBH
   constexpr int NW = kRowGemmThreads / 64;
-  for (int32_t tile = rb * NW + wv; tile * 16 < ga.n; tile += ranges * NW) {
-    const int32_t p = tile * 16 + i;
-    const bool inside = p < ga.n;
-    const int32_t row = inside ? p : 0;
-    const bool valid = inside && ga.mask[row] != 0;
-    // the tile's input, when it fits in registers: k block kb is channels
-    // 32 kb .. + 31 of A, in segment 32 kb / C
-    Raw<T, 8> xh[KBH > 0 ? KBH : 1];
-    if constexpr (held) {
+  // the bias-added, rounded outputs of tile `tile`, columns n0 + sb .. + SB - 1
+  auto store_block = [&](int32_t tile, int sb, const floatx4 (&acc)[NBT]) {
+    const int32_t j0 = n0 + sb;   // a sub-block lies in one output segment (C % SB == 0)
+    T* outp = static_cast<T*>(ga.out[j0 / C]);
+    // tile pairs 2w and 2w + 1 (64 columns): lanes i and i ^ 8 swap one
+    // piece (row rotation by 8 lanes), so that each store writes 8 rows x 128
+    // bytes: rows 0-7 of the tile first, then rows 8-15
+    const int32_t pa = tile * 16 + (i & 7), pb = pa + 8;
+    const uint32_t ccol = (uint32_t)(j0 % C) + (i < 8 ? 8 * g : 32 + 8 * g);
+#pragma unroll
+    for (int w = 0; w < NBT / 4; ++w) {
+      Raw<T, 8> pk[2];
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        float f[8];
+#pragma unroll
+        for (int v = 0; v < 2; ++v) {
+          const int t = 4 * w + 2 * u + v;
+          const float4 bias = *reinterpret_cast<const float4*>(s_b + sb + 16 * t + 4 * g);
+          f[4 * v + 0] = acc[t][0] + bias.x;
+          f[4 * v + 1] = acc[t][1] + bias.y;
+          f[4 * v + 2] = acc[t][2] + bias.z;
+          f[4 * v + 3] = acc[t][3] + bias.w;
+        }
+        pk[u] = F8::from_f32(f);
+      }
+      const uint4 snd = __builtin_bit_cast(uint4, i < 8 ? pk[1] : pk[0]);
+      uint4 rcv;
+      rcv.x = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)snd.x, 0x128, 0xf, 0xf, false);   // row_ror:8
+      rcv.y = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)snd.y, 0x128, 0xf, 0xf, false);
+      rcv.z = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)snd.z, 0x128, 0xf, 0xf, false);
+      rcv.w = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)snd.w, 0x128, 0xf, 0xf, false);
+      const uint4 da = i < 8 ? __builtin_bit_cast(uint4, pk[0]) : rcv;
+      const uint4 db = i < 8 ? rcv : __builtin_bit_cast(uint4, pk[1]);
+      if (pa < ga.n) *reinterpret_cast<uint4*>(elem_at(outp, (uint32_t)pa * (uint32_t)C + ccol + 64 * w)) = da;
+      if (pb < ga.n) *reinterpret_cast<uint4*>(elem_at(outp, (uint32_t)pb * (uint32_t)C + ccol + 64 * w)) = db;
+    }
+  };
+  const int32_t step = ranges * NW;
+  if constexpr (held) {
+    for (int32_t tile = rb * NW + wv; tile * 16 < ga.n; tile += step) {
+      const int32_t p = tile * 16 + i;
+      const bool inside = p < ga.n;
+      const int32_t row = inside ? p : 0;
+      const bool valid = inside && ga.mask[row] != 0;
+      // the tile's input: k block kb is channels 32 kb .. + 31 of A, in
+      // segment 32 kb / C
+      Raw<T, 8> xh[KBH];
 #pragma unroll
       for (int kb = 0; kb < KBH; ++kb) {
         xh[kb] = F8::zero();
@@ -183,13 +222,11 @@ __global__ __launch_bounds__(kRowGemmThreads) void k_rows_gemm(RowGemmArgs ga) {
           if (valid) xh[kb] = xo;
         }
       }
-    }
-    for (int sb = 0; sb < NB; sb += SB) {
-      floatx4 acc[NBT];
+      for (int sb = 0; sb < NB; sb += SB) {
+        floatx4 acc[NBT];
 #pragma unroll
-      for (int t = 0; t < NBT; ++t) acc[t] = zero;
-      const T* wsb = s_w + (sb + i) * LDW + 8 * g;
-      if constexpr (held) {
+        for (int t = 0; t < NBT; ++t) acc[t] = zero;
+        const T* wsb = s_w + (sb + i) * LDW + 8 * g;
 #pragma unroll
         for (int kb = 0; kb < KBH; ++kb) {
           if (32 * kb >= K) break;
@@ -199,75 +236,80 @@ __global__ __launch_bounds__(kRowGemmThreads) void k_rows_gemm(RowGemmArgs ga) {
             acc[t] = F8::mma(wo, xh[kb], acc[t]);
           }
         }
-      } else {
-        // the input one C-channel segment (C = 256) at a time: all of a
-        // segment's pieces are requested together, the next segment's while
-        // this one is formed
-        constexpr int KS = 8;
-        Raw<T, 8> xs[KS], xn[KS];
-        const T* src0 = static_cast<const T*>(ga.a[0]);
+        store_block(tile, sb, acc);
+      }
+    }
+  } else {
+    // The input 128 channels at a time (a step), all of a step's pieces
+    // requested together and the next step's in flight while one is formed;
+    // the next tile's first step and mask byte are requested during this
+    // tile's last step, so that no tile waits a round trip at its start.  The rows are read unconditionally (rows past n read row 0), and
+    // the sums of rows in no window or past n are replaced by those of zero
+    // input.
+    constexpr int KS = 4, HS = 32 * KS;   // pieces and channels per step (C % HS == 0)
+    const int steps = K / HS;
+    auto row_of = [&](int32_t t) -> int32_t {
+      const int32_t p = t * 16 + i;
+      return p < ga.n ? p : 0;
+    };
+    auto fetch_seg = [&](Raw<T, 8>(&x)[KS], int s, int32_t row) {
+      const T* src = static_cast<const T*>(ga.a[(HS * s) / C]);
+      const int c0 = (HS * s) % C;
 #pragma unroll
-        for (int kb = 0; kb < KS; ++kb) {
-          xs[kb] = F8::zero();
-          if (valid)
-            xs[kb] = __builtin_bit_cast(
-                Raw<T, 8>, *reinterpret_cast<const uint4*>(elem_at(src0, (uint32_t)row * (uint32_t)C + 32 * kb + 8 * g)));
-        }
-        for (int s = 0; s < nseg; ++s) {
-          const T* srcn = static_cast<const T*>(ga.a[s + 1 < nseg ? s + 1 : s]);
+      for (int kb = 0; kb < KS; ++kb)
+        x[kb] = __builtin_bit_cast(
+            Raw<T, 8>, *reinterpret_cast<const uint4*>(elem_at(src, (uint32_t)row * (uint32_t)C + c0 + 32 * kb + 8 * g)));
+    };
+    Raw<T, 8> xs[KS], xn[KS];
+    int32_t tile = rb * NW + wv;
+    int32_t row = row_of(tile);
+    uint8_t mk = 0;
+    if (tile * 16 < ga.n) {
+      fetch_seg(xs, 0, row);
+      mk = ga.mask[row];
+    }
+    for (; tile * 16 < ga.n; tile += step) {
+      const bool valid = tile * 16 + i < ga.n && mk != 0;
+      const int32_t nt = tile + step;
+      const bool more = nt * 16 < ga.n;
+      const int32_t nrow = row_of(nt);
+      uint8_t nmk = 0;
+      for (int sb = 0; sb < NB; sb += SB) {
+        floatx4 acc[NBT];
 #pragma unroll
-          for (int kb = 0; kb < KS; ++kb) {
-            xn[kb] = F8::zero();
-            if (valid && s + 1 < nseg)
-              xn[kb] = __builtin_bit_cast(
-                  Raw<T, 8>, *reinterpret_cast<const uint4*>(elem_at(srcn, (uint32_t)row * (uint32_t)C + 32 * kb + 8 * g)));
+        for (int t = 0; t < NBT; ++t) acc[t] = zero;
+        const T* wsb = s_w + (sb + i) * LDW + 8 * g;
+        for (int s = 0; s < steps; ++s) {
+          if (s + 1 < steps) {
+            fetch_seg(xn, s + 1, row);
+          } else if (sb + SB < NB) {
+            fetch_seg(xn, 0, row);
+          } else if (more) {
+            fetch_seg(xn, 0, nrow);
+            nmk = ga.mask[nrow];
           }
 #pragma unroll
           for (int kb = 0; kb < KS; ++kb)
 #pragma unroll
             for (int t = 0; t < NBT; ++t) {
-              const Raw<T, 8> wo = *reinterpret_cast<const Raw<T, 8>*>(wsb + 16 * t * LDW + s * C + 32 * kb);
+              const Raw<T, 8> wo = *reinterpret_cast<const Raw<T, 8>*>(wsb + 16 * t * LDW + HS * s + 32 * kb);
               acc[t] = F8::mma(wo, xs[kb], acc[t]);
             }
+          if (s + 1 < steps) {
 #pragma unroll
-          for (int kb = 0; kb < KS; ++kb) xs[kb] = xn[kb];
-        }
-      }
-      const int32_t j0 = n0 + sb;   // a sub-block lies in one output segment (C % SB == 0)
-      T* outp = static_cast<T*>(ga.out[j0 / C]);
-      // tile pairs 2w and 2w + 1 (64 columns): lanes i and i ^ 8 swap one
-      // piece (row rotation by 8 lanes), so that each store writes 8 rows x 128
-      // bytes: rows 0-7 of the tile first, then rows 8-15
-      const int32_t pa = tile * 16 + (i & 7), pb = pa + 8;
-      const uint32_t ccol = (uint32_t)(j0 % C) + (i < 8 ? 8 * g : 32 + 8 * g);
-#pragma unroll
-      for (int w = 0; w < NBT / 4; ++w) {
-        Raw<T, 8> pk[2];
-#pragma unroll
-        for (int u = 0; u < 2; ++u) {
-          float f[8];
-#pragma unroll
-          for (int v = 0; v < 2; ++v) {
-            const int t = 4 * w + 2 * u + v;
-            const float4 bias = *reinterpret_cast<const float4*>(s_b + sb + 16 * t + 4 * g);
-            f[4 * v + 0] = acc[t][0] + bias.x;
-            f[4 * v + 1] = acc[t][1] + bias.y;
-            f[4 * v + 2] = acc[t][2] + bias.z;
-            f[4 * v + 3] = acc[t][3] + bias.w;
+            for (int kb = 0; kb < KS; ++kb) xs[kb] = xn[kb];
           }
-          pk[u] = F8::from_f32(f);
         }
-        const uint4 snd = __builtin_bit_cast(uint4, i < 8 ? pk[1] : pk[0]);
-        uint4 rcv;
-        rcv.x = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)snd.x, 0x128, 0xf, 0xf, false);   // row_ror:8
-        rcv.y = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)snd.y, 0x128, 0xf, 0xf, false);
-        rcv.z = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)snd.z, 0x128, 0xf, 0xf, false);
-        rcv.w = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)snd.w, 0x128, 0xf, 0xf, false);
-        const uint4 da = i < 8 ? __builtin_bit_cast(uint4, pk[0]) : rcv;
-        const uint4 db = i < 8 ? rcv : __builtin_bit_cast(uint4, pk[1]);
-        if (pa < ga.n) *reinterpret_cast<uint4*>(elem_at(outp, (uint32_t)pa * (uint32_t)C + ccol + 64 * w)) = da;
-        if (pb < ga.n) *reinterpret_cast<uint4*>(elem_at(outp, (uint32_t)pb * (uint32_t)C + ccol + 64 * w)) = db;
+        // lane (i, g) holds row i's sums only: a row in no window or past n
+        // gets the sums of zero input, +0
+#pragma unroll
+        for (int t = 0; t < NBT; ++t) acc[t] = valid ? acc[t] : zero;
+        store_block(tile, sb, acc);
+#pragma unroll
+        for (int kb = 0; kb < KS; ++kb) xs[kb] = xn[kb];
       }
+      row = nrow;
+      mk = nmk;
     }
   }
 }
