@@ -626,9 +626,9 @@ static hipError_t rows_gemm(RowGemmArgs ga, hipStream_t stream) {
   }
   // the input held in registers for K <= 128 or K <= 384, else streamed a
   // segment at a time (K = 3C with C = 256; 128 weight rows of such K exceed the
-  // LDS cap, so a streamed product is never wide)
+  // LDS cap, so a streamed product is never wide; it reads 128 channels a step)
   const bool streamed = ga.K > 32 * 12;
-  if (streamed && (wide || ga.C > 256 || ga.C % 32 != 0)) return hipErrorInvalidValue;
+  if (streamed && (wide || ga.C > 256 || ga.C % 128 != 0)) return hipErrorInvalidValue;
   void (*kern)(RowGemmArgs) =
       streamed ? &k_rows_gemm<T, 4, 0>
       : wide ? (small_k ? &k_rows_gemm<T, 8, 4> : &k_rows_gemm<T, 8, 12>)
