@@ -624,9 +624,9 @@ static hipError_t rows_gemm(RowGemmArgs ga, hipStream_t stream) {
     if (gx > tiles) gx = (tiles + 7) / 8 * 8;
     if (gx < 8) gx = 8;
   }
-  // the input held in registers for K <= 128 or K <= 384, else streamed a
-  // segment at a time (K = 3C with C = 256; 128 weight rows of such K exceed the
-  // LDS cap, so a streamed product is never wide; it reads 128 channels a step)
+  // the input held in registers for K <= 128 or K <= 384, else streamed 128
+  // channels a step (K = 3C with C = 256; 128 weight rows of such K exceed the
+  // LDS cap, so a streamed product is never wide)
   const bool streamed = ga.K > 32 * 12;
   if (streamed && (wide || ga.C > 256 || ga.C % 128 != 0)) return hipErrorInvalidValue;
   void (*kern)(RowGemmArgs) =
