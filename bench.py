@@ -264,7 +264,7 @@ def main():
         print(sq_summary(args.sq_summary))
         return
     if args.gpus != 1:
-        print(f"bench.py: this build measures one GPU only (asked for --gpus {args.gpus}); "
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); "
               "SLA would shard by contiguous window ranges with no exchange between GPUs", file=sys.stderr)
         sys.exit(2)
     import torch
