@@ -353,6 +353,28 @@ def test_xca_backward_binding_rejects_bad_dtau_and_workspace(L):
         sla.backward_xca(*args, dtau=torch.zeros(H), workspace=torch.zeros(64, dtype=torch.uint8)[::2])
 
 
+def test_projected_saved_qkv_argument_errors(L):
+    # the saved q, k, v buffer is checked before the C call: a short, strided,
+    # wrongly typed or foreign buffer would be written past its end by the
+    # forward, or read past it by the backward
+    import torch
+
+    n, H, d = 6, 4, 32
+    C = H * d
+    plan = sla.Plan(buf=torch.zeros(sla.plan_bytes(n, 2), dtype=torch.uint8), n=n, num_windows=2,
+                    chunk_rows=64, perm=None, offsets=None, invalid=None)
+    x = torch.zeros((n, C), dtype=torch.float16)
+    w_qkv = torch.zeros((3 * C, C), dtype=torch.float16)
+    w_o = torch.zeros((C, C), dtype=torch.float16)
+    for bad in (torch.zeros((3, n - 1, C), dtype=torch.float16), torch.zeros((3, n, C), dtype=torch.bfloat16),
+                torch.zeros((3, n, 2 * C), dtype=torch.float16)[:, :, ::2], torch.zeros((n, C), dtype=torch.float16),
+                torch.zeros((3, n, C), dtype=torch.float16, device="meta")):
+        with pytest.raises(ValueError, match="qkv_out must"):
+            sla.forward_projected(plan, x, w_qkv, w_o, H, qkv_out=bad)
+        with pytest.raises(ValueError, match="qkv must"):
+            sla.backward_projected(plan, x, w_qkv, w_o, x, x, H, qkv=bad)
+
+
 def test_xca_backward_noalloc_argument_errors(L):
     # the size limit of the static buffer and the pointer checks are host-side:
     # nothing is enqueued (and no device is touched) when they fail
