@@ -793,13 +793,14 @@ def test_projected_backward_shapes(sla, dtype, shape):
 
 
 @pytest.mark.parametrize("dtype,shape,long", [("f16", (4, 32), False), ("bf16", (8, 32), False),
-                                              ("f16", (2, 32), True)])
+                                              ("f16", (2, 32), True), ("bf16", (8, 16), True)])
 def test_projected_saved_qkv(sla, dtype, shape, long):
     # the forward's saved q, k, v: the projection of x (checked against float64
     # from the same rounded inputs), o and y unchanged by saving, and the
     # backward that reads them equal, bit for bit, to the one that recomputes
     # them (the same products in the same order).  `long` adds a window of 1,024
-    # rows, whose shares are projected job by job (streamed).
+    # rows, whose shares are projected job by job (streamed).  d = 16 stores its
+    # fragments as four 8-byte pieces, d = 32 (16-bit) as one 16-byte piece.
     import torch
 
     H, d = shape
