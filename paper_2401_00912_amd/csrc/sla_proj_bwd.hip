@@ -528,17 +528,18 @@ __global__ __launch_bounds__(256) void k_wgrad_reduce(const float* __restrict__ 
   const size_t total = (size_t)4 * C * C + 4 * (size_t)C;
   for (size_t e = (size_t)blockIdx.x * blockDim.x + threadIdx.x; e < total;
        e += (size_t)gridDim.x * blockDim.x) {
-    // eight loads in flight, added in group order
+    // 32 loads in flight, added in group order (groups past the last are
+    // neither loaded nor added)
+    constexpr int kBatch = 32;
     float s = 0.f;
-    int32_t gi = 0;
-    for (; gi + 8 <= groups; gi += 8) {
-      float v[8];
+    for (int32_t gi = 0; gi < groups; gi += kBatch) {
+      float v[kBatch];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) v[u] = part[(size_t)(gi + u) * total + e];
+      for (int u = 0; u < kBatch; ++u) v[u] = gi + u < groups ? part[(size_t)(gi + u) * total + e] : 0.f;
 #pragma unroll
-      for (int u = 0; u < 8; ++u) s += v[u];
+      for (int u = 0; u < kBatch; ++u)
+        if (gi + u < groups) s += v[u];
     }
-    for (; gi < groups; ++gi) s += part[(size_t)gi * total + e];
     const size_t cc = (size_t)C * C;
     if (e < 3 * cc) dw_qkv[e] = s;
     else if (e < 4 * cc) dw_o[e - 3 * cc] = s;
