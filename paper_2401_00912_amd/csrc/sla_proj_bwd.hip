@@ -79,13 +79,20 @@ __global__ __launch_bounds__(256) void k_prep(PrepArgs pa) {
                    (b - tq) / cb, tile);
     return;
   }
+  // the header, the count of rows in windows and the thread's first
+  // permutation entry are requested together (every plan holds n permutation
+  // entries; a CSR plan's are not used), so the mask waits one round trip
   const PlanHeader* hdr = pa.hdr;
+  const int32_t n = pa.n, stride = pa.mask_blocks * 256;
+  int32_t p = (b - tq - to) * 256 + (int32_t)threadIdx.x;
+  int32_t pr = p < n ? pa.perm[p] : 0;
+  const int32_t nv = *pa.nvalid;
   if (hdr->magic != kPlanMagic || hdr->n != pa.n || hdr->num_windows != pa.W) return;
   const bool csr = hdr->csr != 0;
-  const int32_t n = pa.n;
-  const int32_t nvalid = max(0, min(*pa.nvalid, n));
-  for (int32_t p = (b - tq - to) * 256 + (int32_t)threadIdx.x; p < n; p += pa.mask_blocks * 256) {
-    const int32_t row = csr ? p : pa.perm[p];
+  const int32_t nvalid = max(0, min(nv, n));
+  for (; p < n; p += stride) {
+    const int32_t row = csr ? p : pr;
+    if (p + stride < n) pr = pa.perm[p + stride];
     if ((uint32_t)row < (uint32_t)n) pa.mask[row] = p < nvalid ? 1 : 0;
   }
 }
